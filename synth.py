@@ -1,0 +1,137 @@
+"""Seeded synthetic KV-cache workloads for GSRQ.
+
+This module only draws inputs; it holds none of the quantiser's arithmetic.
+It is shared by the tests, the oracle-based checks and the benchmark, and it
+stands in for the paper's real LLaMA-3-8B KV activations, calibration sets and
+gradient norms (Sec. 6.1, 6.2), none of which are available here.
+
+Recipe (every draw from numpy's PCG64, one child SeedSequence per
+(workload, layer), always in this order):
+  1. key channel scales sigma_c ~ lognormal(0, key_sigma) for c < D;
+  2. outlier channels: round(outlier_frac * D) channels chosen without
+     replacement, their sigma multiplied by outlier_mult;
+  3. keys = N(0, 1) * sigma_c, [N, D];
+  4. values = N(0, 1), [N, D];
+  5. w_K ~ lognormal(0, 1), [N];   6. w_V ~ lognormal(0, 1), [N];
+  7. seed rows for GSKM initialisation: for K then V, for every stage m and
+     subspace g, K distinct row indices drawn without replacement.
+Data are drawn in float32 and rounded to the workload's storage dtype.
+A row is one token's K (or V) vector with all heads concatenated
+(D = heads * 128), so one weight per token is shared by every subspace.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+from typing import Tuple
+
+import numpy as np
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    N: int                  # tokens (rows)
+    D: int                  # heads * head_dim
+    d: int                  # subvector dimension
+    K: int                  # codebook size
+    M: int                  # residual stages
+    T: int                  # GSKM iterations per stage
+    dtype: str              # storage dtype of K/V: "float32" or "float16"
+    layers: int = 1
+    key_sigma: float = 1.0  # lognormal sigma of the per-channel key scale
+    outlier_frac: float = 0.01
+    outlier_mult: float = 10.0
+    note: str = ""
+
+    @property
+    def G(self) -> int:
+        return self.D // self.d
+
+
+WORKLOADS = {
+    # 4096 tokens x 1 head x 128, fp32; d=8, K=256, M=2, T=10
+    "tiny": Workload("tiny", 4096, 128, 8, 256, 2, 10, "float32",
+                     key_sigma=0.5, outlier_frac=0.0,
+                     note="4096 tok x 1 head x 128 fp32, d=8 K=256 M=2 T=10"),
+    # LLaMA-3-8B single layer: 32768 tokens x 8 KV heads x 128, fp16, 1 bit
+    "llama3_8b_layer_1bit": Workload(
+        "llama3_8b_layer_1bit", 32768, 1024, 8, 256, 1, 20, "float16",
+        note="32768 tok x 8 heads x 128 fp16, d=8 K=256 M=1 (1 bit), weighted GSKM T=20"),
+    # full-model cache: 32 layers x 131072 tokens, codebooks from 4096-token slices
+    "llama3_8b_cache_1bit": Workload(
+        "llama3_8b_cache_1bit", 131072, 1024, 8, 256, 1, 20, "float16", layers=32,
+        note="32 layers x 131072 tok x 8 heads x 128 fp16, 1 bit"),
+    # rate sweep at d=16: M in {1, 2, 4} -> 0.5 / 1 / 2 bit
+    "rate_sweep_d16": Workload(
+        "rate_sweep_d16", 65536, 1024, 16, 256, 4, 20, "float16",
+        note="65536 tok x 8 heads x 128 fp16, d=16 K=256 M in {1,2,4}"),
+    # large codebook, full-head vectors
+    "large_codebook_d128": Workload(
+        "large_codebook_d128", 65536, 1024, 128, 4096, 8, 15, "float16",
+        note="65536 tok x 8 heads x 128 fp16, d=128 K=4096 M=8 (0.75 bit)"),
+}
+
+
+def _children(seed: int, workload: str, layer: int) -> np.random.Generator:
+    # one independent stream per (workload, layer); the workload name is
+    # folded into the entropy so different workloads never share draws
+    tag = [ord(c) for c in workload]
+    ss = np.random.SeedSequence([seed, layer] + tag)
+    return np.random.Generator(np.random.PCG64(ss))
+
+
+@dataclass
+class KVBatch:
+    keys: np.ndarray
+    values: np.ndarray
+    w_keys: np.ndarray
+    w_values: np.ndarray
+    seeds_keys: np.ndarray     # [M, G, K] int64
+    seeds_values: np.ndarray   # [M, G, K] int64
+    key_scales: np.ndarray = field(repr=False, default=None)
+
+
+def draw_seed_rows(rng: np.random.Generator, N: int, K: int, M: int, G: int) -> np.ndarray:
+    out = np.empty((M, G, K), dtype=np.int64)
+    for m in range(M):
+        for g in range(G):
+            out[m, g] = rng.choice(N, size=K, replace=False)
+    return out
+
+
+def make_kv(wl: Workload, layer: int = 0, seed: int = 0, N: int | None = None,
+            M: int | None = None) -> KVBatch:
+    """Draw one layer of keys/values, weights and seed rows for workload wl.
+
+    N and M may be overridden (a shorter slice of the same distribution, or
+    fewer stages); the draw order stays the one in the module docstring.
+    """
+    N = wl.N if N is None else int(N)
+    M = wl.M if M is None else int(M)
+    D, G, K = wl.D, wl.G, wl.K
+    rng = _children(seed, wl.name, layer)
+    scales = rng.lognormal(0.0, wl.key_sigma, size=D).astype(np.float32)
+    n_out = int(round(wl.outlier_frac * D))
+    if n_out > 0:
+        ch = rng.choice(D, size=n_out, replace=False)
+        scales[ch] *= np.float32(wl.outlier_mult)
+    keys = rng.standard_normal((N, D), dtype=np.float32) * scales[None, :]
+    values = rng.standard_normal((N, D), dtype=np.float32)
+    w_k = rng.lognormal(0.0, 1.0, size=N).astype(np.float32)
+    w_v = rng.lognormal(0.0, 1.0, size=N).astype(np.float32)
+    sk = draw_seed_rows(rng, N, K, M, G)
+    sv = draw_seed_rows(rng, N, K, M, G)
+    dt = np.float16 if wl.dtype == "float16" else np.float32
+    return KVBatch(keys.astype(dt), values.astype(dt), w_k, w_v, sk, sv, scales)
+
+
+def small_case(N: int, D: int, d: int, K: int, M: int, seed: int = 0,
+               dtype=np.float32, key_sigma: float = 0.5,
+               weights: bool = True) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """A small generic case (X [N, D], w [N], seed rows [M, G, K]) for tests."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, N, D, d, K, M])))
+    scales = rng.lognormal(0.0, key_sigma, size=D).astype(np.float32)
+    X = (rng.standard_normal((N, D), dtype=np.float32) * scales[None, :]).astype(dtype)
+    w = rng.lognormal(0.0, 1.0, size=N).astype(np.float32) if weights else np.ones(N, np.float32)
+    seeds = draw_seed_rows(rng, N, K, M, D // d)
+    return X, w, seeds
