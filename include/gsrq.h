@@ -1,0 +1,182 @@
+/*
+ * gsrq.h -- C ABI of the GSRQ hot path on AMD MI355X (gfx950).
+ *
+ * Gain-Shape Residual Quantization (arXiv 2607.01065): every row x of a
+ * [N][D] matrix (one token's K or V vector, heads concatenated) is split into
+ * G = D/d subvectors of d elements (product quantisation, Sec. 3); subvector
+ * g of stage m is coded by the index k of one codeword c = gain[m][g][k] *
+ * shape[m][g][k][:] of a gain-shape codebook (Sec. 5.2, eq. 3), chosen by
+ * k = argmax_k 2 g_k r.s_k - g_k^2 (eq. 5) on the stage's residual r, which
+ * is then reduced by c (residual quantisation, Sec. 3 / 5.1).  Codebooks are
+ * learnt with weighted gain-shape K-means (Algorithm 1, eqs. 5-8, Sec. 5.3).
+ *
+ * Conventions shared by every entry point
+ *  - Every array argument is DEVICE memory owned by the caller, except the
+ *    seed-row table of gsrq_train_stage, which is host memory.  The library
+ *    allocates nothing; scratch space is the caller's workspace.
+ *  - Calls are ordered on the given HIP stream (NULL = the null stream) and
+ *    return once the work is enqueued.  Synchronise the stream before reading
+ *    any output on the host.
+ *  - Errors are return codes.  Arguments are validated on the host before any
+ *    HIP call; on a validation error no output is touched.  GSRQ_E_HIP means a
+ *    launch or copy failed after validation (outputs are then undefined).
+ *  - Codebook layouts: gain [M][G][K] float32 (g >= 0), shape [M][G][K][d]
+ *    float32 (unit rows), row-major and dense.
+ *  - Code layout (bit-packed): row i owns gsrq_code_words() uint32 words; the
+ *    code of stage m, subspace g is the b = log2 K bit field starting at bit
+ *    t*b, t = m*G + g, of the row's bit string, least significant bit first
+ *    (bit p is bit p%32 of word p/32).
+ *  - Supported on this build: 1 <= d <= 8, 2 <= K <= 256 (power of two).
+ *    Other valid shapes return GSRQ_E_UNSUPPORTED.
+ *  - The library keeps no state between calls; calls on different streams
+ *    with disjoint buffers may run concurrently.
+ */
+#ifndef GSRQ_H
+#define GSRQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GSRQ_OK = 0,
+  GSRQ_E_ARG = 1,          /* invalid argument (null pointer, size, flag)  */
+  GSRQ_E_UNSUPPORTED = 2,  /* valid problem this build does not implement  */
+  GSRQ_E_WORKSPACE = 3,    /* workspace too small                          */
+  GSRQ_E_HIP = 4           /* a HIP runtime call failed                    */
+} gsrq_status;
+
+typedef enum { GSRQ_F32 = 0, GSRQ_F16 = 1 } gsrq_dtype;
+
+/* Problem shape.  N rows of D elements, subvector dimension d (d divides D,
+ * G = D/d subspaces), K codewords per codebook (power of two), M stages. */
+typedef struct {
+  int64_t N;
+  int32_t D;
+  int32_t d;
+  int32_t K;
+  int32_t M;
+} gsrq_shape;
+
+/* Flags of gsrq_train_stage. */
+enum {
+  /* Start from the codebook already in gain/shape instead of seeding from
+   * rows (resume; seed_rows is then ignored and may be NULL). */
+  GSRQ_RESUME = 1u,
+  /* With GSRQ_RESUME: assign_io holds the assignment the previous iteration
+   * produced, so the stop test of the first iteration compares against it.
+   * Without this flag a resumed first iteration always counts as changed. */
+  GSRQ_ASSIGN_IN = 2u,
+  /* Run all T iterations even when an assignment repeats. */
+  GSRQ_NO_EARLY_STOP = 4u
+};
+
+/* Human-readable name of a status code (static string). */
+const char* gsrq_status_string(gsrq_status st);
+
+/* uint32 words per row of packed codes: ceil(M * G * log2(K) / 32).
+ * Returns 0 for an invalid shape. */
+size_t gsrq_code_words(const gsrq_shape* s);
+
+/* Average bits per element, M * log2(K) / d (Sec. 6.2); 0 if invalid. */
+double gsrq_bits_per_element(const gsrq_shape* s);
+
+/* Workspace bytes gsrq_train_stage needs for shape s (s->M is ignored).
+ * Writes the size to *bytes.  GSRQ_E_ARG / GSRQ_E_UNSUPPORTED as above. */
+gsrq_status gsrq_train_workspace_bytes(const gsrq_shape* s, size_t* bytes);
+
+/* Workspace bytes gsrq_encode needs for shape s. */
+gsrq_status gsrq_encode_workspace_bytes(const gsrq_shape* s, size_t* bytes);
+
+/*
+ * gsrq_train_stage -- learn ONE stage's G codebooks with weighted GSKM
+ * (Algorithm 1 with the weighted means of Sec. 5.1 / 5.3), then optionally
+ * re-encode the stage input with the learnt codebook to give the next
+ * stage's residual (Sec. 5.1).  s->M is ignored.
+ *
+ *  X, x_dtype, ldx   stage input, [N][ldx] row-major (ldx >= D elements):
+ *                    the data for stage 0, the residual for later stages.
+ *  w                 [N] float32 per-row weights >= 0, shared by every
+ *                    subspace; NULL means all ones.  A cluster whose members
+ *                    carry zero total weight counts as empty.
+ *  T                 maximum iterations, >= 0; T = 0 (not with GSRQ_RESUME)
+ *                    only initialises: gain/shape receive the initial
+ *                    codebook and assign_io the initial assignment.
+ *  seed_rows         HOST [G][K] int32 row indices; codebook k of subspace g
+ *                    is seeded with the direction of row seed_rows[g][k],
+ *                    which must be a nonzero subvector.  Indices must lie in
+ *                    [0, N) and be distinct within a subspace; N >= K.
+ *  flags             GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP.
+ *  gain, shape       [G][K], [G][K][d] float32 outputs (inputs on resume).
+ *  R_next            [N][D] float32 residual X - c(encode(X)) with the final
+ *                    codebook, or NULL.
+ *  assign_io         [G][N] uint16 final assignment (input too with
+ *                    GSRQ_ASSIGN_IN), or NULL.
+ *  iters_run         [G] int32 iterations run per subspace, or NULL.
+ *  obj_trace         [G][T] float64: entry t-1 is sum_i w_i ||x_i - c_{k_i}||^2
+ *                    of iteration t's assignment against the codebook it was
+ *                    made with; entries past iters_run are 0.  Or NULL.
+ *  workspace         >= gsrq_train_workspace_bytes(s), 256-byte aligned.
+ *
+ * Initialisation (without GSRQ_RESUME): shapes are the normalised seed rows;
+ * rows are assigned to the shape of largest projection, and each gain is the
+ * clamped weighted mean projection of its members (eq. 8), or the seed row's
+ * norm for a cluster without weight.  Iteration t: assign by eq. (5) (ties
+ * to the lowest index), then for clusters with weight: shape = normalised
+ * weighted sum of y_i = x_i / (||x_i|| + 1e-8) (eqs. 6, 7), kept if that sum
+ * is below 1e-6 times the cluster weight; gain = max(0, weighted mean of
+ * x_i . s_k) (eq. 8).  A subspace stops after the iteration whose
+ * assignment equals the previous one (unless GSRQ_NO_EARLY_STOP).
+ */
+gsrq_status gsrq_train_stage(const gsrq_shape* s,
+                             const void* X, gsrq_dtype x_dtype, int64_t ldx,
+                             const float* w, int32_t T,
+                             const int32_t* seed_rows, uint32_t flags,
+                             float* gain, float* shape,
+                             float* R_next, uint16_t* assign_io,
+                             int32_t* iters_run, double* obj_trace,
+                             void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * gsrq_encode -- stage-fused GSRQ encoding (Sec. 3, Sec. 5.1): for every
+ * subspace g and stage m = 0..M-1 in order, k = argmax_k 2 g_k r.s_k - g_k^2
+ * (eq. 5, ties to the lowest index) on the residual r (initially the row's
+ * subvector), then r <- r - gain[m][g][k] shape[m][g][k].
+ *
+ *  X, x_dtype, ldx   [N][ldx] input rows (ldx >= D).
+ *  gain, shape       [M][G][K], [M][G][K][d].
+ *  codes             [N][gsrq_code_words(s)] uint32, packed as above.
+ *  residual          [N][D] float32 final residual, or NULL.
+ *  workspace         >= gsrq_encode_workspace_bytes(s), 256-byte aligned.
+ * Indices agree with a float64 evaluation of eq. (5) whenever the best and
+ * second-best scores differ by more than 1e-4 * ||r||^2.
+ */
+gsrq_status gsrq_encode(const gsrq_shape* s,
+                        const void* X, gsrq_dtype x_dtype, int64_t ldx,
+                        const float* gain, const float* shape,
+                        uint32_t* codes, float* residual,
+                        void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * gsrq_decode -- reconstruction as the sum over the first M_use stages of
+ * gain[m][g][k] * shape[m][g][k][:] (Sec. 3; prefix decoding, Sec. 1),
+ * accumulated in float32 in stage order, stored as out_dtype (float16 by
+ * round-to-nearest-even).
+ *
+ *  codes             [N][gsrq_code_words(s)] uint32.
+ *  M_use             1 <= M_use <= s->M.
+ *  Xhat, ldo         [N][ldo] output (ldo >= D elements).
+ */
+gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes,
+                        int32_t M_use, const float* gain, const float* shape,
+                        void* Xhat, gsrq_dtype out_dtype, int64_t ldo,
+                        void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GSRQ_H */

@@ -131,13 +131,15 @@ def gskm_update(X, w, assign, gain, shape):
     return gain, shape
 
 
-def gskm_init(X, w, init_rows):
+def gskm_init(X, w, init_rows, assign0=None):
     """Initialisation of Algorithm 1 from K seed rows.
 
     Shapes are the normalised seed rows (points on the unit sphere).  Gains
     follow eq. (8) over an equal-gain assignment k_i = argmax_k x_i^T s_k
     (lowest k on ties); a cluster that receives no weight takes the norm of
-    its seed row.  Returns (gain, shape, initial assignment).
+    its seed row.  Passing assign0 uses that assignment instead of the
+    equal-gain one (teacher forcing in the parity tests).
+    Returns (gain, shape, initial assignment).
     """
     X = np.asarray(X, dtype=np.float64)
     w = np.asarray(w, dtype=np.float64)
@@ -147,7 +149,10 @@ def gskm_init(X, w, init_rows):
     if np.any(norms == 0.0):
         raise ValueError("GSKM initialisation needs nonzero seed rows")
     shape = seeds / (norms[:, None] + EPS)
-    assign0 = np.argmax(X @ shape.T, axis=1).astype(np.int64)
+    if assign0 is None:
+        assign0 = np.argmax(X @ shape.T, axis=1).astype(np.int64)
+    else:
+        assign0 = np.asarray(assign0, np.int64)
     K = shape.shape[0]
     gain = np.empty(K, dtype=np.float64)
     for k in range(K):

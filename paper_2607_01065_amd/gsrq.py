@@ -1,0 +1,239 @@
+"""ctypes binding of libgsrq.so (the C ABI in include/gsrq.h).
+
+Argument marshalling only: every step of the GSRQ path runs in the HIP
+kernels of the library.  torch supplies device memory and the stream; a torch
+tensor is passed as its data pointer.  If the library is not built, importing
+functions from here raises instead of falling back to anything else.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgsrq.so")
+
+GSRQ_OK, GSRQ_E_ARG, GSRQ_E_UNSUPPORTED, GSRQ_E_WORKSPACE, GSRQ_E_HIP = range(5)
+GSRQ_F32, GSRQ_F16 = 0, 1
+GSRQ_RESUME, GSRQ_ASSIGN_IN, GSRQ_NO_EARLY_STOP = 1, 2, 4
+
+
+class GsrqError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [("N", ctypes.c_int64), ("D", ctypes.c_int32), ("d", ctypes.c_int32),
+                ("K", ctypes.c_int32), ("M", ctypes.c_int32)]
+
+
+_lib = None
+_vp = ctypes.c_void_p
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libgsrq.so once; raise if it is missing (no fallback exists)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(path)
+    SP = ctypes.POINTER(Shape)
+    lib.gsrq_status_string.restype = ctypes.c_char_p
+    lib.gsrq_status_string.argtypes = [ctypes.c_int]
+    lib.gsrq_code_words.restype = ctypes.c_size_t
+    lib.gsrq_code_words.argtypes = [SP]
+    lib.gsrq_bits_per_element.restype = ctypes.c_double
+    lib.gsrq_bits_per_element.argtypes = [SP]
+    lib.gsrq_train_workspace_bytes.restype = ctypes.c_int
+    lib.gsrq_train_workspace_bytes.argtypes = [SP, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gsrq_encode_workspace_bytes.restype = ctypes.c_int
+    lib.gsrq_encode_workspace_bytes.argtypes = [SP, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gsrq_train_stage.restype = ctypes.c_int
+    lib.gsrq_train_stage.argtypes = [SP, _vp, ctypes.c_int, ctypes.c_int64, _vp, ctypes.c_int32,
+                                     _vp, ctypes.c_uint32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                     _vp, ctypes.c_size_t, _vp]
+    lib.gsrq_encode.restype = ctypes.c_int
+    lib.gsrq_encode.argtypes = [SP, _vp, ctypes.c_int, ctypes.c_int64, _vp, _vp, _vp, _vp,
+                                _vp, ctypes.c_size_t, _vp]
+    lib.gsrq_decode.restype = ctypes.c_int
+    lib.gsrq_decode.argtypes = [SP, _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_int,
+                                ctypes.c_int64, _vp]
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().gsrq_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != GSRQ_OK:
+        raise GsrqError(status, where)
+
+
+def make_shape(N, D, d, K, M=1) -> Shape:
+    return Shape(int(N), int(D), int(d), int(K), int(M))
+
+
+def code_words(N, D, d, K, M) -> int:
+    return int(load_library().gsrq_code_words(ctypes.byref(make_shape(N, D, d, K, M))))
+
+
+def bits_per_element(d, K, M, D=None) -> float:
+    D = d if D is None else D
+    return float(load_library().gsrq_bits_per_element(ctypes.byref(make_shape(1, D, d, K, M))))
+
+
+def train_workspace_bytes(N, D, d, K) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().gsrq_train_workspace_bytes(ctypes.byref(make_shape(N, D, d, K, 1)),
+                                                      ctypes.byref(n)), "train_workspace_bytes")
+    return int(n.value)
+
+
+def encode_workspace_bytes(N, D, d, K, M) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load_library().gsrq_encode_workspace_bytes(ctypes.byref(make_shape(N, D, d, K, M)),
+                                                       ctypes.byref(n)), "encode_workspace_bytes")
+    return int(n.value)
+
+
+# ------------------------------------------------------------ torch plumbing
+
+def _torch():
+    import torch
+    return torch
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else int(t.data_ptr())
+
+
+def _stream_handle(stream) -> Optional[int]:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return int(s.cuda_stream) or None
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.float16:
+        return GSRQ_F16
+    if t.dtype == torch.float32:
+        return GSRQ_F32
+    raise TypeError(f"unsupported dtype {t.dtype}; float16 or float32 expected")
+
+
+def _rows(X):
+    if X.dim() != 2 or X.stride(1) != 1:
+        raise ValueError("X must be a 2-D tensor with unit column stride")
+    return X.shape[0], X.shape[1], X.stride(0)
+
+
+def _workspace(nbytes, device, workspace):
+    torch = _torch()
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < nbytes:
+            raise ValueError("workspace too small")
+        return workspace
+    # torch's caching allocator returns 512-byte aligned blocks
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+@dataclass
+class TrainResult:
+    gain: object          # [G, K] float32
+    shape: object         # [G, K, d] float32
+    assign: object        # [G, N] int16 holding uint16 codes
+    iters: object         # [G] int32
+    trace: object         # [G, T] float64 or None
+    residual: object      # [N, D] float32 or None
+    seed_rows: object = None  # host table kept alive with the results
+
+
+def train_stage(X, d, K, T, seed_rows=None, w=None, *, gain=None, shape=None, assign=None,
+                resume=False, assign_in=False, no_early_stop=False, residual=False,
+                trace=True, workspace=None, stream=None) -> TrainResult:
+    """One stage of weighted GSKM on device tensor X [N, D] (see gsrq_train_stage)."""
+    torch = _torch()
+    lib = load_library()
+    N, D, ldx = _rows(X)
+    G = D // d if d > 0 and D % d == 0 else 0
+    dev = X.device
+    if gain is None:
+        gain = torch.empty((max(G, 1), K), dtype=torch.float32, device=dev)
+    if shape is None:
+        shape = torch.empty((max(G, 1), K, d), dtype=torch.float32, device=dev)
+    if assign is None:
+        assign = torch.empty((max(G, 1), N), dtype=torch.int16, device=dev)
+    iters = torch.empty(max(G, 1), dtype=torch.int32, device=dev)
+    tr = torch.empty((max(G, 1), max(T, 1)), dtype=torch.float64, device=dev) if trace and T > 0 else None
+    res = torch.empty((N, D), dtype=torch.float32, device=dev) if residual else None
+    seeds = None
+    if seed_rows is not None:
+        seeds = np.ascontiguousarray(np.asarray(seed_rows), dtype=np.int32)
+    flags = ((GSRQ_RESUME if resume else 0) | (GSRQ_ASSIGN_IN if assign_in else 0)
+             | (GSRQ_NO_EARLY_STOP if no_early_stop else 0))
+    sh = make_shape(N, D, d, K, 1)
+    n = ctypes.c_size_t(0)
+    st = lib.gsrq_train_workspace_bytes(ctypes.byref(sh), ctypes.byref(n))
+    _check(st, "gsrq_train_workspace_bytes")
+    ws = _workspace(n.value, dev, workspace)
+    st = lib.gsrq_train_stage(
+        ctypes.byref(sh), _ptr(X), _dtype_code(X), ldx, _ptr(w), int(T),
+        None if seeds is None else seeds.ctypes.data, flags, _ptr(gain), _ptr(shape),
+        _ptr(res), _ptr(assign), _ptr(iters), _ptr(tr), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream_handle(stream))
+    _check(st, "gsrq_train_stage")
+    return TrainResult(gain, shape, assign, iters, tr, res, seeds)
+
+
+def encode(X, gain, shape, *, codes=None, residual=False, workspace=None, stream=None):
+    """Stage-fused encode of device tensor X [N, D] with codebooks
+    gain [M, G, K], shape [M, G, K, d].  Returns (codes [N, W] int32 words
+    holding uint32 bit fields, residual [N, D] float32 or None)."""
+    torch = _torch()
+    lib = load_library()
+    N, D, ldx = _rows(X)
+    M, G, K = gain.shape
+    d = shape.shape[-1]
+    sh = make_shape(N, D, d, K, M)
+    W = int(lib.gsrq_code_words(ctypes.byref(sh)))
+    if codes is None:
+        codes = torch.empty((N, max(W, 1)), dtype=torch.int32, device=X.device)
+    res = torch.empty((N, D), dtype=torch.float32, device=X.device) if residual else None
+    n = ctypes.c_size_t(0)
+    _check(lib.gsrq_encode_workspace_bytes(ctypes.byref(sh), ctypes.byref(n)),
+           "gsrq_encode_workspace_bytes")
+    ws = _workspace(n.value, X.device, workspace)
+    st = lib.gsrq_encode(ctypes.byref(sh), _ptr(X), _dtype_code(X), ldx, _ptr(gain),
+                         _ptr(shape), _ptr(codes), _ptr(res), _ptr(ws),
+                         ws.numel() * ws.element_size(), _stream_handle(stream))
+    _check(st, "gsrq_encode")
+    return codes, res
+
+
+def decode(codes, gain, shape, D, M_use=None, *, out_dtype=None, out=None, stream=None):
+    """Gather-sum decode of packed codes [N, W] with codebooks gain [M, G, K],
+    shape [M, G, K, d] into [N, D] (float16 by default)."""
+    torch = _torch()
+    lib = load_library()
+    M, G, K = gain.shape
+    d = shape.shape[-1]
+    N = codes.shape[0]
+    M_use = M if M_use is None else int(M_use)
+    if out is None:
+        out = torch.empty((N, D), dtype=out_dtype or torch.float16, device=codes.device)
+    sh = make_shape(N, D, d, K, M)
+    st = lib.gsrq_decode(ctypes.byref(sh), _ptr(codes), M_use, _ptr(gain), _ptr(shape),
+                         _ptr(out), _dtype_code(out), out.stride(0), _stream_handle(stream))
+    _check(st, "gsrq_decode")
+    return out
