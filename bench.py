@@ -1,0 +1,185 @@
+#!/usr/bin/env python
+"""GSRQ hot-path benchmark on one MI355X.
+
+One step = for the K cache and then the V cache of one LLaMA-3-8B-shaped
+layer (32768 tokens x 8 KV heads x 128, float16; synthetic, see synth.py):
+weighted GSKM codebook learning (d=8, K=256, one stage, T=20 iterations with
+the stop rule of Algorithm 1), then 1-bit GSRQ encode, then gather-sum decode
+to float16.  Inputs are resident in HBM before timing starts.
+
+Prints one JSON line.  `value` is vectors/s over the whole step (a vector is
+one token's 128-element K or V row of one head); the per-kernel figures come
+from HIP events recorded around each launch on its own stream during the
+timed steps.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline"
+PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
+PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
+HEAD_DIM = 128
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="llama3_8b_layer_1bit")
+    ap.add_argument("--cpu-groups", type=int, default=16,
+                    help="subspaces of the K cache the CPU-baseline sample runs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_baseline(kv, wl, n_groups):
+    """Time the float64 oracle on a bounded sample of the same step and scale
+    it to vectors/s of the whole step."""
+    import numpy as np
+    from oracle import gsrq_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    X = kv.keys.astype(np.float64)
+    w = kv.w_keys.astype(np.float64)
+    d, K, T = wl.d, wl.K, wl.T
+    t_init = t_iter = t_enc = t_dec = 0.0
+    n_iter = 2
+    for g in range(n_groups):
+        Xg = X[:, g * d:(g + 1) * d]
+        t0 = time.perf_counter()
+        gain, shape, prev = O.gskm_init(Xg, w, kv.seeds_keys[0, g])
+        t1 = time.perf_counter()
+        for _ in range(n_iter):
+            a = O.gskm_assign(Xg, gain, shape)
+            gain, shape = O.gskm_update(Xg, w, a, gain, shape)
+        t2 = time.perf_counter()
+        codes, _ = O.gsrq_encode(Xg, gain[None, None], shape[None, None])
+        t3 = time.perf_counter()
+        O.gsrq_decode(codes, gain[None, None], shape[None, None])
+        t4 = time.perf_counter()
+        t_init += t1 - t0
+        t_iter += (t2 - t1) / n_iter
+        t_enc += t3 - t2
+        t_dec += t4 - t3
+    per_group = (t_init + T * t_iter + t_enc + t_dec) / n_groups
+    step_s = 2 * wl.G * per_group                       # K and V, every subspace
+    vectors = 2 * wl.N * (wl.D // HEAD_DIM)
+    sample_s = t_init + n_iter * t_iter + t_enc + t_dec
+    return {
+        "value": vectors / step_s, "unit": "vectors/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"float64 oracle on {n_groups} of {wl.G} K-cache subspaces of this workload: "
+                   f"init + {n_iter} GSKM iterations + encode + decode each ({sample_s:.1f} s), "
+                   f"scaled to {T} iterations x {wl.G} subspaces x (K, V)"),
+        "est_step_s": step_s,
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); this path runs on a "
+              f"single MI355X and has no multi-GPU mode", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2607_01065_amd import gsrq as B
+
+    B.load_library()
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a GPU")
+    wl = synth.WORKLOADS[args.workload]
+    N, D, d, K, T = wl.N, wl.D, wl.d, wl.K, wl.T
+    G = D // d
+    kv = synth.make_kv(wl, layer=0, seed=0)
+    dev = torch.device("cuda", 0)
+    caches = []
+    for name, X, w, seeds in (("K", kv.keys, kv.w_keys, kv.seeds_keys),
+                              ("V", kv.values, kv.w_values, kv.seeds_values)):
+        caches.append(dict(
+            name=name, X=torch.from_numpy(X).to(dev), w=torch.from_numpy(w).to(dev),
+            seeds=np.ascontiguousarray(seeds[0], dtype=np.int32),
+            gain=torch.empty((G, K), dtype=torch.float32, device=dev),
+            shape=torch.empty((G, K, d), dtype=torch.float32, device=dev),
+            assign=torch.empty((G, N), dtype=torch.int16, device=dev),
+            codes=torch.empty((N, B.code_words(N, D, d, K, 1)), dtype=torch.int32, device=dev),
+            xhat=torch.empty((N, D), dtype=torch.float16, device=dev),
+        ))
+    ws_train = torch.empty(B.train_workspace_bytes(N, D, d, K), dtype=torch.uint8, device=dev)
+    ws_enc = torch.empty(B.encode_workspace_bytes(N, D, d, K, 1), dtype=torch.uint8, device=dev)
+    iters = []
+
+    def step():
+        for c in caches:
+            r = B.train_stage(c["X"], d, K, T, seed_rows=c["seeds"], w=c["w"], gain=c["gain"],
+                              shape=c["shape"], assign=c["assign"], trace=False,
+                              workspace=ws_train)
+            iters.append(r.iters)
+            gain, shape = c["gain"][None], c["shape"][None]
+            B.encode(c["X"], gain, shape, codes=c["codes"], workspace=ws_enc)
+            B.decode(c["codes"], gain, shape, D, out=c["xhat"])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    iters.clear()
+    B.timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    tim = B.timing_read()
+    B.timing_enable(False)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    vectors = 2 * N * (D // HEAD_DIM)
+    value = vectors / (ms_per_step / 1e3)
+
+    def avg_us(kind):
+        ms, n = tim[kind]
+        return (ms / n * 1e3) if n else None
+
+    a_us, f_us, e_us, dcd_us = avg_us("assign"), avg_us("finalize"), avg_us("encode"), avg_us("decode")
+    iters_run = float(torch.stack(iters).float().mean().item()) if iters else float("nan")
+    flops_assign = 2.0 * N * D * K                         # eq. (5) scores, one pass
+    achieved = flops_assign / (a_us * 1e-6) / 1e12
+    dec_bytes = N * G * np.log2(K) / 8 + N * D * 2         # packed codes in, fp16 out
+    out = {
+        "metric": METRIC, "value": value, "unit": "vectors/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "shape": wl.note, "tokens": N, "kv_heads": D // HEAD_DIM,
+                   "head_dim": HEAD_DIM, "d": d, "K": K, "M": 1, "T": T, "caches": "K and V",
+                   "bits_per_element": B.bits_per_element(d, K, 1)},
+        "encode_vectors_per_s": (N * (D // HEAD_DIM)) / (e_us * 1e-6),
+        "gskm_iter_per_s": 1e6 / (a_us + f_us),
+        "gskm_iters_run_mean": iters_run,
+        "decode_GBps": dec_bytes / (dcd_us * 1e-6) / 1e9,
+        "decode_hbm_frac": dec_bytes / (dcd_us * 1e-6) / 1e9 / PEAK_HBM_GBPS,
+        "kernels_us": {k: {"avg_us": avg_us(k), "launches": tim[k][1]} for k in tim},
+        "roofline": {"kernel": "assign_accumulate (eq. 5 scores + argmin + weighted sums)",
+                     "bound": "mfma", "achieved": achieved, "peak": PEAK_MFMA_F16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_MFMA_F16_TFLOPS,
+                     "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(kv, wl, args.cpu_groups)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

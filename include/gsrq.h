@@ -28,8 +28,9 @@
  *    (bit p is bit p%32 of word p/32).
  *  - Supported on this build: 1 <= d <= 8, 2 <= K <= 256 (power of two).
  *    Other valid shapes return GSRQ_E_UNSUPPORTED.
- *  - The library keeps no state between calls; calls on different streams
- *    with disjoint buffers may run concurrently.
+ *  - Apart from the opt-in launch timing at the end of this header, the
+ *    library keeps no state between calls; calls on different streams with
+ *    disjoint buffers may run concurrently.
  */
 #ifndef GSRQ_H
 #define GSRQ_H
@@ -162,8 +163,9 @@ gsrq_status gsrq_encode(const gsrq_shape* s,
 
 /*
  * gsrq_decode -- reconstruction as the sum over the first M_use stages of
- * gain[m][g][k] * shape[m][g][k][:] (Sec. 3; prefix decoding, Sec. 1),
- * accumulated in float32 in stage order, stored as out_dtype (float16 by
+ * gain[m][g][k] * shape[m][g][k][:] (Sec. 3; prefix decoding, Sec. 1): each
+ * stage's codeword is rounded to float32 and the stages are summed in
+ * float32 in stage order, then stored as out_dtype (float16 by
  * round-to-nearest-even).
  *
  *  codes             [N][gsrq_code_words(s)] uint32.
@@ -174,6 +176,27 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes,
                         int32_t M_use, const float* gain, const float* shape,
                         void* Xhat, gsrq_dtype out_dtype, int64_t ldo,
                         void* stream);
+
+/* Kernel kinds reported by the optional launch timing below. */
+enum {
+  GSRQ_KERNEL_ASSIGN = 0,     /* fused assignment + weighted accumulation */
+  GSRQ_KERNEL_FINALIZE = 1,   /* codebook update + operand tiles          */
+  GSRQ_KERNEL_ENCODE = 2,     /* stage-fused encoder                      */
+  GSRQ_KERNEL_DECODE = 3,     /* gather-sum decoder                       */
+  GSRQ_KERNEL_TRANSPOSE = 4,  /* subspace-major copy of the training input */
+  GSRQ_KERNEL_KINDS = 5
+};
+
+/* Measurement hook, the library's only process state.  While enabled, every
+ * launch of the kernels above is bracketed by two HIP events recorded on the
+ * launch's stream.  Enabling clears earlier records.  Not thread-safe: enable,
+ * run and read from one host thread. */
+gsrq_status gsrq_timing_enable(int on);
+
+/* Wait for the recorded launches and return, per kernel kind k < n_kinds,
+ * the summed event-to-event time in milliseconds and the launch count; then
+ * clear the records. */
+gsrq_status gsrq_timing_read(double* total_ms, int64_t* launches, int n_kinds);
 
 #ifdef __cplusplus
 }

@@ -6,23 +6,22 @@
 // and gather-sum decoding.  How it is computed is specific to gfx950:
 //
 // Scoring (eq. 5) as an MFMA contraction.  For a subspace of dimension
-// d <= 8 and one 16-codeword tile, one v_mfma_f32_16x16x32_f16 produces the
-// squared distances ||r - g s||^2 = ||r||^2 + g^2 - 2 g s.r of 16 rows x 16
-// codewords at once: the 32-long contraction carries the dot product in a
-// hi/lo float16 split (a_hi b_hi + a_lo b_hi + a_hi b_lo, 22 significant
-// bits per operand) plus the two bias terms g^2 and ||r||^2, each split hi/lo
-// too.  Both operands are scaled by powers of two (sigma per codebook, rho
-// per row) so every float16 is in range; the scaling multiplies all
-// distances of a row by the same power of two and leaves the argmin exact.
-// The argmin runs on packed integer keys: the low 6 bits of each float32
-// distance are replaced by its (tile, slot) index and v_min3_i32 reduces two
-// keys per instruction.  Rows whose key precision cannot separate a 1e-4
-// relative top-2 margin are re-scored exactly in float64 (a rare fallback).
+// d <= 8 and one tile of 32 codewords, two chained v_mfma_f32_32x32x16_f16
+// produce the squared distances ||r - g s||^2 = ||r||^2 + g^2 - 2 g s.r of
+// 32 rows x 32 codewords.  The 32-long contraction carries the dot product
+// in a hi/lo float16 split of the codebook side (and of the row side when
+// rows are float32), plus the bias terms g^2 and ||r||^2, each split hi/lo.
+// Powers of two (sigma per codebook, rho per float32 row) keep every float16
+// in range; they scale all distances of a row by one power of two, so the
+// argmin is unchanged.  The argmin runs on packed integer keys: the low 7
+// bits of each float32 distance are replaced by its (tile, slot) index and
+// v_min3_i32 reduces two keys per instruction.  Rows whose key precision
+// cannot separate a 1e-4 relative top-2 margin are re-scored exactly in
+// float64 (a rare fallback).
 //
 // Accumulation (eqs. 6-8): per-workgroup float64 LDS accumulators of
 // sum w y, sum w x, sum w and the member count per codeword, flushed as
-// per-chunk partials and reduced in a fixed order by the finalize kernel,
-// which also rebuilds the MFMA operand tiles for the next iteration.
+// per-chunk partials and reduced in a fixed order by the update kernel.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -34,20 +33,28 @@ namespace {
 
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+typedef float f16v __attribute__((ext_vector_type(16)));
 typedef uint32_t u4 __attribute__((ext_vector_type(4)));
 
-constexpr int DP = 8;            // subvector slots per MFMA k-chunk
-constexpr int TILES = 16;        // 16 tiles x 16 codewords = K <= 256
-constexpr int KMAX = TILES * 16;
+constexpr int DP = 8;            // subvector slots of a k-chunk (d <= 8)
+constexpr int CW = 32;           // codewords per MFMA tile
+constexpr int NT = 8;            // tiles: K <= 256
+constexpr int KMAX = NT * CW;
+constexpr int RB = 32;           // rows per block (MFMA N dimension)
 constexpr int ACC = 18;          // sum w y[8], sum w x[8], W, count
 constexpr int PSTRIDE = KMAX * ACC + 2;  // + objective, changed flag
-constexpr int TRAIN_WAVES = 8;
+constexpr int TRAIN_WAVES = 12;        // one 768-thread workgroup per CU
+constexpr int WAVES_PER_SIMD = 3;      // 168 VGPRs: operand tiles stay in registers
 constexpr int TRAIN_CHUNK_ROWS = 8192;
-constexpr int ENC_WAVES = 8;      // one subspace per wave
+constexpr int ENC_WAVES = 4;           // one subspace per wave, three workgroups per CU
 constexpr int ENC_CHUNK_ROWS = 1024;
+constexpr int ENC_MAX_STAGES = 8;      // stages staged in LDS by one encode launch
 constexpr float Y_EPS = 1e-8f;            // y = x / (||x|| + eps)
 constexpr double SHAPE_KEEP_REL = 1e-6;   // keep s when ||sum w y|| <= 1e-6 W
-constexpr float PAD_BIAS = 32768.f;       // g^2 slot of a padding codeword
+constexpr float PAD_BIAS = 65504.f;       // g^2 slot of a padding codeword
+constexpr int KEY_BITS = 7;               // (tile, slot) bits packed into a key
+constexpr int SA = 12;                    // codeword operand scale 2^SA (no subnormals)
+constexpr int SB = 8;                     // float32-row operand scale 2^SB
 
 enum { MODE_INIT = 0, MODE_ITER = 1 };
 
@@ -60,39 +67,16 @@ __device__ __forceinline__ uint32_t pack2(_Float16 lo, _Float16 hi) {
 
 __device__ __forceinline__ h8 as_h8(u4 v) { return __builtin_bit_cast(h8, v); }
 
-template <typename T> __device__ __forceinline__ float to_f(T v) { return (float)v; }
-
-__device__ __forceinline__ int wave_lane() { return threadIdx.x & 63; }
-
-// Build the 8 float16 A-operand values of tile entry (lane l) for codeword k
-// of one codebook.  ex = exponent of sigma (sigma = 2^ex >= max gain).
-//   lane group q = l / 16 selects the k-chunk:
-//   q0: hi(a)   q1: lo(a)   q2: hi(a)   q3: [hi(gg) lo(gg) 1 1 0 0 0 0]
-// with a_j = -2 g s_j / sigma and gg = (g / sigma)^2.
-__device__ u4 make_a_entry(int q, bool real, float g, const float* s, int d, int ex) {
-  _Float16 v[8];
-  if (!real) {
-    for (int j = 0; j < 8; ++j) v[j] = (_Float16)0.f;
-    if (q == 3) { v[0] = (_Float16)PAD_BIAS; v[2] = (_Float16)1.f; v[3] = (_Float16)1.f; }
-  } else if (q == 3) {
-    float gs = ldexpf(g, -ex);
-    float gg = gs * gs;
-    _Float16 hi = (_Float16)gg;
-    _Float16 lo = (_Float16)(gg - (float)hi);
-    for (int j = 0; j < 8; ++j) v[j] = (_Float16)0.f;
-    v[0] = hi; v[1] = lo; v[2] = (_Float16)1.f; v[3] = (_Float16)1.f;
-  } else {
-    for (int j = 0; j < 8; ++j) {
-      float a = (j < d) ? ldexpf(-2.f * g * s[j], -ex) : 0.f;
-      _Float16 hi = (_Float16)a;
-      v[j] = (q == 1) ? (_Float16)(a - (float)hi) : hi;
-    }
-  }
+__device__ __forceinline__ u4 pack_h8(const _Float16 (&v)[8]) {
   u4 r;
   r[0] = pack2(v[0], v[1]); r[1] = pack2(v[2], v[3]);
   r[2] = pack2(v[4], v[5]); r[3] = pack2(v[6], v[7]);
   return r;
 }
+
+template <typename T> __device__ __forceinline__ float to_f(T v) { return (float)v; }
+
+__device__ __forceinline__ int wave_lane() { return threadIdx.x & 63; }
 
 __device__ __forceinline__ int sigma_exp(float maxg) {
   if (!(maxg > 0.f)) return 0;
@@ -101,108 +85,180 @@ __device__ __forceinline__ int sigma_exp(float maxg) {
   return e;
 }
 
-// One 256-thread block builds the TILES x 64 operand entries of a codebook.
-// gl/sh: gains [K] and shapes [K][d] (may live in LDS); unit_gain treats
-// every gain as 1.  red: >= 256 floats of LDS scratch.
-__device__ void build_codebook_tiles(const float* gl, const float* sh, int d, int K,
-                                     bool unit_gain, u4* frag, int* sig, float* red) {
-  const int tid = threadIdx.x;
-  float m = 0.f;
-  for (int k = tid; k < K; k += blockDim.x) m = fmaxf(m, unit_gain ? 1.f : gl[k]);
-  red[tid] = m;
-  __syncthreads();
-  for (int s = blockDim.x / 2; s > 0; s >>= 1) {
-    if (tid < s) red[tid] = fmaxf(red[tid], red[tid + s]);
-    __syncthreads();
+// Codeword operand tiles of one codebook, in registers.  Tile t covers
+// codewords 32 t + c, c = lane % 32; lane half h = lane / 32 selects the
+// k-chunk.  With a_j = -2 g s_j 2^SA / sigma and gg = (g / sigma)^2 2^SA:
+//   a1: h0 hi(a), h1 lo(a)                        (contraction k 0..15)
+//   a2: h0 hi(a), h1 [hi(gg) lo(gg) 2^SA 2^SA 0 0 0 0]   (k 16..31)
+// The 2^SA factor keeps the lo parts out of the float16 subnormal range.
+struct Tiles {
+  u4 a1[NT], a2[NT];
+};
+
+__device__ __forceinline__ void tile_entry(int h, bool real, float g, const float* s, int ex,
+                                           u4& a1, u4& a2) {
+  // padding codewords (k >= K) have g = 0 and s = 0 in the LDS copy, so only
+  // their bias slot needs a separate value
+  _Float16 hi[8], lo[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const float a = ldexpf(-2.f * g * s[j], SA - ex);
+    hi[j] = (_Float16)a;
+    lo[j] = (_Float16)(a - (float)hi[j]);
   }
-  const int ex = sigma_exp(red[0]);
-  for (int e = tid; e < TILES * 64; e += blockDim.x) {
-    const int t = e >> 6, l = e & 63;
-    const int k = t * 16 + (l & 15);
-    const bool real = k < K;
-    const float g = real ? (unit_gain ? 1.f : gl[k]) : 0.f;
-    frag[e] = make_a_entry(l >> 4, real, g, real ? sh + (size_t)k * d : sh, d, ex);
-  }
-  if (tid == 0) *sig = ex;
-  __syncthreads();
+  const float gs = ldexpf(g, -ex);
+  const float gg = ldexpf(gs * gs, SA);
+  const _Float16 gh = (_Float16)gg;
+  _Float16 bias[8];
+  bias[0] = real ? gh : (_Float16)PAD_BIAS;
+  bias[1] = real ? (_Float16)(gg - (float)gh) : (_Float16)0.f;
+  bias[2] = (_Float16)(float)(1 << SA);
+  bias[3] = (_Float16)(float)(1 << SA);
+  bias[4] = bias[5] = bias[6] = bias[7] = (_Float16)0.f;
+  a1 = pack_h8(h ? lo : hi);
+  a2 = pack_h8(h ? bias : hi);
 }
 
-// Per-row B operand.  x: the row's subvector (zero padded to 8).  ex: sigma
-// exponent.  Returns the lane's operand; sets rr (= ||x||^2 / (sigma rho))
-// and need_exact (row must go to the float64 fallback).
-__device__ __forceinline__ h8 make_b(const float (&x)[8], int ex, int q, float& rr, float& ss,
-                                     bool& need_exact) {
-  float mx = 0.f;
-  ss = 0.f;
+// Build this lane's tiles from an LDS codebook (gains [KMAX], shapes
+// [KMAX][DP], zero padded); unit_gain treats every real gain as 1.
+__device__ __forceinline__ void build_tiles(Tiles& tl, const float* cbg, const float* cbs, int K,
+                                            int ex, bool unit_gain, int lane) {
+  const int c = lane & 31, h = lane >> 5;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) { mx = fmaxf(mx, fabsf(x[j])); ss = fmaf(x[j], x[j], ss); }
-  int er = 0;
-  if (mx > 0.f) frexpf(mx, &er);
-  int sr = ex - er;                        // sigma / rho = 2^sr
-  need_exact = !(mx > 0.f) || sr > 5 || sr < -12 || !(ss < 3.0e38f);
-  sr = sr < -12 ? -12 : (sr > 14 ? 14 : sr);
-  rr = ldexpf(ss, -(ex + er));
-  rr = fminf(rr, 60000.f);
-  h8 b;
-  if (q == 3) {
-    const _Float16 sc = (_Float16)ldexpf(1.f, sr);
-    const _Float16 hi = (_Float16)rr;
-    const _Float16 lo = (_Float16)(rr - (float)hi);
-    b[0] = sc; b[1] = sc; b[2] = hi; b[3] = lo;
-    b[4] = b[5] = b[6] = b[7] = (_Float16)0.f;
+  for (int t = 0; t < NT; ++t) {
+    const int k = t * CW + c;
+    const bool real = k < K;
+    tile_entry(h, real, unit_gain ? 1.f : cbg[k], cbs + k * DP, ex, tl.a1[t], tl.a2[t]);
+  }
+}
+
+// Row-side operands of one row (this lane's row).
+// F16ROWS: the row is exactly float16 (raw16), so it enters the contraction
+// as is (rho = 1, no lo part):
+//   b1 = x,  b2: h0 0, h1 [sigma sigma hi(rr) lo(rr) 0 0 0 0],
+//   rr = ||x||^2 / sigma, giving D = 2^SA dist / sigma.
+// Otherwise (float32 rows x, zero padded) rho = 2^er >= max|x| and
+//   b = x 2^SB / rho, b1 = hi(b),
+//   b2: h0 lo(b), h1 [2^SB sigma/rho (twice) hi(rr) lo(rr) 0 0 0 0],
+//   rr = 2^SB ||x||^2 / (sigma rho), giving D = 2^(SA+SB) dist / (sigma rho).
+// In both cases D <= 2^(SA+1) rr means dist <= 2 ||x||^2.  need_exact flags
+// rows whose operands leave the float16 range.
+template <bool F16ROWS>
+__device__ __forceinline__ void make_b(const float (&x)[8], u4 raw16, int ex, int h, h8& b1,
+                                       h8& b2, float& rr, bool& need_exact) {
+  float ss;
+  int sr;
+  if (F16ROWS) {
+    // ||x||^2 from packed float16 dot products (exact products, float32 sums)
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      // copy the element first: a bit_cast of a vector element reads the
+      // wrong element with this compiler
+      const uint32_t wj = raw16[j];
+      const h2 v = __builtin_bit_cast(h2, wj);
+      ss = __builtin_amdgcn_fdot2(v, v, ss, false);
+    }
+    sr = ex;
+    rr = ldexpf(ss, -ex);
+    need_exact = ex > 15 || ex < -14 || !(rr < 32768.f);
   } else {
+    float mx = 0.f;
+    ss = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) { mx = fmaxf(mx, fabsf(x[j])); ss = fmaf(x[j], x[j], ss); }
+    int er = 0;
+    frexpf(mx, &er);
+    sr = ex - er + SB;
+    rr = ldexpf(ss, SB - ex - er);
+    need_exact = !(mx > 0.f) || sr > 15 || sr < -14 || !(rr < 32768.f);
+    _Float16 hi[8], lo[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
-      const float v = ldexpf(x[j], -er);
-      const _Float16 hi = (_Float16)v;
-      b[j] = (q == 2) ? (_Float16)(v - (float)hi) : hi;
+      const float v = ldexpf(x[j], SB - er);
+      hi[j] = (_Float16)v;
+      lo[j] = (_Float16)(v - (float)hi[j]);
     }
+    b1 = as_h8(pack_h8(hi));
+    raw16 = pack_h8(lo);
   }
-  return b;
+  rr = fminf(rr, 32768.f);
+  sr = sr < -14 ? -14 : (sr > 15 ? 15 : sr);
+  const _Float16 sc = (_Float16)ldexpf(1.f, sr);
+  const _Float16 rh = (_Float16)rr;
+  const _Float16 rl = (_Float16)(rr - (float)rh);
+  const u4 bias = (u4){pack2(sc, sc), pack2(rh, rl), 0u, 0u};
+  if (F16ROWS) {
+    b1 = as_h8(raw16);
+    b2 = as_h8(h ? bias : (u4){0u, 0u, 0u, 0u});
+  } else {
+    b2 = as_h8(h ? bias : raw16);   // raw16 holds lo(b) here
+  }
 }
 
-// 16 MFMA tiles -> the lane's minimum packed key over its 64 codewords.
-// key = (bits(dist) & ~63) | (tile << 2 | slot); the lane's lane group q
-// fixes the remaining index bits (k = 16 tile + 4 q + slot).
-__device__ __forceinline__ int min_key(const u4 (&af)[TILES], h8 b) {
-  const f4 zero = {0.f, 0.f, 0.f, 0.f};
-  f4 c[TILES];
-  // all products first so the scheduler can overlap MFMA latency with the
-  // integer epilogue of earlier tiles
+// Minimum packed key of one tile: the low KEY_BITS bits of each distance
+// are replaced by the slot j (an inline constant), the 16 keys reduced with
+// v_min3, and the tile number OR'd in once (all keys of a tile share it, so
+// the order is unchanged).
+__device__ __forceinline__ int min3i(int a, int b, int c) {
+  int r;
+  asm volatile("v_min3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+__device__ __forceinline__ int tile_min(const f16v& c, int t) {
+  constexpr int MASK = ~((1 << KEY_BITS) - 1);
+  int m = min3i((__float_as_int(c[0]) & MASK) | 0, (__float_as_int(c[1]) & MASK) | 1,
+                (__float_as_int(c[2]) & MASK) | 2);
 #pragma unroll
-  for (int t = 0; t < TILES; ++t)
-    c[t] = __builtin_amdgcn_mfma_f32_16x16x32_f16(as_h8(af[t]), b, zero, 0, 0, 0);
+  for (int j = 3; j < 15; j += 2)
+    m = min3i(m, (__float_as_int(c[j]) & MASK) | j, (__float_as_int(c[j + 1]) & MASK) | (j + 1));
+  m = min(m, (__float_as_int(c[15]) & MASK) | 15);
+  return m | (t << 4);
+}
+
+// All NT tiles -> the lane's minimum packed key over its 128 codewords.
+// Lane l holds distances of codewords 32 t + 8 (j / 4) + 4 h + j % 4 of
+// row l % 32.  The two k-chunks of a tile accumulate in place; the MFMA
+// latency is hidden by the other waves on the SIMD.
+__device__ __forceinline__ int min_key(const Tiles& tl, h8 b1, h8 b2) {
+  const f16v zero = {};
   int best = 0x7fffffff;
 #pragma unroll
-  for (int t = 0; t < TILES; ++t) {
-    const int k0 = (__float_as_int(c[t][0]) & ~63) | (t * 4 + 0);
-    const int k1 = (__float_as_int(c[t][1]) & ~63) | (t * 4 + 1);
-    const int k2 = (__float_as_int(c[t][2]) & ~63) | (t * 4 + 2);
-    const int k3 = (__float_as_int(c[t][3]) & ~63) | (t * 4 + 3);
-    best = min(min(best, k0), min(k1, min(k2, k3)));
+  for (int t = 0; t < NT; t += 2) {
+    f16v c0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(tl.a1[t]), b1, zero, 0, 0, 0);
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(tl.a2[t]), b2, c0, 0, 0, 0);
+    const int m0 = tile_min(c0, t);
+    f16v c1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(tl.a1[t + 1]), b1, zero, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(tl.a2[t + 1]), b2, c1, 0, 0, 0);
+    best = min3i(best, m0, tile_min(c1, t + 1));
   }
   return best;
 }
 
-// Combine the four lane groups of each row: smallest distance key, ties to
+// Combine the two lane halves of each row: smallest distance key, ties to
 // the lowest codeword index.  Returns the codeword; dhat = approximate
 // scaled distance of the winner.
-__device__ __forceinline__ int reduce_rows(int key, int q, float& dhat) {
-  const int kidx = ((key & 63) >> 2) * 16 + q * 4 + (key & 3);
-  long long v = (long long)(key >> 6) * 4294967296ll + (long long)kidx;
-  long long o = __shfl_xor(v, 16);
-  v = o < v ? o : v;
-  o = __shfl_xor(v, 32);
-  v = o < v ? o : v;
-  dhat = __int_as_float((int)(v >> 32) << 6);
+__device__ __forceinline__ int reduce_rows(int key, int h, float& dhat) {
+  const int idx = key & ((1 << KEY_BITS) - 1);
+  const int t = idx >> 4, j = idx & 15;
+  const int kidx = t * CW + (j >> 2) * 8 + h * 4 + (j & 3);
+  const int hi = key >> KEY_BITS;
+  const auto sh = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+  const auto sk = __builtin_amdgcn_permlane32_swap(kidx, kidx, false, false);
+  // both halves see (own, partner) in some order and choose identically
+  const long long v0 = (long long)(int)sh[0] * 4294967296ll + (long long)(unsigned)sk[0];
+  const long long v1 = (long long)(int)sh[1] * 4294967296ll + (long long)(unsigned)sk[1];
+  const long long v = v0 < v1 ? v0 : v1;
+  dhat = __int_as_float((int)(v >> 32) << KEY_BITS);
   return (int)(v & 0xffffffffll);
 }
 
 // Exact float64 argmin over all K codewords for the rows flagged in `mask`
-// (one bit per lane of lane group 0; bit i = row i of the block).  gain /
-// shape: this codebook, [K] / [K][ld] with d used elements per row (any
-// memory).  Every lane of the wave takes part; the lanes of a flagged row
-// receive its codeword in kstar.
+// (bit i = row i of the block, lanes 0..31).  gain / shape: this codebook,
+// [K] / [K][ld] with d used elements per row (any memory).  Every lane of
+// the wave takes part; both lanes of a flagged row receive its codeword.
 __device__ __forceinline__ void exact_rows(unsigned long long mask, const float (&x)[8], int d,
                                            int ld, int K, const float* gain, const float* shape,
                                            bool unit_gain, int& kstar) {
@@ -232,8 +288,83 @@ __device__ __forceinline__ void exact_rows(unsigned long long mask, const float 
       const int ok = __shfl_xor(bk, off);
       if (od < bd || (od == bd && ok < bk)) { bd = od; bk = ok; }
     }
-    if ((lane & 15) == L) kstar = bk;
+    if ((lane & 31) == L) kstar = bk;
   }
+}
+
+// Eight subvector elements of one row in their storage type, kept packed in
+// registers between a prefetch and their use.
+template <typename T> struct RowVec;
+template <> struct RowVec<_Float16> {
+  u4 v;
+  __device__ __forceinline__ void load(const _Float16* p) { v = *(const u4*)p; }
+  __device__ __forceinline__ void zero() { v = (u4){0u, 0u, 0u, 0u}; }
+  __device__ __forceinline__ void get(float (&x)[8]) const {
+    const h8 hv = as_h8(v);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = (float)hv[j];
+  }
+  __device__ __forceinline__ u4 raw16() const { return v; }
+};
+template <> struct RowVec<float> {
+  u4 v0, v1;
+  __device__ __forceinline__ void load(const float* p) {
+    v0 = ((const u4*)p)[0];
+    v1 = ((const u4*)p)[1];
+  }
+  __device__ __forceinline__ void zero() { v0 = v1 = (u4){0u, 0u, 0u, 0u}; }
+  __device__ __forceinline__ void get(float (&x)[8]) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = __uint_as_float(v0[j]);
+      x[4 + j] = __uint_as_float(v1[j]);
+    }
+  }
+  __device__ __forceinline__ u4 raw16() const { return (u4){0u, 0u, 0u, 0u}; }
+};
+
+// One codeword (gain, shape padded to DP) read without branches: indices
+// are clamped to valid entries and the padding is applied to the values.
+__device__ __forceinline__ void read_codeword(const float* gain, const float* shape, int d, int K,
+                                              int k, bool unit_gain, float& g, float (&sv)[DP]) {
+  const int kk = k < K ? k : K - 1;
+  const bool real = k < K;
+  const float gr = unit_gain ? 1.f : gain[kk];
+  g = real ? gr : 0.f;
+  const float* sp = shape + (size_t)kk * d;
+  if (d == DP && (((uintptr_t)sp) & 15) == 0) {
+    const f4 lo4 = ((const f4*)sp)[0], hi4 = ((const f4*)sp)[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      sv[j] = real ? lo4[j] : 0.f;
+      sv[4 + j] = real ? hi4[j] : 0.f;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < DP; ++j) {
+      const float v = sp[j < d ? j : 0];
+      sv[j] = (real && j < d) ? v : 0.f;
+    }
+  }
+}
+
+// Load a codebook (gain [K], shape [K][d]) into zero-padded LDS arrays and
+// return sigma's exponent (every thread of the block calls this).
+__device__ int load_codebook(const float* gain, const float* shape, int d, int K, bool unit_gain,
+                             float* cbg, float* cbs, int* red) {
+  const int tid = threadIdx.x;
+  if (tid == 0) *red = 0;
+  __syncthreads();
+  for (int k = tid; k < KMAX; k += blockDim.x) {
+    float g, sv[DP];
+    read_codeword(gain, shape, d, K, k, unit_gain, g, sv);
+    cbg[k] = g;
+#pragma unroll
+    for (int j = 0; j < DP; ++j) cbs[k * DP + j] = sv[j];
+    if (g > 0.f) atomicMax(red, __float_as_int(g));   // gains >= 0 order as ints
+  }
+  __syncthreads();
+  return sigma_exp(__int_as_float(*red));
 }
 
 // ---------------------------------------------------------------- kernels
@@ -288,14 +419,25 @@ __global__ void seed_kernel(const T* __restrict__ Xt, int64_t N, int d, int K,
   }
 }
 
-// Operand tiles for ncb codebooks (gain [ncb][K], shape [ncb][K][d]).
-__global__ void tiles_kernel(const float* __restrict__ gain, const float* __restrict__ shape,
-                             int d, int K, int unit_gain, u4* __restrict__ frag,
-                             int* __restrict__ sig) {
-  __shared__ float red[256];
+// Operand tiles for ncb codebooks into a table (used by multi-stage encode).
+__global__ void __launch_bounds__(64) tiles_kernel(const float* __restrict__ gain,
+                                                   const float* __restrict__ shape, int d, int K,
+                                                   u4* __restrict__ frag, int* __restrict__ sig) {
+  __shared__ float cbg[KMAX];
+  __shared__ float cbs[KMAX * DP];
+  __shared__ int red;
   const int cb = blockIdx.x;
-  build_codebook_tiles(gain + (size_t)cb * K, shape + (size_t)cb * K * d, d, K, unit_gain != 0,
-                       frag + (size_t)cb * TILES * 64, sig + cb, red);
+  const int ex = load_codebook(gain + (size_t)cb * K, shape + (size_t)cb * K * d, d, K, false,
+                               cbg, cbs, &red);
+  Tiles tl;
+  build_tiles(tl, cbg, cbs, K, ex, false, threadIdx.x);
+  u4* fr = frag + (size_t)cb * NT * 2 * 64;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    fr[(t * 2 + 0) * 64 + threadIdx.x] = tl.a1[t];
+    fr[(t * 2 + 1) * 64 + threadIdx.x] = tl.a2[t];
+  }
+  if (threadIdx.x == 0) sig[cb] = ex;
 }
 
 struct AssignArgs {
@@ -305,108 +447,123 @@ struct AssignArgs {
   const float* w;        // [N] or null
   const float* gain;     // [G][K]
   const float* shape;    // [G][K][d]
-  const u4* frag;        // [G][TILES*64]
-  const int* sig;        // [G]
   uint16_t* assign;      // [G][N]
   const int* done;       // [G]
   double* part;          // [G][chunks][PSTRIDE]
   int chunks;
   int force_changed;
+  int want_obj;          // accumulate the objective (for the trace)
 };
 
 // Fused assignment (eq. 5) + weighted accumulation (eqs. 6-8) for one
 // (chunk of rows, subspace).  MODE_INIT scores with unit gains (largest
-// projection) for the gain initialisation.
+// projection) for the gain initialisation.  Each wave walks 32-row blocks
+// and prefetches the next block's rows, weights and previous codes while
+// scoring the current one.
 template <typename T, int MODE>
-__global__ void __launch_bounds__(TRAIN_WAVES * 64)
+__global__ void __launch_bounds__(TRAIN_WAVES * 64, WAVES_PER_SIMD)
 assign_accumulate_kernel(AssignArgs a) {
+  constexpr bool F16ROWS = sizeof(T) == 2;
   __shared__ double acc[KMAX * ACC];
   __shared__ float cbg[KMAX];
   __shared__ float cbs[KMAX * DP];
   __shared__ double objw[TRAIN_WAVES];
-  __shared__ int changed;
+  __shared__ uint16_t codes_l[TRAIN_CHUNK_ROWS];   // this chunk's new assignment
+  __shared__ int changed, red;
 
   const int g = blockIdx.y;
   const int chunk = blockIdx.x;
   if (a.done[g]) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int i = lane & 15, q = lane >> 4;
+  const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K;
 
   for (int e = tid; e < KMAX * ACC; e += blockDim.x) acc[e] = 0.0;
-  for (int k = tid; k < KMAX; k += blockDim.x) {
-    cbg[k] = (k < K) ? (MODE == MODE_INIT ? 1.f : a.gain[(size_t)g * K + k]) : 0.f;
-    for (int j = 0; j < DP; ++j)
-      cbs[k * DP + j] = (k < K && j < d) ? a.shape[((size_t)g * K + k) * d + j] : 0.f;
-  }
   if (tid == 0) changed = a.force_changed;
-
-  u4 af[TILES];
-  const u4* fr = a.frag + (size_t)g * TILES * 64;
-#pragma unroll
-  for (int t = 0; t < TILES; ++t) af[t] = fr[t * 64 + lane];
-  const int ex = a.sig[g];
-  __syncthreads();
+  const int ex = load_codebook(a.gain + (size_t)g * K, a.shape + (size_t)g * K * d, d, K,
+                               MODE == MODE_INIT, cbg, cbs, &red);
+  Tiles tl;
+  build_tiles(tl, cbg, cbs, K, ex, MODE == MODE_INIT, lane);
 
   const T* xt = (const T*)a.xt + (size_t)g * a.N * 8;
+  uint16_t* asg = a.assign + (size_t)g * a.N;
   const int64_t row_begin = (int64_t)chunk * TRAIN_CHUNK_ROWS;
   int64_t row_end = row_begin + TRAIN_CHUNK_ROWS;
   if (row_end > a.N) row_end = a.N;
-  const int nblk = (int)((row_end - row_begin + 15) / 16);
+  const int nblk = (int)((row_end - row_begin + RB - 1) / RB);
+
+  // loads never branch: past the end they read the chunk's first row and
+  // the values are masked where they are used, so prefetches stay in flight
+  const float one = 1.f;
+  const float* wp = a.w ? a.w : &one;
+  const int64_t wstride = a.w ? 1 : 0;
+  RowVec<T> nx;
+  float nw = 0.f;
+  uint16_t nold = 0;
+  auto fetch = [&](int rb) {
+    int64_t row = row_begin + (int64_t)rb * RB + i;
+    row = row < row_end ? row : row_begin;
+    nx.load(xt + row * 8);
+    nw = wp[row * wstride];
+    if (MODE == MODE_ITER) nold = asg[row];
+  };
+  if (wave < nblk) fetch(wave);
+
   double obj = 0.0;
   bool any_changed = false;
-
   for (int rb = wave; rb < nblk; rb += TRAIN_WAVES) {
-    const int64_t row = row_begin + (int64_t)rb * 16 + i;
+    const int64_t row = row_begin + (int64_t)rb * RB + i;
     const bool valid = row < row_end;
     float x[8];
-    if (valid) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) x[j] = to_f(xt[row * 8 + j]);
-    } else {
+    nx.get(x);
+    u4 raw = nx.raw16();
+    if (!valid) {
 #pragma unroll
       for (int j = 0; j < 8; ++j) x[j] = 0.f;
+      raw = (u4){0u, 0u, 0u, 0u};
     }
-    float rr, ss;
+    const float wcur = nw;
+    const uint16_t old = nold;
+    if (rb + TRAIN_WAVES < nblk) fetch(rb + TRAIN_WAVES);
+
+    h8 b1, b2;
+    float rr;
     bool need_exact;
-    const h8 b = make_b(x, ex, q, rr, ss, need_exact);
-    const int key = min_key(af, b);
+    make_b<F16ROWS>(x, raw, ex, h, b1, b2, rr, need_exact);
+    const int key = min_key(tl, b1, b2);
     float dhat;
-    int kstar = reduce_rows(key, q, dhat);
-    need_exact = need_exact || !(dhat <= 2.f * rr) || kstar >= K;
-    const unsigned long long fb = __ballot(valid && need_exact && q == 0);
+    int kstar = reduce_rows(key, h, dhat);
+    need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
+    const unsigned long long fb = __ballot(valid && need_exact && h == 0);
     if (fb) exact_rows(fb, x, d, DP, K, cbg, cbs, MODE == MODE_INIT, kstar);
     if (kstar >= K) kstar = K - 1;   // only tail rows past N can get here
-    // chosen-codeword distance, exact in float32 (objective)
-    const float gk = cbg[kstar];
-    float dist = 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float r = fmaf(-gk, cbs[kstar * DP + j], x[j]);
-      dist = fmaf(r, r, dist);
-    }
     if (valid) {
-      const double wv = a.w ? (double)a.w[row] : 1.0;
-      const float inv = 1.f / (sqrtf(ss) + Y_EPS);
-      // lane group q adds slots 4q..4q+3: q0/q1 the y half-vectors,
-      // q2/q3 the x half-vectors; q0 also adds W, q1 the member count
+      // lane half 0 adds w y (y = x / ||x||) and W, half 1 adds w x and the
+      // member count
       double* ak = acc + kstar * ACC;
-      const float sc = (q < 2) ? inv : 1.f;
-      // bitwise select keeps x in registers (a conditional would become a
-      // dynamically indexed private array)
-      const int hm = -(q & 1);
-      float xv[4];
+      float ss = 0.f;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        xv[j] = __int_as_float((__float_as_int(x[4 + j]) & hm) | (__float_as_int(x[j]) & ~hm));
+      for (int j = 0; j < 8; ++j) ss = fmaf(x[j], x[j], ss);
+      const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
+      const float sc = h ? wcur : wcur * inv;
 #pragma unroll
-      for (int j = 0; j < 4; ++j) unsafeAtomicAdd(ak + 4 * q + j, wv * (double)(xv[j] * sc));
-      if (q < 2) unsafeAtomicAdd(ak + 16 + q, q == 0 ? wv : 1.0);
-      if (q == 0) {
-        obj += wv * (double)dist;
-        uint16_t* ap = a.assign + (size_t)g * a.N + row;
-        if (MODE == MODE_ITER && *ap != (uint16_t)kstar) any_changed = true;
-        *ap = (uint16_t)kstar;
+      for (int j = 0; j < 8; ++j) unsafeAtomicAdd(ak + 8 * h + j, (double)(x[j] * sc));
+      unsafeAtomicAdd(ak + 16 + h, h ? 1.0 : (double)wcur);
+      if (h == 0) {
+        if (a.want_obj) {
+          const float gk = cbg[kstar];
+          float dist = 0.f;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float r = fmaf(-gk, cbs[kstar * DP + j], x[j]);
+            dist = fmaf(r, r, dist);
+          }
+          obj += (double)wcur * (double)dist;
+        }
+        if (MODE == MODE_ITER && old != (uint16_t)kstar) any_changed = true;
+        // global stores would share vmcnt with the prefetch and stall the
+        // next block, so codes go to LDS and leave in one pass at the end
+        codes_l[row - row_begin] = (uint16_t)kstar;
       }
     }
   }
@@ -416,6 +573,7 @@ assign_accumulate_kernel(AssignArgs a) {
   if (lane == 0) objw[wave] = obj;
   if (__ballot(any_changed) && lane == 0) atomicOr(&changed, 1);
   __syncthreads();
+  for (int64_t r = row_begin + tid; r < row_end; r += blockDim.x) asg[r] = codes_l[r - row_begin];
   double* out = a.part + ((size_t)g * a.chunks + chunk) * PSTRIDE;
   for (int e = tid; e < KMAX * ACC; e += blockDim.x) out[e] = acc[e];
   if (tid == 0) {
@@ -434,92 +592,67 @@ struct FinalizeArgs {
   const float* seednorm;  // [G][K]
   float* gain;            // [G][K]
   float* shape;           // [G][K][d]
-  u4* frag;
-  int* sig;
   int* done;              // [G]
   int* iters;             // [G]
   double* trace;          // [G][T] or null
 };
 
-// Codebook update from the partial sums of every chunk (fixed order):
-// init: eq. (8) gains for the seed shapes; iteration: eqs. (7) and (8).
-// Then the stop test and the operand tiles of the new codebook.
+// Codebook update from the partial sums of every chunk (fixed order), one
+// thread per codeword: init: eq. (8) gains for the seed shapes; iteration:
+// eqs. (7) and (8).  Thread 0 of each subspace also applies the stop test.
 template <int MODE>
-__global__ void __launch_bounds__(256) finalize_kernel(FinalizeArgs a) {
-  __shared__ float gl[KMAX];
-  __shared__ float sh[KMAX * DP];
-  __shared__ float red[256];
-  __shared__ double objc[2];
-  const int g = blockIdx.x;
+__global__ void __launch_bounds__(64) finalize_kernel(FinalizeArgs a) {
+  const int g = blockIdx.y;
   if (MODE == MODE_ITER && a.done[g]) return;
-  const int k = threadIdx.x;
+  const int k = blockIdx.x * 64 + threadIdx.x;
   const int d = a.d, K = a.K;
   if (k < K) {
     double s[ACC];
+#pragma unroll
     for (int e = 0; e < ACC; ++e) s[e] = 0.0;
     for (int c = 0; c < a.chunks; ++c) {
       const double* p = a.part + ((size_t)g * a.chunks + c) * PSTRIDE + (size_t)k * ACC;
+#pragma unroll
       for (int e = 0; e < ACC; ++e) s[e] += p[e];
     }
     float* sk = a.shape + ((size_t)g * K + k) * d;
     float* gk = a.gain + (size_t)g * K + k;
     double sn[DP];
+#pragma unroll
     for (int j = 0; j < DP; ++j) sn[j] = (j < d) ? (double)sk[j] : 0.0;
     double gnew = (MODE == MODE_INIT) ? (double)a.seednorm[(size_t)g * K + k] : (double)*gk;
     const double W = s[16];
     if (W > 0.0) {
       if (MODE == MODE_ITER) {
         double mn = 0.0;
-        for (int j = 0; j < d; ++j) mn = fma(s[j], s[j], mn);
+#pragma unroll
+        for (int j = 0; j < DP; ++j) mn = fma(s[j], s[j], mn);
         mn = sqrt(mn);
-        if (mn > SHAPE_KEEP_REL * W)
-          for (int j = 0; j < d; ++j) sn[j] = s[j] / mn;
+        if (mn > SHAPE_KEEP_REL * W) {
+#pragma unroll
+          for (int j = 0; j < DP; ++j) sn[j] = s[j] / mn;
+        }
       }
       double pr = 0.0;
-      for (int j = 0; j < d; ++j) pr = fma(s[8 + j], sn[j], pr);
+#pragma unroll
+      for (int j = 0; j < DP; ++j) pr = fma(s[8 + j], sn[j], pr);
       gnew = fmax(0.0, pr / W);
     }
-    for (int j = 0; j < d; ++j) sk[j] = (float)sn[j];
+#pragma unroll
+    for (int j = 0; j < DP; ++j)
+      if (j < d) sk[j] = (float)sn[j];
     *gk = (float)gnew;
-    gl[k] = (float)gnew;
-    for (int j = 0; j < DP; ++j) sh[k * DP + j] = (j < d) ? (float)sn[j] : 0.f;
   }
-  if (k == 0) {
+  if (MODE == MODE_ITER && blockIdx.x == 0 && threadIdx.x == 0) {
     double obj = 0.0, ch = 0.0;
     for (int c = 0; c < a.chunks; ++c) {
       const double* p = a.part + ((size_t)g * a.chunks + c) * PSTRIDE + KMAX * ACC;
       obj += p[0];
       ch = fmax(ch, p[1]);
     }
-    objc[0] = obj;
-    objc[1] = ch;
-    if (MODE == MODE_ITER) {
-      if (a.trace) a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
-      a.iters[g] = a.t;
-      if (ch == 0.0 && !a.no_early_stop) a.done[g] = 1;
-    }
-  }
-  __syncthreads();
-  // operand tiles read the float32 codebook just stored (LDS copy, stride DP)
-  {
-    const int tid = threadIdx.x;
-    float m = 0.f;
-    for (int kk = tid; kk < K; kk += blockDim.x) m = fmaxf(m, gl[kk]);
-    red[tid] = m;
-    __syncthreads();
-    for (int s2 = blockDim.x / 2; s2 > 0; s2 >>= 1) {
-      if (tid < s2) red[tid] = fmaxf(red[tid], red[tid + s2]);
-      __syncthreads();
-    }
-    const int ex = sigma_exp(red[0]);
-    u4* fr = a.frag + (size_t)g * TILES * 64;
-    for (int e = tid; e < TILES * 64; e += blockDim.x) {
-      const int t = e >> 6, l = e & 63;
-      const int kk = t * 16 + (l & 15);
-      const bool real = kk < K;
-      fr[e] = make_a_entry(l >> 4, real, real ? gl[kk] : 0.f, real ? sh + kk * DP : sh, d, ex);
-    }
-    if (tid == 0) a.sig[g] = ex;
+    if (a.trace) a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
+    a.iters[g] = a.t;
+    if (ch == 0.0 && !a.no_early_stop) a.done[g] = 1;
   }
 }
 
@@ -529,66 +662,162 @@ struct EncodeArgs {
   int d, K, G, M, b, words;
   const float* gain;     // [M][G][K]
   const float* shape;    // [M][G][K][d]
-  const u4* frag;        // [M*G][TILES*64]
+  const u4* frag;        // [M*G][NT][2][64] (multi-stage only)
   const int* sig;        // [M*G]
   uint32_t* codes;       // [N][words] or null
   float* residual;       // [N][D] or null
   int byte_codes;        // b == 8: plain byte stores, else atomic OR
+  int lds_codes;         // byte codes of 4 whole subspaces per block: LDS-staged
+  int vec_rows;          // d == 8 and 16-byte aligned rows: vector loads
 };
 
-// Stage-fused encoder: one subspace per wave, the residual of a 16-row block
-// stays in registers through all M stages.
-template <typename T, bool MULTI>
-__global__ void __launch_bounds__(ENC_WAVES * 64) encode_kernel(EncodeArgs a) {
+// A row's subvector from row-major X, loaded raw (prefetch) and widened
+// later.  VEC: d == 8 with 16-byte aligned rows (vector loads); otherwise d
+// scalar loads with clamped indices.  Neither form branches.
+template <typename T, bool VEC> struct RowRaw {
+  T v[8];
+  __device__ __forceinline__ void load(const T* p, int d) {
+    if (VEC) {
+      if (sizeof(T) == 2) {
+        *(u4*)v = *(const u4*)p;
+      } else {
+        ((u4*)v)[0] = ((const u4*)p)[0];
+        ((u4*)v)[1] = ((const u4*)p)[1];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) v[j] = p[j < d ? j : 0];
+    }
+  }
+  __device__ __forceinline__ void get(float (&x)[8], int d, bool valid) const {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) x[j] = (valid && (VEC || j < d)) ? (float)v[j] : 0.f;
+  }
+  __device__ __forceinline__ u4 raw16(const float (&x)[8], bool valid) const {
+    // the exact float16 operand: the loaded bits when they are the whole
+    // (valid, 8-wide) row, else rebuilt from the masked float copy
+    if (VEC && sizeof(T) == 2) {
+      const u4 r = *(const u4*)v;
+      return valid ? r : (u4){0u, 0u, 0u, 0u};
+    }
+    _Float16 hv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) hv[j] = (_Float16)x[j];
+    return pack_h8(hv);
+  }
+};
+
+// Stage-fused encoder: one subspace per wave; the residual of a 32-row block
+// stays in registers through all M stages.  A single-stage launch keeps the
+// wave's codebook in LDS and its operand tiles in registers for the whole
+// launch; a multi-stage launch reloads each stage's tiles from a table.
+template <typename T, bool MULTI, bool VEC>
+__global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(EncodeArgs a) {
+  constexpr bool F16IN = sizeof(T) == 2;
+  __shared__ float cbl[MULTI ? 1 : ENC_WAVES * KMAX * (DP + 1)];
+  // byte codes of this block, [stage][row][wave]; written out at the end so
+  // that no global store sits in the loop (stores share vmcnt with loads)
+  __shared__ uint32_t codes_l[(MULTI ? ENC_MAX_STAGES : 1) * ENC_CHUNK_ROWS];
   const int lane = wave_lane(), wave = threadIdx.x >> 6;
   const int g = blockIdx.y * ENC_WAVES + wave;
-  if (g >= a.G) return;
-  const int i = lane & 15, q = lane >> 4;
+  const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K, G = a.G;
-  u4 af[TILES];
-  if (!MULTI) {
-    const u4* fr = a.frag + (size_t)g * TILES * 64;
-#pragma unroll
-    for (int t = 0; t < TILES; ++t) af[t] = fr[t * 64 + lane];
-  }
+  const bool gvalid = g < G;
   const int64_t row_begin = (int64_t)blockIdx.x * ENC_CHUNK_ROWS;
-  int64_t row_end = row_begin + ENC_CHUNK_ROWS;
-  if (row_end > a.N) row_end = a.N;
+  const int64_t row_end = row_begin + ENC_CHUNK_ROWS < a.N ? row_begin + ENC_CHUNK_ROWS : a.N;
+  float* mg = cbl + (MULTI ? 0 : wave * KMAX * (DP + 1));   // gains [KMAX]
+  float* ms = mg + KMAX;                                      // shapes [KMAX][DP]
+  Tiles tl;
+  int ex0 = 0;
+  if (!MULTI) {
+    // this wave's codebook into its LDS slice; sigma from the max gain
+    float m = 0.f;
+    const int gc = gvalid ? g : 0;
+    for (int k = lane; k < KMAX; k += 64) {
+      float gv, sv[DP];
+      read_codeword(a.gain + (size_t)gc * K, a.shape + (size_t)gc * K * d, d, K, k, false, gv,
+                    sv);
+      mg[k] = gv;
+      m = fmaxf(m, gv);
+#pragma unroll
+      for (int j = 0; j < DP; ++j) ms[k * DP + j] = sv[j];
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    ex0 = sigma_exp(m);
+    __syncthreads();
+    build_tiles(tl, mg, ms, K, ex0, false, lane);
+  }
+  const bool lds_codes = a.lds_codes != 0;
+  if (!gvalid) {
+    // the flush at the end needs every wave at its barrier
+    __syncthreads();
+    goto flush;
+  }
+  {
   const T* X = (const T*)a.x;
-  for (int64_t r0 = row_begin; r0 < row_end; r0 += 16) {
+  RowRaw<T, VEC> nx;
+  auto fetch = [&](int64_t r0) {
+    int64_t row = r0 + i;
+    row = row < row_end ? row : row_begin;
+    nx.load(X + row * a.ldx + (int64_t)g * d, d);
+  };
+  fetch(row_begin);
+  for (int64_t r0 = row_begin; r0 < row_end; r0 += RB) {
     const int64_t row = r0 + i;
     const bool valid = row < row_end;
     float x[8];
-    const T* src = X + row * a.ldx + (int64_t)g * d;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] = (valid && j < d) ? to_f(src[j]) : 0.f;
+    nx.get(x, d, valid);
+    const u4 raw = nx.raw16(x, valid);
+    if (r0 + RB < row_end) fetch(r0 + RB);
     for (int m = 0; m < a.M; ++m) {
       const int cb = m * G + g;
+      int ex = ex0;
       if (MULTI) {
-        const u4* fr = a.frag + (size_t)cb * TILES * 64;
+        const u4* fr = a.frag + (size_t)cb * NT * 2 * 64;
 #pragma unroll
-        for (int t = 0; t < TILES; ++t) af[t] = fr[t * 64 + lane];
+        for (int t = 0; t < NT; ++t) {
+          tl.a1[t] = fr[(t * 2 + 0) * 64 + lane];
+          tl.a2[t] = fr[(t * 2 + 1) * 64 + lane];
+        }
+        ex = a.sig[cb];
       }
-      const int ex = a.sig[cb];
-      float rr, ss;
+      h8 b1, b2;
+      float rr;
       bool need_exact;
-      const h8 b = make_b(x, ex, q, rr, ss, need_exact);
-      const int key = min_key(af, b);
+      // after the first stage the residual is no longer float16-exact
+      if (F16IN && m == 0)
+        make_b<true>(x, raw, ex, h, b1, b2, rr, need_exact);
+      else
+        make_b<false>(x, raw, ex, h, b1, b2, rr, need_exact);
+      const int key = min_key(tl, b1, b2);
       float dhat;
-      int kstar = reduce_rows(key, q, dhat);
-      need_exact = need_exact || !(dhat <= 2.f * rr) || kstar >= K;
-      const float* gcb = a.gain + (size_t)cb * K;
-      const float* scb = a.shape + (size_t)cb * K * d;
-      const unsigned long long fb = __ballot(valid && need_exact && q == 0);
-      if (fb) exact_rows(fb, x, d, d, K, gcb, scb, false, kstar);
-      if (kstar >= K) kstar = K - 1;   // only tail rows past N can get here
-      const float gk = gcb[kstar];
+      int kstar = reduce_rows(key, h, dhat);
+      need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
+      const unsigned long long fb = __ballot(valid && need_exact && h == 0);
+      if (MULTI) {
+        const float* gcb = a.gain + (size_t)cb * K;
+        const float* scb = a.shape + (size_t)cb * K * d;
+        if (fb) exact_rows(fb, x, d, d, K, gcb, scb, false, kstar);
+        if (kstar >= K) kstar = K - 1;   // only tail rows past N can get here
+        const float gk = gcb[kstar];
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (j < d) x[j] = fmaf(-gk, scb[(size_t)kstar * d + j], x[j]);
-      if (valid && q == 0 && a.codes) {
+        for (int j = 0; j < 8; ++j)
+          if (j < d) x[j] = fmaf(-gk, scb[(size_t)kstar * d + j], x[j]);
+      } else {
+        if (fb) exact_rows(fb, x, d, DP, K, mg, ms, false, kstar);
+        if (kstar >= K) kstar = K - 1;
+        if (a.residual) {
+          const float gk = mg[kstar];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) x[j] = fmaf(-gk, ms[kstar * DP + j], x[j]);
+        }
+      }
+      if (valid && h == 0 && a.codes) {
         const int64_t t = (int64_t)m * G + g;
-        if (a.byte_codes) {
+        if (lds_codes) {
+          ((uint8_t*)(codes_l + m * ENC_CHUNK_ROWS + (row - row_begin)))[wave] = (uint8_t)kstar;
+        } else if (a.byte_codes) {
           ((uint8_t*)(a.codes + row * a.words))[t] = (uint8_t)kstar;
         } else {
           const int64_t bit = t * a.b;
@@ -599,9 +828,23 @@ __global__ void __launch_bounds__(ENC_WAVES * 64) encode_kernel(EncodeArgs a) {
         }
       }
     }
-    if (valid && a.residual && q == 0) {
+    if (valid && a.residual && h == 0) {
       float* dst = a.residual + row * (int64_t)(G * d) + (int64_t)g * d;
       for (int j = 0; j < d; ++j) dst[j] = x[j];
+    }
+  }
+  __syncthreads();
+  }
+flush:
+  if (lds_codes) {
+    // one 32-bit word per (stage, row): the codes of this block's four
+    // consecutive subspaces
+    const int64_t g0 = (int64_t)blockIdx.y * ENC_WAVES;
+    const int nrows = (int)(row_end - row_begin);
+    for (int e = threadIdx.x; e < a.M * nrows; e += blockDim.x) {
+      const int m = e / nrows, r = e % nrows;
+      uint32_t* dst = (uint32_t*)((uint8_t*)(a.codes + (row_begin + r) * a.words) + m * G + g0);
+      *dst = codes_l[m * ENC_CHUNK_ROWS + r];
     }
   }
 }
@@ -615,10 +858,11 @@ struct DecodeArgs {
   void* out;
 };
 
-// Gather-sum decoder: one thread per (row, subspace), float32 accumulation
-// in stage order with one fused multiply-add per stage.
+// Gather-sum decoder, generic fallback: one thread per (row, subspace),
+// codewords read from global memory.  Used when a subspace's codeword table
+// does not fit the LDS kernel below.
 template <typename TO>
-__global__ void decode_kernel(DecodeArgs a) {
+__global__ void decode_global_kernel(DecodeArgs a) {
   const int64_t total = a.N * a.G;
   for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * blockDim.x) {
@@ -640,14 +884,134 @@ __global__ void decode_kernel(DecodeArgs a) {
       const float* s = a.shape + (cb * a.K + k) * a.d;
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        if (j < a.d) acc[j] = fmaf(gk, s[j], acc[j]);
+        if (j < a.d) acc[j] += gk * s[j];
     }
     TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * a.d;
     for (int j = 0; j < a.d; ++j) dst[j] = (TO)acc[j];
   }
 }
 
+constexpr int DEC_THREADS = 256;
+constexpr int DEC_TABLE_FLOATS = 16384;    // 64 KB of codewords g * s
+constexpr int DEC_ROWS = 2048;             // rows per workgroup
+
+template <typename TO> struct OutVec;
+template <> struct OutVec<_Float16> {
+  static __device__ __forceinline__ void store(_Float16* p, const float (&v)[8]) {
+    h8 h;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = (_Float16)v[j];
+    *(u4*)p = __builtin_bit_cast(u4, h);
+  }
+};
+template <> struct OutVec<float> {
+  static __device__ __forceinline__ void store(float* p, const float (&v)[8]) {
+    ((f4*)p)[0] = (f4){v[0], v[1], v[2], v[3]};
+    ((f4*)p)[1] = (f4){v[4], v[5], v[6], v[7]};
+  }
+};
+
+// Gather-sum decoder with the codeword table in LDS.  A workgroup owns
+// `gpw` consecutive subspaces and DEC_ROWS rows; its table holds the float32
+// codewords g * s of those subspaces for the first M_use stages.  Threads
+// map to (row, subspace) with the subspace fastest, so each row's output
+// slice of gpw * d elements is written contiguously.  Workgroups that share
+// rows (and therefore code words) are numbered so that they land on the same
+// XCD, whose L2 then serves the shared code lines.
+template <typename TO>
+__global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a, int gpw,
+                                                                 int gblocks, int rchunks,
+                                                                 int vec) {
+  __shared__ float tab[DEC_TABLE_FLOATS];
+  const int id = blockIdx.x;
+  const int xcd = id % 8, slot = id / 8;
+  const int gb = slot % gblocks;
+  const int rc = (slot / gblocks) * 8 + xcd;
+  if (rc >= rchunks) return;
+  const int g0 = gb * gpw;
+  const int ngr = min(gpw, a.G - g0);
+  const int K = a.K, M = a.M_use, d = a.d;
+  const int tid = threadIdx.x;
+  for (int e = tid; e < ngr * M * K; e += DEC_THREADS) {
+    const int k = e % K, m = (e / K) % M, gi = e / (K * M);
+    const size_t cb = (size_t)m * a.G + g0 + gi;
+    const float gk = a.gain[cb * K + k];
+    const float* sv = a.shape + (cb * K + k) * d;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) tab[e * 8 + j] = (j < d) ? gk * sv[j] : 0.f;
+  }
+  __syncthreads();
+  const int gi = tid % gpw;
+  if (gi >= ngr) return;
+  const int rstep = DEC_THREADS / gpw;
+  const int64_t r_begin = (int64_t)rc * DEC_ROWS;
+  int64_t r_end = r_begin + DEC_ROWS;
+  if (r_end > a.N) r_end = a.N;
+  const int g = g0 + gi;
+  const uint64_t kmask = (1ull << a.b) - 1;
+#pragma unroll 4
+  for (int64_t row = r_begin + tid / gpw; row < r_end; row += rstep) {
+    const uint32_t* cr = a.codes + row * a.words;
+    float acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    for (int m = 0; m < M; ++m) {
+      const int64_t bit = ((int64_t)m * a.G + g) * a.b;
+      const int64_t wi = bit / 32;
+      const int off = (int)(bit % 32);
+      uint64_t v = cr[wi];
+      if (off + a.b > 32) v |= (uint64_t)cr[wi + 1] << 32;
+      const int k = (int)((v >> off) & kmask);
+      const float* c = tab + ((gi * M + m) * K + k) * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[j] += c[j];
+    }
+    TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
+    if (vec) {
+      OutVec<TO>::store(dst, acc);
+    } else {
+      for (int j = 0; j < d; ++j) dst[j] = (TO)acc[j];
+    }
+  }
+}
+
 // ------------------------------------------------------------- host side
+
+// Optional launch timing (off by default): HIP events bracket every launch
+// of the instrumented kernels on the launch's own stream.
+struct TimingState {
+  bool on = false;
+  struct Rec { hipEvent_t a, b; int kind; };
+  Rec* recs = nullptr;
+  int n = 0, cap = 0;
+};
+TimingState g_timing;
+
+struct TimedLaunch {
+  TimingState::Rec* rec = nullptr;
+  hipStream_t st;
+  TimedLaunch(int kind, hipStream_t s) : st(s) {
+    if (!g_timing.on) return;
+    if (g_timing.n == g_timing.cap) {
+      const int nc = g_timing.cap ? 2 * g_timing.cap : 1024;
+      auto* nr = new TimingState::Rec[nc];
+      for (int i = 0; i < g_timing.n; ++i) nr[i] = g_timing.recs[i];
+      for (int i = g_timing.n; i < nc; ++i) {
+        hipEventCreate(&nr[i].a);
+        hipEventCreate(&nr[i].b);
+      }
+      delete[] g_timing.recs;
+      g_timing.recs = nr;
+      g_timing.cap = nc;
+    }
+    rec = &g_timing.recs[g_timing.n++];
+    rec->kind = kind;
+    hipEventRecord(rec->a, st);
+  }
+  ~TimedLaunch() {
+    if (rec) hipEventRecord(rec->b, st);
+  }
+};
 
 inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
@@ -673,7 +1037,7 @@ gsrq_status check_supported(const gsrq_shape* s) {
 }
 
 struct TrainLayout {
-  size_t xt, frag, sig, part, assign, done, iters, seednorm, seeds, total;
+  size_t xt, part, assign, done, iters, seednorm, seeds, total;
   int chunks;
 };
 
@@ -683,8 +1047,6 @@ TrainLayout train_layout(const gsrq_shape* s, size_t elt) {
   L.chunks = (int)((s->N + TRAIN_CHUNK_ROWS - 1) / TRAIN_CHUNK_ROWS);
   size_t off = 0;
   L.xt = off; off = align256(off + (size_t)G * s->N * 8 * elt);
-  L.frag = off; off = align256(off + (size_t)G * TILES * 64 * sizeof(u4));
-  L.sig = off; off = align256(off + (size_t)G * sizeof(int));
   L.part = off; off = align256(off + (size_t)G * L.chunks * PSTRIDE * sizeof(double));
   L.assign = off; off = align256(off + (size_t)G * s->N * sizeof(uint16_t));
   L.done = off; off = align256(off + (size_t)G * sizeof(int));
@@ -695,9 +1057,11 @@ TrainLayout train_layout(const gsrq_shape* s, size_t elt) {
   return L;
 }
 
+// multi-stage encode keeps per-stage operand tiles in the workspace
 size_t encode_ws(const gsrq_shape* s) {
   const int64_t G = s->D / s->d;
-  return align256((size_t)s->M * G * TILES * 64 * sizeof(u4)) +
+  if (s->M <= 1) return 256;
+  return align256((size_t)s->M * G * NT * 2 * 64 * sizeof(u4)) +
          align256((size_t)s->M * G * sizeof(int));
 }
 
@@ -720,25 +1084,44 @@ gsrq_status fill_u32(void* p, size_t n, uint32_t v, hipStream_t st) {
 
 template <typename T>
 gsrq_status encode_launch(const gsrq_shape* s, const void* X, int64_t ldx, const float* gain,
-                          const float* shape, const u4* frag, const int* sig, int M,
-                          uint32_t* codes, float* residual, hipStream_t st) {
+                          const float* shape, int M, uint32_t* codes, float* residual, void* ws,
+                          hipStream_t st) {
   EncodeArgs a;
   a.x = X; a.ldx = ldx; a.N = s->N; a.d = s->d; a.K = s->K; a.G = s->D / s->d; a.M = M;
   a.b = log2i(s->K);
   a.words = (int)((M * (int64_t)a.G * a.b + 31) / 32);
-  a.gain = gain; a.shape = shape; a.frag = frag; a.sig = sig;
+  a.gain = gain; a.shape = shape; a.frag = nullptr; a.sig = nullptr;
   a.codes = codes; a.residual = residual;
   a.byte_codes = (a.b == 8) && ((M * (int64_t)a.G) % 4 == 0);
+  a.lds_codes = codes && a.byte_codes && (a.G % ENC_WAVES == 0) && M <= ENC_MAX_STAGES;
+  const size_t esz = sizeof(T);
+  a.vec_rows = (s->d == 8) && ((uintptr_t)X % 16 == 0) && ((ldx * esz) % 16 == 0);
+  gsrq_status e;
   if (codes && !a.byte_codes) {
-    gsrq_status e = fill_u32(codes, (size_t)s->N * a.words, 0u, st);
-    if (e) return e;
+    if ((e = fill_u32(codes, (size_t)s->N * a.words, 0u, st))) return e;
+  }
+  if (M > 1) {
+    u4* frag = (u4*)ws;
+    int* sig = (int*)((char*)ws + align256((size_t)M * a.G * NT * 2 * 64 * sizeof(u4)));
+    tiles_kernel<<<(unsigned)(M * a.G), 64, 0, st>>>(gain, shape, s->d, s->K, frag, sig);
+    if ((e = launch_ok())) return e;
+    a.frag = frag;
+    a.sig = sig;
   }
   dim3 grid((unsigned)((s->N + ENC_CHUNK_ROWS - 1) / ENC_CHUNK_ROWS),
             (unsigned)((a.G + ENC_WAVES - 1) / ENC_WAVES));
-  if (M > 1)
-    encode_kernel<T, true><<<grid, ENC_WAVES * 64, 0, st>>>(a);
-  else
-    encode_kernel<T, false><<<grid, ENC_WAVES * 64, 0, st>>>(a);
+  TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
+  if (M > 1) {
+    if (a.vec_rows)
+      encode_kernel<T, true, true><<<grid, ENC_WAVES * 64, 0, st>>>(a);
+    else
+      encode_kernel<T, true, false><<<grid, ENC_WAVES * 64, 0, st>>>(a);
+  } else {
+    if (a.vec_rows)
+      encode_kernel<T, false, true><<<grid, ENC_WAVES * 64, 0, st>>>(a);
+    else
+      encode_kernel<T, false, false><<<grid, ENC_WAVES * 64, 0, st>>>(a);
+  }
   return launch_ok();
 }
 
@@ -750,8 +1133,6 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
   const TrainLayout L = train_layout(s, sizeof(T));
   char* base = (char*)ws;
   T* xt = (T*)(base + L.xt);
-  u4* frag = (u4*)(base + L.frag);
-  int* sig = (int*)(base + L.sig);
   double* part = (double*)(base + L.part);
   uint16_t* assign = assign_io ? assign_io : (uint16_t*)(base + L.assign);
   int* done = (int*)(base + L.done);
@@ -765,6 +1146,7 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
 
   {
     const int64_t work = ((s->N + 7) / 8) * (int64_t)((G + 7) / 8) * 64;
+    TimedLaunch tl(GSRQ_KERNEL_TRANSPOSE, st);
     transpose_kernel<T><<<grid_for(work, 256), 256, 0, st>>>((const T*)X, ldx, s->N, d, G, xt);
     if ((e = launch_ok())) return e;
   }
@@ -774,14 +1156,16 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
 
   AssignArgs aa;
   aa.xt = xt; aa.N = s->N; aa.d = d; aa.K = K; aa.G = G; aa.w = w;
-  aa.gain = gain; aa.shape = shape; aa.frag = frag; aa.sig = sig; aa.assign = assign;
+  aa.gain = gain; aa.shape = shape; aa.assign = assign;
   aa.done = done; aa.part = part; aa.chunks = L.chunks; aa.force_changed = 0;
+  aa.want_obj = trace != nullptr;
   FinalizeArgs fa;
   fa.d = d; fa.K = K; fa.G = G; fa.chunks = L.chunks; fa.T = T_; fa.t = 0;
   fa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
   fa.part = part; fa.seednorm = seednorm; fa.gain = gain; fa.shape = shape;
-  fa.frag = frag; fa.sig = sig; fa.done = done; fa.iters = iters; fa.trace = trace;
+  fa.done = done; fa.iters = iters; fa.trace = trace;
   const dim3 agrid((unsigned)L.chunks, (unsigned)G);
+  const dim3 fgrid((unsigned)((K + 63) / 64), (unsigned)G);
 
   if (!resume) {
     if (hipMemcpyAsync(dseeds, seeds, (size_t)G * K * sizeof(int32_t), hipMemcpyHostToDevice,
@@ -789,29 +1173,37 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
       return GSRQ_E_HIP;
     seed_kernel<T><<<G, 256, 0, st>>>(xt, s->N, d, K, dseeds, shape, seednorm);
     if ((e = launch_ok())) return e;
-    tiles_kernel<<<G, 256, 0, st>>>(gain, shape, d, K, 1, frag, sig);
+    {
+      TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
+      assign_accumulate_kernel<T, MODE_INIT><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
+    }
     if ((e = launch_ok())) return e;
-    assign_accumulate_kernel<T, MODE_INIT><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
-    if ((e = launch_ok())) return e;
-    finalize_kernel<MODE_INIT><<<G, 256, 0, st>>>(fa);
+    {
+      TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
+      finalize_kernel<MODE_INIT><<<fgrid, 64, 0, st>>>(fa);
+    }
     if ((e = launch_ok())) return e;
   } else {
-    tiles_kernel<<<G, 256, 0, st>>>(gain, shape, d, K, 0, frag, sig);
-    if ((e = launch_ok())) return e;
     aa.force_changed = (flags & GSRQ_ASSIGN_IN) ? 0 : 1;
   }
   for (int t = 1; t <= T_; ++t) {
-    assign_accumulate_kernel<T, MODE_ITER><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
+    {
+      TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
+      assign_accumulate_kernel<T, MODE_ITER><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
+    }
     if ((e = launch_ok())) return e;
     aa.force_changed = 0;
     fa.t = t;
-    finalize_kernel<MODE_ITER><<<G, 256, 0, st>>>(fa);
+    {
+      TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
+      finalize_kernel<MODE_ITER><<<fgrid, 64, 0, st>>>(fa);
+    }
     if ((e = launch_ok())) return e;
   }
   if (R_next) {
     gsrq_shape s1 = *s;
     s1.M = 1;
-    return encode_launch<T>(&s1, X, ldx, gain, shape, frag, sig, 1, nullptr, R_next, st);
+    return encode_launch<T>(&s1, X, ldx, gain, shape, 1, nullptr, R_next, nullptr, st);
   }
   return GSRQ_OK;
 }
@@ -924,14 +1316,9 @@ gsrq_status gsrq_encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, 
   if ((e = check_supported(s))) return e;
   if (ws_bytes < encode_ws(s)) return GSRQ_E_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
-  const int64_t G = s->D / s->d;
-  u4* frag = (u4*)workspace;
-  int* sig = (int*)((char*)workspace + align256((size_t)s->M * G * TILES * 64 * sizeof(u4)));
-  tiles_kernel<<<(unsigned)(s->M * G), 256, 0, st>>>(gain, shape, s->d, s->K, 0, frag, sig);
-  if ((e = launch_ok())) return e;
   if (x_dtype == GSRQ_F16)
-    return encode_launch<_Float16>(s, X, ldx, gain, shape, frag, sig, s->M, codes, residual, st);
-  return encode_launch<float>(s, X, ldx, gain, shape, frag, sig, s->M, codes, residual, st);
+    return encode_launch<_Float16>(s, X, ldx, gain, shape, s->M, codes, residual, workspace, st);
+  return encode_launch<float>(s, X, ldx, gain, shape, s->M, codes, residual, workspace, st);
 }
 
 gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_use,
@@ -949,12 +1336,49 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_us
   a.words = (int)((s->M * (int64_t)a.G * a.b + 31) / 32);
   a.gain = gain; a.shape = shape; a.out = Xhat;
   hipStream_t st = (hipStream_t)stream;
-  const int grid = grid_for(s->N * a.G, 256);
-  if (out_dtype == GSRQ_F16)
-    decode_kernel<_Float16><<<grid, 256, 0, st>>>(a);
-  else
-    decode_kernel<float><<<grid, 256, 0, st>>>(a);
+  TimedLaunch tl(GSRQ_KERNEL_DECODE, st);
+  const int64_t per_group = (int64_t)M_use * s->K * 8;    // table floats per subspace
+  if (per_group <= DEC_TABLE_FLOATS) {
+    int gpw = (int)(DEC_TABLE_FLOATS / per_group);
+    if (gpw > 8) gpw = 8;
+    if (gpw > a.G) gpw = a.G;
+    const int gblocks = (a.G + gpw - 1) / gpw;
+    const int rchunks = (int)((s->N + DEC_ROWS - 1) / DEC_ROWS);
+    const int blocks = 8 * gblocks * ((rchunks + 7) / 8);
+    const size_t esz = out_dtype == GSRQ_F16 ? 2 : 4;
+    const int vec = (s->d == 8) && ((uintptr_t)Xhat % 16 == 0) && ((ldo * esz) % 16 == 0);
+    if (out_dtype == GSRQ_F16)
+      decode_lds_kernel<_Float16><<<blocks, DEC_THREADS, 0, st>>>(a, gpw, gblocks, rchunks, vec);
+    else
+      decode_lds_kernel<float><<<blocks, DEC_THREADS, 0, st>>>(a, gpw, gblocks, rchunks, vec);
+  } else {
+    const int grid = grid_for(s->N * a.G, 256);
+    if (out_dtype == GSRQ_F16)
+      decode_global_kernel<_Float16><<<grid, 256, 0, st>>>(a);
+    else
+      decode_global_kernel<float><<<grid, 256, 0, st>>>(a);
+  }
   return launch_ok();
+}
+
+gsrq_status gsrq_timing_enable(int on) {
+  g_timing.on = on != 0;
+  g_timing.n = 0;
+  return GSRQ_OK;
+}
+
+gsrq_status gsrq_timing_read(double* total_ms, int64_t* launches, int n_kinds) {
+  if (!total_ms || !launches || n_kinds < 0) return GSRQ_E_ARG;
+  for (int k = 0; k < n_kinds; ++k) { total_ms[k] = 0.0; launches[k] = 0; }
+  for (int i = 0; i < g_timing.n; ++i) {
+    const auto& r = g_timing.recs[i];
+    if (hipEventSynchronize(r.b) != hipSuccess) return GSRQ_E_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return GSRQ_E_HIP;
+    if (r.kind < n_kinds) { total_ms[r.kind] += ms; launches[r.kind] += 1; }
+  }
+  g_timing.n = 0;
+  return GSRQ_OK;
 }
 
 }  // extern "C"

@@ -66,8 +66,30 @@ def load_library(path: str = LIB_PATH):
     lib.gsrq_decode.restype = ctypes.c_int
     lib.gsrq_decode.argtypes = [SP, _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_int,
                                 ctypes.c_int64, _vp]
+    lib.gsrq_timing_enable.restype = ctypes.c_int
+    lib.gsrq_timing_enable.argtypes = [ctypes.c_int]
+    lib.gsrq_timing_read.restype = ctypes.c_int
+    lib.gsrq_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double),
+                                     ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
     _lib = lib
     return lib
+
+
+KERNEL_KINDS = ("assign", "finalize", "encode", "decode", "transpose")
+
+
+def timing_enable(on: bool = True):
+    """Bracket every kernel launch with HIP events on its stream (measurement)."""
+    _check(load_library().gsrq_timing_enable(1 if on else 0), "gsrq_timing_enable")
+
+
+def timing_read():
+    """{kind: (total_ms, launches)} for the launches recorded since enabling."""
+    n = len(KERNEL_KINDS)
+    ms = (ctypes.c_double * n)()
+    cnt = (ctypes.c_int64 * n)()
+    _check(load_library().gsrq_timing_read(ms, cnt, n), "gsrq_timing_read")
+    return {k: (float(ms[i]), int(cnt[i])) for i, k in enumerate(KERNEL_KINDS)}
 
 
 def status_string(status: int) -> str:
