@@ -23,6 +23,11 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline"
+# HBM bytes per launch of the dominant kernel, from the FETCH_SIZE / WRITE_SIZE
+# rocprofv3 passes (profiles/hbm_traffic_llama3_8b_layer_1bit.md, read counts
+# scaled x2.000 and writes x1.000 against a 256 MiB reference copy).  Valid
+# only for the kernel source those passes measured.
+TRAFFIC = {"source_sha256_prefix": "f61df633d682d24b", "bytes_per_launch": 109767345}
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
 HEAD_DIM = 128
@@ -34,9 +39,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama3_8b_layer_1bit")
-    ap.add_argument("--cpu-groups", type=int, default=16,
+    ap.add_argument("--cpu-groups", type=int, default=128,
                     help="subspaces of the K cache the CPU-baseline sample runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-ref-mib", type=int, default=0,
+                    help="after timing, run one plain device copy of this many MiB "
+                         "(reference dispatch for scaling HBM counters)")
     return ap.parse_args()
 
 
@@ -80,7 +88,7 @@ def cpu_baseline(kv, wl, n_groups):
         "value": vectors / step_s, "unit": "vectors/s", "cores": int(threads), "kind": "oracle",
         "sample": (f"float64 oracle on {n_groups} of {wl.G} K-cache subspaces of this workload: "
                    f"init + {n_iter} GSKM iterations + encode + decode each ({sample_s:.1f} s), "
-                   f"scaled to {T} iterations x {wl.G} subspaces x (K, V)"),
+                   f"scaled to {T} iterations, {wl.G} subspaces and both caches (K, V)"),
         "est_step_s": step_s,
     }
 
@@ -153,6 +161,10 @@ def main():
         return (ms / n * 1e3) if n else None
 
     a_us, f_us, e_us, dcd_us = avg_us("assign"), avg_us("finalize"), avg_us("encode"), avg_us("decode")
+    import hashlib
+    src = os.path.join(ROOT, "paper_2607_01065_amd", "csrc", "gsrq.hip")
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    traffic = TRAFFIC["bytes_per_launch"] if sha == TRAFFIC["source_sha256_prefix"] else None
     iters_run = float(torch.stack(iters).float().mean().item()) if iters else float("nan")
     flops_assign = 2.0 * N * D * K                         # eq. (5) scores, one pass
     achieved = flops_assign / (a_us * 1e-6) / 1e12
@@ -174,10 +186,24 @@ def main():
         "roofline": {"kernel": "assign_accumulate (eq. 5 scores + argmin + weighted sums)",
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_MFMA_F16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_MFMA_F16_TFLOPS,
-                     "traffic": None},
+                     "traffic": traffic, "traffic_unit": "HBM bytes per launch",
+                     "flops_per_launch": flops_assign, "avg_launch_us": a_us,
+                     "alu_view": {"bound": "alu", "unit": "Tscore/s",
+                                  "achieved": N * (D // d) * K / (a_us * 1e-6) / 1e12,
+                                  "peak": 39.3,
+                                  "note": "argmin epilogue: one VALU lane-op per score is the "
+                                          "floor; peak = 256 CU x 64 lanes x 2.4 GHz"}},
     }
+    if args.copy_ref_mib > 0:
+        n = args.copy_ref_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_ref_bytes"] = n * 4
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(kv, wl, args.cpu_groups)
+        out["cpu_baseline"] = cpu_baseline(kv, wl, min(args.cpu_groups, wl.G))
     print(json.dumps(out), flush=True)
 
 
