@@ -856,6 +856,9 @@ struct DecodeArgs {
   const float* gain;
   const float* shape;
   void* out;
+  int gpw, gblocks;      // LDS kernel: subspaces per workgroup, subspace blocks
+  int64_t rows_per_wg;   // LDS kernel: rows per workgroup
+  int vec;               // LDS kernel: 8-element vector stores are aligned
 };
 
 // Gather-sum decoder, generic fallback: one thread per (row, subspace),
@@ -891,9 +894,10 @@ __global__ void decode_global_kernel(DecodeArgs a) {
   }
 }
 
-constexpr int DEC_THREADS = 256;
-constexpr int DEC_TABLE_FLOATS = 16384;    // 64 KB of codewords g * s
-constexpr int DEC_ROWS = 2048;             // rows per workgroup
+constexpr int DEC_THREADS = 1024;
+constexpr int DEC_TABLE_BYTES = 65536;     // codeword table per workgroup
+constexpr int DEC_ROW_BATCH = 4;           // rows in flight per thread
+constexpr int DEC_FILL_BATCH = 8;          // table entries in flight per thread
 
 template <typename TO> struct OutVec;
 template <> struct OutVec<_Float16> {
@@ -911,66 +915,127 @@ template <> struct OutVec<float> {
   }
 };
 
-// Gather-sum decoder with the codeword table in LDS.  A workgroup owns
-// `gpw` consecutive subspaces and DEC_ROWS rows; its table holds the float32
-// codewords g * s of those subspaces for the first M_use stages.  Threads
-// map to (row, subspace) with the subspace fastest, so each row's output
-// slice of gpw * d elements is written contiguously.  Workgroups that share
-// rows (and therefore code words) are numbered so that they land on the same
-// XCD, whose L2 then serves the shared code lines.
-template <typename TO>
-__global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a, int gpw,
-                                                                 int gblocks, int rchunks,
-                                                                 int vec) {
-  __shared__ float tab[DEC_TABLE_FLOATS];
+// Codeword table entry c = g s of DP elements, stored as float32, or as
+// float16 when a single stage is decoded to float16 (the product is then
+// rounded once, exactly as the store would round it).
+template <typename TT> struct TabEntry;
+template <> struct TabEntry<float> {
+  static __device__ __forceinline__ void put(float* t, const float (&c)[8]) {
+    ((f4*)t)[0] = (f4){c[0], c[1], c[2], c[3]};
+    ((f4*)t)[1] = (f4){c[4], c[5], c[6], c[7]};
+  }
+  static __device__ __forceinline__ void add(const float* t, float (&acc)[8]) {
+    const f4 lo = ((const f4*)t)[0], hi = ((const f4*)t)[1];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) { acc[j] += lo[j]; acc[4 + j] += hi[j]; }
+  }
+};
+template <> struct TabEntry<_Float16> {
+  static __device__ __forceinline__ void put(_Float16* t, const float (&c)[8]) {
+    h8 h;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[j] = (_Float16)c[j];
+    *(u4*)t = __builtin_bit_cast(u4, h);
+  }
+  static __device__ __forceinline__ void add(const _Float16* t, float (&acc)[8]) {
+    const h8 h = as_h8(*(const u4*)t);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] += (float)h[j];
+  }
+};
+
+// Code of (stage m, subspace g) from a row's words: b bits at bit
+// (m G + g) b, least significant bit first, possibly straddling two words.
+__device__ __forceinline__ int read_code(const uint32_t* cr, int64_t bit, int b) {
+  const int64_t wi = bit >> 5;
+  const int off = (int)(bit & 31);
+  uint64_t v = cr[wi];
+  if (off + b > 32) v |= (uint64_t)cr[wi + 1] << 32;
+  return (int)((v >> off) & ((1ull << b) - 1));
+}
+
+// Gather-sum decoder with the codeword table in LDS.  A workgroup owns `gpw`
+// consecutive subspaces and a contiguous range of rows; its table holds the
+// codewords g s of those subspaces for the first M_use stages, laid out
+// [gpw][M_use][K][8].  Threads map to (row, subspace) with the subspace
+// fastest, so each row's output slice of gpw * d elements is written
+// contiguously, and every thread keeps DEC_ROW_BATCH rows in flight.
+// Workgroups that share rows (and so share code words) are numbered to land
+// on the same XCD, whose L2 then serves the shared code lines.
+template <typename TO, typename TT>
+__global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a) {
+  extern __shared__ __align__(16) unsigned char dec_smem[];
+  TT* tab = (TT*)dec_smem;
+  const int gpw = a.gpw, gblocks = a.gblocks;
   const int id = blockIdx.x;
   const int xcd = id % 8, slot = id / 8;
   const int gb = slot % gblocks;
   const int rc = (slot / gblocks) * 8 + xcd;
-  if (rc >= rchunks) return;
+  const int64_t r_begin = (int64_t)rc * a.rows_per_wg;
+  if (r_begin >= a.N) return;
+  int64_t r_end = r_begin + a.rows_per_wg;
+  if (r_end > a.N) r_end = a.N;
   const int g0 = gb * gpw;
   const int ngr = min(gpw, a.G - g0);
   const int K = a.K, M = a.M_use, d = a.d;
   const int tid = threadIdx.x;
-  for (int e = tid; e < ngr * M * K; e += DEC_THREADS) {
-    const int k = e % K, m = (e / K) % M, gi = e / (K * M);
-    const size_t cb = (size_t)m * a.G + g0 + gi;
-    const float gk = a.gain[cb * K + k];
-    const float* sv = a.shape + (cb * K + k) * d;
+  // table fill: every load of a batch is issued before the first use
+  const int entries = ngr * M * K;
+  for (int e0 = 0; e0 < entries; e0 += DEC_THREADS * DEC_FILL_BATCH) {
+    float g[DEC_FILL_BATCH], c[DEC_FILL_BATCH][8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) tab[e * 8 + j] = (j < d) ? gk * sv[j] : 0.f;
+    for (int q = 0; q < DEC_FILL_BATCH; ++q) {
+      const int e = min(e0 + q * DEC_THREADS + tid, entries - 1);
+      // K = 2^b; no integer division unless several stages are decoded
+      const int k = e & (K - 1), q2 = e >> a.b;
+      const int m = M == 1 ? 0 : q2 % M, gi = M == 1 ? q2 : q2 / M;
+      const size_t cb = (size_t)m * a.G + g0 + gi;
+      read_codeword(a.gain + cb * K, a.shape + cb * K * d, d, K, k, false, g[q], c[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < DEC_FILL_BATCH; ++q) {
+      const int e = e0 + q * DEC_THREADS + tid;
+      if (e < entries) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) c[q][j] *= g[q];
+        TabEntry<TT>::put(tab + (size_t)e * 8, c[q]);
+      }
+    }
   }
   __syncthreads();
   const int gi = tid % gpw;
   if (gi >= ngr) return;
   const int rstep = DEC_THREADS / gpw;
-  const int64_t r_begin = (int64_t)rc * DEC_ROWS;
-  int64_t r_end = r_begin + DEC_ROWS;
-  if (r_end > a.N) r_end = a.N;
   const int g = g0 + gi;
-  const uint64_t kmask = (1ull << a.b) - 1;
-#pragma unroll 4
-  for (int64_t row = r_begin + tid / gpw; row < r_end; row += rstep) {
-    const uint32_t* cr = a.codes + row * a.words;
-    float acc[8];
+  const TT* tg = tab + (size_t)gi * M * K * 8;
+  for (int64_t r0 = r_begin + tid / gpw; r0 < r_end; r0 += (int64_t)DEC_ROW_BATCH * rstep) {
+    float acc[DEC_ROW_BATCH][8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+    for (int q = 0; q < DEC_ROW_BATCH; ++q)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[q][j] = 0.f;
     for (int m = 0; m < M; ++m) {
-      const int64_t bit = ((int64_t)m * a.G + g) * a.b;
-      const int64_t wi = bit / 32;
-      const int off = (int)(bit % 32);
-      uint64_t v = cr[wi];
-      if (off + a.b > 32) v |= (uint64_t)cr[wi + 1] << 32;
-      const int k = (int)((v >> off) & kmask);
-      const float* c = tab + ((gi * M + m) * K + k) * 8;
+      int k[DEC_ROW_BATCH];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) acc[j] += c[j];
+      for (int q = 0; q < DEC_ROW_BATCH; ++q) {
+        int64_t row = r0 + (int64_t)q * rstep;
+        row = row < r_end ? row : r_begin;    // in-range row; its result is not stored
+        k[q] = read_code(a.codes + row * a.words, ((int64_t)m * a.G + g) * a.b, a.b);
+      }
+#pragma unroll
+      for (int q = 0; q < DEC_ROW_BATCH; ++q)
+        TabEntry<TT>::add(tg + ((size_t)m * K + k[q]) * 8, acc[q]);
     }
-    TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
-    if (vec) {
-      OutVec<TO>::store(dst, acc);
-    } else {
-      for (int j = 0; j < d; ++j) dst[j] = (TO)acc[j];
+#pragma unroll
+    for (int q = 0; q < DEC_ROW_BATCH; ++q) {
+      const int64_t row = r0 + (int64_t)q * rstep;
+      if (row >= r_end) break;
+      TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
+      if (a.vec) {
+        OutVec<TO>::store(dst, acc[q]);
+      } else {
+        for (int j = 0; j < d; ++j) dst[j] = (TO)acc[q][j];
+      }
     }
   }
 }
@@ -1337,20 +1402,32 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_us
   a.gain = gain; a.shape = shape; a.out = Xhat;
   hipStream_t st = (hipStream_t)stream;
   TimedLaunch tl(GSRQ_KERNEL_DECODE, st);
-  const int64_t per_group = (int64_t)M_use * s->K * 8;    // table floats per subspace
-  if (per_group <= DEC_TABLE_FLOATS) {
-    int gpw = (int)(DEC_TABLE_FLOATS / per_group);
-    if (gpw > 8) gpw = 8;
-    if (gpw > a.G) gpw = a.G;
-    const int gblocks = (a.G + gpw - 1) / gpw;
-    const int rchunks = (int)((s->N + DEC_ROWS - 1) / DEC_ROWS);
-    const int blocks = 8 * gblocks * ((rchunks + 7) / 8);
+  // single-stage float16 output: the table holds float16 products
+  const bool half_tab = M_use == 1 && out_dtype == GSRQ_F16;
+  const int64_t per_group = (int64_t)M_use * s->K * 8 * (half_tab ? 2 : 4);  // table bytes
+  if (per_group <= DEC_TABLE_BYTES) {
+    int gpw = 1;   // a power of two, so (row, subspace) threads tile the workgroup
+    while (gpw * 2 <= 64 && gpw * 2 * per_group <= DEC_TABLE_BYTES && gpw < a.G) gpw *= 2;
+    a.gpw = gpw;
+    a.gblocks = (a.G + gpw - 1) / gpw;
+    // about one workgroup per CU, each streaming a contiguous row range (the
+    // table fill is paid once per workgroup)
+    int64_t rchunks = (256 + a.gblocks - 1) / a.gblocks;
+    const int64_t min_rows = 256;
+    if (rchunks * min_rows > s->N) rchunks = (s->N + min_rows - 1) / min_rows;
+    if (rchunks < 1) rchunks = 1;
+    a.rows_per_wg = (s->N + rchunks - 1) / rchunks;
+    rchunks = (s->N + a.rows_per_wg - 1) / a.rows_per_wg;
+    const int blocks = (int)(8 * a.gblocks * ((rchunks + 7) / 8));
     const size_t esz = out_dtype == GSRQ_F16 ? 2 : 4;
-    const int vec = (s->d == 8) && ((uintptr_t)Xhat % 16 == 0) && ((ldo * esz) % 16 == 0);
-    if (out_dtype == GSRQ_F16)
-      decode_lds_kernel<_Float16><<<blocks, DEC_THREADS, 0, st>>>(a, gpw, gblocks, rchunks, vec);
+    a.vec = (s->d == 8) && ((uintptr_t)Xhat % 16 == 0) && ((ldo * esz) % 16 == 0);
+    const size_t lds = (size_t)gpw * per_group;
+    if (out_dtype == GSRQ_F16 && half_tab)
+      decode_lds_kernel<_Float16, _Float16><<<blocks, DEC_THREADS, lds, st>>>(a);
+    else if (out_dtype == GSRQ_F16)
+      decode_lds_kernel<_Float16, float><<<blocks, DEC_THREADS, lds, st>>>(a);
     else
-      decode_lds_kernel<float><<<blocks, DEC_THREADS, 0, st>>>(a, gpw, gblocks, rchunks, vec);
+      decode_lds_kernel<float, float><<<blocks, DEC_THREADS, lds, st>>>(a);
   } else {
     const int grid = grid_for(s->N * a.G, 256);
     if (out_dtype == GSRQ_F16)
