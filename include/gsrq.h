@@ -26,7 +26,8 @@
  *    code of stage m, subspace g is the b = log2 K bit field starting at bit
  *    t*b, t = m*G + g, of the row's bit string, least significant bit first
  *    (bit p is bit p%32 of word p/32).
- *  - Supported on this build: 1 <= d <= 8, 2 <= K <= 256 (power of two).
+ *  - Supported on this build: 1 <= d <= 8 with 2 <= K <= 256, and
+ *    d in {8, 16, 32, 64, 128} with any power-of-two 2 <= K <= 65536.
  *    Other valid shapes return GSRQ_E_UNSUPPORTED.
  *  - Apart from the opt-in launch timing at the end of this header, the
  *    library keeps no state between calls; calls on different streams with
@@ -183,8 +184,10 @@ enum {
   GSRQ_KERNEL_FINALIZE = 1,   /* codebook update + operand tiles          */
   GSRQ_KERNEL_ENCODE = 2,     /* stage-fused encoder                      */
   GSRQ_KERNEL_DECODE = 3,     /* gather-sum decoder                       */
-  GSRQ_KERNEL_TRANSPOSE = 4,  /* subspace-major copy of the training input */
-  GSRQ_KERNEL_KINDS = 5
+  GSRQ_KERNEL_TRANSPOSE = 4,  /* subspace-major copy / seeding of the input */
+  GSRQ_KERNEL_ACCUMULATE = 5, /* weighted sums per codeword slice (d > 8)  */
+  GSRQ_KERNEL_FRAGMENTS = 6,  /* operand fragment tables (d > 8 or K > 256) */
+  GSRQ_KERNEL_KINDS = 7
 };
 
 /* Measurement hook, the library's only process state.  While enabled, every

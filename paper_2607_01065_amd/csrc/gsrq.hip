@@ -22,25 +22,18 @@
 // Accumulation (eqs. 6-8): per-workgroup float64 LDS accumulators of
 // sum w y, sum w x, sum w and the member count per codeword, flushed as
 // per-chunk partials and reduced in a fixed order by the update kernel.
-#include <hip/hip_runtime.h>
-#include <math.h>
-#include <stdint.h>
-#include <string.h>
+#include <algorithm>
 
-#include "gsrq.h"
+#include "gsrq_common.h"
+#include "gsrq_wide.h"
+
+GsrqTimingState g_gsrq_timing;
 
 namespace {
 
-typedef _Float16 h8 __attribute__((ext_vector_type(8)));
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef float f16v __attribute__((ext_vector_type(16)));
-typedef uint32_t u4 __attribute__((ext_vector_type(4)));
-
 constexpr int DP = 8;            // subvector slots of a k-chunk (d <= 8)
-constexpr int CW = 32;           // codewords per MFMA tile
 constexpr int NT = 8;            // tiles: K <= 256
 constexpr int KMAX = NT * CW;
-constexpr int RB = 32;           // rows per block (MFMA N dimension)
 constexpr int ACC = 18;          // sum w y[8], sum w x[8], W, count
 constexpr int PSTRIDE = KMAX * ACC + 2;  // + objective, changed flag
 constexpr int TRAIN_WAVES = 12;        // one 768-thread workgroup per CU
@@ -49,41 +42,11 @@ constexpr int TRAIN_CHUNK_ROWS = 8192;
 constexpr int ENC_WAVES = 4;           // one subspace per wave, three workgroups per CU
 constexpr int ENC_CHUNK_ROWS = 1024;
 constexpr int ENC_MAX_STAGES = 8;      // stages staged in LDS by one encode launch
-constexpr float Y_EPS = 1e-8f;            // y = x / (||x|| + eps)
-constexpr double SHAPE_KEEP_REL = 1e-6;   // keep s when ||sum w y|| <= 1e-6 W
-constexpr float PAD_BIAS = 65504.f;       // g^2 slot of a padding codeword
 constexpr int KEY_BITS = 7;               // (tile, slot) bits packed into a key
-constexpr int SA = 12;                    // codeword operand scale 2^SA (no subnormals)
-constexpr int SB = 8;                     // float32-row operand scale 2^SB
 
 enum { MODE_INIT = 0, MODE_ITER = 1 };
 
 // ---------------------------------------------------------------- helpers
-
-__device__ __forceinline__ uint32_t pack2(_Float16 lo, _Float16 hi) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, lo) |
-         ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
-}
-
-__device__ __forceinline__ h8 as_h8(u4 v) { return __builtin_bit_cast(h8, v); }
-
-__device__ __forceinline__ u4 pack_h8(const _Float16 (&v)[8]) {
-  u4 r;
-  r[0] = pack2(v[0], v[1]); r[1] = pack2(v[2], v[3]);
-  r[2] = pack2(v[4], v[5]); r[3] = pack2(v[6], v[7]);
-  return r;
-}
-
-template <typename T> __device__ __forceinline__ float to_f(T v) { return (float)v; }
-
-__device__ __forceinline__ int wave_lane() { return threadIdx.x & 63; }
-
-__device__ __forceinline__ int sigma_exp(float maxg) {
-  if (!(maxg > 0.f)) return 0;
-  int e;
-  frexpf(maxg, &e);   // maxg = m 2^e, m in [0.5, 1): 2^e >= maxg
-  return e;
-}
 
 // Codeword operand tiles of one codebook, in registers.  Tile t covers
 // codewords 32 t + c, c = lane % 32; lane half h = lane / 32 selects the
@@ -201,12 +164,6 @@ __device__ __forceinline__ void make_b(const float (&x)[8], u4 raw16, int ex, in
 // are replaced by the slot j (an inline constant), the 16 keys reduced with
 // v_min3, and the tile number OR'd in once (all keys of a tile share it, so
 // the order is unchanged).
-__device__ __forceinline__ int min3i(int a, int b, int c) {
-  int r;
-  asm volatile("v_min3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
-
 __device__ __forceinline__ int tile_min(const f16v& c, int t) {
   constexpr int MASK = ~((1 << KEY_BITS) - 1);
   int m = min3i((__float_as_int(c[0]) & MASK) | 0, (__float_as_int(c[1]) & MASK) | 1,
@@ -368,12 +325,6 @@ __device__ int load_codebook(const float* gain, const float* shape, int d, int K
 }
 
 // ---------------------------------------------------------------- kernels
-
-__global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
-       i += (size_t)gridDim.x * blockDim.x)
-    p[i] = v;
-}
 
 // X [N][ldx] -> Xt [G][N][8] (zero padded past d), same element type.
 template <typename T>
@@ -603,7 +554,9 @@ struct FinalizeArgs {
 template <int MODE>
 __global__ void __launch_bounds__(64) finalize_kernel(FinalizeArgs a) {
   const int g = blockIdx.y;
-  if (MODE == MODE_ITER && a.done[g]) return;
+  // done[g] holds the iteration at which subspace g stopped; blocks of that
+  // same iteration still apply its update
+  if (MODE == MODE_ITER && a.done[g] != 0 && a.done[g] < a.t) return;
   const int k = blockIdx.x * 64 + threadIdx.x;
   const int d = a.d, K = a.K;
   if (k < K) {
@@ -652,7 +605,7 @@ __global__ void __launch_bounds__(64) finalize_kernel(FinalizeArgs a) {
     }
     if (a.trace) a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
     a.iters[g] = a.t;
-    if (ch == 0.0 && !a.no_early_stop) a.done[g] = 1;
+    if (ch == 0.0 && !a.no_early_stop) a.done[g] = a.t;
   }
 }
 
@@ -1044,50 +997,6 @@ __global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a) {
 
 // Optional launch timing (off by default): HIP events bracket every launch
 // of the instrumented kernels on the launch's own stream.
-struct TimingState {
-  bool on = false;
-  struct Rec { hipEvent_t a, b; int kind; };
-  Rec* recs = nullptr;
-  int n = 0, cap = 0;
-};
-TimingState g_timing;
-
-struct TimedLaunch {
-  TimingState::Rec* rec = nullptr;
-  hipStream_t st;
-  TimedLaunch(int kind, hipStream_t s) : st(s) {
-    if (!g_timing.on) return;
-    if (g_timing.n == g_timing.cap) {
-      const int nc = g_timing.cap ? 2 * g_timing.cap : 1024;
-      auto* nr = new TimingState::Rec[nc];
-      for (int i = 0; i < g_timing.n; ++i) nr[i] = g_timing.recs[i];
-      for (int i = g_timing.n; i < nc; ++i) {
-        hipEventCreate(&nr[i].a);
-        hipEventCreate(&nr[i].b);
-      }
-      delete[] g_timing.recs;
-      g_timing.recs = nr;
-      g_timing.cap = nc;
-    }
-    rec = &g_timing.recs[g_timing.n++];
-    rec->kind = kind;
-    hipEventRecord(rec->a, st);
-  }
-  ~TimedLaunch() {
-    if (rec) hipEventRecord(rec->b, st);
-  }
-};
-
-inline size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
-
-bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
-
-int log2i(int64_t v) {
-  int b = 0;
-  while ((1ll << b) < v) ++b;
-  return b;
-}
-
 gsrq_status check_shape(const gsrq_shape* s, bool need_m) {
   if (!s) return GSRQ_E_ARG;
   if (s->N < 1 || s->D < 1 || s->d < 1 || s->D % s->d != 0) return GSRQ_E_ARG;
@@ -1096,9 +1005,13 @@ gsrq_status check_shape(const gsrq_shape* s, bool need_m) {
   return GSRQ_OK;
 }
 
+// Shapes of the narrow family (this file); gsrq_wide::serves() names the
+// shapes of the wide one.
+bool narrow(const gsrq_shape* s) { return s->d <= DP && s->K <= KMAX; }
+
 gsrq_status check_supported(const gsrq_shape* s) {
-  if (s->d > DP || s->K > KMAX) return GSRQ_E_UNSUPPORTED;
-  return GSRQ_OK;
+  if (narrow(s) || gsrq_wide::serves(s)) return GSRQ_OK;
+  return GSRQ_E_UNSUPPORTED;
 }
 
 struct TrainLayout {
@@ -1128,23 +1041,6 @@ size_t encode_ws(const gsrq_shape* s) {
   if (s->M <= 1) return 256;
   return align256((size_t)s->M * G * NT * 2 * 64 * sizeof(u4)) +
          align256((size_t)s->M * G * sizeof(int));
-}
-
-int grid_for(int64_t work, int block) {
-  int64_t b = (work + block - 1) / block;
-  if (b > 65536) b = 65536;
-  if (b < 1) b = 1;
-  return (int)b;
-}
-
-gsrq_status launch_ok() {
-  return hipGetLastError() == hipSuccess ? GSRQ_OK : GSRQ_E_HIP;
-}
-
-gsrq_status fill_u32(void* p, size_t n, uint32_t v, hipStream_t st) {
-  if (n == 0) return GSRQ_OK;
-  fill_u32_kernel<<<grid_for((int64_t)n, 256), 256, 0, st>>>((uint32_t*)p, n, v);
-  return launch_ok();
 }
 
 template <typename T>
@@ -1307,7 +1203,8 @@ gsrq_status gsrq_train_workspace_bytes(const gsrq_shape* s, size_t* bytes) {
   if (!bytes) return GSRQ_E_ARG;
   if ((e = check_supported(s))) return e;
   // sized for the wider input type so one workspace serves both
-  *bytes = train_layout(s, sizeof(float)).total;
+  *bytes = narrow(s) ? train_layout(s, sizeof(float)).total
+                     : gsrq_wide::train_workspace_bytes(s, 0);
   return GSRQ_OK;
 }
 
@@ -1316,7 +1213,7 @@ gsrq_status gsrq_encode_workspace_bytes(const gsrq_shape* s, size_t* bytes) {
   if (e) return e;
   if (!bytes) return GSRQ_E_ARG;
   if ((e = check_supported(s))) return e;
-  *bytes = encode_ws(s);
+  *bytes = narrow(s) ? encode_ws(s) : gsrq_wide::encode_workspace_bytes(s);
   return GSRQ_OK;
 }
 
@@ -1345,22 +1242,20 @@ gsrq_status gsrq_train_stage(const gsrq_shape* s, const void* X, gsrq_dtype x_dt
       // distinct within the subspace: sort a copy
       int32_t* tmp = new int32_t[s->K];
       memcpy(tmp, r, sizeof(int32_t) * s->K);
-      // insertion-free check via counting on a bitmap would need N bits;
-      // K is at most 256 here, so a simple sort suffices
-      for (int a = 1; a < s->K; ++a) {
-        int32_t v = tmp[a];
-        int b = a - 1;
-        while (b >= 0 && tmp[b] > v) { tmp[b + 1] = tmp[b]; --b; }
-        tmp[b + 1] = v;
-      }
+      std::sort(tmp, tmp + s->K);
       bool dup = false;
       for (int a = 1; a < s->K; ++a) dup |= tmp[a] == tmp[a - 1];
       delete[] tmp;
       if (dup) return GSRQ_E_ARG;
     }
   }
-  const size_t need = train_layout(s, x_dtype == GSRQ_F16 ? sizeof(_Float16) : sizeof(float)).total;
+  const size_t elt = x_dtype == GSRQ_F16 ? sizeof(_Float16) : sizeof(float);
+  const size_t need = narrow(s) ? train_layout(s, elt).total
+                                : gsrq_wide::train_workspace_bytes(s, elt);
   if (ws_bytes < need) return GSRQ_E_WORKSPACE;
+  if (!narrow(s))
+    return gsrq_wide::train_stage(s, X, x_dtype, ldx, w, T, seed_rows, flags, gain, shape,
+                                  R_next, assign_io, iters_run, obj_trace, workspace, stream);
   hipStream_t st = (hipStream_t)stream;
   if (x_dtype == GSRQ_F16)
     return train_impl<_Float16>(s, X, ldx, w, T, seed_rows, flags, gain, shape, R_next,
@@ -1379,6 +1274,10 @@ gsrq_status gsrq_encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, 
   if (ldx < s->D) return GSRQ_E_ARG;
   if (((uintptr_t)workspace & 255) != 0) return GSRQ_E_ARG;
   if ((e = check_supported(s))) return e;
+  if (!narrow(s)) {
+    if (ws_bytes < gsrq_wide::encode_workspace_bytes(s)) return GSRQ_E_WORKSPACE;
+    return gsrq_wide::encode(s, X, x_dtype, ldx, gain, shape, codes, residual, workspace, stream);
+  }
   if (ws_bytes < encode_ws(s)) return GSRQ_E_WORKSPACE;
   hipStream_t st = (hipStream_t)stream;
   if (x_dtype == GSRQ_F16)
@@ -1395,6 +1294,8 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_us
   if (M_use < 1 || M_use > s->M || ldo < s->D) return GSRQ_E_ARG;
   if (out_dtype != GSRQ_F32 && out_dtype != GSRQ_F16) return GSRQ_E_ARG;
   if ((e = check_supported(s))) return e;
+  if (!narrow(s))
+    return gsrq_wide::decode(s, codes, M_use, gain, shape, Xhat, out_dtype, ldo, stream);
   DecodeArgs a;
   a.codes = codes; a.N = s->N; a.ldo = ldo; a.d = s->d; a.K = s->K; a.G = s->D / s->d;
   a.M_use = M_use; a.b = log2i(s->K);
@@ -1439,22 +1340,22 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_us
 }
 
 gsrq_status gsrq_timing_enable(int on) {
-  g_timing.on = on != 0;
-  g_timing.n = 0;
+  g_gsrq_timing.on = on != 0;
+  g_gsrq_timing.n = 0;
   return GSRQ_OK;
 }
 
 gsrq_status gsrq_timing_read(double* total_ms, int64_t* launches, int n_kinds) {
   if (!total_ms || !launches || n_kinds < 0) return GSRQ_E_ARG;
   for (int k = 0; k < n_kinds; ++k) { total_ms[k] = 0.0; launches[k] = 0; }
-  for (int i = 0; i < g_timing.n; ++i) {
-    const auto& r = g_timing.recs[i];
+  for (int i = 0; i < g_gsrq_timing.n; ++i) {
+    const auto& r = g_gsrq_timing.recs[i];
     if (hipEventSynchronize(r.b) != hipSuccess) return GSRQ_E_HIP;
     float ms = 0.f;
     if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return GSRQ_E_HIP;
     if (r.kind < n_kinds) { total_ms[r.kind] += ms; launches[r.kind] += 1; }
   }
-  g_timing.n = 0;
+  g_gsrq_timing.n = 0;
   return GSRQ_OK;
 }
 

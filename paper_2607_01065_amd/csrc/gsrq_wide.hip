@@ -1,0 +1,1237 @@
+// Wide-subspace kernel family of the GSRQ hot path for AMD MI355X (gfx950):
+// subvectors of d = 8 C elements (C = 1, 2, 4, 8 or 16 groups of eight) and
+// codebooks of any power-of-two size K.  It serves the shapes the narrow
+// family in gsrq.hip cannot hold in registers (d > 8 or K > 256).
+//
+// What is computed is the same as in the narrow family (arXiv 2607.01065:
+// gain-shape scoring of eq. 5, argmin with ties to the lowest index, the
+// weighted updates of eqs. 6-8 with the safeguards of Sec. 5.2, greedy
+// residual encoding of Sec. 3 / 5.1, gather-sum decoding).  How:
+//  * Operand fragments.  For every codebook and 32-codeword tile a small
+//    kernel writes the A operands of each MFMA of the distance contraction
+//    (hi/lo float16 split of a = -2 g s 2^SA / sigma, and the bias terms) to
+//    a table in the workspace.  The scoring kernel stages the table through
+//    LDS: whole when it fits (resident), else chunk by chunk, double
+//    buffered (streamed), so the codebook side is read from L2 once per
+//    workgroup and from LDS by every wave.
+//  * Rows are the B operands and stay in registers across all tiles.
+//    Float16 stage inputs enter exactly; float32 ones (residuals) as a hi/lo
+//    pair scaled by a per-row power of two.
+//  * Argmin.  Per tile, packed keys with a 4-bit slot (v_min3), then the
+//    tile index of the smallest key; the two lane halves holding a row are
+//    combined at the end.  Rows whose operands leave the float16 range, or
+//    whose best distance exceeds twice their energy, are re-scored exactly
+//    in float64.
+//  * Training accumulation is a kernel of its own: a workgroup owns a slice
+//    of codewords and a chunk of rows, collects the chunk's members of its
+//    slice from the assignment, and sums them in float64 LDS accumulators;
+//    a finalize kernel reduces the per-chunk partials in a fixed order and
+//    applies eqs. 7 and 8 and the stop test.
+//  * Multi-stage encode runs one scoring launch per stage; the float32
+//    residual passes between stages through HBM (a d = 128 residual does
+//    not fit in registers next to the operands).
+#include <algorithm>
+
+#include "gsrq_common.h"
+#include "gsrq_wide.h"
+
+namespace {
+
+constexpr int W_WAVES = 8;
+constexpr int W_THREADS = W_WAVES * 64;
+constexpr int W_ROWS = W_WAVES * RB;            // rows per workgroup round
+constexpr int W_CMAX = 16;                      // d <= 128
+constexpr int W_RESIDENT_BYTES = 63 * 1024;     // fragment tables kept whole in LDS
+constexpr int W_STREAM_BYTES = 30720;           // one staging buffer when streamed
+constexpr int W_SREG = (W_STREAM_BYTES / 16 + W_THREADS - 1) / W_THREADS;  // staged u4 per thread
+constexpr int W_ACC_LDS_BYTES = 98304;          // accumulator slice in LDS
+constexpr int W_ACC_BATCH = 4;                  // rows per thread per collection pass
+constexpr int W_DEC_TABLE_BYTES = 65536;
+constexpr int W_DEC_THREADS = 1024;
+
+enum { W_TRAIN = 0, W_ENCODE = 1 };
+
+// Group pairs of a subvector: lane half h holds group 2p + h of pair p.
+__host__ __device__ constexpr int w_pairs(int C) { return (C + 1) / 2; }
+// Fragments per tile: HI_p, LO_p for every pair, then the bias fragment.
+__host__ __device__ constexpr int w_frags(int C) { return 2 * w_pairs(C) + 1; }
+
+// ------------------------------------------------------------------ kernels
+
+// sigma exponent of each codebook: 2^sig >= its largest gain (unit_gain: 1).
+__global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ gain, int K,
+                                                      int unit_gain, const int* __restrict__ done,
+                                                      int G, int cb0, int* __restrict__ sig) {
+  __shared__ float wm[4];
+  const int cb = cb0 + blockIdx.x;
+  if (done && done[blockIdx.x % G]) return;
+  float m = 0.f;
+  for (int k = threadIdx.x; k < K; k += blockDim.x)
+    m = fmaxf(m, unit_gain ? 1.f : gain[(size_t)cb * K + k]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    sig[cb] = sigma_exp(fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3])));
+}
+
+// Operand fragments of one 32-codeword tile (grid: tiles x codebooks, one
+// wave).  Lane = codeword c (0..31) + 32 h; lane half h covers the 8-element
+// group 2p + h of pair p.  With a_j = -2 g s_j 2^SA / sigma and
+// gg = (g / sigma)^2 2^SA, the tile's fragments are, per lane:
+//   HI_p (p < P)   hi(a[16p + 8h, 16p + 8h + 8))
+//   LO_p (p < P)   lo(a[16p + 8h, 16p + 8h + 8))
+//   bias           h0 [hi(gg) lo(gg) 2^SA 2^SA 0 0 0 0], h1 zero
+// Padding codewords (k >= K) have a = 0 and a float16-max g^2 slot.
+__global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ gain,
+                                                    const float* __restrict__ shape, int d, int K,
+                                                    int C, int unit_gain,
+                                                    const int* __restrict__ sig,
+                                                    const int* __restrict__ done, int G, int cb0,
+                                                    u4* __restrict__ frag) {
+  const int t = blockIdx.x, tiles = gridDim.x;
+  const int cbl = blockIdx.y, cb = cb0 + cbl;
+  if (done && done[cbl % G]) return;
+  const int lane = threadIdx.x, c = lane & 31, h = lane >> 5;
+  const int k = t * CW + c;
+  const bool real = k < K;
+  const int kk = real ? k : K - 1;
+  const float g = real ? (unit_gain ? 1.f : gain[(size_t)cb * K + kk]) : 0.f;
+  const int ex = sig[cb];
+  const float* s = shape + ((size_t)cb * K + kk) * d;
+  const int P = w_pairs(C);
+  u4* out = frag + ((size_t)cbl * tiles + t) * w_frags(C) * 64;
+  for (int p = 0; p < P; ++p) {
+    _Float16 hi[8], lo[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int e = 16 * p + 8 * h + j;
+      const float sv = (real && e < d) ? s[e] : 0.f;
+      const float av = ldexpf(-2.f * g * sv, SA - ex);
+      hi[j] = (_Float16)av;
+      lo[j] = (_Float16)(av - (float)hi[j]);
+    }
+    out[p * 64 + lane] = pack_h8(hi);
+    out[(P + p) * 64 + lane] = pack_h8(lo);
+  }
+  const float gs = ldexpf(g, -ex);
+  const float gg = ldexpf(gs * gs, SA);
+  const _Float16 gh = (_Float16)gg;
+  _Float16 b[8];
+  b[0] = real ? gh : (_Float16)PAD_BIAS;
+  b[1] = real ? (_Float16)(gg - (float)gh) : (_Float16)0.f;
+  b[2] = b[3] = (_Float16)(float)(1 << SA);
+  b[4] = b[5] = b[6] = b[7] = (_Float16)0.f;
+  out[2 * P * 64 + lane] = h ? (u4){0u, 0u, 0u, 0u} : pack_h8(b);
+}
+
+// Seed shapes s_k = x_r / (||x_r|| + eps) from rows of the row-major input.
+template <typename T>
+__global__ void w_seed_kernel(const T* __restrict__ X, int64_t ldx, int d, int K,
+                              const int32_t* __restrict__ seeds, float* __restrict__ shape,
+                              float* __restrict__ seednorm) {
+  const int g = blockIdx.y;
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= K) return;
+  const int64_t row = seeds[(size_t)g * K + k];
+  const T* x = X + row * ldx + (int64_t)g * d;
+  double ss = 0.0;
+  for (int j = 0; j < d; ++j) { const double v = to_f(x[j]); ss = fma(v, v, ss); }
+  const double nrm = sqrt(ss);
+  float* sk = shape + ((size_t)g * K + k) * d;
+  for (int j = 0; j < d; ++j) sk[j] = (float)((double)to_f(x[j]) / (nrm + (double)Y_EPS));
+  seednorm[(size_t)g * K + k] = (float)nrm;
+}
+
+struct WScoreArgs {
+  const void* x;          // stage input rows [N][ldx]
+  int64_t ldx, N;
+  int d, K, G, tiles, QF;
+  int cb0;                // codebook index (gain, shape, sig) of subspace 0: m G
+  int fcb0;               // codebook index of fragment-table entry 0
+  const u4* frag;         // [ncb][tiles][QF][64]
+  const int* sig;         // [ncb]
+  const float* gain;      // [ncb][K]
+  const float* shape;     // [ncb][K][d]
+  int unit_gain;          // score with unit gains (equal-gain initial assignment)
+  // training outputs
+  const float* w;         // [N] or null (all ones)
+  const int* done;        // [G] or null
+  uint16_t* assign;       // [G][N]: old assignment in, new one out
+  int* changed;           // [G][nwg]
+  double* obj;            // [G][nwg] or null
+  // encode outputs
+  uint32_t* codes;        // [N][words], zeroed beforehand, or null
+  int words, b, m;
+  float* res_out;         // [N][G d] float32 residual or null
+  // launch geometry
+  int nwg, rounds, tpc, map_xcd, lg;
+};
+
+// Row-side operands of one row (this lane's row) for all tiles; lane half h
+// holds the groups 2p + h (elements [16p + 8h, 16p + 8h + 8)).
+// F16 rows (the exact float16 stage input, rho = 1):
+//   bx[p] = x of the group;  bias (h0) [sigma sigma hi(rr) lo(rr) 0 0 0 0],
+//   rr = ||x||^2 / sigma, giving D = 2^SA dist / sigma.
+// F32 rows: rho = 2^er >= max|x|, b = x 2^SB / rho:
+//   bx[p] = hi(b), blo[p] = lo(b) of the group,
+//   bias (h0) [2^SB sigma / rho (twice) hi(rr) lo(rr) 0 0 0 0],
+//   rr = 2^SB ||x||^2 / (sigma rho), giving D = 2^(SA+SB) dist / (sigma rho).
+// need_exact flags rows whose operands leave the float16 range.
+template <typename T, int P>
+__device__ __forceinline__ void w_make_b(const T* xp, int d, bool vec, bool valid, int ex, int h,
+                                         u4 (&bx)[P], u4 (&blo)[P], u4& bias, float& rr,
+                                         bool& need_exact) {
+  constexpr bool F16 = sizeof(T) == 2;
+  int sr;
+  if (F16) {
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    float ss = 0.f;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int e0 = 16 * p + 8 * h;
+      if (vec) {
+        // a lone last group (d = 8) leaves lane half 1 empty
+        bx[p] = e0 < d ? ((const u4*)xp)[2 * p + h] : (u4){0u, 0u, 0u, 0u};
+      } else {
+        _Float16 v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = e0 + j < d ? (_Float16)xp[e0 + j] : (_Float16)0.f;
+        bx[p] = pack_h8(v);
+      }
+      if (!valid) bx[p] = (u4){0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // copy the element first: a bit_cast of a vector element reads the
+        // wrong element with this compiler
+        const uint32_t wj = bx[p][j];
+        const h2 v2 = __builtin_bit_cast(h2, wj);
+        ss = __builtin_amdgcn_fdot2(v2, v2, ss, false);
+      }
+    }
+    ss += __shfl_xor(ss, 32);
+    sr = ex;
+    rr = ldexpf(ss, -ex);
+    need_exact = ex > 15 || ex < -14 || !(rr < 32768.f);
+  } else {
+    // pass 1: the row's scale; pass 2 re-reads the (cached) row and splits it
+    float mx = 0.f, ss = 0.f;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int e0 = 16 * p + 8 * h;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e = e0 + j;
+        const float v = (valid && e < d) ? (float)xp[e < d ? e : 0] : 0.f;
+        mx = fmaxf(mx, fabsf(v));
+        ss = fmaf(v, v, ss);
+      }
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    ss += __shfl_xor(ss, 32);
+    int er = 0;
+    frexpf(mx, &er);
+    sr = ex - er + SB;
+    rr = ldexpf(ss, SB - ex - er);
+    need_exact = !(mx > 0.f) || sr > 15 || sr < -14 || !(rr < 32768.f);
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int e0 = 16 * p + 8 * h;
+      _Float16 hi[8], lo[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e = e0 + j;
+        const float x = (valid && e < d) ? (float)xp[e < d ? e : 0] : 0.f;
+        const float v = ldexpf(x, SB - er);
+        hi[j] = (_Float16)v;
+        lo[j] = (_Float16)(v - (float)hi[j]);
+      }
+      bx[p] = pack_h8(hi);
+      blo[p] = pack_h8(lo);
+    }
+  }
+  rr = fminf(rr, 32768.f);
+  sr = sr < -14 ? -14 : (sr > 15 ? 15 : sr);
+  const _Float16 sc = (_Float16)ldexpf(1.f, sr);
+  const _Float16 rh = (_Float16)rr;
+  const _Float16 rl = (_Float16)(rr - (float)rh);
+  bias = h ? (u4){0u, 0u, 0u, 0u} : (u4){pack2(sc, sc), pack2(rh, rl), 0u, 0u};
+}
+
+// Distances of one tile: the MFMA chain over the tile's fragments at `ta`
+// (this lane's entry of fragment 0; fragments are 64 u4 apart).  Per pair:
+// hi(a) x + lo(a) x (float16 rows) or hi(a) hi(b) + lo(a) hi(b) + hi(a) lo(b)
+// (float32 rows); then the bias terms.
+template <bool F16, int P>
+__device__ __forceinline__ f16v w_tile(const u4* ta, const u4 (&bx)[P], const u4 (&blo)[P],
+                                       u4 bias) {
+  f16v acc = {};
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const h8 ahi = as_h8(ta[p * 64]);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi, as_h8(bx[p]), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[(P + p) * 64]), as_h8(bx[p]), acc, 0,
+                                                 0, 0);
+    if (!F16) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi, as_h8(blo[p]), acc, 0, 0, 0);
+  }
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[2 * P * 64]), as_h8(bias), acc, 0, 0,
+                                                0);
+}
+
+// Smallest packed key of a tile: the low 4 bits of each distance carry its
+// slot j (lane l holds codewords 8 (j / 4) + 4 h + j % 4 of row l % 32).
+__device__ __forceinline__ int w_tile_key(const f16v& c) {
+  constexpr int MASK = ~15;
+  int m = min3i((__float_as_int(c[0]) & MASK) | 0, (__float_as_int(c[1]) & MASK) | 1,
+                (__float_as_int(c[2]) & MASK) | 2);
+#pragma unroll
+  for (int j = 3; j < 15; j += 2)
+    m = min3i(m, (__float_as_int(c[j]) & MASK) | j, (__float_as_int(c[j + 1]) & MASK) | (j + 1));
+  return min(m, (__float_as_int(c[15]) & MASK) | 15);
+}
+
+// Running best over tiles in increasing order: a later tile replaces the
+// best only with a strictly smaller distance, so ties keep the lower index.
+__device__ __forceinline__ void w_take(int key, int t, int& best, int& bt) {
+  if (key < (best & ~15)) { best = key; bt = t; }
+}
+
+// Exact float64 argmin over all K codewords for the rows flagged in `mask`
+// (bit i = row i of the wave's block).  Rows are re-read from memory.
+template <typename T>
+__device__ void w_exact_rows(unsigned long long mask, const T* X, int64_t ldx, int64_t r0, int g,
+                             int d, int K, const float* gain, const float* shape, bool unit_gain,
+                             int& kstar) {
+  const int lane = wave_lane();
+  while (mask) {
+    const int L = __ffsll((long long)mask) - 1;
+    mask &= mask - 1;
+    const T* xr = X + (r0 + L) * ldx + (int64_t)g * d;
+    double bd = INFINITY;
+    int bk = 0x7fffffff;
+    for (int k = lane; k < K; k += 64) {
+      const double gk = unit_gain ? 1.0 : (double)gain[k];
+      const float* sk = shape + (size_t)k * d;
+      double dist = 0.0;
+      for (int j = 0; j < d; ++j) {
+        const double r = (double)to_f(xr[j]) - gk * (double)sk[j];
+        dist = fma(r, r, dist);
+      }
+      if (dist < bd) { bd = dist; bk = k; }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const double od = __shfl_xor(bd, off);
+      const int ok = __shfl_xor(bk, off);
+      if (od < bd || (od == bd && ok < bk)) { bd = od; bk = ok; }
+    }
+    if ((lane & 31) == L) kstar = bk;
+  }
+}
+
+// Stage `n` u4 of fragments (tiles t0.. of one codebook, QU fragments each)
+// into registers, then into LDS.
+template <int QU>
+__device__ __forceinline__ void w_stage_load(const u4* ftab, int QF, int t0, int n,
+                                             u4 (&reg)[W_SREG]) {
+#pragma unroll
+  for (int r = 0; r < W_SREG; ++r) {
+    const int e = r * W_THREADS + (int)threadIdx.x;
+    if (e < n) {
+      const int t = e / (QU * 64), o = e - t * (QU * 64);
+      reg[r] = ftab[((size_t)(t0 + t) * QF) * 64 + o];
+    }
+  }
+}
+__device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[W_SREG]) {
+#pragma unroll
+  for (int r = 0; r < W_SREG; ++r) {
+    const int e = r * W_THREADS + (int)threadIdx.x;
+    if (e < n) buf[e] = reg[r];
+  }
+}
+
+// Scoring kernel: assignment (eq. 5) of every row of a chunk for one
+// subspace, then the mode's outputs (training: assignment, changed flag,
+// objective; encode: code bits and residual).  Grid: G x nwg workgroups,
+// numbered so that subspaces whose rows share cache lines run on one XCD.
+// Waves per SIMD: four (two workgroups per CU) with a resident table and
+// narrow rows; two when d >= 64 (row operands up to 68 VGPRs) or when the
+// table is streamed (staging registers).
+template <typename T, int C, int MODE, bool RESIDENT>
+__global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
+    w_score_kernel(WScoreArgs a) {
+  extern __shared__ __align__(16) u4 wtab[];
+  __shared__ double red_obj[W_WAVES];
+  __shared__ int red_changed;
+  constexpr bool F16 = sizeof(T) == 2;
+  constexpr int P = w_pairs(C);
+  constexpr int QU = w_frags(C);
+  // two tiles in flight while the row operands are small
+  constexpr bool PAIR_TILES = C <= 4;
+
+  int g, rc;
+  {
+    const int id = blockIdx.x;
+    if (a.map_xcd) {
+      const int xcd = id & 7, slot = id >> 3, gpx = a.G >> 3;
+      const int j = slot % gpx;
+      rc = slot / gpx;
+      g = ((j / a.lg) * 8 + xcd) * a.lg + (j % a.lg);
+    } else {
+      g = id % a.G;
+      rc = id / a.G;
+    }
+  }
+  if (a.done && a.done[g]) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i = lane & 31, h = lane >> 5;
+  const int d = a.d, K = a.K, tiles = a.tiles;
+  const int cb = a.cb0 + g;
+  const int ex = a.sig[cb];
+  const u4* ftab = a.frag + (size_t)(cb - a.fcb0) * tiles * a.QF * 64;
+  const float* gcb = a.gain + (size_t)cb * K;
+  const float* scb = a.shape + (size_t)cb * K * d;
+  const T* X = (const T*)a.x;
+  const bool vec = (d == 8 * C) && ((a.ldx * (int64_t)sizeof(T)) % 16 == 0) &&
+                   (((uintptr_t)X) % 16 == 0);
+  if (tid == 0) red_changed = 0;
+  if (RESIDENT) {
+    const int n = tiles * QU * 64;
+    for (int e = tid; e < n; e += W_THREADS) {
+      const int t = e / (QU * 64), o = e - t * (QU * 64);
+      wtab[e] = ftab[(size_t)t * a.QF * 64 + o];
+    }
+  }
+  __syncthreads();
+
+  double obj = 0.0;
+  bool any_changed = false;
+  for (int rd = 0; rd < a.rounds; ++rd) {
+    const int64_t r0 = ((int64_t)rc * a.rounds + rd) * W_ROWS + (int64_t)wave * RB;
+    const int64_t row = r0 + i;
+    const bool valid = row < a.N;
+    const T* xp = X + (valid ? row : 0) * a.ldx + (int64_t)g * d;
+    u4 bx[P], blo[P], bias;
+    float rr;
+    bool need_exact;
+    w_make_b<T, P>(xp, d, vec, valid, ex, h, bx, blo, bias, rr, need_exact);
+
+    int best = 0x7fffffff, bt = 0;
+    if (RESIDENT) {
+      for (int t = 0; t < tiles; t += (PAIR_TILES ? 2 : 1)) {
+        const u4* ta = wtab + (size_t)t * QU * 64 + lane;
+        const f16v c0 = w_tile<F16, P>(ta, bx, blo, bias);
+        if (PAIR_TILES && t + 1 < tiles) {
+          const f16v c1 = w_tile<F16, P>(ta + QU * 64, bx, blo, bias);
+          w_take(w_tile_key(c0), t, best, bt);
+          w_take(w_tile_key(c1), t + 1, best, bt);
+        } else {
+          w_take(w_tile_key(c0), t, best, bt);
+        }
+      }
+    } else {
+      const int tpc = a.tpc;
+      const int nch = (tiles + tpc - 1) / tpc;
+      const int chunk_u4 = tpc * QU * 64;
+      u4 reg[W_SREG];
+      {
+        const int n = min(tpc, tiles) * QU * 64;
+        w_stage_load<QU>(ftab, a.QF, 0, n, reg);
+        w_stage_store(wtab, n, reg);
+      }
+      __syncthreads();
+      for (int c = 0; c < nch; ++c) {
+        const int t0 = c * tpc;
+        const int nt = min(tpc, tiles - t0);
+        const int n_next = (c + 1 < nch) ? min(tpc, tiles - t0 - tpc) * QU * 64 : 0;
+        if (n_next) w_stage_load<QU>(ftab, a.QF, t0 + tpc, n_next, reg);
+        const u4* buf = wtab + (size_t)(c & 1) * chunk_u4;
+        for (int tt = 0; tt < nt; tt += (PAIR_TILES ? 2 : 1)) {
+          const u4* ta = buf + (size_t)tt * QU * 64 + lane;
+          const f16v c0 = w_tile<F16, P>(ta, bx, blo, bias);
+          if (PAIR_TILES && tt + 1 < nt) {
+            const f16v c1 = w_tile<F16, P>(ta + QU * 64, bx, blo, bias);
+            w_take(w_tile_key(c0), t0 + tt, best, bt);
+            w_take(w_tile_key(c1), t0 + tt + 1, best, bt);
+          } else {
+            w_take(w_tile_key(c0), t0 + tt, best, bt);
+          }
+        }
+        if (n_next) w_stage_store(wtab + (size_t)((c + 1) & 1) * chunk_u4, n_next, reg);
+        __syncthreads();
+      }
+    }
+
+    // combine the two lane halves of each row: smallest distance, then the
+    // lowest codeword index
+    int kstar;
+    float dhat;
+    {
+      const int j = best & 15;
+      const int kidx = bt * CW + (j >> 2) * 8 + h * 4 + (j & 3);
+      const int hv = best >> 4;
+      const auto sh = __builtin_amdgcn_permlane32_swap(hv, hv, false, false);
+      const auto sk = __builtin_amdgcn_permlane32_swap(kidx, kidx, false, false);
+      const long long v0 = (long long)(int)sh[0] * 4294967296ll + (long long)(unsigned)sk[0];
+      const long long v1 = (long long)(int)sh[1] * 4294967296ll + (long long)(unsigned)sk[1];
+      const long long v = v0 < v1 ? v0 : v1;
+      dhat = __int_as_float((int)(v >> 32) << 4);
+      kstar = (int)(v & 0xffffffffll);
+    }
+    need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
+    const unsigned long long fb = __ballot(valid && need_exact && h == 0);
+    if (fb) w_exact_rows<T>(fb, X, a.ldx, r0, g, d, K, gcb, scb, a.unit_gain != 0, kstar);
+    if (kstar >= K) kstar = K - 1;   // only rows past N can get here
+
+    const float gk = a.unit_gain ? 1.f : gcb[kstar];
+    const float* sk = scb + (size_t)kstar * d;
+    if (MODE == W_TRAIN) {
+      if (valid && h == 0) {
+        uint16_t* ap = a.assign + (size_t)g * a.N + row;
+        if (*ap != (uint16_t)kstar) any_changed = true;
+        *ap = (uint16_t)kstar;
+      }
+      if (a.obj) {
+        // weighted distortion of this assignment under the scoring codebook;
+        // each lane half sums half of the elements
+        float dist = 0.f;
+        const int jb = h * (d / 2), je = jb + d / 2;
+        for (int j = jb; j < je; ++j) {
+          const float r = fmaf(-gk, sk[j], (float)xp[j]);
+          dist = fmaf(r, r, dist);
+        }
+        dist += __shfl_xor(dist, 32);
+        if (valid && h == 0) obj += (double)(a.w ? a.w[row] : 1.f) * (double)dist;
+      }
+    } else {
+      if (valid && h == 0 && a.codes) {
+        const int64_t bit = ((int64_t)a.m * a.G + g) * a.b;
+        uint32_t* wp = a.codes + row * a.words;
+        if (a.b == 8) {
+          ((uint8_t*)wp)[bit >> 3] = (uint8_t)kstar;
+        } else if (a.b == 16) {
+          ((uint16_t*)wp)[bit >> 4] = (uint16_t)kstar;
+        } else {
+          const int off = (int)(bit & 31);
+          atomicOr(wp + (bit >> 5), (uint32_t)kstar << off);
+          if (off + a.b > 32) atomicOr(wp + (bit >> 5) + 1, (uint32_t)kstar >> (32 - off));
+        }
+      }
+      if (valid && a.res_out) {
+        float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d;
+        const int jb = h * (d / 2), je = jb + d / 2;
+        for (int j = jb; j < je; ++j) dst[j] = fmaf(-gk, sk[j], (float)xp[j]);
+      }
+    }
+  }
+  if (MODE == W_TRAIN) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) obj += __shfl_xor(obj, off);
+    if (lane == 0) red_obj[wave] = obj;
+    if (__ballot(any_changed) && lane == 0) atomicOr(&red_changed, 1);
+    __syncthreads();
+    if (tid == 0) {
+      a.changed[(size_t)g * a.nwg + rc] = red_changed;
+      if (a.obj) {
+        double s = 0.0;
+        for (int w = 0; w < W_WAVES; ++w) s += red_obj[w];
+        a.obj[(size_t)g * a.nwg + rc] = s;
+      }
+    }
+  }
+}
+
+struct WAccArgs {
+  const void* x;
+  int64_t ldx, N;
+  int d, K, G;
+  const float* w;          // [N] or null
+  const uint16_t* assign;  // [G][N]
+  const int* done;         // [G] or null
+  double* part;            // [G][rchunks][K][2d+2]
+  int ks, slices, rchunks;
+  int64_t rows_per_chunk;
+};
+
+// Weighted sums of eqs. 6-8 for one (codeword slice, row chunk, subspace):
+// sum w y and sum w x (y = x / (||x|| + eps)), sum w and the member count
+// per codeword, accumulated in float64 LDS and written as one partial.
+// The chunk's members of the slice are collected into an LDS list first;
+// then lanes groups of d/2 lanes take one member row each (two elements
+// per lane).
+template <typename T>
+__global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
+  extern __shared__ double wacc[];
+  __shared__ int list[W_THREADS * W_ACC_BATCH];
+  __shared__ int nlist;
+  const int g = blockIdx.y;
+  if (a.done && a.done[g]) return;
+  const int slice = blockIdx.x % a.slices, rc = blockIdx.x / a.slices;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d, S = 2 * d + 2;
+  const int k0 = slice * a.ks, k1 = min(a.K, k0 + a.ks);
+  for (int e = tid; e < a.ks * S; e += W_THREADS) wacc[e] = 0.0;
+  const int64_t r0 = (int64_t)rc * a.rows_per_chunk;
+  const int64_t r1 = min(a.N, r0 + a.rows_per_chunk);
+  const uint16_t* asg = a.assign + (size_t)g * a.N;
+  const T* X = (const T*)a.x;
+  const int L = d / 2;                 // lanes per member row (power of two)
+  const int per_wave = 64 / L;
+  const int sub = lane / L, li = lane % L;
+  for (int64_t base = r0; base < r1; base += (int64_t)W_THREADS * W_ACC_BATCH) {
+    if (tid == 0) nlist = 0;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < W_ACC_BATCH; ++q) {
+      const int64_t row = base + (int64_t)q * W_THREADS + tid;
+      if (row < r1) {
+        const int k = asg[row];
+        if (k >= k0 && k < k1) list[atomicAdd(&nlist, 1)] = (int)(row - r0);
+      }
+    }
+    __syncthreads();
+    const int n = nlist;
+    for (int it = wave * per_wave + sub; it < n; it += W_WAVES * per_wave) {
+      const int64_t row = r0 + list[it];
+      const int k = asg[row];
+      const T* xr = X + row * a.ldx + (int64_t)g * d;
+      const float x0 = (float)xr[2 * li], x1 = (float)xr[2 * li + 1];
+      float ss = fmaf(x0, x0, x1 * x1);
+      for (int off = L / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
+      const float wt = a.w ? a.w[row] : 1.f;
+      double* ak = wacc + (size_t)(k - k0) * S;
+      unsafeAtomicAdd(ak + 2 * li, (double)(x0 * (wt * inv)));
+      unsafeAtomicAdd(ak + 2 * li + 1, (double)(x1 * (wt * inv)));
+      unsafeAtomicAdd(ak + d + 2 * li, (double)(x0 * wt));
+      unsafeAtomicAdd(ak + d + 2 * li + 1, (double)(x1 * wt));
+      if (li == 0) {
+        unsafeAtomicAdd(ak + 2 * d, (double)wt);
+        unsafeAtomicAdd(ak + 2 * d + 1, 1.0);
+      }
+    }
+    __syncthreads();
+  }
+  double* out = a.part + (((size_t)g * a.rchunks + rc) * a.K + k0) * S;
+  const int n = (k1 - k0) * S;
+  for (int e = tid; e < n; e += W_THREADS) out[e] = wacc[e];
+}
+
+struct WFinArgs {
+  int d, K, G, rchunks, T;
+  int t;                  // iteration (1-based); 0 for the initial gains
+  int no_early_stop, force_changed, nwg;
+  const double* part;     // [G][rchunks][K][2d+2]
+  const int* changed;     // [G][nwg]
+  const double* obj;      // [G][nwg] or null
+  const float* seednorm;  // [G][K]
+  float* gain;            // [G][K]
+  float* shape;           // [G][K][d]
+  int* done;              // [G]: 0 running, else the iteration that stopped
+  int* iters;             // [G]
+  double* trace;          // [G][T] or null
+};
+
+// Codebook update from the chunk partials (fixed order): d/2 lanes per
+// codeword, two elements per lane.  Initial pass (t = 0): eq. (8) gains for
+// the seed shapes (a codeword without members keeps its seed row's norm).
+// Iteration: eqs. (7) and (8) with the safeguards; thread 0 of block 0
+// applies the stop test of its subspace.
+__global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
+  const int g = blockIdx.y;
+  if (a.t > 0 && a.done[g] != 0 && a.done[g] < a.t) return;
+  const int d = a.d, K = a.K, S = 2 * d + 2;
+  const int L = d / 2;
+  const int tid = threadIdx.x;
+  const int k = blockIdx.x * (256 / L) + tid / L;
+  const int li = tid % L;
+  const bool active = k < K;
+  const int kk = active ? k : K - 1;
+  double sy0 = 0, sy1 = 0, sx0 = 0, sx1 = 0, W = 0;
+  for (int c = 0; c < a.rchunks; ++c) {
+    const double* p = a.part + (((size_t)g * a.rchunks + c) * K + kk) * S;
+    sy0 += p[2 * li]; sy1 += p[2 * li + 1];
+    sx0 += p[d + 2 * li]; sx1 += p[d + 2 * li + 1];
+    W += p[2 * d];
+  }
+  float* sk = a.shape + ((size_t)g * K + kk) * d;
+  float* gk = a.gain + (size_t)g * K + kk;
+  double s0 = sk[2 * li], s1 = sk[2 * li + 1];
+  double gnew = (a.t == 0) ? (double)a.seednorm[(size_t)g * K + kk] : (double)*gk;
+  if (W > 0.0) {
+    if (a.t > 0) {
+      double mn = fma(sy0, sy0, sy1 * sy1);
+      for (int off = L / 2; off > 0; off >>= 1) mn += __shfl_xor(mn, off);
+      mn = sqrt(mn);
+      if (mn > SHAPE_KEEP_REL * W) { s0 = sy0 / mn; s1 = sy1 / mn; }
+    }
+    double pr = fma(sx0, s0, sx1 * s1);
+    for (int off = L / 2; off > 0; off >>= 1) pr += __shfl_xor(pr, off);
+    gnew = fmax(0.0, pr / W);
+  }
+  if (active) {
+    sk[2 * li] = (float)s0;
+    sk[2 * li + 1] = (float)s1;
+    if (li == 0) *gk = (float)gnew;
+  }
+  if (a.t > 0 && blockIdx.x == 0 && tid == 0) {
+    int ch = a.force_changed;
+    double obj = 0.0;
+    for (int c = 0; c < a.nwg; ++c) {
+      ch |= a.changed[(size_t)g * a.nwg + c];
+      if (a.obj) obj += a.obj[(size_t)g * a.nwg + c];
+    }
+    if (a.trace) a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
+    a.iters[g] = a.t;
+    if (!ch && !a.no_early_stop) a.done[g] = a.t;
+  }
+}
+
+// --------------------------------------------------------------- decoders
+
+struct WDecArgs {
+  const uint32_t* codes;
+  int64_t N, ldo;
+  int d, K, G, M_use, b, words;
+  const float* gain;
+  const float* shape;
+  void* out;
+  int gpw, gblocks, vec;
+  int64_t rows_per_wg;
+};
+
+__device__ __forceinline__ int w_read_code(const uint32_t* cr, int64_t bit, int b) {
+  const int64_t wi = bit >> 5;
+  const int off = (int)(bit & 31);
+  uint64_t v = cr[wi];
+  if (off + b > 32) v |= (uint64_t)cr[wi + 1] << 32;
+  return (int)((v >> off) & ((1ull << b) - 1));
+}
+
+template <typename TO> __device__ __forceinline__ void w_store8(TO* p, const float* v, bool vec,
+                                                                int n);
+template <> __device__ __forceinline__ void w_store8<_Float16>(_Float16* p, const float* v,
+                                                               bool vec, int n) {
+  if (vec) {
+    h8 hv;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) hv[j] = (_Float16)v[j];
+    *(u4*)p = __builtin_bit_cast(u4, hv);
+  } else {
+    for (int j = 0; j < n; ++j) p[j] = (_Float16)v[j];
+  }
+}
+template <> __device__ __forceinline__ void w_store8<float>(float* p, const float* v, bool vec,
+                                                            int n) {
+  if (vec) {
+    ((f4*)p)[0] = (f4){v[0], v[1], v[2], v[3]};
+    ((f4*)p)[1] = (f4){v[4], v[5], v[6], v[7]};
+  } else {
+    for (int j = 0; j < n; ++j) p[j] = v[j];
+  }
+}
+
+// Gather-sum decoder with the codeword table (g s, float32 or, for one
+// float16 stage, float16) of `gpw` subspaces in LDS; entries of EW = 8 C
+// elements.  One thread per (row, subspace), subspace fastest.
+template <typename TO, typename TT, int C>
+__global__ void __launch_bounds__(W_DEC_THREADS) w_decode_lds_kernel(WDecArgs a) {
+  extern __shared__ __align__(16) unsigned char wdec_smem[];
+  constexpr int EW = 8 * C;
+  TT* tab = (TT*)wdec_smem;
+  const int gpw = a.gpw;
+  const int id = blockIdx.x;
+  const int xcd = id % 8, slot = id / 8;
+  const int gb = slot % a.gblocks;
+  const int rc = (slot / a.gblocks) * 8 + xcd;
+  const int64_t r_begin = (int64_t)rc * a.rows_per_wg;
+  if (r_begin >= a.N) return;
+  const int64_t r_end = min(a.N, r_begin + a.rows_per_wg);
+  const int g0 = gb * gpw;
+  const int ngr = min(gpw, a.G - g0);
+  const int K = a.K, M = a.M_use, d = a.d;
+  const int tid = threadIdx.x;
+  const int entries = ngr * M * K;
+  for (int e = tid; e < entries; e += W_DEC_THREADS) {
+    const int k = e & (K - 1), q2 = e >> a.b;
+    const int m = q2 % M, gi = q2 / M;
+    const size_t cb = (size_t)m * a.G + g0 + gi;
+    const float gk = a.gain[cb * K + k];
+    const float* sv = a.shape + (cb * K + k) * d;
+#pragma unroll
+    for (int j = 0; j < EW; ++j) tab[(size_t)e * EW + j] = (TT)(j < d ? gk * sv[j] : 0.f);
+  }
+  __syncthreads();
+  const int gi = tid % gpw;
+  if (gi >= ngr) return;
+  const int rstep = W_DEC_THREADS / gpw;
+  const int g = g0 + gi;
+  const TT* tg = tab + (size_t)gi * M * K * EW;
+  for (int64_t row = r_begin + tid / gpw; row < r_end; row += rstep) {
+    float acc[EW];
+#pragma unroll
+    for (int j = 0; j < EW; ++j) acc[j] = 0.f;
+    const uint32_t* cr = a.codes + row * a.words;
+    for (int m = 0; m < M; ++m) {
+      const int k = w_read_code(cr, ((int64_t)m * a.G + g) * a.b, a.b);
+      const TT* c = tg + ((size_t)m * K + k) * EW;
+#pragma unroll
+      for (int j = 0; j < EW; ++j) acc[j] += (float)c[j];
+    }
+    TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
+#pragma unroll
+    for (int q = 0; q < C; ++q)
+      w_store8<TO>(dst + 8 * q, acc + 8 * q, a.vec != 0, min(8, d - 8 * q));
+  }
+}
+
+// Gather-sum decoder for codebooks too large for LDS: C lanes per (row,
+// subspace), eight elements per lane, codewords read from global memory.
+template <typename TO>
+__global__ void __launch_bounds__(256) w_decode_gather_kernel(WDecArgs a, int C) {
+  const int tid = threadIdx.x;
+  const int per_block = 256 / C;
+  const int64_t item = (int64_t)blockIdx.x * per_block + tid / C;
+  const int q = tid % C;
+  if (tid / C >= per_block || item >= a.N * a.G) return;
+  const int64_t row = item / a.G;
+  const int g = (int)(item % a.G);
+  const int d = a.d, K = a.K;
+  const uint32_t* cr = a.codes + row * a.words;
+  float acc[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) acc[j] = 0.f;
+  for (int m = 0; m < a.M_use; ++m) {
+    const int k = w_read_code(cr, ((int64_t)m * a.G + g) * a.b, a.b);
+    const size_t cb = (size_t)m * a.G + g;
+    const float gk = a.gain[cb * K + k];
+    const float* sv = a.shape + (cb * K + k) * d + 8 * q;
+    if (a.vec) {
+      const f4 lo = ((const f4*)sv)[0], hi = ((const f4*)sv)[1];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        acc[j] = fmaf(gk, lo[j], acc[j]);
+        acc[4 + j] = fmaf(gk, hi[j], acc[4 + j]);
+      }
+    } else {
+      for (int j = 0; j < 8 && 8 * q + j < d; ++j) acc[j] = fmaf(gk, sv[j], acc[j]);
+    }
+  }
+  TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d + 8 * q;
+  w_store8<TO>(dst, acc, a.vec != 0, min(8, d - 8 * q));
+}
+
+// ------------------------------------------------------------- host side
+
+int w_groups(int d) { return (d + 7) / 8; }
+
+// Template width C (1, 2, 4, 8, 16) that holds d elements.
+int w_cwidth(int d) {
+  const int c = w_groups(d);
+  int C = 1;
+  while (C < c) C *= 2;
+  return C;
+}
+
+struct WLayout {
+  int C, QF, tiles, nwg, rounds, tpc, map_xcd, lg;
+  size_t frag_bytes;
+  bool resident;
+  int Qu;
+  size_t lds;
+};
+
+// Launch geometry of the scoring kernel for one stage input type.
+WLayout w_score_layout(const gsrq_shape* s, size_t x_elt, bool f16rows) {
+  WLayout L;
+  const int64_t G = s->D / s->d;
+  L.C = w_cwidth(s->d);
+  L.QF = w_frags(L.C);
+  L.tiles = (s->K + CW - 1) / CW;
+  L.frag_bytes = (size_t)L.tiles * L.QF * 64 * sizeof(u4);
+  L.Qu = L.QF;
+  (void)f16rows;
+  const size_t used = (size_t)L.tiles * L.Qu * 64 * sizeof(u4);
+  L.resident = used <= (size_t)W_RESIDENT_BYTES;
+  const int64_t row_rounds = (s->N + W_ROWS - 1) / W_ROWS;
+  if (L.resident) {
+    // enough rounds per workgroup to amortise the table load, while
+    // keeping about four workgroups per CU in the grid
+    int64_t r = (row_rounds * G + 1023) / 1024;
+    if (r < 1) r = 1;
+    L.rounds = (int)r;
+    L.tpc = 0;
+    L.lds = used;
+  } else {
+    L.rounds = 1;
+    L.tpc = std::max(1, (int)(W_STREAM_BYTES / (L.Qu * 64 * sizeof(u4))));
+    L.lds = 2 * (size_t)L.tpc * L.Qu * 64 * sizeof(u4);
+  }
+  L.nwg = (int)((row_rounds + L.rounds - 1) / L.rounds);
+  const size_t seg = (size_t)s->d * x_elt;
+  L.lg = seg < 128 ? (int)(128 / seg) : 1;
+  L.map_xcd = (G % (8 * L.lg) == 0) ? 1 : 0;
+  return L;
+}
+
+size_t w_stream_need(const WLayout& L) {
+  return 2 * (size_t)L.tpc * L.Qu * 64 * sizeof(u4);
+}
+
+template <typename T, int C, int MODE>
+gsrq_status w_score_launch_c(const WScoreArgs& a, const WLayout& L, hipStream_t st) {
+  const dim3 grid((unsigned)(a.G * L.nwg));
+  if (L.resident)
+    w_score_kernel<T, C, MODE, true><<<grid, W_THREADS, L.lds, st>>>(a);
+  else
+    w_score_kernel<T, C, MODE, false><<<grid, W_THREADS, L.lds, st>>>(a);
+  return launch_ok();
+}
+
+template <typename T, int MODE>
+gsrq_status w_score_launch(const WScoreArgs& a, const WLayout& L, hipStream_t st) {
+  switch (L.C) {
+    case 1: return w_score_launch_c<T, 1, MODE>(a, L, st);
+    case 2: return w_score_launch_c<T, 2, MODE>(a, L, st);
+    case 4: return w_score_launch_c<T, 4, MODE>(a, L, st);
+    case 8: return w_score_launch_c<T, 8, MODE>(a, L, st);
+    case 16: return w_score_launch_c<T, 16, MODE>(a, L, st);
+  }
+  return GSRQ_E_UNSUPPORTED;
+}
+
+// Fragment tables (and sigma) of `ncb` codebooks starting at cb0.
+gsrq_status w_build_frags(const float* gain, const float* shape, int d, int K, int C, int ncb,
+                          int cb0, bool unit_gain, const int* done, int G, int* sig, u4* frag,
+                          hipStream_t st) {
+  TimedLaunch tl(GSRQ_KERNEL_FRAGMENTS, st);
+  w_sigma_kernel<<<ncb, 256, 0, st>>>(gain, K, unit_gain ? 1 : 0, done, G, cb0, sig);
+  gsrq_status e = launch_ok();
+  if (e) return e;
+  const int tiles = (K + CW - 1) / CW;
+  w_frag_kernel<<<dim3(tiles, ncb), 64, 0, st>>>(gain, shape, d, K, C, unit_gain ? 1 : 0, sig,
+                                                 done, G, cb0, frag);
+  return launch_ok();
+}
+
+struct WAccLayout {
+  int ks, slices, rchunks;
+  int64_t rows_per_chunk;
+  size_t lds;
+};
+
+WAccLayout w_acc_layout(const gsrq_shape* s) {
+  WAccLayout A;
+  const int64_t G = s->D / s->d;
+  const size_t per_k = (size_t)(2 * s->d + 2) * sizeof(double);
+  int ks = 1;
+  while (ks * 2 <= s->K && (size_t)(ks * 2) * per_k <= (size_t)W_ACC_LDS_BYTES) ks *= 2;
+  A.ks = ks;
+  A.slices = (s->K + ks - 1) / ks;
+  int64_t rc = (1024 + A.slices * G - 1) / (A.slices * G);
+  const int64_t max_rc = (s->N + 2047) / 2048;
+  if (rc > max_rc) rc = max_rc;
+  if (rc < 1) rc = 1;
+  A.rows_per_chunk = (s->N + rc - 1) / rc;
+  A.rchunks = (int)((s->N + A.rows_per_chunk - 1) / A.rows_per_chunk);
+  A.lds = (size_t)ks * per_k;
+  return A;
+}
+
+struct WTrainWs {
+  size_t frag, sig, part, changed, obj, assign, done, iters, seednorm, seeds, total;
+};
+
+WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
+  WTrainWs W;
+  const int64_t G = s->D / s->d;
+  // the larger of the two geometries (a later stage may train on float32)
+  const WLayout L16 = w_score_layout(s, x_elt, x_elt == 2);
+  const WAccLayout A = w_acc_layout(s);
+  size_t off = 0;
+  W.frag = off; off = align256(off + (size_t)G * L16.frag_bytes);
+  W.sig = off; off = align256(off + (size_t)G * sizeof(int));
+  W.part = off;
+  off = align256(off + (size_t)G * A.rchunks * s->K * (2 * s->d + 2) * sizeof(double));
+  W.changed = off; off = align256(off + (size_t)G * L16.nwg * sizeof(int));
+  W.obj = off; off = align256(off + (size_t)G * L16.nwg * sizeof(double));
+  W.assign = off; off = align256(off + (size_t)G * s->N * sizeof(uint16_t));
+  W.done = off; off = align256(off + (size_t)G * sizeof(int));
+  W.iters = off; off = align256(off + (size_t)G * sizeof(int));
+  W.seednorm = off; off = align256(off + (size_t)G * s->K * sizeof(float));
+  W.seeds = off; off = align256(off + (size_t)G * s->K * sizeof(int32_t));
+  W.total = off;
+  return W;
+}
+
+struct WEncWs {
+  size_t frag, sig, res0, res1, total;
+};
+
+WEncWs w_encode_ws(const gsrq_shape* s) {
+  WEncWs W;
+  const int64_t G = s->D / s->d;
+  const WLayout L = w_score_layout(s, 4, false);
+  size_t off = 0;
+  W.frag = off; off = align256(off + (size_t)G * L.frag_bytes);
+  W.sig = off; off = align256(off + (size_t)s->M * G * sizeof(int));
+  W.res0 = W.res1 = off;
+  if (s->M > 1) {
+    W.res0 = off; off = align256(off + (size_t)s->N * s->D * sizeof(float));
+    W.res1 = off; off = align256(off + (size_t)s->N * s->D * sizeof(float));
+  }
+  W.total = std::max(off, (size_t)256);
+  return W;
+}
+
+// One encode stage: input rows (type T) -> code bits of stage m and the
+// residual (optional).  The stage's fragment table must be built.
+template <typename T>
+gsrq_status w_encode_stage(const gsrq_shape* s, int m, const void* x, int64_t ldx,
+                           const float* gain, const float* shape, const int* sig, const u4* frag,
+                           uint32_t* codes, int words, float* res_out, hipStream_t st) {
+  const bool f16 = sizeof(T) == 2;
+  const WLayout L = w_score_layout(s, sizeof(T), f16);
+  WScoreArgs a = {};
+  a.x = x; a.ldx = ldx; a.N = s->N; a.d = s->d; a.K = s->K; a.G = s->D / s->d;
+  a.tiles = L.tiles; a.QF = L.QF; a.cb0 = m * a.G; a.fcb0 = m * a.G;
+  a.frag = frag; a.sig = sig; a.gain = gain; a.shape = shape; a.unit_gain = 0;
+  a.codes = codes; a.words = words; a.b = log2i(s->K); a.m = m; a.res_out = res_out;
+  a.nwg = L.nwg; a.rounds = L.rounds; a.tpc = L.tpc; a.map_xcd = L.map_xcd; a.lg = L.lg;
+  TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
+  return w_score_launch<T, W_ENCODE>(a, L, st);
+}
+
+template <typename T>
+gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float* w, int T_,
+                    const int32_t* seed_rows, uint32_t flags, float* gain, float* shape,
+                    float* R_next, uint16_t* assign_io, int32_t* iters_run, double* obj_trace,
+                    void* ws, hipStream_t st) {
+  const int G = s->D / s->d;
+  const int d = s->d, K = s->K;
+  const bool f16 = sizeof(T) == 2;
+  const WLayout L = w_score_layout(s, sizeof(T), f16);
+  const WAccLayout A = w_acc_layout(s);
+  const WTrainWs W = w_train_ws(s, sizeof(T));
+  char* base = (char*)ws;
+  u4* frag = (u4*)(base + W.frag);
+  int* sig = (int*)(base + W.sig);
+  double* part = (double*)(base + W.part);
+  int* changed = (int*)(base + W.changed);
+  double* objp = (double*)(base + W.obj);
+  uint16_t* assign = assign_io ? assign_io : (uint16_t*)(base + W.assign);
+  int* done = (int*)(base + W.done);
+  int* iters = iters_run ? (int*)iters_run : (int*)(base + W.iters);
+  float* seednorm = (float*)(base + W.seednorm);
+  int32_t* seeds = (int32_t*)(base + W.seeds);
+  gsrq_status e;
+  if ((e = fill_u32(done, G, 0, st))) return e;
+  if ((e = fill_u32(iters, G, 0, st))) return e;
+
+  WScoreArgs sa = {};
+  sa.x = X; sa.ldx = ldx; sa.N = s->N; sa.d = d; sa.K = K; sa.G = G;
+  sa.tiles = L.tiles; sa.QF = L.QF; sa.cb0 = 0; sa.fcb0 = 0; sa.frag = frag; sa.sig = sig;
+  sa.gain = gain; sa.shape = shape; sa.w = w; sa.done = done; sa.assign = assign;
+  sa.changed = changed; sa.obj = nullptr;
+  sa.nwg = L.nwg; sa.rounds = L.rounds; sa.tpc = L.tpc; sa.map_xcd = L.map_xcd; sa.lg = L.lg;
+
+  WAccArgs aa;
+  aa.x = X; aa.ldx = ldx; aa.N = s->N; aa.d = d; aa.K = K; aa.G = G; aa.w = w;
+  aa.assign = assign; aa.done = done; aa.part = part;
+  aa.ks = A.ks; aa.slices = A.slices; aa.rchunks = A.rchunks; aa.rows_per_chunk = A.rows_per_chunk;
+  const dim3 agrid((unsigned)(A.slices * A.rchunks), (unsigned)G);
+
+  WFinArgs fa;
+  fa.d = d; fa.K = K; fa.G = G; fa.rchunks = A.rchunks; fa.T = T_; fa.t = 0;
+  fa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
+  fa.force_changed = 0; fa.nwg = L.nwg; fa.part = part; fa.changed = changed; fa.obj = nullptr;
+  fa.seednorm = seednorm; fa.gain = gain; fa.shape = shape; fa.done = done; fa.iters = iters;
+  fa.trace = obj_trace;
+  const int cpb = 256 / (d / 2);
+  const dim3 fgrid((unsigned)((K + cpb - 1) / cpb), (unsigned)G);
+
+  // the accumulator slice can exceed the default dynamic LDS limit
+  if (hipFuncSetAttribute((const void*)w_accumulate_kernel<T>,
+                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)A.lds) != hipSuccess)
+    return GSRQ_E_HIP;
+  auto accumulate_finalize = [&]() -> gsrq_status {
+    gsrq_status e2;
+    {
+      TimedLaunch tl(GSRQ_KERNEL_ACCUMULATE, st);
+      w_accumulate_kernel<T><<<agrid, W_THREADS, A.lds, st>>>(aa);
+    }
+    if ((e2 = launch_ok())) return e2;
+    {
+      TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
+      w_finalize_kernel<<<fgrid, 256, 0, st>>>(fa);
+    }
+    return launch_ok();
+  };
+
+  if (!(flags & GSRQ_RESUME)) {
+    if (hipMemcpyAsync(seeds, seed_rows, (size_t)G * K * sizeof(int32_t), hipMemcpyHostToDevice,
+                       st) != hipSuccess)
+      return GSRQ_E_HIP;
+    {
+      TimedLaunch tl(GSRQ_KERNEL_TRANSPOSE, st);
+      w_seed_kernel<T><<<dim3((K + 255) / 256, G), 256, 0, st>>>((const T*)X, ldx, d, K, seeds,
+                                                                 shape, seednorm);
+    }
+    if ((e = launch_ok())) return e;
+    // equal-gain assignment, then eq. (8) gains for the seed shapes
+    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, true, nullptr, G, sig, frag, st)))
+      return e;
+    sa.unit_gain = 1;
+    sa.done = nullptr;
+    {
+      TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
+      if ((e = w_score_launch<T, W_TRAIN>(sa, L, st))) return e;
+    }
+    sa.unit_gain = 0;
+    sa.done = done;
+    fa.t = 0;
+    if ((e = accumulate_finalize())) return e;
+    fa.force_changed = 0;
+  } else {
+    fa.force_changed = (flags & GSRQ_ASSIGN_IN) ? 0 : 1;
+  }
+  sa.obj = obj_trace ? objp : nullptr;
+  fa.obj = sa.obj;
+  for (int t = 1; t <= T_; ++t) {
+    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, false, done, G, sig, frag, st))) return e;
+    {
+      TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
+      if ((e = w_score_launch<T, W_TRAIN>(sa, L, st))) return e;
+    }
+    fa.t = t;
+    if ((e = accumulate_finalize())) return e;
+    fa.force_changed = 0;
+  }
+  if (R_next) {
+    // next stage's input: the rows re-encoded with the final codebook
+    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, false, nullptr, G, sig, frag, st)))
+      return e;
+    gsrq_shape s1 = *s;
+    s1.M = 1;
+    return w_encode_stage<T>(&s1, 0, X, ldx, gain, shape, sig, frag, nullptr, 0, R_next, st);
+  }
+  return GSRQ_OK;
+}
+
+}  // namespace
+
+namespace gsrq_wide {
+
+bool serves(const gsrq_shape* s) {
+  // d / 8 a power of two: lane groups of d / 2 lanes share a row
+  if (s->d % 8 != 0 || s->d > 8 * W_CMAX || !is_pow2(s->d / 8)) return false;
+  return s->d > 8 || s->K > 256;
+}
+
+size_t train_workspace_bytes(const gsrq_shape* s, size_t x_elt) {
+  if (x_elt == 0)   // either input type
+    return std::max(w_train_ws(s, 2).total, w_train_ws(s, 4).total);
+  return w_train_ws(s, x_elt).total;
+}
+
+size_t encode_workspace_bytes(const gsrq_shape* s) { return w_encode_ws(s).total; }
+
+gsrq_status train_stage(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64_t ldx,
+                        const float* w, int32_t T, const int32_t* seed_rows, uint32_t flags,
+                        float* gain, float* shape, float* R_next, uint16_t* assign_io,
+                        int32_t* iters_run, double* obj_trace, void* workspace, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  if (x_dtype == GSRQ_F16)
+    return w_train<_Float16>(s, X, ldx, w, T, seed_rows, flags, gain, shape, R_next, assign_io,
+                             iters_run, obj_trace, workspace, st);
+  return w_train<float>(s, X, ldx, w, T, seed_rows, flags, gain, shape, R_next, assign_io,
+                        iters_run, obj_trace, workspace, st);
+}
+
+gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64_t ldx,
+                   const float* gain, const float* shape, uint32_t* codes, float* residual,
+                   void* workspace, void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  const int G = s->D / s->d;
+  const WEncWs W = w_encode_ws(s);
+  char* base = (char*)workspace;
+  u4* frag = (u4*)(base + W.frag);
+  int* sig = (int*)(base + W.sig);
+  float* res[2] = {(float*)(base + W.res0), (float*)(base + W.res1)};
+  const int words = (int)((s->M * (int64_t)G * log2i(s->K) + 31) / 32);
+  gsrq_status e;
+  if (codes && (e = fill_u32(codes, (size_t)s->N * words, 0u, st))) return e;
+  const int C = w_cwidth(s->d);
+  for (int m = 0; m < s->M; ++m) {
+    if ((e = w_build_frags(gain, shape, s->d, s->K, C, G, m * G, false, nullptr, G, sig, frag,
+                           st)))
+      return e;
+    float* out = (m + 1 < s->M) ? res[m & 1] : residual;
+    if (m == 0 && x_dtype == GSRQ_F16)
+      e = w_encode_stage<_Float16>(s, m, X, ldx, gain, shape, sig, frag, codes, words, out, st);
+    else if (m == 0)
+      e = w_encode_stage<float>(s, m, X, ldx, gain, shape, sig, frag, codes, words, out, st);
+    else
+      e = w_encode_stage<float>(s, m, res[(m - 1) & 1], s->D, gain, shape, sig, frag, codes,
+                                words, out, st);
+    if (e) return e;
+  }
+  return GSRQ_OK;
+}
+
+gsrq_status decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_use, const float* gain,
+                   const float* shape, void* Xhat, gsrq_dtype out_dtype, int64_t ldo,
+                   void* stream) {
+  hipStream_t st = (hipStream_t)stream;
+  WDecArgs a;
+  a.codes = codes; a.N = s->N; a.ldo = ldo; a.d = s->d; a.K = s->K; a.G = s->D / s->d;
+  a.M_use = M_use; a.b = log2i(s->K);
+  a.words = (int)((s->M * (int64_t)a.G * a.b + 31) / 32);
+  a.gain = gain; a.shape = shape; a.out = Xhat;
+  const size_t esz = out_dtype == GSRQ_F16 ? 2 : 4;
+  // vector stores, and (gather kernel) vector codeword loads
+  a.vec = ((uintptr_t)Xhat % 16 == 0) && ((ldo * esz) % 16 == 0) && (s->d % 8 == 0) &&
+          ((uintptr_t)shape % 16 == 0);
+  const int C = w_cwidth(s->d);
+  TimedLaunch tl(GSRQ_KERNEL_DECODE, st);
+  const bool half_tab = M_use == 1 && out_dtype == GSRQ_F16;
+  const int64_t per_group = (int64_t)M_use * s->K * 8 * C * (half_tab ? 2 : 4);
+  if (C <= 2 && per_group <= W_DEC_TABLE_BYTES) {
+    int gpw = 1;
+    while (gpw * 2 <= 64 && gpw * 2 * per_group <= W_DEC_TABLE_BYTES && gpw < a.G) gpw *= 2;
+    a.gpw = gpw;
+    a.gblocks = (a.G + gpw - 1) / gpw;
+    int64_t rchunks = (256 + a.gblocks - 1) / a.gblocks;
+    if (rchunks * 256 > s->N) rchunks = (s->N + 255) / 256;
+    if (rchunks < 1) rchunks = 1;
+    a.rows_per_wg = (s->N + rchunks - 1) / rchunks;
+    rchunks = (s->N + a.rows_per_wg - 1) / a.rows_per_wg;
+    const int blocks = (int)(8 * a.gblocks * ((rchunks + 7) / 8));
+    const size_t lds = (size_t)gpw * per_group;
+#define W_DEC(TO, TT, CC) w_decode_lds_kernel<TO, TT, CC><<<blocks, W_DEC_THREADS, lds, st>>>(a)
+    if (C == 1) {
+      if (half_tab) W_DEC(_Float16, _Float16, 1);
+      else if (out_dtype == GSRQ_F16) W_DEC(_Float16, float, 1);
+      else W_DEC(float, float, 1);
+    } else {
+      if (half_tab) W_DEC(_Float16, _Float16, 2);
+      else if (out_dtype == GSRQ_F16) W_DEC(_Float16, float, 2);
+      else W_DEC(float, float, 2);
+    }
+#undef W_DEC
+  } else {
+    const int cg = w_groups(s->d);
+    const int per_block = 256 / cg;
+    const int64_t items = s->N * a.G;
+    const int blocks = (int)((items + per_block - 1) / per_block);
+    if (out_dtype == GSRQ_F16)
+      w_decode_gather_kernel<_Float16><<<blocks, 256, 0, st>>>(a, cg);
+    else
+      w_decode_gather_kernel<float><<<blocks, 256, 0, st>>>(a, cg);
+  }
+  return launch_ok();
+}
+
+}  // namespace gsrq_wide

@@ -75,7 +75,8 @@ def load_library(path: str = LIB_PATH):
     return lib
 
 
-KERNEL_KINDS = ("assign", "finalize", "encode", "decode", "transpose")
+KERNEL_KINDS = ("assign", "finalize", "encode", "decode", "transpose", "accumulate",
+                "fragments")
 
 
 def timing_enable(on: bool = True):

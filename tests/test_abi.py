@@ -65,9 +65,15 @@ def test_workspace_queries():
     # per-stage tile table (16 KiB per codebook) in the workspace
     assert B.encode_workspace_bytes(32768, 1024, 8, 256, 1) >= 256
     assert B.encode_workspace_bytes(32768, 1024, 8, 256, 4) >= 4 * 128 * 16 * 1024
-    with pytest.raises(B.GsrqError) as e:
-        B.train_workspace_bytes(100, 64, 16, 256)      # d > 8 not in this build
-    assert e.value.status == B.GSRQ_E_UNSUPPORTED
+    # wide subvectors: fragment tables, per-chunk partials of 2d+2 sums
+    assert B.train_workspace_bytes(65536, 1024, 16, 256) >= 64 * 256 * 34 * 8
+    assert B.train_workspace_bytes(65536, 1024, 128, 4096) >= 8 * 4096 * 258 * 8
+    # multi-stage wide encode passes the float32 residual through the workspace
+    assert B.encode_workspace_bytes(65536, 1024, 128, 4096, 8) >= 2 * 65536 * 1024 * 4
+    for D, d, K in ((48, 24, 256), (512, 256, 256), (16, 4, 512)):
+        with pytest.raises(B.GsrqError) as e:
+            B.train_workspace_bytes(1000, D, d, K)     # not in this build
+        assert e.value.status == B.GSRQ_E_UNSUPPORTED
 
 
 DUMMY = 0x10000  # never dereferenced: validation returns first
@@ -108,8 +114,8 @@ def test_train_stage_validation_before_any_hip_call():
     assert _train(lib, B.make_shape(4, 16, 8, 8, 1), seeds=sp) == B.GSRQ_E_ARG   # N < K
     assert _train(lib, B.make_shape(100, 15, 8, 8, 1), seeds=sp) == B.GSRQ_E_ARG  # d !| D
     assert _train(lib, B.make_shape(100, 16, 8, 6, 1), seeds=sp) == B.GSRQ_E_ARG  # K not 2^b
-    assert _train(lib, B.make_shape(1000, 32, 16, 8, 1), seeds=sp, ldx=32) == B.GSRQ_E_UNSUPPORTED
-    assert _train(lib, B.make_shape(1000, 16, 8, 512, 1), seeds=sp) == B.GSRQ_E_UNSUPPORTED
+    assert _train(lib, B.make_shape(1000, 48, 24, 8, 1), seeds=sp, ldx=48) == B.GSRQ_E_UNSUPPORTED
+    assert _train(lib, B.make_shape(1000, 16, 4, 512, 1), seeds=sp) == B.GSRQ_E_UNSUPPORTED
 
 
 def test_encode_decode_validation_before_any_hip_call():
@@ -123,7 +129,7 @@ def test_encode_decode_validation_before_any_hip_call():
     assert enc(ldx=8) == B.GSRQ_E_ARG
     assert enc(nws=1) == B.GSRQ_E_WORKSPACE
     assert enc(shape=B.make_shape(100, 16, 8, 256, 0)) == B.GSRQ_E_ARG
-    assert enc(shape=B.make_shape(100, 16, 8, 1024, 1)) == B.GSRQ_E_UNSUPPORTED
+    assert enc(shape=B.make_shape(100, 16, 4, 1024, 1)) == B.GSRQ_E_UNSUPPORTED
     dec = lambda **kw: lib.gsrq_decode(
         ctypes.byref(kw.get("shape", sh)), kw.get("codes", DUMMY), kw.get("M_use", 1),
         kw.get("gain", DUMMY), kw.get("shp", DUMMY), kw.get("out", DUMMY),

@@ -216,10 +216,10 @@ def test_argument_errors_on_device():
     with pytest.raises(B.GsrqError) as e:
         B.train_stage(X, 8, 16, 1, seed_rows=np.zeros((2, 16), np.int32))   # N < K
     assert e.value.status == B.GSRQ_E_ARG
-    gain = torch.ones((1, 2, 512), device="cuda")
-    shape = torch.ones((1, 2, 512, 8), device="cuda")
+    gain = torch.ones((1, 4, 512), device="cuda")
+    shape = torch.ones((1, 4, 512, 4), device="cuda")
     with pytest.raises(B.GsrqError) as e:
-        B.encode(X, gain, shape)                                               # K > 256
+        B.encode(X, gain, shape)                                   # d = 4 with K > 256
     assert e.value.status == B.GSRQ_E_UNSUPPORTED
     empty = torch.zeros((0, 16), dtype=torch.float16, device="cuda")
     with pytest.raises(B.GsrqError) as e:
