@@ -81,14 +81,15 @@ def cpu_baseline(kv, wl, n_groups):
         t_enc += t3 - t2
         t_dec += t4 - t3
     per_group = (t_init + T * t_iter + t_enc + t_dec) / n_groups
-    step_s = 2 * wl.G * per_group                       # K and V, every subspace
+    step_s = 2 * wl.G * wl.M * per_group                # K and V, every subspace and stage
     vectors = 2 * wl.N * (wl.D // HEAD_DIM)
     sample_s = t_init + n_iter * t_iter + t_enc + t_dec
     return {
         "value": vectors / step_s, "unit": "vectors/s", "cores": int(threads), "kind": "oracle",
         "sample": (f"float64 oracle on {n_groups} of {wl.G} K-cache subspaces of this workload: "
                    f"init + {n_iter} GSKM iterations + encode + decode each ({sample_s:.1f} s), "
-                   f"scaled to {T} iterations, {wl.G} subspaces and both caches (K, V)"),
+                   f"scaled to {T} iterations, {wl.G} subspaces, {wl.M} stage(s) and both "
+                   f"caches (K, V)"),
         "est_step_s": step_s,
     }
 
@@ -109,7 +110,9 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     wl = synth.WORKLOADS[args.workload]
-    N, D, d, K, T = wl.N, wl.D, wl.d, wl.K, wl.T
+    if wl.layers > 1:
+        raise SystemExit(f"{wl.name} is a multi-layer workload; bench.py times one layer")
+    N, D, d, K, T, M = wl.N, wl.D, wl.d, wl.K, wl.T, wl.M
     G = D // d
     kv = synth.make_kv(wl, layer=0, seed=0)
     dev = torch.device("cuda", 0)
@@ -118,26 +121,31 @@ def main():
                               ("V", kv.values, kv.w_values, kv.seeds_values)):
         caches.append(dict(
             name=name, X=torch.from_numpy(X).to(dev), w=torch.from_numpy(w).to(dev),
-            seeds=np.ascontiguousarray(seeds[0], dtype=np.int32),
-            gain=torch.empty((G, K), dtype=torch.float32, device=dev),
-            shape=torch.empty((G, K, d), dtype=torch.float32, device=dev),
+            seeds=[np.ascontiguousarray(seeds[m], dtype=np.int32) for m in range(M)],
+            gain=torch.empty((M, G, K), dtype=torch.float32, device=dev),
+            shape=torch.empty((M, G, K, d), dtype=torch.float32, device=dev),
             assign=torch.empty((G, N), dtype=torch.int16, device=dev),
-            codes=torch.empty((N, B.code_words(N, D, d, K, 1)), dtype=torch.int32, device=dev),
+            codes=torch.empty((N, B.code_words(N, D, d, K, M)), dtype=torch.int32, device=dev),
             xhat=torch.empty((N, D), dtype=torch.float16, device=dev),
         ))
+    # stage inputs after the first: float32 residuals (ping-pong)
+    rbuf = [torch.empty((N, D), dtype=torch.float32, device=dev) for _ in range(min(M - 1, 2))]
     ws_train = torch.empty(B.train_workspace_bytes(N, D, d, K), dtype=torch.uint8, device=dev)
-    ws_enc = torch.empty(B.encode_workspace_bytes(N, D, d, K, 1), dtype=torch.uint8, device=dev)
+    ws_enc = torch.empty(B.encode_workspace_bytes(N, D, d, K, M), dtype=torch.uint8, device=dev)
     iters = []
 
     def step():
         for c in caches:
-            r = B.train_stage(c["X"], d, K, T, seed_rows=c["seeds"], w=c["w"], gain=c["gain"],
-                              shape=c["shape"], assign=c["assign"], trace=False,
-                              workspace=ws_train)
-            iters.append(r.iters)
-            gain, shape = c["gain"][None], c["shape"][None]
-            B.encode(c["X"], gain, shape, codes=c["codes"], workspace=ws_enc)
-            B.decode(c["codes"], gain, shape, D, out=c["xhat"])
+            R = c["X"]
+            for m in range(M):
+                r = B.train_stage(R, d, K, T, seed_rows=c["seeds"][m], w=c["w"],
+                                  gain=c["gain"][m], shape=c["shape"][m], assign=c["assign"],
+                                  trace=False, workspace=ws_train,
+                                  residual=rbuf[m % 2] if m + 1 < M else False)
+                iters.append(r.iters)
+                R = r.residual
+            B.encode(c["X"], c["gain"], c["shape"], codes=c["codes"], workspace=ws_enc)
+            B.decode(c["codes"], c["gain"], c["shape"], D, out=c["xhat"])
 
     for _ in range(args.warmup):
         step()
@@ -168,17 +176,19 @@ def main():
     iters_run = float(torch.stack(iters).float().mean().item()) if iters else float("nan")
     flops_assign = 2.0 * N * D * K                         # eq. (5) scores, one pass
     achieved = flops_assign / (a_us * 1e-6) / 1e12
-    dec_bytes = N * G * np.log2(K) / 8 + N * D * 2         # packed codes in, fp16 out
+    dec_bytes = N * M * G * np.log2(K) / 8 + N * D * 2     # packed codes in, fp16 out
     out = {
         "metric": METRIC, "value": value, "unit": "vectors/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": wl.name, "shape": wl.note, "tokens": N, "kv_heads": D // HEAD_DIM,
-                   "head_dim": HEAD_DIM, "d": d, "K": K, "M": 1, "T": T, "caches": "K and V",
-                   "bits_per_element": B.bits_per_element(d, K, 1)},
-        "encode_vectors_per_s": (N * (D // HEAD_DIM)) / (e_us * 1e-6),
-        "gskm_iter_per_s": 1e6 / (a_us + f_us),
+                   "head_dim": HEAD_DIM, "d": d, "K": K, "M": M, "T": T, "caches": "K and V",
+                   "bits_per_element": B.bits_per_element(d, K, M)},
+        "encode_vectors_per_s": (N * (D // HEAD_DIM)) / (e_us * 1e-6) / tim["encode"][1]
+                                * (2 * args.steps),
+        "gskm_iter_per_s": 1e6 / (a_us + f_us + (avg_us("accumulate") or 0.0)
+                                  + (avg_us("fragments") or 0.0)),
         "gskm_iters_run_mean": iters_run,
         "decode_GBps": dec_bytes / (dcd_us * 1e-6) / 1e9,
         "decode_hbm_frac": dec_bytes / (dcd_us * 1e-6) / 1e9 / PEAK_HBM_GBPS,

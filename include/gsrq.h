@@ -187,7 +187,8 @@ enum {
   GSRQ_KERNEL_TRANSPOSE = 4,  /* subspace-major copy / seeding of the input */
   GSRQ_KERNEL_ACCUMULATE = 5, /* weighted sums per codeword slice (d > 8)  */
   GSRQ_KERNEL_FRAGMENTS = 6,  /* operand fragment tables (d > 8 or K > 256) */
-  GSRQ_KERNEL_KINDS = 7
+  GSRQ_KERNEL_EXACT = 7,      /* float64 rescoring of deferred rows         */
+  GSRQ_KERNEL_KINDS = 8
 };
 
 /* Measurement hook, the library's only process state.  While enabled, every

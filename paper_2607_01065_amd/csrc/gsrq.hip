@@ -71,15 +71,8 @@ __device__ __forceinline__ void tile_entry(int h, bool real, float g, const floa
   }
   const float gs = ldexpf(g, -ex);
   const float gg = ldexpf(gs * gs, SA);
-  const _Float16 gh = (_Float16)gg;
-  _Float16 bias[8];
-  bias[0] = real ? gh : (_Float16)PAD_BIAS;
-  bias[1] = real ? (_Float16)(gg - (float)gh) : (_Float16)0.f;
-  bias[2] = (_Float16)(float)(1 << SA);
-  bias[3] = (_Float16)(float)(1 << SA);
-  bias[4] = bias[5] = bias[6] = bias[7] = (_Float16)0.f;
   a1 = pack_h8(h ? lo : hi);
-  a2 = pack_h8(h ? bias : hi);
+  a2 = h ? bias_codeword(real, gg) : pack_h8(hi);
 }
 
 // Build this lane's tiles from an LDS codebook (gains [KMAX], shapes
@@ -133,9 +126,16 @@ __device__ __forceinline__ void make_b(const float (&x)[8], u4 raw16, int ex, in
     for (int j = 0; j < 8; ++j) { mx = fmaxf(mx, fabsf(x[j])); ss = fmaf(x[j], x[j], ss); }
     int er = 0;
     frexpf(mx, &er);
+    // a row far below the codebook's scale is scaled relative to sigma
+    // instead (keeps 2^sr in float16 range; b and rr shrink with it, D stays
+    // a positive multiple of the distance); rows so small that b would
+    // leave float16's normal range are re-scored exactly
+    const int er_min = ex + SB - 15;
+    const bool tiny = er < er_min - 12;
+    er = er > er_min ? er : er_min;
     sr = ex - er + SB;
     rr = ldexpf(ss, SB - ex - er);
-    need_exact = !(mx > 0.f) || sr > 15 || sr < -14 || !(rr < 32768.f);
+    need_exact = tiny || !(mx > 0.f) || sr < -14 || !(rr < 32768.f);
     _Float16 hi[8], lo[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -148,10 +148,7 @@ __device__ __forceinline__ void make_b(const float (&x)[8], u4 raw16, int ex, in
   }
   rr = fminf(rr, 32768.f);
   sr = sr < -14 ? -14 : (sr > 15 ? 15 : sr);
-  const _Float16 sc = (_Float16)ldexpf(1.f, sr);
-  const _Float16 rh = (_Float16)rr;
-  const _Float16 rl = (_Float16)(rr - (float)rh);
-  const u4 bias = (u4){pack2(sc, sc), pack2(rh, rl), 0u, 0u};
+  const u4 bias = bias_row(sr, rr);
   if (F16ROWS) {
     b1 = as_h8(raw16);
     b2 = as_h8(h ? bias : (u4){0u, 0u, 0u, 0u});
@@ -212,8 +209,8 @@ __device__ __forceinline__ int reduce_rows(int key, int h, float& dhat) {
   return (int)(v & 0xffffffffll);
 }
 
-// Exact float64 argmin over all K codewords for the rows flagged in `mask`
-// (bit i = row i of the block, lanes 0..31).  gain / shape: this codebook,
+// Exact float64 argmin of eq. (5) over all K codewords for the rows flagged
+// in `mask` (bit i = row i of the block, lanes 0..31).  gain / shape: this codebook,
 // [K] / [K][ld] with d used elements per row (any memory).  Every lane of
 // the wave takes part; both lanes of a flagged row receive its codeword.
 __device__ __forceinline__ void exact_rows(unsigned long long mask, const float (&x)[8], int d,
@@ -229,14 +226,13 @@ __device__ __forceinline__ void exact_rows(unsigned long long mask, const float 
     double bd = INFINITY;
     int bk = 0x7fffffff;
     for (int k = lane; k < K; k += 64) {
+      // eq. (5) up to the row constant ||x||^2: g^2 - 2 g s.x
       const double g = unit_gain ? 1.0 : (double)gain[k];
-      double dist = 0.0;
+      double dot = 0.0;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const double c = (j < d) ? g * (double)shape[(size_t)k * ld + j] : 0.0;
-        const double r = xr[j] - c;
-        dist = fma(r, r, dist);
-      }
+      for (int j = 0; j < 8; ++j)
+        if (j < d) dot = fma(xr[j], (double)shape[(size_t)k * ld + j], dot);
+      const double dist = fma(-2.0 * g, dot, g * g);
       if (dist < bd) { bd = dist; bk = k; }
     }
 #pragma unroll

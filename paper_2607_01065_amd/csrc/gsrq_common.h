@@ -72,6 +72,52 @@ __device__ __forceinline__ int min3i(int a, int b, int c) {
   return r;
 }
 
+// Bias terms of the distance contraction.  The codeword side supplies
+//   [gg_h gg_l 2^SA 2^SA | gg'_h gg'_l 2^(SA-16) 2^(SA-16)]
+// and the row side
+//   [c c rr_h rr_l | c 2^-16  c 2^-16  rr'_h rr'_l],
+// whose dot product is gg c + 2^SA rr.  A value of at least 1/8 goes to the
+// plain hi/lo pair; a smaller one, scaled by 2^16, to the primed pair, so
+// near-zero gains and rows far below the codebook's scale keep a hi/lo pair
+// of normal float16 numbers (about 22 bits) instead of float16 subnormals.
+constexpr float BIAS_SPLIT = 0.125f;
+constexpr int BIAS_SHIFT = 16;
+
+__device__ __forceinline__ void split_bias(float v, _Float16& h, _Float16& l, _Float16& hs,
+                                           _Float16& ls) {
+  const bool big = v >= BIAS_SPLIT;
+  const float vb = big ? v : 0.f;
+  const float vs = big ? 0.f : ldexpf(v, BIAS_SHIFT);
+  h = (_Float16)vb;
+  l = (_Float16)(vb - (float)h);
+  hs = (_Float16)vs;
+  ls = (_Float16)(vs - (float)hs);
+}
+
+// Codeword-side bias entries for gg = (g / sigma)^2 2^SA; a padding
+// codeword (real = false) gets a float16-max g^2 slot.
+__device__ __forceinline__ u4 bias_codeword(bool real, float gg) {
+  _Float16 h, l, hs, ls;
+  split_bias(gg, h, l, hs, ls);
+  if (!real) {
+    h = (_Float16)PAD_BIAS;
+    l = hs = ls = (_Float16)0.f;
+  }
+  const _Float16 one = (_Float16)(float)(1 << SA);
+  const _Float16 one_s = (_Float16)ldexpf(1.f, SA - BIAS_SHIFT);
+  return (u4){pack2(h, l), pack2(one, one), pack2(hs, ls), pack2(one_s, one_s)};
+}
+
+// Row-side bias entries for the bias scale c = 2^sr (sr in [-14, 15]) and
+// the row term rr.
+__device__ __forceinline__ u4 bias_row(int sr, float rr) {
+  const _Float16 c = (_Float16)ldexpf(1.f, sr);
+  const _Float16 cs = (_Float16)ldexpf(1.f, sr - BIAS_SHIFT);
+  _Float16 h, l, hs, ls;
+  split_bias(rr, h, l, hs, ls);
+  return (u4){pack2(c, c), pack2(h, l), pack2(cs, cs), pack2(hs, ls)};
+}
+
 __global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n;
        i += (size_t)gridDim.x * blockDim.x)

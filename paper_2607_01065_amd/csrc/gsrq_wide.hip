@@ -59,21 +59,42 @@ __host__ __device__ constexpr int w_frags(int C) { return 2 * w_pairs(C) + 1; }
 // ------------------------------------------------------------------ kernels
 
 // sigma exponent of each codebook: 2^sig >= its largest gain (unit_gain: 1).
+// Also records the codebook's smallest gain (gmin, for the exact kernel's
+// pruning) and clears the deferred-row state of its subspace (xcount,
+// xchanged, xobj) before a scoring launch.
 __global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ gain, int K,
                                                       int unit_gain, const int* __restrict__ done,
-                                                      int G, int cb0, int* __restrict__ sig) {
-  __shared__ float wm[4];
+                                                      int G, int cb0, int* __restrict__ sig,
+                                                      float* __restrict__ gmin,
+                                                      int* __restrict__ xcount,
+                                                      int* __restrict__ xchanged,
+                                                      double* __restrict__ xobj) {
+  __shared__ float wm[4], wn[4];
   const int cb = cb0 + blockIdx.x;
   if (done && done[blockIdx.x % G]) return;
-  float m = 0.f;
-  for (int k = threadIdx.x; k < K; k += blockDim.x)
-    m = fmaxf(m, unit_gain ? 1.f : gain[(size_t)cb * K + k]);
+  float m = 0.f, n = INFINITY;
+  for (int k = threadIdx.x; k < K; k += blockDim.x) {
+    const float v = unit_gain ? 1.f : gain[(size_t)cb * K + k];
+    m = fmaxf(m, v);
+    n = fminf(n, v);
+  }
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
-  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+  for (int off = 32; off > 0; off >>= 1) {
+    m = fmaxf(m, __shfl_xor(m, off));
+    n = fminf(n, __shfl_xor(n, off));
+  }
+  if ((threadIdx.x & 63) == 0) {
+    wm[threadIdx.x >> 6] = m;
+    wn[threadIdx.x >> 6] = n;
+  }
   __syncthreads();
-  if (threadIdx.x == 0)
+  if (threadIdx.x == 0) {
     sig[cb] = sigma_exp(fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3])));
+    gmin[blockIdx.x] = fminf(fminf(wn[0], wn[1]), fminf(wn[2], wn[3]));
+    xcount[blockIdx.x] = 0;
+    xchanged[blockIdx.x] = 0;
+    xobj[blockIdx.x] = 0.0;
+  }
 }
 
 // Operand fragments of one 32-codeword tile (grid: tiles x codebooks, one
@@ -117,13 +138,7 @@ __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ ga
   }
   const float gs = ldexpf(g, -ex);
   const float gg = ldexpf(gs * gs, SA);
-  const _Float16 gh = (_Float16)gg;
-  _Float16 b[8];
-  b[0] = real ? gh : (_Float16)PAD_BIAS;
-  b[1] = real ? (_Float16)(gg - (float)gh) : (_Float16)0.f;
-  b[2] = b[3] = (_Float16)(float)(1 << SA);
-  b[4] = b[5] = b[6] = b[7] = (_Float16)0.f;
-  out[2 * P * 64 + lane] = h ? (u4){0u, 0u, 0u, 0u} : pack_h8(b);
+  out[2 * P * 64 + lane] = h ? (u4){0u, 0u, 0u, 0u} : bias_codeword(real, gg);
 }
 
 // Seed shapes s_k = x_r / (||x_r|| + eps) from rows of the row-major input.
@@ -151,6 +166,11 @@ struct WScoreArgs {
   int cb0;                // codebook index (gain, shape, sig) of subspace 0: m G
   int fcb0;               // codebook index of fragment-table entry 0
   const u4* frag;         // [ncb][tiles][QF][64]
+  const float* gmin;      // [ncb] smallest gain (same indexing as frag)
+  int* xcount;            // [G] rows deferred to the exact kernel (reset with sigma)
+  int* xrows;             // [G][N] their row indices
+  int* xchanged;          // [G] exact kernel: some deferred row changed code
+  double* xobj;           // [G] exact kernel: their weighted distortion
   const int* sig;         // [ncb]
   const float* gain;      // [ncb][K]
   const float* shape;     // [ncb][K][d]
@@ -169,8 +189,55 @@ struct WScoreArgs {
   int nwg, rounds, tpc, map_xcd, lg;
 };
 
-// Row-side operands of one row (this lane's row) for all tiles; lane half h
-// holds the groups 2p + h (elements [16p + 8h, 16p + 8h + 8)).
+// Raw elements of this lane's half of a row: the groups 2p + h (elements
+// [16p + 8h, 16p + 8h + 8)), in the stage input's type.  The loads never
+// branch (indices clamped into the subvector, values masked later), so a
+// prefetch stays in flight.
+template <typename T, int P> struct WRaw {
+  static constexpr int NV = sizeof(T) == 2 ? P : 2 * P;
+  u4 v[NV];
+  __device__ __forceinline__ void load(const T* xp, int d, bool vec, int h) {
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const int e0 = 16 * p + 8 * h;
+      if (vec) {
+        // a lone last group (d = 8) leaves lane half 1 empty: read group 0
+        const int q = e0 < d ? 2 * p + h : 0;
+        if (sizeof(T) == 2) {
+          v[p] = ((const u4*)xp)[q];
+        } else {
+          v[2 * p] = ((const u4*)xp)[2 * q];
+          v[2 * p + 1] = ((const u4*)xp)[2 * q + 1];
+        }
+      } else {
+        T t[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) t[j] = xp[min(e0 + j, d - 1)];
+        if (sizeof(T) == 2) {
+          v[p] = *(const u4*)t;
+        } else {
+          v[2 * p] = ((const u4*)t)[0];
+          v[2 * p + 1] = ((const u4*)t)[1];
+        }
+      }
+    }
+  }
+  // element j of pair p (as float), zero past d or for an invalid row
+  __device__ __forceinline__ float at(int p, int j, int d, int h, bool valid) const {
+    const int e = 16 * p + 8 * h + j;
+    float x;
+    if (sizeof(T) == 2) {
+      const uint32_t w = v[p][j >> 1];
+      x = (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> (16 * (j & 1))));
+    } else {
+      x = __uint_as_float(v[2 * p + (j >> 2)][j & 3]);
+    }
+    return (valid && e < d) ? x : 0.f;
+  }
+};
+
+// Row-side operands of one row (this lane's row) for all tiles, built from
+// the raw elements; lane half h holds the groups 2p + h.
 // F16 rows (the exact float16 stage input, rho = 1):
 //   bx[p] = x of the group;  bias (h0) [sigma sigma hi(rr) lo(rr) 0 0 0 0],
 //   rr = ||x||^2 / sigma, giving D = 2^SA dist / sigma.
@@ -180,7 +247,77 @@ struct WScoreArgs {
 //   rr = 2^SB ||x||^2 / (sigma rho), giving D = 2^(SA+SB) dist / (sigma rho).
 // need_exact flags rows whose operands leave the float16 range.
 template <typename T, int P>
-__device__ __forceinline__ void w_make_b(const T* xp, int d, bool vec, bool valid, int ex, int h,
+__device__ __forceinline__ void w_make_b(const WRaw<T, P>& raw, int d, bool valid, int ex, int h,
+                                         u4 (&bx)[P], u4 (&blo)[P], u4& bias, float& rr,
+                                         bool& need_exact) {
+  constexpr bool F16 = sizeof(T) == 2;
+  int sr;
+  if (F16) {
+    typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+    float ss = 0.f;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      const bool live = valid && 16 * p + 8 * h < d;   // d is a multiple of 8
+      bx[p] = live ? raw.v[p] : (u4){0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        // copy the element first: a bit_cast of a vector element reads the
+        // wrong element with this compiler
+        const uint32_t wj = bx[p][j];
+        const h2 v2 = __builtin_bit_cast(h2, wj);
+        ss = __builtin_amdgcn_fdot2(v2, v2, ss, false);
+      }
+    }
+    ss += __shfl_xor(ss, 32);
+    sr = ex;
+    rr = ldexpf(ss, -ex);
+    need_exact = ex > 15 || ex < -14 || !(rr < 32768.f);
+  } else {
+    float mx = 0.f, ss = 0.f;
+#pragma unroll
+    for (int p = 0; p < P; ++p)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float v = raw.at(p, j, d, h, valid);
+        mx = fmaxf(mx, fabsf(v));
+        ss = fmaf(v, v, ss);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    ss += __shfl_xor(ss, 32);
+    int er = 0;
+    frexpf(mx, &er);
+    // a row far below the codebook's scale is scaled relative to sigma
+    // instead (keeps 2^sr in float16 range; b and rr shrink with it, D stays
+    // a positive multiple of the distance); rows so small that b would
+    // leave float16's normal range are re-scored exactly
+    const int er_min = ex + SB - 15;
+    const bool tiny = er < er_min - 12;
+    er = er > er_min ? er : er_min;
+    sr = ex - er + SB;
+    rr = ldexpf(ss, SB - ex - er);
+    need_exact = tiny || !(mx > 0.f) || sr < -14 || !(rr < 32768.f);
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      _Float16 hi[8], lo[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float v = ldexpf(raw.at(p, j, d, h, valid), SB - er);
+        hi[j] = (_Float16)v;
+        lo[j] = (_Float16)(v - (float)hi[j]);
+      }
+      bx[p] = pack_h8(hi);
+      blo[p] = pack_h8(lo);
+    }
+  }
+  rr = fminf(rr, 32768.f);
+  sr = sr < -14 ? -14 : (sr > 15 ? 15 : sr);
+  bias = h ? (u4){0u, 0u, 0u, 0u} : bias_row(sr, rr);
+}
+
+// The same operands loaded straight from memory (no prefetch): fewer live
+// registers for wide rows, where a workgroup scores a single round.
+template <typename T, int P>
+__device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bool valid, int ex, int h,
                                          u4 (&bx)[P], u4 (&blo)[P], u4& bias, float& rr,
                                          bool& need_exact) {
   constexpr bool F16 = sizeof(T) == 2;
@@ -232,9 +369,16 @@ __device__ __forceinline__ void w_make_b(const T* xp, int d, bool vec, bool vali
     ss += __shfl_xor(ss, 32);
     int er = 0;
     frexpf(mx, &er);
+    // a row far below the codebook's scale is scaled relative to sigma
+    // instead (keeps 2^sr in float16 range; b and rr shrink with it, D stays
+    // a positive multiple of the distance); rows so small that b would
+    // leave float16's normal range are re-scored exactly
+    const int er_min = ex + SB - 15;
+    const bool tiny = er < er_min - 12;
+    er = er > er_min ? er : er_min;
     sr = ex - er + SB;
     rr = ldexpf(ss, SB - ex - er);
-    need_exact = !(mx > 0.f) || sr > 15 || sr < -14 || !(rr < 32768.f);
+    need_exact = tiny || !(mx > 0.f) || sr < -14 || !(rr < 32768.f);
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       const int e0 = 16 * p + 8 * h;
@@ -253,10 +397,7 @@ __device__ __forceinline__ void w_make_b(const T* xp, int d, bool vec, bool vali
   }
   rr = fminf(rr, 32768.f);
   sr = sr < -14 ? -14 : (sr > 15 ? 15 : sr);
-  const _Float16 sc = (_Float16)ldexpf(1.f, sr);
-  const _Float16 rh = (_Float16)rr;
-  const _Float16 rl = (_Float16)(rr - (float)rh);
-  bias = h ? (u4){0u, 0u, 0u, 0u} : (u4){pack2(sc, sc), pack2(rh, rl), 0u, 0u};
+  bias = h ? (u4){0u, 0u, 0u, 0u} : bias_row(sr, rr);
 }
 
 // Distances of one tile: the MFMA chain over the tile's fragments at `ta`
@@ -297,51 +438,16 @@ __device__ __forceinline__ void w_take(int key, int t, int& best, int& bt) {
   if (key < (best & ~15)) { best = key; bt = t; }
 }
 
-// Exact float64 argmin over all K codewords for the rows flagged in `mask`
-// (bit i = row i of the wave's block).  Rows are re-read from memory.
-template <typename T>
-__device__ void w_exact_rows(unsigned long long mask, const T* X, int64_t ldx, int64_t r0, int g,
-                             int d, int K, const float* gain, const float* shape, bool unit_gain,
-                             int& kstar) {
-  const int lane = wave_lane();
-  while (mask) {
-    const int L = __ffsll((long long)mask) - 1;
-    mask &= mask - 1;
-    const T* xr = X + (r0 + L) * ldx + (int64_t)g * d;
-    double bd = INFINITY;
-    int bk = 0x7fffffff;
-    for (int k = lane; k < K; k += 64) {
-      const double gk = unit_gain ? 1.0 : (double)gain[k];
-      const float* sk = shape + (size_t)k * d;
-      double dist = 0.0;
-      for (int j = 0; j < d; ++j) {
-        const double r = (double)to_f(xr[j]) - gk * (double)sk[j];
-        dist = fma(r, r, dist);
-      }
-      if (dist < bd) { bd = dist; bk = k; }
-    }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
-      const double od = __shfl_xor(bd, off);
-      const int ok = __shfl_xor(bk, off);
-      if (od < bd || (od == bd && ok < bk)) { bd = od; bk = ok; }
-    }
-    if ((lane & 31) == L) kstar = bk;
-  }
-}
-
-// Stage `n` u4 of fragments (tiles t0.. of one codebook, QU fragments each)
-// into registers, then into LDS.
+// The loads never branch (indices past n are clamped and their values never
+// stored), so they stay in flight while the current chunk is scored.
 template <int QU>
 __device__ __forceinline__ void w_stage_load(const u4* ftab, int QF, int t0, int n,
                                              u4 (&reg)[W_SREG]) {
 #pragma unroll
   for (int r = 0; r < W_SREG; ++r) {
-    const int e = r * W_THREADS + (int)threadIdx.x;
-    if (e < n) {
-      const int t = e / (QU * 64), o = e - t * (QU * 64);
-      reg[r] = ftab[((size_t)(t0 + t) * QF) * 64 + o];
-    }
+    const int e = min(r * W_THREADS + (int)threadIdx.x, n - 1);
+    const int t = e / (QU * 64), o = e - t * (QU * 64);
+    reg[r] = ftab[((size_t)(t0 + t) * QF) * 64 + o];
   }
 }
 __device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[W_SREG]) {
@@ -349,6 +455,20 @@ __device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[W_
   for (int r = 0; r < W_SREG; ++r) {
     const int e = r * W_THREADS + (int)threadIdx.x;
     if (e < n) buf[e] = reg[r];
+  }
+}
+
+// Writes code k into the b-bit field at `bit` of a row's words (zeroed
+// beforehand): byte and half-word fields are stored, others OR'd in.
+__device__ __forceinline__ void w_put_code(uint32_t* wp, int64_t bit, int b, int k) {
+  if (b == 8) {
+    ((uint8_t*)wp)[bit >> 3] = (uint8_t)k;
+  } else if (b == 16) {
+    ((uint16_t*)wp)[bit >> 4] = (uint16_t)k;
+  } else {
+    const int off = (int)(bit & 31);
+    atomicOr(wp + (bit >> 5), (uint32_t)k << off);
+    if (off + b > 32) atomicOr(wp + (bit >> 5) + 1, (uint32_t)k >> (32 - off));
   }
 }
 
@@ -368,8 +488,10 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   constexpr bool F16 = sizeof(T) == 2;
   constexpr int P = w_pairs(C);
   constexpr int QU = w_frags(C);
-  // two tiles in flight while the row operands are small
+  // two tiles' MFMA chains in flight, and the next round's row prefetched,
+  // while the row operands are small enough to leave registers for both
   constexpr bool PAIR_TILES = C <= 4;
+  constexpr bool PREFETCH = C <= 2;
 
   int g, rc;
   {
@@ -408,15 +530,29 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
 
   double obj = 0.0;
   bool any_changed = false;
+  // this lane's row of round rd
+  auto row_of = [&](int rd) -> int64_t {
+    return ((int64_t)rc * a.rounds + rd) * W_ROWS + (int64_t)wave * RB + i;
+  };
+  auto row_ptr = [&](int64_t row) -> const T* {
+    return X + (row < a.N ? row : 0) * a.ldx + (int64_t)g * d;
+  };
+  WRaw<T, P> raw;
+  if (PREFETCH) raw.load(row_ptr(row_of(0)), d, vec, h);
   for (int rd = 0; rd < a.rounds; ++rd) {
-    const int64_t r0 = ((int64_t)rc * a.rounds + rd) * W_ROWS + (int64_t)wave * RB;
+    const int64_t r0 = row_of(rd) - i;
     const int64_t row = r0 + i;
     const bool valid = row < a.N;
-    const T* xp = X + (valid ? row : 0) * a.ldx + (int64_t)g * d;
+    const T* xp = row_ptr(row);
     u4 bx[P], blo[P], bias;
     float rr;
     bool need_exact;
-    w_make_b<T, P>(xp, d, vec, valid, ex, h, bx, blo, bias, rr, need_exact);
+    if (PREFETCH)
+      w_make_b<T, P>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact);
+    else
+      w_make_b_direct<T, P>(xp, d, vec, valid, ex, h, bx, blo, bias, rr, need_exact);
+    // the next round's row is fetched while this one is scored
+    if (PREFETCH && rd + 1 < a.rounds) raw.load(row_ptr(row_of(rd + 1)), d, vec, h);
 
     int best = 0x7fffffff, bt = 0;
     if (RESIDENT) {
@@ -481,14 +617,27 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       kstar = (int)(v & 0xffffffffll);
     }
     need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
-    const unsigned long long fb = __ballot(valid && need_exact && h == 0);
-    if (fb) w_exact_rows<T>(fb, X, a.ldx, r0, g, d, K, gcb, scb, a.unit_gain != 0, kstar);
-    if (kstar >= K) kstar = K - 1;   // only rows past N can get here
+    // rows the key cannot decide go to the subspace's list for the exact
+    // kernel, which also writes their outputs; here they are skipped
+    const bool defer = valid && need_exact;
+    {
+      const unsigned long long fb = __ballot(defer && h == 0);
+      if (fb) {
+        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(fb >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)fb, 0u));
+        int base = 0;
+        if (lane == 0) base = atomicAdd(a.xcount + g, __popcll(fb));
+        base = __shfl(base, 0);
+        if (defer && h == 0) a.xrows[(size_t)g * a.N + base + rank] = (int)row;
+      }
+    }
+    if (kstar >= K) kstar = K - 1;   // deferred rows and rows past N only
+    const bool own = valid && !defer;
 
     const float gk = a.unit_gain ? 1.f : gcb[kstar];
     const float* sk = scb + (size_t)kstar * d;
     if (MODE == W_TRAIN) {
-      if (valid && h == 0) {
+      if (own && h == 0) {
         uint16_t* ap = a.assign + (size_t)g * a.N + row;
         if (*ap != (uint16_t)kstar) any_changed = true;
         *ap = (uint16_t)kstar;
@@ -503,23 +652,12 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
           dist = fmaf(r, r, dist);
         }
         dist += __shfl_xor(dist, 32);
-        if (valid && h == 0) obj += (double)(a.w ? a.w[row] : 1.f) * (double)dist;
+        if (own && h == 0) obj += (double)(a.w ? a.w[row] : 1.f) * (double)dist;
       }
     } else {
-      if (valid && h == 0 && a.codes) {
-        const int64_t bit = ((int64_t)a.m * a.G + g) * a.b;
-        uint32_t* wp = a.codes + row * a.words;
-        if (a.b == 8) {
-          ((uint8_t*)wp)[bit >> 3] = (uint8_t)kstar;
-        } else if (a.b == 16) {
-          ((uint16_t*)wp)[bit >> 4] = (uint16_t)kstar;
-        } else {
-          const int off = (int)(bit & 31);
-          atomicOr(wp + (bit >> 5), (uint32_t)kstar << off);
-          if (off + a.b > 32) atomicOr(wp + (bit >> 5) + 1, (uint32_t)kstar >> (32 - off));
-        }
-      }
-      if (valid && a.res_out) {
+      if (own && h == 0 && a.codes)
+        w_put_code(a.codes + row * a.words, ((int64_t)a.m * a.G + g) * a.b, a.b, kstar);
+      if (own && a.res_out) {
         float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d;
         const int jb = h * (d / 2), je = jb + d / 2;
         for (int j = jb; j < je; ++j) dst[j] = fmaf(-gk, sk[j], (float)xp[j]);
@@ -540,6 +678,173 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
         a.obj[(size_t)g * a.nwg + rc] = s;
       }
     }
+  }
+}
+
+// Deferred exact rows: the eq. (5) argmin in float64 (ties to the lowest
+// index) for the rows the scoring kernel listed, and their outputs.  Grid:
+// (workgroups, G); a workgroup takes batches of 16 listed rows of its
+// subspace.  Candidates are pruned by gain per batch, which is exact: with
+// E_k = ||x||^2 + g_k^2 - 2 g_k s_k.x and |s_k.x| <= ||x|| (shapes of norm at
+// most 1), (g_k - ||x||)^2 <= E_k <= (g_k + ||x||)^2, so a codeword with
+// g_k > gmin + 2 max ||x|| (1e-5 relative slack) wins for no row of the
+// batch.  The survivors' s_k.x are accumulated in float64 by 4 waves, wave w
+// holding rows 4w..4w+3 and each lane 4 codewords at a time (a 4 x 4
+// register block over 8-element steps).
+constexpr int W_XROWS = 16;
+constexpr int W_XTHREADS = 256;
+constexpr int W_XKMAX = 8192;    // candidate list capacity (codewords)
+
+template <typename T, int MODE>
+__global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
+  __shared__ __align__(16) float xs[W_XROWS][8 * W_CMAX];
+  __shared__ double xn[W_XROWS];
+  __shared__ int rows[W_XROWS];
+  __shared__ int cand[W_XKMAX];
+  __shared__ int ncand;
+  const int g = blockIdx.y;
+  if (a.done && a.done[g]) return;
+  const int cnt = a.xcount[g];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d, K = a.K;
+  const int cb = a.cb0 + g;
+  const float* gcb = a.gain + (size_t)cb * K;
+  const float* scb = a.shape + (size_t)cb * K * d;
+  const double gmin = (double)a.gmin[cb - a.fcb0];
+  const T* X = (const T*)a.x;
+  for (int b0 = blockIdx.x * W_XROWS; b0 < cnt; b0 += gridDim.x * W_XROWS) {
+    const int nb = min(W_XROWS, cnt - b0);
+    if (tid < W_XROWS) rows[tid] = a.xrows[(size_t)g * a.N + b0 + min(tid, nb - 1)];
+    if (tid == 0) ncand = 0;
+    __syncthreads();
+    for (int e = tid; e < W_XROWS * 8 * W_CMAX; e += W_XTHREADS) {
+      const int i = e / (8 * W_CMAX), j = e % (8 * W_CMAX);
+      xs[i][j] = j < d ? to_f(X[(int64_t)rows[i] * a.ldx + (int64_t)g * d + j]) : 0.f;
+    }
+    __syncthreads();
+    if (tid < W_XROWS) {
+      double q = 0.0;
+      for (int j = 0; j < d; ++j) q = fma((double)xs[tid][j], (double)xs[tid][j], q);
+      xn[tid] = sqrt(q);
+    }
+    __syncthreads();
+    double xmax = 0.0;
+    for (int i = 0; i < W_XROWS; ++i) xmax = fmax(xmax, xn[i]);
+    const double thr = (gmin + 2.0 * xmax) * (1.0 + 1e-5);
+    // candidate list (any order; ties are broken by index below)
+    for (int k0 = 0; k0 < K; k0 += W_XTHREADS) {
+      const int k = k0 + tid;
+      const bool c = k < K && (a.unit_gain ? 1.0 : (double)gcb[k]) <= thr;
+      const unsigned long long m = __ballot(c);
+      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      int base = 0;
+      if (lane == 0 && m) base = atomicAdd(&ncand, __popcll(m));
+      base = __shfl(base, 0);
+      if (c && base + rank < W_XKMAX) cand[base + rank] = k;
+    }
+    __syncthreads();
+    // a list that overflowed falls back to every codeword
+    const int nc = ncand <= W_XKMAX ? ncand : K;
+    const bool all = ncand > W_XKMAX;
+    double bd[4];
+    int bk[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) { bd[r] = INFINITY; bk[r] = 0x7fffffff; }
+    for (int c0 = lane * 4; c0 < nc; c0 += 64 * 4) {
+      int kk[4];
+      double gk[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int ci = min(c0 + q, nc - 1);
+        kk[q] = all ? ci : cand[ci];
+        gk[q] = a.unit_gain ? 1.0 : (double)gcb[kk[q]];
+      }
+      double acc[4][4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[r][q] = 0.0;
+      for (int j0 = 0; j0 < d; j0 += 8) {
+        f4 sv[4][2];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f4* sp = (const f4*)(scb + (size_t)kk[q] * d + j0);
+          sv[q][0] = sp[0];
+          sv[q][1] = sp[1];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const f4* xp = (const f4*)&xs[wave * 4 + r][j0];
+          const f4 x0 = xp[0], x1 = xp[1];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              acc[r][q] = fma((double)x0[j], (double)sv[q][0][j], acc[r][q]);
+              acc[r][q] = fma((double)x1[j], (double)sv[q][1][j], acc[r][q]);
+            }
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (c0 + q >= nc) break;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          // eq. (5) up to the row constant ||x||^2: g^2 - 2 g s.x
+          const double e = fma(-2.0 * gk[q], acc[r][q], gk[q] * gk[q]);
+          if (e < bd[r] || (e == bd[r] && kk[q] < bk[r])) {
+            bd[r] = e;
+            bk[r] = kk[q];
+          }
+        }
+      }
+    }
+    // wave minimum per row, lowest index on ties
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const double od = __shfl_xor(bd[r], off);
+        const int ok = __shfl_xor(bk[r], off);
+        if (od < bd[r] || (od == bd[r] && ok < bk[r])) { bd[r] = od; bk[r] = ok; }
+      }
+    // outputs of this wave's rows
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = wave * 4 + r;
+      if (i >= nb) break;
+      const int64_t row = rows[i];
+      const int k = bk[r];
+      if (MODE == W_TRAIN) {
+        if (a.obj) {
+          // weighted distortion ||x - g s||^2 of the chosen codeword
+          const double gk = a.unit_gain ? 1.0 : (double)gcb[k];
+          double dist = 0.0;
+          for (int j = lane; j < d; j += 64) {
+            const double e = (double)xs[i][j] - gk * (double)scb[(size_t)k * d + j];
+            dist = fma(e, e, dist);
+          }
+#pragma unroll
+          for (int off = 32; off > 0; off >>= 1) dist += __shfl_xor(dist, off);
+          if (lane == 0) atomicAdd(a.xobj + g, (double)(a.w ? a.w[row] : 1.f) * dist);
+        }
+        if (lane == 0) {
+          uint16_t* ap = a.assign + (size_t)g * a.N + row;
+          if (*ap != (uint16_t)k) a.xchanged[g] = 1;
+          *ap = (uint16_t)k;
+        }
+      } else {
+        if (lane == 0 && a.codes)
+          w_put_code(a.codes + row * a.words, ((int64_t)a.m * a.G + g) * a.b, a.b, k);
+        if (a.res_out) {
+          const float gk = gcb[k];
+          float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d;
+          for (int j = lane; j < d; j += 64) dst[j] = fmaf(-gk, scb[(size_t)k * d + j], xs[i][j]);
+        }
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -585,11 +890,17 @@ __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < W_ACC_BATCH; ++q) {
+      // one LDS atomic per wave: members are placed by their rank in the wave
       const int64_t row = base + (int64_t)q * W_THREADS + tid;
-      if (row < r1) {
-        const int k = asg[row];
-        if (k >= k0 && k < k1) list[atomicAdd(&nlist, 1)] = (int)(row - r0);
-      }
+      const int k = row < r1 ? (int)asg[row] : -1;
+      const bool in = k >= k0 && k < k1;
+      const unsigned long long m = __ballot(in);
+      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      int base_idx = 0;
+      if (lane == 0 && m) base_idx = atomicAdd(&nlist, __popcll(m));
+      base_idx = __shfl(base_idx, 0);
+      if (in) list[base_idx + rank] = (int)(row - r0);
     }
     __syncthreads();
     const int n = nlist;
@@ -632,6 +943,8 @@ struct WFinArgs {
   int* done;              // [G]: 0 running, else the iteration that stopped
   int* iters;             // [G]
   double* trace;          // [G][T] or null
+  const int* xchanged;    // [G] changed flag of the exact kernel's rows
+  const double* xobj;     // [G] their objective
 };
 
 // Codebook update from the chunk partials (fixed order): d/2 lanes per
@@ -677,8 +990,8 @@ __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
     if (li == 0) *gk = (float)gnew;
   }
   if (a.t > 0 && blockIdx.x == 0 && tid == 0) {
-    int ch = a.force_changed;
-    double obj = 0.0;
+    int ch = a.force_changed | a.xchanged[g];
+    double obj = a.obj ? a.xobj[g] : 0.0;
     for (int c = 0; c < a.nwg; ++c) {
       ch |= a.changed[(size_t)g * a.nwg + c];
       if (a.obj) obj += a.obj[(size_t)g * a.nwg + c];
@@ -769,21 +1082,37 @@ __global__ void __launch_bounds__(W_DEC_THREADS) w_decode_lds_kernel(WDecArgs a)
   const int rstep = W_DEC_THREADS / gpw;
   const int g = g0 + gi;
   const TT* tg = tab + (size_t)gi * M * K * EW;
-  for (int64_t row = r_begin + tid / gpw; row < r_end; row += rstep) {
-    float acc[EW];
+  constexpr int RBATCH = 4;    // rows in flight per thread
+  for (int64_t r0 = r_begin + tid / gpw; r0 < r_end; r0 += (int64_t)RBATCH * rstep) {
+    float acc[RBATCH][EW];
 #pragma unroll
-    for (int j = 0; j < EW; ++j) acc[j] = 0.f;
-    const uint32_t* cr = a.codes + row * a.words;
+    for (int q = 0; q < RBATCH; ++q)
+#pragma unroll
+      for (int j = 0; j < EW; ++j) acc[q][j] = 0.f;
     for (int m = 0; m < M; ++m) {
-      const int k = w_read_code(cr, ((int64_t)m * a.G + g) * a.b, a.b);
-      const TT* c = tg + ((size_t)m * K + k) * EW;
+      int k[RBATCH];
 #pragma unroll
-      for (int j = 0; j < EW; ++j) acc[j] += (float)c[j];
+      for (int q = 0; q < RBATCH; ++q) {
+        int64_t row = r0 + (int64_t)q * rstep;
+        row = row < r_end ? row : r_begin;    // in range; its result is not stored
+        k[q] = w_read_code(a.codes + row * a.words, ((int64_t)m * a.G + g) * a.b, a.b);
+      }
+#pragma unroll
+      for (int q = 0; q < RBATCH; ++q) {
+        const TT* c = tg + ((size_t)m * K + k[q]) * EW;
+#pragma unroll
+        for (int j = 0; j < EW; ++j) acc[q][j] += (float)c[j];
+      }
     }
-    TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
 #pragma unroll
-    for (int q = 0; q < C; ++q)
-      w_store8<TO>(dst + 8 * q, acc + 8 * q, a.vec != 0, min(8, d - 8 * q));
+    for (int q = 0; q < RBATCH; ++q) {
+      const int64_t row = r0 + (int64_t)q * rstep;
+      if (row >= r_end) break;
+      TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
+#pragma unroll
+      for (int c8 = 0; c8 < C; ++c8)
+        w_store8<TO>(dst + 8 * c8, acc[q] + 8 * c8, a.vec != 0, min(8, d - 8 * c8));
+    }
   }
 }
 
@@ -902,17 +1231,45 @@ gsrq_status w_score_launch(const WScoreArgs& a, const WLayout& L, hipStream_t st
   return GSRQ_E_UNSUPPORTED;
 }
 
-// Fragment tables (and sigma) of `ncb` codebooks starting at cb0.
+// Deferred-row state of the G codebooks a scoring launch uses: smallest
+// gains, row lists and what the exact kernel adds to the stop test and the
+// objective.
+struct WDefer {
+  float* gmin;      // [G]
+  int* xcount;      // [G]
+  int* xrows;       // [G][N]
+  int* xchanged;    // [G]
+  double* xobj;     // [G]
+};
+
+// Fragment tables (and sigma, smallest gain, cleared deferred-row state) of
+// the `ncb` codebooks starting at cb0.
 gsrq_status w_build_frags(const float* gain, const float* shape, int d, int K, int C, int ncb,
                           int cb0, bool unit_gain, const int* done, int G, int* sig, u4* frag,
-                          hipStream_t st) {
+                          const WDefer& X, hipStream_t st) {
   TimedLaunch tl(GSRQ_KERNEL_FRAGMENTS, st);
-  w_sigma_kernel<<<ncb, 256, 0, st>>>(gain, K, unit_gain ? 1 : 0, done, G, cb0, sig);
+  w_sigma_kernel<<<ncb, 256, 0, st>>>(gain, K, unit_gain ? 1 : 0, done, G, cb0, sig, X.gmin,
+                                      X.xcount, X.xchanged, X.xobj);
   gsrq_status e = launch_ok();
   if (e) return e;
   const int tiles = (K + CW - 1) / CW;
   w_frag_kernel<<<dim3(tiles, ncb), 64, 0, st>>>(gain, shape, d, K, C, unit_gain ? 1 : 0, sig,
                                                  done, G, cb0, frag);
+  return launch_ok();
+}
+
+// A scoring launch, then the exact kernel for the rows it deferred.
+constexpr int W_XGRID = 64;    // exact-kernel workgroups per subspace
+
+template <typename T, int MODE>
+gsrq_status w_score_and_exact(const WScoreArgs& a, const WLayout& L, int kind, hipStream_t st) {
+  gsrq_status e;
+  {
+    TimedLaunch tl(kind, st);
+    if ((e = w_score_launch<T, MODE>(a, L, st))) return e;
+  }
+  TimedLaunch tl(GSRQ_KERNEL_EXACT, st);
+  w_exact_kernel<T, MODE><<<dim3(W_XGRID, a.G), W_XTHREADS, 0, st>>>(a);
   return launch_ok();
 }
 
@@ -941,7 +1298,8 @@ WAccLayout w_acc_layout(const gsrq_shape* s) {
 }
 
 struct WTrainWs {
-  size_t frag, sig, part, changed, obj, assign, done, iters, seednorm, seeds, total;
+  size_t frag, gmin, xcount, xrows, xchanged, xobj, sig, part, changed, obj, assign, done, iters,
+      seednorm, seeds, total;
 };
 
 WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
@@ -952,6 +1310,11 @@ WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
   const WAccLayout A = w_acc_layout(s);
   size_t off = 0;
   W.frag = off; off = align256(off + (size_t)G * L16.frag_bytes);
+  W.gmin = off; off = align256(off + (size_t)G * sizeof(float));
+  W.xcount = off; off = align256(off + (size_t)G * sizeof(int));
+  W.xrows = off; off = align256(off + (size_t)G * s->N * sizeof(int));
+  W.xchanged = off; off = align256(off + (size_t)G * sizeof(int));
+  W.xobj = off; off = align256(off + (size_t)G * sizeof(double));
   W.sig = off; off = align256(off + (size_t)G * sizeof(int));
   W.part = off;
   off = align256(off + (size_t)G * A.rchunks * s->K * (2 * s->d + 2) * sizeof(double));
@@ -967,7 +1330,7 @@ WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
 }
 
 struct WEncWs {
-  size_t frag, sig, res0, res1, total;
+  size_t frag, gmin, xcount, xrows, xchanged, xobj, sig, res0, res1, total;
 };
 
 WEncWs w_encode_ws(const gsrq_shape* s) {
@@ -976,6 +1339,11 @@ WEncWs w_encode_ws(const gsrq_shape* s) {
   const WLayout L = w_score_layout(s, 4, false);
   size_t off = 0;
   W.frag = off; off = align256(off + (size_t)G * L.frag_bytes);
+  W.gmin = off; off = align256(off + (size_t)G * sizeof(float));
+  W.xcount = off; off = align256(off + (size_t)G * sizeof(int));
+  W.xrows = off; off = align256(off + (size_t)G * s->N * sizeof(int));
+  W.xchanged = off; off = align256(off + (size_t)G * sizeof(int));
+  W.xobj = off; off = align256(off + (size_t)G * sizeof(double));
   W.sig = off; off = align256(off + (size_t)s->M * G * sizeof(int));
   W.res0 = W.res1 = off;
   if (s->M > 1) {
@@ -991,17 +1359,19 @@ WEncWs w_encode_ws(const gsrq_shape* s) {
 template <typename T>
 gsrq_status w_encode_stage(const gsrq_shape* s, int m, const void* x, int64_t ldx,
                            const float* gain, const float* shape, const int* sig, const u4* frag,
-                           uint32_t* codes, int words, float* res_out, hipStream_t st) {
+                           const WDefer& X, uint32_t* codes, int words, float* res_out,
+                           hipStream_t st) {
   const bool f16 = sizeof(T) == 2;
   const WLayout L = w_score_layout(s, sizeof(T), f16);
   WScoreArgs a = {};
   a.x = x; a.ldx = ldx; a.N = s->N; a.d = s->d; a.K = s->K; a.G = s->D / s->d;
   a.tiles = L.tiles; a.QF = L.QF; a.cb0 = m * a.G; a.fcb0 = m * a.G;
   a.frag = frag; a.sig = sig; a.gain = gain; a.shape = shape; a.unit_gain = 0;
+  a.gmin = X.gmin; a.xcount = X.xcount; a.xrows = X.xrows; a.xchanged = X.xchanged;
+  a.xobj = X.xobj;
   a.codes = codes; a.words = words; a.b = log2i(s->K); a.m = m; a.res_out = res_out;
   a.nwg = L.nwg; a.rounds = L.rounds; a.tpc = L.tpc; a.map_xcd = L.map_xcd; a.lg = L.lg;
-  TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
-  return w_score_launch<T, W_ENCODE>(a, L, st);
+  return w_score_and_exact<T, W_ENCODE>(a, L, GSRQ_KERNEL_ENCODE, st);
 }
 
 template <typename T>
@@ -1017,6 +1387,8 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   const WTrainWs W = w_train_ws(s, sizeof(T));
   char* base = (char*)ws;
   u4* frag = (u4*)(base + W.frag);
+  const WDefer XD = {(float*)(base + W.gmin), (int*)(base + W.xcount), (int*)(base + W.xrows),
+                     (int*)(base + W.xchanged), (double*)(base + W.xobj)};
   int* sig = (int*)(base + W.sig);
   double* part = (double*)(base + W.part);
   int* changed = (int*)(base + W.changed);
@@ -1033,6 +1405,8 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   WScoreArgs sa = {};
   sa.x = X; sa.ldx = ldx; sa.N = s->N; sa.d = d; sa.K = K; sa.G = G;
   sa.tiles = L.tiles; sa.QF = L.QF; sa.cb0 = 0; sa.fcb0 = 0; sa.frag = frag; sa.sig = sig;
+  sa.gmin = XD.gmin; sa.xcount = XD.xcount; sa.xrows = XD.xrows; sa.xchanged = XD.xchanged;
+  sa.xobj = XD.xobj;
   sa.gain = gain; sa.shape = shape; sa.w = w; sa.done = done; sa.assign = assign;
   sa.changed = changed; sa.obj = nullptr;
   sa.nwg = L.nwg; sa.rounds = L.rounds; sa.tpc = L.tpc; sa.map_xcd = L.map_xcd; sa.lg = L.lg;
@@ -1048,7 +1422,7 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   fa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
   fa.force_changed = 0; fa.nwg = L.nwg; fa.part = part; fa.changed = changed; fa.obj = nullptr;
   fa.seednorm = seednorm; fa.gain = gain; fa.shape = shape; fa.done = done; fa.iters = iters;
-  fa.trace = obj_trace;
+  fa.trace = obj_trace; fa.xchanged = XD.xchanged; fa.xobj = XD.xobj;
   const int cpb = 256 / (d / 2);
   const dim3 fgrid((unsigned)((K + cpb - 1) / cpb), (unsigned)G);
 
@@ -1081,14 +1455,11 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
     }
     if ((e = launch_ok())) return e;
     // equal-gain assignment, then eq. (8) gains for the seed shapes
-    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, true, nullptr, G, sig, frag, st)))
+    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, true, nullptr, G, sig, frag, XD, st)))
       return e;
     sa.unit_gain = 1;
     sa.done = nullptr;
-    {
-      TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
-      if ((e = w_score_launch<T, W_TRAIN>(sa, L, st))) return e;
-    }
+    if ((e = w_score_and_exact<T, W_TRAIN>(sa, L, GSRQ_KERNEL_ASSIGN, st))) return e;
     sa.unit_gain = 0;
     sa.done = done;
     fa.t = 0;
@@ -1100,22 +1471,21 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   sa.obj = obj_trace ? objp : nullptr;
   fa.obj = sa.obj;
   for (int t = 1; t <= T_; ++t) {
-    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, false, done, G, sig, frag, st))) return e;
-    {
-      TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
-      if ((e = w_score_launch<T, W_TRAIN>(sa, L, st))) return e;
-    }
+    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, false, done, G, sig, frag, XD, st)))
+      return e;
+    if ((e = w_score_and_exact<T, W_TRAIN>(sa, L, GSRQ_KERNEL_ASSIGN, st))) return e;
     fa.t = t;
     if ((e = accumulate_finalize())) return e;
     fa.force_changed = 0;
   }
   if (R_next) {
     // next stage's input: the rows re-encoded with the final codebook
-    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, false, nullptr, G, sig, frag, st)))
+    if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, false, nullptr, G, sig, frag, XD, st)))
       return e;
     gsrq_shape s1 = *s;
     s1.M = 1;
-    return w_encode_stage<T>(&s1, 0, X, ldx, gain, shape, sig, frag, nullptr, 0, R_next, st);
+    return w_encode_stage<T>(&s1, 0, X, ldx, gain, shape, sig, frag, XD, nullptr, 0, R_next,
+                             st);
   }
   return GSRQ_OK;
 }
@@ -1158,6 +1528,8 @@ gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64
   const WEncWs W = w_encode_ws(s);
   char* base = (char*)workspace;
   u4* frag = (u4*)(base + W.frag);
+  const WDefer XD = {(float*)(base + W.gmin), (int*)(base + W.xcount), (int*)(base + W.xrows),
+                     (int*)(base + W.xchanged), (double*)(base + W.xobj)};
   int* sig = (int*)(base + W.sig);
   float* res[2] = {(float*)(base + W.res0), (float*)(base + W.res1)};
   const int words = (int)((s->M * (int64_t)G * log2i(s->K) + 31) / 32);
@@ -1166,16 +1538,18 @@ gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64
   const int C = w_cwidth(s->d);
   for (int m = 0; m < s->M; ++m) {
     if ((e = w_build_frags(gain, shape, s->d, s->K, C, G, m * G, false, nullptr, G, sig, frag,
-                           st)))
+                           XD, st)))
       return e;
     float* out = (m + 1 < s->M) ? res[m & 1] : residual;
     if (m == 0 && x_dtype == GSRQ_F16)
-      e = w_encode_stage<_Float16>(s, m, X, ldx, gain, shape, sig, frag, codes, words, out, st);
+      e = w_encode_stage<_Float16>(s, m, X, ldx, gain, shape, sig, frag, XD, codes, words, out,
+                                   st);
     else if (m == 0)
-      e = w_encode_stage<float>(s, m, X, ldx, gain, shape, sig, frag, codes, words, out, st);
+      e = w_encode_stage<float>(s, m, X, ldx, gain, shape, sig, frag, XD, codes, words, out,
+                                st);
     else
-      e = w_encode_stage<float>(s, m, res[(m - 1) & 1], s->D, gain, shape, sig, frag, codes,
-                                words, out, st);
+      e = w_encode_stage<float>(s, m, res[(m - 1) & 1], s->D, gain, shape, sig, frag, XD,
+                                codes, words, out, st);
     if (e) return e;
   }
   return GSRQ_OK;

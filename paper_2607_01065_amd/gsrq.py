@@ -76,7 +76,7 @@ def load_library(path: str = LIB_PATH):
 
 
 KERNEL_KINDS = ("assign", "finalize", "encode", "decode", "transpose", "accumulate",
-                "fragments")
+                "fragments", "exact")
 
 
 def timing_enable(on: bool = True):
@@ -185,7 +185,10 @@ class TrainResult:
 def train_stage(X, d, K, T, seed_rows=None, w=None, *, gain=None, shape=None, assign=None,
                 resume=False, assign_in=False, no_early_stop=False, residual=False,
                 trace=True, workspace=None, stream=None) -> TrainResult:
-    """One stage of weighted GSKM on device tensor X [N, D] (see gsrq_train_stage)."""
+    """One stage of weighted GSKM on device tensor X [N, D] (see gsrq_train_stage).
+
+    residual: True for a new R_next tensor, or an [N, D] float32 tensor to
+    write it into."""
     torch = _torch()
     lib = load_library()
     N, D, ldx = _rows(X)
@@ -199,7 +202,10 @@ def train_stage(X, d, K, T, seed_rows=None, w=None, *, gain=None, shape=None, as
         assign = torch.empty((max(G, 1), N), dtype=torch.int16, device=dev)
     iters = torch.empty(max(G, 1), dtype=torch.int32, device=dev)
     tr = torch.empty((max(G, 1), max(T, 1)), dtype=torch.float64, device=dev) if trace and T > 0 else None
-    res = torch.empty((N, D), dtype=torch.float32, device=dev) if residual else None
+    if residual is True:
+        res = torch.empty((N, D), dtype=torch.float32, device=dev)
+    else:   # False / None, or an [N, D] float32 output tensor
+        res = residual if residual is not False else None
     seeds = None
     if seed_rows is not None:
         seeds = np.ascontiguousarray(np.asarray(seed_rows), dtype=np.int32)

@@ -194,3 +194,32 @@ def test_wide_train_stop_rule_and_residual():
     r2 = B.train_stage(to_dev(X), d, K, 5, seed_rows=seeds, w=to_dev(w), no_early_stop=True)
     torch.cuda.synchronize()
     assert np.all(r2.iters.cpu().numpy() == 5)
+
+
+@pytest.mark.parametrize("N,D,d,K", [(700, 32, 8, 256), (700, 64, 16, 256), (300, 256, 128, 512)])
+def test_rows_far_below_codebook_scale(N, D, d, K):
+    """Float32 rows (residuals) 1e3 to 1e5 times smaller than the largest
+    gains, as late residual stages produce: indices follow the margin rule
+    and the residual output is exact (both kernel families)."""
+    say("tiny rows", N, D, d, K)
+    rng = _rng(26, N, D, d, K)
+    G = D // d
+    scale = np.where(rng.random(N) < 0.5, 1e-3, 1e-5)[:, None]
+    X = (rng.standard_normal((N, D)) * scale).astype(np.float32)
+    sh = rng.standard_normal((1, G, K, d))
+    sh /= np.linalg.norm(sh, axis=-1, keepdims=True)
+    gain = rng.uniform(50.0, 150.0, size=(1, G, K))
+    gain[:, :, :K // 8] = rng.uniform(0.0, 2e-3, size=(1, G, K // 8))   # small codewords
+    gain[:, :, K // 8 + 1] = gain[:, :, K // 8]                            # equal gains
+    gain, shape = gain.astype(np.float32), sh.astype(np.float32)
+    codes, res = B.encode(to_dev(X), to_dev(gain), to_dev(shape), residual=True)
+    torch.cuda.synchronize()
+    k = unpack(codes, 1, G, K)
+    X64 = X.astype(np.float64)
+    R = res.cpu().numpy().astype(np.float64)
+    for g in range(G):
+        cols = slice(g * d, (g + 1) * d)
+        check_assignment(X64[:, cols], gain[0, g], shape[0, g], k[:, 0, g], f"g{g}")
+        kk = k[:, 0, g]
+        ref = X64[:, cols] - gain[0, g].astype(np.float64)[kk, None] * shape[0, g].astype(np.float64)[kk]
+        assert np.allclose(R[:, cols], ref, rtol=1e-5, atol=1e-6 * np.abs(ref).max())
