@@ -71,8 +71,10 @@ __device__ __forceinline__ void tile_entry(int h, bool real, float g, const floa
   }
   const float gs = ldexpf(g, -ex);
   const float gg = ldexpf(gs * gs, SA);
+  _Float16 bias[8];
+  bias_codeword_h(real, gg, bias);
   a1 = pack_h8(h ? lo : hi);
-  a2 = h ? bias_codeword(real, gg) : pack_h8(hi);
+  a2 = pack_h8(h ? bias : hi);
 }
 
 // Build this lane's tiles from an LDS codebook (gains [KMAX], shapes

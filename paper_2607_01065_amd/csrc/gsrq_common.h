@@ -73,13 +73,15 @@ __device__ __forceinline__ int min3i(int a, int b, int c) {
 }
 
 // Bias terms of the distance contraction.  The codeword side supplies
-//   [gg_h gg_l 2^SA 2^SA | gg'_h gg'_l 2^(SA-16) 2^(SA-16)]
+//   [gg_h gg_l 2^SA 2^SA | gg'_h gg'_l 0 0]
 // and the row side
-//   [c c rr_h rr_l | c 2^-16  c 2^-16  rr'_h rr'_l],
-// whose dot product is gg c + 2^SA rr.  A value of at least 1/8 goes to the
+//   [c c rr_h rr_l | c 2^-16  c 2^-16  0 0],
+// whose dot product is gg c + 2^SA rr.  A gg of at least 1/8 goes to the
 // plain hi/lo pair; a smaller one, scaled by 2^16, to the primed pair, so
-// near-zero gains and rows far below the codebook's scale keep a hi/lo pair
-// of normal float16 numbers (about 22 bits) instead of float16 subnormals.
+// near-zero gains keep a hi/lo pair of normal float16 numbers (about 22
+// bits) instead of float16 subnormals: their g^2 decides between codewords
+// for rows far below the codebook's scale.  rr is the same for every
+// codeword of a row, so its rounding cannot change the row's argmin.
 constexpr float BIAS_SPLIT = 0.125f;
 constexpr int BIAS_SHIFT = 16;
 
@@ -96,16 +98,21 @@ __device__ __forceinline__ void split_bias(float v, _Float16& h, _Float16& l, _F
 
 // Codeword-side bias entries for gg = (g / sigma)^2 2^SA; a padding
 // codeword (real = false) gets a float16-max g^2 slot.
-__device__ __forceinline__ u4 bias_codeword(bool real, float gg) {
+__device__ __forceinline__ void bias_codeword_h(bool real, float gg, _Float16 (&b)[8]) {
   _Float16 h, l, hs, ls;
   split_bias(gg, h, l, hs, ls);
-  if (!real) {
-    h = (_Float16)PAD_BIAS;
-    l = hs = ls = (_Float16)0.f;
-  }
-  const _Float16 one = (_Float16)(float)(1 << SA);
-  const _Float16 one_s = (_Float16)ldexpf(1.f, SA - BIAS_SHIFT);
-  return (u4){pack2(h, l), pack2(one, one), pack2(hs, ls), pack2(one_s, one_s)};
+  b[0] = real ? h : (_Float16)PAD_BIAS;
+  b[1] = real ? l : (_Float16)0.f;
+  b[2] = b[3] = (_Float16)(float)(1 << SA);
+  b[4] = real ? hs : (_Float16)0.f;
+  b[5] = real ? ls : (_Float16)0.f;
+  b[6] = b[7] = (_Float16)0.f;
+}
+
+__device__ __forceinline__ u4 bias_codeword(bool real, float gg) {
+  _Float16 b[8];
+  bias_codeword_h(real, gg, b);
+  return pack_h8(b);
 }
 
 // Row-side bias entries for the bias scale c = 2^sr (sr in [-14, 15]) and
@@ -113,9 +120,9 @@ __device__ __forceinline__ u4 bias_codeword(bool real, float gg) {
 __device__ __forceinline__ u4 bias_row(int sr, float rr) {
   const _Float16 c = (_Float16)ldexpf(1.f, sr);
   const _Float16 cs = (_Float16)ldexpf(1.f, sr - BIAS_SHIFT);
-  _Float16 h, l, hs, ls;
-  split_bias(rr, h, l, hs, ls);
-  return (u4){pack2(c, c), pack2(h, l), pack2(cs, cs), pack2(hs, ls)};
+  const _Float16 h = (_Float16)rr;
+  const _Float16 l = (_Float16)(rr - (float)h);
+  return (u4){pack2(c, c), pack2(h, l), pack2(cs, cs), 0u};
 }
 
 __global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
