@@ -693,7 +693,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
 // register block over 8-element steps).
 constexpr int W_XROWS = 16;
 constexpr int W_XTHREADS = 256;
-constexpr int W_XKMAX = 8192;    // candidate list capacity (codewords)
+constexpr int W_XKMAX = 4096;    // candidate list capacity (codewords)
 
 template <typename T, int MODE>
 __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
@@ -1082,7 +1082,7 @@ __global__ void __launch_bounds__(W_DEC_THREADS) w_decode_lds_kernel(WDecArgs a)
   const int rstep = W_DEC_THREADS / gpw;
   const int g = g0 + gi;
   const TT* tg = tab + (size_t)gi * M * K * EW;
-  constexpr int RBATCH = 4;    // rows in flight per thread
+  constexpr int RBATCH = C == 1 ? 4 : 2;    // rows in flight per thread (no spills)
   for (int64_t r0 = r_begin + tid / gpw; r0 < r_end; r0 += (int64_t)RBATCH * rstep) {
     float acc[RBATCH][EW];
 #pragma unroll
@@ -1258,8 +1258,10 @@ gsrq_status w_build_frags(const float* gain, const float* shape, int d, int K, i
   return launch_ok();
 }
 
-// A scoring launch, then the exact kernel for the rows it deferred.
-constexpr int W_XGRID = 64;    // exact-kernel workgroups per subspace
+// A scoring launch, then the exact kernel for the rows it deferred (about
+// 512 workgroups in all: most subspaces defer few rows or none, and an empty
+// workgroup only reads its count).
+constexpr int W_XWGS = 512;
 
 template <typename T, int MODE>
 gsrq_status w_score_and_exact(const WScoreArgs& a, const WLayout& L, int kind, hipStream_t st) {
@@ -1269,7 +1271,8 @@ gsrq_status w_score_and_exact(const WScoreArgs& a, const WLayout& L, int kind, h
     if ((e = w_score_launch<T, MODE>(a, L, st))) return e;
   }
   TimedLaunch tl(GSRQ_KERNEL_EXACT, st);
-  w_exact_kernel<T, MODE><<<dim3(W_XGRID, a.G), W_XTHREADS, 0, st>>>(a);
+  const int per_g = std::max(1, std::min(64, W_XWGS / a.G));
+  w_exact_kernel<T, MODE><<<dim3(per_g, a.G), W_XTHREADS, 0, st>>>(a);
   return launch_ok();
 }
 
