@@ -18,6 +18,13 @@ Recipe (every draw from numpy's PCG64, one child SeedSequence per
 Data are drawn in float32 and rounded to the workload's storage dtype.
 A row is one token's K (or V) vector with all heads concatenated
 (D = heads * 128), so one weight per token is shared by every subspace.
+
+Full-cache workloads (many layers of 131072 tokens) draw a layer's tokens on
+the GPU (`make_kv_device`: torch's Philox generator seeded from the layer's
+SeedSequence; keys N(0,1) * sigma_c, values N(0,1), lognormal weights) with
+the channel scales of steps 1-2 above, and calibrate on a separate 4096-token
+draw of the same layer (`make_calibration`, numpy, same recipe from step 3 on
+with its own stream).
 """
 from __future__ import annotations
 
@@ -135,3 +142,52 @@ def small_case(N: int, D: int, d: int, K: int, M: int, seed: int = 0,
     w = rng.lognormal(0.0, 1.0, size=N).astype(np.float32) if weights else np.ones(N, np.float32)
     seeds = draw_seed_rows(rng, N, K, M, D // d)
     return X, w, seeds
+
+
+def layer_scales(wl: Workload, layer: int = 0, seed: int = 0) -> np.ndarray:
+    """Key channel scales of a layer: steps 1-2 of the recipe, from the same
+    stream as make_kv (so both see the same channels)."""
+    rng = _children(seed, wl.name, layer)
+    scales = rng.lognormal(0.0, wl.key_sigma, size=wl.D).astype(np.float32)
+    n_out = int(round(wl.outlier_frac * wl.D))
+    if n_out > 0:
+        ch = rng.choice(wl.D, size=n_out, replace=False)
+        scales[ch] *= np.float32(wl.outlier_mult)
+    return scales
+
+
+def make_calibration(wl: Workload, layer: int = 0, seed: int = 0, N: int = 4096,
+                     M: int | None = None) -> KVBatch:
+    """A calibration slice of a layer: N tokens drawn from their own stream
+    (steps 3-7 of the recipe) with the layer's channel scales."""
+    M = wl.M if M is None else int(M)
+    scales = layer_scales(wl, layer, seed)
+    rng = _children(seed, wl.name + "/calibration", layer)
+    keys = rng.standard_normal((N, wl.D), dtype=np.float32) * scales[None, :]
+    values = rng.standard_normal((N, wl.D), dtype=np.float32)
+    w_k = rng.lognormal(0.0, 1.0, size=N).astype(np.float32)
+    w_v = rng.lognormal(0.0, 1.0, size=N).astype(np.float32)
+    sk = draw_seed_rows(rng, N, wl.K, M, wl.G)
+    sv = draw_seed_rows(rng, N, wl.K, M, wl.G)
+    dt = np.float16 if wl.dtype == "float16" else np.float32
+    return KVBatch(keys.astype(dt), values.astype(dt), w_k, w_v, sk, sv, scales)
+
+
+def make_kv_device(wl: Workload, layer: int = 0, seed: int = 0, device="cuda",
+                   N: int | None = None):
+    """(keys, values, w_keys, w_values) of one layer drawn on the device with
+    torch's generator seeded from the layer's SeedSequence; keys use the
+    layer's channel scales.  Storage dtype as the workload's."""
+    import torch
+
+    N = wl.N if N is None else int(N)
+    scales = torch.from_numpy(layer_scales(wl, layer, seed)).to(device)
+    ss = np.random.SeedSequence([seed, layer] + [ord(c) for c in wl.name + "/device"])
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(ss.generate_state(1, dtype=np.uint64)[0] & ((1 << 63) - 1)))
+    dt = torch.float16 if wl.dtype == "float16" else torch.float32
+    keys = (torch.randn((N, wl.D), generator=gen, device=device) * scales[None, :]).to(dt)
+    values = torch.randn((N, wl.D), generator=gen, device=device).to(dt)
+    w_k = torch.empty(N, device=device).log_normal_(0.0, 1.0, generator=gen)
+    w_v = torch.empty(N, device=device).log_normal_(0.0, 1.0, generator=gen)
+    return keys, values, w_k, w_v

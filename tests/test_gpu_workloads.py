@@ -226,3 +226,32 @@ def test_argument_errors_on_device():
         B.encode(empty, torch.ones((1, 2, 16), device="cuda"),
                  torch.ones((1, 2, 16, 8), device="cuda"))                     # N = 0
     assert e.value.status == B.GSRQ_E_ARG
+
+
+@pytest.mark.parametrize("layer", [0, 31])
+def test_full_cache_layer_sampled(layer):
+    """Full-model cache workload, one layer at full size: K and V codebooks
+    trained on the layer's 4096-token calibration draw, then all 131072 tokens
+    encoded and decoded; sampled subspaces follow the margin rule on the GPU's
+    codebook, sampled decoded rows are exact."""
+    wl = synth.WORKLOADS["llama3_8b_cache_1bit"]
+    N, D, d, K = wl.N, wl.D, wl.d, wl.K
+    say("full cache layer", layer, N, D, d, K)
+    cal = synth.make_calibration(wl, layer, seed=0, N=4096, M=1)
+    keys, values, _, _ = synth.make_kv_device(wl, layer, seed=0)
+    rows = np.sort(np.random.default_rng(layer).choice(N, 4096, replace=False))
+    for name, X, Xc, wc, seeds in (("keys", keys, cal.keys, cal.w_keys, cal.seeds_keys),
+                                   ("values", values, cal.values, cal.w_values, cal.seeds_values)):
+        r = B.train_stage(to_dev(Xc), d, K, wl.T, seed_rows=seeds[0], w=to_dev(wc), trace=False)
+        gain, shape = r.gain[None].contiguous(), r.shape[None].contiguous()
+        codes, _ = B.encode(X, gain, shape)
+        xh = B.decode(codes, gain, shape, D, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        g_np, s_np = gain.cpu().numpy(), shape.cpu().numpy()
+        k = O.unpack_codes(codes.cpu().numpy().view(np.uint32)[rows], 1, wl.G, K)
+        Xs = X[torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+        for g in [0, 17, 64, 127]:
+            check_assignment(Xs[:, g * d:(g + 1) * d], g_np[0, g], s_np[0, g], k[:, 0, g],
+                             f"{name} layer {layer} g{g}")
+        ref = O.gsrq_decode(k, g_np, s_np)
+        assert np.array_equal(xh.cpu().numpy()[rows], ref.astype(np.float32))
