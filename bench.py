@@ -269,7 +269,7 @@ def main():
                    "bits_per_element": B.bits_per_element(d, K, M)},
         "encode_vectors_per_s": (N * (D // HEAD_DIM)) / (e_us * 1e-6) / tim["encode"][1]
                                 * (2 * args.steps),
-        "gskm_iter_per_s": 1e6 / (a_us + f_us + (avg_us("accumulate") or 0.0)
+        "gskm_iter_per_s": 1e6 / (a_us + (f_us or 0.0) + (avg_us("accumulate") or 0.0)
                                   + (avg_us("fragments") or 0.0)),
         "gskm_iters_run_mean": iters_run,
         "decode_GBps": dec_bytes / (dcd_us * 1e-6) / 1e9,

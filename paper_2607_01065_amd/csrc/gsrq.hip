@@ -38,7 +38,9 @@ constexpr int ACC = 18;          // sum w y[8], sum w x[8], W, count
 constexpr int PSTRIDE = KMAX * ACC + 2;  // + objective, changed flag
 constexpr int TRAIN_WAVES = 12;        // one 768-thread workgroup per CU
 constexpr int WAVES_PER_SIMD = 3;      // 168 VGPRs: operand tiles stay in registers
-constexpr int TRAIN_CHUNK_ROWS = 8192;
+constexpr int TRAIN_CHUNK_MAX = 16384;  // rows of one (chunk, subspace) workgroup, at most
+constexpr int TRAIN_CHUNK_MIN = 2048;   // and at least (unless N is smaller)
+constexpr int TRAIN_SLOTS = 256;        // workgroups resident at once (one per CU)
 constexpr int ENC_WAVES = 4;           // one subspace per wave, three workgroups per CU
 constexpr int ENC_CHUNK_ROWS = 1024;
 constexpr int ENC_MAX_STAGES = 8;      // stages staged in LDS by one encode launch
@@ -103,8 +105,7 @@ __device__ __forceinline__ void build_tiles(Tiles& tl, const float* cbg, const f
 // rows whose operands leave the float16 range.
 template <bool F16ROWS>
 __device__ __forceinline__ void make_b(const float (&x)[8], u4 raw16, int ex, int h, h8& b1,
-                                       h8& b2, float& rr, bool& need_exact) {
-  float ss;
+                                       h8& b2, float& rr, bool& need_exact, float& ss) {
   int sr;
   if (F16ROWS) {
     // ||x||^2 from packed float16 dot products (exact products, float32 sums)
@@ -394,15 +395,155 @@ struct AssignArgs {
   int64_t N;
   int d, K, G;
   const float* w;        // [N] or null
-  const float* gain;     // [G][K]
-  const float* shape;    // [G][K][d]
+  float* gain;           // [G][K]; updated in place by the update kernel
+  float* shape;          // [G][K][d]; likewise
   uint16_t* assign;      // [G][N]
-  const int* done;       // [G]
+  int* done;             // [G] iteration at which the subspace stopped, 0 = running
+  int* iters;            // [G] iterations run
   double* part;          // [G][chunks][PSTRIDE]
+  const float* seednorm; // [G][K] seed row norms (initial gains)
+  double* trace;         // [G][T] objective per iteration, or null
+  double* wxx;           // [G] sum_i w_i ||x_i||^2 (constant over the iterations)
+  int want_wxx;          // this launch accumulates wxx (first pass that needs it)
   int chunks;
+  int chunk_rows;        // rows per chunk (a multiple of RB)
   int force_changed;
-  int want_obj;          // accumulate the objective (for the trace)
+  int t;                 // iteration number (1-based); 0 for the initialisation
+  int T;
+  int no_early_stop;
 };
+
+// Codebook update of subspace g from the partial sums of all its chunks,
+// reduced in chunk order (the result does not depend on which workgroup
+// finishes last).  Initialisation: eq. (8) gains of the seed shapes.
+// Iteration: eqs. (7) and (8), plus the weighted objective of the
+// assignment just made, from the sufficient statistics of the codebook it
+// was made with:
+//   sum_i w_i ||x_i - g s||^2 = sum_i w_i ||x_i||^2
+//                               - sum_k (2 g_k s_k . S_k - g_k^2 ||s_k||^2 W_k),
+// S_k = sum of w x over the members of k, W_k = their weight (products and
+// sums in float64, so the cancellation costs no accuracy); and the stop
+// test (no assignment changed).  One workgroup per subspace; thread k
+// updates codeword k.
+constexpr int UPD_THREADS = 1024;
+constexpr int UPD_EPT = (KMAX * ACC + 2 + UPD_THREADS - 1) / UPD_THREADS;  // sums per thread
+constexpr int UPD_CBATCH = 4;                                             // chunks per load batch
+static_assert(KMAX <= UPD_THREADS, "one thread per codeword");
+template <int MODE>
+__global__ void __launch_bounds__(UPD_THREADS) update_kernel(AssignArgs a) {
+  __shared__ double sums[KMAX * ACC + 2];
+  __shared__ double wred[UPD_THREADS / 64];
+  const int g = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d, K = a.K;
+  const double* pg = a.part + (size_t)g * a.chunks * PSTRIDE;
+  // every input is requested up front: the stop flag, this thread's old
+  // codeword and the partial sums; a subspace that had already stopped
+  // (its partials are stale) writes nothing
+  const int stopped = MODE == MODE_ITER ? a.done[g] : 0;
+  const int kmine = tid < K ? tid : 0;
+  float* sk = a.shape + ((size_t)g * K + kmine) * d;
+  float* gk = a.gain + (size_t)g * K + kmine;
+  float sold[DP];
+#pragma unroll
+  for (int j = 0; j < DP; ++j) sold[j] = sk[j < d ? j : 0];
+  const float gold = MODE == MODE_INIT ? a.seednorm[(size_t)g * K + kmine] : *gk;
+  // element-wise chunk sums (coalesced, in chunk order) into LDS; loads are
+  // unconditional (clamped indices, masked values) so a batch is in flight
+  // at once
+  const int nsum = K * ACC + 2;
+  double v[UPD_EPT];
+#pragma unroll
+  for (int u = 0; u < UPD_EPT; ++u) v[u] = 0.0;
+  for (int c0 = 0; c0 < a.chunks; c0 += UPD_CBATCH) {
+    double pv[UPD_CBATCH][UPD_EPT];
+#pragma unroll
+    for (int cc = 0; cc < UPD_CBATCH; ++cc)
+#pragma unroll
+      for (int u = 0; u < UPD_EPT; ++u) {
+        const int e = tid + u * UPD_THREADS;
+        const int src = e < K * ACC ? e : KMAX * ACC + (e < nsum ? e - K * ACC : 0);
+        const int c = c0 + cc < a.chunks ? c0 + cc : 0;
+        pv[cc][u] = pg[(size_t)c * PSTRIDE + src];
+      }
+#pragma unroll
+    for (int cc = 0; cc < UPD_CBATCH; ++cc)
+#pragma unroll
+      for (int u = 0; u < UPD_EPT; ++u) {
+        const int e = tid + u * UPD_THREADS;
+        const double x = c0 + cc < a.chunks ? pv[cc][u] : 0.0;
+        v[u] = e == nsum - 1 ? fmax(v[u], x) : v[u] + x;
+      }
+  }
+#pragma unroll
+  for (int u = 0; u < UPD_EPT; ++u) {
+    const int e = tid + u * UPD_THREADS;
+    if (e < nsum) sums[e < K * ACC ? e : KMAX * ACC + (e - K * ACC)] = v[u];
+  }
+  __syncthreads();
+  if (stopped) return;
+  double term = 0.0;
+  if (tid < K) {
+    const int k = tid;
+    double s[ACC];
+#pragma unroll
+    for (int e = 0; e < ACC; ++e) s[e] = sums[k * ACC + e];
+    double sn[DP];
+#pragma unroll
+    for (int j = 0; j < DP; ++j) sn[j] = (j < d) ? (double)sold[j] : 0.0;
+    double gnew = (double)gold;
+    const double W = s[16];
+    if (MODE == MODE_ITER) {
+      // the stored shapes are unit only to float32 rounding: use ||s||^2
+      double ps = 0.0, s2 = 0.0;
+#pragma unroll
+      for (int j = 0; j < DP; ++j) {
+        ps = fma(s[8 + j], sn[j], ps);
+        s2 = fma(sn[j], sn[j], s2);
+      }
+      term += gnew * (2.0 * ps - gnew * s2 * W);
+    }
+    if (W > 0.0) {
+      if (MODE == MODE_ITER) {
+        double mn = 0.0;
+#pragma unroll
+        for (int j = 0; j < DP; ++j) mn = fma(s[j], s[j], mn);
+        mn = sqrt(mn);
+        if (mn > SHAPE_KEEP_REL * W) {
+#pragma unroll
+          for (int j = 0; j < DP; ++j) sn[j] = s[j] / mn;
+        }
+      }
+      double pr = 0.0;
+#pragma unroll
+      for (int j = 0; j < DP; ++j) pr = fma(s[8 + j], sn[j], pr);
+      gnew = fmax(0.0, pr / W);
+    }
+#pragma unroll
+    for (int j = 0; j < DP; ++j)
+      if (j < d) sk[j] = (float)sn[j];
+    *gk = (float)gnew;
+  }
+  if (MODE == MODE_INIT) {
+    if (tid == 0 && a.want_wxx) a.wxx[g] = sums[KMAX * ACC];
+  } else {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) term += __shfl_xor(term, off);
+    if (lane == 0) wred[wave] = term;
+    __syncthreads();
+    if (tid == 0) {
+      const double ch = sums[KMAX * ACC + 1];
+      if (a.want_wxx) a.wxx[g] = sums[KMAX * ACC];
+      if (a.trace) {
+        double obj = a.wxx[g];
+        for (int w = 0; w < UPD_THREADS / 64; ++w) obj -= wred[w];
+        a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
+      }
+      a.iters[g] = a.t;
+      if (ch == 0.0 && !a.no_early_stop) a.done[g] = a.t;
+    }
+  }
+}
 
 // Fused assignment (eq. 5) + weighted accumulation (eqs. 6-8) for one
 // (chunk of rows, subspace).  MODE_INIT scores with unit gains (largest
@@ -416,8 +557,9 @@ assign_accumulate_kernel(AssignArgs a) {
   __shared__ double acc[KMAX * ACC];
   __shared__ float cbg[KMAX];
   __shared__ float cbs[KMAX * DP];
+  __shared__ u4 tiles_l[NT * 2 * 64];
   __shared__ double objw[TRAIN_WAVES];
-  __shared__ uint16_t codes_l[TRAIN_CHUNK_ROWS];   // this chunk's new assignment
+  __shared__ uint16_t codes_l[TRAIN_CHUNK_MAX];   // this chunk's new assignment
   __shared__ int changed, red;
 
   const int g = blockIdx.y;
@@ -431,15 +573,31 @@ assign_accumulate_kernel(AssignArgs a) {
   if (tid == 0) changed = a.force_changed;
   const int ex = load_codebook(a.gain + (size_t)g * K, a.shape + (size_t)g * K * d, d, K,
                                MODE == MODE_INIT, cbg, cbs, &red);
+  // operand tiles built once per workgroup (one (tile, lane) entry per
+  // thread), then read by every wave into its registers
+  for (int e = tid; e < NT * 64; e += blockDim.x) {
+    const int t = e >> 6, l = e & 63;
+    const int k = t * CW + (l & 31);
+    u4 a1, a2;
+    tile_entry(l >> 5, k < K, MODE == MODE_INIT ? 1.f : cbg[k], cbs + k * DP, ex, a1, a2);
+    tiles_l[(2 * t) * 64 + l] = a1;
+    tiles_l[(2 * t + 1) * 64 + l] = a2;
+  }
+  __syncthreads();
   Tiles tl;
-  build_tiles(tl, cbg, cbs, K, ex, MODE == MODE_INIT, lane);
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    tl.a1[t] = tiles_l[(2 * t) * 64 + lane];
+    tl.a2[t] = tiles_l[(2 * t + 1) * 64 + lane];
+  }
 
   const T* xt = (const T*)a.xt + (size_t)g * a.N * 8;
   uint16_t* asg = a.assign + (size_t)g * a.N;
-  const int64_t row_begin = (int64_t)chunk * TRAIN_CHUNK_ROWS;
-  int64_t row_end = row_begin + TRAIN_CHUNK_ROWS;
+  const int64_t row_begin = (int64_t)chunk * a.chunk_rows;
+  int64_t row_end = row_begin + a.chunk_rows;
   if (row_end > a.N) row_end = a.N;
   const int nblk = (int)((row_end - row_begin + RB - 1) / RB);
+  const bool want_wxx = a.want_wxx != 0;
 
   // loads never branch: past the end they read the chunk's first row and
   // the values are masked where they are used, so prefetches stay in flight
@@ -476,9 +634,9 @@ assign_accumulate_kernel(AssignArgs a) {
     if (rb + TRAIN_WAVES < nblk) fetch(rb + TRAIN_WAVES);
 
     h8 b1, b2;
-    float rr;
+    float rr, ss;
     bool need_exact;
-    make_b<F16ROWS>(x, raw, ex, h, b1, b2, rr, need_exact);
+    make_b<F16ROWS>(x, raw, ex, h, b1, b2, rr, need_exact, ss);
     const int key = min_key(tl, b1, b2);
     float dhat;
     int kstar = reduce_rows(key, h, dhat);
@@ -490,24 +648,19 @@ assign_accumulate_kernel(AssignArgs a) {
       // lane half 0 adds w y (y = x / ||x||) and W, half 1 adds w x and the
       // member count
       double* ak = acc + kstar * ACC;
-      float ss = 0.f;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) ss = fmaf(x[j], x[j], ss);
       const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
       const float sc = h ? wcur : wcur * inv;
+      // float64 products: exact for half 1, whose w x sums also give the
+      // objective
 #pragma unroll
-      for (int j = 0; j < 8; ++j) unsafeAtomicAdd(ak + 8 * h + j, (double)(x[j] * sc));
+      for (int j = 0; j < 8; ++j) unsafeAtomicAdd(ak + 8 * h + j, (double)x[j] * (double)sc);
       unsafeAtomicAdd(ak + 16 + h, h ? 1.0 : (double)wcur);
       if (h == 0) {
-        if (a.want_obj) {
-          const float gk = cbg[kstar];
-          float dist = 0.f;
+        if (want_wxx) {
+          double s2 = 0.0;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) {
-            const float r = fmaf(-gk, cbs[kstar * DP + j], x[j]);
-            dist = fmaf(r, r, dist);
-          }
-          obj += (double)wcur * (double)dist;
+          for (int j = 0; j < 8; ++j) s2 = fma((double)x[j], (double)x[j], s2);
+          obj = fma((double)wcur, s2, obj);
         }
         if (MODE == MODE_ITER && old != (uint16_t)kstar) any_changed = true;
         // global stores would share vmcnt with the prefetch and stall the
@@ -524,86 +677,12 @@ assign_accumulate_kernel(AssignArgs a) {
   __syncthreads();
   for (int64_t r = row_begin + tid; r < row_end; r += blockDim.x) asg[r] = codes_l[r - row_begin];
   double* out = a.part + ((size_t)g * a.chunks + chunk) * PSTRIDE;
-  for (int e = tid; e < KMAX * ACC; e += blockDim.x) out[e] = acc[e];
+  for (int e = tid; e < K * ACC; e += blockDim.x) out[e] = acc[e];
   if (tid == 0) {
     double s = 0.0;
     for (int w = 0; w < TRAIN_WAVES; ++w) s += objw[w];
     out[KMAX * ACC] = s;
     out[KMAX * ACC + 1] = (double)changed;
-  }
-}
-
-struct FinalizeArgs {
-  int d, K, G, chunks, T;
-  int t;                  // iteration number (1-based); 0 for init
-  int no_early_stop;
-  const double* part;
-  const float* seednorm;  // [G][K]
-  float* gain;            // [G][K]
-  float* shape;           // [G][K][d]
-  int* done;              // [G]
-  int* iters;             // [G]
-  double* trace;          // [G][T] or null
-};
-
-// Codebook update from the partial sums of every chunk (fixed order), one
-// thread per codeword: init: eq. (8) gains for the seed shapes; iteration:
-// eqs. (7) and (8).  Thread 0 of each subspace also applies the stop test.
-template <int MODE>
-__global__ void __launch_bounds__(64) finalize_kernel(FinalizeArgs a) {
-  const int g = blockIdx.y;
-  // done[g] holds the iteration at which subspace g stopped; blocks of that
-  // same iteration still apply its update
-  if (MODE == MODE_ITER && a.done[g] != 0 && a.done[g] < a.t) return;
-  const int k = blockIdx.x * 64 + threadIdx.x;
-  const int d = a.d, K = a.K;
-  if (k < K) {
-    double s[ACC];
-#pragma unroll
-    for (int e = 0; e < ACC; ++e) s[e] = 0.0;
-    for (int c = 0; c < a.chunks; ++c) {
-      const double* p = a.part + ((size_t)g * a.chunks + c) * PSTRIDE + (size_t)k * ACC;
-#pragma unroll
-      for (int e = 0; e < ACC; ++e) s[e] += p[e];
-    }
-    float* sk = a.shape + ((size_t)g * K + k) * d;
-    float* gk = a.gain + (size_t)g * K + k;
-    double sn[DP];
-#pragma unroll
-    for (int j = 0; j < DP; ++j) sn[j] = (j < d) ? (double)sk[j] : 0.0;
-    double gnew = (MODE == MODE_INIT) ? (double)a.seednorm[(size_t)g * K + k] : (double)*gk;
-    const double W = s[16];
-    if (W > 0.0) {
-      if (MODE == MODE_ITER) {
-        double mn = 0.0;
-#pragma unroll
-        for (int j = 0; j < DP; ++j) mn = fma(s[j], s[j], mn);
-        mn = sqrt(mn);
-        if (mn > SHAPE_KEEP_REL * W) {
-#pragma unroll
-          for (int j = 0; j < DP; ++j) sn[j] = s[j] / mn;
-        }
-      }
-      double pr = 0.0;
-#pragma unroll
-      for (int j = 0; j < DP; ++j) pr = fma(s[8 + j], sn[j], pr);
-      gnew = fmax(0.0, pr / W);
-    }
-#pragma unroll
-    for (int j = 0; j < DP; ++j)
-      if (j < d) sk[j] = (float)sn[j];
-    *gk = (float)gnew;
-  }
-  if (MODE == MODE_ITER && blockIdx.x == 0 && threadIdx.x == 0) {
-    double obj = 0.0, ch = 0.0;
-    for (int c = 0; c < a.chunks; ++c) {
-      const double* p = a.part + ((size_t)g * a.chunks + c) * PSTRIDE + KMAX * ACC;
-      obj += p[0];
-      ch = fmax(ch, p[1]);
-    }
-    if (a.trace) a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
-    a.iters[g] = a.t;
-    if (ch == 0.0 && !a.no_early_stop) a.done[g] = a.t;
   }
 }
 
@@ -734,13 +813,13 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
         ex = a.sig[cb];
       }
       h8 b1, b2;
-      float rr;
+      float rr, ss;
       bool need_exact;
       // after the first stage the residual is no longer float16-exact
       if (F16IN && m == 0)
-        make_b<true>(x, raw, ex, h, b1, b2, rr, need_exact);
+        make_b<true>(x, raw, ex, h, b1, b2, rr, need_exact, ss);
       else
-        make_b<false>(x, raw, ex, h, b1, b2, rr, need_exact);
+        make_b<false>(x, raw, ex, h, b1, b2, rr, need_exact, ss);
       const int key = min_key(tl, b1, b2);
       float dhat;
       int kstar = reduce_rows(key, h, dhat);
@@ -1013,20 +1092,31 @@ gsrq_status check_supported(const gsrq_shape* s) {
 }
 
 struct TrainLayout {
-  size_t xt, part, assign, done, iters, seednorm, seeds, total;
-  int chunks;
+  size_t xt, part, assign, done, iters, wxx, seednorm, seeds, total;
+  int chunks, chunk_rows;
 };
 
 TrainLayout train_layout(const gsrq_shape* s, size_t elt) {
   TrainLayout L;
   const int64_t G = s->D / s->d;
-  L.chunks = (int)((s->N + TRAIN_CHUNK_ROWS - 1) / TRAIN_CHUNK_ROWS);
+  // about one workgroup per CU in all: chunks per subspace from the CU
+  // count, within the per-workgroup row limits
+  int64_t chunks = (TRAIN_SLOTS + G - 1) / G;
+  const int64_t lo = (s->N + TRAIN_CHUNK_MAX - 1) / TRAIN_CHUNK_MAX;
+  const int64_t hi = (s->N + TRAIN_CHUNK_MIN - 1) / TRAIN_CHUNK_MIN;
+  chunks = chunks < hi ? chunks : hi;
+  chunks = chunks > lo ? chunks : lo;
+  int64_t rows = (s->N + chunks - 1) / chunks;
+  rows = (rows + RB - 1) / RB * RB;
+  L.chunk_rows = (int)rows;
+  L.chunks = (int)((s->N + rows - 1) / rows);
   size_t off = 0;
   L.xt = off; off = align256(off + (size_t)G * s->N * 8 * elt);
   L.part = off; off = align256(off + (size_t)G * L.chunks * PSTRIDE * sizeof(double));
   L.assign = off; off = align256(off + (size_t)G * s->N * sizeof(uint16_t));
   L.done = off; off = align256(off + (size_t)G * sizeof(int));
   L.iters = off; off = align256(off + (size_t)G * sizeof(int));
+  L.wxx = off; off = align256(off + (size_t)G * sizeof(double));
   L.seednorm = off; off = align256(off + (size_t)G * s->K * sizeof(float));
   L.seeds = off; off = align256(off + (size_t)G * s->K * sizeof(int32_t));
   L.total = off;
@@ -1116,15 +1206,13 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
   AssignArgs aa;
   aa.xt = xt; aa.N = s->N; aa.d = d; aa.K = K; aa.G = G; aa.w = w;
   aa.gain = gain; aa.shape = shape; aa.assign = assign;
-  aa.done = done; aa.part = part; aa.chunks = L.chunks; aa.force_changed = 0;
-  aa.want_obj = trace != nullptr;
-  FinalizeArgs fa;
-  fa.d = d; fa.K = K; fa.G = G; fa.chunks = L.chunks; fa.T = T_; fa.t = 0;
-  fa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
-  fa.part = part; fa.seednorm = seednorm; fa.gain = gain; fa.shape = shape;
-  fa.done = done; fa.iters = iters; fa.trace = trace;
+  aa.done = done; aa.iters = iters; aa.part = part;
+  aa.seednorm = seednorm; aa.trace = trace;
+  aa.wxx = (double*)(base + L.wxx);
+  aa.want_wxx = trace != nullptr;   // the first pass computes it
+  aa.chunks = L.chunks; aa.chunk_rows = L.chunk_rows; aa.force_changed = 0; aa.t = 0; aa.T = T_;
+  aa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
   const dim3 agrid((unsigned)L.chunks, (unsigned)G);
-  const dim3 fgrid((unsigned)((K + 63) / 64), (unsigned)G);
 
   if (!resume) {
     if (hipMemcpyAsync(dseeds, seeds, (size_t)G * K * sizeof(int32_t), hipMemcpyHostToDevice,
@@ -1139,25 +1227,27 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
     if ((e = launch_ok())) return e;
     {
       TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
-      finalize_kernel<MODE_INIT><<<fgrid, 64, 0, st>>>(fa);
+      update_kernel<MODE_INIT><<<G, UPD_THREADS, 0, st>>>(aa);
     }
     if ((e = launch_ok())) return e;
+    aa.want_wxx = 0;
   } else {
     aa.force_changed = (flags & GSRQ_ASSIGN_IN) ? 0 : 1;
   }
   for (int t = 1; t <= T_; ++t) {
+    aa.t = t;
     {
       TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
       assign_accumulate_kernel<T, MODE_ITER><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
     }
     if ((e = launch_ok())) return e;
-    aa.force_changed = 0;
-    fa.t = t;
     {
       TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
-      finalize_kernel<MODE_ITER><<<fgrid, 64, 0, st>>>(fa);
+      update_kernel<MODE_ITER><<<G, UPD_THREADS, 0, st>>>(aa);
     }
     if ((e = launch_ok())) return e;
+    aa.force_changed = 0;
+    aa.want_wxx = 0;
   }
   if (R_next) {
     gsrq_shape s1 = *s;
