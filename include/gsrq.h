@@ -197,6 +197,12 @@ enum {
  * run and read from one host thread. */
 gsrq_status gsrq_timing_enable(int on);
 
+/* As gsrq_timing_enable, restricted to the kernel kinds whose bit
+ * (1u << kind) is set in kinds; 0 switches timing off.  Each recorded launch
+ * costs two event records on its stream, so timing only the kinds of
+ * interest keeps the measured work close to the unmeasured one. */
+gsrq_status gsrq_timing_enable_kinds(uint32_t kinds);
+
 /* Wait for the recorded launches and return, per kernel kind k < n_kinds,
  * the summed event-to-event time in milliseconds and the launch count; then
  * clear the records. */

@@ -591,45 +591,42 @@ assign_accumulate_kernel(AssignArgs a) {
     tl.a2[t] = tiles_l[(2 * t + 1) * 64 + lane];
   }
 
-  const T* xt = (const T*)a.xt + (size_t)g * a.N * 8;
-  uint16_t* asg = a.assign + (size_t)g * a.N;
+  // this chunk's rows, weights and codes, indexed from 0 in 32 bits
   const int64_t row_begin = (int64_t)chunk * a.chunk_rows;
-  int64_t row_end = row_begin + a.chunk_rows;
-  if (row_end > a.N) row_end = a.N;
-  const int nblk = (int)((row_end - row_begin + RB - 1) / RB);
+  const int nrows = (int)(a.N - row_begin < a.chunk_rows ? a.N - row_begin : a.chunk_rows);
+  const T* xc = (const T*)a.xt + ((size_t)g * a.N + row_begin) * 8;
+  uint16_t* ac = a.assign + (size_t)g * a.N + row_begin;
+  const int nblk = (nrows + RB - 1) / RB;
   const bool want_wxx = a.want_wxx != 0;
 
-  // loads never branch: past the end they read the chunk's first row and
-  // the values are masked where they are used, so prefetches stay in flight
-  const float one = 1.f;
-  const float* wp = a.w ? a.w : &one;
-  const int64_t wstride = a.w ? 1 : 0;
+  // loads never branch: past the end they read the chunk's first row, whose
+  // results are discarded, so prefetches stay in flight (without weights
+  // the load reads a gain in place of a weight and the value is replaced by
+  // 1: a global pointer keeps it a global load)
+  const bool has_w = a.w != nullptr;
+  const float* wc = has_w ? a.w + row_begin : a.gain;
+  const int wstride = has_w ? 1 : 0;
   RowVec<T> nx;
   float nw = 0.f;
   uint16_t nold = 0;
   auto fetch = [&](int rb) {
-    int64_t row = row_begin + (int64_t)rb * RB + i;
-    row = row < row_end ? row : row_begin;
-    nx.load(xt + row * 8);
-    nw = wp[row * wstride];
-    if (MODE == MODE_ITER) nold = asg[row];
+    int r = rb * RB + i;
+    r = r < nrows ? r : 0;
+    nx.load(xc + r * 8);
+    nw = wc[r * wstride];
+    if (MODE == MODE_ITER) nold = ac[r];
   };
   if (wave < nblk) fetch(wave);
 
   double obj = 0.0;
   bool any_changed = false;
   for (int rb = wave; rb < nblk; rb += TRAIN_WAVES) {
-    const int64_t row = row_begin + (int64_t)rb * RB + i;
-    const bool valid = row < row_end;
+    const int r = rb * RB + i;
+    const bool valid = r < nrows;
     float x[8];
     nx.get(x);
-    u4 raw = nx.raw16();
-    if (!valid) {
-#pragma unroll
-      for (int j = 0; j < 8; ++j) x[j] = 0.f;
-      raw = (u4){0u, 0u, 0u, 0u};
-    }
-    const float wcur = nw;
+    const u4 raw = nx.raw16();
+    const float wcur = has_w ? nw : 1.f;
     const uint16_t old = nold;
     if (rb + TRAIN_WAVES < nblk) fetch(rb + TRAIN_WAVES);
 
@@ -643,7 +640,7 @@ assign_accumulate_kernel(AssignArgs a) {
     need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
     const unsigned long long fb = __ballot(valid && need_exact && h == 0);
     if (fb) exact_rows(fb, x, d, DP, K, cbg, cbs, MODE == MODE_INIT, kstar);
-    if (kstar >= K) kstar = K - 1;   // only tail rows past N can get here
+    if (kstar >= K) kstar = K - 1;   // only discarded rows can get here
     if (valid) {
       // lane half 0 adds w y (y = x / ||x||) and W, half 1 adds w x and the
       // member count
@@ -665,7 +662,7 @@ assign_accumulate_kernel(AssignArgs a) {
         if (MODE == MODE_ITER && old != (uint16_t)kstar) any_changed = true;
         // global stores would share vmcnt with the prefetch and stall the
         // next block, so codes go to LDS and leave in one pass at the end
-        codes_l[row - row_begin] = (uint16_t)kstar;
+        codes_l[r] = (uint16_t)kstar;
       }
     }
   }
@@ -675,7 +672,7 @@ assign_accumulate_kernel(AssignArgs a) {
   if (lane == 0) objw[wave] = obj;
   if (__ballot(any_changed) && lane == 0) atomicOr(&changed, 1);
   __syncthreads();
-  for (int64_t r = row_begin + tid; r < row_end; r += blockDim.x) asg[r] = codes_l[r - row_begin];
+  for (int r = tid; r < nrows; r += blockDim.x) ac[r] = codes_l[r];
   double* out = a.part + ((size_t)g * a.chunks + chunk) * PSTRIDE;
   for (int e = tid; e < K * ACC; e += blockDim.x) out[e] = acc[e];
   if (tid == 0) {
@@ -1427,10 +1424,15 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_us
   return launch_ok();
 }
 
-gsrq_status gsrq_timing_enable(int on) {
-  g_gsrq_timing.on = on != 0;
+gsrq_status gsrq_timing_enable_kinds(uint32_t kinds) {
+  g_gsrq_timing.on = kinds != 0;
+  g_gsrq_timing.kinds = kinds;
   g_gsrq_timing.n = 0;
   return GSRQ_OK;
+}
+
+gsrq_status gsrq_timing_enable(int on) {
+  return gsrq_timing_enable_kinds(on ? ~0u : 0u);
 }
 
 gsrq_status gsrq_timing_read(double* total_ms, int64_t* launches, int n_kinds) {

@@ -17,6 +17,7 @@
 // own streams (gsrq_timing_enable / gsrq_timing_read).
 struct GsrqTimingState {
   bool on = false;
+  uint32_t kinds = 0;     // bit k: launches of kind k are recorded
   struct Rec { hipEvent_t a, b; int kind; };
   Rec* recs = nullptr;
   int n = 0, cap = 0;
@@ -138,14 +139,16 @@ struct TimedLaunch {
   hipStream_t st;
   TimedLaunch(int kind, hipStream_t s) : st(s) {
     GsrqTimingState& T = g_gsrq_timing;
-    if (!T.on) return;
+    if (!T.on || !((T.kinds >> kind) & 1u)) return;
     if (T.n == T.cap) {
       const int nc = T.cap ? 2 * T.cap : 1024;
       auto* nr = new GsrqTimingState::Rec[nc];
       for (int i = 0; i < T.n; ++i) nr[i] = T.recs[i];
+      // timing-only events: no system-scope cache writeback per record
+      // (results are read after a full device synchronisation)
       for (int i = T.n; i < nc; ++i) {
-        hipEventCreate(&nr[i].a);
-        hipEventCreate(&nr[i].b);
+        hipEventCreateWithFlags(&nr[i].a, hipEventDisableSystemFence);
+        hipEventCreateWithFlags(&nr[i].b, hipEventDisableSystemFence);
       }
       delete[] T.recs;
       T.recs = nr;

@@ -68,6 +68,8 @@ def load_library(path: str = LIB_PATH):
                                 ctypes.c_int64, _vp]
     lib.gsrq_timing_enable.restype = ctypes.c_int
     lib.gsrq_timing_enable.argtypes = [ctypes.c_int]
+    lib.gsrq_timing_enable_kinds.restype = ctypes.c_int
+    lib.gsrq_timing_enable_kinds.argtypes = [ctypes.c_uint32]
     lib.gsrq_timing_read.restype = ctypes.c_int
     lib.gsrq_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(ctypes.c_int64), ctypes.c_int]
@@ -79,9 +81,17 @@ KERNEL_KINDS = ("assign", "finalize", "encode", "decode", "transpose", "accumula
                 "fragments", "exact")
 
 
-def timing_enable(on: bool = True):
-    """Bracket every kernel launch with HIP events on its stream (measurement)."""
-    _check(load_library().gsrq_timing_enable(1 if on else 0), "gsrq_timing_enable")
+def timing_enable(on: bool = True, kinds=None):
+    """Bracket kernel launches with HIP events on their stream (measurement):
+    every kind, or only the named ones (names from KERNEL_KINDS)."""
+    if kinds is None:
+        _check(load_library().gsrq_timing_enable(1 if on else 0), "gsrq_timing_enable")
+        return
+    mask = 0
+    for k in kinds:
+        mask |= 1 << KERNEL_KINDS.index(k)
+    _check(load_library().gsrq_timing_enable_kinds(ctypes.c_uint32(mask if on else 0)),
+           "gsrq_timing_enable_kinds")
 
 
 def timing_read():
