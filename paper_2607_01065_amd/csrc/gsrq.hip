@@ -36,6 +36,9 @@ constexpr int NT = 8;            // tiles: K <= 256
 constexpr int KMAX = NT * CW;
 constexpr int ACC = 18;          // sum w y[8], sum w x[8], W, count
 constexpr int PSTRIDE = KMAX * ACC + 2;  // + objective, changed flag
+// LDS stride of a codeword's sums: odd in 8-byte units, so the rows of a wave
+// (random codewords) spread over all bank pairs instead of one in eight
+constexpr int ACC_LDS = ACC + 1;
 constexpr int TRAIN_WAVES = 12;        // one 768-thread workgroup per CU
 constexpr int WAVES_PER_SIMD = 3;      // 168 VGPRs: operand tiles stay in registers
 constexpr int TRAIN_CHUNK_MAX = 16384;  // rows of one (chunk, subspace) workgroup, at most
@@ -554,7 +557,7 @@ template <typename T, int MODE>
 __global__ void __launch_bounds__(TRAIN_WAVES * 64, WAVES_PER_SIMD)
 assign_accumulate_kernel(AssignArgs a) {
   constexpr bool F16ROWS = sizeof(T) == 2;
-  __shared__ double acc[KMAX * ACC];
+  __shared__ double acc[KMAX * ACC_LDS];
   __shared__ float cbg[KMAX];
   __shared__ float cbs[KMAX * DP];
   __shared__ u4 tiles_l[NT * 2 * 64];
@@ -569,7 +572,7 @@ assign_accumulate_kernel(AssignArgs a) {
   const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K;
 
-  for (int e = tid; e < KMAX * ACC; e += blockDim.x) acc[e] = 0.0;
+  for (int e = tid; e < KMAX * ACC_LDS; e += blockDim.x) acc[e] = 0.0;
   if (tid == 0) changed = a.force_changed;
   const int ex = load_codebook(a.gain + (size_t)g * K, a.shape + (size_t)g * K * d, d, K,
                                MODE == MODE_INIT, cbg, cbs, &red);
@@ -644,7 +647,7 @@ assign_accumulate_kernel(AssignArgs a) {
     if (valid) {
       // lane half 0 adds w y (y = x / ||x||) and W, half 1 adds w x and the
       // member count
-      double* ak = acc + kstar * ACC;
+      double* ak = acc + kstar * ACC_LDS;
       const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
       const float sc = h ? wcur : wcur * inv;
       // float64 products: exact for half 1, whose w x sums also give the
@@ -674,7 +677,7 @@ assign_accumulate_kernel(AssignArgs a) {
   __syncthreads();
   for (int r = tid; r < nrows; r += blockDim.x) ac[r] = codes_l[r];
   double* out = a.part + ((size_t)g * a.chunks + chunk) * PSTRIDE;
-  for (int e = tid; e < K * ACC; e += blockDim.x) out[e] = acc[e];
+  for (int e = tid; e < K * ACC; e += blockDim.x) out[e] = acc[(e / ACC) * ACC_LDS + e % ACC];
   if (tid == 0) {
     double s = 0.0;
     for (int w = 0; w < TRAIN_WAVES; ++w) s += objw[w];
