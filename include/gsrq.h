@@ -73,7 +73,19 @@ enum {
    * Without this flag a resumed first iteration always counts as changed. */
   GSRQ_ASSIGN_IN = 2u,
   /* Run all T iterations even when an assignment repeats. */
-  GSRQ_NO_EARLY_STOP = 4u
+  GSRQ_NO_EARLY_STOP = 4u,
+  /* Standard weighted K-means, the baseline GSKM replaces (Sec. 4, Sec. 6.1),
+   * with the same kernels: centroid k is held as gain = ||c_k|| and
+   * shape = c_k / ||c_k|| (shape 0 for a zero centroid), so scoring by eq. (5)
+   * is the squared distance to c_k.  Seeding (without GSRQ_RESUME): c_k = the
+   * seed row itself (a zero row is allowed); there is no initial assignment
+   * (assign_io is not written), T = 0 only writes the seed centroids, and
+   * the first iteration counts as changed.  Iteration t: assign to the
+   * nearest centroid (ties to the lowest index), then c_k = weighted mean of
+   * its members for clusters with weight (others keep c_k); obj_trace entry
+   * t-1 is the weighted distortion AFTER that update.  GSRQ_RESUME,
+   * GSRQ_ASSIGN_IN and the stop rule act as for GSKM. */
+  GSRQ_KMEANS = 8u
 };
 
 /* Human-readable name of a status code (static string). */
@@ -111,7 +123,8 @@ gsrq_status gsrq_encode_workspace_bytes(const gsrq_shape* s, size_t* bytes);
  *                    is seeded with the direction of row seed_rows[g][k],
  *                    which must be a nonzero subvector.  Indices must lie in
  *                    [0, N) and be distinct within a subspace; N >= K.
- *  flags             GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP.
+ *  flags             GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP |
+ *                    GSRQ_KMEANS (the K-means baseline, see the flag).
  *  gain, shape       [G][K], [G][K][d] float32 outputs (inputs on resume).
  *  R_next            [N][D] float32 residual X - c(encode(X)) with the final
  *                    codebook, or NULL.
@@ -120,7 +133,8 @@ gsrq_status gsrq_encode_workspace_bytes(const gsrq_shape* s, size_t* bytes);
  *  iters_run         [G] int32 iterations run per subspace, or NULL.
  *  obj_trace         [G][T] float64: entry t-1 is sum_i w_i ||x_i - c_{k_i}||^2
  *                    of iteration t's assignment against the codebook it was
- *                    made with; entries past iters_run are 0.  Or NULL.
+ *                    made with (GSRQ_KMEANS: against the updated centroids);
+ *                    entries past iters_run are 0.  Or NULL.
  *  workspace         >= gsrq_train_workspace_bytes(s), 256-byte aligned.
  *
  * Initialisation (without GSRQ_RESUME): shapes are the normalised seed rows;

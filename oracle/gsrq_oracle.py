@@ -367,28 +367,52 @@ def log_weight(norms, tau=1.0, eps=1e-8):
 # Standard l2 K-means, the baseline GSKM replaces (Sec. 4, Sec. 6.1)
 # ----------------------------------------------------------------------------
 
-def kmeans(X, w, K, T, init_rows):
+def kmeans_assign(X, C):
+    """Nearest centroid by squared l2 distance, lowest index on ties."""
+    X = np.asarray(X, np.float64)
+    C = np.asarray(C, np.float64)
+    d2 = np.sum((X[:, None, :] - C[None, :, :]) ** 2, axis=2)
+    return np.argmin(d2, axis=1).astype(np.int64)
+
+
+def kmeans_update(X, w, assign, C):
+    """Centroid of every cluster with weight = weighted mean of its members;
+    clusters without weight keep their centroid.  Returns the new [K, d]."""
+    X = np.asarray(X, np.float64)
+    w = np.asarray(w, np.float64)
+    C = np.array(C, dtype=np.float64, copy=True)
+    for k in range(C.shape[0]):
+        members = np.nonzero(assign == k)[0]
+        Wk = np.sum(w[members]) if members.size else 0.0
+        if Wk > 0.0:
+            C[k] = np.sum(w[members, None] * X[members], axis=0) / Wk
+    return C
+
+
+def kmeans(X, w, K, T, init_rows, *, centroids=None, prev_assign=None):
     """Weighted Lloyd K-means from seed rows: assign to the nearest centroid
     (lowest index on ties), centroid = weighted mean of its members, empty
     clusters keep their centroid, stop when the assignment repeats.
+    Passing centroids resumes from them (prev_assign, if given, is what the
+    stop test compares against at t = 1).
     Returns dict(centroids [K, d], iters_run, assign, trace) where trace[t-1]
     is the weighted distortion after the iteration-t update."""
     X = np.asarray(X, np.float64)
     N = X.shape[0]
     w = np.ones(N) if w is None else np.asarray(w, np.float64)
-    C = X[np.asarray(init_rows, np.int64)].copy()
-    prev = None
+    if centroids is None:
+        C = X[np.asarray(init_rows, np.int64)].copy()
+        prev = None
+    else:
+        C = np.array(centroids, dtype=np.float64, copy=True)
+        prev = None if prev_assign is None else np.asarray(prev_assign, np.int64)
+    assert C.shape[0] == K
     trace = []
     iters_run = 0
     assign = None
     for t in range(1, T + 1):
-        d2 = np.sum((X[:, None, :] - C[None, :, :]) ** 2, axis=2)
-        assign = np.argmin(d2, axis=1)
-        for k in range(K):
-            members = np.nonzero(assign == k)[0]
-            Wk = np.sum(w[members]) if members.size else 0.0
-            if Wk > 0.0:
-                C[k] = np.sum(w[members, None] * X[members], axis=0) / Wk
+        assign = kmeans_assign(X, C)
+        C = kmeans_update(X, w, assign, C)
         R = X - C[assign]
         trace.append(float(np.sum(w * np.sum(R * R, axis=1))))
         iters_run = t

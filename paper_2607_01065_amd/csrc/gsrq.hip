@@ -355,10 +355,12 @@ __global__ void transpose_kernel(const T* __restrict__ X, int64_t ldx, int64_t N
 }
 
 // Seed shapes: s_k = x_r / (||x_r|| + eps) for r = seed row of codeword k.
+// K-means seeding (kmeans != 0): the centroid is the seed row itself, held
+// as gain ||x_r|| and shape x_r / ||x_r|| (0 for a zero row).
 template <typename T>
 __global__ void seed_kernel(const T* __restrict__ Xt, int64_t N, int d, int K,
                             const int32_t* __restrict__ seeds, float* __restrict__ shape,
-                            float* __restrict__ seednorm) {
+                            float* __restrict__ seednorm, int kmeans, float* __restrict__ gain) {
   const int g = blockIdx.x;
   for (int k = threadIdx.x; k < K; k += blockDim.x) {
     const int64_t row = seeds[(size_t)g * K + k];
@@ -366,9 +368,11 @@ __global__ void seed_kernel(const T* __restrict__ Xt, int64_t N, int d, int K,
     double ss = 0.0;
     for (int j = 0; j < d; ++j) { const double v = to_f(x[j]); ss = fma(v, v, ss); }
     const double nrm = sqrt(ss);
+    const double den = kmeans ? (nrm > 0.0 ? nrm : 1.0) : nrm + (double)Y_EPS;
     for (int j = 0; j < d; ++j)
-      shape[((size_t)g * K + k) * d + j] = (float)((double)to_f(x[j]) / (nrm + (double)Y_EPS));
+      shape[((size_t)g * K + k) * d + j] = (float)((double)to_f(x[j]) / den);
     seednorm[(size_t)g * K + k] = (float)nrm;
+    if (kmeans) gain[(size_t)g * K + k] = (float)nrm;
   }
 }
 
@@ -414,6 +418,7 @@ struct AssignArgs {
   int t;                 // iteration number (1-based); 0 for the initialisation
   int T;
   int no_early_stop;
+  int kmeans;            // K-means baseline update instead of eqs. (7)(8)
 };
 
 // Codebook update of subspace g from the partial sums of all its chunks,
@@ -427,7 +432,9 @@ struct AssignArgs {
 // S_k = sum of w x over the members of k, W_k = their weight (products and
 // sums in float64, so the cancellation costs no accuracy); and the stop
 // test (no assignment changed).  One workgroup per subspace; thread k
-// updates codeword k.
+// updates codeword k.  K-means baseline: the centroid becomes S_k / W_k
+// (held as its norm and direction) and the objective is the distortion
+// after the update, sum_i w_i ||x_i||^2 - sum_k ||S_k||^2 / W_k.
 constexpr int UPD_THREADS = 1024;
 constexpr int UPD_EPT = (KMAX * ACC + 2 + UPD_THREADS - 1) / UPD_THREADS;  // sums per thread
 constexpr int UPD_CBATCH = 4;                                             // chunks per load batch
@@ -496,7 +503,22 @@ __global__ void __launch_bounds__(UPD_THREADS) update_kernel(AssignArgs a) {
     for (int j = 0; j < DP; ++j) sn[j] = (j < d) ? (double)sold[j] : 0.0;
     double gnew = (double)gold;
     const double W = s[16];
-    if (MODE == MODE_ITER) {
+    if (MODE == MODE_ITER && a.kmeans) {
+      if (W > 0.0) {
+        double c[DP], cn = 0.0, s2 = 0.0;
+#pragma unroll
+        for (int j = 0; j < DP; ++j) {
+          c[j] = s[8 + j] / W;
+          cn = fma(c[j], c[j], cn);
+          s2 = fma(s[8 + j], s[8 + j], s2);
+        }
+        term += s2 / W;
+        cn = sqrt(cn);
+#pragma unroll
+        for (int j = 0; j < DP; ++j) sn[j] = cn > 0.0 ? c[j] / cn : 0.0;
+        gnew = cn;
+      }
+    } else if (MODE == MODE_ITER) {
       // the stored shapes are unit only to float32 rounding: use ||s||^2
       double ps = 0.0, s2 = 0.0;
 #pragma unroll
@@ -506,7 +528,7 @@ __global__ void __launch_bounds__(UPD_THREADS) update_kernel(AssignArgs a) {
       }
       term += gnew * (2.0 * ps - gnew * s2 * W);
     }
-    if (W > 0.0) {
+    if (W > 0.0 && !(MODE == MODE_ITER && a.kmeans)) {
       if (MODE == MODE_ITER) {
         double mn = 0.0;
 #pragma unroll
@@ -1212,14 +1234,20 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
   aa.want_wxx = trace != nullptr;   // the first pass computes it
   aa.chunks = L.chunks; aa.chunk_rows = L.chunk_rows; aa.force_changed = 0; aa.t = 0; aa.T = T_;
   aa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
+  aa.kmeans = (flags & GSRQ_KMEANS) ? 1 : 0;
   const dim3 agrid((unsigned)L.chunks, (unsigned)G);
 
   if (!resume) {
     if (hipMemcpyAsync(dseeds, seeds, (size_t)G * K * sizeof(int32_t), hipMemcpyHostToDevice,
                        st) != hipSuccess)
       return GSRQ_E_HIP;
-    seed_kernel<T><<<G, 256, 0, st>>>(xt, s->N, d, K, dseeds, shape, seednorm);
+    seed_kernel<T><<<G, 256, 0, st>>>(xt, s->N, d, K, dseeds, shape, seednorm, aa.kmeans, gain);
     if ((e = launch_ok())) return e;
+  }
+  if (!resume && aa.kmeans) {
+    // K-means starts from the seed centroids; there is no previous assignment
+    aa.force_changed = 1;
+  } else if (!resume) {
     {
       TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
       assign_accumulate_kernel<T, MODE_INIT><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
@@ -1316,7 +1344,8 @@ gsrq_status gsrq_train_stage(const gsrq_shape* s, const void* X, gsrq_dtype x_dt
   if (x_dtype != GSRQ_F32 && x_dtype != GSRQ_F16) return GSRQ_E_ARG;
   if (ldx < s->D || T < 0 || s->N < s->K) return GSRQ_E_ARG;
   if (T == 0 && (flags & GSRQ_RESUME)) return GSRQ_E_ARG;
-  if (flags & ~(uint32_t)(GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP)) return GSRQ_E_ARG;
+  if (flags & ~(uint32_t)(GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP | GSRQ_KMEANS))
+    return GSRQ_E_ARG;
   if ((flags & GSRQ_ASSIGN_IN) && (!(flags & GSRQ_RESUME) || !assign_io)) return GSRQ_E_ARG;
   if (((uintptr_t)workspace & 255) != 0) return GSRQ_E_ARG;
   if ((e = check_supported(s))) return e;

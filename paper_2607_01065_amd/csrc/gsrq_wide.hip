@@ -142,10 +142,13 @@ __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ ga
 }
 
 // Seed shapes s_k = x_r / (||x_r|| + eps) from rows of the row-major input.
+// K-means seeding (kmeans != 0): the centroid is the seed row itself, held
+// as gain ||x_r|| and shape x_r / ||x_r|| (0 for a zero row).
 template <typename T>
 __global__ void w_seed_kernel(const T* __restrict__ X, int64_t ldx, int d, int K,
                               const int32_t* __restrict__ seeds, float* __restrict__ shape,
-                              float* __restrict__ seednorm) {
+                              float* __restrict__ seednorm, int kmeans,
+                              float* __restrict__ gain) {
   const int g = blockIdx.y;
   const int k = blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= K) return;
@@ -154,9 +157,11 @@ __global__ void w_seed_kernel(const T* __restrict__ X, int64_t ldx, int d, int K
   double ss = 0.0;
   for (int j = 0; j < d; ++j) { const double v = to_f(x[j]); ss = fma(v, v, ss); }
   const double nrm = sqrt(ss);
+  const double den = kmeans ? (nrm > 0.0 ? nrm : 1.0) : nrm + (double)Y_EPS;
   float* sk = shape + ((size_t)g * K + k) * d;
-  for (int j = 0; j < d; ++j) sk[j] = (float)((double)to_f(x[j]) / (nrm + (double)Y_EPS));
+  for (int j = 0; j < d; ++j) sk[j] = (float)((double)to_f(x[j]) / den);
   seednorm[(size_t)g * K + k] = (float)nrm;
+  if (kmeans) gain[(size_t)g * K + k] = (float)nrm;
 }
 
 struct WScoreArgs {
@@ -945,14 +950,21 @@ struct WFinArgs {
   double* trace;          // [G][T] or null
   const int* xchanged;    // [G] changed flag of the exact kernel's rows
   const double* xobj;     // [G] their objective
+  int kmeans;             // K-means baseline update instead of eqs. (7)(8)
 };
 
 // Codebook update from the chunk partials (fixed order): d/2 lanes per
 // codeword, two elements per lane.  Initial pass (t = 0): eq. (8) gains for
 // the seed shapes (a codeword without members keeps its seed row's norm).
 // Iteration: eqs. (7) and (8) with the safeguards; thread 0 of block 0
-// applies the stop test of its subspace.
+// applies the stop test of its subspace.  The trace entry (zeroed by the
+// host) receives the objective by atomic adds.  K-means baseline: centroid
+// = (sum w x) / W, held as norm and direction, and the trace is the
+// distortion after the update, J_before - sum_k W_k ||m_k - c_k||^2 (the
+// weighted mean m_k replacing the old centroid c_k), each block adding its
+// codewords' share.
 __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
+  __shared__ double red[4];
   const int g = blockIdx.y;
   if (a.t > 0 && a.done[g] != 0 && a.done[g] < a.t) return;
   const int d = a.d, K = a.K, S = 2 * d + 2;
@@ -973,7 +985,28 @@ __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
   float* gk = a.gain + (size_t)g * K + kk;
   double s0 = sk[2 * li], s1 = sk[2 * li + 1];
   double gnew = (a.t == 0) ? (double)a.seednorm[(size_t)g * K + kk] : (double)*gk;
-  if (W > 0.0) {
+  if (a.t > 0 && a.kmeans) {
+    double drop = 0.0;
+    if (W > 0.0) {
+      const double c0 = sx0 / W, c1 = sx1 / W;
+      const double e0 = c0 - gnew * s0, e1 = c1 - gnew * s1;
+      drop = W * fma(e0, e0, e1 * e1);
+      double cn = fma(c0, c0, c1 * c1);
+      for (int off = L / 2; off > 0; off >>= 1) cn += __shfl_xor(cn, off);
+      cn = sqrt(cn);
+      s0 = cn > 0.0 ? c0 / cn : 0.0;
+      s1 = cn > 0.0 ? c1 / cn : 0.0;
+      gnew = cn;
+    }
+    if (!active) drop = 0.0;
+    if (a.trace) {
+      for (int off = 32; off > 0; off >>= 1) drop += __shfl_xor(drop, off);
+      if ((tid & 63) == 0) red[tid >> 6] = drop;
+      __syncthreads();
+      if (tid == 0)
+        atomicAdd(a.trace + (size_t)g * a.T + (a.t - 1), -(red[0] + red[1] + red[2] + red[3]));
+    }
+  } else if (W > 0.0) {
     if (a.t > 0) {
       double mn = fma(sy0, sy0, sy1 * sy1);
       for (int off = L / 2; off > 0; off >>= 1) mn += __shfl_xor(mn, off);
@@ -996,7 +1029,7 @@ __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
       ch |= a.changed[(size_t)g * a.nwg + c];
       if (a.obj) obj += a.obj[(size_t)g * a.nwg + c];
     }
-    if (a.trace) a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
+    if (a.trace) atomicAdd(a.trace + (size_t)g * a.T + (a.t - 1), obj);
     a.iters[g] = a.t;
     if (!ch && !a.no_early_stop) a.done[g] = a.t;
   }
@@ -1404,6 +1437,8 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   gsrq_status e;
   if ((e = fill_u32(done, G, 0, st))) return e;
   if ((e = fill_u32(iters, G, 0, st))) return e;
+  if (obj_trace && T_ > 0 && (e = fill_u32(obj_trace, (size_t)G * T_ * 2, 0, st))) return e;
+  const int kmeans = (flags & GSRQ_KMEANS) ? 1 : 0;
 
   WScoreArgs sa = {};
   sa.x = X; sa.ldx = ldx; sa.N = s->N; sa.d = d; sa.K = K; sa.G = G;
@@ -1425,7 +1460,7 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   fa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
   fa.force_changed = 0; fa.nwg = L.nwg; fa.part = part; fa.changed = changed; fa.obj = nullptr;
   fa.seednorm = seednorm; fa.gain = gain; fa.shape = shape; fa.done = done; fa.iters = iters;
-  fa.trace = obj_trace; fa.xchanged = XD.xchanged; fa.xobj = XD.xobj;
+  fa.trace = obj_trace; fa.xchanged = XD.xchanged; fa.xobj = XD.xobj; fa.kmeans = kmeans;
   const int cpb = 256 / (d / 2);
   const dim3 fgrid((unsigned)((K + cpb - 1) / cpb), (unsigned)G);
 
@@ -1454,9 +1489,14 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
     {
       TimedLaunch tl(GSRQ_KERNEL_TRANSPOSE, st);
       w_seed_kernel<T><<<dim3((K + 255) / 256, G), 256, 0, st>>>((const T*)X, ldx, d, K, seeds,
-                                                                 shape, seednorm);
+                                                                 shape, seednorm, kmeans, gain);
     }
     if ((e = launch_ok())) return e;
+  }
+  if (!(flags & GSRQ_RESUME) && kmeans) {
+    // K-means starts from the seed centroids; there is no previous assignment
+    fa.force_changed = 1;
+  } else if (!(flags & GSRQ_RESUME)) {
     // equal-gain assignment, then eq. (8) gains for the seed shapes
     if ((e = w_build_frags(gain, shape, d, K, L.C, G, 0, true, nullptr, G, sig, frag, XD, st)))
       return e;

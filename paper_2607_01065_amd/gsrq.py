@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libgsrq.so")
 
 GSRQ_OK, GSRQ_E_ARG, GSRQ_E_UNSUPPORTED, GSRQ_E_WORKSPACE, GSRQ_E_HIP = range(5)
 GSRQ_F32, GSRQ_F16 = 0, 1
-GSRQ_RESUME, GSRQ_ASSIGN_IN, GSRQ_NO_EARLY_STOP = 1, 2, 4
+GSRQ_RESUME, GSRQ_ASSIGN_IN, GSRQ_NO_EARLY_STOP, GSRQ_KMEANS = 1, 2, 4, 8
 
 
 class GsrqError(RuntimeError):
@@ -194,11 +194,12 @@ class TrainResult:
 
 def train_stage(X, d, K, T, seed_rows=None, w=None, *, gain=None, shape=None, assign=None,
                 resume=False, assign_in=False, no_early_stop=False, residual=False,
-                trace=True, workspace=None, stream=None) -> TrainResult:
+                trace=True, kmeans=False, workspace=None, stream=None) -> TrainResult:
     """One stage of weighted GSKM on device tensor X [N, D] (see gsrq_train_stage).
 
     residual: True for a new R_next tensor, or an [N, D] float32 tensor to
-    write it into."""
+    write it into.  kmeans: the K-means baseline (GSRQ_KMEANS) instead of
+    GSKM; its centroids are gain[:, :, None] * shape."""
     torch = _torch()
     lib = load_library()
     N, D, ldx = _rows(X)
@@ -220,7 +221,7 @@ def train_stage(X, d, K, T, seed_rows=None, w=None, *, gain=None, shape=None, as
     if seed_rows is not None:
         seeds = np.ascontiguousarray(np.asarray(seed_rows), dtype=np.int32)
     flags = ((GSRQ_RESUME if resume else 0) | (GSRQ_ASSIGN_IN if assign_in else 0)
-             | (GSRQ_NO_EARLY_STOP if no_early_stop else 0))
+             | (GSRQ_NO_EARLY_STOP if no_early_stop else 0) | (GSRQ_KMEANS if kmeans else 0))
     sh = make_shape(N, D, d, K, 1)
     n = ctypes.c_size_t(0)
     st = lib.gsrq_train_workspace_bytes(ctypes.byref(sh), ctypes.byref(n))

@@ -103,6 +103,8 @@ def test_train_stage_validation_before_any_hip_call():
     assert _train(lib, sh, seeds=None) == B.GSRQ_E_ARG                    # seeds needed
     assert _train(lib, sh, seeds=sp, dt=7) == B.GSRQ_E_ARG                # dtype
     assert _train(lib, sh, seeds=sp, flags=64) == B.GSRQ_E_ARG            # unknown flag
+    assert _train(lib, sh, seeds=sp, flags=16) == B.GSRQ_E_ARG            # unknown flag
+    assert _train(lib, sh, seeds=sp, flags=8 | 2) == B.GSRQ_E_ARG         # K-means, ASSIGN_IN alone
     assert _train(lib, sh, seeds=sp, flags=2) == B.GSRQ_E_ARG             # ASSIGN_IN w/o RESUME
     assert _train(lib, sh, seeds=sp, flags=3) == B.GSRQ_E_ARG             # ... and w/o assign
     assert _train(lib, sh, seeds=sp, ws=DUMMY * 16 + 8) == B.GSRQ_E_ARG   # misaligned ws

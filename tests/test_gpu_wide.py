@@ -185,6 +185,7 @@ def test_wide_train_stop_rule_and_residual():
         ref = O.gskm(X[:, g * d:(g + 1) * d].astype(np.float64), w.astype(np.float64), K, 20, seeds[g])
         assert iters[g] == ref["iters_run"] < 20
         assert np.allclose(r.trace.cpu().numpy()[g, :iters[g]], ref["trace"], rtol=1e-5)
+        assert np.all(r.trace.cpu().numpy()[g, iters[g]:] == 0)
         assert np.allclose(r.gain.cpu().numpy()[g], ref["gain"], rtol=1e-5)
         assert np.allclose(r.shape.cpu().numpy()[g], ref["shape"], atol=1e-5)
         cols = slice(g * d, (g + 1) * d)

@@ -416,3 +416,40 @@ def test_gskm_beats_kmeans_direction_on_gaussian_under_capacity():
     assert mg["cos"] > mk["cos"]
     assert mg["gain_err"] < mk["gain_err"]
     assert mg["mse"] < mk["mse"]
+
+
+def test_kmeans_steps_hand_worked():
+    """Lloyd steps on a hand-worked 1-D case: X = (0, 2, 10), w = (1, 3, 1),
+    centroids (1, 9).  Nearest: 0 and 2 go to centroid 1 (distance 1 each),
+    10 goes to 9.  New
+    centroids: (1*0 + 3*2) / 4 = 1.5 and 10; distortion after the update
+    1 * 1.5^2 + 3 * 0.5^2 + 0 = 3.  A point equidistant from two centroids
+    goes to the lower index."""
+    X = np.array([[0.0], [2.0], [10.0]])
+    w = np.array([1.0, 3.0, 1.0])
+    C = np.array([[1.0], [9.0]])
+    a = O.kmeans_assign(X, C)
+    assert a.tolist() == [0, 0, 1]
+    C1 = O.kmeans_update(X, w, a, C)
+    assert C1.ravel().tolist() == [1.5, 10.0]
+    out = O.kmeans(X, w, 2, 1, [0, 2], centroids=C)
+    assert out["trace"][0] == pytest.approx(3.0, abs=1e-15)
+    assert O.kmeans_assign(np.array([[5.0]]), C).tolist() == [0]
+    # an empty cluster keeps its centroid
+    C2 = O.kmeans_update(X, w, np.array([0, 0, 0]), C)
+    assert C2[1, 0] == 9.0 and C2[0, 0] == pytest.approx(16.0 / 5.0)
+
+
+def test_kmeans_assign_matches_brute_force():
+    rng = _rng(22)
+    X = rng.standard_normal((50, 3))
+    C = rng.standard_normal((7, 3))
+    C[4] = C[2]                               # duplicate: the lower index wins
+    a = O.kmeans_assign(X, C)
+    for i in range(50):
+        best, bk = None, -1
+        for k in range(7):
+            dd = sum((X[i, j] - C[k, j]) ** 2 for j in range(3))
+            if best is None or dd < best:
+                best, bk = dd, k
+        assert a[i] == bk
