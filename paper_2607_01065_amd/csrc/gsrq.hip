@@ -910,6 +910,7 @@ struct DecodeArgs {
   void* out;
   int gpw, gblocks;      // LDS kernel: subspaces per workgroup, subspace blocks
   int64_t rows_per_wg;   // LDS kernel: rows per workgroup
+  int tab_bytes;         // LDS kernel: table bytes (staged code words follow)
   int vec;               // LDS kernel: 8-element vector stores are aligned
 };
 
@@ -949,7 +950,8 @@ __global__ void decode_global_kernel(DecodeArgs a) {
 constexpr int DEC_THREADS = 1024;
 constexpr int DEC_TABLE_BYTES = 65536;     // codeword table per workgroup
 constexpr int DEC_ROW_BATCH = 4;           // rows in flight per thread
-constexpr int DEC_FILL_BATCH = 8;          // table entries in flight per thread
+constexpr int DEC_FILL_BATCH = 4;          // table entries in flight per thread
+constexpr int DEC_CODE_PT = 16;            // staged code words per thread, at most
 
 template <typename TO> struct OutVec;
 template <> struct OutVec<_Float16> {
@@ -996,20 +998,24 @@ template <> struct TabEntry<_Float16> {
   }
 };
 
-// Code of (stage m, subspace g) from a row's words: b bits at bit
-// (m G + g) b, least significant bit first, possibly straddling two words.
-__device__ __forceinline__ int read_code(const uint32_t* cr, int64_t bit, int b) {
-  const int64_t wi = bit >> 5;
-  const int off = (int)(bit & 31);
-  uint64_t v = cr[wi];
-  if (off + b > 32) v |= (uint64_t)cr[wi + 1] << 32;
-  return (int)((v >> off) & ((1ull << b) - 1));
+// Code words of subspaces [g0, g0 + ngr) of stage m within a row: the
+// word range [lo, lo + n) holding their b-bit fields.
+__device__ __forceinline__ void stage_words(int m, int G, int g0, int ngr, int b, int& lo,
+                                            int& n) {
+  const int64_t first = ((int64_t)m * G + g0) * b;
+  const int64_t last = first + (int64_t)ngr * b - 1;
+  lo = (int)(first >> 5);
+  n = (int)(last >> 5) - lo + 1;
 }
 
 // Gather-sum decoder with the codeword table in LDS.  A workgroup owns `gpw`
 // consecutive subspaces and a contiguous range of rows; its table holds the
 // codewords g s of those subspaces for the first M_use stages, laid out
-// [gpw][M_use][K][8].  Threads map to (row, subspace) with the subspace
+// [gpw][M_use][K][8].  The code words of its rows and subspaces are staged
+// in LDS too ([rows][words of stage 0, stage 1, ...]), loaded together with
+// the table, so the output loop issues no global loads: its stores stream
+// without waiting on loads (a wait on a load also waits for every store
+// issued before it).  Threads map to (row, subspace) with the subspace
 // fastest, so each row's output slice of gpw * d elements is written
 // contiguously, and every thread keeps DEC_ROW_BATCH rows in flight.
 // Workgroups that share rows (and so share code words) are numbered to land
@@ -1018,6 +1024,7 @@ template <typename TO, typename TT>
 __global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a) {
   extern __shared__ __align__(16) unsigned char dec_smem[];
   TT* tab = (TT*)dec_smem;
+  uint32_t* cwl = (uint32_t*)(dec_smem + a.tab_bytes);
   const int gpw = a.gpw, gblocks = a.gblocks;
   const int id = blockIdx.x;
   const int xcd = id % 8, slot = id / 8;
@@ -1027,10 +1034,36 @@ __global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a) {
   if (r_begin >= a.N) return;
   int64_t r_end = r_begin + a.rows_per_wg;
   if (r_end > a.N) r_end = a.N;
+  const int nrows = (int)(r_end - r_begin);
   const int g0 = gb * gpw;
   const int ngr = min(gpw, a.G - g0);
-  const int K = a.K, M = a.M_use, d = a.d;
+  const int K = a.K, M = a.M_use, d = a.d, G = a.G, b = a.b;
   const int tid = threadIdx.x;
+  // staged code words per row (host-checked: nrows * rs <= DEC_CODE_PT * DEC_THREADS)
+  int rs = 0;
+  for (int m = 0; m < M; ++m) {
+    int lo, n;
+    stage_words(m, G, g0, ngr, b, lo, n);
+    rs += n;
+  }
+  const int ncw = nrows * rs;
+  const uint32_t* crow = a.codes + r_begin * a.words;
+  uint32_t cw[DEC_CODE_PT];
+#pragma unroll
+  for (int q = 0; q < DEC_CODE_PT; ++q) {
+    if (q * DEC_THREADS < ncw) {           // uniform per q
+      const int e = min(q * DEC_THREADS + tid, ncw - 1);
+      const int row = e / rs;
+      int j = e - row * rs, m = 0, lo, n;
+      stage_words(0, G, g0, ngr, b, lo, n);
+      while (j >= n) {
+        j -= n;
+        ++m;
+        stage_words(m, G, g0, ngr, b, lo, n);
+      }
+      cw[q] = crow[(int64_t)row * a.words + lo + j];
+    }
+  }
   // table fill: every load of a batch is issued before the first use
   const int entries = ngr * M * K;
   for (int e0 = 0; e0 < entries; e0 += DEC_THREADS * DEC_FILL_BATCH) {
@@ -1039,9 +1072,9 @@ __global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a) {
     for (int q = 0; q < DEC_FILL_BATCH; ++q) {
       const int e = min(e0 + q * DEC_THREADS + tid, entries - 1);
       // K = 2^b; no integer division unless several stages are decoded
-      const int k = e & (K - 1), q2 = e >> a.b;
+      const int k = e & (K - 1), q2 = e >> b;
       const int m = M == 1 ? 0 : q2 % M, gi = M == 1 ? q2 : q2 / M;
-      const size_t cb = (size_t)m * a.G + g0 + gi;
+      const size_t cb = (size_t)m * G + g0 + gi;
       read_codeword(a.gain + cb * K, a.shape + cb * K * d, d, K, k, false, g[q], c[q]);
     }
 #pragma unroll
@@ -1054,35 +1087,50 @@ __global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a) {
       }
     }
   }
+#pragma unroll
+  for (int q = 0; q < DEC_CODE_PT; ++q) {
+    const int e = q * DEC_THREADS + tid;
+    if (e < ncw) cwl[e] = cw[q];
+  }
   __syncthreads();
   const int gi = tid % gpw;
   if (gi >= ngr) return;
   const int rstep = DEC_THREADS / gpw;
   const int g = g0 + gi;
   const TT* tg = tab + (size_t)gi * M * K * 8;
-  for (int64_t r0 = r_begin + tid / gpw; r0 < r_end; r0 += (int64_t)DEC_ROW_BATCH * rstep) {
+  for (int r0 = tid / gpw; r0 < nrows; r0 += DEC_ROW_BATCH * rstep) {
     float acc[DEC_ROW_BATCH][8];
 #pragma unroll
     for (int q = 0; q < DEC_ROW_BATCH; ++q)
 #pragma unroll
       for (int j = 0; j < 8; ++j) acc[q][j] = 0.f;
+    int off = 0;                            // staged words of the stages before m
     for (int m = 0; m < M; ++m) {
+      int lo, n;
+      stage_words(m, G, g0, ngr, b, lo, n);
+      const int p = (int)(((int64_t)m * G + g) * b - (int64_t)lo * 32);
+      const int wi = off + (p >> 5), sh = p & 31;
+      const bool two = sh + b > 32;
       int k[DEC_ROW_BATCH];
 #pragma unroll
       for (int q = 0; q < DEC_ROW_BATCH; ++q) {
-        int64_t row = r0 + (int64_t)q * rstep;
-        row = row < r_end ? row : r_begin;    // in-range row; its result is not stored
-        k[q] = read_code(a.codes + row * a.words, ((int64_t)m * a.G + g) * a.b, a.b);
+        int row = r0 + q * rstep;
+        row = row < nrows ? row : 0;       // in-range row; its result is not stored
+        const uint32_t* w = cwl + row * rs + wi;
+        uint64_t v = w[0];
+        if (two) v |= (uint64_t)w[1] << 32;
+        k[q] = (int)((v >> sh) & ((1u << b) - 1));
       }
 #pragma unroll
       for (int q = 0; q < DEC_ROW_BATCH; ++q)
         TabEntry<TT>::add(tg + ((size_t)m * K + k[q]) * 8, acc[q]);
+      off += n;
     }
 #pragma unroll
     for (int q = 0; q < DEC_ROW_BATCH; ++q) {
-      const int64_t row = r0 + (int64_t)q * rstep;
-      if (row >= r_end) break;
-      TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
+      const int row = r0 + q * rstep;
+      if (row >= nrows) break;
+      TO* dst = (TO*)a.out + (r_begin + row) * a.ldo + (int64_t)g * d;
       if (a.vec) {
         OutVec<TO>::store(dst, acc[q]);
       } else {
@@ -1428,24 +1476,53 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_us
     while (gpw * 2 <= 64 && gpw * 2 * per_group <= DEC_TABLE_BYTES && gpw < a.G) gpw *= 2;
     a.gpw = gpw;
     a.gblocks = (a.G + gpw - 1) / gpw;
+    // staged code words per row: the most any subspace block needs
+    int64_t rs = 1;
+    for (int gb = 0; gb < a.gblocks; ++gb) {
+      const int64_t g0 = (int64_t)gb * gpw, ngr = std::min<int64_t>(gpw, a.G - g0);
+      int64_t n = 0;
+      for (int m = 0; m < M_use; ++m) {
+        const int64_t first = (m * (int64_t)a.G + g0) * a.b, last = first + ngr * a.b - 1;
+        n += (last >> 5) - (first >> 5) + 1;
+      }
+      rs = std::max(rs, n);
+    }
     // about one workgroup per CU, each streaming a contiguous row range (the
-    // table fill is paid once per workgroup)
+    // table fill is paid once per workgroup), with at most DEC_CODE_PT
+    // staged code words per thread
     int64_t rchunks = (256 + a.gblocks - 1) / a.gblocks;
     const int64_t min_rows = 256;
     if (rchunks * min_rows > s->N) rchunks = (s->N + min_rows - 1) / min_rows;
     if (rchunks < 1) rchunks = 1;
+    const int64_t max_rows = (int64_t)DEC_CODE_PT * DEC_THREADS / rs;
+    if (max_rows < 1) return GSRQ_E_UNSUPPORTED;
     a.rows_per_wg = (s->N + rchunks - 1) / rchunks;
+    if (a.rows_per_wg > max_rows) a.rows_per_wg = max_rows;
     rchunks = (s->N + a.rows_per_wg - 1) / a.rows_per_wg;
+    if (8 * a.gblocks * ((rchunks + 7) / 8) > INT32_MAX) return GSRQ_E_UNSUPPORTED;
     const int blocks = (int)(8 * a.gblocks * ((rchunks + 7) / 8));
     const size_t esz = out_dtype == GSRQ_F16 ? 2 : 4;
     a.vec = (s->d == 8) && ((uintptr_t)Xhat % 16 == 0) && ((ldo * esz) % 16 == 0);
-    const size_t lds = (size_t)gpw * per_group;
+    a.tab_bytes = (int)(gpw * per_group);
+    const size_t lds = (size_t)a.tab_bytes + (size_t)a.rows_per_wg * rs * sizeof(uint32_t);
+    auto launch = [&](const void* fn, auto kern) -> gsrq_status {
+      if (lds > 65536 &&
+          hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+              hipSuccess)
+        return GSRQ_E_HIP;
+      kern<<<blocks, DEC_THREADS, lds, st>>>(a);
+      return GSRQ_OK;
+    };
+    gsrq_status e;
     if (out_dtype == GSRQ_F16 && half_tab)
-      decode_lds_kernel<_Float16, _Float16><<<blocks, DEC_THREADS, lds, st>>>(a);
+      e = launch((const void*)decode_lds_kernel<_Float16, _Float16>,
+                 decode_lds_kernel<_Float16, _Float16>);
     else if (out_dtype == GSRQ_F16)
-      decode_lds_kernel<_Float16, float><<<blocks, DEC_THREADS, lds, st>>>(a);
+      e = launch((const void*)decode_lds_kernel<_Float16, float>,
+                 decode_lds_kernel<_Float16, float>);
     else
-      decode_lds_kernel<float, float><<<blocks, DEC_THREADS, lds, st>>>(a);
+      e = launch((const void*)decode_lds_kernel<float, float>, decode_lds_kernel<float, float>);
+    if (e) return e;
   } else {
     const int grid = grid_for(s->N * a.G, 256);
     if (out_dtype == GSRQ_F16)

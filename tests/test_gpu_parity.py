@@ -102,7 +102,8 @@ def test_encode_multi_stage_teacher_forced(M, K, d, D):
     assert np.allclose(Rg, R, rtol=1e-5, atol=1e-6 * scale)
 
 
-@pytest.mark.parametrize("M,K,d,D,N", [(1, 256, 8, 64, 1000), (3, 16, 4, 24, 333), (2, 4096 // 16, 8, 16, 50)])
+@pytest.mark.parametrize("M,K,d,D,N", [(1, 256, 8, 64, 1000), (3, 16, 4, 24, 333), (2, 4096 // 16, 8, 16, 50),
+                                        (3, 8, 2, 6, 2000), (2, 32, 4, 40, 5000), (1, 256, 8, 1024, 4100)])
 def test_decode(M, K, d, D, N):
     say("decode", M, K, d, D, N)
     G = D // d
@@ -220,3 +221,27 @@ def test_train_stop_rule_and_residual():
     r2 = B.train_stage(to_dev(X), d, K, 7, seed_rows=seeds, w=to_dev(w), no_early_stop=True)
     torch.cuda.synchronize()
     assert np.all(r2.iters.cpu().numpy() == 7)
+
+
+def test_decode_row_cap_sampled():
+    """1-bit layer shape with more tokens than one workgroup can stage codes
+    for (140000 rows x 128 subspaces: the row range per workgroup is capped
+    and the grid grows): sampled rows, including the ragged tail, against
+    the oracle's decode of the same codes."""
+    say("decode row cap")
+    N, D, d, K = 140000, 1024, 8, 256
+    G = D // d
+    rng = _rng(16)
+    codes = rng.integers(0, K, size=(N, 1, G))
+    words = O.pack_codes(codes, K).view(np.int32)
+    gain = rng.uniform(0.0, 5.0, size=(1, G, K)).astype(np.float32)
+    sh = rng.standard_normal((1, G, K, d))
+    shape = (sh / np.linalg.norm(sh, axis=-1, keepdims=True)).astype(np.float32)
+    out = B.decode(to_dev(words), to_dev(gain), to_dev(shape), D, out_dtype=torch.float16)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([rng.choice(N, size=3000, replace=False), np.arange(N - 300, N),
+                                     np.arange(0, 300)]))
+    ref = O.gsrq_decode(codes[rows], gain, shape)
+    got = out.cpu().numpy()[rows].astype(np.float64)
+    ulp = np.spacing(np.abs(ref).astype(np.float16)).astype(np.float64)
+    assert np.all(np.abs(got - ref) <= ulp + 1e-6 * np.abs(ref).max())
