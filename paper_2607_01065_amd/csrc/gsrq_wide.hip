@@ -465,6 +465,44 @@ __device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[W_
 
 // Writes code k into the b-bit field at `bit` of a row's words (zeroed
 // beforehand): byte and half-word fields are stored, others OR'd in.
+// Four consecutive elements of a stage-input row as float32 (vector load:
+// 16 bytes of float32, 8 bytes of float16).
+__device__ __forceinline__ f4 w_load4(const float* p) { return *(const f4*)p; }
+__device__ __forceinline__ f4 w_load4(const _Float16* p) {
+  typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+  const h4 v = *(const h4*)p;
+  return (f4){(float)v[0], (float)v[1], (float)v[2], (float)v[3]};
+}
+
+// Residual r = x - g s over n consecutive elements (a lane half's share of
+// a row), written to dst when dst is non-null; returns ||r||^2 (float32).
+// vec: n % 4 == 0 and x, s, dst 16-byte (float16 x: 8-byte) aligned, so
+// every access is a vector access; otherwise element by element.
+template <typename T>
+__device__ __forceinline__ float w_residual(const T* xp, const float* sk, float gk, int n,
+                                            bool vec, float* dst) {
+  float dist = 0.f;
+  if (vec) {
+    for (int j = 0; j < n; j += 4) {
+      const f4 x = w_load4(xp + j), sv = *(const f4*)(sk + j);
+      f4 r;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        r[u] = fmaf(-gk, sv[u], x[u]);
+        dist = fmaf(r[u], r[u], dist);
+      }
+      if (dst) *(f4*)(dst + j) = r;
+    }
+  } else {
+    for (int j = 0; j < n; ++j) {
+      const float r = fmaf(-gk, sk[j], (float)xp[j]);
+      dist = fmaf(r, r, dist);
+      if (dst) dst[j] = r;
+    }
+  }
+  return dist;
+}
+
 __device__ __forceinline__ void w_put_code(uint32_t* wp, int64_t bit, int b, int k) {
   if (b == 8) {
     ((uint8_t*)wp)[bit >> 3] = (uint8_t)k;
@@ -523,6 +561,10 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   const T* X = (const T*)a.x;
   const bool vec = (d == 8 * C) && ((a.ldx * (int64_t)sizeof(T)) % 16 == 0) &&
                    (((uintptr_t)X) % 16 == 0);
+  // vector accesses in the residual / objective epilogue: row, codeword and
+  // residual output aligned (d is a multiple of 8)
+  const bool rvec = vec && (((uintptr_t)scb) % 16 == 0) &&
+                    (a.res_out == nullptr || ((uintptr_t)a.res_out) % 16 == 0);
   if (tid == 0) red_changed = 0;
   if (RESIDENT) {
     const int n = tiles * QU * 64;
@@ -650,12 +692,8 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       if (a.obj) {
         // weighted distortion of this assignment under the scoring codebook;
         // each lane half sums half of the elements
-        float dist = 0.f;
-        const int jb = h * (d / 2), je = jb + d / 2;
-        for (int j = jb; j < je; ++j) {
-          const float r = fmaf(-gk, sk[j], (float)xp[j]);
-          dist = fmaf(r, r, dist);
-        }
+        const int jb = h * (d / 2);
+        float dist = w_residual<T>(xp + jb, sk + jb, gk, d / 2, rvec, nullptr);
         dist += __shfl_xor(dist, 32);
         if (own && h == 0) obj += (double)(a.w ? a.w[row] : 1.f) * (double)dist;
       }
@@ -663,9 +701,10 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       if (own && h == 0 && a.codes)
         w_put_code(a.codes + row * a.words, ((int64_t)a.m * a.G + g) * a.b, a.b, kstar);
       if (own && a.res_out) {
-        float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d;
-        const int jb = h * (d / 2), je = jb + d / 2;
-        for (int j = jb; j < je; ++j) dst[j] = fmaf(-gk, sk[j], (float)xp[j]);
+        // each lane half writes its half of the row's residual
+        const int jb = h * (d / 2);
+        float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d + jb;
+        w_residual<T>(xp + jb, sk + jb, gk, d / 2, rvec, dst);
       }
     }
   }
