@@ -46,6 +46,7 @@ constexpr int W_STREAM_BYTES = 30720;           // one staging buffer when strea
 constexpr int W_SREG = (W_STREAM_BYTES / 16 + W_THREADS - 1) / W_THREADS;  // staged u4 per thread
 constexpr int W_ACC_LDS_BYTES = 98304;          // accumulator slice in LDS
 constexpr int W_ACC_BATCH = 4;                  // rows per thread per collection pass
+constexpr int W_ACC_MEMBERS = 8;                // member rows per lane group in flight
 constexpr int W_DEC_TABLE_BYTES = 65536;
 constexpr int W_DEC_THREADS = 1024;
 
@@ -948,23 +949,38 @@ __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
     }
     __syncthreads();
     const int n = nlist;
-    for (int it = wave * per_wave + sub; it < n; it += W_WAVES * per_wave) {
-      const int64_t row = r0 + list[it];
-      const int k = asg[row];
-      const T* xr = X + row * a.ldx + (int64_t)g * d;
-      const float x0 = (float)xr[2 * li], x1 = (float)xr[2 * li + 1];
-      float ss = fmaf(x0, x0, x1 * x1);
-      for (int off = L / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-      const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
-      const float wt = a.w ? a.w[row] : 1.f;
-      double* ak = wacc + (size_t)(k - k0) * S;
-      unsafeAtomicAdd(ak + 2 * li, (double)(x0 * (wt * inv)));
-      unsafeAtomicAdd(ak + 2 * li + 1, (double)(x1 * (wt * inv)));
-      unsafeAtomicAdd(ak + d + 2 * li, (double)(x0 * wt));
-      unsafeAtomicAdd(ak + d + 2 * li + 1, (double)(x1 * wt));
-      if (li == 0) {
-        unsafeAtomicAdd(ak + 2 * d, (double)wt);
-        unsafeAtomicAdd(ak + 2 * d + 1, 1.0);
+    // W_ACC_MEMBERS members per lane group in flight: every load of a batch
+    // is issued before the first use (past the list's end a lane group
+    // re-reads its first member and adds nothing)
+    const int stride = W_WAVES * per_wave;
+    for (int it0 = wave * per_wave + sub; it0 < n; it0 += W_ACC_MEMBERS * stride) {
+      float x0[W_ACC_MEMBERS], x1[W_ACC_MEMBERS], wt[W_ACC_MEMBERS];
+      int k[W_ACC_MEMBERS];
+#pragma unroll
+      for (int u = 0; u < W_ACC_MEMBERS; ++u) {
+        const int it = it0 + u * stride < n ? it0 + u * stride : it0;
+        const int64_t row = r0 + list[it];
+        k[u] = asg[row];
+        const T* xr = X + row * a.ldx + (int64_t)g * d;
+        x0[u] = (float)xr[2 * li];
+        x1[u] = (float)xr[2 * li + 1];
+        wt[u] = a.w ? a.w[row] : 1.f;
+      }
+#pragma unroll
+      for (int u = 0; u < W_ACC_MEMBERS; ++u) {
+        float ss = fmaf(x0[u], x0[u], x1[u] * x1[u]);
+        for (int off = L / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+        if (it0 + u * stride >= n) continue;   // uniform within the lane group
+        const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
+        double* ak = wacc + (size_t)(k[u] - k0) * S;
+        unsafeAtomicAdd(ak + 2 * li, (double)(x0[u] * (wt[u] * inv)));
+        unsafeAtomicAdd(ak + 2 * li + 1, (double)(x1[u] * (wt[u] * inv)));
+        unsafeAtomicAdd(ak + d + 2 * li, (double)(x0[u] * wt[u]));
+        unsafeAtomicAdd(ak + d + 2 * li + 1, (double)(x1[u] * wt[u]));
+        if (li == 0) {
+          unsafeAtomicAdd(ak + 2 * d, (double)wt[u]);
+          unsafeAtomicAdd(ak + 2 * d + 1, 1.0);
+        }
       }
     }
     __syncthreads();
