@@ -47,6 +47,7 @@ constexpr int W_SREG = (W_STREAM_BYTES / 16 + W_THREADS - 1) / W_THREADS;  // st
 constexpr int W_ACC_LDS_BYTES = 98304;          // accumulator slice in LDS
 constexpr int W_ACC_BATCH = 4;                  // rows per thread per collection pass
 constexpr int W_ACC_MEMBERS = 8;                // member rows per lane group in flight
+constexpr int W_BUCKET_KMAX = 16384;            // codewords the bucketing histogram holds
 constexpr int W_DEC_TABLE_BYTES = 65536;
 constexpr int W_DEC_THREADS = 1024;
 
@@ -903,14 +904,113 @@ struct WAccArgs {
   double* part;            // [G][rchunks][K][2d+2]
   int ks, slices, rchunks;
   int64_t rows_per_chunk;
+  const int* sorted;       // [G][N] rows bucketed by codeword, or null
+  const int* boff;         // [G][K + 1] bucket offsets into sorted
 };
+
+// Rows of each subspace bucketed by codeword (a counting sort): boff[g][k]
+// is the first position of codeword k's members in sorted[g], boff[g][K] =
+// N.  One workgroup per subspace; the histogram and the bucket cursors live
+// in LDS (K ints).  The order within a bucket is that of LDS atomics (the
+// sums built from it are then exact up to float64 rounding order).
+__global__ void __launch_bounds__(1024) w_bucket_kernel(const uint16_t* __restrict__ assign,
+                                                        int64_t N, int K,
+                                                        const int* __restrict__ done,
+                                                        int* __restrict__ boff,
+                                                        int* __restrict__ sorted) {
+  extern __shared__ int hist[];
+  __shared__ int wsum[16];
+  const int g = blockIdx.x;
+  if (done && done[g]) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint16_t* asg = assign + (size_t)g * N;
+  for (int k = tid; k < K; k += 1024) hist[k] = 0;
+  __syncthreads();
+  for (int64_t r = tid; r < N; r += 1024) atomicAdd(&hist[asg[r]], 1);
+  __syncthreads();
+  // exclusive scan: thread tid owns bins [b, e)
+  const int per = (K + 1023) / 1024;
+  const int b = min(K, tid * per), e = min(K, b + per);
+  int tot = 0;
+  for (int k = b; k < e; ++k) tot += hist[k];
+  int inc = tot;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(inc, off);
+    if (lane >= off) inc += v;
+  }
+  if (lane == 63) wsum[wave] = inc;
+  __syncthreads();
+  int base = inc - tot;
+  for (int w2 = 0; w2 < wave; ++w2) base += wsum[w2];
+  int* bo = boff + (size_t)g * (K + 1);
+  for (int k = b; k < e; ++k) {
+    const int c = hist[k];
+    bo[k] = base;
+    hist[k] = base;
+    base += c;
+  }
+  if (tid == 0) bo[K] = (int)N;
+  __syncthreads();
+  int* srt = sorted + (size_t)g * N;
+  for (int64_t r = tid; r < N; r += 1024) srt[atomicAdd(&hist[asg[r]], 1)] = (int)r;
+}
+
+// Batched member loop of the accumulation: members [0, n), member `it` is
+// row row_of(it) of codeword asg[row] in [k0, k0 + ks).  Lane groups of d/2
+// lanes take one member each (two elements per lane), W_ACC_MEMBERS members
+// per lane group in flight: every load of a batch is issued before the
+// first use (past the end a lane group re-reads its first member and adds
+// nothing).
+template <typename T, typename RowOf>
+__device__ __forceinline__ void w_acc_members(const WAccArgs& a, int g, int k0, double* wacc,
+                                              int n, RowOf row_of) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int d = a.d, S = 2 * d + 2;
+  const int L = d / 2;                 // lanes per member row (power of two)
+  const int per_wave = 64 / L;
+  const int sub = lane / L, li = lane % L;
+  const uint16_t* asg = a.assign + (size_t)g * a.N;
+  const T* X = (const T*)a.x;
+  const int stride = W_WAVES * per_wave;
+  for (int it0 = wave * per_wave + sub; it0 < n; it0 += W_ACC_MEMBERS * stride) {
+    float x0[W_ACC_MEMBERS], x1[W_ACC_MEMBERS], wt[W_ACC_MEMBERS];
+    int k[W_ACC_MEMBERS];
+#pragma unroll
+    for (int u = 0; u < W_ACC_MEMBERS; ++u) {
+      const int it = it0 + u * stride < n ? it0 + u * stride : it0;
+      const int64_t row = row_of(it);
+      k[u] = asg[row];
+      const T* xr = X + row * a.ldx + (int64_t)g * d;
+      x0[u] = (float)xr[2 * li];
+      x1[u] = (float)xr[2 * li + 1];
+      wt[u] = a.w ? a.w[row] : 1.f;
+    }
+#pragma unroll
+    for (int u = 0; u < W_ACC_MEMBERS; ++u) {
+      float ss = fmaf(x0[u], x0[u], x1[u] * x1[u]);
+      for (int off = L / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      if (it0 + u * stride >= n) continue;   // uniform within the lane group
+      const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
+      double* ak = wacc + (size_t)(k[u] - k0) * S;
+      unsafeAtomicAdd(ak + 2 * li, (double)(x0[u] * (wt[u] * inv)));
+      unsafeAtomicAdd(ak + 2 * li + 1, (double)(x1[u] * (wt[u] * inv)));
+      unsafeAtomicAdd(ak + d + 2 * li, (double)(x0[u] * wt[u]));
+      unsafeAtomicAdd(ak + d + 2 * li + 1, (double)(x1[u] * wt[u]));
+      if (li == 0) {
+        unsafeAtomicAdd(ak + 2 * d, (double)wt[u]);
+        unsafeAtomicAdd(ak + 2 * d + 1, 1.0);
+      }
+    }
+  }
+}
 
 // Weighted sums of eqs. 6-8 for one (codeword slice, row chunk, subspace):
 // sum w y and sum w x (y = x / (||x|| + eps)), sum w and the member count
 // per codeword, accumulated in float64 LDS and written as one partial.
-// The chunk's members of the slice are collected into an LDS list first;
-// then lanes groups of d/2 lanes take one member row each (two elements
-// per lane).
+// Members: with one slice, every row of the chunk; with bucketed rows, the
+// chunk's share of the slice's buckets; otherwise the chunk's members of
+// the slice, collected into an LDS list first.
 template <typename T>
 __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
   extern __shared__ double wacc[];
@@ -919,71 +1019,49 @@ __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
   const int g = blockIdx.y;
   if (a.done && a.done[g]) return;
   const int slice = blockIdx.x % a.slices, rc = blockIdx.x / a.slices;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
   const int d = a.d, S = 2 * d + 2;
   const int k0 = slice * a.ks, k1 = min(a.K, k0 + a.ks);
   for (int e = tid; e < a.ks * S; e += W_THREADS) wacc[e] = 0.0;
-  const int64_t r0 = (int64_t)rc * a.rows_per_chunk;
-  const int64_t r1 = min(a.N, r0 + a.rows_per_chunk);
-  const uint16_t* asg = a.assign + (size_t)g * a.N;
-  const T* X = (const T*)a.x;
-  const int L = d / 2;                 // lanes per member row (power of two)
-  const int per_wave = 64 / L;
-  const int sub = lane / L, li = lane % L;
-  for (int64_t base = r0; base < r1; base += (int64_t)W_THREADS * W_ACC_BATCH) {
-    if (tid == 0) nlist = 0;
+  __syncthreads();
+  if (a.sorted) {
+    const int* bo = a.boff + (size_t)g * (a.K + 1);
+    const int m0 = bo[k0], m1 = bo[k1];
+    const int mb = m0 + (int)((int64_t)(m1 - m0) * rc / a.rchunks);
+    const int me = m0 + (int)((int64_t)(m1 - m0) * (rc + 1) / a.rchunks);
+    const int* srt = a.sorted + (size_t)g * a.N + mb;
+    w_acc_members<T>(a, g, k0, wacc, me - mb, [&](int it) { return (int64_t)srt[it]; });
     __syncthreads();
+  } else {
+    const int64_t r0 = (int64_t)rc * a.rows_per_chunk;
+    const int64_t r1 = min(a.N, r0 + a.rows_per_chunk);
+    if (a.slices == 1) {
+      w_acc_members<T>(a, g, k0, wacc, (int)(r1 - r0), [&](int it) { return r0 + it; });
+      __syncthreads();
+    } else {
+      const uint16_t* asg = a.assign + (size_t)g * a.N;
+      for (int64_t base = r0; base < r1; base += (int64_t)W_THREADS * W_ACC_BATCH) {
+        if (tid == 0) nlist = 0;
+        __syncthreads();
 #pragma unroll
-    for (int q = 0; q < W_ACC_BATCH; ++q) {
-      // one LDS atomic per wave: members are placed by their rank in the wave
-      const int64_t row = base + (int64_t)q * W_THREADS + tid;
-      const int k = row < r1 ? (int)asg[row] : -1;
-      const bool in = k >= k0 && k < k1;
-      const unsigned long long m = __ballot(in);
-      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                 __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-      int base_idx = 0;
-      if (lane == 0 && m) base_idx = atomicAdd(&nlist, __popcll(m));
-      base_idx = __shfl(base_idx, 0);
-      if (in) list[base_idx + rank] = (int)(row - r0);
-    }
-    __syncthreads();
-    const int n = nlist;
-    // W_ACC_MEMBERS members per lane group in flight: every load of a batch
-    // is issued before the first use (past the list's end a lane group
-    // re-reads its first member and adds nothing)
-    const int stride = W_WAVES * per_wave;
-    for (int it0 = wave * per_wave + sub; it0 < n; it0 += W_ACC_MEMBERS * stride) {
-      float x0[W_ACC_MEMBERS], x1[W_ACC_MEMBERS], wt[W_ACC_MEMBERS];
-      int k[W_ACC_MEMBERS];
-#pragma unroll
-      for (int u = 0; u < W_ACC_MEMBERS; ++u) {
-        const int it = it0 + u * stride < n ? it0 + u * stride : it0;
-        const int64_t row = r0 + list[it];
-        k[u] = asg[row];
-        const T* xr = X + row * a.ldx + (int64_t)g * d;
-        x0[u] = (float)xr[2 * li];
-        x1[u] = (float)xr[2 * li + 1];
-        wt[u] = a.w ? a.w[row] : 1.f;
-      }
-#pragma unroll
-      for (int u = 0; u < W_ACC_MEMBERS; ++u) {
-        float ss = fmaf(x0[u], x0[u], x1[u] * x1[u]);
-        for (int off = L / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-        if (it0 + u * stride >= n) continue;   // uniform within the lane group
-        const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
-        double* ak = wacc + (size_t)(k[u] - k0) * S;
-        unsafeAtomicAdd(ak + 2 * li, (double)(x0[u] * (wt[u] * inv)));
-        unsafeAtomicAdd(ak + 2 * li + 1, (double)(x1[u] * (wt[u] * inv)));
-        unsafeAtomicAdd(ak + d + 2 * li, (double)(x0[u] * wt[u]));
-        unsafeAtomicAdd(ak + d + 2 * li + 1, (double)(x1[u] * wt[u]));
-        if (li == 0) {
-          unsafeAtomicAdd(ak + 2 * d, (double)wt[u]);
-          unsafeAtomicAdd(ak + 2 * d + 1, 1.0);
+        for (int q = 0; q < W_ACC_BATCH; ++q) {
+          // one LDS atomic per wave: members are placed by their rank in the wave
+          const int64_t row = base + (int64_t)q * W_THREADS + tid;
+          const int k = row < r1 ? (int)asg[row] : -1;
+          const bool in = k >= k0 && k < k1;
+          const unsigned long long m = __ballot(in);
+          const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+          int base_idx = 0;
+          if (lane == 0 && m) base_idx = atomicAdd(&nlist, __popcll(m));
+          base_idx = __shfl(base_idx, 0);
+          if (in) list[base_idx + rank] = (int)(row - r0);
         }
+        __syncthreads();
+        w_acc_members<T>(a, g, k0, wacc, nlist, [&](int it) { return r0 + list[it]; });
+        __syncthreads();
       }
     }
-    __syncthreads();
   }
   double* out = a.part + (((size_t)g * a.rchunks + rc) * a.K + k0) * S;
   const int n = (k1 - k0) * S;
@@ -1368,6 +1446,7 @@ struct WAccLayout {
   int ks, slices, rchunks;
   int64_t rows_per_chunk;
   size_t lds;
+  bool bucket;          // rows bucketed by codeword before accumulating
 };
 
 WAccLayout w_acc_layout(const gsrq_shape* s) {
@@ -1385,12 +1464,15 @@ WAccLayout w_acc_layout(const gsrq_shape* s) {
   A.rows_per_chunk = (s->N + rc - 1) / rc;
   A.rchunks = (int)((s->N + A.rows_per_chunk - 1) / A.rows_per_chunk);
   A.lds = (size_t)ks * per_k;
+  // several slices: bucket the rows by codeword once per pass instead of
+  // every slice scanning every row (the histogram is K ints of LDS)
+  A.bucket = A.slices > 1 && s->K <= W_BUCKET_KMAX;
   return A;
 }
 
 struct WTrainWs {
   size_t frag, gmin, xcount, xrows, xchanged, xobj, sig, part, changed, obj, assign, done, iters,
-      seednorm, seeds, total;
+      seednorm, seeds, sorted, boff, total;
 };
 
 WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
@@ -1416,6 +1498,8 @@ WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
   W.iters = off; off = align256(off + (size_t)G * sizeof(int));
   W.seednorm = off; off = align256(off + (size_t)G * s->K * sizeof(float));
   W.seeds = off; off = align256(off + (size_t)G * s->K * sizeof(int32_t));
+  W.sorted = off; off = align256(off + (A.bucket ? (size_t)G * s->N * sizeof(int) : 0));
+  W.boff = off; off = align256(off + (A.bucket ? (size_t)G * (s->K + 1) * sizeof(int) : 0));
   W.total = off;
   return W;
 }
@@ -1508,6 +1592,8 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   aa.x = X; aa.ldx = ldx; aa.N = s->N; aa.d = d; aa.K = K; aa.G = G; aa.w = w;
   aa.assign = assign; aa.done = done; aa.part = part;
   aa.ks = A.ks; aa.slices = A.slices; aa.rchunks = A.rchunks; aa.rows_per_chunk = A.rows_per_chunk;
+  aa.sorted = A.bucket ? (const int*)(base + W.sorted) : nullptr;
+  aa.boff = A.bucket ? (const int*)(base + W.boff) : nullptr;
   const dim3 agrid((unsigned)(A.slices * A.rchunks), (unsigned)G);
 
   WFinArgs fa;
@@ -1527,6 +1613,11 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
     gsrq_status e2;
     {
       TimedLaunch tl(GSRQ_KERNEL_ACCUMULATE, st);
+      if (A.bucket) {
+        w_bucket_kernel<<<G, 1024, (size_t)K * sizeof(int), st>>>(
+            assign, s->N, K, aa.done, (int*)(base + W.boff), (int*)(base + W.sorted));
+        if ((e2 = launch_ok())) return e2;
+      }
       w_accumulate_kernel<T><<<agrid, W_THREADS, A.lds, st>>>(aa);
     }
     if ((e2 = launch_ok())) return e2;
