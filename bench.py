@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="llama3_8b_layer_1bit")
+    ap.add_argument("--stages", type=int, default=0,
+                    help="override the workload's number of residual stages M")
     ap.add_argument("--cpu-groups", type=int, default=128,
                     help="subspaces of the K cache the CPU-baseline sample runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -209,6 +211,9 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     wl = synth.WORKLOADS[args.workload]
+    if args.stages > 0:
+        import dataclasses
+        wl = dataclasses.replace(wl, M=args.stages)
     if wl.layers > 1:
         return full_cache(args, wl)
     N, D, d, K, T, M = wl.N, wl.D, wl.d, wl.K, wl.T, wl.M

@@ -1303,15 +1303,20 @@ __global__ void __launch_bounds__(256) w_decode_gather_kernel(WDecArgs a, int C)
     const size_t cb = (size_t)m * a.G + g;
     const float gk = a.gain[cb * K + k];
     const float* sv = a.shape + (cb * K + k) * d + 8 * q;
-    if (a.vec) {
-      const f4 lo = ((const f4*)sv)[0], hi = ((const f4*)sv)[1];
+    {
+      // the codeword g s is rounded to float32 before the stage sum (no
+      // fused multiply-add), as the decode contract states
+#pragma clang fp contract(off)
+      if (a.vec) {
+        const f4 lo = ((const f4*)sv)[0], hi = ((const f4*)sv)[1];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        acc[j] = fmaf(gk, lo[j], acc[j]);
-        acc[4 + j] = fmaf(gk, hi[j], acc[4 + j]);
+        for (int j = 0; j < 4; ++j) {
+          acc[j] += gk * lo[j];
+          acc[4 + j] += gk * hi[j];
+        }
+      } else {
+        for (int j = 0; j < 8 && 8 * q + j < d; ++j) acc[j] += gk * sv[j];
       }
-    } else {
-      for (int j = 0; j < 8 && 8 * q + j < d; ++j) acc[j] = fmaf(gk, sv[j], acc[j]);
     }
   }
   TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d + 8 * q;

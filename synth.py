@@ -72,6 +72,12 @@ WORKLOADS = {
     "rate_sweep_d16": Workload(
         "rate_sweep_d16", 65536, 1024, 16, 256, 4, 20, "float16",
         note="65536 tok x 8 heads x 128 fp16, d=16 K=256 M in {1,2,4}"),
+    # the paper's own rate configuration: full-head subvectors, K = 256,
+    # 32 stages (2 bits); its 12- and 16-stage prefixes are 0.75 and 1 bit
+    "paper_rates_d128": Workload(
+        "paper_rates_d128", 32768, 1024, 128, 256, 32, 20, "float16",
+        note="32768 tok x 8 heads x 128 fp16, d=128 K=256 M=32 (2 bit; 12/16-stage prefixes "
+             "are 0.75/1 bit)"),
     # large codebook, full-head vectors
     "large_codebook_d128": Workload(
         "large_codebook_d128", 65536, 1024, 128, 4096, 8, 15, "float16",

@@ -86,6 +86,47 @@ def test_wide_encode_multi_stage_teacher_forced(dtype, M, K, d, D, N):
     assert np.allclose(Rg, R, rtol=1e-5, atol=1e-6 * np.abs(X.astype(np.float64)).max())
 
 
+def test_paper_rate_deep_stages():
+    """The paper's own rate configuration (Sec. 6.2 / Appendix A): d = 128,
+    K = 256, M = 32 stages (2 bits per element; its prefixes of 12 and 16
+    stages are the 0.75- and 1-bit configurations).  Codebooks from the
+    oracle's GSRQ training; the 32-stage encode is checked stage by stage on
+    the residual the GPU's own earlier choices leave (margin rule), the
+    residual output against that, and the prefix decodes (12, 16, 32 stages)
+    bit for bit against a float32 emulation of the decode contract (each
+    codeword rounded to float32, stages summed in float32 in order)."""
+    M, K, d, D, N = 32, 256, 128, 256, 600
+    say("paper rate deep stages", M, K, d, D, N)
+    X, w, seeds = synth.small_case(N, D, d, K, M, seed=26, dtype=np.float16)
+    G = D // d
+    cb = O.gsrq_train(X.astype(np.float64), w, d, K, M, 2, seeds)
+    gain = cb["gains"].astype(np.float32)
+    shape = cb["shapes"].astype(np.float32)
+    Xd, gd, sd = to_dev(X), to_dev(gain), to_dev(shape)
+    codes, res = B.encode(Xd, gd, sd, residual=True)
+    torch.cuda.synchronize()
+    k = unpack(codes, M, G, K)
+    R = X.astype(np.float64)
+    for m in range(M):
+        for g in range(G):
+            cols = slice(g * d, (g + 1) * d)
+            check_assignment(R[:, cols], gain[m, g], shape[m, g], k[:, m, g], f"m{m} g{g}")
+            kk = k[:, m, g]
+            R[:, cols] -= gain[m, g].astype(np.float64)[kk, None] * shape[m, g].astype(np.float64)[kk]
+    assert np.allclose(res.cpu().numpy().astype(np.float64), R, rtol=1e-5,
+                       atol=1e-6 * np.abs(X.astype(np.float64)).max())
+    for M_use in (12, 16, 32):
+        out = B.decode(codes, gd, sd, D, M_use, out_dtype=torch.float32)
+        torch.cuda.synchronize()
+        acc = np.zeros((N, D), np.float32)
+        for m in range(M_use):
+            for g in range(G):
+                kk = k[:, m, g]
+                acc[:, g * d:(g + 1) * d] += gain[m, g][kk, None] * shape[m, g][kk]
+        assert np.array_equal(out.cpu().numpy(), acc), f"decode prefix {M_use}"
+        assert B.bits_per_element(d, K, M_use) == pytest.approx(M_use * 8 / 128)
+
+
 @pytest.mark.parametrize("M,K,d,D,N", [
     (2, 256, 16, 64, 1000),     # LDS table, 16-element entries
     (1, 1024, 8, 32, 333),      # LDS table, K > 256
