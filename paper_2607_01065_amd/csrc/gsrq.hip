@@ -938,9 +938,13 @@ __global__ void decode_global_kernel(DecodeArgs a) {
       const size_t cb = (size_t)m * a.G + g;
       const float gk = a.gain[cb * a.K + k];
       const float* s = a.shape + (cb * a.K + k) * a.d;
+      {
+        // the codeword g s is rounded to float32 before the stage sum
+#pragma clang fp contract(off)
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (j < a.d) acc[j] += gk * s[j];
+        for (int j = 0; j < 8; ++j)
+          if (j < a.d) acc[j] += gk * s[j];
+      }
     }
     TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * a.d;
     for (int j = 0; j < a.d; ++j) dst[j] = (TO)acc[j];

@@ -103,7 +103,8 @@ def test_encode_multi_stage_teacher_forced(M, K, d, D):
 
 
 @pytest.mark.parametrize("M,K,d,D,N", [(1, 256, 8, 64, 1000), (3, 16, 4, 24, 333), (2, 4096 // 16, 8, 16, 50),
-                                        (3, 8, 2, 6, 2000), (2, 32, 4, 40, 5000), (1, 256, 8, 1024, 4100)])
+                                        (3, 8, 2, 6, 2000), (2, 32, 4, 40, 5000), (1, 256, 8, 1024, 4100),
+                                        (12, 256, 8, 32, 300)])
 def test_decode(M, K, d, D, N):
     say("decode", M, K, d, D, N)
     G = D // d
@@ -120,8 +121,14 @@ def test_decode(M, K, d, D, N):
         torch.cuda.synchronize()
         o32 = out32.cpu().numpy().astype(np.float64)
         assert np.allclose(o32, ref, rtol=1e-6, atol=1e-6 * np.abs(ref).max())
-        if M_use == 1:
-            assert np.array_equal(out32.cpu().numpy(), ref.astype(np.float32))
+        # bit for bit against the decode contract: each codeword rounded to
+        # float32, stages summed in float32 in order
+        acc = np.zeros((N, D), np.float32)
+        for m in range(M_use):
+            for g in range(G):
+                kk = codes[:, m, g]
+                acc[:, g * d:(g + 1) * d] += gain[m, g][kk, None] * shape[m, g][kk]
+        assert np.array_equal(out32.cpu().numpy(), acc)
         o16 = out16.cpu().numpy().astype(np.float64)
         ulp = np.spacing(np.abs(ref).astype(np.float16)).astype(np.float64)
         assert np.all(np.abs(o16 - ref) <= ulp + 1e-6 * np.abs(ref).max())

@@ -149,8 +149,14 @@ def test_wide_decode(M, K, d, D, N):
         torch.cuda.synchronize()
         o32 = out32.cpu().numpy().astype(np.float64)
         assert np.allclose(o32, ref, rtol=1e-6, atol=1e-6 * np.abs(ref).max())
-        if M_use == 1:
-            assert np.array_equal(out32.cpu().numpy(), ref.astype(np.float32))
+        # bit for bit against the decode contract (float32 codewords, summed
+        # in float32 in stage order)
+        acc = np.zeros((N, D), np.float32)
+        for m in range(M_use):
+            for g in range(G):
+                kk = codes[:, m, g]
+                acc[:, g * d:(g + 1) * d] += gain[m, g][kk, None] * shape[m, g][kk]
+        assert np.array_equal(out32.cpu().numpy(), acc)
         o16 = out16.cpu().numpy().astype(np.float64)
         ulp = np.spacing(np.abs(ref).astype(np.float16)).astype(np.float64)
         assert np.all(np.abs(o16 - ref) <= ulp + 1e-6 * np.abs(ref).max())
