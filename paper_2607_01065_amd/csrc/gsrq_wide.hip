@@ -48,7 +48,9 @@ constexpr int W_ACC_LDS_BYTES = 98304;          // accumulator slice in LDS
 constexpr int W_ACC_BATCH = 4;                  // rows per thread per collection pass
 constexpr int W_ACC_MEMBERS = 8;                // member rows per lane group in flight
 constexpr int W_BUCKET_KMAX = 16384;            // codewords the bucketing histogram holds
-constexpr int W_DEC_TABLE_BYTES = 65536;
+constexpr int W_DEC_TABLE_BYTES = 131072;        // codeword table per workgroup, at most
+constexpr int W_DEC_LDS_BYTES = 152 * 1024;      // table + staged code words
+constexpr int W_DEC_CODE_PT = 16;               // staged code words per thread, at most
 constexpr int W_DEC_THREADS = 1024;
 
 enum { W_TRAIN = 0, W_ENCODE = 1 };
@@ -1179,6 +1181,8 @@ struct WDecArgs {
   void* out;
   int gpw, gblocks, vec;
   int64_t rows_per_wg;
+  int tab_bytes;          // LDS kernel: table bytes (staged code words follow)
+  int vshape;             // shape rows 16-byte aligned (vector table fill)
 };
 
 __device__ __forceinline__ int w_read_code(const uint32_t* cr, int64_t bit, int b) {
@@ -1212,14 +1216,74 @@ template <> __device__ __forceinline__ void w_store8<float>(float* p, const floa
   }
 }
 
+// Code words of subspaces [g0, g0 + ngr) of stage m within a row: the
+// word range [lo, lo + n) holding their b-bit fields.
+__device__ __forceinline__ void w_stage_words(int m, int G, int g0, int ngr, int b, int& lo,
+                                              int& n) {
+  const int64_t first = ((int64_t)m * G + g0) * b;
+  const int64_t last = first + (int64_t)ngr * b - 1;
+  lo = (int)(first >> 5);
+  n = (int)(last >> 5) - lo + 1;
+}
+
+// Swizzled decode-table entries: EW elements of type TT in NCH 16-byte
+// chunks, chunk c of entry e in slot (c + e / (16 / NCH)) mod NCH.
+template <typename TT, int EW> struct WTab {
+  static constexpr int NCH = EW * (int)sizeof(TT) / 16;   // 16-byte chunks per entry
+  static constexpr int PER = 16 / (int)sizeof(TT);        // elements per chunk
+  static constexpr int SH = NCH == 4 ? 2 : (NCH == 2 ? 3 : 4);  // log2(16 / NCH)
+};
+template <typename TT, int EW>
+__device__ __forceinline__ void w_tab_put(TT* tab, int e, const float (&v)[EW]) {
+  using W = WTab<TT, EW>;
+  u4* base = (u4*)tab + (size_t)e * W::NCH;
+#pragma unroll
+  for (int c = 0; c < W::NCH; ++c) {
+    const int slot = (c + (e >> W::SH)) & (W::NCH - 1);
+    u4 chunk;
+    if (sizeof(TT) == 2) {
+      h8 hv;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) hv[j] = (_Float16)v[c * 8 + j];
+      chunk = __builtin_bit_cast(u4, hv);
+    } else {
+      chunk = (u4){__float_as_uint(v[c * 4]), __float_as_uint(v[c * 4 + 1]),
+                   __float_as_uint(v[c * 4 + 2]), __float_as_uint(v[c * 4 + 3])};
+    }
+    base[slot] = chunk;
+  }
+}
+template <typename TT, int EW>
+__device__ __forceinline__ void w_tab_add(const TT* tab, int e, float (&acc)[EW]) {
+  using W = WTab<TT, EW>;
+  const u4* base = (const u4*)tab + (size_t)e * W::NCH;
+#pragma unroll
+  for (int c = 0; c < W::NCH; ++c) {
+    const u4 chunk = base[(c + (e >> W::SH)) & (W::NCH - 1)];
+    if (sizeof(TT) == 2) {
+      const h8 hv = __builtin_bit_cast(h8, chunk);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) acc[c * 8 + j] += (float)hv[j];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[c * 4 + j] += __uint_as_float(chunk[j]);
+    }
+  }
+}
+
 // Gather-sum decoder with the codeword table (g s, float32 or, for one
 // float16 stage, float16) of `gpw` subspaces in LDS; entries of EW = 8 C
-// elements.  One thread per (row, subspace), subspace fastest.
+// elements.  One thread per (row, subspace), subspace fastest.  The code
+// words of the workgroup's rows and subspaces are staged in LDS with the
+// table ([rows][words of stage 0, stage 1, ...]), so the output loop issues
+// no global loads (a wait for a load would also wait for the stores issued
+// before it).
 template <typename TO, typename TT, int C>
 __global__ void __launch_bounds__(W_DEC_THREADS) w_decode_lds_kernel(WDecArgs a) {
   extern __shared__ __align__(16) unsigned char wdec_smem[];
   constexpr int EW = 8 * C;
   TT* tab = (TT*)wdec_smem;
+  uint32_t* cwl = (uint32_t*)(wdec_smem + a.tab_bytes);
   const int gpw = a.gpw;
   const int id = blockIdx.x;
   const int xcd = id % 8, slot = id / 8;
@@ -1228,53 +1292,106 @@ __global__ void __launch_bounds__(W_DEC_THREADS) w_decode_lds_kernel(WDecArgs a)
   const int64_t r_begin = (int64_t)rc * a.rows_per_wg;
   if (r_begin >= a.N) return;
   const int64_t r_end = min(a.N, r_begin + a.rows_per_wg);
+  const int nrows = (int)(r_end - r_begin);
   const int g0 = gb * gpw;
   const int ngr = min(gpw, a.G - g0);
-  const int K = a.K, M = a.M_use, d = a.d;
+  const int K = a.K, M = a.M_use, d = a.d, G = a.G, b = a.b;
   const int tid = threadIdx.x;
+  // staged code words per row (host-checked: nrows * rs <= W_DEC_CODE_PT * W_DEC_THREADS)
+  int rs = 0;
+  for (int m = 0; m < M; ++m) {
+    int lo, n;
+    w_stage_words(m, G, g0, ngr, b, lo, n);
+    rs += n;
+  }
+  const int ncw = nrows * rs;
+  const uint32_t* crow = a.codes + r_begin * a.words;
+  uint32_t cw[W_DEC_CODE_PT];
+#pragma unroll
+  for (int q = 0; q < W_DEC_CODE_PT; ++q) {
+    if (q * W_DEC_THREADS < ncw) {         // uniform per q
+      const int e = min(q * W_DEC_THREADS + tid, ncw - 1);
+      const int row = e / rs;
+      int j = e - row * rs, m = 0, lo, n;
+      w_stage_words(0, G, g0, ngr, b, lo, n);
+      while (j >= n) {
+        j -= n;
+        ++m;
+        w_stage_words(m, G, g0, ngr, b, lo, n);
+      }
+      cw[q] = crow[(int64_t)row * a.words + lo + j];
+    }
+  }
+  // table fill: entry e = (gi M + m) K + k holds g s of codeword k, as NCH
+  // 16-byte chunks; chunk c sits in slot (c + e / (16 / NCH)) mod NCH, so
+  // entries that share LDS banks (e mod 16/NCH) differ in which chunk they
+  // keep where, and random lookups spread over all bank groups
   const int entries = ngr * M * K;
   for (int e = tid; e < entries; e += W_DEC_THREADS) {
-    const int k = e & (K - 1), q2 = e >> a.b;
+    const int k = e & (K - 1), q2 = e >> b;
     const int m = q2 % M, gi = q2 / M;
-    const size_t cb = (size_t)m * a.G + g0 + gi;
+    const size_t cb = (size_t)m * G + g0 + gi;
     const float gk = a.gain[cb * K + k];
     const float* sv = a.shape + (cb * K + k) * d;
+    float v[EW];
+    if (d == EW && a.vshape) {
 #pragma unroll
-    for (int j = 0; j < EW; ++j) tab[(size_t)e * EW + j] = (TT)(j < d ? gk * sv[j] : 0.f);
+      for (int j = 0; j < EW; j += 4) {
+        const f4 t = *(const f4*)(sv + j);
+        v[j] = t[0]; v[j + 1] = t[1]; v[j + 2] = t[2]; v[j + 3] = t[3];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < EW; ++j) v[j] = j < d ? sv[j] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < EW; ++j) v[j] *= gk;
+    w_tab_put<TT, EW>(tab, e, v);
+  }
+#pragma unroll
+  for (int q = 0; q < W_DEC_CODE_PT; ++q) {
+    const int e = q * W_DEC_THREADS + tid;
+    if (e < ncw) cwl[e] = cw[q];
   }
   __syncthreads();
   const int gi = tid % gpw;
   if (gi >= ngr) return;
   const int rstep = W_DEC_THREADS / gpw;
   const int g = g0 + gi;
-  const TT* tg = tab + (size_t)gi * M * K * EW;
   constexpr int RBATCH = C == 1 ? 4 : 2;    // rows in flight per thread (no spills)
-  for (int64_t r0 = r_begin + tid / gpw; r0 < r_end; r0 += (int64_t)RBATCH * rstep) {
+  for (int r0 = tid / gpw; r0 < nrows; r0 += RBATCH * rstep) {
     float acc[RBATCH][EW];
 #pragma unroll
     for (int q = 0; q < RBATCH; ++q)
 #pragma unroll
       for (int j = 0; j < EW; ++j) acc[q][j] = 0.f;
+    int off = 0;                            // staged words of the stages before m
     for (int m = 0; m < M; ++m) {
+      int lo, n;
+      w_stage_words(m, G, g0, ngr, b, lo, n);
+      const int p = (int)(((int64_t)m * G + g) * b - (int64_t)lo * 32);
+      const int wi = off + (p >> 5), sh = p & 31;
+      const bool two = sh + b > 32;
       int k[RBATCH];
 #pragma unroll
       for (int q = 0; q < RBATCH; ++q) {
-        int64_t row = r0 + (int64_t)q * rstep;
-        row = row < r_end ? row : r_begin;    // in range; its result is not stored
-        k[q] = w_read_code(a.codes + row * a.words, ((int64_t)m * a.G + g) * a.b, a.b);
+        int row = r0 + q * rstep;
+        row = row < nrows ? row : 0;        // in range; its result is not stored
+        const uint32_t* w = cwl + row * rs + wi;
+        uint64_t v = w[0];
+        if (two) v |= (uint64_t)w[1] << 32;
+        k[q] = (int)((v >> sh) & ((1ull << b) - 1));
       }
 #pragma unroll
-      for (int q = 0; q < RBATCH; ++q) {
-        const TT* c = tg + ((size_t)m * K + k[q]) * EW;
-#pragma unroll
-        for (int j = 0; j < EW; ++j) acc[q][j] += (float)c[j];
-      }
+      for (int q = 0; q < RBATCH; ++q)
+        w_tab_add<TT, EW>(tab, (gi * M + m) * K + k[q], acc[q]);
+      off += n;
     }
 #pragma unroll
     for (int q = 0; q < RBATCH; ++q) {
-      const int64_t row = r0 + (int64_t)q * rstep;
-      if (row >= r_end) break;
-      TO* dst = (TO*)a.out + row * a.ldo + (int64_t)g * d;
+      const int row = r0 + q * rstep;
+      if (row >= nrows) break;
+      TO* dst = (TO*)a.out + (r_begin + row) * a.ldo + (int64_t)g * d;
 #pragma unroll
       for (int c8 = 0; c8 < C; ++c8)
         w_store8<TO>(dst + 8 * c8, acc[q] + 8 * c8, a.vec != 0, min(8, d - 8 * c8));
@@ -1762,6 +1879,7 @@ gsrq_status decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_use, co
   // vector stores, and (gather kernel) vector codeword loads
   a.vec = ((uintptr_t)Xhat % 16 == 0) && ((ldo * esz) % 16 == 0) && (s->d % 8 == 0) &&
           ((uintptr_t)shape % 16 == 0);
+  a.vshape = ((uintptr_t)shape % 16 == 0) && (s->d % 4 == 0);
   const int C = w_cwidth(s->d);
   TimedLaunch tl(GSRQ_KERNEL_DECODE, st);
   const bool half_tab = M_use == 1 && out_dtype == GSRQ_F16;
@@ -1771,14 +1889,42 @@ gsrq_status decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_use, co
     while (gpw * 2 <= 64 && gpw * 2 * per_group <= W_DEC_TABLE_BYTES && gpw < a.G) gpw *= 2;
     a.gpw = gpw;
     a.gblocks = (a.G + gpw - 1) / gpw;
+    // staged code words per row: the most any subspace block needs
+    int64_t rs = 1;
+    for (int gb = 0; gb < a.gblocks; ++gb) {
+      const int64_t g0 = (int64_t)gb * gpw, ngr = std::min<int64_t>(gpw, a.G - g0);
+      int64_t n = 0;
+      for (int m = 0; m < M_use; ++m) {
+        const int64_t first = (m * (int64_t)a.G + g0) * a.b, last = first + ngr * a.b - 1;
+        n += (last >> 5) - (first >> 5) + 1;
+      }
+      rs = std::max(rs, n);
+    }
+    a.tab_bytes = (int)(gpw * per_group);
+    // code words fill the LDS the table leaves, up to W_DEC_CODE_PT per thread
+    const int64_t code_words = std::min<int64_t>(
+        (int64_t)W_DEC_CODE_PT * W_DEC_THREADS, ((int64_t)W_DEC_LDS_BYTES - a.tab_bytes) / 4);
+    const int64_t max_rows = code_words / rs;
+    if (max_rows < 1) return GSRQ_E_UNSUPPORTED;
     int64_t rchunks = (256 + a.gblocks - 1) / a.gblocks;
     if (rchunks * 256 > s->N) rchunks = (s->N + 255) / 256;
     if (rchunks < 1) rchunks = 1;
     a.rows_per_wg = (s->N + rchunks - 1) / rchunks;
+    if (a.rows_per_wg > max_rows) a.rows_per_wg = max_rows;
     rchunks = (s->N + a.rows_per_wg - 1) / a.rows_per_wg;
+    if (8 * a.gblocks * ((rchunks + 7) / 8) > INT32_MAX) return GSRQ_E_UNSUPPORTED;
     const int blocks = (int)(8 * a.gblocks * ((rchunks + 7) / 8));
-    const size_t lds = (size_t)gpw * per_group;
-#define W_DEC(TO, TT, CC) w_decode_lds_kernel<TO, TT, CC><<<blocks, W_DEC_THREADS, lds, st>>>(a)
+    const size_t lds = (size_t)a.tab_bytes + (size_t)a.rows_per_wg * rs * sizeof(uint32_t);
+    gsrq_status e = GSRQ_OK;
+#define W_DEC(TO, TT, CC)                                                                    \
+  do {                                                                                       \
+    if (lds > 65536 && hipFuncSetAttribute((const void*)w_decode_lds_kernel<TO, TT, CC>,     \
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,       \
+                                           (int)lds) != hipSuccess)                          \
+      e = GSRQ_E_HIP;                                                                        \
+    else                                                                                     \
+      w_decode_lds_kernel<TO, TT, CC><<<blocks, W_DEC_THREADS, lds, st>>>(a);                \
+  } while (0)
     if (C == 1) {
       if (half_tab) W_DEC(_Float16, _Float16, 1);
       else if (out_dtype == GSRQ_F16) W_DEC(_Float16, float, 1);
@@ -1788,6 +1934,7 @@ gsrq_status decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_use, co
       else if (out_dtype == GSRQ_F16) W_DEC(_Float16, float, 2);
       else W_DEC(float, float, 2);
     }
+    if (e) return e;
 #undef W_DEC
   } else {
     const int cg = w_groups(s->d);
