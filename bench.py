@@ -184,6 +184,45 @@ def full_cache(args, wl):
     print(json.dumps(out), flush=True)
 
 
+def extra_paths(B, cache, wl, dev, reps=50):
+    """Measured after the timed region, outside `value`: per-token weights
+    from gradient rows of the layer's shape (Sec. 5.3, Appendix B), and the
+    encode latency of a few appended tokens with the layer's trained codebook
+    (the per-step append of autoregressive decoding)."""
+    import torch
+
+    import synth
+    out = {}
+    G = torch.from_numpy(synth.gradient_rows(wl.N, wl.D, seed=1)).to(dev)
+    B.row_weights(G)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        B.row_weights(G)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / reps * 1e3
+    out["row_weights"] = {"us": us, "tokens": wl.N, "grad_GBps": G.numel() * 2 / (us * 1e-6) / 1e9}
+    del G
+    app = {}
+    for n in (1, 8, 64):
+        X = cache["X"][:n].contiguous()
+        codes = torch.empty((n, cache["codes"].shape[1]), dtype=torch.int32, device=dev)
+        ws = torch.empty(B.encode_workspace_bytes(n, wl.D, wl.d, wl.K, wl.M), dtype=torch.uint8,
+                         device=dev)
+        B.encode(X, cache["gain"], cache["shape"], codes=codes, workspace=ws)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            B.encode(X, cache["gain"], cache["shape"], codes=codes, workspace=ws)
+        e1.record()
+        torch.cuda.synchronize()
+        app[str(n)] = e0.elapsed_time(e1) / reps * 1e3
+    out["append_encode_us"] = app
+    return out
+
+
 def breakdown(B, step):
     """Per-kernel event times of one extra step (every kind recorded)."""
     import torch
@@ -316,6 +355,7 @@ def main():
                                   "note": "argmin epilogue: one VALU lane-op per score is the "
                                           "floor; peak = 256 CU x 64 lanes x 2.4 GHz"}},
     }
+    out.update(extra_paths(B, caches[0], wl, dev))
     if args.copy_ref_mib > 0:
         n = args.copy_ref_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)

@@ -192,6 +192,30 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes,
                         void* Xhat, gsrq_dtype out_dtype, int64_t ldo,
                         void* stream);
 
+/*
+ * gsrq_row_weights -- per-token weights of weighted GSKM (Sec. 5.3,
+ * Appendix B): w_i = ||g_i||_2, the l2 norm of token i's gradient row, then
+ * the log smoothing  w~_i = log(1 + lambda w_i),  lambda = tau /
+ * (median(w) + 1e-8)  (the paper selects tau = 1).  The median is exact
+ * (selection over the float32 norms); for even N it is the mean of the two
+ * middle values.  The result feeds gsrq_train_stage's w.
+ *
+ *  grad, dtype, ldg  [N][ldg] gradient rows (ldg >= D), float16 or float32;
+ *                    or NULL, in which case norms holds the N norms on entry
+ *                    (non-negative, finite).
+ *  N, D              rows (1 <= N <= 2^31 - 1) and row length (D >= 1 when
+ *                    grad is given).
+ *  tau               target median, finite and > 0.
+ *  norms             [N] float32: output ||g_i||_2 (input when grad is NULL).
+ *  w                 [N] float32 output, the smoothed weights.
+ *  stats             [2] float64 output {median, lambda}.
+ * All arrays are device memory; nothing else is written.  Arguments are
+ * validated before any HIP call (GSRQ_E_ARG).
+ */
+gsrq_status gsrq_row_weights(const void* grad, gsrq_dtype dtype, int64_t N, int32_t D,
+                             int64_t ldg, float tau, float* norms, float* w, double* stats,
+                             void* stream);
+
 /* Kernel kinds reported by the optional launch timing below. */
 enum {
   GSRQ_KERNEL_ASSIGN = 0,     /* fused assignment + weighted accumulation */

@@ -1,8 +1,9 @@
-// Private header shared by the two kernel families of libgsrq (subvectors of
-// d <= 8 in gsrq.hip, wider subvectors in gsrq_wide.hip): operand types, the
+// Private header shared by the translation units of libgsrq (subvectors of
+// d <= 8 in gsrq.hip, wider subvectors in gsrq_wide.hip, per-token weights in
+// gsrq_weights.hip): operand types, the
 // scaling constants of the MFMA distance contraction, small device helpers
 // and host-side launch plumbing.  Everything here has internal linkage except
-// the launch-timing state, which both translation units share.
+// the launch-timing state, which every translation unit shares.
 #ifndef GSRQ_COMMON_H
 #define GSRQ_COMMON_H
 

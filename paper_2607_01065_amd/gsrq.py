@@ -66,6 +66,9 @@ def load_library(path: str = LIB_PATH):
     lib.gsrq_decode.restype = ctypes.c_int
     lib.gsrq_decode.argtypes = [SP, _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_int,
                                 ctypes.c_int64, _vp]
+    lib.gsrq_row_weights.restype = ctypes.c_int
+    lib.gsrq_row_weights.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_int64, ctypes.c_float, _vp, _vp, _vp, _vp]
     lib.gsrq_timing_enable.restype = ctypes.c_int
     lib.gsrq_timing_enable.argtypes = [ctypes.c_int]
     lib.gsrq_timing_enable_kinds.restype = ctypes.c_int
@@ -277,3 +280,28 @@ def decode(codes, gain, shape, D, M_use=None, *, out_dtype=None, out=None, strea
                          _ptr(out), _dtype_code(out), out.stride(0), _stream_handle(stream))
     _check(st, "gsrq_decode")
     return out
+
+
+def row_weights(grad=None, *, norms=None, tau=1.0, stream=None):
+    """Per-token weights of Sec. 5.3 / Appendix B (see gsrq_row_weights):
+    from gradient rows grad [N, D] (float16/float32), or from precomputed
+    norms [N] float32 when grad is None.  Returns (w [N], norms [N],
+    stats [2] float64 = (median, lambda))."""
+    torch = _torch()
+    lib = load_library()
+    if grad is not None:
+        N, D, ldg = _rows(grad)
+        dev = grad.device
+        if norms is None:
+            norms = torch.empty(N, dtype=torch.float32, device=dev)
+        dt = _dtype_code(grad)
+    else:
+        if norms is None:
+            raise ValueError("either grad or norms is needed")
+        N, D, ldg, dev, dt = norms.shape[0], 0, 0, norms.device, GSRQ_F32
+    w = torch.empty(N, dtype=torch.float32, device=dev)
+    stats = torch.empty(2, dtype=torch.float64, device=dev)
+    st = lib.gsrq_row_weights(_ptr(grad), dt, N, D, ldg, float(tau), _ptr(norms), _ptr(w),
+                              _ptr(stats), _stream_handle(stream))
+    _check(st, "gsrq_row_weights")
+    return w, norms, stats

@@ -197,3 +197,18 @@ def make_kv_device(wl: Workload, layer: int = 0, seed: int = 0, device="cuda",
     w_k = torch.empty(N, device=device).log_normal_(0.0, 1.0, generator=gen)
     w_v = torch.empty(N, device=device).log_normal_(0.0, 1.0, generator=gen)
     return keys, values, w_k, w_v
+
+
+def gradient_rows(N: int, D: int, seed: int = 0, sigma: float = 1.5,
+                  dtype=np.float16) -> np.ndarray:
+    """Synthetic per-token gradient rows g_i = s_i z_i with z_i ~ N(0, I_D)
+    and a heavy-tailed scale s_i ~ lognormal(0, sigma): stand-ins for the
+    gradients of the loss with respect to the KV activations (Sec. 5.3),
+    whose norms the paper reports as heavy-tailed (max/median > 400, and
+    below 10 after the log smoothing, which with tau = 1 also bounds the raw
+    ratio below 2^10 - 1).  sigma = 1.5 gives max/median ~ 700 at 32768
+    rows."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, N, D, 77])))
+    s = rng.lognormal(0.0, sigma, size=N).astype(np.float32)
+    z = rng.standard_normal((N, D), dtype=np.float32)
+    return (s[:, None] * z).astype(dtype)

@@ -141,3 +141,18 @@ def test_encode_decode_validation_before_any_hip_call():
     assert dec(out=None) == B.GSRQ_E_ARG
     assert dec(ldo=4) == B.GSRQ_E_ARG
     assert dec(dt=5) == B.GSRQ_E_ARG
+
+
+def test_row_weights_validation_before_any_hip_call():
+    lib = B.load_library()
+    f = lib.gsrq_row_weights
+    D = DUMMY
+    assert f(D, B.GSRQ_F16, 0, 8, 8, 1.0, D, D, D, None) == B.GSRQ_E_ARG         # N < 1
+    assert f(D, B.GSRQ_F16, 10, 8, 4, 1.0, D, D, D, None) == B.GSRQ_E_ARG        # ldg < D
+    assert f(D, B.GSRQ_F16, 10, 0, 8, 1.0, D, D, D, None) == B.GSRQ_E_ARG        # D < 1
+    assert f(D, 7, 10, 8, 8, 1.0, D, D, D, None) == B.GSRQ_E_ARG                 # dtype
+    assert f(D, B.GSRQ_F16, 10, 8, 8, 0.0, D, D, D, None) == B.GSRQ_E_ARG        # tau <= 0
+    assert f(D, B.GSRQ_F16, 10, 8, 8, float("inf"), D, D, D, None) == B.GSRQ_E_ARG
+    assert f(D, B.GSRQ_F16, 10, 8, 8, 1.0, None, D, D, None) == B.GSRQ_E_ARG     # norms
+    assert f(D, B.GSRQ_F16, 10, 8, 8, 1.0, D, None, D, None) == B.GSRQ_E_ARG     # w
+    assert f(D, B.GSRQ_F16, 10, 8, 8, 1.0, D, D, None, None) == B.GSRQ_E_ARG     # stats

@@ -453,3 +453,17 @@ def test_kmeans_assign_matches_brute_force():
             if best is None or dd < best:
                 best, bk = dd, k
         assert a[i] == bk
+
+
+def test_log_weight_tames_heavy_tailed_norms():
+    """Sec. 5.3: gradient norms with max/median > 400 come out of the log
+    smoothing (tau = 1) with max/median < 10.  Heavy-tailed synthetic norms
+    (the stand-in gradient rows of the benchmark inputs)."""
+    import synth
+    G = synth.gradient_rows(32768, 64, seed=7, dtype=np.float32)
+    n = np.linalg.norm(G.astype(np.float64), axis=1)
+    w = O.log_weight(n, tau=1.0)
+    assert n.max() / np.median(n) > 400
+    assert w.max() / np.median(w) < 10
+    # median maps to log(2) exactly in exact arithmetic (lambda * median = 1)
+    assert np.median(w) == pytest.approx(math.log(2.0), rel=1e-6)
