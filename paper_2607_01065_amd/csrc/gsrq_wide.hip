@@ -48,6 +48,7 @@ constexpr int W_ACC_LDS_BYTES = 98304;          // accumulator slice in LDS
 constexpr int W_ACC_BATCH = 4;                  // rows per thread per collection pass
 constexpr int W_ACC_MEMBERS = 8;                // member rows per lane group in flight
 constexpr int W_BUCKET_KMAX = 16384;            // codewords the bucketing histogram holds
+constexpr int W_FUSED_ROUNDS = 4;               // row rounds a stage-fused encode workgroup keeps
 constexpr int W_DEC_TABLE_BYTES = 131072;        // codeword table per workgroup, at most
 constexpr int W_DEC_LDS_BYTES = 152 * 1024;      // table + staged code words
 constexpr int W_DEC_CODE_PT = 16;               // staged code words per thread, at most
@@ -467,8 +468,6 @@ __device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[W_
   }
 }
 
-// Writes code k into the b-bit field at `bit` of a row's words (zeroed
-// beforehand): byte and half-word fields are stored, others OR'd in.
 // Four consecutive elements of a stage-input row as float32 (vector load:
 // 16 bytes of float32, 8 bytes of float16).
 __device__ __forceinline__ f4 w_load4(const float* p) { return *(const f4*)p; }
@@ -507,6 +506,8 @@ __device__ __forceinline__ float w_residual(const T* xp, const float* sk, float 
   return dist;
 }
 
+// Writes code k into the b-bit field at `bit` of a row's words (zeroed
+// beforehand): byte and half-word fields are stored, others OR'd in.
 __device__ __forceinline__ void w_put_code(uint32_t* wp, int64_t bit, int b, int k) {
   if (b == 8) {
     ((uint8_t*)wp)[bit >> 3] = (uint8_t)k;
@@ -724,6 +725,196 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
         double s = 0.0;
         for (int w = 0; w < W_WAVES; ++w) s += red_obj[w];
         a.obj[(size_t)g * a.nwg + rc] = s;
+      }
+    }
+  }
+}
+
+// Stage-fused encode for narrow wide rows (d <= 16) with resident fragment
+// tables: a workgroup keeps the float32 residuals of its W_FUSED_ROUNDS x
+// W_ROWS rows in registers (lane half h holds elements [8h, 8h + 8) of its
+// row) through all M stages.  Per stage the stage's table is copied into
+// LDS and every round is scored (float32 operand path, packed-key argmin);
+// rows the key cannot decide are re-scored in float64 by the whole wave
+// (eq. 5 form, every codeword; rare at these shapes); the code is written
+// and the winning codeword fetched, and after the stage's last round the
+// codewords are subtracted (the fetches overlap the later rounds' scoring).
+// The residual leaves the registers only at the end, when it is requested.
+struct WFusedArgs {
+  const void* x;          // [N][ldx] input rows
+  int64_t ldx, N;
+  int d, K, G, M, tiles, QF, b, words;
+  const u4* frag;         // [M G][tiles][QF][64]
+  const int* sig;         // [M G]
+  const float* gain;      // [M][G][K]
+  const float* shape;     // [M][G][K][d]
+  uint32_t* codes;        // [N][words], zeroed beforehand, or null
+  float* res_out;         // [N][G d] or null
+  int res_vec;            // res_out 16-byte aligned
+  int svec;               // shape 16-byte aligned
+  int nwg, map_xcd, lg;
+};
+
+template <typename T, int C>
+__global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_kernel(WFusedArgs a) {
+  extern __shared__ __align__(16) u4 wtab[];
+  static_assert(C <= 2, "one 16-element group pair per row");
+  constexpr int R = W_FUSED_ROUNDS;
+  constexpr int QU = w_frags(C);
+  int g, rc;
+  {
+    const int id = blockIdx.x;
+    if (a.map_xcd) {
+      const int xcd = id & 7, slot = id >> 3, gpx = a.G >> 3;
+      const int j = slot % gpx;
+      rc = slot / gpx;
+      g = ((j / a.lg) * 8 + xcd) * a.lg + (j % a.lg);
+    } else {
+      g = id % a.G;
+      rc = id / a.G;
+    }
+  }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i = lane & 31, h = lane >> 5;
+  const int d = a.d, K = a.K, G = a.G;
+  const T* X = (const T*)a.x;
+  float r[R][8];
+  int64_t rows[R];
+  const bool xvec = ((a.ldx * (int64_t)sizeof(T)) % 16 == 0) && (((uintptr_t)X) % 16 == 0);
+#pragma unroll
+  for (int rd = 0; rd < R; ++rd) {
+    rows[rd] = ((int64_t)rc * R + rd) * W_ROWS + (int64_t)wave * RB + i;
+    const bool valid = rows[rd] < a.N;
+    const T* xp = X + (valid ? rows[rd] : 0) * a.ldx + (int64_t)g * d;
+    WRaw<T, 1> raw;
+    raw.load(xp, d, xvec, h);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) r[rd][j] = raw.at(0, j, d, h, valid);
+  }
+  for (int m = 0; m < a.M; ++m) {
+    const int cb = m * G + g;
+    const int ex = a.sig[cb];
+    const float* gcb = a.gain + (size_t)cb * K;
+    const float* scb = a.shape + (size_t)cb * K * d;
+    {
+      const u4* ftab = a.frag + (size_t)cb * a.tiles * a.QF * 64;
+      const int n = a.tiles * QU * 64;
+      __syncthreads();                      // the previous stage's table is no longer read
+      for (int e = tid; e < n; e += W_THREADS) {
+        const int t = e / (QU * 64), o = e - t * (QU * 64);
+        wtab[e] = ftab[(size_t)t * a.QF * 64 + o];
+      }
+      __syncthreads();
+    }
+    float gsel[R];
+    f4 ssel[R][2];
+#pragma unroll
+    for (int rd = 0; rd < R; ++rd) {
+      const int64_t row = rows[rd];
+      const bool valid = row < a.N;
+      WRaw<float, 1> raw;
+      raw.v[0] = (u4){__float_as_uint(r[rd][0]), __float_as_uint(r[rd][1]),
+                      __float_as_uint(r[rd][2]), __float_as_uint(r[rd][3])};
+      raw.v[1] = (u4){__float_as_uint(r[rd][4]), __float_as_uint(r[rd][5]),
+                      __float_as_uint(r[rd][6]), __float_as_uint(r[rd][7])};
+      u4 bx[1], blo[1], bias;
+      float rr;
+      bool need_exact;
+      w_make_b<float, 1>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact);
+      int best = 0x7fffffff, bt = 0;
+      for (int t = 0; t < a.tiles; t += 2) {
+        const u4* ta = wtab + (size_t)t * QU * 64 + lane;
+        const f16v c0 = w_tile<false, 1>(ta, bx, blo, bias);
+        if (t + 1 < a.tiles) {
+          const f16v c1 = w_tile<false, 1>(ta + QU * 64, bx, blo, bias);
+          w_take(w_tile_key(c0), t, best, bt);
+          w_take(w_tile_key(c1), t + 1, best, bt);
+        } else {
+          w_take(w_tile_key(c0), t, best, bt);
+        }
+      }
+      int kstar;
+      float dhat;
+      {
+        const int j = best & 15;
+        const int kidx = bt * CW + (j >> 2) * 8 + h * 4 + (j & 3);
+        const int hv = best >> 4;
+        const auto sh = __builtin_amdgcn_permlane32_swap(hv, hv, false, false);
+        const auto sk = __builtin_amdgcn_permlane32_swap(kidx, kidx, false, false);
+        const long long v0 = (long long)(int)sh[0] * 4294967296ll + (long long)(unsigned)sk[0];
+        const long long v1 = (long long)(int)sh[1] * 4294967296ll + (long long)(unsigned)sk[1];
+        const long long v = v0 < v1 ? v0 : v1;
+        dhat = __int_as_float((int)(v >> 32) << 4);
+        kstar = (int)(v & 0xffffffffll);
+      }
+      need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
+      unsigned long long fb = __ballot(valid && need_exact && h == 0);
+      while (fb) {
+        // the whole wave re-scores row L in float64: g^2 - 2 g s.x over all K
+        const int L = __ffsll((long long)fb) - 1;
+        fb &= fb - 1;
+        double xr[16];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          xr[j] = (double)__shfl(r[rd][j], L);
+          xr[8 + j] = (double)__shfl(r[rd][j], L + 32);
+        }
+        double bd = INFINITY;
+        int bk = 0x7fffffff;
+        for (int k = lane; k < K; k += 64) {
+          const double gk = (double)gcb[k];
+          double dot = 0.0;
+          for (int j = 0; j < d; ++j) dot = fma(xr[j], (double)scb[(size_t)k * d + j], dot);
+          const double dist = fma(-2.0 * gk, dot, gk * gk);
+          if (dist < bd) { bd = dist; bk = k; }
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+          const double od = __shfl_xor(bd, off);
+          const int ok = __shfl_xor(bk, off);
+          if (od < bd || (od == bd && ok < bk)) { bd = od; bk = ok; }
+        }
+        if (i == L) kstar = bk;
+      }
+      if (kstar >= K) kstar = K - 1;        // rows past N only
+      if (valid && h == 0 && a.codes)
+        w_put_code(a.codes + row * a.words, ((int64_t)m * G + g) * a.b, a.b, kstar);
+      // the codeword is fetched now and subtracted after the stage's last
+      // round, so the loads overlap the next rounds' scoring
+      const int e0 = 8 * h < d ? 8 * h : 0;   // d = 8: lane half 1 holds no elements
+      gsel[rd] = gcb[kstar] * ((8 * h < d) ? 1.f : 0.f);
+      const float* sp = scb + (size_t)kstar * d + e0;
+      if (a.svec) {
+        ssel[rd][0] = ((const f4*)sp)[0];
+        ssel[rd][1] = ((const f4*)sp)[1];
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          ssel[rd][0][j] = sp[j];
+          ssel[rd][1][j] = sp[4 + j];
+        }
+      }
+    }
+#pragma unroll
+    for (int rd = 0; rd < R; ++rd)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        r[rd][j] = fmaf(-gsel[rd], ssel[rd][0][j], r[rd][j]);
+        r[rd][4 + j] = fmaf(-gsel[rd], ssel[rd][1][j], r[rd][4 + j]);
+      }
+  }
+  if (a.res_out) {
+#pragma unroll
+    for (int rd = 0; rd < R; ++rd) {
+      const int64_t row = rows[rd];
+      if (row >= a.N || 8 * h >= d) continue;
+      float* dst = a.res_out + row * ((int64_t)G * d) + (int64_t)g * d + 8 * h;
+      if (a.res_vec) {
+        ((f4*)dst)[0] = (f4){r[rd][0], r[rd][1], r[rd][2], r[rd][3]};
+        ((f4*)dst)[1] = (f4){r[rd][4], r[rd][5], r[rd][6], r[rd][7]};
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dst[j] = r[rd][j];
       }
     }
   }
@@ -1630,11 +1821,33 @@ struct WEncWs {
   size_t frag, gmin, xcount, xrows, xchanged, xobj, sig, res0, res1, total;
 };
 
+// Several stages of narrow wide rows (d <= 16) with resident fragment
+// tables are encoded by the stage-fused kernel.
+bool w_fused(const gsrq_shape* s) {
+  if (s->M <= 1 || w_cwidth(s->d) > 2) return false;
+  return w_score_layout(s, 4, false).resident;
+}
+
 WEncWs w_encode_ws(const gsrq_shape* s) {
   WEncWs W;
   const int64_t G = s->D / s->d;
   const WLayout L = w_score_layout(s, 4, false);
   size_t off = 0;
+  if (w_fused(s)) {
+    // every stage's fragment table, per-codebook sigma state; no residual
+    // buffers and no deferred-row lists
+    const size_t ncb = (size_t)s->M * G;
+    W.frag = off; off = align256(off + ncb * L.frag_bytes);
+    W.gmin = off; off = align256(off + ncb * sizeof(float));
+    W.xcount = off; off = align256(off + ncb * sizeof(int));
+    W.xrows = off;
+    W.xchanged = off; off = align256(off + ncb * sizeof(int));
+    W.xobj = off; off = align256(off + ncb * sizeof(double));
+    W.sig = off; off = align256(off + ncb * sizeof(int));
+    W.res0 = W.res1 = off;
+    W.total = std::max(off, (size_t)256);
+    return W;
+  }
   W.frag = off; off = align256(off + (size_t)G * L.frag_bytes);
   W.gmin = off; off = align256(off + (size_t)G * sizeof(float));
   W.xcount = off; off = align256(off + (size_t)G * sizeof(int));
@@ -1847,6 +2060,32 @@ gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64
   gsrq_status e;
   if (codes && (e = fill_u32(codes, (size_t)s->N * words, 0u, st))) return e;
   const int C = w_cwidth(s->d);
+  if (w_fused(s)) {
+    // all stages' fragment tables, then one launch for every stage
+    if ((e = w_build_frags(gain, shape, s->d, s->K, C, s->M * G, 0, false, nullptr, G, sig, frag,
+                           XD, st)))
+      return e;
+    const WLayout L = w_score_layout(s, 4, false);
+    WFusedArgs a;
+    a.x = X; a.ldx = ldx; a.N = s->N; a.d = s->d; a.K = s->K; a.G = G; a.M = s->M;
+    a.tiles = L.tiles; a.QF = L.QF; a.b = log2i(s->K); a.words = words;
+    a.frag = frag; a.sig = sig; a.gain = gain; a.shape = shape; a.codes = codes;
+    a.res_out = residual; a.res_vec = ((uintptr_t)residual % 16) == 0;
+    a.svec = ((uintptr_t)shape % 16) == 0;
+    const int64_t row_rounds = (s->N + W_ROWS - 1) / W_ROWS;
+    a.nwg = (int)((row_rounds + W_FUSED_ROUNDS - 1) / W_FUSED_ROUNDS);
+    a.map_xcd = L.map_xcd; a.lg = L.lg;
+    const dim3 grid((unsigned)(G * a.nwg));
+    TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
+    if (x_dtype == GSRQ_F16) {
+      if (C == 1) w_encode_fused_kernel<_Float16, 1><<<grid, W_THREADS, L.lds, st>>>(a);
+      else w_encode_fused_kernel<_Float16, 2><<<grid, W_THREADS, L.lds, st>>>(a);
+    } else {
+      if (C == 1) w_encode_fused_kernel<float, 1><<<grid, W_THREADS, L.lds, st>>>(a);
+      else w_encode_fused_kernel<float, 2><<<grid, W_THREADS, L.lds, st>>>(a);
+    }
+    return launch_ok();
+  }
   for (int m = 0; m < s->M; ++m) {
     if ((e = w_build_frags(gain, shape, s->d, s->K, C, G, m * G, false, nullptr, G, sig, frag,
                            XD, st)))

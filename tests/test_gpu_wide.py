@@ -59,19 +59,36 @@ def test_wide_encode_single_stage(dtype, N, D, d, K):
     say("below-margin index differences:", below, "of", N * G)
 
 
-@pytest.mark.parametrize("dtype,M,K,d,D,N", [
-    (np.float32, 3, 64, 16, 48, 613),
-    (np.float16, 2, 256, 128, 256, 400),
-    (np.float16, 4, 16, 32, 64, 301),
+@pytest.mark.parametrize("dtype,M,K,d,D,N,exact_rows", [
+    (np.float32, 3, 64, 16, 48, 613, False),     # stage-fused kernel (d <= 16)
+    (np.float16, 4, 256, 16, 128, 2000, False),  # stage-fused, the rate-sweep shape
+    (np.float32, 3, 512, 8, 32, 700, None),      # stage-fused, d = 8 with K > 256
+    (np.float16, 3, 256, 16, 64, 900, True),     # stage-fused, rows re-scored in float64
+    (np.float16, 2, 256, 128, 256, 400, False),  # one launch per stage (d = 128)
+    (np.float16, 4, 16, 32, 64, 301, False),     # one launch per stage (d = 32)
 ])
-def test_wide_encode_multi_stage_teacher_forced(dtype, M, K, d, D, N):
-    """Stage m is checked on the residual the GPU's own earlier choices leave."""
-    say("wide encode multi stage", dtype.__name__, M, K, d, D, N)
+def test_wide_encode_multi_stage_teacher_forced(dtype, M, K, d, D, N, exact_rows):
+    """Stage m is checked on the residual the GPU's own earlier choices leave.
+    exact_rows: a quarter of the rows are set to stage-0 codewords, so their
+    stage-1 residual is zero (or float32 noise) and the key cannot decide
+    them: the float64 re-scoring path.  None: random codebooks instead of the
+    oracle's training (K > N / 2 leaves exactly coded rows whose zero
+    residuals cannot seed the next stage)."""
+    say("wide encode multi stage", dtype.__name__, M, K, d, D, N, exact_rows)
     X, w, seeds = synth.small_case(N, D, d, K, M, seed=22, dtype=dtype)
     G = D // d
-    cb = O.gsrq_train(X.astype(np.float64), w, d, K, M, 3, seeds)
-    gain = cb["gains"].astype(np.float32)
-    shape = cb["shapes"].astype(np.float32)
+    if exact_rows is None:
+        gain, shape = random_codebook(X, M, G, K, d, seed=28)
+    else:
+        cb = O.gsrq_train(X.astype(np.float64), w, d, K, M, 3, seeds)
+        gain = cb["gains"].astype(np.float32)
+        shape = cb["shapes"].astype(np.float32)
+    if exact_rows:
+        rng = _rng(27, N)
+        pick = rng.choice(N, size=N // 4, replace=False)
+        for g in range(G):
+            k = rng.integers(0, K, size=pick.size)
+            X[pick, g * d:(g + 1) * d] = (gain[0, g][k, None] * shape[0, g][k]).astype(dtype)
     codes, res = B.encode(to_dev(X), to_dev(gain), to_dev(shape), residual=True)
     torch.cuda.synchronize()
     k = unpack(codes, M, G, K)
