@@ -231,8 +231,9 @@ enum {
 
 /* Measurement hook, the library's only process state.  While enabled, every
  * launch of the kernels above is bracketed by two HIP events recorded on the
- * launch's stream.  Enabling clears earlier records.  Not thread-safe: enable,
- * run and read from one host thread. */
+ * launch's stream.  Enabling clears earlier records; switching off keeps them
+ * for gsrq_timing_read (launches enqueued while enabled stay recorded).  Not
+ * thread-safe: enable, run and read from one host thread. */
 gsrq_status gsrq_timing_enable(int on);
 
 /* As gsrq_timing_enable, restricted to the kernel kinds whose bit

@@ -50,6 +50,7 @@ constexpr int ENC_MAX_STAGES = 8;      // stages staged in LDS by one encode lau
 constexpr int KEY_BITS = 7;               // (tile, slot) bits packed into a key
 
 enum { MODE_INIT = 0, MODE_ITER = 1 };
+enum { UPD_NONE = 0, UPD_INIT = 1, UPD_ITER = 2 };   // update fused into an assignment launch
 
 // ---------------------------------------------------------------- helpers
 
@@ -402,8 +403,25 @@ struct AssignArgs {
   int64_t N;
   int d, K, G;
   const float* w;        // [N] or null
-  float* gain;           // [G][K]; updated in place by the update kernel
-  float* shape;          // [G][K][d]; likewise
+  const float* gain;     // [G][K] codebook to score with (no fused update)
+  const float* shape;    // [G][K][d]
+  // codebook update at the start of an assignment launch (upd != UPD_NONE)
+  // and in the update kernel: C_{t-1} is computed from the previous pass's
+  // partial sums and the codebook before it (old_*), written to new_* by
+  // the subspace's first chunk; the update kernel writes fin_* (the
+  // caller's arrays) and, for subspaces that stopped inside a fused update,
+  // copies their final codebook there from buf_*[iteration % 2]
+  int upd;
+  int upd_has_wxx;       // the previous pass accumulated sum w ||x||^2
+  const float* old_gain;
+  const float* old_shape;
+  float* new_gain;
+  float* new_shape;
+  float* fin_gain;
+  float* fin_shape;
+  const float* buf_gain[2];
+  const float* buf_shape[2];
+  int copy_done;
   uint16_t* assign;      // [G][N]
   int* done;             // [G] iteration at which the subspace stopped, 0 = running
   int* iters;            // [G] iterations run
@@ -422,56 +440,39 @@ struct AssignArgs {
 };
 
 // Codebook update of subspace g from the partial sums of all its chunks,
-// reduced in chunk order (the result does not depend on which workgroup
-// finishes last).  Initialisation: eq. (8) gains of the seed shapes.
-// Iteration: eqs. (7) and (8), plus the weighted objective of the
-// assignment just made, from the sufficient statistics of the codebook it
-// was made with:
+// reduced in chunk order (every workgroup that computes it gets the same
+// result).  Initialisation: eq. (8) gains of the seed shapes.  Iteration:
+// eqs. (7) and (8), plus the weighted objective of the assignment just made,
+// from the sufficient statistics of the codebook it was made with:
 //   sum_i w_i ||x_i - g s||^2 = sum_i w_i ||x_i||^2
 //                               - sum_k (2 g_k s_k . S_k - g_k^2 ||s_k||^2 W_k),
 // S_k = sum of w x over the members of k, W_k = their weight (products and
 // sums in float64, so the cancellation costs no accuracy); and the stop
-// test (no assignment changed).  One workgroup per subspace; thread k
-// updates codeword k.  K-means baseline: the centroid becomes S_k / W_k
-// (held as its norm and direction) and the objective is the distortion
-// after the update, sum_i w_i ||x_i||^2 - sum_k ||S_k||^2 / W_k.
-constexpr int UPD_THREADS = 1024;
-constexpr int UPD_EPT = (KMAX * ACC + 2 + UPD_THREADS - 1) / UPD_THREADS;  // sums per thread
+// test (no assignment changed).  K-means baseline: the centroid becomes
+// S_k / W_k (held as its norm and direction) and the objective is the
+// distortion after the update, sum_i w_i ||x_i||^2 - sum_k ||S_k||^2 / W_k.
+
+// Element-wise chunk sums of subspace g (coalesced, in chunk order) into
+// sums[0, K ACC) and sums[KMAX ACC + {0, 1}] (sum w ||x||^2, changed flag);
+// loads are unconditional (clamped indices, masked values) so a batch of
+// chunks is in flight at once.
 constexpr int UPD_CBATCH = 4;                                             // chunks per load batch
-static_assert(KMAX <= UPD_THREADS, "one thread per codeword");
-template <int MODE>
-__global__ void __launch_bounds__(UPD_THREADS) update_kernel(AssignArgs a) {
-  __shared__ double sums[KMAX * ACC + 2];
-  __shared__ double wred[UPD_THREADS / 64];
-  const int g = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int d = a.d, K = a.K;
+template <int NT>
+__device__ __forceinline__ void sum_partials(const AssignArgs& a, int g, double* sums) {
+  constexpr int EPT = (KMAX * ACC + 2 + NT - 1) / NT;
+  const int tid = threadIdx.x, K = a.K;
   const double* pg = a.part + (size_t)g * a.chunks * PSTRIDE;
-  // every input is requested up front: the stop flag, this thread's old
-  // codeword and the partial sums; a subspace that had already stopped
-  // (its partials are stale) writes nothing
-  const int stopped = MODE == MODE_ITER ? a.done[g] : 0;
-  const int kmine = tid < K ? tid : 0;
-  float* sk = a.shape + ((size_t)g * K + kmine) * d;
-  float* gk = a.gain + (size_t)g * K + kmine;
-  float sold[DP];
-#pragma unroll
-  for (int j = 0; j < DP; ++j) sold[j] = sk[j < d ? j : 0];
-  const float gold = MODE == MODE_INIT ? a.seednorm[(size_t)g * K + kmine] : *gk;
-  // element-wise chunk sums (coalesced, in chunk order) into LDS; loads are
-  // unconditional (clamped indices, masked values) so a batch is in flight
-  // at once
   const int nsum = K * ACC + 2;
-  double v[UPD_EPT];
+  double v[EPT];
 #pragma unroll
-  for (int u = 0; u < UPD_EPT; ++u) v[u] = 0.0;
+  for (int u = 0; u < EPT; ++u) v[u] = 0.0;
   for (int c0 = 0; c0 < a.chunks; c0 += UPD_CBATCH) {
-    double pv[UPD_CBATCH][UPD_EPT];
+    double pv[UPD_CBATCH][EPT];
 #pragma unroll
     for (int cc = 0; cc < UPD_CBATCH; ++cc)
 #pragma unroll
-      for (int u = 0; u < UPD_EPT; ++u) {
-        const int e = tid + u * UPD_THREADS;
+      for (int u = 0; u < EPT; ++u) {
+        const int e = tid + u * NT;
         const int src = e < K * ACC ? e : KMAX * ACC + (e < nsum ? e - K * ACC : 0);
         const int c = c0 + cc < a.chunks ? c0 + cc : 0;
         pv[cc][u] = pg[(size_t)c * PSTRIDE + src];
@@ -479,93 +480,149 @@ __global__ void __launch_bounds__(UPD_THREADS) update_kernel(AssignArgs a) {
 #pragma unroll
     for (int cc = 0; cc < UPD_CBATCH; ++cc)
 #pragma unroll
-      for (int u = 0; u < UPD_EPT; ++u) {
-        const int e = tid + u * UPD_THREADS;
+      for (int u = 0; u < EPT; ++u) {
+        const int e = tid + u * NT;
         const double x = c0 + cc < a.chunks ? pv[cc][u] : 0.0;
         v[u] = e == nsum - 1 ? fmax(v[u], x) : v[u] + x;
       }
   }
 #pragma unroll
-  for (int u = 0; u < UPD_EPT; ++u) {
-    const int e = tid + u * UPD_THREADS;
+  for (int u = 0; u < EPT; ++u) {
+    const int e = tid + u * NT;
     if (e < nsum) sums[e < K * ACC ? e : KMAX * ACC + (e - K * ACC)] = v[u];
   }
+}
+
+// Update of one codeword from its ACC sums s (w y[8], w x[8], W, count) and
+// its previous gain / shape (float64, padded with zeros past d); returns its
+// term of the objective (iteration) and leaves the new codeword in gnew, sn.
+__device__ __forceinline__ double update_codeword(bool init, bool kmeans, const double* s,
+                                                  double& gnew, double (&sn)[DP]) {
+  double term = 0.0;
+  const double W = s[16];
+  if (!init && kmeans) {
+    if (W > 0.0) {
+      double c[DP], cn = 0.0, s2 = 0.0;
+#pragma unroll
+      for (int j = 0; j < DP; ++j) {
+        c[j] = s[8 + j] / W;
+        cn = fma(c[j], c[j], cn);
+        s2 = fma(s[8 + j], s[8 + j], s2);
+      }
+      term += s2 / W;
+      cn = sqrt(cn);
+#pragma unroll
+      for (int j = 0; j < DP; ++j) sn[j] = cn > 0.0 ? c[j] / cn : 0.0;
+      gnew = cn;
+    }
+    return term;
+  }
+  if (!init) {
+    // the stored shapes are unit only to float32 rounding: use ||s||^2
+    double ps = 0.0, s2 = 0.0;
+#pragma unroll
+    for (int j = 0; j < DP; ++j) {
+      ps = fma(s[8 + j], sn[j], ps);
+      s2 = fma(sn[j], sn[j], s2);
+    }
+    term += gnew * (2.0 * ps - gnew * s2 * W);
+  }
+  if (W > 0.0) {
+    if (!init) {
+      double mn = 0.0;
+#pragma unroll
+      for (int j = 0; j < DP; ++j) mn = fma(s[j], s[j], mn);
+      mn = sqrt(mn);
+      if (mn > SHAPE_KEEP_REL * W) {
+#pragma unroll
+        for (int j = 0; j < DP; ++j) sn[j] = s[j] / mn;
+      }
+    }
+    double pr = 0.0;
+#pragma unroll
+    for (int j = 0; j < DP; ++j) pr = fma(s[8 + j], sn[j], pr);
+    gnew = fmax(0.0, pr / W);
+  }
+  return term;
+}
+
+// Sum of v over the workgroup (NT threads, per-wave partials in wred).
+template <int NT>
+__device__ __forceinline__ double block_sum(double v, double* wred) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
   __syncthreads();
-  if (stopped) return;
+  if (lane == 0) wred[wave] = v;
+  __syncthreads();
+  double sum = 0.0;
+  for (int w = 0; w < NT / 64; ++w) sum += wred[w];
+  return sum;
+}
+
+// The objective entry, iteration count and stop flag of iteration t (one
+// thread): returns whether the subspace stops.
+__device__ __forceinline__ bool finish_iteration(const AssignArgs& a, int g, int t, double wxx,
+                                                 double terms, double changed) {
+  if (a.trace) a.trace[(size_t)g * a.T + (t - 1)] = wxx - terms;
+  a.iters[g] = t;
+  const bool stop = changed == 0.0 && !a.no_early_stop;
+  if (stop) a.done[g] = t;
+  return stop;
+}
+
+constexpr int UPD_THREADS = 1024;
+static_assert(KMAX <= UPD_THREADS, "one thread per codeword");
+// Standalone update: initialisation (T = 0) or the last iteration's update,
+// old codebook from old_*, result to fin_* (the caller's arrays, possibly
+// the same arrays: each thread reads its codeword before writing it).
+template <int MODE>
+__global__ void __launch_bounds__(UPD_THREADS) update_kernel(AssignArgs a) {
+  __shared__ double sums[KMAX * ACC + 2];
+  __shared__ double wred[UPD_THREADS / 64];
+  const int g = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int d = a.d, K = a.K;
+  const int stopped = MODE == MODE_ITER ? a.done[g] : 0;
+  const int kmine = tid < K ? tid : 0;
+  if (stopped) {
+    // stopped inside a fused update: its final codebook is in buf_*
+    if (a.copy_done && tid < K) {
+      const float* gs = a.buf_gain[stopped & 1] + (size_t)g * K + tid;
+      const float* ss = a.buf_shape[stopped & 1] + ((size_t)g * K + tid) * d;
+      a.fin_gain[(size_t)g * K + tid] = *gs;
+      for (int j = 0; j < d; ++j) a.fin_shape[((size_t)g * K + tid) * d + j] = ss[j];
+    }
+    return;
+  }
+  const float* so = a.old_shape + ((size_t)g * K + kmine) * d;
+  float sold[DP];
+#pragma unroll
+  for (int j = 0; j < DP; ++j) sold[j] = so[j < d ? j : 0];
+  const float gold = MODE == MODE_INIT ? a.seednorm[(size_t)g * K + kmine]
+                                       : a.old_gain[(size_t)g * K + kmine];
+  sum_partials<UPD_THREADS>(a, g, sums);
+  __syncthreads();
   double term = 0.0;
   if (tid < K) {
-    const int k = tid;
-    double s[ACC];
-#pragma unroll
-    for (int e = 0; e < ACC; ++e) s[e] = sums[k * ACC + e];
     double sn[DP];
 #pragma unroll
     for (int j = 0; j < DP; ++j) sn[j] = (j < d) ? (double)sold[j] : 0.0;
     double gnew = (double)gold;
-    const double W = s[16];
-    if (MODE == MODE_ITER && a.kmeans) {
-      if (W > 0.0) {
-        double c[DP], cn = 0.0, s2 = 0.0;
-#pragma unroll
-        for (int j = 0; j < DP; ++j) {
-          c[j] = s[8 + j] / W;
-          cn = fma(c[j], c[j], cn);
-          s2 = fma(s[8 + j], s[8 + j], s2);
-        }
-        term += s2 / W;
-        cn = sqrt(cn);
-#pragma unroll
-        for (int j = 0; j < DP; ++j) sn[j] = cn > 0.0 ? c[j] / cn : 0.0;
-        gnew = cn;
-      }
-    } else if (MODE == MODE_ITER) {
-      // the stored shapes are unit only to float32 rounding: use ||s||^2
-      double ps = 0.0, s2 = 0.0;
-#pragma unroll
-      for (int j = 0; j < DP; ++j) {
-        ps = fma(s[8 + j], sn[j], ps);
-        s2 = fma(sn[j], sn[j], s2);
-      }
-      term += gnew * (2.0 * ps - gnew * s2 * W);
-    }
-    if (W > 0.0 && !(MODE == MODE_ITER && a.kmeans)) {
-      if (MODE == MODE_ITER) {
-        double mn = 0.0;
-#pragma unroll
-        for (int j = 0; j < DP; ++j) mn = fma(s[j], s[j], mn);
-        mn = sqrt(mn);
-        if (mn > SHAPE_KEEP_REL * W) {
-#pragma unroll
-          for (int j = 0; j < DP; ++j) sn[j] = s[j] / mn;
-        }
-      }
-      double pr = 0.0;
-#pragma unroll
-      for (int j = 0; j < DP; ++j) pr = fma(s[8 + j], sn[j], pr);
-      gnew = fmax(0.0, pr / W);
-    }
+    term = update_codeword(MODE == MODE_INIT, a.kmeans != 0, sums + tid * ACC, gnew, sn);
+    float* sk = a.fin_shape + ((size_t)g * K + tid) * d;
 #pragma unroll
     for (int j = 0; j < DP; ++j)
       if (j < d) sk[j] = (float)sn[j];
-    *gk = (float)gnew;
+    a.fin_gain[(size_t)g * K + tid] = (float)gnew;
   }
   if (MODE == MODE_INIT) {
     if (tid == 0 && a.want_wxx) a.wxx[g] = sums[KMAX * ACC];
   } else {
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) term += __shfl_xor(term, off);
-    if (lane == 0) wred[wave] = term;
-    __syncthreads();
+    const double terms = block_sum<UPD_THREADS>(term, wred);
     if (tid == 0) {
-      const double ch = sums[KMAX * ACC + 1];
-      if (a.want_wxx) a.wxx[g] = sums[KMAX * ACC];
-      if (a.trace) {
-        double obj = a.wxx[g];
-        for (int w = 0; w < UPD_THREADS / 64; ++w) obj -= wred[w];
-        a.trace[(size_t)g * a.T + (a.t - 1)] = obj;
-      }
-      a.iters[g] = a.t;
-      if (ch == 0.0 && !a.no_early_stop) a.done[g] = a.t;
+      if (a.upd_has_wxx) a.wxx[g] = sums[KMAX * ACC];
+      finish_iteration(a, g, a.t, a.wxx[g], terms, sums[KMAX * ACC + 1]);
     }
   }
 }
@@ -594,10 +651,54 @@ assign_accumulate_kernel(AssignArgs a) {
   const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K;
 
+  int ex;
+  if (MODE == MODE_ITER && a.upd != UPD_NONE) {
+    // the previous pass's codebook update, computed here by every workgroup
+    // of the subspace (same sums, same order, same result) straight into
+    // LDS; the first chunk's workgroup stores it and records the iteration
+    const bool init = a.upd == UPD_INIT;
+    const int kmine = tid < K ? tid : 0;
+    const float* so = a.old_shape + ((size_t)g * K + kmine) * d;
+    float sold[DP];
+#pragma unroll
+    for (int j = 0; j < DP; ++j) sold[j] = so[j < d ? j : 0];
+    const float gold = init ? a.seednorm[(size_t)g * K + kmine] : a.old_gain[(size_t)g * K + kmine];
+    if (tid == 0) red = 0;
+    sum_partials<TRAIN_WAVES * 64>(a, g, acc);   // acc holds the dense sums for now
+    __syncthreads();
+    double term = 0.0;
+    if (tid < KMAX) {
+      const bool real = tid < K;
+      double sn[DP];
+#pragma unroll
+      for (int j = 0; j < DP; ++j) sn[j] = (real && j < d) ? (double)sold[j] : 0.0;
+      double gnew = real ? (double)gold : 0.0;
+      if (real) term = update_codeword(init, a.kmeans != 0, acc + tid * ACC, gnew, sn);
+      cbg[tid] = (float)gnew;
+#pragma unroll
+      for (int j = 0; j < DP; ++j) cbs[tid * DP + j] = (float)sn[j];
+      if ((float)gnew > 0.f) atomicMax(&red, __float_as_int((float)gnew));
+      if (chunk == 0 && real) {
+        a.new_gain[(size_t)g * K + tid] = (float)gnew;
+        for (int j = 0; j < d; ++j) a.new_shape[((size_t)g * K + tid) * d + j] = (float)sn[j];
+      }
+    }
+    const double wxx_p = acc[KMAX * ACC], chg = acc[KMAX * ACC + 1];
+    const double terms = block_sum<TRAIN_WAVES * 64>(term, objw);
+    if (chunk == 0 && tid == 0) {
+      if (a.upd_has_wxx) a.wxx[g] = wxx_p;
+      if (!init) finish_iteration(a, g, a.t - 1, a.upd_has_wxx ? wxx_p : a.wxx[g], terms, chg);
+    }
+    // a subspace whose previous assignment repeated stops here (uniform)
+    if (!init && chg == 0.0 && !a.no_early_stop) return;
+    __syncthreads();
+    ex = sigma_exp(__int_as_float(red));
+  } else {
+    ex = load_codebook(a.gain + (size_t)g * K, a.shape + (size_t)g * K * d, d, K,
+                       MODE == MODE_INIT, cbg, cbs, &red);
+  }
   for (int e = tid; e < KMAX * ACC_LDS; e += blockDim.x) acc[e] = 0.0;
   if (tid == 0) changed = a.force_changed;
-  const int ex = load_codebook(a.gain + (size_t)g * K, a.shape + (size_t)g * K * d, d, K,
-                               MODE == MODE_INIT, cbg, cbs, &red);
   // operand tiles built once per workgroup (one (tile, lane) entry per
   // thread), then read by every wave into its registers
   for (int e = tid; e < NT * 64; e += blockDim.x) {
@@ -1166,7 +1267,7 @@ gsrq_status check_supported(const gsrq_shape* s) {
 }
 
 struct TrainLayout {
-  size_t xt, part, assign, done, iters, wxx, seednorm, seeds, total;
+  size_t xt, part, assign, done, iters, wxx, seednorm, seeds, cbg[2], cbs[2], total;
   int chunks, chunk_rows;
 };
 
@@ -1193,6 +1294,12 @@ TrainLayout train_layout(const gsrq_shape* s, size_t elt) {
   L.wxx = off; off = align256(off + (size_t)G * sizeof(double));
   L.seednorm = off; off = align256(off + (size_t)G * s->K * sizeof(float));
   L.seeds = off; off = align256(off + (size_t)G * s->K * sizeof(int32_t));
+  // codebooks of consecutive iterations (updates fused into the assignment
+  // launches write one while the next launch reads the other)
+  for (int b = 0; b < 2; ++b) {
+    L.cbg[b] = off; off = align256(off + (size_t)G * s->K * sizeof(float));
+    L.cbs[b] = off; off = align256(off + (size_t)G * s->K * s->d * sizeof(float));
+  }
   L.total = off;
   return L;
 }
@@ -1277,7 +1384,7 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
   if ((e = fill_u32(iters, G, 0u, st))) return e;
   if (trace && T_ > 0 && (e = fill_u32(trace, (size_t)G * T_ * 2, 0u, st))) return e;
 
-  AssignArgs aa;
+  AssignArgs aa = {};
   aa.xt = xt; aa.N = s->N; aa.d = d; aa.K = K; aa.G = G; aa.w = w;
   aa.gain = gain; aa.shape = shape; aa.assign = assign;
   aa.done = done; aa.iters = iters; aa.part = part;
@@ -1287,6 +1394,11 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
   aa.chunks = L.chunks; aa.chunk_rows = L.chunk_rows; aa.force_changed = 0; aa.t = 0; aa.T = T_;
   aa.no_early_stop = (flags & GSRQ_NO_EARLY_STOP) ? 1 : 0;
   aa.kmeans = (flags & GSRQ_KMEANS) ? 1 : 0;
+  float* bufg[2] = {(float*)(base + L.cbg[0]), (float*)(base + L.cbg[1])};
+  float* bufs[2] = {(float*)(base + L.cbs[0]), (float*)(base + L.cbs[1])};
+  aa.buf_gain[0] = bufg[0]; aa.buf_gain[1] = bufg[1];
+  aa.buf_shape[0] = bufs[0]; aa.buf_shape[1] = bufs[1];
+  aa.fin_gain = gain; aa.fin_shape = shape;
   const dim3 agrid((unsigned)L.chunks, (unsigned)G);
 
   if (!resume) {
@@ -1296,39 +1408,71 @@ gsrq_status train_impl(const gsrq_shape* s, const void* X, int64_t ldx, const fl
     seed_kernel<T><<<G, 256, 0, st>>>(xt, s->N, d, K, dseeds, shape, seednorm, aa.kmeans, gain);
     if ((e = launch_ok())) return e;
   }
+  // GSKM from seed rows: an initial assignment with unit gains; its gains
+  // (eq. 8) are computed at the start of the first iteration's launch
+  const bool seeded_gskm = !resume && !aa.kmeans;
+  int prev_wxx = 0;   // the last pass accumulated sum w ||x||^2
   if (!resume && aa.kmeans) {
     // K-means starts from the seed centroids; there is no previous assignment
     aa.force_changed = 1;
-  } else if (!resume) {
+  } else if (seeded_gskm) {
     {
       TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
       assign_accumulate_kernel<T, MODE_INIT><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
     }
     if ((e = launch_ok())) return e;
-    {
+    prev_wxx = aa.want_wxx;
+    aa.want_wxx = 0;
+    if (T_ == 0) {
+      // initialisation only: the gains straight into the caller's arrays
+      aa.old_shape = shape;
+      aa.upd_has_wxx = prev_wxx;
       TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
       update_kernel<MODE_INIT><<<G, UPD_THREADS, 0, st>>>(aa);
+      return launch_ok();
     }
-    if ((e = launch_ok())) return e;
-    aa.want_wxx = 0;
   } else {
     aa.force_changed = (flags & GSRQ_ASSIGN_IN) ? 0 : 1;
   }
+  // where codebook C_j (the one iteration j + 1 scores with) lives: C_0 in
+  // the caller's arrays (seeded K-means, resume) or, computed by the first
+  // launch, in buffer 0; later ones alternate between the two buffers
+  auto cb_gain = [&](int j) -> float* { return (j == 0 && !seeded_gskm) ? gain : bufg[j & 1]; };
+  auto cb_shape = [&](int j) -> float* { return (j == 0 && !seeded_gskm) ? shape : bufs[j & 1]; };
   for (int t = 1; t <= T_; ++t) {
     aa.t = t;
+    aa.upd_has_wxx = prev_wxx;
+    if (t == 1 && !seeded_gskm) {
+      aa.upd = UPD_NONE;
+      aa.gain = gain;
+      aa.shape = shape;
+    } else {
+      aa.upd = t == 1 ? UPD_INIT : UPD_ITER;
+      aa.old_gain = t == 1 ? nullptr : cb_gain(t - 2);
+      aa.old_shape = t == 1 ? shape : cb_shape(t - 2);   // seed shapes for the first
+      aa.new_gain = cb_gain(t - 1);
+      aa.new_shape = cb_shape(t - 1);
+    }
     {
       TimedLaunch tl(GSRQ_KERNEL_ASSIGN, st);
       assign_accumulate_kernel<T, MODE_ITER><<<agrid, TRAIN_WAVES * 64, 0, st>>>(aa);
     }
     if ((e = launch_ok())) return e;
-    {
-      TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
-      update_kernel<MODE_ITER><<<G, UPD_THREADS, 0, st>>>(aa);
-    }
-    if ((e = launch_ok())) return e;
+    prev_wxx = aa.want_wxx;
     aa.force_changed = 0;
     aa.want_wxx = 0;
   }
+  if (T_ > 0) {
+    // the last iteration's update into the caller's arrays; subspaces that
+    // stopped earlier get their final codebook copied there
+    aa.upd_has_wxx = prev_wxx;
+    aa.old_gain = cb_gain(T_ - 1);
+    aa.old_shape = cb_shape(T_ - 1);
+    aa.copy_done = 1;
+    TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
+    update_kernel<MODE_ITER><<<G, UPD_THREADS, 0, st>>>(aa);
+  }
+  if ((e = launch_ok())) return e;
   if (R_next) {
     gsrq_shape s1 = *s;
     s1.M = 1;
@@ -1540,7 +1684,7 @@ gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_us
 gsrq_status gsrq_timing_enable_kinds(uint32_t kinds) {
   g_gsrq_timing.on = kinds != 0;
   g_gsrq_timing.kinds = kinds;
-  g_gsrq_timing.n = 0;
+  if (kinds) g_gsrq_timing.n = 0;   // switching off keeps the records for reading
   return GSRQ_OK;
 }
 
