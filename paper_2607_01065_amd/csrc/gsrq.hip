@@ -651,6 +651,35 @@ assign_accumulate_kernel(AssignArgs a) {
   const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K;
 
+  // this chunk's rows, weights and codes, indexed from 0 in 32 bits
+  const int64_t row_begin = (int64_t)chunk * a.chunk_rows;
+  const int nrows = (int)(a.N - row_begin < a.chunk_rows ? a.N - row_begin : a.chunk_rows);
+  const T* xc = (const T*)a.xt + ((size_t)g * a.N + row_begin) * 8;
+  uint16_t* ac = a.assign + (size_t)g * a.N + row_begin;
+  const int nblk = (nrows + RB - 1) / RB;
+  const bool want_wxx = a.want_wxx != 0;
+
+  // loads never branch: past the end they read the chunk's first row, whose
+  // results are discarded, so prefetches stay in flight (without weights
+  // the load reads a gain in place of a weight and the value is replaced by
+  // 1: a global pointer keeps it a global load)
+  const bool has_w = a.w != nullptr;
+  const float* wc = has_w ? a.w + row_begin : a.gain;
+  const int wstride = has_w ? 1 : 0;
+  RowVec<T> nx;
+  float nw = 0.f;
+  uint16_t nold = 0;
+  auto fetch = [&](int rb) {
+    int r = rb * RB + i;
+    r = r < nrows ? r : 0;
+    nx.load(xc + r * 8);
+    nw = wc[r * wstride];
+    if (MODE == MODE_ITER) nold = ac[r];
+  };
+  // the first block's loads are issued before the codebook is ready, so
+  // they overlap its load or update
+  if (wave < nblk) fetch(wave);
+
   int ex;
   if (MODE == MODE_ITER && a.upd != UPD_NONE) {
     // the previous pass's codebook update, computed here by every workgroup
@@ -717,32 +746,6 @@ assign_accumulate_kernel(AssignArgs a) {
     tl.a2[t] = tiles_l[(2 * t + 1) * 64 + lane];
   }
 
-  // this chunk's rows, weights and codes, indexed from 0 in 32 bits
-  const int64_t row_begin = (int64_t)chunk * a.chunk_rows;
-  const int nrows = (int)(a.N - row_begin < a.chunk_rows ? a.N - row_begin : a.chunk_rows);
-  const T* xc = (const T*)a.xt + ((size_t)g * a.N + row_begin) * 8;
-  uint16_t* ac = a.assign + (size_t)g * a.N + row_begin;
-  const int nblk = (nrows + RB - 1) / RB;
-  const bool want_wxx = a.want_wxx != 0;
-
-  // loads never branch: past the end they read the chunk's first row, whose
-  // results are discarded, so prefetches stay in flight (without weights
-  // the load reads a gain in place of a weight and the value is replaced by
-  // 1: a global pointer keeps it a global load)
-  const bool has_w = a.w != nullptr;
-  const float* wc = has_w ? a.w + row_begin : a.gain;
-  const int wstride = has_w ? 1 : 0;
-  RowVec<T> nx;
-  float nw = 0.f;
-  uint16_t nold = 0;
-  auto fetch = [&](int rb) {
-    int r = rb * RB + i;
-    r = r < nrows ? r : 0;
-    nx.load(xc + r * 8);
-    nw = wc[r * wstride];
-    if (MODE == MODE_ITER) nold = ac[r];
-  };
-  if (wave < nblk) fetch(wave);
 
   double obj = 0.0;
   bool any_changed = false;
