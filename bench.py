@@ -27,7 +27,7 @@ METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline
 # rocprofv3 passes (profiles/hbm_traffic_llama3_8b_layer_1bit.md, read counts
 # scaled x2.000 and writes x1.000 against a 256 MiB reference copy).  Valid
 # only for the kernel source those passes measured.
-TRAFFIC = {"source_sha256_prefix": "ce18ce54f6588ac4", "bytes_per_launch": 96367089}
+TRAFFIC = {"source_sha256_prefix": "b9e95e6ffcbefa9f", "bytes_per_launch": 116571602}
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
 HEAD_DIM = 128
