@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--cpu-groups", type=int, default=128,
                     help="subspaces of the K cache the CPU-baseline sample runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the measurements outside the step (per-token weights, "
+                         "appended-token encode), e.g. for kernel profiles of the step alone")
     ap.add_argument("--copy-ref-mib", type=int, default=0,
                     help="after timing, run one plain device copy of this many MiB "
                          "(reference dispatch for scaling HBM counters)")
@@ -358,7 +361,8 @@ def main():
                                   "note": "argmin epilogue: one VALU lane-op per score is the "
                                           "floor; peak = 256 CU x 64 lanes x 2.4 GHz"}},
     }
-    out.update(extra_paths(B, caches[0], wl, dev))
+    if not args.no_extra:
+        out.update(extra_paths(B, caches[0], wl, dev))
     if args.copy_ref_mib > 0:
         n = args.copy_ref_mib * (1 << 20) // 4
         src = torch.ones(n, dtype=torch.float32, device=dev)
