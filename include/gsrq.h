@@ -219,6 +219,8 @@ gsrq_status gsrq_row_weights(const void* grad, gsrq_dtype dtype, int64_t N, int3
 /* Kernel kinds reported by the optional launch timing below. */
 enum {
   GSRQ_KERNEL_ASSIGN = 0,     /* fused assignment + weighted accumulation */
+                              /* (d <= 8: from the second iteration on also */
+                              /* the previous iteration's codebook update)  */
   GSRQ_KERNEL_FINALIZE = 1,   /* codebook update + operand tiles          */
   GSRQ_KERNEL_ENCODE = 2,     /* stage-fused encoder                      */
   GSRQ_KERNEL_DECODE = 3,     /* gather-sum decoder                       */
