@@ -1,4 +1,4 @@
-"""Plain float64 CPU oracle of GSKM and GSRQ.
+"""Plain float64 CPU oracle of GSKM, GSRQ and decode attention over a coded cache.
 
 TEST INFRASTRUCTURE ONLY.  This module is the parity reference for the HIP
 path.  Only the test suite, the smoke check of the graft entry point and the
@@ -421,3 +421,75 @@ def kmeans(X, w, K, T, init_rows, *, centroids=None, prev_assign=None):
         prev = assign
     return dict(centroids=C, iters_run=iters_run, assign=assign,
                 trace=np.asarray(trace))
+
+
+# ----------------------------------------------------------------------------
+# One decoding step of attention over a coded KV cache (Appendix C: the
+# decoding kernel unpacks the codes, dequantises, applies RoPE and computes
+# attention).  Readings (the paper names the steps only):
+#   * keys are quantised before RoPE, so RoPE is applied to each dequantised
+#     key at its position;
+#   * RoPE in the rotate-half form of the LLaMA family: for a head of hd
+#     elements, element j < hd/2 and element j + hd/2 form a pair rotated by
+#     the angle p * theta_j, theta_j = base^(-2j/hd), p the token position;
+#   * the cached tokens of a sequence sit at positions 0 .. L-1 and the query
+#     is the newest token, at position L-1 (its own key is in the cache);
+#   * grouped-query attention: query head h reads key/value head h // (Hq/Hkv);
+#   * softmax scale 1/sqrt(hd); an empty cache (L = 0) gives a zero output.
+# ----------------------------------------------------------------------------
+
+def rope_theta(hd, base):
+    """theta_j = base^(-2j/hd) for j = 0 .. hd/2 - 1 (float64)."""
+    j = np.arange(hd // 2, dtype=np.float64)
+    return np.power(float(base), -2.0 * j / hd)
+
+
+def rope(x, positions, base):
+    """Rotate-half RoPE of the last axis of x [..., P, hd] at integer
+    positions [P]: pair (j, j + hd/2) is rotated by positions * theta_j."""
+    x = np.asarray(x, np.float64)
+    hd = x.shape[-1]
+    ang = np.asarray(positions, np.float64)[:, None] * rope_theta(hd, base)[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    a, b = x[..., :hd // 2], x[..., hd // 2:]
+    return np.concatenate([a * c - b * s, a * s + b * c], axis=-1)
+
+
+def attn_decode(q, K, V, base, scale=None, *, operands_f16=False):
+    """Attention of one query token over one sequence's decoded cache.
+
+    q  [Hq, hd]        the newest token's query, before RoPE;
+    K  [L, Hkv, hd]    dequantised keys before RoPE, token i at position i;
+    V  [L, Hkv, hd]    dequantised values.
+    Returns [Hq, hd] float64: softmax(RoPE(q) . RoPE(K)^T * scale) V per head.
+
+    operands_f16 rounds the rotated query and the rotated keys to float16
+    (round to nearest even) before their dot products: the operand precision
+    a float16 matrix-core kernel declares, not part of the method.
+    """
+    q = np.asarray(q, np.float64)
+    K = np.asarray(K, np.float64)
+    V = np.asarray(V, np.float64)
+    Hq, hd = q.shape
+    L, Hkv = K.shape[0], K.shape[1]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    scale = 1.0 / np.sqrt(hd) if scale is None else float(scale)
+    out = np.zeros((Hq, hd), dtype=np.float64)
+    if L == 0:
+        return out
+    pos = np.arange(L)
+    # RoPE of the query at position L-1 (same rotation for every head)
+    qr = rope(q[:, None, :], np.array([L - 1]), base)[:, 0, :]
+    kr = rope(np.transpose(K, (1, 0, 2)), pos, base)          # [Hkv, L, hd]
+    if operands_f16:
+        qr = qr.astype(np.float16).astype(np.float64)
+        kr = kr.astype(np.float16).astype(np.float64)
+    group = Hq // Hkv
+    for h in range(Hq):
+        kv = h // group
+        s = (kr[kv] @ qr[h]) * scale                             # [L]
+        p = np.exp(s - np.max(s))
+        p /= np.sum(p)
+        out[h] = p @ V[:, kv, :]
+    return out

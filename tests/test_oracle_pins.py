@@ -467,3 +467,113 @@ def test_log_weight_tames_heavy_tailed_norms():
     assert w.max() / np.median(w) < 10
     # median maps to log(2) exactly in exact arithmetic (lambda * median = 1)
     assert np.median(w) == pytest.approx(math.log(2.0), rel=1e-6)
+
+
+# ------------------------------------------- decode attention (Appendix C)
+
+@pytest.mark.parametrize("hd,base", [(128, 500000.0), (128, 10000.0), (8, 10.0)])
+def test_rope_first_pair_turns_by_position_in_radians(hd, base):
+    """theta_0 = base^0 = 1 for every base: the pair (0, hd/2) turns by
+    exactly p radians at position p (rotate-half form)."""
+    for p in (0, 1, 2, 1000, 123457):
+        e0 = np.zeros((1, hd))
+        e0[0, 0] = 1.0
+        r = O.rope(e0, np.array([p]), base)[0]
+        assert r[0] == pytest.approx(math.cos(p), abs=1e-12)
+        assert r[hd // 2] == pytest.approx(math.sin(p), abs=1e-12)
+        assert np.count_nonzero(np.abs(r) > 1e-15) <= 2
+        eh = np.zeros((1, hd))
+        eh[0, hd // 2] = 1.0
+        r = O.rope(eh, np.array([p]), base)[0]
+        assert r[0] == pytest.approx(-math.sin(p), abs=1e-12)
+        assert r[hd // 2] == pytest.approx(math.cos(p), abs=1e-12)
+
+
+def test_rope_last_pair_frequency():
+    """theta_63 of a 128-element head with base 10^4 is 10^(-4 * 126/128)
+    = 10^-3.9375 = 1.1547819846894583e-4 (hand value); at position 1000 the
+    pair (63, 127) turns by 0.11547819846894583 rad."""
+    th = O.rope_theta(128, 10000.0)
+    assert th[63] == pytest.approx(1.1547819846894583e-4, rel=1e-14)
+    assert th[0] == 1.0
+    x = np.zeros((1, 128))
+    x[0, 63] = 1.0
+    r = O.rope(x, np.array([1000]), 10000.0)[0]
+    a = 0.11547819846894583
+    assert r[63] == pytest.approx(math.cos(a), abs=1e-13)
+    assert r[127] == pytest.approx(math.sin(a), abs=1e-13)
+
+
+def test_rope_scores_depend_on_relative_position_only():
+    rng = _rng(70)
+    q, k = rng.standard_normal((2, 128))
+    for a, b, sh in ((5, 17, 3), (1000, 2, 99), (0, 0, 131071)):
+        s1 = O.rope(q[None], np.array([a]), 500000.0)[0] @ O.rope(k[None], np.array([b]), 500000.0)[0]
+        s2 = (O.rope(q[None], np.array([a + sh]), 500000.0)[0]
+              @ O.rope(k[None], np.array([b + sh]), 500000.0)[0])
+        assert s1 == pytest.approx(s2, rel=1e-9, abs=1e-9)
+        n = np.linalg.norm(O.rope(k[None], np.array([b]), 500000.0)[0])
+        assert n == pytest.approx(np.linalg.norm(k), rel=1e-13)
+
+
+def test_attention_two_tokens_hand_worked():
+    """Keys e_0 at positions 0 and 1, query at position 1 with scale*q = e_0:
+    scores cos(-1) and 1, so o = (e^cos1 v0 + e v1) / (e^cos1 + e).  With
+    scale*q = e_64 instead the scores are sin(-1) and 0 (the sign of the
+    rotation shows here)."""
+    hd = 128
+    v = np.zeros((2, 1, hd))
+    v[0, 0, :] = 1.0
+    v[1, 0, :] = -2.0
+    K = np.zeros((2, 1, hd))
+    K[:, 0, 0] = 1.0
+    q = np.zeros((1, hd))
+    q[0, 0] = math.sqrt(hd)
+    o = O.attn_decode(q, K, v, 500000.0)
+    a0, a1 = math.exp(math.cos(1.0)), math.exp(1.0)
+    assert o[0, 5] == pytest.approx((a0 * 1.0 + a1 * -2.0) / (a0 + a1), rel=1e-12)
+    q = np.zeros((1, hd))
+    q[0, 64] = math.sqrt(hd)
+    o = O.attn_decode(q, K, v, 10000.0)
+    a0, a1 = math.exp(-math.sin(1.0)), 1.0
+    assert o[0, 7] == pytest.approx((a0 * 1.0 + a1 * -2.0) / (a0 + a1), rel=1e-12)
+
+
+def test_attention_special_cases():
+    """One token: the output is its value; a zero query: the mean value;
+    query head h reads key/value head h // (Hq / Hkv); empty cache: zeros."""
+    rng = _rng(71)
+    Hq, Hkv, hd = 4, 2, 128
+    q = rng.standard_normal((Hq, hd))
+    K = rng.standard_normal((1, Hkv, hd))
+    V = rng.standard_normal((1, Hkv, hd))
+    o = O.attn_decode(q, K, V, 500000.0)
+    for h in range(Hq):
+        assert np.allclose(o[h], V[0, h // 2], rtol=0, atol=1e-14)
+    K = rng.standard_normal((9, Hkv, hd))
+    V = rng.standard_normal((9, Hkv, hd))
+    o = O.attn_decode(np.zeros((Hq, hd)), K, V, 500000.0)
+    for h in range(Hq):
+        assert np.allclose(o[h], V[:, h // 2].mean(axis=0), rtol=0, atol=1e-13)
+    assert np.all(O.attn_decode(q, K[:0], V[:0], 500000.0) == 0.0)
+
+
+def test_attention_float16_operand_error_within_bound():
+    """The error of float16 operands stays inside the bound used by the GPU
+    tests: each rotated operand element is off by at most 2^-11 of itself, so
+    a score moves by at most eps = scale 2^-10 ||q|| max_t ||k_t|| (plus
+    float32 summation, covered by the 1e-5 term), the softmax weights by a
+    factor within e^(+-2 eps), and the output by (e^(2 eps) - 1) max|v|."""
+    rng = _rng(72)
+    Hq, Hkv, hd, L = 4, 1, 128, 500
+    q = rng.standard_normal((Hq, hd))
+    K = rng.standard_normal((L, Hkv, hd)) * rng.uniform(0.5, 2.0, size=(L, 1, 1))
+    V = rng.standard_normal((L, Hkv, hd))
+    o = O.attn_decode(q, K, V, 500000.0)
+    o16 = O.attn_decode(q, K, V, 500000.0, operands_f16=True)
+    scale = 1.0 / math.sqrt(hd)
+    for h in range(Hq):
+        eps = scale * 2.0 ** -10 * np.linalg.norm(q[h]) * np.max(np.linalg.norm(K[:, 0], axis=1))
+        bound = (math.expm1(2 * eps) + 1e-5) * np.max(np.abs(V))
+        err = np.max(np.abs(o16[h] - o[h]))
+        assert 0 < err <= bound
