@@ -216,6 +216,58 @@ gsrq_status gsrq_row_weights(const void* grad, gsrq_dtype dtype, int64_t N, int3
                              int64_t ldg, float tau, float* norms, float* w, double* stats,
                              void* stream);
 
+/* Shape of one decoding step of attention over coded K and V caches. */
+typedef struct {
+  int32_t B;          /* sequences in the batch                              */
+  int32_t cap;        /* cache rows reserved per sequence                    */
+  int32_t Hq;         /* query heads                                         */
+  int32_t Hkv;        /* key/value heads; Hq is a multiple of Hkv            */
+  int32_t head_dim;   /* elements per head                                   */
+  float rope_base;    /* RoPE base: theta_j = rope_base^(-2j / head_dim)     */
+  float scale;        /* softmax scale, normally 1 / sqrt(head_dim)          */
+} gsrq_attn_shape;
+
+/* Workspace bytes gsrq_attn_decode needs for shape a. */
+gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes);
+
+/*
+ * gsrq_attn_decode -- one decoding step of attention over GSRQ-coded key and
+ * value caches: the codes are unpacked, the keys dequantised and rotated by
+ * RoPE, and softmax attention is taken without a float16 K/V tensor (the
+ * fused decoding kernel of the paper's latency analysis, Appendix C).  For
+ * sequence b of L = seq_len[b] tokens and query head h, reading key/value
+ * head h / (Hq / Hkv):
+ *   o = sum_i p_i vhat_i,
+ *   p = softmax_i( scale * RoPE(q, L - 1) . RoPE(khat_i, i) ),  i = 0 .. L-1,
+ * where khat_i, vhat_i are token i's decoded key and value rows (Sec. 3)
+ * and RoPE turns elements j and j + head_dim/2 of a head together by the
+ * angle position * theta_j (rotate-half form).  Keys are cached before RoPE;
+ * the query is the newest token's, at position L - 1, before RoPE.
+ *
+ *  kv                code shape: D = Hkv * head_dim, d = 8, K = 256, M = 1
+ *                    (other valid shapes: GSRQ_E_UNSUPPORTED); N >= B * cap.
+ *  k_codes, v_codes  [B][cap][gsrq_code_words(kv)] uint32 packed codes, token
+ *                    i of sequence b in row b * cap + i; 16-byte aligned.
+ *  seq_len           [B] int32 (device), clamped to [0, cap]; a sequence of
+ *                    length 0 gets a zero output.
+ *  k_gain, k_shape   key codebook [1][G][256], [1][G][256][8] (shape 16-byte
+ *  v_gain, v_shape   aligned) and value codebook.
+ *  q, q_dtype        [B][Hq][head_dim] queries, 16-byte aligned.
+ *  out               [B][Hq][head_dim] float32.
+ *  workspace         >= gsrq_attn_workspace_bytes(a), 256-byte aligned.
+ * Precision: keys enter as their float16 decode (g * s rounded to float32,
+ * then to float16); the rotated query and keys are rounded to float16 for
+ * their dot products, which are summed in float32; softmax weights and the
+ * value sums are float32 with float32 value codewords; chunks are merged in
+ * float64.  This build: head_dim = 128 and Hq / Hkv in {1, 2, 4}.
+ */
+gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                             const uint32_t* k_codes, const uint32_t* v_codes,
+                             const int32_t* seq_len, const float* k_gain, const float* k_shape,
+                             const float* v_gain, const float* v_shape, const void* q,
+                             gsrq_dtype q_dtype, float* out, void* workspace, size_t ws_bytes,
+                             void* stream);
+
 /* Kernel kinds reported by the optional launch timing below. */
 enum {
   GSRQ_KERNEL_ASSIGN = 0,     /* fused assignment + weighted accumulation */
@@ -228,7 +280,8 @@ enum {
   GSRQ_KERNEL_ACCUMULATE = 5, /* weighted sums per codeword slice (d > 8)  */
   GSRQ_KERNEL_FRAGMENTS = 6,  /* operand fragment tables (d > 8 or K > 256) */
   GSRQ_KERNEL_EXACT = 7,      /* float64 rescoring of deferred rows         */
-  GSRQ_KERNEL_KINDS = 8
+  GSRQ_KERNEL_ATTENTION = 8,  /* decode attention over a coded cache       */
+  GSRQ_KERNEL_KINDS = 9
 };
 
 /* Measurement hook, the library's only process state.  While enabled, every

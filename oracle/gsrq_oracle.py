@@ -455,41 +455,56 @@ def rope(x, positions, base):
     return np.concatenate([a * c - b * s, a * s + b * c], axis=-1)
 
 
+def attn_weights(q, K, base, scale=None, *, operands_f16=False):
+    """Softmax weights of one query token over one sequence's cache:
+    p[h, i] = softmax_i(scale * RoPE(q_h, L-1) . RoPE(K[i, h // (Hq/Hkv)], i)).
+
+    q [Hq, hd] before RoPE; K [L, Hkv, hd] dequantised keys before RoPE.
+    operands_f16 rounds the rotated query and the rotated keys to float16
+    (round to nearest even) before their dot products: the operand precision
+    of a float16 matrix-core kernel, not part of the method.
+    Returns (p [Hq, L], s [Hq, L] scaled scores), float64."""
+    q = np.asarray(q, np.float64)
+    K = np.asarray(K, np.float64)
+    Hq, hd = q.shape
+    L, Hkv = K.shape[0], K.shape[1]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    scale = 1.0 / np.sqrt(hd) if scale is None else float(scale)
+    p = np.zeros((Hq, L), dtype=np.float64)
+    sc = np.zeros((Hq, L), dtype=np.float64)
+    if L == 0:
+        return p, sc
+    # RoPE of the query at position L-1 (same rotation for every head)
+    qr = rope(q[:, None, :], np.array([L - 1]), base)[:, 0, :]
+    kr = rope(np.transpose(K, (1, 0, 2)), np.arange(L), base)   # [Hkv, L, hd]
+    if operands_f16:
+        qr = qr.astype(np.float16).astype(np.float64)
+        kr = kr.astype(np.float16).astype(np.float64)
+    group = Hq // Hkv
+    for h in range(Hq):
+        s = (kr[h // group] @ qr[h]) * scale
+        e = np.exp(s - np.max(s))
+        p[h] = e / np.sum(e)
+        sc[h] = s
+    return p, sc
+
+
 def attn_decode(q, K, V, base, scale=None, *, operands_f16=False):
     """Attention of one query token over one sequence's decoded cache.
 
     q  [Hq, hd]        the newest token's query, before RoPE;
     K  [L, Hkv, hd]    dequantised keys before RoPE, token i at position i;
     V  [L, Hkv, hd]    dequantised values.
-    Returns [Hq, hd] float64: softmax(RoPE(q) . RoPE(K)^T * scale) V per head.
-
-    operands_f16 rounds the rotated query and the rotated keys to float16
-    (round to nearest even) before their dot products: the operand precision
-    a float16 matrix-core kernel declares, not part of the method.
-    """
+    Returns [Hq, hd] float64: o_h = sum_i p[h, i] V[i, h // (Hq/Hkv)] with the
+    weights of attn_weights (zero for an empty cache)."""
     q = np.asarray(q, np.float64)
-    K = np.asarray(K, np.float64)
     V = np.asarray(V, np.float64)
     Hq, hd = q.shape
-    L, Hkv = K.shape[0], K.shape[1]
-    if Hq % Hkv:
-        raise ValueError("Hq must be a multiple of Hkv")
-    scale = 1.0 / np.sqrt(hd) if scale is None else float(scale)
+    Hkv = np.asarray(K).shape[1]
+    p, _ = attn_weights(q, K, base, scale, operands_f16=operands_f16)
     out = np.zeros((Hq, hd), dtype=np.float64)
-    if L == 0:
-        return out
-    pos = np.arange(L)
-    # RoPE of the query at position L-1 (same rotation for every head)
-    qr = rope(q[:, None, :], np.array([L - 1]), base)[:, 0, :]
-    kr = rope(np.transpose(K, (1, 0, 2)), pos, base)          # [Hkv, L, hd]
-    if operands_f16:
-        qr = qr.astype(np.float16).astype(np.float64)
-        kr = kr.astype(np.float16).astype(np.float64)
     group = Hq // Hkv
     for h in range(Hq):
-        kv = h // group
-        s = (kr[kv] @ qr[h]) * scale                             # [L]
-        p = np.exp(s - np.max(s))
-        p /= np.sum(p)
-        out[h] = p @ V[:, kv, :]
+        out[h] = p[h] @ V[:, h // group, :]
     return out

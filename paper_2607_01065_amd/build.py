@@ -6,7 +6,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRCS = [os.path.join(HERE, "csrc", f) for f in ("gsrq.hip", "gsrq_wide.hip", "gsrq_weights.hip")]
+SRCS = [os.path.join(HERE, "csrc", f) for f in ("gsrq.hip", "gsrq_wide.hip", "gsrq_weights.hip", "gsrq_attn.hip")]
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libgsrq.so")
 

@@ -8,6 +8,7 @@ functions from here raises instead of falling back to anything else.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from dataclasses import dataclass
 from typing import Optional
@@ -31,6 +32,12 @@ class GsrqError(RuntimeError):
 class Shape(ctypes.Structure):
     _fields_ = [("N", ctypes.c_int64), ("D", ctypes.c_int32), ("d", ctypes.c_int32),
                 ("K", ctypes.c_int32), ("M", ctypes.c_int32)]
+
+
+class AttnShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("cap", ctypes.c_int32), ("Hq", ctypes.c_int32),
+                ("Hkv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("rope_base", ctypes.c_float), ("scale", ctypes.c_float)]
 
 
 _lib = None
@@ -69,6 +76,12 @@ def load_library(path: str = LIB_PATH):
     lib.gsrq_row_weights.restype = ctypes.c_int
     lib.gsrq_row_weights.argtypes = [_vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int32,
                                      ctypes.c_int64, ctypes.c_float, _vp, _vp, _vp, _vp]
+    AP = ctypes.POINTER(AttnShape)
+    lib.gsrq_attn_workspace_bytes.restype = ctypes.c_int
+    lib.gsrq_attn_workspace_bytes.argtypes = [AP, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gsrq_attn_decode.restype = ctypes.c_int
+    lib.gsrq_attn_decode.argtypes = [AP, SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                     ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]
     lib.gsrq_timing_enable.restype = ctypes.c_int
     lib.gsrq_timing_enable.argtypes = [ctypes.c_int]
     lib.gsrq_timing_enable_kinds.restype = ctypes.c_int
@@ -81,7 +94,7 @@ def load_library(path: str = LIB_PATH):
 
 
 KERNEL_KINDS = ("assign", "finalize", "encode", "decode", "transpose", "accumulate",
-                "fragments", "exact")
+                "fragments", "exact", "attention")
 
 
 def timing_enable(on: bool = True, kinds=None):
@@ -305,3 +318,53 @@ def row_weights(grad=None, *, norms=None, tau=1.0, stream=None):
                               _ptr(stats), _stream_handle(stream))
     _check(st, "gsrq_row_weights")
     return w, norms, stats
+
+
+def make_attn_shape(B, cap, Hq, Hkv, head_dim=128, rope_base=500000.0, scale=None) -> AttnShape:
+    scale = 1.0 / math.sqrt(head_dim) if scale is None else float(scale)
+    return AttnShape(int(B), int(cap), int(Hq), int(Hkv), int(head_dim), float(rope_base), scale)
+
+
+def attn_workspace_bytes(B, cap, Hq, Hkv, head_dim=128) -> int:
+    n = ctypes.c_size_t()
+    sh = make_attn_shape(B, cap, Hq, Hkv, head_dim)
+    _check(load_library().gsrq_attn_workspace_bytes(ctypes.byref(sh), ctypes.byref(n)),
+           "gsrq_attn_workspace_bytes")
+    return int(n.value)
+
+
+def attn_decode(k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, *,
+                rope_base=500000.0, scale=None, out=None, workspace=None, stream=None):
+    """One decoding step of attention over coded caches (see gsrq_attn_decode).
+    k_codes, v_codes [B, cap, W] packed codes; seq_len [B] int32; codebooks
+    [1, G, 256] / [1, G, 256, 8]; q [B, Hq, 128] (float16/float32).  Returns
+    out [B, Hq, 128] float32."""
+    torch = _torch()
+    lib = load_library()
+    B, cap, W = k_codes.shape
+    Hq, hd = q.shape[1], q.shape[2]
+    M, G, K = k_gain.shape
+    d = k_shape.shape[-1]
+    D = G * d
+    Hkv = D // hd
+    for t in (k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q):
+        if not t.is_contiguous():
+            raise ValueError("attn_decode expects contiguous tensors")
+    if tuple(v_codes.shape) != (B, cap, W) or q.shape[0] != B or seq_len.numel() != B:
+        raise ValueError("inconsistent shapes")
+    if seq_len.dtype != torch.int32:
+        raise TypeError("seq_len must be int32")
+    ash = make_attn_shape(B, cap, Hq, Hkv, hd, rope_base, scale)
+    sh = make_shape(B * cap, D, d, K, M)
+    n = ctypes.c_size_t()
+    _check(lib.gsrq_attn_workspace_bytes(ctypes.byref(ash), ctypes.byref(n)),
+           "gsrq_attn_workspace_bytes")
+    ws = _workspace(n.value, q.device, workspace)
+    if out is None:
+        out = torch.empty((B, Hq, hd), dtype=torch.float32, device=q.device)
+    st = lib.gsrq_attn_decode(ctypes.byref(ash), ctypes.byref(sh), _ptr(k_codes), _ptr(v_codes),
+                              _ptr(seq_len), _ptr(k_gain), _ptr(k_shape), _ptr(v_gain),
+                              _ptr(v_shape), _ptr(q), _dtype_code(q), _ptr(out), _ptr(ws),
+                              ws.numel() * ws.element_size(), _stream_handle(stream))
+    _check(st, "gsrq_attn_decode")
+    return out

@@ -212,3 +212,33 @@ def gradient_rows(N: int, D: int, seed: int = 0, sigma: float = 1.5,
     s = rng.lognormal(0.0, sigma, size=N).astype(np.float32)
     z = rng.standard_normal((N, D), dtype=np.float32)
     return (s[:, None] * z).astype(dtype)
+
+
+def attn_case(B: int, cap: int, lens, Hkv: int, GQ: int, seed: int = 0, q_dtype="float32",
+              q_scale: float = 1.0, hd: int = 128, K: int = 256, d: int = 8):
+    """One decoding step over coded caches (1-bit cache: d = 8, K = 256,
+    one stage): random codebooks and codes stand in for a calibrated layer's
+    (any code is a valid input), queries N(0, q_scale^2).
+
+    Draw order (PCG64 from SeedSequence([seed, B, cap, Hkv, GQ])): key gains
+    sqrt(d) * lognormal(0, 0.25) [1, G, K], key shapes (unit rows of
+    N(0, I_d)) [1, G, K, d], the same for values, key codes and value codes
+    (uniform bytes, packed 4 per uint32 word, subspace g in byte g of a row)
+    [B, cap, G / 4], queries [B, Hkv * GQ, hd].  lens gives seq_len."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, B, cap, Hkv, GQ])))
+    G = Hkv * hd // d
+
+    def codebook():
+        gain = (np.sqrt(d) * rng.lognormal(0.0, 0.25, size=(1, G, K))).astype(np.float32)
+        sh = rng.standard_normal((1, G, K, d))
+        sh /= np.linalg.norm(sh, axis=-1, keepdims=True)
+        return gain, sh.astype(np.float32)
+
+    k_gain, k_shape = codebook()
+    v_gain, v_shape = codebook()
+    k_codes = rng.integers(0, K, size=(B, cap, G), dtype=np.uint8).view(np.uint32)
+    v_codes = rng.integers(0, K, size=(B, cap, G), dtype=np.uint8).view(np.uint32)
+    q = (q_scale * rng.standard_normal((B, Hkv * GQ, hd))).astype(q_dtype)
+    return dict(k_codes=np.ascontiguousarray(k_codes), v_codes=np.ascontiguousarray(v_codes),
+                lens=np.asarray(lens, np.int32), k_gain=k_gain, k_shape=k_shape,
+                v_gain=v_gain, v_shape=v_shape, q=q, Hkv=Hkv, GQ=GQ)

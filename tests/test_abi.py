@@ -156,3 +156,42 @@ def test_row_weights_validation_before_any_hip_call():
     assert f(D, B.GSRQ_F16, 10, 8, 8, 1.0, None, D, D, None) == B.GSRQ_E_ARG     # norms
     assert f(D, B.GSRQ_F16, 10, 8, 8, 1.0, D, None, D, None) == B.GSRQ_E_ARG     # w
     assert f(D, B.GSRQ_F16, 10, 8, 8, 1.0, D, D, None, None) == B.GSRQ_E_ARG     # stats
+
+
+def test_attn_decode_validation_before_any_hip_call():
+    lib = B.load_library()
+    a0 = dict(B=2, cap=100, Hq=32, Hkv=8, head_dim=128)
+    kv0 = B.make_shape(200, 1024, 8, 256, 1)
+    D = DUMMY
+
+    def call(a=None, kv=None, ws_bytes=1 << 30, **ptr):
+        ash = B.make_attn_shape(**{**a0, **(a or {})})
+        p = {n: D for n in ("kc", "vc", "len", "kg", "ks", "vg", "vs", "q", "out")}
+        p.update(ptr)
+        return lib.gsrq_attn_decode(ctypes.byref(ash), ctypes.byref(kv or kv0), p["kc"], p["vc"],
+                                    p["len"], p["kg"], p["ks"], p["vg"], p["vs"], p["q"],
+                                    ptr.get("dt", B.GSRQ_F16), p["out"], ptr.get("ws", D * 16),
+                                    ws_bytes, None)
+
+    assert call(a=dict(B=0)) == B.GSRQ_E_ARG
+    assert call(a=dict(cap=0)) == B.GSRQ_E_ARG
+    assert call(a=dict(Hq=30)) == B.GSRQ_E_ARG                  # not a multiple of Hkv
+    assert call(a=dict(Hq=64)) == B.GSRQ_E_UNSUPPORTED          # GQ = 8
+    assert call(a=dict(head_dim=64), kv=B.make_shape(200, 512, 8, 256, 1)) == B.GSRQ_E_UNSUPPORTED
+    assert call(kv=B.make_shape(199, 1024, 8, 256, 1)) == B.GSRQ_E_ARG     # N < B * cap
+    assert call(kv=B.make_shape(200, 512, 8, 256, 1)) == B.GSRQ_E_ARG      # D != Hkv * hd
+    assert call(kv=B.make_shape(200, 1024, 8, 256, 2)) == B.GSRQ_E_UNSUPPORTED
+    assert call(kv=B.make_shape(200, 1024, 16, 256, 1)) == B.GSRQ_E_UNSUPPORTED
+    assert call(kv=B.make_shape(200, 1024, 8, 128, 1)) == B.GSRQ_E_UNSUPPORTED
+    assert call(q=None) == B.GSRQ_E_ARG
+    assert call(len=None) == B.GSRQ_E_ARG
+    assert call(kc=D + 4) == B.GSRQ_E_ARG                       # codes not 16-byte aligned
+    assert call(dt=3) == B.GSRQ_E_ARG
+    assert call(ws=D + 16) == B.GSRQ_E_ARG                      # workspace alignment
+    assert call(ws_bytes=1) == B.GSRQ_E_WORKSPACE
+    ash = B.make_attn_shape(**a0)
+    n = ctypes.c_size_t()
+    assert lib.gsrq_attn_workspace_bytes(ctypes.byref(ash), ctypes.byref(n)) == B.GSRQ_OK
+    assert n.value >= 2 * 8 * 4 * 130 * 4
+    bad = B.make_attn_shape(**a0, rope_base=0.0)
+    assert lib.gsrq_attn_workspace_bytes(ctypes.byref(bad), ctypes.byref(n)) == B.GSRQ_E_ARG

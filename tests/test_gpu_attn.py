@@ -1,0 +1,174 @@
+"""GPU parity of one decoding step of attention over coded caches
+(gsrq_attn_decode, the fused unpack + dequantise + RoPE + attention kernel
+of Appendix C) against the float64 oracle, through the C ABI.
+
+Inputs come from synth.attn_case (seeded codebooks, codes and queries).  The
+oracle decodes the codes itself (unpack_codes, then g * s), takes the keys'
+float16 decode (g * s rounded to float32, then float16: the keys the library
+declares it reads) and float32-rounded value codewords, and computes the
+attention in float64 (attn_weights / attn_decode).
+
+Tolerance, derived from the kernel's arithmetic (every term is a bound on
+one rounding step; u = 2^-24):
+  * scores: query and rotated keys enter the matrix cores as hi + lo float16
+    pairs (three products per element, the lo.lo product dropped, |lo| <=
+    2^-11 |hi|), after float32 rotations whose error is a few u per element:
+    together <= 16 u |q| |k|; the float32 sums of the 3 x 128 exact products
+    add at most 8 sqrt(385) u sum|q'_j k'_j| under the probabilistic rounding
+    model (independent roundings, 8 standard deviations), <= that times
+    |q| |k| by Cauchy-Schwarz.  So |ds| <= eps_s = scale (16 + 8 sqrt(385)) u
+    |q| max_t |k_t|.
+  * weights: a score error eps_s moves every weight by a factor within
+    e^(+-2 eps_s); the float32 scaling, reference subtraction and exp2 add
+    8 u (|s| log2 e + 8) to the exponent.
+  * sums: the value table of a codeword sums <= c_max float32 terms, the
+    softmax denominator <= L: 8 (sqrt(c_max) + sqrt(L)) u relative.
+  * so |o_n - o_ref_n| <= C sum_t p_t |v_tn| (+ 1e-7 max|v| for the float64
+    merge), C = expm1(2 eps_s + 8u (smax + 8)) + 8 (sqrt(c_max) + sqrt(L)) u + 4u.
+The test also reports the worst observed error relative to that bound.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import gsrq_oracle as O
+from tests.gpu_util import say
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+from paper_2607_01065_amd import gsrq as B  # noqa: E402
+
+U = 2.0 ** -24
+BASE = 500000.0
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.load_library()
+
+
+def _dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _run(case, base=BASE):
+    t = {k: _dev(case[k]) for k in ("k_codes", "v_codes", "lens", "k_gain", "k_shape",
+                                    "v_gain", "v_shape")}
+    q = _dev(case["q"])
+    out = B.attn_decode(t["k_codes"], t["v_codes"], t["lens"], t["k_gain"], t["k_shape"],
+                        t["v_gain"], t["v_shape"], q, rope_base=base)
+    torch.cuda.synchronize()
+    return out.cpu().numpy().astype(np.float64)
+
+
+def _decode_rows(codes_rows, gain, shape):
+    """Decoded rows in float32 arithmetic: (float32 g * s) per codeword,
+    from the oracle's own unpacking."""
+    G = gain.shape[1]
+    idx = O.unpack_codes(codes_rows, 1, G, gain.shape[2])[:, 0, :]        # [L, G]
+    cw = gain[0][np.arange(G)[None, :], idx][..., None] * shape[0][np.arange(G)[None, :], idx]
+    return cw.astype(np.float32).reshape(codes_rows.shape[0], -1)          # [L, D] float32
+
+
+def _reference(case, b, heads=None, base=BASE):
+    """Oracle output [Hq, 128] and per-element tolerance for sequence b."""
+    Hkv, GQ = case["Hkv"], case["GQ"]
+    Hq, hd = Hkv * GQ, 128
+    cap = case["k_codes"].shape[1]
+    L = int(min(max(int(case["lens"][b]), 0), cap))
+    q = case["q"][b].astype(np.float64)
+    ref = np.zeros((Hq, hd))
+    tol = np.zeros((Hq, hd))
+    if L == 0:
+        return ref, tol + 1e-30
+    k16 = _decode_rows(case["k_codes"][b, :L], case["k_gain"], case["k_shape"])
+    k16 = k16.astype(np.float16).astype(np.float64).reshape(L, Hkv, hd)
+    v32 = _decode_rows(case["v_codes"][b, :L], case["v_gain"], case["v_shape"])
+    v32 = v32.astype(np.float64).reshape(L, Hkv, hd)
+    p, s = O.attn_weights(q, k16, base)
+    scale = 1.0 / math.sqrt(hd)
+    vcodes = O.unpack_codes(case["v_codes"][b, :L], 1, Hkv * 16, 256)[:, 0, :]
+    cmax = max(int(np.max(np.bincount(vcodes[:, g], minlength=256))) for g in range(Hkv * 16))
+    for h in range(Hq) if heads is None else heads:
+        kv = h // GQ
+        ref[h] = p[h] @ v32[:, kv]
+        kmax = float(np.max(np.linalg.norm(k16[:, kv], axis=1)))
+        eps_s = scale * (16 + 8 * math.sqrt(385)) * U * np.linalg.norm(q[h]) * kmax
+        smax = float(np.max(np.abs(s[h]))) * math.log2(math.e)
+        C = (math.expm1(2 * eps_s + 8 * U * (smax + 8)) + 8 * (math.sqrt(cmax) + math.sqrt(L)) * U
+             + 4 * U)
+        tol[h] = C * (p[h] @ np.abs(v32[:, kv])) + 1e-7 * float(np.max(np.abs(v32[:, kv])))
+    return ref, tol
+
+
+def _check(case, out, heads=None, what=""):
+    worst = 0.0
+    for b in range(out.shape[0]):
+        ref, tol = _reference(case, b, heads)
+        hs = range(out.shape[1]) if heads is None else heads
+        for h in hs:
+            err = np.abs(out[b, h] - ref[h])
+            assert np.all(err <= tol[h]), (
+                f"{what} b{b} h{h}: err {err.max():.3g} > tol {tol[h][err.argmax()]:.3g} "
+                f"(ref {ref[h][err.argmax()]:.4g})")
+            worst = max(worst, float(np.max(err / tol[h])))
+    say(what, "worst err / tolerance", f"{worst:.3g}")
+    return worst
+
+
+@pytest.mark.parametrize("Bn,cap,lens,Hkv,GQ,qdt", [
+    (1, 40, [37], 1, 4, "float32"),                # one partial block pair
+    (3, 5000, [5000, 1, 0], 2, 4, "float32"),      # ragged: full, one token, empty
+    (2, 3000, [2999, 1025], 3, 2, "float16"),      # GQ = 2, float16 queries
+    (2, 4100, [4097, 64], 2, 1, "float32"),        # GQ = 1 (32 blocks per wave group)
+    (2, 2048, [2048, 2000], 8, 4, "float16"),      # 8 heads: 1024-wide rows
+    (2, 700, [900, -3], 1, 4, "float32"),          # lengths clamped to [0, cap]
+])
+def test_attn_decode_parity(Bn, cap, lens, Hkv, GQ, qdt):
+    say("attn parity", Bn, cap, lens, Hkv, GQ, qdt)
+    case = synth.attn_case(Bn, cap, lens, Hkv, GQ, seed=41, q_dtype=qdt)
+    out = _run(case)
+    assert np.all(np.isfinite(out))
+    _check(case, out, what=f"attn {Bn}x{cap} GQ{GQ}")
+    for b, L in enumerate(lens):
+        if L <= 0:
+            assert np.all(out[b] == 0.0)
+
+
+def test_attn_decode_peaked_and_rising_scores():
+    """Peaked softmax (queries x 3), and keys whose scores jump in the later
+    rounds of a chunk (large-gain codewords used only after token 2500), so
+    the reference maximum is raised and the value tables rescaled."""
+    case = synth.attn_case(2, 6000, [6000, 5300], 2, 4, seed=42, q_scale=3.0)
+    G = case["k_gain"].shape[1]
+    case["k_gain"][0, :, 255] *= 4.0
+    kb = case["k_codes"].view(np.uint8).reshape(2, 6000, G)
+    kb[:, :2500][kb[:, :2500] == 255] = 0
+    kb[:, 2500::7, :] = 255
+    say("attn peaked / rising")
+    out = _run(case)
+    _check(case, out, what="attn rising")
+
+
+def test_attn_decode_full_size_sampled():
+    """The benchmark's shape: 8 sequences x 32768 tokens, 8 key/value heads,
+    32 query heads, one chunking of the launch; a few (sequence, head) pairs
+    against the oracle."""
+    Bn, cap, Hkv, GQ = 8, 32768, 8, 4
+    lens = [32768, 32768, 30001, 32768, 17, 32768, 32767, 1]
+    case = synth.attn_case(Bn, cap, lens, Hkv, GQ, seed=43, q_dtype="float16")
+    say("attn full size sampled")
+    out = _run(case)
+    assert np.all(np.isfinite(out))
+    for b in (0, 2, 4, 6, 7):
+        heads = [0, 13, 31] if b != 2 else [5, 22]
+        ref, tol = _reference(case, b, heads)
+        for h in heads:
+            err = np.abs(out[b, h] - ref[h])
+            assert np.all(err <= tol[h]), f"b{b} h{h}: {err.max():.3g} > {tol[h][err.argmax()]:.3g}"
+
