@@ -190,9 +190,10 @@ def full_cache(args, wl):
 
 def extra_paths(B, cache, wl, dev, reps=50):
     """Measured after the timed region, outside `value`: per-token weights
-    from gradient rows of the layer's shape (Sec. 5.3, Appendix B), and the
+    from gradient rows of the layer's shape (Sec. 5.3, Appendix B), the
     encode latency of a few appended tokens with the layer's trained codebook
-    (the per-step append of autoregressive decoding)."""
+    (the per-step append of autoregressive decoding), and one decoding step
+    of attention over coded caches (Appendix C)."""
     import torch
 
     import synth
@@ -224,7 +225,83 @@ def extra_paths(B, cache, wl, dev, reps=50):
         torch.cuda.synchronize()
         app[str(n)] = e0.elapsed_time(e1) / reps * 1e3
     out["append_encode_us"] = app
+    out.update(attention_measure(B, dev))
     return out
+
+
+ATTN_SHAPE = dict(B=8, cap=32768, Hkv=8, GQ=4)   # LLaMA-3-8B heads, 32K-token context
+
+
+def attention_measure(B, dev, reps=50, shape=ATTN_SHAPE):
+    """One decoding step of attention over 1-bit coded K/V caches
+    (gsrq_attn_decode: unpack, dequantise, RoPE, attention) for 8 sequences
+    of 32768 tokens, 32 query / 8 key-value heads, next to float16 attention
+    over an already dequantised and rotated cache of the same shape (two
+    float16 matmuls and a float32 softmax, reading 1.07 GB)."""
+    import math
+
+    import torch
+
+    import synth
+    Bn, cap, Hkv, GQ = shape["B"], shape["cap"], shape["Hkv"], shape["GQ"]
+    Hq = Hkv * GQ
+    case = synth.attn_case(Bn, cap, [cap] * Bn, Hkv, GQ, seed=0, q_dtype="float16")
+    t = {k: torch.from_numpy(case[k]).to(dev) for k in
+         ("k_codes", "v_codes", "lens", "k_gain", "k_shape", "v_gain", "v_shape", "q")}
+    ws = torch.empty(B.attn_workspace_bytes(Bn, cap, Hq, Hkv), dtype=torch.uint8, device=dev)
+    out = torch.empty((Bn, Hq, HEAD_DIM), dtype=torch.float32, device=dev)
+
+    def call():
+        B.attn_decode(t["k_codes"], t["v_codes"], t["lens"], t["k_gain"], t["k_shape"],
+                      t["v_gain"], t["v_shape"], t["q"], out=out, workspace=ws)
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    call_us = timed(call)
+    B.timing_enable(True, kinds=["attention"])
+    timed(call)
+    tim = B.timing_read()
+    B.timing_enable(False)
+    kern_us = tim["attention"][0] / tim["attention"][1] * 1e3
+    tok_heads = Bn * cap * Hkv
+    code_bytes = 2 * tok_heads * 16                  # 8-bit codes of 16 subspaces, K and V
+    G = Hkv * 16
+    cb_bytes = 2 * G * 256 * 9 * 4                   # both codebooks (gain + 8-element shape)
+    io_bytes = Bn * Hq * HEAD_DIM * (2 + 4)          # float16 queries in, float32 out
+    alg_bytes = code_bytes + cb_bytes + io_bytes
+    del t, ws, out, case
+    # float16 attention over a dequantised, rotated cache of the same shape
+    scale = 1.0 / math.sqrt(HEAD_DIM)
+    kT = torch.randn((Bn * Hkv, HEAD_DIM, cap), dtype=torch.float16, device=dev)
+    vf = torch.randn((Bn * Hkv, cap, HEAD_DIM), dtype=torch.float16, device=dev)
+    qf = torch.randn((Bn * Hkv, GQ, HEAD_DIM), dtype=torch.float16, device=dev)
+
+    def fp16_attn():
+        s = torch.matmul(qf, kT).float() * scale
+        torch.matmul(torch.softmax(s, dim=-1).half(), vf)
+
+    fp16_us = timed(fp16_attn)
+    del kT, vf, qf
+    return {"decode_attention": {
+        "shape": f"{Bn} seq x {cap} tok, {Hq} q / {Hkv} kv heads x {HEAD_DIM}, 1-bit K/V "
+                 f"(d=8 K=256 M=1), RoPE base 500000",
+        "call_us": call_us, "kernel_us": kern_us,
+        "token_heads_per_s": tok_heads / (call_us * 1e-6),
+        "algorithmic_bytes": alg_bytes,
+        "hbm_GBps": alg_bytes / (kern_us * 1e-6) / 1e9,
+        "hbm_frac": alg_bytes / (kern_us * 1e-6) / 1e9 / PEAK_HBM_GBPS,
+        "fp16_attention_us": fp16_us,
+        "speedup_vs_fp16_attention": fp16_us / call_us}}
 
 
 def breakdown(B, step):
@@ -253,6 +330,17 @@ def main():
     B.load_library()
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
+    if args.workload == "decode_attention_1bit":
+        r = attention_measure(B, torch.device("cuda", 0), reps=args.steps)["decode_attention"]
+        print(json.dumps({"metric": "decode attention token-heads/s over 1-bit coded K/V",
+                          "value": r["token_heads_per_s"], "unit": "token-heads/s",
+                          "n_gpus": 1, "steps": args.steps, "warmup": 1,
+                          "ms_per_step": r["call_us"] / 1e3, "higher_is_better": True,
+                          "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+                          "data": "synthetic",
+                          "config": {"workload": "decode_attention_1bit", "shape": r["shape"]},
+                          **{k: v for k, v in r.items() if k != "shape"}}), flush=True)
+        return
     wl = synth.WORKLOADS[args.workload]
     if args.stages > 0:
         import dataclasses

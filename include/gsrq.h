@@ -255,11 +255,12 @@ gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes);
  *  q, q_dtype        [B][Hq][head_dim] queries, 16-byte aligned.
  *  out               [B][Hq][head_dim] float32.
  *  workspace         >= gsrq_attn_workspace_bytes(a), 256-byte aligned.
- * Precision: keys enter as their float16 decode (g * s rounded to float32,
- * then to float16); the rotated query and keys are rounded to float16 for
- * their dot products, which are summed in float32; softmax weights and the
- * value sums are float32 with float32 value codewords; chunks are merged in
- * float64.  This build: head_dim = 128 and Hq / Hkv in {1, 2, 4}.
+ * Precision: keys and values enter as their float16 decode (g * s rounded
+ * to float32, then to float16, as gsrq_decode's float16 output); the
+ * rotated query and keys, and the softmax weights, enter the matrix
+ * products as hi + lo float16 pairs (about 22 bits), with float32 sums;
+ * chunks are merged in float64.  This build: head_dim = 128 and
+ * Hq / Hkv in {1, 2, 4}.
  */
 gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
                              const uint32_t* k_codes, const uint32_t* v_codes,

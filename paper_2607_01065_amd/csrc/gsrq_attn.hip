@@ -6,27 +6,29 @@
 // 128-element heads (16 subspaces per head), grouped-query attention with
 // GQ = Hq / Hkv in {1, 2, 4}.
 //
-// One workgroup owns (sequence, key/value head, chunk of tokens) and runs
-// rounds of 4096 / GQ tokens:
-//  * Scores on the matrix cores.  A wave takes U = 32 / GQ blocks of 32
-//    tokens.  The A operand of a v_mfma_f32_32x32x16_f16 holds 32 tokens'
-//    keys (each lane one 8-element codeword gathered from a float16 table of
-//    the head's 16 codebooks in LDS, rotated in float32); the B operand's 32
-//    columns are the GQ query heads of the U blocks.  Both sides enter as
-//    hi + lo float16 pairs (three products per k-step), so scores carry
-//    about 22 bits, as a float32 dot product would.  RoPE enters as a relative rotation:
-//    score(i) = (R_{pq - 32b} q) . (R_t k_i) for token i = 32 b + t, so the
-//    rotation of a key depends only on its row t in the block (fixed per
-//    lane) and that of the query on the block (one sine/cosine per lane per
-//    wave group).
-//  * Softmax weights in float32 with a workgroup-wide reference maximum per
-//    query head (raised, and the partial sums rescaled, when a round's
+// One workgroup owns (sequence, key/value head, chunk of tokens); its four
+// waves work through groups of U = 32 / GQ blocks of 32 tokens
+// independently (flash-decoding within the chunk):
+//  * Scores on the matrix cores.  The A operand of a v_mfma_f32_32x32x16_f16
+//    holds 32 tokens' keys (each lane one 8-element codeword gathered from a
+//    float16 table of the head's 16 codebooks in LDS, rotated in float32);
+//    the B operand's 32 columns are the GQ query heads of the U blocks of a
+//    group.  Both sides enter as hi + lo float16 pairs (three products per
+//    k-step), so scores carry about 22 bits, as a float32 dot product would.
+//    RoPE enters as a relative rotation: score(i) = (R_{pq - 32b} q) .
+//    (R_t k_i) for token i = 32 b + t, so the rotation of a key depends only
+//    on its row t in the block (fixed per lane) and that of the query on the
+//    group (one sine/cosine per lane per group).
+//  * Softmax per wave with a running reference maximum per query head
+//    (raised by a margin, with the wave's sums rescaled, when a block's
 //    scores exceed it).
-//  * Values without dequantisation.  The softmax weight p of token i is
-//    added to a per-head table H[g][k] at the token's value code k of every
-//    subspace g (float32 LDS atomics); at the end of the chunk the output
-//    is H times the value codebook, o[8g + e] = sum_k H[g][k] c_g,k[e].
-//  * A second kernel merges the chunks of every (sequence, query head) with
+//  * Values on the matrix cores: the weights leave the score accumulators
+//    already in the A-operand layout of the value product (hi + lo float16),
+//    and the B operand gathers each token's float16 value codeword element
+//    from a second LDS table, in the transposed layout the product needs,
+//    through the block's value codes staged in LDS by subspace.
+//  * The waves' partial results are merged at the end of the chunk, and a
+//    second kernel merges the chunks of every (sequence, query head) with
 //    their reference maxima (the split form of one softmax).
 #include <algorithm>
 
@@ -43,19 +45,20 @@ constexpr int AT_BLK = 32;            // tokens per MFMA block
 constexpr int AT_PART = AT_HD + 2;    // partial record: o[128], reference max, sum
 constexpr int AT_TARGET_WG = 512;     // workgroups aimed for per launch (2 per CU)
 constexpr float AT_HEADROOM = 8.f;    // log2 margin of a raised reference maximum
-constexpr int AT_HSTRIDE = AT_SUB * AT_K;   // floats of one head's value table
+constexpr float AT_PSHIFT = 15.f;     // weights 2^(s - m + 15) <= 2^15: float16 range
+constexpr int AT_TAB = AT_SUB * AT_K * 8;   // float16 elements of one codeword table
+constexpr int AT_RED = 8 + 4 * AT_HD;       // floats per wave in the final merge
 
 template <int GQ> struct AtCfg {
   static constexpr int U = 32 / GQ;                         // blocks per wave group
-  static constexpr int ROUND = AT_WAVES * U * AT_BLK;       // tokens per round
-  static constexpr int TOK_PT = ROUND / AT_THREADS;         // tokens per thread when summing
+  static constexpr int ROUND = AT_WAVES * U * AT_BLK;       // tokens of one group per wave
   // LDS layout in bytes
-  static constexpr int KTAB = 0;                                      // f16 [16][256][8]
-  static constexpr int HIST = KTAB + AT_SUB * AT_K * 8 * 2;           // f32 [GQ][16][256]
-  static constexpr int STAGE = HIST + GQ * AT_HSTRIDE * 4;            // f32 [WAVES*U][GQ][32]
-  static constexpr int ANG = STAGE + AT_WAVES * U * GQ * AT_BLK * 4;  // float2 [WAVES][64]
-  static constexpr int RED = ANG + AT_WAVES * 64 * 8;                 // f32 [2][WAVES][4]
-  static constexpr int BYTES = RED + 2 * AT_WAVES * 4 * 4;
+  static constexpr int KTAB = 0;                            // f16 [16][256][8] keys
+  static constexpr int VTAB = KTAB + AT_TAB * 2;            // f16 [16][256][8] values
+  static constexpr int VCS = VTAB + AT_TAB * 2;             // u8 [WAVES][16][32] value codes
+  static constexpr int ANG = VCS + AT_WAVES * AT_SUB * AT_BLK;      // float2 [WAVES][64]
+  static constexpr int RED = ANG + AT_WAVES * 64 * 8;               // f32 [WAVES][AT_RED]
+  static constexpr int BYTES = RED + AT_WAVES * AT_RED * 4;
 };
 static_assert(AtCfg<4>::BYTES <= 160 * 1024, "LDS budget");
 
@@ -99,29 +102,21 @@ __device__ __forceinline__ void split16(float v, _Float16& hi, _Float16& lo) {
   lo = (_Float16)(v - (float)hi);
 }
 
-__device__ __forceinline__ float wave_max_keep(float v, int keep_mask) {
-  // max over the lanes that differ from this one only in bits outside keep_mask
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1)
-    if (!(off & keep_mask)) v = fmaxf(v, __shfl_xor(v, off));
-  return v;
-}
-
 template <int GQ>
 __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
   using C = AtCfg<GQ>;
   constexpr int U = C::U;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   _Float16* ktab = (_Float16*)(lds + C::KTAB);
-  float* hist = (float*)(lds + C::HIST);
-  float* stage = (float*)(lds + C::STAGE);
-  float2* ang = (float2*)(lds + C::ANG);
+  _Float16* vtab = (_Float16*)(lds + C::VTAB);
   float* red = (float*)(lds + C::RED);
 
   const int chunk = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int tl = lane & 31, hh = lane >> 5;
   const int ul = tl / GQ, hl = tl % GQ;      // B-operand column: block variant, query head
+  unsigned char* vcs = lds + C::VCS + w * AT_SUB * AT_BLK;
+  float2* ang = (float2*)(lds + C::ANG) + w * 64;
   const int len = min(max(a.seq_len[b], 0), a.cap);
   const int tok0 = chunk * a.rpc * C::ROUND;
   float* outp = a.part + (((size_t)b * a.Hkv + hk) * a.nch + chunk) * GQ * AT_PART;
@@ -132,26 +127,28 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
     }
     return;
   }
+  const int tend = min(len, tok0 + a.rpc * C::ROUND);
   const int Hq = a.Hkv * GQ;
   const int g0 = hk * AT_SUB;
   const size_t seq_row0 = (size_t)b * a.cap;
 
-  // key codeword table: fp16(fp32(g * s)), the float16 decode of a codeword
+  // codeword tables: fp16(fp32(g * s)), the float16 decode of a codeword
   for (int i = tid; i < AT_SUB * AT_K * 2; i += AT_THREADS) {
     const int cw = i >> 1, half = i & 1;
-    const float gk = a.kg[(size_t)g0 * AT_K + cw];
-    const f4 s = *(const f4*)(a.ks + ((size_t)g0 * AT_K + cw) * 8 + half * 4);
-    uint2 v;
-    v.x = pack2((_Float16)(gk * s[0]), (_Float16)(gk * s[1]));
-    v.y = pack2((_Float16)(gk * s[2]), (_Float16)(gk * s[3]));
-    *(uint2*)(ktab + cw * 8 + half * 4) = v;
+    const size_t src = ((size_t)g0 * AT_K + cw) * 8 + half * 4;
+    const float gk = a.kg[(size_t)g0 * AT_K + cw], gv = a.vg[(size_t)g0 * AT_K + cw];
+    const f4 sk = *(const f4*)(a.ks + src), sv = *(const f4*)(a.vs + src);
+    *(uint2*)(ktab + cw * 8 + half * 4) =
+        make_uint2(pack2((_Float16)(gk * sk[0]), (_Float16)(gk * sk[1])),
+                   pack2((_Float16)(gk * sk[2]), (_Float16)(gk * sk[3])));
+    *(uint2*)(vtab + cw * 8 + half * 4) =
+        make_uint2(pack2((_Float16)(gv * sv[0]), (_Float16)(gv * sv[1])),
+                   pack2((_Float16)(gv * sv[2]), (_Float16)(gv * sv[3])));
   }
-  for (int i = tid; i < GQ * AT_HSTRIDE / 4; i += AT_THREADS) ((f4*)hist)[i] = f4{0.f, 0.f, 0.f, 0.f};
 
-  // lane constants: R_t for the lane's token row, and the query of its
-  // column turned by R_{-32u}; element m < 32 of a lane is head element
-  // jd = 32 hh + m, paired with jd + 64
-  float ct[32], st[32], qx[32], qy[32];
+  // lane constant: R_t for the lane's token row; element m < 32 of a lane
+  // is head element jd = 32 hh + m, paired with jd + 64
+  float ct[32], st[32];
   {
     const float4* t1 = (const float4*)(a.t1 + tl * 64 + 32 * hh);
 #pragma unroll
@@ -159,241 +156,245 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       const float4 v = t1[m];
       ct[2 * m] = v.x; st[2 * m] = v.y; ct[2 * m + 1] = v.z; st[2 * m + 1] = v.w;
     }
-    const size_t qoff = ((size_t)b * Hq + hk * GQ + hl) * AT_HD + 32 * hh;
-    if (a.q_f16) {
-      const u4* qp = (const u4*)((const _Float16*)a.q + qoff);
-#pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const h8 x = as_h8(qp[m]), y = as_h8(qp[m + 8]);
-#pragma unroll
-        for (int e = 0; e < 8; ++e) { qx[8 * m + e] = (float)x[e]; qy[8 * m + e] = (float)y[e]; }
-      }
-    } else {
-      const f4* qp = (const f4*)((const float*)a.q + qoff);
-#pragma unroll
-      for (int m = 0; m < 8; ++m) {
-        const f4 x = qp[m], y = qp[m + 16];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) { qx[4 * m + e] = x[e]; qy[4 * m + e] = y[e]; }
-      }
-    }
-    const float4* t2 = (const float4*)(a.t2 + ul * 64 + 32 * hh);
-#pragma unroll
-    for (int m = 0; m < 16; ++m) {
-      const float4 v = t2[m];
-#pragma unroll
-      for (int r = 0; r < 2; ++r) {
-        const float c = r ? v.z : v.x, s = r ? v.w : v.y;
-        const float x = qx[2 * m + r], y = qy[2 * m + r];
-        qx[2 * m + r] = x * c + y * s;       // R_{-32u}: angle -32 u theta
-        qy[2 * m + r] = y * c - x * s;
-      }
-    }
   }
+  const size_t qoff = ((size_t)b * Hq + hk * GQ + hl) * AT_HD + 32 * hh;
   const double thl = a.th[lane];
-  float mref[GQ], lsum[GQ];
-#pragma unroll
-  for (int h = 0; h < GQ; ++h) { mref[h] = -INFINITY; lsum[h] = 0.f; }
   __syncthreads();
 
-  for (int r = 0; r < a.rpc; ++r) {
-    const int rt0 = tok0 + r * C::ROUND;
-    if (rt0 >= len) break;
-    // value codes of the tokens this thread sums, fetched before the scores
-    u4 vcode[C::TOK_PT];
+  float mw[GQ];                  // running reference maximum per head (log2 units)
 #pragma unroll
-    for (int k = 0; k < C::TOK_PT; ++k) {
-      const int tok = rt0 + tid + k * AT_THREADS;
-      vcode[k] = tok < len ? *(const u4*)(a.vc + (seq_row0 + tok) * a.W + 4 * hk) : u4{0, 0, 0, 0};
+  for (int h = 0; h < GQ; ++h) mw[h] = -INFINITY;
+  float lsum = 0.f;              // softmax sum of this lane's column (scaled by 2^PSHIFT)
+  f16v o[4] = {};                // value sums: rows = columns (variant, head), cols = dims
+  const int ngroups = (tend - tok0 + 32 * U - 1) / (32 * U);
+  for (int gi = w; gi < ngroups; gi += AT_WAVES) {
+    const int gb0 = (tok0 >> 5) + gi * U;
+    {
+      const int n = (len - 1) - 32 * gb0;           // query-side angle in positions, >= 0
+      double rev = (double)n * thl;
+      rev -= floor(rev);
+      float s, c;
+      sincosf((float)(rev * (2.0 * M_PI)), &s, &c);
+      ang[lane] = make_float2(c, s);
     }
-
-    // ---- scores of this wave's U blocks
-    const int gb0 = (rt0 >> 5) + w * U;
-    if (32 * gb0 < len) {
+    __builtin_amdgcn_wave_barrier();
+    // query of the lane's column turned by R_{pq - 32 gb0} R_{-32u} (its
+    // block's relative rotation), split hi + lo into float16 pairs; loaded
+    // again for every group so that no float32 copy stays live
+    u4 bqh[8], bql[8];
+    {
+      int zero = 0;
+      asm volatile("" : "+s"(zero));
+      float qx[32], qy[32];
+      if (a.q_f16) {
+        const u4* qp = (const u4*)((const _Float16*)a.q + qoff + zero);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+          const h8 x = as_h8(qp[m]), y = as_h8(qp[m + 8]);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) { qx[8 * m + e] = (float)x[e]; qy[8 * m + e] = (float)y[e]; }
+        }
+      } else {
+        const f4* qp = (const f4*)((const float*)a.q + qoff + zero);
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+          const f4 x = qp[m], y = qp[m + 16];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) { qx[4 * m + e] = x[e]; qy[4 * m + e] = y[e]; }
+        }
+      }
+      const float4* t2 = (const float4*)(a.t2 + ul * 64 + 32 * hh + zero);
+      const float4* ap = (const float4*)(ang + 32 * hh);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        _Float16 xh[8], xl[8], yh[8], yl[8];
+#pragma unroll
+        for (int m2 = 0; m2 < 4; ++m2) {
+          const float4 v2 = t2[4 * i + m2];
+          const float4 v = ap[4 * i + m2];
+#pragma unroll
+          for (int r2 = 0; r2 < 2; ++r2) {
+            const int e = 2 * m2 + r2, m = 8 * i + e;
+            const float c2 = r2 ? v2.z : v2.x, s2 = r2 ? v2.w : v2.y;
+            const float x1 = qx[m] * c2 + qy[m] * s2;     // R_{-32u}
+            const float y1 = qy[m] * c2 - qx[m] * s2;
+            const float c = r2 ? v.z : v.x, s = r2 ? v.w : v.y;
+            split16(x1 * c - y1 * s, xh[e], xl[e]);       // R_{pq - 32 gb0}
+            split16(x1 * s + y1 * c, yh[e], yl[e]);
+          }
+        }
+        bqh[i] = pack_h8(xh); bql[i] = pack_h8(xl);
+        bqh[i + 4] = pack_h8(yh); bql[i + 4] = pack_h8(yl);
+      }
+    }
+    const int nblk = min(U, (len - 32 * gb0 + 31) >> 5);
+    u4 kcn = u4{0, 0, 0, 0}, vcn = u4{0, 0, 0, 0};
+    {
+      const int row = 32 * gb0 + tl;
+      if (row < len) {
+        kcn = *(const u4*)(a.kc + (seq_row0 + row) * a.W + 4 * hk);
+        vcn = *(const u4*)(a.vc + (seq_row0 + row) * a.W + 4 * hk);
+      }
+    }
+    for (int u = 0; u < nblk; ++u) {
+      const u4 kcw = kcn, vcw = vcn;
       {
-        const int n = (len - 1) - 32 * gb0;           // query-side angle in positions, >= 0
-        double rev = (double)n * thl;
-        rev -= floor(rev);
-        float s, c;
-        sincosf((float)(rev * (2.0 * M_PI)), &s, &c);
-        ang[w * 64 + lane] = make_float2(c, s);
+        const int row = 32 * (gb0 + u + 1) + tl;
+        const bool nx = u + 1 < nblk && row < len;
+        kcn = nx ? *(const u4*)(a.kc + (seq_row0 + row) * a.W + 4 * hk) : u4{0, 0, 0, 0};
+        vcn = nx ? *(const u4*)(a.vc + (seq_row0 + row) * a.W + 4 * hk) : u4{0, 0, 0, 0};
+      }
+      // value codes of the block, by subspace: vcs[g][t]; lane half hh
+      // writes subspaces 8 hh .. 8 hh + 7 of its token
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        vcs[(8 * hh + e) * AT_BLK + tl] = (unsigned char)(vcw[2 * hh + (e >> 2)] >> (8 * (e & 3)));
+
+      // ---- scores: pair (i, i + 4) of k-steps holds elements jd and jd + 64;
+      // R_t, then hi + lo float16 pairs; scores = khi.qhi + khi.qlo + klo.qhi
+      f16v acc = {};
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int cx = (kcw[hh] >> (8 * i)) & 255, cy = (kcw[2 + hh] >> (8 * i)) & 255;
+        const h8 x = as_h8(*(const u4*)(ktab + ((4 * hh + i) * AT_K + cx) * 8));
+        const h8 y = as_h8(*(const u4*)(ktab + ((8 + 4 * hh + i) * AT_K + cy) * 8));
+        _Float16 xh[8], xl[8], yh[8], yl[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float xf = (float)x[e], yf = (float)y[e];
+          const float c = ct[8 * i + e], s = st[8 * i + e];
+          split16(xf * c - yf * s, xh[e], xl[e]);
+          split16(xf * s + yf * c, yh[e], yl[e]);
+        }
+        const h8 kxh = as_h8(pack_h8(xh)), kxl = as_h8(pack_h8(xl));
+        const h8 kyh = as_h8(pack_h8(yh)), kyl = as_h8(pack_h8(yl));
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxl, as_h8(bqh[i]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxh, as_h8(bql[i]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxh, as_h8(bqh[i]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyl, as_h8(bqh[i + 4]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bql[i + 4]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bqh[i + 4]), acc, 0, 0, 0);
+      }
+
+      // ---- softmax weights of this block (only the columns of variant u)
+      // register v holds token row t = 8 (v / 4) + 4 hh + v % 4
+      const int rowb = 32 * (gb0 + u);
+      float sc[16];
+      float ml = -INFINITY;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int t = 8 * (v >> 2) + 4 * hh + (v & 3);
+        sc[v] = (ul == u && rowb + t < len) ? acc[v] * a.qscale : -INFINITY;
+        ml = fmaxf(ml, sc[v]);
+      }
+      ml = fmaxf(ml, __shfl_xor(ml, 32));
+#pragma unroll
+      for (int h = 0; h < GQ; ++h) {
+        const float mb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ml), u * GQ + h));
+        if (mb > mw[h]) {                            // uniform
+          const float nref = mb + AT_HEADROOM;
+          if (mw[h] > -INFINITY) {
+            const float fac = exp2f(mw[h] - nref);
+            if (hl == h) lsum *= fac;
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+              for (int v = 0; v < 16; ++v)
+                if ((v & 3) % GQ == h) o[c][v] *= fac;
+          }
+          mw[h] = nref;
+        }
+      }
+      float mine = mw[0];
+#pragma unroll
+      for (int h = 1; h < GQ; ++h) mine = hl == h ? mw[h] : mine;
+      u4 ph[2], pl[2];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        _Float16 xh[8], xl[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float sv = sc[8 * s2 + e];
+          const float pv = sv == -INFINITY ? 0.f : exp2f(sv - mine + AT_PSHIFT);
+          lsum += pv;
+          split16(pv, xh[e], xl[e]);
+        }
+        ph[s2] = pack_h8(xh);
+        pl[s2] = pack_h8(xl);
+      }
+
+      // ---- value sums: o[c] += P . V, V gathered in the k order of P
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const int g = 4 * c + (tl >> 3), e = tl & 7;
+        const unsigned char* cp = vcs + g * AT_BLK + 4 * hh;
+        const _Float16* vt = vtab + g * AT_K * 8 + e;
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const uint32_t c0 = *(const uint32_t*)(cp + 16 * s2);
+          const uint32_t c1 = *(const uint32_t*)(cp + 16 * s2 + 8);
+          _Float16 vv[8];
+#pragma unroll
+          for (int e2 = 0; e2 < 4; ++e2) {
+            vv[e2] = vt[((c0 >> (8 * e2)) & 255) * 8];
+            vv[4 + e2] = vt[((c1 >> (8 * e2)) & 255) * 8];
+          }
+          const h8 vb = as_h8(pack_h8(vv));
+          o[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pl[s2]), vb, o[c], 0, 0, 0);
+          o[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), vb, o[c], 0, 0, 0);
+        }
       }
       __builtin_amdgcn_wave_barrier();
-      // rotated query of every column, split hi + lo into float16 pairs
-      u4 bqh[8], bql[8];
-      {
-        const float4* ap = (const float4*)(ang + w * 64 + 32 * hh);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          _Float16 xh[8], xl[8], yh[8], yl[8];
-#pragma unroll
-          for (int m2 = 0; m2 < 4; ++m2) {
-            const float4 v = ap[4 * i + m2];
-#pragma unroll
-            for (int r2 = 0; r2 < 2; ++r2) {
-              const int e = 2 * m2 + r2, m = 8 * i + e;
-              const float c = r2 ? v.z : v.x, s = r2 ? v.w : v.y;
-              split16(qx[m] * c - qy[m] * s, xh[e], xl[e]);
-              split16(qx[m] * s + qy[m] * c, yh[e], yl[e]);
-            }
-          }
-          bqh[i] = pack_h8(xh); bql[i] = pack_h8(xl);
-          bqh[i + 4] = pack_h8(yh); bql[i + 4] = pack_h8(yl);
-        }
-      }
-      const int nblk = min(U, (len - 32 * gb0 + 31) >> 5);
-      u4 kcn = u4{0, 0, 0, 0};
-      {
-        const int row = 32 * gb0 + tl;
-        if (row < len) kcn = *(const u4*)(a.kc + (seq_row0 + row) * a.W + 4 * hk);
-      }
-      for (int u = 0; u < nblk; ++u) {
-        const u4 kcw = kcn;
-        {
-          const int row = 32 * (gb0 + u + 1) + tl;
-          kcn = (u + 1 < nblk && row < len) ? *(const u4*)(a.kc + (seq_row0 + row) * a.W + 4 * hk)
-                                             : u4{0, 0, 0, 0};
-        }
-        u4 ak[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const uint32_t word = i < 4 ? kcw[hh] : kcw[2 + hh];
-          const int code = (word >> (8 * (i & 3))) & 255;
-          const int sub = i < 4 ? 4 * hh + i : 8 + 4 * hh + (i - 4);
-          ak[i] = *(const u4*)(ktab + (sub * AT_K + code) * 8);
-        }
-        // R_t, then hi + lo float16 pairs; scores = khi.qhi + khi.qlo + klo.qhi
-        u4 akl[8];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const h8 x = as_h8(ak[i]), y = as_h8(ak[i + 4]);
-          _Float16 xh[8], xl[8], yh[8], yl[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float xf = (float)x[e], yf = (float)y[e];
-            const float c = ct[8 * i + e], s = st[8 * i + e];
-            split16(xf * c - yf * s, xh[e], xl[e]);
-            split16(xf * s + yf * c, yh[e], yl[e]);
-          }
-          ak[i] = pack_h8(xh); akl[i] = pack_h8(xl);
-          ak[i + 4] = pack_h8(yh); akl[i + 4] = pack_h8(yl);
-        }
-        f16v acc = {};
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(akl[i]), as_h8(bqh[i]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ak[i]), as_h8(bql[i]), acc, 0, 0, 0);
-          acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ak[i]), as_h8(bqh[i]), acc, 0, 0, 0);
-        }
-        if (ul == u) {
-          float* sp = stage + ((w * U + u) * GQ + hl) * AT_BLK + 4 * hh;
-#pragma unroll
-          for (int q4 = 0; q4 < 4; ++q4)
-            *(f4*)(sp + 8 * q4) = f4{acc[4 * q4] * a.qscale, acc[4 * q4 + 1] * a.qscale,
-                                     acc[4 * q4 + 2] * a.qscale, acc[4 * q4 + 3] * a.qscale};
-        }
-      }
     }
-    __syncthreads();
-
-    // ---- round maximum per query head; raise the reference if exceeded
-    {
-      const int run = tid >> 1, h = run % GQ, blk = run / GQ;
-      const int qi0 = blk * AT_BLK + (tid & 1) * 16;
-      const f4* sp = (const f4*)(stage + run * AT_BLK + (tid & 1) * 16);
-      float m = -INFINITY;
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const f4 x = sp[v];
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          if (rt0 + qi0 + 4 * v + e < len) m = fmaxf(m, x[e]);
-      }
-      m = wave_max_keep(m, 2 * (GQ - 1));
-      if (lane < 2 * GQ && !(lane & 1)) red[w * 4 + (lane >> 1)] = m;
-      (void)h;
-    }
-    __syncthreads();
-    bool rescale = false;
-    float fac[GQ];
-#pragma unroll
-    for (int h = 0; h < GQ; ++h) {
-      float m = red[h];
-#pragma unroll
-      for (int v = 1; v < AT_WAVES; ++v) m = fmaxf(m, red[v * 4 + h]);
-      fac[h] = 1.f;
-      if (m > mref[h]) {
-        const float nref = m + AT_HEADROOM;
-        if (mref[h] > -INFINITY) {
-          fac[h] = exp2f(mref[h] - nref);
-          rescale = true;
-        }
-        mref[h] = nref;
-      }
-    }
-    if (rescale) {
-#pragma unroll
-      for (int h = 0; h < GQ; ++h) {
-        if (fac[h] == 1.f) continue;
-        lsum[h] *= fac[h];
-        f4* hp = (f4*)(hist + h * AT_HSTRIDE) + tid * (AT_HSTRIDE / 4 / AT_THREADS);
-#pragma unroll
-        for (int v = 0; v < AT_HSTRIDE / 4 / AT_THREADS; ++v) hp[v] = hp[v] * fac[h];
-      }
-      __syncthreads();
-    }
-
-    // ---- softmax weights into the value tables
-#pragma unroll
-    for (int k = 0; k < C::TOK_PT; ++k) {
-      const int qi = tid + k * AT_THREADS;
-      if (rt0 + qi >= len) continue;
-      const float* sp = stage + (qi >> 5) * GQ * AT_BLK + (qi & 31);
-      float p[GQ];
-#pragma unroll
-      for (int h = 0; h < GQ; ++h) {
-        p[h] = exp2f(sp[h * AT_BLK] - mref[h]);
-        lsum[h] += p[h];
-      }
-#pragma unroll
-      for (int g = 0; g < AT_SUB; ++g) {
-        const int code = (vcode[k][g >> 2] >> (8 * (g & 3))) & 255;
-        float* hp = hist + g * AT_K + code;
-#pragma unroll
-        for (int h = 0; h < GQ; ++h)
-          __hip_atomic_fetch_add(hp + h * AT_HSTRIDE, p[h], __ATOMIC_RELAXED,
-                                 __HIP_MEMORY_SCOPE_WORKGROUP);
-      }
-    }
-    __syncthreads();
   }
 
-  // ---- chunk result: softmax sums and o = H x value codebook
-  float* lred = red + AT_WAVES * 4;
+  // ---- merge the four waves: per head the reference, the sum and o
+  float* rw = red + w * AT_RED;
+  {
+    float l = lsum;
 #pragma unroll
-  for (int h = 0; h < GQ; ++h) {
-    float v = lsum[h];
+    for (int off = GQ; off < 64; off <<= 1) l += __shfl_xor(l, off);
+    if (lane < GQ) {
+      rw[lane] = mw[0];
 #pragma unroll
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if (lane == 0) lred[w * 4 + h] = v;
+      for (int h = 1; h < GQ; ++h)
+        if (lane == h) rw[lane] = mw[h];
+      rw[4 + lane] = l;
+    }
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int h = 0; h < GQ; ++h) {
+        float v = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if ((r & 3) % GQ == h) v += o[c][r];
+        v += __shfl_xor(v, 32);
+        if (hh == 0) rw[8 + h * AT_HD + 32 * c + tl] = v;
+      }
   }
   __syncthreads();
-  for (int o = tid; o < GQ * AT_HD; o += AT_THREADS) {
-    const int h = o / AT_HD, n = o % AT_HD, g = n >> 3, e = n & 7;
-    const float* gp = a.vg + (size_t)(g0 + g) * AT_K;
-    const float* sp = a.vs + (size_t)(g0 + g) * AT_K * 8 + e;
-    const float* hp = hist + h * AT_HSTRIDE + g * AT_K;
-    double acc = 0.0;
-#pragma unroll 8
-    for (int k = 0; k < AT_K; ++k) acc += (double)hp[k] * (double)(gp[k] * sp[8 * k]);
-    outp[h * AT_PART + n] = (float)acc;
-  }
-  if (tid < GQ) {
-    float l = 0.f;
+  for (int i = tid; i < GQ * AT_HD; i += AT_THREADS) {
+    const int h = i / AT_HD, n = i % AT_HD;
+    float M = -INFINITY;
 #pragma unroll
-    for (int v = 0; v < AT_WAVES; ++v) l += lred[v * 4 + tid];
-    outp[tid * AT_PART + AT_HD] = mref[tid];
-    outp[tid * AT_PART + AT_HD + 1] = l;
+    for (int v = 0; v < AT_WAVES; ++v)
+      if (red[v * AT_RED + 4 + h] > 0.f) M = fmaxf(M, red[v * AT_RED + h]);
+    double num = 0.0, den = 0.0;
+#pragma unroll
+    for (int v = 0; v < AT_WAVES; ++v) {
+      const float* r = red + v * AT_RED;
+      if (!(r[4 + h] > 0.f)) continue;
+      const double f = exp2((double)r[h] - (double)M);
+      num += f * (double)r[8 + h * AT_HD + n];
+      den += f * (double)r[4 + h];
+    }
+    outp[h * AT_PART + n] = (float)num;
+    if (n == 0) {
+      outp[h * AT_PART + AT_HD] = M - AT_PSHIFT;
+      outp[h * AT_PART + AT_HD + 1] = (float)den;
+    }
   }
 }
 
