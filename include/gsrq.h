@@ -250,8 +250,8 @@ gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes);
  *                    i of sequence b in row b * cap + i; 16-byte aligned.
  *  seq_len           [B] int32 (device), clamped to [0, cap]; a sequence of
  *                    length 0 gets a zero output.
- *  k_gain, k_shape   key codebook [1][G][256], [1][G][256][8] (shape 16-byte
- *  v_gain, v_shape   aligned) and value codebook.
+ *  k_gain, k_shape   key codebook [1][G][256], [1][G][256][8] and value
+ *  v_gain, v_shape   codebook (shapes 16-byte aligned).
  *  q, q_dtype        [B][Hq][head_dim] queries, 16-byte aligned.
  *  out               [B][Hq][head_dim] float32.
  *  workspace         >= gsrq_attn_workspace_bytes(a), 256-byte aligned.

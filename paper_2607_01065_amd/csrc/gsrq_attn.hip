@@ -55,45 +55,80 @@ template <int GQ> struct AtCfg {
   // LDS layout in bytes
   static constexpr int KTAB = 0;                            // f16 [16][256][8] keys
   static constexpr int VTAB = KTAB + AT_TAB * 2;            // f16 [16][256][8] values
-  static constexpr int VCS = VTAB + AT_TAB * 2;             // u8 [WAVES][16][32] value codes
-  static constexpr int ANG = VCS + AT_WAVES * AT_SUB * AT_BLK;      // float2 [WAVES][64]
-  static constexpr int RED = ANG + AT_WAVES * 64 * 8;               // f32 [WAVES][AT_RED]
-  static constexpr int BYTES = RED + AT_WAVES * AT_RED * 4;
+  static constexpr int QT = VTAB + AT_TAB * 2;              // f32 [32][128] queries
+  // per wave: the value tile of half a head [64 dims][32 tokens] f16; the
+  // group's angle table (float2 [64]) shares it at the start of a group,
+  // and the final merge (f32 [AT_RED]) after the last group
+  static constexpr int TILE = QT + 32 * AT_HD * 4;
+  static constexpr int TILE_BYTES = 64 * AT_BLK * 2;
+  static constexpr int BYTES = TILE + AT_WAVES * TILE_BYTES;
 };
+static_assert(AT_RED * 4 <= 64 * AT_BLK * 2 && 64 * 8 <= 64 * AT_BLK * 2, "tile aliases");
 static_assert(AtCfg<4>::BYTES <= 160 * 1024, "LDS budget");
 
 struct AttnArgs {
   const uint32_t* kc;       // [B][cap][W] key codes
   const uint32_t* vc;       // [B][cap][W] value codes
   const int32_t* seq_len;   // [B]
-  const float* kg;          // [G][256] key gains
-  const float* ks;          // [G][256][8] key shapes
-  const float* vg;
-  const float* vs;
   const void* q;            // [B][Hq][128]
   int q_f16;
   const float2* t1;         // [32][64] cos/sin of t theta_j
   const float2* t2;         // [32][64] cos/sin of 32 u theta_j
   const double* th;         // [64] theta_j / 2 pi
+  const u4* tabk;           // [Hkv][16][256][8] f16 key codewords (16-byte rows)
+  const u4* tabv;           // same for values
   float* part;              // [B][Hkv][nch][GQ][AT_PART]
   int cap, W, Hkv, nch, rpc;
   float qscale;             // softmax scale * log2(e)
 };
 
-// cos/sin tables of the rotations a block needs (float64 arithmetic).
+// Per call: cos/sin tables of the rotations a block needs (float64
+// arithmetic; blocks 0-7), and the float16 decode fp16(fp32(g * s)) of every
+// key and value codeword (the other blocks, one codeword per thread).
 __global__ void __launch_bounds__(256) attn_tables_kernel(double base, float2* __restrict__ t1,
                                                           float2* __restrict__ t2,
-                                                          double* __restrict__ th) {
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= 32 * 64) return;
-  const int t = i >> 6, j = i & 63;
-  const double theta = pow(base, -2.0 * j / AT_HD);
-  double s, c;
-  sincos((double)t * theta, &s, &c);
-  t1[i] = make_float2((float)c, (float)s);
-  sincos(32.0 * t * theta, &s, &c);
-  t2[i] = make_float2((float)c, (float)s);
-  if (t == 0) th[j] = theta / (2.0 * M_PI);
+                                                          double* __restrict__ th,
+                                                          const float* __restrict__ kg,
+                                                          const float* __restrict__ ks,
+                                                          const float* __restrict__ vg,
+                                                          const float* __restrict__ vs, int ncw,
+                                                          u4* __restrict__ tabk,
+                                                          u4* __restrict__ tabv) {
+  if (blockIdx.x < 8) {
+    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int t = i >> 6, j = i & 63;
+    const double theta = pow(base, -2.0 * j / AT_HD);
+    double s, c;
+    sincos((double)t * theta, &s, &c);
+    t1[i] = make_float2((float)c, (float)s);
+    sincos(32.0 * t * theta, &s, &c);
+    t2[i] = make_float2((float)c, (float)s);
+    if (t == 0) th[j] = theta / (2.0 * M_PI);
+    return;
+  }
+  const int cw = (blockIdx.x - 8) * 256 + threadIdx.x;
+  if (cw >= 2 * ncw) return;
+  const bool val = cw >= ncw;
+  const int k = val ? cw - ncw : cw;
+  const float g = (val ? vg : kg)[k];
+  const f4* sp = (const f4*)((val ? vs : ks) + (size_t)k * 8);
+  const f4 a = sp[0], b = sp[1];
+  _Float16 h[8];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    h[e] = (_Float16)(g * a[e]);
+    h[4 + e] = (_Float16)(g * b[e]);
+  }
+  (val ? tabv : tabk)[k] = pack_h8(h);
+}
+
+// Order a wave's own LDS accesses around this point: the tile is read and
+// written through different types, so the compiler must not move accesses
+// across it (the LDS itself serves one wave's accesses in order).
+__device__ __forceinline__ void wave_lds_order() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_wave_barrier();
+  asm volatile("" ::: "memory");
 }
 
 // v = hi + lo with hi = fp16(v), lo = fp16(v - hi): about 22 bits of v.
@@ -109,14 +144,17 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   _Float16* ktab = (_Float16*)(lds + C::KTAB);
   _Float16* vtab = (_Float16*)(lds + C::VTAB);
-  float* red = (float*)(lds + C::RED);
 
   const int chunk = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int tl = lane & 31, hh = lane >> 5;
   const int ul = tl / GQ, hl = tl % GQ;      // B-operand column: block variant, query head
-  unsigned char* vcs = lds + C::VCS + w * AT_SUB * AT_BLK;
-  float2* ang = (float2*)(lds + C::ANG) + w * 64;
+  _Float16* tile = (_Float16*)(lds + C::TILE + w * C::TILE_BYTES);
+  float2* ang = (float2*)tile;
+  // k position of the lane's token row in the value product: token t sits
+  // where the score accumulators hold it, 16 (t / 16) + 8 ((t / 4) % 2) +
+  // 4 ((t / 8) % 2) + t % 4 (bits 2 and 3 of t exchanged)
+  const int kpos = (tl & ~12) | ((tl & 4) << 1) | ((tl & 8) >> 1);
   const int len = min(max(a.seq_len[b], 0), a.cap);
   const int tok0 = chunk * a.rpc * C::ROUND;
   float* outp = a.part + (((size_t)b * a.Hkv + hk) * a.nch + chunk) * GQ * AT_PART;
@@ -132,18 +170,50 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
   const int g0 = hk * AT_SUB;
   const size_t seq_row0 = (size_t)b * a.cap;
 
-  // codeword tables: fp16(fp32(g * s)), the float16 decode of a codeword
-  for (int i = tid; i < AT_SUB * AT_K * 2; i += AT_THREADS) {
-    const int cw = i >> 1, half = i & 1;
-    const size_t src = ((size_t)g0 * AT_K + cw) * 8 + half * 4;
-    const float gk = a.kg[(size_t)g0 * AT_K + cw], gv = a.vg[(size_t)g0 * AT_K + cw];
-    const f4 sk = *(const f4*)(a.ks + src), sv = *(const f4*)(a.vs + src);
-    *(uint2*)(ktab + cw * 8 + half * 4) =
-        make_uint2(pack2((_Float16)(gk * sk[0]), (_Float16)(gk * sk[1])),
-                   pack2((_Float16)(gk * sk[2]), (_Float16)(gk * sk[3])));
-    *(uint2*)(vtab + cw * 8 + half * 4) =
-        make_uint2(pack2((_Float16)(gv * sv[0]), (_Float16)(gv * sv[1])),
-                   pack2((_Float16)(gv * sv[2]), (_Float16)(gv * sv[3])));
+  // this head's float16 codeword tables (16 u4 of keys and 16 of values
+  // per thread, every load issued before the first store)
+  {
+    const u4* sk = a.tabk + (size_t)hk * AT_SUB * AT_K;
+    const u4* sv = a.tabv + (size_t)hk * AT_SUB * AT_K;
+    constexpr int PER = AT_SUB * AT_K / AT_THREADS;
+    u4 rk[PER], rv[PER];
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      rk[m] = sk[m * AT_THREADS + tid];
+      rv[m] = sv[m * AT_THREADS + tid];
+    }
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      ((u4*)ktab)[m * AT_THREADS + tid] = rk[m];
+      ((u4*)vtab)[m * AT_THREADS + tid] = rv[m];
+    }
+  }
+  // query of every B-operand column j = (u, h), turned by R_{-32u}:
+  // qt[j][jd], qt[j][jd + 64] for the pairs jd < 64
+  float* qt = (float*)(lds + C::QT);
+  {
+    constexpr int PER = 32 * 64 / AT_THREADS;
+    float x[PER], y[PER];
+    float2 cs[PER];
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      const int it = m * AT_THREADS + tid, j = it >> 6, jd = it & 63;
+      const size_t qo = ((size_t)b * Hq + hk * GQ + j % GQ) * AT_HD + jd;
+      if (a.q_f16) {
+        x[m] = (float)((const _Float16*)a.q)[qo];
+        y[m] = (float)((const _Float16*)a.q)[qo + 64];
+      } else {
+        x[m] = ((const float*)a.q)[qo];
+        y[m] = ((const float*)a.q)[qo + 64];
+      }
+      cs[m] = a.t2[(j / GQ) * 64 + jd];
+    }
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      const int it = m * AT_THREADS + tid, j = it >> 6, jd = it & 63;
+      qt[j * AT_HD + jd] = x[m] * cs[m].x + y[m] * cs[m].y;        // R_{-32u}
+      qt[j * AT_HD + jd + 64] = y[m] * cs[m].x - x[m] * cs[m].y;
+    }
   }
 
   // lane constant: R_t for the lane's token row; element m < 32 of a lane
@@ -157,7 +227,6 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       ct[2 * m] = v.x; st[2 * m] = v.y; ct[2 * m + 1] = v.z; st[2 * m + 1] = v.w;
     }
   }
-  const size_t qoff = ((size_t)b * Hq + hk * GQ + hl) * AT_HD + 32 * hh;
   const double thl = a.th[lane];
   __syncthreads();
 
@@ -177,85 +246,66 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       sincosf((float)(rev * (2.0 * M_PI)), &s, &c);
       ang[lane] = make_float2(c, s);
     }
-    __builtin_amdgcn_wave_barrier();
+    wave_lds_order();
     // query of the lane's column turned by R_{pq - 32 gb0} R_{-32u} (its
-    // block's relative rotation), split hi + lo into float16 pairs; loaded
-    // again for every group so that no float32 copy stays live
+    // block's relative rotation), split hi + lo into float16 pairs
     u4 bqh[8], bql[8];
     {
-      int zero = 0;
-      asm volatile("" : "+s"(zero));
-      float qx[32], qy[32];
-      if (a.q_f16) {
-        const u4* qp = (const u4*)((const _Float16*)a.q + qoff + zero);
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-          const h8 x = as_h8(qp[m]), y = as_h8(qp[m + 8]);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) { qx[8 * m + e] = (float)x[e]; qy[8 * m + e] = (float)y[e]; }
-        }
-      } else {
-        const f4* qp = (const f4*)((const float*)a.q + qoff + zero);
-#pragma unroll
-        for (int m = 0; m < 8; ++m) {
-          const f4 x = qp[m], y = qp[m + 16];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) { qx[4 * m + e] = x[e]; qy[4 * m + e] = y[e]; }
-        }
-      }
-      const float4* t2 = (const float4*)(a.t2 + ul * 64 + 32 * hh + zero);
+      const float4* qxp = (const float4*)(qt + tl * AT_HD + 32 * hh);
+      const float4* qyp = (const float4*)(qt + tl * AT_HD + 64 + 32 * hh);
       const float4* ap = (const float4*)(ang + 32 * hh);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         _Float16 xh[8], xl[8], yh[8], yl[8];
 #pragma unroll
-        for (int m2 = 0; m2 < 4; ++m2) {
-          const float4 v2 = t2[4 * i + m2];
-          const float4 v = ap[4 * i + m2];
+        for (int m2 = 0; m2 < 2; ++m2) {
+          const float4 qx4 = qxp[2 * i + m2], qy4 = qyp[2 * i + m2];
+          const float4 va = ap[4 * i + 2 * m2], vb = ap[4 * i + 2 * m2 + 1];
+          const float qxv[4] = {qx4.x, qx4.y, qx4.z, qx4.w};
+          const float qyv[4] = {qy4.x, qy4.y, qy4.z, qy4.w};
+          const float cv[4] = {va.x, va.z, vb.x, vb.z};
+          const float sv[4] = {va.y, va.w, vb.y, vb.w};
 #pragma unroll
-          for (int r2 = 0; r2 < 2; ++r2) {
-            const int e = 2 * m2 + r2, m = 8 * i + e;
-            const float c2 = r2 ? v2.z : v2.x, s2 = r2 ? v2.w : v2.y;
-            const float x1 = qx[m] * c2 + qy[m] * s2;     // R_{-32u}
-            const float y1 = qy[m] * c2 - qx[m] * s2;
-            const float c = r2 ? v.z : v.x, s = r2 ? v.w : v.y;
-            split16(x1 * c - y1 * s, xh[e], xl[e]);       // R_{pq - 32 gb0}
-            split16(x1 * s + y1 * c, yh[e], yl[e]);
+          for (int r = 0; r < 4; ++r) {
+            const int e = 4 * m2 + r;
+            split16(qxv[r] * cv[r] - qyv[r] * sv[r], xh[e], xl[e]);
+            split16(qxv[r] * sv[r] + qyv[r] * cv[r], yh[e], yl[e]);
           }
         }
         bqh[i] = pack_h8(xh); bql[i] = pack_h8(xl);
         bqh[i + 4] = pack_h8(yh); bql[i + 4] = pack_h8(yl);
       }
     }
+    wave_lds_order();                               // angle table reads before tile writes
     const int nblk = min(U, (len - 32 * gb0 + 31) >> 5);
-    u4 kcn = u4{0, 0, 0, 0}, vcn = u4{0, 0, 0, 0};
+    // codes of the next block are loaded while this one is scored; rows
+    // past the sequence end read the last row instead (their weights are
+    // zero), so that every load is unconditional and the wait for the
+    // current block's codes leaves the next block's loads in flight
+    const u4* kcp = (const u4*)(a.kc + seq_row0 * a.W + 4 * hk);
+    const u4* vcp = (const u4*)(a.vc + seq_row0 * a.W + 4 * hk);
+    const int wq = a.W / 4;                          // u4 per row
+    u4 kcn, vcn;
     {
-      const int row = 32 * gb0 + tl;
-      if (row < len) {
-        kcn = *(const u4*)(a.kc + (seq_row0 + row) * a.W + 4 * hk);
-        vcn = *(const u4*)(a.vc + (seq_row0 + row) * a.W + 4 * hk);
-      }
+      const int row = min(32 * gb0 + tl, len - 1);
+      kcn = kcp[(size_t)row * wq];
+      vcn = vcp[(size_t)row * wq];
     }
     for (int u = 0; u < nblk; ++u) {
       const u4 kcw = kcn, vcw = vcn;
       {
-        const int row = 32 * (gb0 + u + 1) + tl;
-        const bool nx = u + 1 < nblk && row < len;
-        kcn = nx ? *(const u4*)(a.kc + (seq_row0 + row) * a.W + 4 * hk) : u4{0, 0, 0, 0};
-        vcn = nx ? *(const u4*)(a.vc + (seq_row0 + row) * a.W + 4 * hk) : u4{0, 0, 0, 0};
+        const int row = min(32 * (gb0 + min(u + 1, nblk - 1)) + tl, len - 1);
+        kcn = kcp[(size_t)row * wq];
+        vcn = vcp[(size_t)row * wq];
       }
-      // value codes of the block, by subspace: vcs[g][t]; lane half hh
-      // writes subspaces 8 hh .. 8 hh + 7 of its token
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        vcs[(8 * hh + e) * AT_BLK + tl] = (unsigned char)(vcw[2 * hh + (e >> 2)] >> (8 * (e & 3)));
+      const uint32_t kw0 = hh ? kcw[1] : kcw[0], kw1 = hh ? kcw[3] : kcw[2];
 
       // ---- scores: pair (i, i + 4) of k-steps holds elements jd and jd + 64;
       // R_t, then hi + lo float16 pairs; scores = khi.qhi + khi.qlo + klo.qhi
-      f16v acc = {};
+      f16v acc = {}, acc2 = {};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int cx = (kcw[hh] >> (8 * i)) & 255, cy = (kcw[2 + hh] >> (8 * i)) & 255;
+        const int cx = (kw0 >> (8 * i)) & 255, cy = (kw1 >> (8 * i)) & 255;
         const h8 x = as_h8(*(const u4*)(ktab + ((4 * hh + i) * AT_K + cx) * 8));
         const h8 y = as_h8(*(const u4*)(ktab + ((8 + 4 * hh + i) * AT_K + cy) * 8));
         _Float16 xh[8], xl[8], yh[8], yl[8];
@@ -271,10 +321,11 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
         acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxl, as_h8(bqh[i]), acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxh, as_h8(bql[i]), acc, 0, 0, 0);
         acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxh, as_h8(bqh[i]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyl, as_h8(bqh[i + 4]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bql[i + 4]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bqh[i + 4]), acc, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyl, as_h8(bqh[i + 4]), acc2, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bql[i + 4]), acc2, 0, 0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bqh[i + 4]), acc2, 0, 0, 0);
       }
+      acc += acc2;
 
       // ---- softmax weights of this block (only the columns of variant u)
       // register v holds token row t = 8 (v / 4) + 4 hh + v % 4
@@ -288,22 +339,31 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
         ml = fmaxf(ml, sc[v]);
       }
       ml = fmaxf(ml, __shfl_xor(ml, 32));
+      // raise the references of the heads whose block maximum exceeds
+      // them, rescaling this wave's sums once for all heads (rare)
+      float mbh[GQ];
+      bool raise = false;
 #pragma unroll
       for (int h = 0; h < GQ; ++h) {
-        const float mb = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ml), u * GQ + h));
-        if (mb > mw[h]) {                            // uniform
-          const float nref = mb + AT_HEADROOM;
-          if (mw[h] > -INFINITY) {
-            const float fac = exp2f(mw[h] - nref);
-            if (hl == h) lsum *= fac;
+        mbh[h] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ml), u * GQ + h));
+        raise |= mbh[h] > mw[h];
+      }
+      if (raise) {                                   // uniform
+        float fac[GQ];
 #pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-              for (int v = 0; v < 16; ++v)
-                if ((v & 3) % GQ == h) o[c][v] *= fac;
-          }
+        for (int h = 0; h < GQ; ++h) {
+          const float nref = mbh[h] > mw[h] ? mbh[h] + AT_HEADROOM : mw[h];
+          fac[h] = exp2f(mw[h] - nref);              // 1 if kept, 0 from -inf
           mw[h] = nref;
         }
+        float fl = fac[0];
+#pragma unroll
+        for (int h = 1; h < GQ; ++h) fl = hl == h ? fac[h] : fl;
+        lsum *= fl;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) o[c][v] *= fac[(v & 3) % GQ];
       }
       float mine = mw[0];
 #pragma unroll
@@ -323,34 +383,42 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
         pl[s2] = pack_h8(xl);
       }
 
-      // ---- value sums: o[c] += P . V, V gathered in the k order of P
-      __builtin_amdgcn_wave_barrier();
+      // ---- value sums o[c] += P . V, in two halves of the head (tiles
+      // c = 2 hp, 2 hp + 1): every lane writes the elements of its token's
+      // four value codewords of that half into the wave's tile at
+      // [dim][kpos], then reads its B operands (8 tokens of one dim) back
+      const uint32_t vw0 = hh ? vcw[1] : vcw[0], vw1 = hh ? vcw[3] : vcw[2];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const int g = 4 * c + (tl >> 3), e = tl & 7;
-        const unsigned char* cp = vcs + g * AT_BLK + 4 * hh;
-        const _Float16* vt = vtab + g * AT_K * 8 + e;
+      for (int hp = 0; hp < 2; ++hp) {
+        const uint32_t vw = hp ? vw1 : vw0;
 #pragma unroll
-        for (int s2 = 0; s2 < 2; ++s2) {
-          const uint32_t c0 = *(const uint32_t*)(cp + 16 * s2);
-          const uint32_t c1 = *(const uint32_t*)(cp + 16 * s2 + 8);
-          _Float16 vv[8];
+        for (int i = 0; i < 4; ++i) {
+          const int code = (vw >> (8 * i)) & 255;
+          const int sub = 8 * hp + 4 * hh + i;
+          const h8 v8 = as_h8(*(const u4*)(vtab + (sub * AT_K + code) * 8));
+          // dims of this codeword within the half: 32 hh + 8 i + e
 #pragma unroll
-          for (int e2 = 0; e2 < 4; ++e2) {
-            vv[e2] = vt[((c0 >> (8 * e2)) & 255) * 8];
-            vv[4 + e2] = vt[((c1 >> (8 * e2)) & 255) * 8];
-          }
-          const h8 vb = as_h8(pack_h8(vv));
-          o[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pl[s2]), vb, o[c], 0, 0, 0);
-          o[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), vb, o[c], 0, 0, 0);
+          for (int e = 0; e < 8; ++e) tile[(32 * hh + 8 * i + e) * AT_BLK + kpos] = v8[e];
         }
+        wave_lds_order();
+#pragma unroll
+        for (int cc = 0; cc < 2; ++cc) {
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const h8 vb = as_h8(*(const u4*)(tile + (32 * cc + tl) * AT_BLK + 16 * s2 + 8 * hh));
+            o[2 * hp + cc] =
+                __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pl[s2]), vb, o[2 * hp + cc], 0, 0, 0);
+            o[2 * hp + cc] =
+                __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), vb, o[2 * hp + cc], 0, 0, 0);
+          }
+        }
+        wave_lds_order();
       }
-      __builtin_amdgcn_wave_barrier();
     }
   }
 
   // ---- merge the four waves: per head the reference, the sum and o
-  float* rw = red + w * AT_RED;
+  float* rw = (float*)tile;
   {
     float l = lsum;
 #pragma unroll
@@ -375,16 +443,18 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       }
   }
   __syncthreads();
+  const float* red = (const float*)(lds + C::TILE);
+  constexpr int RS = C::TILE_BYTES / 4;              // floats between waves' records
   for (int i = tid; i < GQ * AT_HD; i += AT_THREADS) {
     const int h = i / AT_HD, n = i % AT_HD;
     float M = -INFINITY;
 #pragma unroll
     for (int v = 0; v < AT_WAVES; ++v)
-      if (red[v * AT_RED + 4 + h] > 0.f) M = fmaxf(M, red[v * AT_RED + h]);
+      if (red[v * RS + 4 + h] > 0.f) M = fmaxf(M, red[v * RS + h]);
     double num = 0.0, den = 0.0;
 #pragma unroll
     for (int v = 0; v < AT_WAVES; ++v) {
-      const float* r = red + v * AT_RED;
+      const float* r = red + v * RS;
       if (!(r[4 + h] > 0.f)) continue;
       const double f = exp2((double)r[h] - (double)M);
       num += f * (double)r[8 + h * AT_HD + n];
@@ -423,7 +493,7 @@ __global__ void __launch_bounds__(AT_HD) attn_merge_kernel(const float* __restri
 
 struct AttnPlan {
   int GQ, rpc, nch;
-  size_t off_t1, off_t2, off_th, off_part, bytes;
+  size_t off_t1, off_t2, off_th, off_tk, off_tv, off_part, bytes;
 };
 
 int at_round(int GQ) { return AT_WAVES * (32 / GQ) * AT_BLK; }
@@ -448,7 +518,9 @@ gsrq_status attn_plan(const gsrq_attn_shape* a, AttnPlan& p) {
   p.off_t1 = 0;
   p.off_t2 = align256(32 * 64 * sizeof(float2));
   p.off_th = p.off_t2 + align256(32 * 64 * sizeof(float2));
-  p.off_part = p.off_th + align256(64 * sizeof(double));
+  p.off_tk = p.off_th + align256(64 * sizeof(double));
+  p.off_tv = p.off_tk + align256((size_t)a->Hkv * AT_SUB * AT_K * 16);
+  p.off_part = p.off_tv + align256((size_t)a->Hkv * AT_SUB * AT_K * 16);
   p.bytes = p.off_part + align256((size_t)pairs * p.nch * p.GQ * AT_PART * sizeof(float));
   return GSRQ_OK;
 }
@@ -498,7 +570,7 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
       !out)
     return GSRQ_E_ARG;
   if ((uintptr_t)k_codes % 16 || (uintptr_t)v_codes % 16 || (uintptr_t)k_shape % 16 ||
-      (uintptr_t)q % 16)
+      (uintptr_t)v_shape % 16 || (uintptr_t)q % 16)
     return GSRQ_E_ARG;
   if (q_dtype != GSRQ_F32 && q_dtype != GSRQ_F16) return GSRQ_E_ARG;
   if (!workspace || (uintptr_t)workspace % 256) return GSRQ_E_ARG;
@@ -509,15 +581,13 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   args.kc = k_codes;
   args.vc = v_codes;
   args.seq_len = seq_len;
-  args.kg = k_gain;
-  args.ks = k_shape;
-  args.vg = v_gain;
-  args.vs = v_shape;
   args.q = q;
   args.q_f16 = q_dtype == GSRQ_F16;
   args.t1 = (const float2*)(ws + p.off_t1);
   args.t2 = (const float2*)(ws + p.off_t2);
   args.th = (const double*)(ws + p.off_th);
+  args.tabk = (const u4*)(ws + p.off_tk);
+  args.tabv = (const u4*)(ws + p.off_tv);
   args.part = (float*)(ws + p.off_part);
   args.cap = a->cap;
   args.W = a->Hkv * 4;
@@ -525,8 +595,11 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   args.nch = p.nch;
   args.rpc = p.rpc;
   args.qscale = (float)((double)a->scale * 1.4426950408889634);
-  attn_tables_kernel<<<8, 256, 0, st>>>((double)a->rope_base, (float2*)(ws + p.off_t1),
-                                        (float2*)(ws + p.off_t2), (double*)(ws + p.off_th));
+  const int ncw = a->Hkv * AT_SUB * AT_K;
+  attn_tables_kernel<<<8 + (2 * ncw + 255) / 256, 256, 0, st>>>(
+      (double)a->rope_base, (float2*)(ws + p.off_t1), (float2*)(ws + p.off_t2),
+      (double*)(ws + p.off_th), k_gain, k_shape, v_gain, v_shape, ncw, (u4*)(ws + p.off_tk),
+      (u4*)(ws + p.off_tv));
   e = launch_ok();
   if (e) return e;
   if (p.GQ == 1) e = attn_launch<1>(args, a->B, a->Hkv, st);
