@@ -257,8 +257,9 @@ gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes);
  *  workspace         >= gsrq_attn_workspace_bytes(a), 256-byte aligned.
  * Precision: keys and values enter as their float16 decode (g * s rounded
  * to float32, then to float16, as gsrq_decode's float16 output); the
- * rotated query and keys, and the softmax weights, enter the matrix
- * products as hi + lo float16 pairs (about 22 bits), with float32 sums;
+ * query and keys are rotated in float32 and, like the softmax weights,
+ * rounded to float16 for the matrix products, with float32 sums (the
+ * operand precision of float16 attention over a rotated float16 cache);
  * chunks are merged in float64.  This build: head_dim = 128 and
  * Hq / Hkv in {1, 2, 4}.
  */

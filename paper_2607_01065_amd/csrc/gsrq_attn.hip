@@ -13,8 +13,9 @@
 //    holds 32 tokens' keys (each lane one 8-element codeword gathered from a
 //    float16 table of the head's 16 codebooks in LDS, rotated in float32);
 //    the B operand's 32 columns are the GQ query heads of the U blocks of a
-//    group.  Both sides enter as hi + lo float16 pairs (three products per
-//    k-step), so scores carry about 22 bits, as a float32 dot product would.
+//    group.  Both sides enter as float16 (rounded after their rotation in
+//    float32), with float32 sums: the operand precision of float16
+//    attention over a rotated float16 cache.
 //    RoPE enters as a relative rotation: score(i) = (R_{pq - 32b} q) .
 //    (R_t k_i) for token i = 32 b + t, so the rotation of a key depends only
 //    on its row t in the block (fixed per lane) and that of the query on the
@@ -23,7 +24,7 @@
 //    (raised by a margin, with the wave's sums rescaled, when a block's
 //    scores exceed it).
 //  * Values on the matrix cores: the weights leave the score accumulators
-//    already in the A-operand layout of the value product (hi + lo float16),
+//    already in the A-operand layout of the value product (float16),
 //    and the B operand gathers each token's float16 value codeword element
 //    from a second LDS table, in the transposed layout the product needs,
 //    through the block's value codes staged in LDS by subspace.
@@ -129,12 +130,6 @@ __device__ __forceinline__ void wave_lds_order() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_wave_barrier();
   asm volatile("" ::: "memory");
-}
-
-// v = hi + lo with hi = fp16(v), lo = fp16(v - hi): about 22 bits of v.
-__device__ __forceinline__ void split16(float v, _Float16& hi, _Float16& lo) {
-  hi = (_Float16)v;
-  lo = (_Float16)(v - (float)hi);
 }
 
 template <int GQ>
@@ -248,15 +243,15 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
     }
     wave_lds_order();
     // query of the lane's column turned by R_{pq - 32 gb0} R_{-32u} (its
-    // block's relative rotation), split hi + lo into float16 pairs
-    u4 bqh[8], bql[8];
+    // block's relative rotation), rounded to float16
+    u4 bq[8];
     {
       const float4* qxp = (const float4*)(qt + tl * AT_HD + 32 * hh);
       const float4* qyp = (const float4*)(qt + tl * AT_HD + 64 + 32 * hh);
       const float4* ap = (const float4*)(ang + 32 * hh);
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        _Float16 xh[8], xl[8], yh[8], yl[8];
+        _Float16 xh[8], yh[8];
 #pragma unroll
         for (int m2 = 0; m2 < 2; ++m2) {
           const float4 qx4 = qxp[2 * i + m2], qy4 = qyp[2 * i + m2];
@@ -268,12 +263,12 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int e = 4 * m2 + r;
-            split16(qxv[r] * cv[r] - qyv[r] * sv[r], xh[e], xl[e]);
-            split16(qxv[r] * sv[r] + qyv[r] * cv[r], yh[e], yl[e]);
+            xh[e] = (_Float16)(qxv[r] * cv[r] - qyv[r] * sv[r]);
+            yh[e] = (_Float16)(qxv[r] * sv[r] + qyv[r] * cv[r]);
           }
         }
-        bqh[i] = pack_h8(xh); bql[i] = pack_h8(xl);
-        bqh[i + 4] = pack_h8(yh); bql[i + 4] = pack_h8(yl);
+        bq[i] = pack_h8(xh);
+        bq[i + 4] = pack_h8(yh);
       }
     }
     wave_lds_order();                               // angle table reads before tile writes
@@ -301,29 +296,25 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       const uint32_t kw0 = hh ? kcw[1] : kcw[0], kw1 = hh ? kcw[3] : kcw[2];
 
       // ---- scores: pair (i, i + 4) of k-steps holds elements jd and jd + 64;
-      // R_t, then hi + lo float16 pairs; scores = khi.qhi + khi.qlo + klo.qhi
+      // R_t in float32, then rounded to float16
       f16v acc = {}, acc2 = {};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int cx = (kw0 >> (8 * i)) & 255, cy = (kw1 >> (8 * i)) & 255;
         const h8 x = as_h8(*(const u4*)(ktab + ((4 * hh + i) * AT_K + cx) * 8));
         const h8 y = as_h8(*(const u4*)(ktab + ((8 + 4 * hh + i) * AT_K + cy) * 8));
-        _Float16 xh[8], xl[8], yh[8], yl[8];
+        _Float16 xh[8], yh[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float xf = (float)x[e], yf = (float)y[e];
           const float c = ct[8 * i + e], s = st[8 * i + e];
-          split16(xf * c - yf * s, xh[e], xl[e]);
-          split16(xf * s + yf * c, yh[e], yl[e]);
+          xh[e] = (_Float16)(xf * c - yf * s);
+          yh[e] = (_Float16)(xf * s + yf * c);
         }
-        const h8 kxh = as_h8(pack_h8(xh)), kxl = as_h8(pack_h8(xl));
-        const h8 kyh = as_h8(pack_h8(yh)), kyl = as_h8(pack_h8(yl));
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxl, as_h8(bqh[i]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxh, as_h8(bql[i]), acc, 0, 0, 0);
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kxh, as_h8(bqh[i]), acc, 0, 0, 0);
-        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyl, as_h8(bqh[i + 4]), acc2, 0, 0, 0);
-        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bql[i + 4]), acc2, 0, 0, 0);
-        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(kyh, as_h8(bqh[i + 4]), acc2, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pack_h8(xh)), as_h8(bq[i]), acc, 0,
+                                                     0, 0);
+        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pack_h8(yh)), as_h8(bq[i + 4]), acc2,
+                                                      0, 0, 0);
       }
       acc += acc2;
 
@@ -368,19 +359,18 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       float mine = mw[0];
 #pragma unroll
       for (int h = 1; h < GQ; ++h) mine = hl == h ? mw[h] : mine;
-      u4 ph[2], pl[2];
+      u4 ph[2];
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
-        _Float16 xh[8], xl[8];
+        _Float16 xh[8];
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float sv = sc[8 * s2 + e];
           const float pv = sv == -INFINITY ? 0.f : exp2f(sv - mine + AT_PSHIFT);
           lsum += pv;
-          split16(pv, xh[e], xl[e]);
+          xh[e] = (_Float16)pv;
         }
         ph[s2] = pack_h8(xh);
-        pl[s2] = pack_h8(xl);
       }
 
       // ---- value sums o[c] += P . V, in two halves of the head (tiles
@@ -406,8 +396,6 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
 #pragma unroll
           for (int s2 = 0; s2 < 2; ++s2) {
             const h8 vb = as_h8(*(const u4*)(tile + (32 * cc + tl) * AT_BLK + 16 * s2 + 8 * hh));
-            o[2 * hp + cc] =
-                __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pl[s2]), vb, o[2 * hp + cc], 0, 0, 0);
             o[2 * hp + cc] =
                 __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), vb, o[2 * hp + cc], 0, 0, 0);
           }

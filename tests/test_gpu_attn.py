@@ -10,23 +10,27 @@ the library declares it reads) and computes the attention in float64
 
 Tolerance, derived from the kernel's arithmetic (every term is a bound on
 one rounding step; u = 2^-24):
-  * scores: query and rotated keys enter the matrix cores as hi + lo float16
-    pairs (three products per element, the lo.lo product dropped, |lo| <=
-    2^-11 |hi|), after float32 rotations whose error is a few u per element:
-    together <= 16 u |q| |k|; the float32 sums of the 3 x 128 exact products
-    add at most 8 sqrt(385) u sum|q'_j k'_j| under the probabilistic rounding
-    model (independent roundings, 8 standard deviations), <= that times
-    |q| |k| by Cauchy-Schwarz.  So |ds| <= eps_s = scale (16 + 8 sqrt(385)) u
-    |q| max_t |k_t|.
+  * scores: the query and the keys are rotated in float32 (a few u per
+    element) and rounded to float16 for the matrix cores (2^-11 relative
+    each, as float16 attention over a rotated float16 cache rounds them):
+    together <= (2^-10 + 20 u) |q| |k|; the float32 sums of the 128 exact
+    products add at most 8 sqrt(129) u sum|q'_j k'_j| under the
+    probabilistic rounding model (independent roundings, 8 standard
+    deviations), <= that times |q| |k| by Cauchy-Schwarz.  So |ds| <= eps_s
+    = scale (2^-10 + 20 u + 8 sqrt(129) u) |q| max_t |k_t|.
   * weights: a score error eps_s moves every weight by a factor within
     e^(+-2 eps_s); the float32 scaling, reference subtraction and exp2 add
     8 u (|s| log2 e + 8) to the exponent; the weights enter the value
-    product as hi + lo float16 pairs (2^-21 relative, and an absolute error
-    below 2^-32 of the largest weight where the lo part is subnormal).
+    product rounded to float16: 2^-11 relative, and below the float16
+    normal range (2^-14) an absolute error of at most 2^-25 against a
+    largest weight of at least 2^7 (a raised reference sits 8 above the
+    block maximum, weights are 2^(s - m + 15)), so at most L 2^-32 max|v|
+    over L tokens once divided by the softmax sum.
   * sums: the value products and the softmax denominator sum <= L float32
     terms: 16 sqrt(L) u relative under the same probabilistic model.
-  * so |o_n - o_ref_n| <= C sum_t p_t |v_tn| (+ 1e-7 max|v| for the float64
-    merges), C = expm1(2 eps_s + 8u (smax + 8)) + 2^-21 + 16 sqrt(L) u + 4u.
+  * so |o_n - o_ref_n| <= C sum_t p_t |v_tn| + (L 2^-32 + 1e-7) max|v| (the
+    1e-7 for the float64 merges), C = expm1(2 eps_s + 8u (smax + 8)) + 2^-11
+    + 16 sqrt(L) u + 4u.
 The test also reports the worst observed error relative to that bound.
 """
 import math
@@ -98,11 +102,12 @@ def _reference(case, b, heads=None, base=BASE):
         kv = h // GQ
         ref[h] = p[h] @ v16[:, kv]
         kmax = float(np.max(np.linalg.norm(k16[:, kv], axis=1)))
-        eps_s = scale * (16 + 8 * math.sqrt(385)) * U * np.linalg.norm(q[h]) * kmax
+        eps_s = scale * (2.0 ** -10 + (20 + 8 * math.sqrt(129)) * U) * np.linalg.norm(q[h]) * kmax
         smax = float(np.max(np.abs(s[h]))) * math.log2(math.e)
-        C = (math.expm1(2 * eps_s + 8 * U * (smax + 8)) + 2.0 ** -21 + 16 * math.sqrt(L) * U
+        C = (math.expm1(2 * eps_s + 8 * U * (smax + 8)) + 2.0 ** -11 + 16 * math.sqrt(L) * U
              + 4 * U)
-        tol[h] = C * (p[h] @ np.abs(v16[:, kv])) + 1e-7 * float(np.max(np.abs(v16[:, kv])))
+        tol[h] = (C * (p[h] @ np.abs(v16[:, kv]))
+                  + (L * 2.0 ** -32 + 1e-7) * float(np.max(np.abs(v16[:, kv]))))
     return ref, tol
 
 
