@@ -25,14 +25,50 @@ def hipcc():
     raise RuntimeError("hipcc not found")
 
 
+# Flags of single translation units.  The attention kernel keeps its MFMA
+# accumulators in ordinary VGPRs: with them in AGPRs, the rare rescaling of
+# the output sums (VALU work) made the compiler copy all 64 accumulators to
+# VGPRs on every token block.
+SRC_FLAGS = {
+    "gsrq_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
+def flags_for(src):
+    """hipcc flags of one source (without -shared)."""
+    return [f for f in HIPCC_FLAGS if f != "-shared"] + SRC_FLAGS.get(os.path.basename(src), [])
+
+
 def build(verbose=False, extra=()):
+    """Compile every source to an object (in parallel), then link
+    libgsrq.so; always recompiles."""
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-I", INCLUDE, "-o", tmp, *SRCS]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
+    objs = [LIB + "." + os.path.basename(src) + ".o" for src in SRCS]
+    procs = []
+    for src, obj in zip(SRCS, objs):
+        cmd = [hipcc(), *flags_for(src), *extra, "-c", "-I", INCLUDE, "-o", obj, src]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append(subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE,
+                                      text=True))
+    failed = False
+    for p in procs:
+        out, err = p.communicate()
+        if p.returncode != 0:
+            sys.stderr.write(out + err)
+            failed = True
+    if not failed:
+        cmd = [hipcc(), "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            failed = True
+    for obj in objs:
+        if os.path.exists(obj):
+            os.remove(obj)
+    if failed:
         raise RuntimeError("hipcc failed building libgsrq.so")
     os.replace(tmp, LIB)
     return LIB

@@ -37,6 +37,8 @@
 
 namespace {
 
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
 constexpr int AT_HD = 128;            // head dimension
 constexpr int AT_SUB = 16;            // d = 8 subspaces per head
 constexpr int AT_K = 256;             // codewords per codebook
@@ -183,8 +185,9 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       ((u4*)vtab)[m * AT_THREADS + tid] = rv[m];
     }
   }
-  // query of every B-operand column j = (u, h), turned by R_{-32u}:
-  // qt[j][jd], qt[j][jd + 64] for the pairs jd < 64
+  // query of every B-operand column j = (u, h), turned by R_{-32u} and
+  // scaled by the softmax scale times log2(e) (scores come out in log2
+  // units): qt[j][jd], qt[j][jd + 64] for the pairs jd < 64
   float* qt = (float*)(lds + C::QT);
   {
     constexpr int PER = 32 * 64 / AT_THREADS;
@@ -206,20 +209,22 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
 #pragma unroll
     for (int m = 0; m < PER; ++m) {
       const int it = m * AT_THREADS + tid, j = it >> 6, jd = it & 63;
-      qt[j * AT_HD + jd] = x[m] * cs[m].x + y[m] * cs[m].y;        // R_{-32u}
-      qt[j * AT_HD + jd + 64] = y[m] * cs[m].x - x[m] * cs[m].y;
+      qt[j * AT_HD + jd] = (x[m] * cs[m].x + y[m] * cs[m].y) * a.qscale;   // R_{-32u}
+      qt[j * AT_HD + jd + 64] = (y[m] * cs[m].x - x[m] * cs[m].y) * a.qscale;
     }
   }
 
-  // lane constant: R_t for the lane's token row; element m < 32 of a lane
-  // is head element jd = 32 hh + m, paired with jd + 64
-  float ct[32], st[32];
+  // lane constant: R_t for the lane's token row as float16 pairs; element
+  // m < 32 of a lane is head element jd = 32 hh + m, paired with jd + 64;
+  // cp[m / 2] holds the cosines of elements m, m + 1 (m even), sp the sines
+  h2 cp[16], sp[16];
   {
     const float4* t1 = (const float4*)(a.t1 + tl * 64 + 32 * hh);
 #pragma unroll
     for (int m = 0; m < 16; ++m) {
       const float4 v = t1[m];
-      ct[2 * m] = v.x; st[2 * m] = v.y; ct[2 * m + 1] = v.z; st[2 * m + 1] = v.w;
+      cp[m] = (h2){(_Float16)v.x, (_Float16)v.z};
+      sp[m] = (h2){(_Float16)v.y, (_Float16)v.w};
     }
   }
   const double thl = a.th[lane];
@@ -296,39 +301,50 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       const uint32_t kw0 = hh ? kcw[1] : kcw[0], kw1 = hh ? kcw[3] : kcw[2];
 
       // ---- scores: pair (i, i + 4) of k-steps holds elements jd and jd + 64;
-      // R_t in float32, then rounded to float16
-      f16v acc = {}, acc2 = {};
+      // R_t in packed float16 arithmetic (x' = x c - y s, y' = x s + y c)
+      f16v acc = {};
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int cx = (kw0 >> (8 * i)) & 255, cy = (kw1 >> (8 * i)) & 255;
-        const h8 x = as_h8(*(const u4*)(ktab + ((4 * hh + i) * AT_K + cx) * 8));
-        const h8 y = as_h8(*(const u4*)(ktab + ((8 + 4 * hh + i) * AT_K + cy) * 8));
-        _Float16 xh[8], yh[8];
+        const u4 x = *(const u4*)(ktab + ((4 * hh + i) * AT_K + cx) * 8);
+        const u4 y = *(const u4*)(ktab + ((8 + 4 * hh + i) * AT_K + cy) * 8);
+        h2 xr[4], yr[4];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const float xf = (float)x[e], yf = (float)y[e];
-          const float c = ct[8 * i + e], s = st[8 * i + e];
-          xh[e] = (_Float16)(xf * c - yf * s);
-          yh[e] = (_Float16)(xf * s + yf * c);
+        for (int p = 0; p < 4; ++p) {
+          const uint32_t xw = x[p], yw = y[p];    // scalar copies before the bit casts
+          const h2 xp = __builtin_bit_cast(h2, xw), yp = __builtin_bit_cast(h2, yw);
+          const h2 c = cp[4 * i + p], sn = sp[4 * i + p];
+          xr[p] = __builtin_elementwise_fma(xp, c, -(yp * sn));
+          yr[p] = __builtin_elementwise_fma(xp, sn, yp * c);
         }
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pack_h8(xh)), as_h8(bq[i]), acc, 0,
-                                                     0, 0);
-        acc2 = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(pack_h8(yh)), as_h8(bq[i + 4]), acc2,
-                                                      0, 0, 0);
+        const h8 kx = __builtin_shufflevector(__builtin_shufflevector(xr[0], xr[1], 0, 1, 2, 3),
+                                              __builtin_shufflevector(xr[2], xr[3], 0, 1, 2, 3),
+                                              0, 1, 2, 3, 4, 5, 6, 7);
+        const h8 ky = __builtin_shufflevector(__builtin_shufflevector(yr[0], yr[1], 0, 1, 2, 3),
+                                              __builtin_shufflevector(yr[2], yr[3], 0, 1, 2, 3),
+                                              0, 1, 2, 3, 4, 5, 6, 7);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(kx, as_h8(bq[i]), acc, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ky, as_h8(bq[i + 4]), acc, 0, 0, 0);
       }
-      acc += acc2;
 
       // ---- softmax weights of this block (only the columns of variant u)
       // register v holds token row t = 8 (v / 4) + 4 hh + v % 4
       const int rowb = 32 * (gb0 + u);
+      // (a lane's maximum is read only for columns of variant u; rows past
+      // the sequence end, only in its last block, are masked out)
       float sc[16];
-      float ml = -INFINITY;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int t = 8 * (v >> 2) + 4 * hh + (v & 3);
-        sc[v] = (ul == u && rowb + t < len) ? acc[v] * a.qscale : -INFINITY;
-        ml = fmaxf(ml, sc[v]);
+      for (int v = 0; v < 16; ++v) sc[v] = acc[v];
+      if (rowb + 32 > len) {                         // uniform
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int t = 8 * (v >> 2) + 4 * hh + (v & 3);
+          if (rowb + t >= len) sc[v] = -INFINITY;
+        }
       }
+      float ml = sc[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) ml = fmaxf(ml, sc[v]);
       ml = fmaxf(ml, __shfl_xor(ml, 32));
       // raise the references of the heads whose block maximum exceeds
       // them, rescaling this wave's sums once for all heads (rare)
@@ -356,9 +372,12 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
 #pragma unroll
           for (int v = 0; v < 16; ++v) o[c][v] *= fac[(v & 3) % GQ];
       }
+      // weights 2^(s - m + PSHIFT) of the lane's column; columns of other
+      // variants get 2^-inf = 0
       float mine = mw[0];
 #pragma unroll
       for (int h = 1; h < GQ; ++h) mine = hl == h ? mw[h] : mine;
+      mine = ul == u ? mine - AT_PSHIFT : INFINITY;
       u4 ph[2];
 #pragma unroll
       for (int s2 = 0; s2 < 2; ++s2) {
@@ -366,7 +385,7 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float sv = sc[8 * s2 + e];
-          const float pv = sv == -INFINITY ? 0.f : exp2f(sv - mine + AT_PSHIFT);
+          const float pv = __builtin_amdgcn_exp2f(sv - mine);
           lsum += pv;
           xh[e] = (_Float16)pv;
         }

@@ -25,7 +25,7 @@ MAX_SCRATCH = 16   # bytes per lane
 def _remarks(src):
     hipcc = BUILD.hipcc()
     with tempfile.TemporaryDirectory() as tmp:
-        cmd = [hipcc, *[f for f in BUILD.HIPCC_FLAGS if f != "-shared"], "-c",
+        cmd = [hipcc, *BUILD.flags_for(src), "-c",
                "-I", BUILD.INCLUDE, "-o", os.path.join(tmp, "x.o"), src,
                "-Rpass-analysis=kernel-resource-usage"]
         res = subprocess.run(cmd, capture_output=True, text=True)

@@ -10,14 +10,20 @@ the library declares it reads) and computes the attention in float64
 
 Tolerance, derived from the kernel's arithmetic (every term is a bound on
 one rounding step; u = 2^-24):
-  * scores: the query and the keys are rotated in float32 (a few u per
-    element) and rounded to float16 for the matrix cores (2^-11 relative
-    each, as float16 attention over a rotated float16 cache rounds them):
-    together <= (2^-10 + 20 u) |q| |k|; the float32 sums of the 128 exact
-    products add at most 8 sqrt(129) u sum|q'_j k'_j| under the
+  * scores: the query, turned in float32 and scaled by scale log2(e) (a few
+    u per element), is rounded to float16 (2^-11 relative); each key pair
+    (x, y), already float16, is turned in packed float16 arithmetic with
+    float16 cosines and sines c, s: x' = fl(x c - fl(y s)), y' = fl(x s +
+    fl(y c)), each within 3 2^-11 |(x, y)| of the exact rotation (the
+    roundings of c, s, the product and the fused multiply-add), as float16
+    RoPE is.  Over the 64 pairs, by Cauchy-Schwarz, the key side adds at most
+    3 sqrt(2) 2^-11 |q| |k| and the query side 2^-11 |q| |k|: together
+    <= 6 2^-11 |q| |k|; float16 subnormals (below 2^-14) add at most 2^-25
+    per element: 2^-25 sqrt(128) (|k| + 2 |q|).  The float32 sums of the 128
+    exact products add at most 8 sqrt(129) u sum|q'_j k'_j| under the
     probabilistic rounding model (independent roundings, 8 standard
-    deviations), <= that times |q| |k| by Cauchy-Schwarz.  So |ds| <= eps_s
-    = scale (2^-10 + 20 u + 8 sqrt(129) u) |q| max_t |k_t|.
+    deviations).  So |ds| <= eps_s = scale (6 2^-11 + (20 + 8 sqrt(129)) u)
+    |q| max_t |k_t| + 2^-25 sqrt(128) (max_t |k_t| + 2 |q|).
   * weights: a score error eps_s moves every weight by a factor within
     e^(+-2 eps_s); the float32 scaling, reference subtraction and exp2 add
     8 u (|s| log2 e + 8) to the exponent; the weights enter the value
@@ -102,7 +108,9 @@ def _reference(case, b, heads=None, base=BASE):
         kv = h // GQ
         ref[h] = p[h] @ v16[:, kv]
         kmax = float(np.max(np.linalg.norm(k16[:, kv], axis=1)))
-        eps_s = scale * (2.0 ** -10 + (20 + 8 * math.sqrt(129)) * U) * np.linalg.norm(q[h]) * kmax
+        qn = float(np.linalg.norm(q[h]))
+        eps_s = (scale * (6 * 2.0 ** -11 + (20 + 8 * math.sqrt(129)) * U) * qn * kmax
+                 + 2.0 ** -25 * math.sqrt(128) * (kmax + 2 * qn))
         smax = float(np.max(np.abs(s[h]))) * math.log2(math.e)
         C = (math.expm1(2 * eps_s + 8 * U * (smax + 8)) + 2.0 ** -11 + 16 * math.sqrt(L) * U
              + 4 * U)
