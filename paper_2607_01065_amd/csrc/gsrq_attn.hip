@@ -134,6 +134,28 @@ __device__ __forceinline__ void wave_lds_order() {
   asm volatile("" ::: "memory");
 }
 
+// Offset in float16 elements of 16-byte chunk c (dims 8 c .. 8 c + 7) of row
+// r in a wave's value tile [32 k positions][64 dims].  Chunks are permuted
+// per row by c ^ rot3((r / 2) % 8), rot3 a 3-bit rotation, so that the
+// 16-byte writes of 16 consecutive rows (one chunk each) and the 8-byte
+// transposing reads of 4 consecutive rows (4 chunks each) hit distinct
+// banks.
+__device__ __forceinline__ int tile_off(int r, int c) {
+  const int x = (r >> 1) & 7;
+  const int sw = ((x & 1) << 2) | (x >> 1);
+  return r * 64 + ((c ^ sw) << 3);
+}
+
+// ds_read_b64_tr_b16: lane l of each group of 16 lanes receives element
+// l % 4 of the 8-byte chunks addressed by lanes 4 r + l / 4 of its group,
+// r = 0 .. 3 (the MFMA operand layout of a row-major 16-bit matrix).
+__device__ __forceinline__ uint2 tr_load_b64(const _Float16* p) {
+  typedef __attribute__((__vector_size__(4 * sizeof(__fp16)))) __fp16 fp16x4;
+  typedef __attribute__((address_space(3))) fp16x4* lds_fp16x4;
+  const fp16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4f16((lds_fp16x4)(p));
+  return __builtin_bit_cast(uint2, v);
+}
+
 template <int GQ>
 __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
   using C = AtCfg<GQ>;
@@ -393,9 +415,10 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       }
 
       // ---- value sums o[c] += P . V, in two halves of the head (tiles
-      // c = 2 hp, 2 hp + 1): every lane writes the elements of its token's
-      // four value codewords of that half into the wave's tile at
-      // [dim][kpos], then reads its B operands (8 tokens of one dim) back
+      // c = 2 hp, 2 hp + 1): every lane writes its token's four value
+      // codewords of that half into row kpos of the wave's tile
+      // ([kpos][64 dims], swizzled 16-byte chunks), then reads its B
+      // operands (8 k positions of one dim) with transposing loads
       const uint32_t vw0 = hh ? vcw[1] : vcw[0], vw1 = hh ? vcw[3] : vcw[2];
 #pragma unroll
       for (int hp = 0; hp < 2; ++hp) {
@@ -404,19 +427,25 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
         for (int i = 0; i < 4; ++i) {
           const int code = (vw >> (8 * i)) & 255;
           const int sub = 8 * hp + 4 * hh + i;
-          const h8 v8 = as_h8(*(const u4*)(vtab + (sub * AT_K + code) * 8));
-          // dims of this codeword within the half: 32 hh + 8 i + e
-#pragma unroll
-          for (int e = 0; e < 8; ++e) tile[(32 * hh + 8 * i + e) * AT_BLK + kpos] = v8[e];
+          const u4 v8 = *(const u4*)(vtab + (sub * AT_K + code) * 8);
+          *(u4*)(tile + tile_off(kpos, 4 * hh + i)) = v8;     // dims 32 hh + 8 i ..
         }
         wave_lds_order();
 #pragma unroll
         for (int cc = 0; cc < 2; ++cc) {
 #pragma unroll
           for (int s2 = 0; s2 < 2; ++s2) {
-            const h8 vb = as_h8(*(const u4*)(tile + (32 * cc + tl) * AT_BLK + 16 * s2 + 8 * hh));
-            o[2 * hp + cc] =
-                __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), vb, o[2 * hp + cc], 0, 0, 0);
+            // lane j of a 16-lane group supplies k position 16 s2 + 8 hh +
+            // 4 ld + (j % 16) / 4, dims 32 cc + 16 ((j / 16) % 2) + 4 (j % 4)
+            // .. + 3; lane l then receives dim 32 cc + l % 32 at the four k
+            // positions 16 s2 + 8 hh + 4 ld + 0..3
+            const int cq = 4 * cc + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+            const int r0 = 16 * s2 + 8 * hh + ((lane >> 2) & 3);
+            const uint2 t0 = tr_load_b64(tile + tile_off(r0, cq) + 4 * (lane & 1));
+            const uint2 t1 = tr_load_b64(tile + tile_off(r0 + 4, cq) + 4 * (lane & 1));
+            const u4 vb = {t0.x, t0.y, t1.x, t1.y};
+            o[2 * hp + cc] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), as_h8(vb),
+                                                                    o[2 * hp + cc], 0, 0, 0);
           }
         }
         wave_lds_order();
