@@ -42,11 +42,11 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 constexpr int AT_HD = 128;            // head dimension
 constexpr int AT_SUB = 16;            // d = 8 subspaces per head
 constexpr int AT_K = 256;             // codewords per codebook
-constexpr int AT_WAVES = 4;
+constexpr int AT_WAVES = 8;            // two waves per SIMD share the tables
 constexpr int AT_THREADS = AT_WAVES * 64;
 constexpr int AT_BLK = 32;            // tokens per MFMA block
 constexpr int AT_PART = AT_HD + 2;    // partial record: o[128], reference max, sum
-constexpr int AT_TARGET_WG = 512;     // workgroups aimed for per launch (2 per CU)
+constexpr int AT_TARGET_WG = 256;     // workgroups aimed for per launch (1 per CU)
 constexpr float AT_HEADROOM = 8.f;    // log2 margin of a raised reference maximum
 constexpr float AT_PSHIFT = 15.f;     // weights 2^(s - m + 15) <= 2^15: float16 range
 constexpr int AT_TAB = AT_SUB * AT_K * 8;   // float16 elements of one codeword table
@@ -59,14 +59,15 @@ template <int GQ> struct AtCfg {
   static constexpr int KTAB = 0;                            // f16 [16][256][8] keys
   static constexpr int VTAB = KTAB + AT_TAB * 2;            // f16 [16][256][8] values
   static constexpr int QT = VTAB + AT_TAB * 2;              // f32 [32][128] queries
-  // per wave: the value tile of half a head [64 dims][32 tokens] f16; the
-  // group's angle table (float2 [64]) shares it at the start of a group,
-  // and the final merge (f32 [AT_RED]) after the last group
+  // per wave: the value tile of a quarter head [32 k positions][32 dims]
+  // f16; the group's angle table (float2 [64]) shares it at the start of a
+  // group.  The final merge (f32 [AT_WAVES][AT_RED]) reuses the key table.
   static constexpr int TILE = QT + 32 * AT_HD * 4;
-  static constexpr int TILE_BYTES = 64 * AT_BLK * 2;
+  static constexpr int TILE_BYTES = 32 * AT_BLK * 2;
   static constexpr int BYTES = TILE + AT_WAVES * TILE_BYTES;
 };
-static_assert(AT_RED * 4 <= 64 * AT_BLK * 2 && 64 * 8 <= 64 * AT_BLK * 2, "tile aliases");
+static_assert(64 * 8 <= 32 * AT_BLK * 2, "angle table fits the tile");
+static_assert(AT_WAVES * AT_RED * 4 <= AT_TAB * 2, "merge records fit the key table");
 static_assert(AtCfg<4>::BYTES <= 160 * 1024, "LDS budget");
 
 struct AttnArgs {
@@ -135,15 +136,13 @@ __device__ __forceinline__ void wave_lds_order() {
 }
 
 // Offset in float16 elements of 16-byte chunk c (dims 8 c .. 8 c + 7) of row
-// r in a wave's value tile [32 k positions][64 dims].  Chunks are permuted
-// per row by c ^ rot3((r / 2) % 8), rot3 a 3-bit rotation, so that the
-// 16-byte writes of 16 consecutive rows (one chunk each) and the 8-byte
-// transposing reads of 4 consecutive rows (4 chunks each) hit distinct
-// banks.
+// r in a wave's value tile [32 k positions][32 dims] (64-byte rows, four to
+// 256 bytes of banks).  Chunks are permuted per row by c ^ ((r / 4) % 4), so
+// that the 16-byte writes of 16 consecutive rows (one chunk each) and the
+// 8-byte transposing reads of 4 consecutive rows (4 chunks each) hit
+// distinct banks.
 __device__ __forceinline__ int tile_off(int r, int c) {
-  const int x = (r >> 1) & 7;
-  const int sw = ((x & 1) << 2) | (x >> 1);
-  return r * 64 + ((c ^ sw) << 3);
+  return r * 32 + ((c ^ ((r >> 2) & 3)) << 3);
 }
 
 // ds_read_b64_tr_b16: lane l of each group of 16 lanes receives element
@@ -414,47 +413,44 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
         ph[s2] = pack_h8(xh);
       }
 
-      // ---- value sums o[c] += P . V, in two halves of the head (tiles
-      // c = 2 hp, 2 hp + 1): every lane writes its token's four value
-      // codewords of that half into row kpos of the wave's tile
-      // ([kpos][64 dims], swizzled 16-byte chunks), then reads its B
-      // operands (8 k positions of one dim) with transposing loads
-      const uint32_t vw0 = hh ? vcw[1] : vcw[0], vw1 = hh ? vcw[3] : vcw[2];
+      // ---- value sums o[c] += P . V over four quarters of the head (tile
+      // c = 2 hp + cc: dims 32 c .. 32 c + 31, subspaces 4 c .. 4 c + 3):
+      // every lane writes two of its token's value codewords of the quarter
+      // into row kpos of the wave's tile ([kpos][32 dims], swizzled 16-byte
+      // chunks), then reads its B operands (8 k positions of one dim) with
+      // transposing loads
 #pragma unroll
-      for (int hp = 0; hp < 2; ++hp) {
-        const uint32_t vw = hp ? vw1 : vw0;
+      for (int c = 0; c < 4; ++c) {
+        const uint32_t vw = vcw[c];                  // codes of subspaces 4 c .. 4 c + 3
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int code = (vw >> (8 * i)) & 255;
-          const int sub = 8 * hp + 4 * hh + i;
-          const u4 v8 = *(const u4*)(vtab + (sub * AT_K + code) * 8);
-          *(u4*)(tile + tile_off(kpos, 4 * hh + i)) = v8;     // dims 32 hh + 8 i ..
+        for (int i = 0; i < 2; ++i) {
+          const int code = (vw >> (8 * (2 * hh + i))) & 255;
+          const u4 v8 = *(const u4*)(vtab + ((4 * c + 2 * hh + i) * AT_K + code) * 8);
+          *(u4*)(tile + tile_off(kpos, 2 * hh + i)) = v8;     // dims 16 hh + 8 i ..
         }
         wave_lds_order();
 #pragma unroll
-        for (int cc = 0; cc < 2; ++cc) {
-#pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2) {
-            // lane j of a 16-lane group supplies k position 16 s2 + 8 hh +
-            // 4 ld + (j % 16) / 4, dims 32 cc + 16 ((j / 16) % 2) + 4 (j % 4)
-            // .. + 3; lane l then receives dim 32 cc + l % 32 at the four k
-            // positions 16 s2 + 8 hh + 4 ld + 0..3
-            const int cq = 4 * cc + 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
-            const int r0 = 16 * s2 + 8 * hh + ((lane >> 2) & 3);
-            const uint2 t0 = tr_load_b64(tile + tile_off(r0, cq) + 4 * (lane & 1));
-            const uint2 t1 = tr_load_b64(tile + tile_off(r0 + 4, cq) + 4 * (lane & 1));
-            const u4 vb = {t0.x, t0.y, t1.x, t1.y};
-            o[2 * hp + cc] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), as_h8(vb),
-                                                                    o[2 * hp + cc], 0, 0, 0);
-          }
+        for (int s2 = 0; s2 < 2; ++s2) {
+          // lane j of a 16-lane group supplies k position 16 s2 + 8 hh + 4 ld
+          // + (j % 16) / 4, dims 16 ((j / 16) % 2) + 4 (j % 4) .. + 3; lane l
+          // then receives dim l % 32 of the quarter at the four k positions
+          // 16 s2 + 8 hh + 4 ld + 0..3
+          const int cq = 2 * ((lane >> 4) & 1) + ((lane & 3) >> 1);
+          const int r0 = 16 * s2 + 8 * hh + ((lane >> 2) & 3);
+          const uint2 t0 = tr_load_b64(tile + tile_off(r0, cq) + 4 * (lane & 1));
+          const uint2 t1 = tr_load_b64(tile + tile_off(r0 + 4, cq) + 4 * (lane & 1));
+          const u4 vb = {t0.x, t0.y, t1.x, t1.y};
+          o[c] = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ph[s2]), as_h8(vb), o[c], 0, 0, 0);
         }
         wave_lds_order();
       }
     }
   }
 
-  // ---- merge the four waves: per head the reference, the sum and o
-  float* rw = (float*)tile;
+  // ---- merge the waves: per head the reference, the sum and o (records
+  // in the key table, once every wave is done with it)
+  __syncthreads();
+  float* rw = (float*)(lds + C::KTAB) + w * AT_RED;
   {
     float l = lsum;
 #pragma unroll
@@ -479,8 +475,8 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
       }
   }
   __syncthreads();
-  const float* red = (const float*)(lds + C::TILE);
-  constexpr int RS = C::TILE_BYTES / 4;              // floats between waves' records
+  const float* red = (const float*)(lds + C::KTAB);
+  constexpr int RS = AT_RED;                         // floats between waves' records
   for (int i = tid; i < GQ * AT_HD; i += AT_THREADS) {
     const int h = i / AT_HD, n = i % AT_HD;
     float M = -INFINITY;
