@@ -30,6 +30,7 @@ METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline
 TRAFFIC = {"source_sha256_prefix": "b9e95e6ffcbefa9f", "bytes_per_launch": 116571602}
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
+PEAK_LDS_TBPS = 256 * 128 * 2.4e9 / 1e12   # LDS: 256 CUs x 128 B/clk x 2.4 GHz
 HEAD_DIM = 128
 
 
@@ -298,10 +299,49 @@ def attention_measure(B, dev, reps=50, shape=ATTN_SHAPE):
         "call_us": call_us, "kernel_us": kern_us,
         "token_heads_per_s": tok_heads / (call_us * 1e-6),
         "algorithmic_bytes": alg_bytes,
+        # LDS bytes: 16 key and 16 value codewords gathered (16 B each), the
+        # value codewords stored to and read back from the tile: 1 KiB per
+        # token and key/value head
+        "lds_bytes": tok_heads * 1024,
         "hbm_GBps": alg_bytes / (kern_us * 1e-6) / 1e9,
         "hbm_frac": alg_bytes / (kern_us * 1e-6) / 1e9 / PEAK_HBM_GBPS,
         "fp16_attention_us": fp16_us,
         "speedup_vs_fp16_attention": fp16_us / call_us}}
+
+
+def attention_cpu_baseline(shape=ATTN_SHAPE, budget_s=10.0):
+    """Time the float64 oracle on whole sequences of the attention workload
+    (unpack, dequantise, RoPE, attention), as many as fit in about budget_s
+    seconds (at least one), and scale to token-heads/s of the workload."""
+    import numpy as np
+
+    import synth
+    from oracle import gsrq_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    Bn, cap, Hkv, GQ = shape["B"], shape["cap"], shape["Hkv"], shape["GQ"]
+    case = synth.attn_case(Bn, cap, [cap] * Bn, Hkv, GQ, seed=0, q_dtype="float16")
+    G = Hkv * HEAD_DIM // 8
+    done, t = 0, 0.0
+    while done < Bn and (done == 0 or t < budget_s):
+        t0 = time.perf_counter()
+        kc = O.unpack_codes(case["k_codes"][done], 1, G, 256)
+        vc = O.unpack_codes(case["v_codes"][done], 1, G, 256)
+        k = O.gsrq_decode(kc, case["k_gain"], case["k_shape"])
+        v = O.gsrq_decode(vc, case["v_gain"], case["v_shape"])
+        k = k.astype(np.float32).astype(np.float16).reshape(cap, Hkv, HEAD_DIM)
+        v = v.astype(np.float32).astype(np.float16).reshape(cap, Hkv, HEAD_DIM)
+        O.attn_decode(case["q"][done], k, v, 500000.0)
+        t += time.perf_counter() - t0
+        done += 1
+    return {"value": done * cap * Hkv / t, "unit": "token-heads/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": (f"float64 oracle (unpack, decode, float16 rounding, RoPE, attention) on "
+                       f"{done} of {Bn} sequences of {cap} tokens x {Hkv} key/value heads "
+                       f"({t:.1f} s)")}
 
 
 def breakdown(B, step):
@@ -332,14 +372,30 @@ def main():
         raise SystemExit("bench.py needs a GPU")
     if args.workload == "decode_attention_1bit":
         r = attention_measure(B, torch.device("cuda", 0), reps=args.steps)["decode_attention"]
-        print(json.dumps({"metric": "decode attention token-heads/s over 1-bit coded K/V",
-                          "value": r["token_heads_per_s"], "unit": "token-heads/s",
-                          "n_gpus": 1, "steps": args.steps, "warmup": 1,
-                          "ms_per_step": r["call_us"] / 1e3, "higher_is_better": True,
-                          "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-                          "data": "synthetic",
-                          "config": {"workload": "decode_attention_1bit", "shape": r["shape"]},
-                          **{k: v for k, v in r.items() if k != "shape"}}), flush=True)
+        line = {"metric": "decode attention token-heads/s over 1-bit coded K/V",
+                "value": r["token_heads_per_s"], "unit": "token-heads/s",
+                "n_gpus": 1, "steps": args.steps, "warmup": 1,
+                "ms_per_step": r["call_us"] / 1e3, "higher_is_better": True,
+                "scaling": "weak", "vs_baseline": None, "dtype": "f16",
+                "data": "synthetic",
+                "config": {"workload": "decode_attention_1bit", "shape": r["shape"]},
+                **{k: v for k, v in r.items() if k != "shape"}}
+        gbps = r["algorithmic_bytes"] / (r["kernel_us"] * 1e-6) / 1e9
+        lds_tbps = r["lds_bytes"] / (r["kernel_us"] * 1e-6) / 1e12
+        line["roofline"] = {
+            "kernel": "attn_chunk_kernel (unpack + dequantise + RoPE + attention)",
+            "bound": "hbm", "achieved": gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+            "frac": gbps / PEAK_HBM_GBPS, "traffic": None,
+            "bytes_per_launch": r["algorithmic_bytes"], "avg_launch_us": r["kernel_us"],
+            "lds_view": {"achieved": lds_tbps, "peak": PEAK_LDS_TBPS, "unit": "TB/s",
+                         "frac": lds_tbps / PEAK_LDS_TBPS, "bytes_per_launch": r["lds_bytes"],
+                         "note": "codeword gathers, value-tile stores and transposing loads: "
+                                 "1 KiB per token and key/value head; peak = 256 CU x 128 "
+                                 "B/clk x 2.4 GHz; the kernel is bound by LDS bank conflicts "
+                                 "of the random gathers, not by HBM"}}
+        if not args.no_cpu_baseline:
+            line["cpu_baseline"] = attention_cpu_baseline()
+        print(json.dumps(line), flush=True)
         return
     wl = synth.WORKLOADS[args.workload]
     if args.stages > 0:

@@ -501,7 +501,9 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
 }
 
 // Merge the chunks of every (sequence, query head): o = sum_c 2^(m_c - M) o_c
-// / sum_c 2^(m_c - M) l_c over the chunks holding tokens.
+// / sum_c 2^(m_c - M) l_c over the chunks holding tokens.  Both passes are
+// branch-free and unrolled, so that the loads of several chunks are in
+// flight together.
 __global__ void __launch_bounds__(AT_HD) attn_merge_kernel(const float* __restrict__ part, int Hq,
                                                           int Hkv, int nch,
                                                           float* __restrict__ out) {
@@ -510,14 +512,17 @@ __global__ void __launch_bounds__(AT_HD) attn_merge_kernel(const float* __restri
   const float* p = part + (((size_t)b * Hkv + hk) * nch * GQ + h) * AT_PART;
   const size_t cs = (size_t)GQ * AT_PART;
   float M = -INFINITY;
-  for (int c = 0; c < nch; ++c)
-    if (p[c * cs + AT_HD + 1] > 0.f) M = fmaxf(M, p[c * cs + AT_HD]);
-  double num = 0.0, den = 0.0;
+#pragma unroll 8
   for (int c = 0; c < nch; ++c) {
-    const float l = p[c * cs + AT_HD + 1];
-    if (!(l > 0.f)) continue;
-    const double f = exp2((double)p[c * cs + AT_HD] - (double)M);
-    num += f * (double)p[c * cs + n];
+    const float m = p[c * cs + AT_HD], l = p[c * cs + AT_HD + 1];
+    M = l > 0.f ? fmaxf(M, m) : M;
+  }
+  double num = 0.0, den = 0.0;
+#pragma unroll 8
+  for (int c = 0; c < nch; ++c) {
+    const float m = p[c * cs + AT_HD], l = p[c * cs + AT_HD + 1], o = p[c * cs + n];
+    const double f = l > 0.f ? exp2((double)m - (double)M) : 0.0;
+    num += f * (double)o;
     den += f * (double)l;
   }
   out[(size_t)bq * AT_HD + n] = den > 0.0 ? (float)(num / den) : 0.f;
