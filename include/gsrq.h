@@ -27,7 +27,7 @@
  *    t*b, t = m*G + g, of the row's bit string, least significant bit first
  *    (bit p is bit p%32 of word p/32).
  *  - Supported on this build: 1 <= d <= 8 with 2 <= K <= 256, and
- *    d in {8, 16, 32, 64, 128} with any power-of-two 2 <= K <= 65536.
+ *    d in {8, 16, 32, 64, 128, 256} with any power-of-two 2 <= K <= 65536.
  *    Other valid shapes return GSRQ_E_UNSUPPORTED.
  *  - Apart from the opt-in launch timing at the end of this header, the
  *    library keeps no state between calls; calls on different streams with

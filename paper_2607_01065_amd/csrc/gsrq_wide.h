@@ -11,7 +11,7 @@
 
 namespace gsrq_wide {
 
-// d a multiple of 8 with 8 <= d <= 128, and d > 8 or K > 256.
+// d = 8 C with C a power of two, 8 <= d <= 256, and d > 8 or K > 256.
 bool serves(const gsrq_shape* s);
 
 size_t train_workspace_bytes(const gsrq_shape* s, size_t x_elt);

@@ -1,5 +1,5 @@
 // Wide-subspace kernel family of the GSRQ hot path for AMD MI355X (gfx950):
-// subvectors of d = 8 C elements (C = 1, 2, 4, 8 or 16 groups of eight) and
+// subvectors of d = 8 C elements (C = 1, 2, 4, 8, 16 or 32 groups of eight) and
 // codebooks of any power-of-two size K.  It serves the shapes the narrow
 // family in gsrq.hip cannot hold in registers (d > 8 or K > 256).
 //
@@ -40,7 +40,7 @@ namespace {
 constexpr int W_WAVES = 8;
 constexpr int W_THREADS = W_WAVES * 64;
 constexpr int W_ROWS = W_WAVES * RB;            // rows per workgroup round
-constexpr int W_CMAX = 16;                      // d <= 128
+constexpr int W_CMAX = 32;                      // d <= 256
 constexpr int W_RESIDENT_BYTES = 63 * 1024;     // fragment tables kept whole in LDS
 constexpr int W_STREAM_BYTES = 30720;           // one staging buffer when streamed
 constexpr int W_SREG = (W_STREAM_BYTES / 16 + W_THREADS - 1) / W_THREADS;  // staged u4 per thread
@@ -60,6 +60,14 @@ enum { W_TRAIN = 0, W_ENCODE = 1 };
 __host__ __device__ constexpr int w_pairs(int C) { return (C + 1) / 2; }
 // Fragments per tile: HI_p, LO_p for every pair, then the bias fragment.
 __host__ __device__ constexpr int w_frags(int C) { return 2 * w_pairs(C) + 1; }
+// Staged u4 per thread of a streamed chunk: a chunk holds at least one whole
+// tile (33 fragments at d = 256 exceed the W_STREAM_BYTES budget).
+__host__ __device__ constexpr int w_sreg(int C) {
+  return W_SREG > (w_frags(C) * 64 + W_THREADS - 1) / W_THREADS
+             ? W_SREG
+             : (w_frags(C) * 64 + W_THREADS - 1) / W_THREADS;
+}
+static_assert(w_sreg(W_CMAX) * W_THREADS >= w_frags(W_CMAX) * 64, "staging holds one tile");
 
 // ------------------------------------------------------------------ kernels
 
@@ -450,19 +458,20 @@ __device__ __forceinline__ void w_take(int key, int t, int& best, int& bt) {
 
 // The loads never branch (indices past n are clamped and their values never
 // stored), so they stay in flight while the current chunk is scored.
-template <int QU>
+template <int QU, int SR>
 __device__ __forceinline__ void w_stage_load(const u4* ftab, int QF, int t0, int n,
-                                             u4 (&reg)[W_SREG]) {
+                                             u4 (&reg)[SR]) {
 #pragma unroll
-  for (int r = 0; r < W_SREG; ++r) {
+  for (int r = 0; r < SR; ++r) {
     const int e = min(r * W_THREADS + (int)threadIdx.x, n - 1);
     const int t = e / (QU * 64), o = e - t * (QU * 64);
     reg[r] = ftab[((size_t)(t0 + t) * QF) * 64 + o];
   }
 }
-__device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[W_SREG]) {
+template <int SR>
+__device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[SR]) {
 #pragma unroll
-  for (int r = 0; r < W_SREG; ++r) {
+  for (int r = 0; r < SR; ++r) {
     const int e = r * W_THREADS + (int)threadIdx.x;
     if (e < n) buf[e] = reg[r];
   }
@@ -623,7 +632,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       const int tpc = a.tpc;
       const int nch = (tiles + tpc - 1) / tpc;
       const int chunk_u4 = tpc * QU * 64;
-      u4 reg[W_SREG];
+      u4 reg[w_sreg(C)];
       {
         const int n = min(tpc, tiles) * QU * 64;
         w_stage_load<QU>(ftab, a.QF, 0, n, reg);
@@ -1150,24 +1159,24 @@ __global__ void __launch_bounds__(1024) w_bucket_kernel(const uint16_t* __restri
 }
 
 // Batched member loop of the accumulation: members [0, n), member `it` is
-// row row_of(it) of codeword asg[row] in [k0, k0 + ks).  Lane groups of d/2
-// lanes take one member each (two elements per lane), W_ACC_MEMBERS members
+// row row_of(it) of codeword asg[row] in [k0, k0 + ks).  Lane groups of d / E
+// lanes take one member each (E elements per lane), W_ACC_MEMBERS members
 // per lane group in flight: every load of a batch is issued before the
 // first use (past the end a lane group re-reads its first member and adds
 // nothing).
-template <typename T, typename RowOf>
+template <typename T, int E, typename RowOf>
 __device__ __forceinline__ void w_acc_members(const WAccArgs& a, int g, int k0, double* wacc,
                                               int n, RowOf row_of) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = a.d, S = 2 * d + 2;
-  const int L = d / 2;                 // lanes per member row (power of two)
+  const int L = d / E;                 // lanes per member row (power of two, <= 64)
   const int per_wave = 64 / L;
   const int sub = lane / L, li = lane % L;
   const uint16_t* asg = a.assign + (size_t)g * a.N;
   const T* X = (const T*)a.x;
   const int stride = W_WAVES * per_wave;
   for (int it0 = wave * per_wave + sub; it0 < n; it0 += W_ACC_MEMBERS * stride) {
-    float x0[W_ACC_MEMBERS], x1[W_ACC_MEMBERS], wt[W_ACC_MEMBERS];
+    float xv[W_ACC_MEMBERS][E], wt[W_ACC_MEMBERS];
     int k[W_ACC_MEMBERS];
 #pragma unroll
     for (int u = 0; u < W_ACC_MEMBERS; ++u) {
@@ -1175,21 +1184,24 @@ __device__ __forceinline__ void w_acc_members(const WAccArgs& a, int g, int k0, 
       const int64_t row = row_of(it);
       k[u] = asg[row];
       const T* xr = X + row * a.ldx + (int64_t)g * d;
-      x0[u] = (float)xr[2 * li];
-      x1[u] = (float)xr[2 * li + 1];
+#pragma unroll
+      for (int e = 0; e < E; ++e) xv[u][e] = (float)xr[E * li + e];
       wt[u] = a.w ? a.w[row] : 1.f;
     }
 #pragma unroll
     for (int u = 0; u < W_ACC_MEMBERS; ++u) {
-      float ss = fmaf(x0[u], x0[u], x1[u] * x1[u]);
+      float ss = xv[u][E - 1] * xv[u][E - 1];
+#pragma unroll
+      for (int e = E - 2; e >= 0; --e) ss = fmaf(xv[u][e], xv[u][e], ss);
       for (int off = L / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
       if (it0 + u * stride >= n) continue;   // uniform within the lane group
       const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
       double* ak = wacc + (size_t)(k[u] - k0) * S;
-      unsafeAtomicAdd(ak + 2 * li, (double)(x0[u] * (wt[u] * inv)));
-      unsafeAtomicAdd(ak + 2 * li + 1, (double)(x1[u] * (wt[u] * inv)));
-      unsafeAtomicAdd(ak + d + 2 * li, (double)(x0[u] * wt[u]));
-      unsafeAtomicAdd(ak + d + 2 * li + 1, (double)(x1[u] * wt[u]));
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        unsafeAtomicAdd(ak + E * li + e, (double)(xv[u][e] * (wt[u] * inv)));
+#pragma unroll
+      for (int e = 0; e < E; ++e) unsafeAtomicAdd(ak + d + E * li + e, (double)(xv[u][e] * wt[u]));
       if (li == 0) {
         unsafeAtomicAdd(ak + 2 * d, (double)wt[u]);
         unsafeAtomicAdd(ak + 2 * d + 1, 1.0);
@@ -1203,8 +1215,9 @@ __device__ __forceinline__ void w_acc_members(const WAccArgs& a, int g, int k0, 
 // per codeword, accumulated in float64 LDS and written as one partial.
 // Members: with one slice, every row of the chunk; with bucketed rows, the
 // chunk's share of the slice's buckets; otherwise the chunk's members of
-// the slice, collected into an LDS list first.
-template <typename T>
+// the slice, collected into an LDS list first.  E elements per lane: 2, or
+// 4 for d = 256 (a lane group is at most one wave).
+template <typename T, int E>
 __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
   extern __shared__ double wacc[];
   __shared__ int list[W_THREADS * W_ACC_BATCH];
@@ -1223,13 +1236,13 @@ __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
     const int mb = m0 + (int)((int64_t)(m1 - m0) * rc / a.rchunks);
     const int me = m0 + (int)((int64_t)(m1 - m0) * (rc + 1) / a.rchunks);
     const int* srt = a.sorted + (size_t)g * a.N + mb;
-    w_acc_members<T>(a, g, k0, wacc, me - mb, [&](int it) { return (int64_t)srt[it]; });
+    w_acc_members<T, E>(a, g, k0, wacc, me - mb, [&](int it) { return (int64_t)srt[it]; });
     __syncthreads();
   } else {
     const int64_t r0 = (int64_t)rc * a.rows_per_chunk;
     const int64_t r1 = min(a.N, r0 + a.rows_per_chunk);
     if (a.slices == 1) {
-      w_acc_members<T>(a, g, k0, wacc, (int)(r1 - r0), [&](int it) { return r0 + it; });
+      w_acc_members<T, E>(a, g, k0, wacc, (int)(r1 - r0), [&](int it) { return r0 + it; });
       __syncthreads();
     } else {
       const uint16_t* asg = a.assign + (size_t)g * a.N;
@@ -1251,7 +1264,7 @@ __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
           if (in) list[base_idx + rank] = (int)(row - r0);
         }
         __syncthreads();
-        w_acc_members<T>(a, g, k0, wacc, nlist, [&](int it) { return r0 + list[it]; });
+        w_acc_members<T, E>(a, g, k0, wacc, nlist, [&](int it) { return r0 + list[it]; });
         __syncthreads();
       }
     }
@@ -1279,8 +1292,8 @@ struct WFinArgs {
   int kmeans;             // K-means baseline update instead of eqs. (7)(8)
 };
 
-// Codebook update from the chunk partials (fixed order): d/2 lanes per
-// codeword, two elements per lane.  Initial pass (t = 0): eq. (8) gains for
+// Codebook update from the chunk partials (fixed order): d / E lanes per
+// codeword, E elements per lane (E = 2, or 4 for d = 256).  Initial pass (t = 0): eq. (8) gains for
 // the seed shapes (a codeword without members keeps its seed row's norm).
 // Iteration: eqs. (7) and (8) with the safeguards; thread 0 of block 0
 // applies the stop test of its subspace.  The trace entry (zeroed by the
@@ -1289,39 +1302,56 @@ struct WFinArgs {
 // distortion after the update, J_before - sum_k W_k ||m_k - c_k||^2 (the
 // weighted mean m_k replacing the old centroid c_k), each block adding its
 // codewords' share.
+template <int E>
 __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
   __shared__ double red[4];
   const int g = blockIdx.y;
   if (a.t > 0 && a.done[g] != 0 && a.done[g] < a.t) return;
   const int d = a.d, K = a.K, S = 2 * d + 2;
-  const int L = d / 2;
+  const int L = d / E;                 // lanes per codeword (power of two, <= 64)
   const int tid = threadIdx.x;
   const int k = blockIdx.x * (256 / L) + tid / L;
   const int li = tid % L;
   const bool active = k < K;
   const int kk = active ? k : K - 1;
-  double sy0 = 0, sy1 = 0, sx0 = 0, sx1 = 0, W = 0;
+  double sy[E], sx[E], W = 0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) sy[e] = sx[e] = 0.0;
   for (int c = 0; c < a.rchunks; ++c) {
     const double* p = a.part + (((size_t)g * a.rchunks + c) * K + kk) * S;
-    sy0 += p[2 * li]; sy1 += p[2 * li + 1];
-    sx0 += p[d + 2 * li]; sx1 += p[d + 2 * li + 1];
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      sy[e] += p[E * li + e];
+      sx[e] += p[d + E * li + e];
+    }
     W += p[2 * d];
   }
   float* sk = a.shape + ((size_t)g * K + kk) * d;
   float* gk = a.gain + (size_t)g * K + kk;
-  double s0 = sk[2 * li], s1 = sk[2 * li + 1];
+  double sv[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) sv[e] = sk[E * li + e];
   double gnew = (a.t == 0) ? (double)a.seednorm[(size_t)g * K + kk] : (double)*gk;
   if (a.t > 0 && a.kmeans) {
     double drop = 0.0;
     if (W > 0.0) {
-      const double c0 = sx0 / W, c1 = sx1 / W;
-      const double e0 = c0 - gnew * s0, e1 = c1 - gnew * s1;
-      drop = W * fma(e0, e0, e1 * e1);
-      double cn = fma(c0, c0, c1 * c1);
+      double c[E], ee[E];
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        c[e] = sx[e] / W;
+        ee[e] = c[e] - gnew * sv[e];
+      }
+      double q = ee[E - 1] * ee[E - 1], cn = c[E - 1] * c[E - 1];
+#pragma unroll
+      for (int e = E - 2; e >= 0; --e) {
+        q = fma(ee[e], ee[e], q);
+        cn = fma(c[e], c[e], cn);
+      }
+      drop = W * q;
       for (int off = L / 2; off > 0; off >>= 1) cn += __shfl_xor(cn, off);
       cn = sqrt(cn);
-      s0 = cn > 0.0 ? c0 / cn : 0.0;
-      s1 = cn > 0.0 ? c1 / cn : 0.0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) sv[e] = cn > 0.0 ? c[e] / cn : 0.0;
       gnew = cn;
     }
     if (!active) drop = 0.0;
@@ -1334,18 +1364,25 @@ __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
     }
   } else if (W > 0.0) {
     if (a.t > 0) {
-      double mn = fma(sy0, sy0, sy1 * sy1);
+      double mn = sy[E - 1] * sy[E - 1];
+#pragma unroll
+      for (int e = E - 2; e >= 0; --e) mn = fma(sy[e], sy[e], mn);
       for (int off = L / 2; off > 0; off >>= 1) mn += __shfl_xor(mn, off);
       mn = sqrt(mn);
-      if (mn > SHAPE_KEEP_REL * W) { s0 = sy0 / mn; s1 = sy1 / mn; }
+      if (mn > SHAPE_KEEP_REL * W) {
+#pragma unroll
+        for (int e = 0; e < E; ++e) sv[e] = sy[e] / mn;
+      }
     }
-    double pr = fma(sx0, s0, sx1 * s1);
+    double pr = sx[E - 1] * sv[E - 1];
+#pragma unroll
+    for (int e = E - 2; e >= 0; --e) pr = fma(sx[e], sv[e], pr);
     for (int off = L / 2; off > 0; off >>= 1) pr += __shfl_xor(pr, off);
     gnew = fmax(0.0, pr / W);
   }
   if (active) {
-    sk[2 * li] = (float)s0;
-    sk[2 * li + 1] = (float)s1;
+#pragma unroll
+    for (int e = 0; e < E; ++e) sk[E * li + e] = (float)sv[e];
     if (li == 0) *gk = (float)gnew;
   }
   if (a.t > 0 && blockIdx.x == 0 && tid == 0) {
@@ -1691,6 +1728,14 @@ size_t w_stream_need(const WLayout& L) {
 template <typename T, int C, int MODE>
 gsrq_status w_score_launch_c(const WScoreArgs& a, const WLayout& L, hipStream_t st) {
   const dim3 grid((unsigned)(a.G * L.nwg));
+  // a streamed d = 256 tile pair (2 x 33 KiB) exceeds the default 64 KiB of
+  // dynamic LDS
+  const void* fn = L.resident ? (const void*)w_score_kernel<T, C, MODE, true>
+                              : (const void*)w_score_kernel<T, C, MODE, false>;
+  if (L.lds > 65536 &&
+      hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.lds) !=
+          hipSuccess)
+    return GSRQ_E_HIP;
   if (L.resident)
     w_score_kernel<T, C, MODE, true><<<grid, W_THREADS, L.lds, st>>>(a);
   else
@@ -1706,6 +1751,7 @@ gsrq_status w_score_launch(const WScoreArgs& a, const WLayout& L, hipStream_t st
     case 4: return w_score_launch_c<T, 4, MODE>(a, L, st);
     case 8: return w_score_launch_c<T, 8, MODE>(a, L, st);
     case 16: return w_score_launch_c<T, 16, MODE>(a, L, st);
+    case 32: return w_score_launch_c<T, 32, MODE>(a, L, st);
   }
   return GSRQ_E_UNSUPPORTED;
 }
@@ -1937,11 +1983,15 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   fa.force_changed = 0; fa.nwg = L.nwg; fa.part = part; fa.changed = changed; fa.obj = nullptr;
   fa.seednorm = seednorm; fa.gain = gain; fa.shape = shape; fa.done = done; fa.iters = iters;
   fa.trace = obj_trace; fa.xchanged = XD.xchanged; fa.xobj = XD.xobj; fa.kmeans = kmeans;
-  const int cpb = 256 / (d / 2);
+  // elements per lane of the accumulation and the update: lane groups of
+  // d / E lanes, at most one wave
+  const bool e4 = d > 128;
+  const int cpb = 256 / (d / (e4 ? 4 : 2));
   const dim3 fgrid((unsigned)((K + cpb - 1) / cpb), (unsigned)G);
 
   // the accumulator slice can exceed the default dynamic LDS limit
-  if (hipFuncSetAttribute((const void*)w_accumulate_kernel<T>,
+  if (hipFuncSetAttribute(e4 ? (const void*)w_accumulate_kernel<T, 4>
+                             : (const void*)w_accumulate_kernel<T, 2>,
                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)A.lds) != hipSuccess)
     return GSRQ_E_HIP;
   auto accumulate_finalize = [&]() -> gsrq_status {
@@ -1953,12 +2003,18 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
             assign, s->N, K, aa.done, (int*)(base + W.boff), (int*)(base + W.sorted));
         if ((e2 = launch_ok())) return e2;
       }
-      w_accumulate_kernel<T><<<agrid, W_THREADS, A.lds, st>>>(aa);
+      if (e4)
+        w_accumulate_kernel<T, 4><<<agrid, W_THREADS, A.lds, st>>>(aa);
+      else
+        w_accumulate_kernel<T, 2><<<agrid, W_THREADS, A.lds, st>>>(aa);
     }
     if ((e2 = launch_ok())) return e2;
     {
       TimedLaunch tl(GSRQ_KERNEL_FINALIZE, st);
-      w_finalize_kernel<<<fgrid, 256, 0, st>>>(fa);
+      if (e4)
+        w_finalize_kernel<4><<<fgrid, 256, 0, st>>>(fa);
+      else
+        w_finalize_kernel<2><<<fgrid, 256, 0, st>>>(fa);
     }
     return launch_ok();
   };

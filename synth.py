@@ -78,6 +78,11 @@ WORKLOADS = {
         "paper_rates_d128", 32768, 1024, 128, 256, 32, 20, "float16",
         note="32768 tok x 8 heads x 128 fp16, d=128 K=256 M=32 (2 bit; 12/16-stage prefixes "
              "are 0.75/1 bit)"),
+    # the paper's lowest rate: subvectors of two heads (d = 256), K = 256,
+    # 12 stages = 0.375 bit per element
+    "paper_rates_d256": Workload(
+        "paper_rates_d256", 32768, 1024, 256, 256, 12, 20, "float16",
+        note="32768 tok x 8 heads x 128 fp16, d=256 K=256 M=12 (0.375 bit)"),
     # large codebook, full-head vectors
     "large_codebook_d128": Workload(
         "large_codebook_d128", 65536, 1024, 128, 4096, 8, 15, "float16",

@@ -70,7 +70,7 @@ def test_workspace_queries():
     assert B.train_workspace_bytes(65536, 1024, 128, 4096) >= 8 * 4096 * 258 * 8
     # multi-stage wide encode passes the float32 residual through the workspace
     assert B.encode_workspace_bytes(65536, 1024, 128, 4096, 8) >= 2 * 65536 * 1024 * 4
-    for D, d, K in ((48, 24, 256), (512, 256, 256), (16, 4, 512)):
+    for D, d, K in ((48, 24, 256), (1024, 512, 256), (16, 4, 512)):
         with pytest.raises(B.GsrqError) as e:
             B.train_workspace_bytes(1000, D, d, K)     # not in this build
         assert e.value.status == B.GSRQ_E_UNSUPPORTED

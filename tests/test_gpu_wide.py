@@ -36,6 +36,7 @@ def _gpu():
     (700, 256, 128, 512),    # streamed, d = 128
     (1300, 32, 8, 1024),     # streamed, one group (d = 8, K > 256)
     (130, 128, 64, 32),      # one tile
+    (400, 512, 256, 256),    # streamed, d = 256 (two heads per subvector)
 ])
 def test_wide_encode_single_stage(dtype, N, D, d, K):
     say("wide encode single stage", dtype.__name__, N, D, d, K)
@@ -66,6 +67,7 @@ def test_wide_encode_single_stage(dtype, N, D, d, K):
     (np.float16, 3, 256, 16, 64, 900, True),     # stage-fused, rows re-scored in float64
     (np.float16, 2, 256, 128, 256, 400, False),  # one launch per stage (d = 128)
     (np.float16, 4, 16, 32, 64, 301, False),     # one launch per stage (d = 32)
+    (np.float32, 3, 128, 256, 512, 300, False),  # one launch per stage (d = 256)
 ])
 def test_wide_encode_multi_stage_teacher_forced(dtype, M, K, d, D, N, exact_rows):
     """Stage m is checked on the residual the GPU's own earlier choices leave.
@@ -103,16 +105,20 @@ def test_wide_encode_multi_stage_teacher_forced(dtype, M, K, d, D, N, exact_rows
     assert np.allclose(Rg, R, rtol=1e-5, atol=1e-6 * np.abs(X.astype(np.float64)).max())
 
 
-def test_paper_rate_deep_stages():
-    """The paper's own rate configuration (Sec. 6.2 / Appendix A): d = 128,
-    K = 256, M = 32 stages (2 bits per element; its prefixes of 12 and 16
-    stages are the 0.75- and 1-bit configurations).  Codebooks from the
-    oracle's GSRQ training; the 32-stage encode is checked stage by stage on
-    the residual the GPU's own earlier choices leave (margin rule), the
-    residual output against that, and the prefix decodes (12, 16, 32 stages)
-    bit for bit against a float32 emulation of the decode contract (each
-    codeword rounded to float32, stages summed in float32 in order)."""
-    M, K, d, D, N = 32, 256, 128, 256, 600
+@pytest.mark.parametrize("M,K,d,D,N,prefixes", [
+    (32, 256, 128, 256, 600, (12, 16, 32)),   # 2 bit; prefixes 0.75 / 1 / 2 bit
+    (12, 256, 256, 512, 400, (4, 12)),        # 0.375 bit (d = 256: two heads)
+])
+def test_paper_rate_deep_stages(M, K, d, D, N, prefixes):
+    """The paper's own rate configurations (Sec. 6.2 / Appendix A): K = 256
+    with d = 128 and M = 32 stages (2 bits per element; its prefixes of 12
+    and 16 stages are the 0.75- and 1-bit configurations), and d = 256 with
+    M = 12 (0.375 bit).  Codebooks from the oracle's GSRQ training; the
+    encode is checked stage by stage on the residual the GPU's own earlier
+    choices leave (margin rule), the residual output against that, and the
+    prefix decodes bit for bit against a float32 emulation of the decode
+    contract (each codeword rounded to float32, stages summed in float32 in
+    order)."""
     say("paper rate deep stages", M, K, d, D, N)
     X, w, seeds = synth.small_case(N, D, d, K, M, seed=26, dtype=np.float16)
     G = D // d
@@ -132,7 +138,7 @@ def test_paper_rate_deep_stages():
             R[:, cols] -= gain[m, g].astype(np.float64)[kk, None] * shape[m, g].astype(np.float64)[kk]
     assert np.allclose(res.cpu().numpy().astype(np.float64), R, rtol=1e-5,
                        atol=1e-6 * np.abs(X.astype(np.float64)).max())
-    for M_use in (12, 16, 32):
+    for M_use in prefixes:
         out = B.decode(codes, gd, sd, D, M_use, out_dtype=torch.float32)
         torch.cuda.synchronize()
         acc = np.zeros((N, D), np.float32)
@@ -141,7 +147,7 @@ def test_paper_rate_deep_stages():
                 kk = k[:, m, g]
                 acc[:, g * d:(g + 1) * d] += gain[m, g][kk, None] * shape[m, g][kk]
         assert np.array_equal(out.cpu().numpy(), acc), f"decode prefix {M_use}"
-        assert B.bits_per_element(d, K, M_use) == pytest.approx(M_use * 8 / 128)
+        assert B.bits_per_element(d, K, M_use) == pytest.approx(M_use * 8 / d)
 
 
 @pytest.mark.parametrize("M,K,d,D,N", [
@@ -149,6 +155,7 @@ def test_paper_rate_deep_stages():
     (1, 1024, 8, 32, 333),      # LDS table, K > 256
     (3, 4096, 128, 256, 77),    # gather from global memory, 12-bit codes
     (2, 64, 64, 128, 50),       # gather, d = 64
+    (2, 256, 256, 512, 60),     # gather, d = 256
 ])
 def test_wide_decode(M, K, d, D, N):
     say("wide decode", M, K, d, D, N)
@@ -184,6 +191,7 @@ def test_wide_decode(M, K, d, D, N):
     (np.float32, 2000, 256, 128, 128, True),
     (np.float16, 4100, 16, 8, 512, False),
     (np.float32, 1500, 64, 32, 32, True),
+    (np.float16, 1200, 512, 256, 128, True),
 ])
 def test_wide_train_teacher_forced(dtype, N, D, d, K, weighted):
     say("wide train teacher forced", dtype.__name__, N, D, d, K, weighted)
