@@ -2,6 +2,7 @@
 
 Rate sweep: 65536 tokens x 8 heads x 128 float16, d = 16, K = 256 (0.5 bit per
 stage).  Large codebook: the same rows with d = 128, K = 4096 (12-bit codes).
+The paper's lowest rate: 32768 tokens, d = 256 (two heads), K = 256.
 Both run in the launch configuration the benchmark uses, for two stages (the
 second trains on the first stage's float32 residual); the oracle checks
 sampled subspaces (and, at K = 4096, sampled rows for the index rule) with the
@@ -77,7 +78,8 @@ def _stage_checks(R, w, seeds, d, K, groups, rows, what):
 
 
 @pytest.mark.parametrize("name,groups", [("rate_sweep_d16", [0, 21, 63]),
-                                         ("large_codebook_d128", [0, 5])])
+                                         ("large_codebook_d128", [0, 5]),
+                                         ("paper_rates_d256", [0, 3])])
 def test_wide_workload_two_stages_sampled(name, groups):
     """Two stages of training at full size (stage 1 on stage 0's float32
     residual), then the two-stage encode and decode of every row."""
