@@ -23,11 +23,16 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline"
-# HBM bytes per launch of the dominant kernel, from the FETCH_SIZE / WRITE_SIZE
-# rocprofv3 passes (profiles/hbm_traffic_llama3_8b_layer_1bit.md, read counts
+# HBM bytes per launch of each workload's dominant kernel, from the FETCH_SIZE /
+# WRITE_SIZE rocprofv3 passes (profiles/hbm_traffic_<workload>.md, read counts
 # scaled x2.000 and writes x1.000 against a 256 MiB reference copy).  Valid
-# only for the kernel source those passes measured.
-TRAFFIC = {"source_sha256_prefix": "b9e95e6ffcbefa9f", "bytes_per_launch": 116571602}
+# only for the kernel source those passes measured; other workloads: null.
+TRAFFIC = {
+    "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "b9e95e6ffcbefa9f",
+                             "bytes_per_launch": 116571824},
+    "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "9e1c64146ab1d392",
+                            "bytes_per_launch": 411513874},
+}
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
 PEAK_LDS_TBPS = 256 * 128 * 2.4e9 / 1e12   # LDS: 256 CUs x 128 B/clk x 2.4 GHz
@@ -470,9 +475,12 @@ def main():
 
     a_us, f_us, e_us, dcd_us = avg_us("assign"), avg_us("finalize"), avg_us("encode"), avg_us("decode")
     import hashlib
-    src = os.path.join(ROOT, "paper_2607_01065_amd", "csrc", "gsrq.hip")
-    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    traffic = TRAFFIC["bytes_per_launch"] if sha == TRAFFIC["source_sha256_prefix"] else None
+    traffic = None
+    tr = TRAFFIC.get(wl.name)
+    if tr is not None:
+        src = os.path.join(ROOT, "paper_2607_01065_amd", "csrc", tr["source"])
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        traffic = tr["bytes_per_launch"] if sha == tr["source_sha256_prefix"] else None
     iters_run = float(torch.stack(iters).float().mean().item()) if iters else float("nan")
     flops_assign = 2.0 * N * D * K                         # eq. (5) scores, one pass
     achieved = flops_assign / (a_us * 1e-6) / 1e12
