@@ -225,7 +225,17 @@ typedef struct {
   int32_t head_dim;   /* elements per head                                   */
   float rope_base;    /* RoPE base: theta_j = rope_base^(-2j / head_dim)     */
   float scale;        /* softmax scale, normally 1 / sqrt(head_dim)          */
+  uint32_t flags;     /* GSRQ_ATTN_* below, or 0                             */
 } gsrq_attn_shape;
+
+/* The workspace already holds this call's tables: the float16 decode of the
+ * key and value codebooks and the RoPE tables, written by an earlier
+ * gsrq_attn_decode with the same workspace, codebooks (contents unchanged),
+ * Hkv, head_dim and rope_base, so this call does not rebuild them (a
+ * layer's codebooks are fixed across decoding steps).  Other arguments may
+ * differ.  Not checked: a workspace without those tables gives wrong
+ * outputs. */
+enum { GSRQ_ATTN_TABLES_READY = 1 };
 
 /* Workspace bytes gsrq_attn_decode needs for shape a. */
 gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes);

@@ -541,6 +541,7 @@ gsrq_status attn_plan(const gsrq_attn_shape* a, AttnPlan& p) {
   if (a->Hq % a->Hkv) return GSRQ_E_ARG;
   if (!(a->rope_base > 0.f) || !(a->rope_base < INFINITY)) return GSRQ_E_ARG;
   if (!(a->scale > 0.f) || !(a->scale < INFINITY)) return GSRQ_E_ARG;
+  if (a->flags & ~(uint32_t)GSRQ_ATTN_TABLES_READY) return GSRQ_E_ARG;
   if (a->B > 65535 || a->Hkv > 65535) return GSRQ_E_ARG;
   p.GQ = a->Hq / a->Hkv;
   if (a->head_dim != AT_HD) return GSRQ_E_UNSUPPORTED;
@@ -633,12 +634,14 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   args.rpc = p.rpc;
   args.qscale = (float)((double)a->scale * 1.4426950408889634);
   const int ncw = a->Hkv * AT_SUB * AT_K;
-  attn_tables_kernel<<<8 + (2 * ncw + 255) / 256, 256, 0, st>>>(
-      (double)a->rope_base, (float2*)(ws + p.off_t1), (float2*)(ws + p.off_t2),
-      (double*)(ws + p.off_th), k_gain, k_shape, v_gain, v_shape, ncw, (u4*)(ws + p.off_tk),
-      (u4*)(ws + p.off_tv));
-  e = launch_ok();
-  if (e) return e;
+  if (!(a->flags & GSRQ_ATTN_TABLES_READY)) {
+    attn_tables_kernel<<<8 + (2 * ncw + 255) / 256, 256, 0, st>>>(
+        (double)a->rope_base, (float2*)(ws + p.off_t1), (float2*)(ws + p.off_t2),
+        (double*)(ws + p.off_th), k_gain, k_shape, v_gain, v_shape, ncw, (u4*)(ws + p.off_tk),
+        (u4*)(ws + p.off_tv));
+    e = launch_ok();
+    if (e) return e;
+  }
   if (p.GQ == 1) e = attn_launch<1>(args, a->B, a->Hkv, st);
   else if (p.GQ == 2) e = attn_launch<2>(args, a->B, a->Hkv, st);
   else e = attn_launch<4>(args, a->B, a->Hkv, st);

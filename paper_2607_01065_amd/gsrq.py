@@ -37,7 +37,8 @@ class Shape(ctypes.Structure):
 class AttnShape(ctypes.Structure):
     _fields_ = [("B", ctypes.c_int32), ("cap", ctypes.c_int32), ("Hq", ctypes.c_int32),
                 ("Hkv", ctypes.c_int32), ("head_dim", ctypes.c_int32),
-                ("rope_base", ctypes.c_float), ("scale", ctypes.c_float)]
+                ("rope_base", ctypes.c_float), ("scale", ctypes.c_float),
+                ("flags", ctypes.c_uint32)]
 
 
 _lib = None
@@ -320,9 +321,14 @@ def row_weights(grad=None, *, norms=None, tau=1.0, stream=None):
     return w, norms, stats
 
 
-def make_attn_shape(B, cap, Hq, Hkv, head_dim=128, rope_base=500000.0, scale=None) -> AttnShape:
+GSRQ_ATTN_TABLES_READY = 1
+
+
+def make_attn_shape(B, cap, Hq, Hkv, head_dim=128, rope_base=500000.0, scale=None,
+                    flags=0) -> AttnShape:
     scale = 1.0 / math.sqrt(head_dim) if scale is None else float(scale)
-    return AttnShape(int(B), int(cap), int(Hq), int(Hkv), int(head_dim), float(rope_base), scale)
+    return AttnShape(int(B), int(cap), int(Hq), int(Hkv), int(head_dim), float(rope_base), scale,
+                     int(flags))
 
 
 def attn_workspace_bytes(B, cap, Hq, Hkv, head_dim=128) -> int:
@@ -334,11 +340,13 @@ def attn_workspace_bytes(B, cap, Hq, Hkv, head_dim=128) -> int:
 
 
 def attn_decode(k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, *,
-                rope_base=500000.0, scale=None, out=None, workspace=None, stream=None):
+                rope_base=500000.0, scale=None, out=None, workspace=None, stream=None,
+                tables_ready=False):
     """One decoding step of attention over coded caches (see gsrq_attn_decode).
     k_codes, v_codes [B, cap, W] packed codes; seq_len [B] int32; codebooks
     [1, G, 256] / [1, G, 256, 8]; q [B, Hq, 128] (float16/float32).  Returns
-    out [B, Hq, 128] float32."""
+    out [B, Hq, 128] float32.  tables_ready: the given workspace holds the
+    tables of these codebooks from an earlier call (GSRQ_ATTN_TABLES_READY)."""
     torch = _torch()
     lib = load_library()
     B, cap, W = k_codes.shape
@@ -354,7 +362,8 @@ def attn_decode(k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, 
         raise ValueError("inconsistent shapes")
     if seq_len.dtype != torch.int32:
         raise TypeError("seq_len must be int32")
-    ash = make_attn_shape(B, cap, Hq, Hkv, hd, rope_base, scale)
+    ash = make_attn_shape(B, cap, Hq, Hkv, hd, rope_base, scale,
+                          GSRQ_ATTN_TABLES_READY if tables_ready else 0)
     sh = make_shape(B * cap, D, d, K, M)
     n = ctypes.c_size_t()
     _check(lib.gsrq_attn_workspace_bytes(ctypes.byref(ash), ctypes.byref(n)),

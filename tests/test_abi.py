@@ -189,6 +189,7 @@ def test_attn_decode_validation_before_any_hip_call():
     assert call(dt=3) == B.GSRQ_E_ARG
     assert call(ws=D + 16) == B.GSRQ_E_ARG                      # workspace alignment
     assert call(ws_bytes=1) == B.GSRQ_E_WORKSPACE
+    assert call(a=dict(flags=2)) == B.GSRQ_E_ARG                # unknown flag
     ash = B.make_attn_shape(**a0)
     n = ctypes.c_size_t()
     assert lib.gsrq_attn_workspace_bytes(ctypes.byref(ash), ctypes.byref(n)) == B.GSRQ_OK

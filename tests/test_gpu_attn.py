@@ -185,3 +185,26 @@ def test_attn_decode_full_size_sampled():
             err = np.abs(out[b, h] - ref[h])
             assert np.all(err <= tol[h]), f"b{b} h{h}: {err.max():.3g} > {tol[h][err.argmax()]:.3g}"
 
+
+
+def test_attn_decode_tables_ready_reuses_workspace():
+    """A second call on the same workspace with GSRQ_ATTN_TABLES_READY (same
+    codebooks, new queries and lengths) skips the table build and gives the
+    output of a call that builds them, bit for bit, and the oracle's."""
+    case = synth.attn_case(3, 3000, [3000, 1700, 5], 2, 4, seed=7, q_dtype="float16")
+    t = {k: _dev(case[k]) for k in ("k_codes", "v_codes", "lens", "k_gain", "k_shape",
+                                    "v_gain", "v_shape", "q")}
+    ws = torch.empty(B.attn_workspace_bytes(3, 3000, 8, 2), dtype=torch.uint8, device="cuda")
+    args = [t[k] for k in ("k_codes", "v_codes")]
+    cb = [t[k] for k in ("k_gain", "k_shape", "v_gain", "v_shape")]
+    B.attn_decode(*args, t["lens"], *cb, t["q"], workspace=ws)
+    rng = np.random.default_rng(8)
+    case["q"] = rng.standard_normal(case["q"].shape).astype(np.float16)
+    case["lens"] = np.array([2999, 3000, 1], np.int32)
+    q2, lens2 = _dev(case["q"]), _dev(case["lens"])
+    say("attn tables ready")
+    ready = B.attn_decode(*args, lens2, *cb, q2, workspace=ws, tables_ready=True)
+    fresh = B.attn_decode(*args, lens2, *cb, q2)
+    torch.cuda.synchronize()
+    assert torch.equal(ready, fresh)
+    _check(case, ready.cpu().numpy().astype(np.float64), what="attn tables ready")
