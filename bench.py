@@ -359,6 +359,19 @@ def attention_cpu_baseline(shape=ATTN_SHAPE, budget_s=10.0):
                        f"({t:.1f} s)")}
 
 
+def copy_reference(mib, dev):
+    """A plain device-to-device copy of mib MiB: the reference dispatch that
+    scales the FETCH_SIZE / WRITE_SIZE counters of a profiling run."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    return n * 4
+
+
 def breakdown(B, step):
     """Per-kernel event times of one extra step (every kind recorded)."""
     import torch
@@ -408,6 +421,8 @@ def main():
                                  "1 KiB per token and key/value head; peak = 256 CU x 128 "
                                  "B/clk x 2.4 GHz; the kernel is bound by LDS bank conflicts "
                                  "of the random gathers, not by HBM"}}
+        if args.copy_ref_mib > 0:
+            line["copy_ref_bytes"] = copy_reference(args.copy_ref_mib, torch.device("cuda", 0))
         if not args.no_cpu_baseline:
             line["cpu_baseline"] = attention_cpu_baseline()
         print(json.dumps(line), flush=True)
@@ -526,13 +541,7 @@ def main():
     if not args.no_extra:
         out.update(extra_paths(B, caches[0], wl, dev))
     if args.copy_ref_mib > 0:
-        n = args.copy_ref_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        out["copy_ref_bytes"] = n * 4
+        out["copy_ref_bytes"] = copy_reference(args.copy_ref_mib, dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(kv, wl, min(args.cpu_groups, wl.G))
     print(json.dumps(out), flush=True)

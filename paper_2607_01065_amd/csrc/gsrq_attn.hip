@@ -83,6 +83,7 @@ struct AttnArgs {
   const u4* tabv;           // same for values
   float* part;              // [B][Hkv][nch][GQ][AT_PART]
   int cap, W, Hkv, nch, rpc;
+  int xmap;                 // XCD-grouped block order (B * nch a multiple of 8)
   float qscale;             // softmax scale * log2(e)
 };
 
@@ -163,7 +164,25 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
   _Float16* ktab = (_Float16*)(lds + C::KTAB);
   _Float16* vtab = (_Float16*)(lds + C::VTAB);
 
-  const int chunk = blockIdx.x, hk = blockIdx.y, b = blockIdx.z;
+  // Blocks go round-robin to the 8 XCDs.  With xmap, the Hkv workgroups of
+  // one (sequence, chunk), which read the same 128-byte code rows (each its
+  // head's 16 bytes), are numbered onto one XCD, so its L2 serves the rows
+  // once instead of each XCD fetching them from HBM.
+  int chunk, hk, b;
+  {
+    const int id = blockIdx.x;
+    if (a.xmap) {
+      const int x = id & 7, slot = id >> 3;
+      const int gid = (slot / a.Hkv) * 8 + x;
+      hk = slot % a.Hkv;
+      b = gid / a.nch;
+      chunk = gid % a.nch;
+    } else {
+      chunk = id % a.nch;
+      hk = (id / a.nch) % a.Hkv;
+      b = id / (a.nch * a.Hkv);
+    }
+  }
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int tl = lane & 31, hh = lane >> 5;
   const int ul = tl / GQ, hl = tl % GQ;      // B-operand column: block variant, query head
@@ -553,6 +572,7 @@ gsrq_status attn_plan(const gsrq_attn_shape* a, AttnPlan& p) {
   r = std::max<int64_t>(1, std::min<int64_t>(r, rounds));
   p.rpc = (int)r;
   p.nch = (int)((rounds + r - 1) / r);
+  if ((int64_t)p.nch * a->Hkv * a->B > INT32_MAX) return GSRQ_E_UNSUPPORTED;
   p.off_t1 = 0;
   p.off_t2 = align256(32 * 64 * sizeof(float2));
   p.off_th = p.off_t2 + align256(32 * 64 * sizeof(float2));
@@ -573,7 +593,8 @@ template <int GQ> gsrq_status attn_launch(const AttnArgs& args, int B, int Hkv, 
     attr_set = true;
   }
   TimedLaunch tm(GSRQ_KERNEL_ATTENTION, st);
-  attn_chunk_kernel<GQ><<<dim3(args.nch, Hkv, B), AT_THREADS, AtCfg<GQ>::BYTES, st>>>(args);
+  const int blocks = args.nch * Hkv * B;
+  attn_chunk_kernel<GQ><<<blocks, AT_THREADS, AtCfg<GQ>::BYTES, st>>>(args);
   return launch_ok();
 }
 
@@ -632,6 +653,7 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   args.Hkv = a->Hkv;
   args.nch = p.nch;
   args.rpc = p.rpc;
+  args.xmap = ((int64_t)a->B * p.nch) % 8 == 0 ? 1 : 0;
   args.qscale = (float)((double)a->scale * 1.4426950408889634);
   const int ncw = a->Hkv * AT_SUB * AT_K;
   if (!(a->flags & GSRQ_ATTN_TABLES_READY)) {
