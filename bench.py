@@ -32,6 +32,8 @@ TRAFFIC = {
                              "bytes_per_launch": 116571824},
     "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "9e1c64146ab1d392",
                             "bytes_per_launch": 411513874},
+    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "7d0270831607dd87",
+                              "bytes_per_launch": 89587510},
 }
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
@@ -410,10 +412,16 @@ def main():
                 **{k: v for k, v in r.items() if k != "shape"}}
         gbps = r["algorithmic_bytes"] / (r["kernel_us"] * 1e-6) / 1e9
         lds_tbps = r["lds_bytes"] / (r["kernel_us"] * 1e-6) / 1e12
+        import hashlib
+        tr = TRAFFIC["decode_attention_1bit"]
+        src = os.path.join(ROOT, "paper_2607_01065_amd", "csrc", tr["source"])
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
         line["roofline"] = {
             "kernel": "attn_chunk_kernel (unpack + dequantise + RoPE + attention)",
             "bound": "hbm", "achieved": gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-            "frac": gbps / PEAK_HBM_GBPS, "traffic": None,
+            "frac": gbps / PEAK_HBM_GBPS,
+            "traffic": tr["bytes_per_launch"] if sha == tr["source_sha256_prefix"] else None,
+            "traffic_unit": "HBM bytes per launch",
             "bytes_per_launch": r["algorithmic_bytes"], "avg_launch_us": r["kernel_us"],
             "lds_view": {"achieved": lds_tbps, "peak": PEAK_LDS_TBPS, "unit": "TB/s",
                          "frac": lds_tbps / PEAK_LDS_TBPS, "bytes_per_launch": r["lds_bytes"],
