@@ -51,6 +51,7 @@ constexpr float AT_HEADROOM = 8.f;    // log2 margin of a raised reference maxim
 constexpr float AT_PSHIFT = 15.f;     // weights 2^(s - m + 15) <= 2^15: float16 range
 constexpr int AT_TAB = AT_SUB * AT_K * 8;   // float16 elements of one codeword table
 constexpr int AT_RED = 8 + 4 * AT_HD;       // floats per wave in the final merge
+constexpr int AT_TRIG_BLOCKS = 16;          // tables kernel: 2 x 32 x 64 angles, one per thread
 
 template <int GQ> struct AtCfg {
   static constexpr int U = 32 / GQ;                         // blocks per wave group
@@ -88,8 +89,9 @@ struct AttnArgs {
 };
 
 // Per call: cos/sin tables of the rotations a block needs (float64
-// arithmetic; blocks 0-7), and the float16 decode fp16(fp32(g * s)) of every
-// key and value codeword (the other blocks, one codeword per thread).
+// arithmetic; the first AT_TRIG_BLOCKS blocks), and the float16 decode
+// fp16(fp32(g * s)) of every key and value codeword (the other blocks, one
+// codeword per thread).
 __global__ void __launch_bounds__(256) attn_tables_kernel(double base, float2* __restrict__ t1,
                                                           float2* __restrict__ t2,
                                                           double* __restrict__ th,
@@ -99,19 +101,22 @@ __global__ void __launch_bounds__(256) attn_tables_kernel(double base, float2* _
                                                           const float* __restrict__ vs, int ncw,
                                                           u4* __restrict__ tabk,
                                                           u4* __restrict__ tabv) {
-  if (blockIdx.x < 8) {
+  if (blockIdx.x < AT_TRIG_BLOCKS) {
+    // one angle per thread: the entries of t1 (n = t), then those of t2
+    // (n = 32 t), reduced to one turn in float64 before the sine and cosine
     const int i = blockIdx.x * 256 + threadIdx.x;
-    const int t = i >> 6, j = i & 63;
+    const int e = i & 2047, t = e >> 6, j = e & 63;
     const double theta = pow(base, -2.0 * j / AT_HD);
+    const double n = i < 2048 ? (double)t : 32.0 * t;
+    double rev = n * (theta / (2.0 * M_PI));
+    rev -= floor(rev);
     double s, c;
-    sincos((double)t * theta, &s, &c);
-    t1[i] = make_float2((float)c, (float)s);
-    sincos(32.0 * t * theta, &s, &c);
-    t2[i] = make_float2((float)c, (float)s);
-    if (t == 0) th[j] = theta / (2.0 * M_PI);
+    sincos(rev * (2.0 * M_PI), &s, &c);
+    (i < 2048 ? t1 : t2)[e] = make_float2((float)c, (float)s);
+    if (i < 64) th[j] = theta / (2.0 * M_PI);
     return;
   }
-  const int cw = (blockIdx.x - 8) * 256 + threadIdx.x;
+  const int cw = (blockIdx.x - AT_TRIG_BLOCKS) * 256 + threadIdx.x;
   if (cw >= 2 * ncw) return;
   const bool val = cw >= ncw;
   const int k = val ? cw - ncw : cw;
@@ -657,7 +662,7 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   args.qscale = (float)((double)a->scale * 1.4426950408889634);
   const int ncw = a->Hkv * AT_SUB * AT_K;
   if (!(a->flags & GSRQ_ATTN_TABLES_READY)) {
-    attn_tables_kernel<<<8 + (2 * ncw + 255) / 256, 256, 0, st>>>(
+    attn_tables_kernel<<<AT_TRIG_BLOCKS + (2 * ncw + 255) / 256, 256, 0, st>>>(
         (double)a->rope_base, (float2*)(ws + p.off_t1), (float2*)(ws + p.off_t2),
         (double*)(ws + p.off_th), k_gain, k_shape, v_gain, v_shape, ncw, (u4*)(ws + p.off_tk),
         (u4*)(ws + p.off_tv));
