@@ -32,8 +32,8 @@ TRAFFIC = {
                              "bytes_per_launch": 116571824},
     "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "9e1c64146ab1d392",
                             "bytes_per_launch": 411513874},
-    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "7d0270831607dd87",
-                              "bytes_per_launch": 89587510},
+    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "581f5ff42648ad4d",
+                              "bytes_per_launch": 89589400},
 }
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
