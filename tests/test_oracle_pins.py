@@ -337,6 +337,136 @@ def test_residual_energy_falls_with_stages():
     assert errs[-1] < 0.5 * np.mean(np.sum(X * X, axis=1))
 
 
+def test_two_stage_recursion_hand_worked():
+    """GSRQ recursion (Sec. 3 residual quantisation, Sec. 5.1), worked by hand
+    with one codeword per stage (K = 1 converges in one iteration).
+
+    X = (3, 0), (0, 1), w = 1, d = D = 2.  Stage 0: y = (1, 0), (0, 1) (up to
+    the 1e-8 safeguard), so s1 = (1, 1)/sqrt2, projections 3/sqrt2 and
+    1/sqrt2, g1 = sqrt2 and the codeword is (1, 1).  The residuals
+    r = (2, -1), (-1, 0) are stage 1's training data: y = (2, -1)/sqrt5 and
+    (-1, 0), so s2 = m / ||m|| with m = (2/sqrt5 - 1, -1/sqrt5), and g2 is
+    the mean of r.s2.  A stage trained on X instead would repeat stage 0.
+    """
+    X = np.array([[3.0, 0.0], [0.0, 1.0]])
+    seeds = np.zeros((2, 1, 1), dtype=np.int64)
+    cb = O.gsrq_train(X, None, 2, 1, 2, 5, seeds)
+    r2, r5 = math.sqrt(2.0), math.sqrt(5.0)
+    assert np.allclose(cb["shapes"][0, 0, 0], [1 / r2, 1 / r2], atol=1e-8)
+    assert cb["gains"][0, 0, 0] == pytest.approx(r2, rel=1e-8)
+    m = np.array([2.0 / r5 - 1.0, -1.0 / r5])
+    s2 = m / math.hypot(m[0], m[1])
+    g2 = 0.5 * ((2.0 * s2[0] - s2[1]) + (-s2[0]))
+    assert g2 > 0.1
+    assert np.allclose(cb["shapes"][1, 0, 0], s2, atol=1e-8)
+    assert cb["gains"][1, 0, 0] == pytest.approx(g2, rel=1e-7)
+    assert list(cb["iters_run"][:, 0]) == [1, 1]
+    # the final residual is X minus both codewords
+    codes, R = O.gsrq_encode(X, cb["gains"], cb["shapes"])
+    c2 = g2 * s2
+    assert np.allclose(R, [[2.0 - c2[0], -1.0 - c2[1]], [-1.0 - c2[0], -c2[1]]], atol=1e-7)
+
+
+def _nearest_by_loops(r, gains, shapes):
+    """Nearest codeword g_k s_k to r by explicit loops over k and the
+    elements (squared distance, lowest index on ties)."""
+    best, bk = None, -1
+    for k in range(len(gains)):
+        dist = 0.0
+        for j in range(len(r)):
+            e = r[j] - gains[k] * shapes[k][j]
+            dist += e * e
+        if best is None or dist < best:
+            best, bk = dist, k
+    return bk
+
+
+def _recursion_case():
+    rng = _rng(40)
+    N, D, d, K, M, T = 40, 4, 2, 4, 3, 1
+    G = D // d
+    X = rng.standard_normal((N, D)) * np.array([2.0, 1.0, 0.7, 1.5])
+    w = rng.lognormal(0.0, 1.0, size=N)
+    seeds = np.stack([np.stack([rng.choice(N, K, replace=False) for _ in range(G)])
+                      for _ in range(M)])
+    return X, w, d, K, M, T, seeds
+
+
+def _recursion_holds(train):
+    """Whether train(X, w, d, K, M, T, seeds) gives, at every stage, the
+    codebook of weighted GSKM on the residual built by per-row
+    nearest-codeword subtraction (explicit loops) with the earlier stages'
+    final codebooks.  Also returns whether the case separates re-encoding
+    from reusing the last training assignment."""
+    X, w, d, K, M, T, seeds = _recursion_case()
+    N, D = X.shape
+    G = D // d
+    cb = train(X, w, d, K, M, T, seeds)
+    R = [list(map(float, row)) for row in X]
+    ok, reused_differs = True, False
+    for m in range(M):
+        for g in range(G):
+            Rg = np.array([row[g * d:(g + 1) * d] for row in R])
+            ref = O.gskm(Rg, w, K, T, seeds[m][g])
+            ok &= bool(np.allclose(cb["gains"][m, g], ref["gain"], rtol=1e-12, atol=1e-14))
+            ok &= bool(np.allclose(cb["shapes"][m, g], ref["shape"], rtol=1e-12, atol=1e-14))
+            for i in range(N):
+                r = R[i][g * d:(g + 1) * d]
+                k = _nearest_by_loops(r, ref["gain"], ref["shape"])
+                reused_differs |= k != ref["assign"][i]
+                for j in range(d):
+                    R[i][g * d + j] -= ref["gain"][k] * ref["shape"][k][j]
+    return ok, reused_differs
+
+
+def test_stage_recursion_trains_on_reencoded_residual():
+    """Reading of Sec. 5.1: the next stage trains on the stage input minus
+    its reconstruction with the stage's FINAL codebook (re-encoding).  With
+    T = 1 the last training assignment was made with the pre-update
+    codebook, so it differs from the re-encode for some rows (asserted)."""
+    ok, reused_differs = _recursion_holds(O.gsrq_train)
+    assert reused_differs, "case does not separate re-encoding from the last assignment"
+    assert ok
+    X, w, d, K, M, T, seeds = _recursion_case()
+    cb = O.gsrq_train(X, w, d, K, M, T, seeds)
+    codes, Rend = O.gsrq_encode(X, cb["gains"], cb["shapes"])
+    assert np.allclose(Rend + O.gsrq_decode(codes, cb["gains"], cb["shapes"]), X, atol=1e-12)
+
+
+def _train_mutant(on_input, reuse_assignment):
+    """gsrq_train with a planted mistake: every stage trained on X, or the
+    next residual taken from the last training assignment."""
+    def train(X, w, d, K, M, T, seeds):
+        X = np.asarray(X, np.float64)
+        R = X.copy()
+        G = X.shape[1] // d
+        gains, shapes = np.zeros((M, G, K)), np.zeros((M, G, K, d))
+        for m in range(M):
+            for g in range(G):
+                cols = slice(g * d, (g + 1) * d)
+                out = O.gskm((X if on_input else R)[:, cols], w, K, T, seeds[m][g])
+                gains[m, g], shapes[m, g] = out["gain"], out["shape"]
+                if reuse_assignment:
+                    k = out["assign"]
+                    R[:, cols] -= gains[m, g][k, None] * shapes[m, g][k]
+            if not reuse_assignment:
+                _, R = O.gsrq_encode(R, gains[m:m + 1], shapes[m:m + 1])
+        return dict(gains=gains, shapes=shapes)
+    return train
+
+
+@pytest.mark.parametrize("on_input,reuse", [(True, False), (False, True)])
+def test_stage_recursion_check_rejects_planted_mistakes(on_input, reuse):
+    """The recursion check fails for a stage trained on X and for a residual
+    taken from the last training assignment (both planted in a copy of the
+    recursion, on the CPU)."""
+    ok, _ = _recursion_holds(_train_mutant(on_input, reuse))
+    assert not ok
+    # the correct recursion written the same way passes
+    ok, _ = _recursion_holds(_train_mutant(False, False))
+    assert ok
+
+
 def test_rate_formula_matches_paper_configurations():
     with open(os.path.join(GOLDEN, "rate_configs.json")) as f:
         fx = json.load(f)
