@@ -8,44 +8,21 @@ decode of keys and values (g * s rounded to float32, then float16: the values
 the library declares it reads) and computes the attention in float64
 (attn_weights).
 
-Tolerance, derived from the kernel's arithmetic (every term is a bound on
-one rounding step; u = 2^-24):
-  * scores: the query, turned in float32 and scaled by scale log2(e) (a few
-    u per element), is rounded to float16 (2^-11 relative); each key pair
-    (x, y), already float16, is turned in packed float16 arithmetic with
-    float16 cosines and sines c, s: x' = fl(x c - fl(y s)), y' = fl(x s +
-    fl(y c)), each within 3 2^-11 |(x, y)| of the exact rotation (the
-    roundings of c, s, the product and the fused multiply-add), as float16
-    RoPE is.  Over the 64 pairs, by Cauchy-Schwarz, the key side adds at most
-    3 sqrt(2) 2^-11 |q| |k| and the query side 2^-11 |q| |k|: together
-    <= 6 2^-11 |q| |k|; float16 subnormals (below 2^-14) add at most 2^-25
-    per element: 2^-25 sqrt(128) (|k| + 2 |q|).  The float32 sums of the 128
-    exact products add at most 8 sqrt(129) u sum|q'_j k'_j| under the
-    probabilistic rounding model (independent roundings, 8 standard
-    deviations).  So |ds| <= eps_s = scale (6 2^-11 + (20 + 8 sqrt(129)) u)
-    |q| max_t |k_t| + 2^-25 sqrt(128) (max_t |k_t| + 2 |q|).
-  * weights: a score error eps_s moves every weight by a factor within
-    e^(+-2 eps_s); the float32 scaling, reference subtraction and exp2 add
-    8 u (|s| log2 e + 8) to the exponent; the weights enter the value
-    product rounded to float16: 2^-11 relative, and below the float16
-    normal range (2^-14) an absolute error of at most 2^-25 against a
-    largest weight of at least 2^7 (a raised reference sits 8 above the
-    block maximum, weights are 2^(s - m + 15)), so at most L 2^-32 max|v|
-    over L tokens once divided by the softmax sum.
-  * sums: the value products and the softmax denominator sum <= L float32
-    terms: 16 sqrt(L) u relative under the same probabilistic model.
-  * so |o_n - o_ref_n| <= C sum_t p_t |v_tn| + (L 2^-32 + 1e-7) max|v| (the
-    1e-7 for the float64 merges), C = expm1(2 eps_s + 8u (smax + 8)) + 2^-11
-    + 16 sqrt(L) u + 4u.
+Tolerance: tests/attn_bound.py, a statistical bound from the realised
+operands (8 standard deviations of the first-order output error under the
+probabilistic model of every rounding the kernel declares: float16 query
+per 32-token block, float16 RoPE of the keys with float16 cosines/sines,
+float16 weights in the value product, float32 sums) plus the deterministic
+subnormal and store terms.  tests/test_attn_tolerance.py shows on the CPU
+that it admits those roundings and rejects an output with a 32-token block
+left out or with the key positions shifted by one.
 The test also reports the worst observed error relative to that bound.
 """
-import math
-
 import numpy as np
 import pytest
 
 import synth
-from oracle import gsrq_oracle as O
+from tests import attn_bound as AB
 from tests.gpu_util import say
 
 torch = pytest.importorskip("torch")
@@ -53,7 +30,6 @@ pytestmark = pytest.mark.gpu
 
 from paper_2607_01065_amd import gsrq as B  # noqa: E402
 
-U = 2.0 ** -24
 BASE = 500000.0
 
 
@@ -78,45 +54,9 @@ def _run(case, base=BASE):
     return out.cpu().numpy().astype(np.float64)
 
 
-def _decode_rows(codes_rows, gain, shape):
-    """Decoded rows in float32 arithmetic: (float32 g * s) per codeword,
-    from the oracle's own unpacking."""
-    G = gain.shape[1]
-    idx = O.unpack_codes(codes_rows, 1, G, gain.shape[2])[:, 0, :]        # [L, G]
-    cw = gain[0][np.arange(G)[None, :], idx][..., None] * shape[0][np.arange(G)[None, :], idx]
-    return cw.astype(np.float32).reshape(codes_rows.shape[0], -1)          # [L, D] float32
-
-
 def _reference(case, b, heads=None, base=BASE):
     """Oracle output [Hq, 128] and per-element tolerance for sequence b."""
-    Hkv, GQ = case["Hkv"], case["GQ"]
-    Hq, hd = Hkv * GQ, 128
-    cap = case["k_codes"].shape[1]
-    L = int(min(max(int(case["lens"][b]), 0), cap))
-    q = case["q"][b].astype(np.float64)
-    ref = np.zeros((Hq, hd))
-    tol = np.zeros((Hq, hd))
-    if L == 0:
-        return ref, tol + 1e-30
-    k16 = _decode_rows(case["k_codes"][b, :L], case["k_gain"], case["k_shape"])
-    k16 = k16.astype(np.float16).astype(np.float64).reshape(L, Hkv, hd)
-    v16 = _decode_rows(case["v_codes"][b, :L], case["v_gain"], case["v_shape"])
-    v16 = v16.astype(np.float16).astype(np.float64).reshape(L, Hkv, hd)
-    p, s = O.attn_weights(q, k16, base)
-    scale = 1.0 / math.sqrt(hd)
-    for h in range(Hq) if heads is None else heads:
-        kv = h // GQ
-        ref[h] = p[h] @ v16[:, kv]
-        kmax = float(np.max(np.linalg.norm(k16[:, kv], axis=1)))
-        qn = float(np.linalg.norm(q[h]))
-        eps_s = (scale * (6 * 2.0 ** -11 + (20 + 8 * math.sqrt(129)) * U) * qn * kmax
-                 + 2.0 ** -25 * math.sqrt(128) * (kmax + 2 * qn))
-        smax = float(np.max(np.abs(s[h]))) * math.log2(math.e)
-        C = (math.expm1(2 * eps_s + 8 * U * (smax + 8)) + 2.0 ** -11 + 16 * math.sqrt(L) * U
-             + 4 * U)
-        tol[h] = (C * (p[h] @ np.abs(v16[:, kv]))
-                  + (L * 2.0 ** -32 + 1e-7) * float(np.max(np.abs(v16[:, kv]))))
-    return ref, tol
+    return AB.reference(case, b, heads, base)
 
 
 def _check(case, out, heads=None, what=""):
