@@ -85,7 +85,17 @@ enum {
    * its members for clusters with weight (others keep c_k); obj_trace entry
    * t-1 is the weighted distortion AFTER that update.  GSRQ_RESUME,
    * GSRQ_ASSIGN_IN and the stop rule act as for GSKM. */
-  GSRQ_KMEANS = 8u
+  GSRQ_KMEANS = 8u,
+  /* Check the inputs on the device before any other work and return
+   * GSRQ_E_ARG, with no output touched, when a weight is negative or not
+   * finite, an element of X is not finite, or (GSKM seeding: without
+   * GSRQ_RESUME and GSRQ_KMEANS) a seed row's subvector is zero, which has
+   * no direction to start a shape from (Alg. 1 draws the initial shapes on
+   * the unit sphere).  The check reads X once and the call then waits for
+   * the stream (it is synchronous, unlike the unchecked call).  Without the
+   * flag these inputs are the caller's to avoid: a zero seed subvector gives
+   * a zero initial shape. */
+  GSRQ_CHECK_INPUTS = 16u
 };
 
 /* Human-readable name of a status code (static string). */
@@ -124,7 +134,8 @@ gsrq_status gsrq_encode_workspace_bytes(const gsrq_shape* s, size_t* bytes);
  *                    which must be a nonzero subvector.  Indices must lie in
  *                    [0, N) and be distinct within a subspace; N >= K.
  *  flags             GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP |
- *                    GSRQ_KMEANS (the K-means baseline, see the flag).
+ *                    GSRQ_KMEANS (the K-means baseline, see the flag) |
+ *                    GSRQ_CHECK_INPUTS (device check of w, X and the seeds).
  *  gain, shape       [G][K], [G][K][d] float32 outputs (inputs on resume).
  *  R_next            [N][D] float32 residual X - c(encode(X)) with the final
  *                    codebook, or NULL.
@@ -233,8 +244,12 @@ typedef struct {
  * gsrq_attn_decode with the same workspace, codebooks (contents unchanged),
  * Hkv, head_dim and rope_base, so this call does not rebuild them (a
  * layer's codebooks are fixed across decoding steps).  Other arguments may
- * differ.  Not checked: a workspace without those tables gives wrong
- * outputs. */
+ * differ.  Checked on the device: the table build records the codebook
+ * pointers, Hkv, head_dim and rope_base in a tag at the start of the
+ * workspace, and a call whose arguments do not match the tag (a workspace
+ * without tables, or tables of other codebook arrays or settings) writes
+ * NaN to every output element.  Not checked: the codebook CONTENTS, which
+ * the caller must not change while reusing the tables. */
 enum { GSRQ_ATTN_TABLES_READY = 1 };
 
 /* Workspace bytes gsrq_attn_decode needs for shape a. */

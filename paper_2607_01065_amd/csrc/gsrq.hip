@@ -1248,6 +1248,49 @@ __global__ void __launch_bounds__(DEC_THREADS) decode_lds_kernel(DecodeArgs a) {
   }
 }
 
+// Input check of gsrq_train_stage (flag GSRQ_CHECK_INPUTS).  Bits of *bad:
+// 1 a weight that is negative or not finite, 2 an element of X that is not
+// finite, 4 a seed row whose subvector is zero (GSKM seeding needs a
+// direction: Alg. 1 starts from shapes on the unit sphere).  Every block
+// walks rows; the threads of a block stride over the row's D elements.
+constexpr uint32_t CHK_WEIGHT = 1u, CHK_NONFINITE = 2u, CHK_ZERO_SEED = 4u;
+
+__device__ __forceinline__ bool finite_bits(float v) {
+  return (__float_as_uint(v) & 0x7f800000u) != 0x7f800000u;
+}
+__device__ __forceinline__ bool finite_bits(_Float16 v) {
+  return (__builtin_bit_cast(uint16_t, v) & 0x7c00u) != 0x7c00u;
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256) check_inputs_kernel(const T* __restrict__ X, int64_t ldx,
+                                                           int64_t N, int D, int d,
+                                                           const float* __restrict__ w,
+                                                           const int32_t* __restrict__ seeds,
+                                                           int nseeds, int K,
+                                                           uint32_t* __restrict__ bad) {
+  uint32_t flags = 0;
+  for (int64_t r = blockIdx.x; r < N; r += gridDim.x) {
+    const T* row = X + r * ldx;
+    for (int c = threadIdx.x; c < D; c += blockDim.x)
+      if (!finite_bits(row[c])) flags |= CHK_NONFINITE;
+    if (threadIdx.x == 0 && w) {
+      const float v = w[r];
+      if (!finite_bits(v) || v < 0.f) flags |= CHK_WEIGHT;
+    }
+  }
+  // seed subvectors: entry e = g K + k names row seeds[e] of subspace g
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < nseeds;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int g = (int)(e / K);
+    const T* sub = X + (int64_t)seeds[e] * ldx + (int64_t)g * d;
+    bool zero = true;
+    for (int j = 0; j < d; ++j) zero &= (float)sub[j] == 0.f;
+    if (zero) flags |= CHK_ZERO_SEED;
+  }
+  if (flags) atomicOr(bad, flags);
+}
+
 // ------------------------------------------------------------- host side
 
 // Optional launch timing (off by default): HIP events bracket every launch
@@ -1543,7 +1586,8 @@ gsrq_status gsrq_train_stage(const gsrq_shape* s, const void* X, gsrq_dtype x_dt
   if (x_dtype != GSRQ_F32 && x_dtype != GSRQ_F16) return GSRQ_E_ARG;
   if (ldx < s->D || T < 0 || s->N < s->K) return GSRQ_E_ARG;
   if (T == 0 && (flags & GSRQ_RESUME)) return GSRQ_E_ARG;
-  if (flags & ~(uint32_t)(GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP | GSRQ_KMEANS))
+  if (flags & ~(uint32_t)(GSRQ_RESUME | GSRQ_ASSIGN_IN | GSRQ_NO_EARLY_STOP | GSRQ_KMEANS |
+                          GSRQ_CHECK_INPUTS))
     return GSRQ_E_ARG;
   if ((flags & GSRQ_ASSIGN_IN) && (!(flags & GSRQ_RESUME) || !assign_io)) return GSRQ_E_ARG;
   if (((uintptr_t)workspace & 255) != 0) return GSRQ_E_ARG;
@@ -1569,6 +1613,34 @@ gsrq_status gsrq_train_stage(const gsrq_shape* s, const void* X, gsrq_dtype x_dt
   const size_t need = narrow(s) ? train_layout(s, elt).total
                                 : gsrq_wide::train_workspace_bytes(s, elt);
   if (ws_bytes < need) return GSRQ_E_WORKSPACE;
+  if (flags & GSRQ_CHECK_INPUTS) {
+    // the check runs before anything else and uses the start of the
+    // workspace (a status word, then a device copy of the seed table); the
+    // call waits for it, and on a failed check returns with no output touched
+    const bool seeded = !(flags & GSRQ_RESUME) && !(flags & GSRQ_KMEANS);
+    const size_t nseeds = seeded ? (size_t)G * s->K : 0;
+    if (need < 256 + nseeds * sizeof(int32_t)) return GSRQ_E_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    uint32_t* bad = (uint32_t*)workspace;
+    int32_t* dseeds = (int32_t*)((char*)workspace + 256);
+    if ((e = fill_u32(bad, 1, 0u, st))) return e;
+    if (nseeds && hipMemcpyAsync(dseeds, seed_rows, nseeds * sizeof(int32_t),
+                                 hipMemcpyHostToDevice, st) != hipSuccess)
+      return GSRQ_E_HIP;
+    const int grid = (int)std::min<int64_t>(s->N, 2048);
+    if (x_dtype == GSRQ_F16)
+      check_inputs_kernel<_Float16><<<grid, 256, 0, st>>>((const _Float16*)X, ldx, s->N, s->D,
+                                                          s->d, w, dseeds, (int)nseeds, s->K, bad);
+    else
+      check_inputs_kernel<float><<<grid, 256, 0, st>>>((const float*)X, ldx, s->N, s->D, s->d,
+                                                       w, dseeds, (int)nseeds, s->K, bad);
+    if ((e = launch_ok())) return e;
+    uint32_t hbad = 0;
+    if (hipMemcpyAsync(&hbad, bad, sizeof(hbad), hipMemcpyDeviceToHost, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess)
+      return GSRQ_E_HIP;
+    if (hbad) return GSRQ_E_ARG;
+  }
   if (!narrow(s))
     return gsrq_wide::train_stage(s, X, x_dtype, ldx, w, T, seed_rows, flags, gain, shape,
                                   R_next, assign_io, iters_run, obj_trace, workspace, stream);

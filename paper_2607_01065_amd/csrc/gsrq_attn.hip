@@ -88,6 +88,17 @@ struct AttnArgs {
   float qscale;             // softmax scale * log2(e)
 };
 
+// Tag of the tables in a workspace: written by the tables kernel, compared
+// by the merge kernel with what the call expects, so that a call that skips
+// the table build (GSRQ_ATTN_TABLES_READY) on a workspace that holds no
+// tables, or tables of other codebook arrays, head count or RoPE base,
+// returns NaN outputs instead of plausible wrong ones.
+constexpr uint32_t AT_TAG_MAGIC = 0x47535251u;
+constexpr int AT_TAG_WORDS = 16;
+struct AttnTag {
+  uint32_t w[AT_TAG_WORDS];
+};
+
 // Per call: cos/sin tables of the rotations a block needs (float64
 // arithmetic; the first AT_TRIG_BLOCKS blocks), and the float16 decode
 // fp16(fp32(g * s)) of every key and value codeword (the other blocks, one
@@ -100,7 +111,9 @@ __global__ void __launch_bounds__(256) attn_tables_kernel(double base, float2* _
                                                           const float* __restrict__ vg,
                                                           const float* __restrict__ vs, int ncw,
                                                           u4* __restrict__ tabk,
-                                                          u4* __restrict__ tabv) {
+                                                          u4* __restrict__ tabv, AttnTag tag,
+                                                          uint32_t* __restrict__ tagp) {
+  if (blockIdx.x == 0 && threadIdx.x < AT_TAG_WORDS) tagp[threadIdx.x] = tag.w[threadIdx.x];
   if (blockIdx.x < AT_TRIG_BLOCKS) {
     // one angle per thread: the entries of t1 (n = t), then those of t2
     // (n = 32 t), reduced to one turn in float64 before the sine and cosine
@@ -530,8 +543,16 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_chunk_kernel(AttnArgs a) {
 // flight together.
 __global__ void __launch_bounds__(AT_HD) attn_merge_kernel(const float* __restrict__ part, int Hq,
                                                           int Hkv, int nch,
-                                                          float* __restrict__ out) {
+                                                          float* __restrict__ out, AttnTag tag,
+                                                          const uint32_t* __restrict__ tagp) {
   const int bq = blockIdx.x, b = bq / Hq, hq = bq % Hq;
+  bool tag_ok = true;
+#pragma unroll
+  for (int i = 0; i < AT_TAG_WORDS; ++i) tag_ok &= tagp[i] == tag.w[i];
+  if (!tag_ok) {
+    out[(size_t)bq * AT_HD + threadIdx.x] = __builtin_nanf("");
+    return;
+  }
   const int GQ = Hq / Hkv, hk = hq / GQ, h = hq % GQ, n = threadIdx.x;
   const float* p = part + (((size_t)b * Hkv + hk) * nch * GQ + h) * AT_PART;
   const size_t cs = (size_t)GQ * AT_PART;
@@ -554,7 +575,7 @@ __global__ void __launch_bounds__(AT_HD) attn_merge_kernel(const float* __restri
 
 struct AttnPlan {
   int GQ, rpc, nch;
-  size_t off_t1, off_t2, off_th, off_tk, off_tv, off_part, bytes;
+  size_t off_tag, off_t1, off_t2, off_th, off_tk, off_tv, off_part, bytes;
 };
 
 int at_round(int GQ) { return AT_WAVES * (32 / GQ) * AT_BLK; }
@@ -578,8 +599,9 @@ gsrq_status attn_plan(const gsrq_attn_shape* a, AttnPlan& p) {
   p.rpc = (int)r;
   p.nch = (int)((rounds + r - 1) / r);
   if ((int64_t)p.nch * a->Hkv * a->B > INT32_MAX) return GSRQ_E_UNSUPPORTED;
-  p.off_t1 = 0;
-  p.off_t2 = align256(32 * 64 * sizeof(float2));
+  p.off_tag = 0;
+  p.off_t1 = 256;
+  p.off_t2 = p.off_t1 + align256(32 * 64 * sizeof(float2));
   p.off_th = p.off_t2 + align256(32 * 64 * sizeof(float2));
   p.off_tk = p.off_th + align256(64 * sizeof(double));
   p.off_tv = p.off_tk + align256((size_t)a->Hkv * AT_SUB * AT_K * 16);
@@ -661,11 +683,26 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   args.xmap = ((int64_t)a->B * p.nch) % 8 == 0 ? 1 : 0;
   args.qscale = (float)((double)a->scale * 1.4426950408889634);
   const int ncw = a->Hkv * AT_SUB * AT_K;
+  AttnTag tag = {};
+  {
+    const void* ptrs[4] = {k_gain, k_shape, v_gain, v_shape};
+    tag.w[0] = AT_TAG_MAGIC;
+    tag.w[1] = (uint32_t)a->Hkv;
+    tag.w[2] = (uint32_t)a->head_dim;
+    memcpy(&tag.w[3], &a->rope_base, sizeof(float));
+    for (int i = 0; i < 4; ++i) {
+      const uint64_t v = (uint64_t)(uintptr_t)ptrs[i];
+      tag.w[4 + 2 * i] = (uint32_t)v;
+      tag.w[5 + 2 * i] = (uint32_t)(v >> 32);
+    }
+    tag.w[12] = ~AT_TAG_MAGIC;
+  }
+  uint32_t* tagp = (uint32_t*)(ws + p.off_tag);
   if (!(a->flags & GSRQ_ATTN_TABLES_READY)) {
     attn_tables_kernel<<<AT_TRIG_BLOCKS + (2 * ncw + 255) / 256, 256, 0, st>>>(
         (double)a->rope_base, (float2*)(ws + p.off_t1), (float2*)(ws + p.off_t2),
         (double*)(ws + p.off_th), k_gain, k_shape, v_gain, v_shape, ncw, (u4*)(ws + p.off_tk),
-        (u4*)(ws + p.off_tv));
+        (u4*)(ws + p.off_tv), tag, tagp);
     e = launch_ok();
     if (e) return e;
   }
@@ -673,7 +710,8 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   else if (p.GQ == 2) e = attn_launch<2>(args, a->B, a->Hkv, st);
   else e = attn_launch<4>(args, a->B, a->Hkv, st);
   if (e) return e;
-  attn_merge_kernel<<<a->B * a->Hq, AT_HD, 0, st>>>(args.part, a->Hq, a->Hkv, p.nch, out);
+  attn_merge_kernel<<<a->B * a->Hq, AT_HD, 0, st>>>(args.part, a->Hq, a->Hkv, p.nch, out, tag,
+                                                     tagp);
   return launch_ok();
 }
 

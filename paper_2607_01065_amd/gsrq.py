@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libgsrq.so")
 
 GSRQ_OK, GSRQ_E_ARG, GSRQ_E_UNSUPPORTED, GSRQ_E_WORKSPACE, GSRQ_E_HIP = range(5)
 GSRQ_F32, GSRQ_F16 = 0, 1
-GSRQ_RESUME, GSRQ_ASSIGN_IN, GSRQ_NO_EARLY_STOP, GSRQ_KMEANS = 1, 2, 4, 8
+GSRQ_RESUME, GSRQ_ASSIGN_IN, GSRQ_NO_EARLY_STOP, GSRQ_KMEANS, GSRQ_CHECK_INPUTS = 1, 2, 4, 8, 16
 
 
 class GsrqError(RuntimeError):
@@ -188,6 +188,21 @@ def _rows(X):
     return X.shape[0], X.shape[1], X.stride(0)
 
 
+def _need(t, name, dtypes, device, shape=None):
+    """Check a tensor argument passed as a dense pointer: dtype, device,
+    contiguity and (optionally) shape; None passes."""
+    if t is None:
+        return
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} must be {' or '.join(str(d) for d in dtypes)}, not {t.dtype}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if shape is not None and t.numel() != int(np.prod(shape)):
+        raise ValueError(f"{name} has {t.numel()} elements, expected {tuple(shape)}")
+
+
 def _workspace(nbytes, device, workspace):
     torch = _torch()
     if workspace is not None:
@@ -211,17 +226,26 @@ class TrainResult:
 
 def train_stage(X, d, K, T, seed_rows=None, w=None, *, gain=None, shape=None, assign=None,
                 resume=False, assign_in=False, no_early_stop=False, residual=False,
-                trace=True, kmeans=False, workspace=None, stream=None) -> TrainResult:
+                trace=True, kmeans=False, check_inputs=False, workspace=None,
+                stream=None) -> TrainResult:
     """One stage of weighted GSKM on device tensor X [N, D] (see gsrq_train_stage).
 
     residual: True for a new R_next tensor, or an [N, D] float32 tensor to
     write it into.  kmeans: the K-means baseline (GSRQ_KMEANS) instead of
-    GSKM; its centroids are gain[:, :, None] * shape."""
+    GSKM; its centroids are gain[:, :, None] * shape.  check_inputs: the
+    device check of GSRQ_CHECK_INPUTS (weights, finite X, nonzero seeds;
+    the call then waits for the stream)."""
     torch = _torch()
     lib = load_library()
     N, D, ldx = _rows(X)
     G = D // d if d > 0 and D % d == 0 else 0
     dev = X.device
+    _need(w, "w", (torch.float32,), dev, (N,))
+    _need(gain, "gain", (torch.float32,), dev, (G, K))
+    _need(shape, "shape", (torch.float32,), dev, (G, K, d))
+    _need(assign, "assign", (torch.int16, torch.uint16), dev, (G, N))
+    if residual is not True and residual is not False and residual is not None:
+        _need(residual, "residual", (torch.float32,), dev, (N, D))
     if gain is None:
         gain = torch.empty((max(G, 1), K), dtype=torch.float32, device=dev)
     if shape is None:
@@ -238,7 +262,8 @@ def train_stage(X, d, K, T, seed_rows=None, w=None, *, gain=None, shape=None, as
     if seed_rows is not None:
         seeds = np.ascontiguousarray(np.asarray(seed_rows), dtype=np.int32)
     flags = ((GSRQ_RESUME if resume else 0) | (GSRQ_ASSIGN_IN if assign_in else 0)
-             | (GSRQ_NO_EARLY_STOP if no_early_stop else 0) | (GSRQ_KMEANS if kmeans else 0))
+             | (GSRQ_NO_EARLY_STOP if no_early_stop else 0) | (GSRQ_KMEANS if kmeans else 0)
+             | (GSRQ_CHECK_INPUTS if check_inputs else 0))
     sh = make_shape(N, D, d, K, 1)
     n = ctypes.c_size_t(0)
     st = lib.gsrq_train_workspace_bytes(ctypes.byref(sh), ctypes.byref(n))
@@ -262,8 +287,11 @@ def encode(X, gain, shape, *, codes=None, residual=False, workspace=None, stream
     N, D, ldx = _rows(X)
     M, G, K = gain.shape
     d = shape.shape[-1]
+    _need(gain, "gain", (torch.float32,), X.device)
+    _need(shape, "shape", (torch.float32,), X.device, (M, G, K, d))
     sh = make_shape(N, D, d, K, M)
     W = int(lib.gsrq_code_words(ctypes.byref(sh)))
+    _need(codes, "codes", (torch.int32, torch.uint32), X.device, (N, max(W, 1)))
     if codes is None:
         codes = torch.empty((N, max(W, 1)), dtype=torch.int32, device=X.device)
     res = torch.empty((N, D), dtype=torch.float32, device=X.device) if residual else None
@@ -287,8 +315,14 @@ def decode(codes, gain, shape, D, M_use=None, *, out_dtype=None, out=None, strea
     d = shape.shape[-1]
     N = codes.shape[0]
     M_use = M if M_use is None else int(M_use)
+    dev = codes.device
+    _need(codes, "codes", (torch.int32, torch.uint32), dev)
+    _need(gain, "gain", (torch.float32,), dev)
+    _need(shape, "shape", (torch.float32,), dev, (M, G, K, d))
     if out is None:
-        out = torch.empty((N, D), dtype=out_dtype or torch.float16, device=codes.device)
+        out = torch.empty((N, D), dtype=out_dtype or torch.float16, device=dev)
+    elif out.dim() != 2 or out.stride(1) != 1 or out.device != dev or tuple(out.shape) != (N, D):
+        raise ValueError("out must be an [N, D] tensor with unit column stride on the codes' device")
     sh = make_shape(N, D, d, K, M)
     st = lib.gsrq_decode(ctypes.byref(sh), _ptr(codes), M_use, _ptr(gain), _ptr(shape),
                          _ptr(out), _dtype_code(out), out.stride(0), _stream_handle(stream))

@@ -103,7 +103,10 @@ def test_train_stage_validation_before_any_hip_call():
     assert _train(lib, sh, seeds=None) == B.GSRQ_E_ARG                    # seeds needed
     assert _train(lib, sh, seeds=sp, dt=7) == B.GSRQ_E_ARG                # dtype
     assert _train(lib, sh, seeds=sp, flags=64) == B.GSRQ_E_ARG            # unknown flag
-    assert _train(lib, sh, seeds=sp, flags=16) == B.GSRQ_E_ARG            # unknown flag
+    assert _train(lib, sh, seeds=sp, flags=32) == B.GSRQ_E_ARG            # unknown flag
+    # the input-check flag runs its device check only after host validation
+    assert _train(lib, sh, seeds=sp, flags=16, ldx=15) == B.GSRQ_E_ARG
+    assert _train(lib, sh, seeds=sp, flags=16, nws=10) == B.GSRQ_E_WORKSPACE
     assert _train(lib, sh, seeds=sp, flags=8 | 2) == B.GSRQ_E_ARG         # K-means, ASSIGN_IN alone
     assert _train(lib, sh, seeds=sp, flags=2) == B.GSRQ_E_ARG             # ASSIGN_IN w/o RESUME
     assert _train(lib, sh, seeds=sp, flags=3) == B.GSRQ_E_ARG             # ... and w/o assign
