@@ -70,7 +70,7 @@ def decode_rows(codes_rows, gain, shape):
     G = gain.shape[1]
     idx = O.unpack_codes(codes_rows, 1, G, gain.shape[2])[:, 0, :]
     cw = gain[0][np.arange(G)[None, :], idx][..., None] * shape[0][np.arange(G)[None, :], idx]
-    return cw.astype(np.float32).reshape(codes_rows.shape[0], -1)
+    return cw.astype(np.float32).reshape(codes_rows.shape[0], G * shape.shape[-1])
 
 
 def case_sequence(case, b):
