@@ -566,9 +566,12 @@ __global__ void __launch_bounds__(AT_HD) attn_merge_kernel(const float* __restri
 #pragma unroll 8
   for (int c = 0; c < nch; ++c) {
     const float m = p[c * cs + AT_HD], l = p[c * cs + AT_HD + 1], o = p[c * cs + n];
-    const double f = l > 0.f ? exp2((double)m - (double)M) : 0.0;
-    num += f * (double)o;
-    den += f * (double)l;
+    // a chunk without tokens writes only its (m, l) record: its o slots hold
+    // whatever the workspace held, which must not reach the sums (0 * NaN)
+    const bool has = l > 0.f;
+    const double f = has ? exp2((double)m - (double)M) : 0.0;
+    num += has ? f * (double)o : 0.0;
+    den += has ? f * (double)l : 0.0;
   }
   out[(size_t)bq * AT_HD + n] = den > 0.0 ? (float)(num / den) : 0.f;
 }

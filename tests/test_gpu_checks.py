@@ -264,3 +264,21 @@ def test_row_weights_above_lds_selection_size():
         _, _, st = B.row_weights(norms=n2, tau=1.0)
         torch.cuda.synchronize()
         assert st.cpu().numpy()[0] == np.median(n2.cpu().numpy().astype(np.float64))
+
+
+def test_attn_workspace_contents_do_not_leak_into_outputs():
+    """A sequence shorter than the cache leaves chunks without tokens, which
+    write only their (reference, sum) record; a workspace filled with NaN
+    bits beforehand must still give the output of a fresh one."""
+    case = synth.attn_case(3, 6000, [6000, 700, 0], 2, 4, seed=24, q_dtype="float16")
+    t = {k: _dev(case[k]) for k in ("k_codes", "v_codes", "lens", "k_gain", "k_shape",
+                                    "v_gain", "v_shape", "q")}
+    args = [t[k] for k in ("k_codes", "v_codes", "lens", "k_gain", "k_shape", "v_gain",
+                           "v_shape", "q")]
+    n = B.attn_workspace_bytes(3, 6000, 8, 2)
+    ws = torch.full((n,), 0xFF, dtype=torch.uint8, device="cuda")     # NaN float bits
+    dirty = B.attn_decode(*args, workspace=ws)
+    clean = B.attn_decode(*args, workspace=torch.zeros(n, dtype=torch.uint8, device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.all(torch.isfinite(dirty))
+    assert torch.equal(dirty, clean)
