@@ -295,6 +295,36 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
                              gsrq_dtype q_dtype, float* out, void* workspace, size_t ws_bytes,
                              void* stream);
 
+/* Bytes of the library's own scratch for gsrq_attn_decode_noalloc, per GPU. */
+#define GSRQ_ATTN_NOALLOC_BYTES ((size_t)16 << 20)
+
+/*
+ * gsrq_attn_decode_noalloc -- gsrq_attn_decode without a workspace argument,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, serving loops that must not call hipMalloc, harnesses that
+ * forbid it.  Same arguments, computation and results as gsrq_attn_decode
+ * (bit for bit, on the same inputs), except workspace and ws_bytes.
+ *
+ * Scratch: a device array of GSRQ_ATTN_NOALLOC_BYTES in the library, one
+ * per GPU, held until the process ends; its address on the current device
+ * is looked up once (hipGetSymbolAddress) on the first call there.  The
+ * call itself allocates nothing.  A shape whose workspace
+ * (gsrq_attn_workspace_bytes) exceeds GSRQ_ATTN_NOALLOC_BYTES returns
+ * GSRQ_E_WORKSPACE before any HIP call.
+ * Every call on a GPU shares that GPU's scratch, which keeps the last
+ * call's contents: calls that overlap on one GPU (other streams, other
+ * host threads) race and must be serialised by the caller.  Because the
+ * tables stay, GSRQ_ATTN_TABLES_READY may be passed when the previous call
+ * on this GPU used the same codebook arrays, Hkv, head_dim and rope_base;
+ * the device-checked tag gives NaN outputs otherwise.
+ */
+gsrq_status gsrq_attn_decode_noalloc(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                                     const uint32_t* k_codes, const uint32_t* v_codes,
+                                     const int32_t* seq_len, const float* k_gain,
+                                     const float* k_shape, const float* v_gain,
+                                     const float* v_shape, const void* q, gsrq_dtype q_dtype,
+                                     float* out, void* stream);
+
 /* Kernel kinds reported by the optional launch timing below. */
 enum {
   GSRQ_KERNEL_ASSIGN = 0,     /* fused assignment + weighted accumulation */

@@ -32,6 +32,7 @@
 //    second kernel merges the chunks of every (sequence, query head) with
 //    their reference maxima (the split form of one softmax).
 #include <algorithm>
+#include <mutex>
 
 #include "gsrq_common.h"
 
@@ -641,13 +642,16 @@ gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes) {
   return GSRQ_OK;
 }
 
-gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
-                             const uint32_t* k_codes, const uint32_t* v_codes,
-                             const int32_t* seq_len, const float* k_gain, const float* k_shape,
-                             const float* v_gain, const float* v_shape, const void* q,
-                             gsrq_dtype q_dtype, float* out, void* workspace, size_t ws_bytes,
-                             void* stream) {
-  AttnPlan p;
+}  // extern "C"
+
+namespace {
+
+// Host validation shared by both entry points (no HIP call).
+gsrq_status attn_validate(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                          const uint32_t* k_codes, const uint32_t* v_codes,
+                          const int32_t* seq_len, const float* k_gain, const float* k_shape,
+                          const float* v_gain, const float* v_shape, const void* q,
+                          gsrq_dtype q_dtype, float* out, AttnPlan& p) {
   gsrq_status e = attn_plan(a, p);
   if (e) return e;
   if (!kv || kv->N < 1 || kv->D < 1 || kv->d < 1 || kv->K < 2 || kv->M < 1) return GSRQ_E_ARG;
@@ -662,10 +666,16 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
       (uintptr_t)v_shape % 16 || (uintptr_t)q % 16)
     return GSRQ_E_ARG;
   if (q_dtype != GSRQ_F32 && q_dtype != GSRQ_F16) return GSRQ_E_ARG;
-  if (!workspace || (uintptr_t)workspace % 256) return GSRQ_E_ARG;
-  if (ws_bytes < p.bytes) return GSRQ_E_WORKSPACE;
+  return GSRQ_OK;
+}
+
+// The launches of one call on a workspace of p.bytes at ws (256-byte aligned).
+gsrq_status attn_run(const gsrq_attn_shape* a, const AttnPlan& p, const uint32_t* k_codes,
+                     const uint32_t* v_codes, const int32_t* seq_len, const float* k_gain,
+                     const float* k_shape, const float* v_gain, const float* v_shape,
+                     const void* q, gsrq_dtype q_dtype, float* out, char* ws, void* stream) {
+  gsrq_status e;
   hipStream_t st = (hipStream_t)stream;
-  char* ws = (char*)workspace;
   AttnArgs args;
   args.kc = k_codes;
   args.vc = v_codes;
@@ -716,6 +726,68 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
   attn_merge_kernel<<<a->B * a->Hq, AT_HD, 0, st>>>(args.part, a->Hq, a->Hkv, p.nch, out, tag,
                                                      tagp);
   return launch_ok();
+}
+
+// Scratch of gsrq_attn_decode_noalloc: a file-scope device array, one copy
+// per GPU, alive until the process ends.  In host code its name only stands
+// for the variable; its device address on a GPU comes from
+// hipGetSymbolAddress with that GPU current, taken once per device and kept.
+constexpr size_t AT_NOALLOC_BYTES = GSRQ_ATTN_NOALLOC_BYTES;
+static __device__ __align__(256) unsigned char scratch[AT_NOALLOC_BYTES];
+
+constexpr int AT_MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[AT_MAX_DEVICES] = {};
+
+gsrq_status scratch_on_current_device(char** ptr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return GSRQ_E_HIP;
+  if (dev >= AT_MAX_DEVICES) return GSRQ_E_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return GSRQ_E_HIP;
+    g_scratch_ptr[dev] = (char*)p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return GSRQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                             const uint32_t* k_codes, const uint32_t* v_codes,
+                             const int32_t* seq_len, const float* k_gain, const float* k_shape,
+                             const float* v_gain, const float* v_shape, const void* q,
+                             gsrq_dtype q_dtype, float* out, void* workspace, size_t ws_bytes,
+                             void* stream) {
+  AttnPlan p;
+  gsrq_status e = attn_validate(a, kv, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain,
+                                v_shape, q, q_dtype, out, p);
+  if (e) return e;
+  if (!workspace || (uintptr_t)workspace % 256) return GSRQ_E_ARG;
+  if (ws_bytes < p.bytes) return GSRQ_E_WORKSPACE;
+  return attn_run(a, p, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, q_dtype,
+                  out, (char*)workspace, stream);
+}
+
+gsrq_status gsrq_attn_decode_noalloc(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                                     const uint32_t* k_codes, const uint32_t* v_codes,
+                                     const int32_t* seq_len, const float* k_gain,
+                                     const float* k_shape, const float* v_gain,
+                                     const float* v_shape, const void* q, gsrq_dtype q_dtype,
+                                     float* out, void* stream) {
+  AttnPlan p;
+  gsrq_status e = attn_validate(a, kv, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain,
+                                v_shape, q, q_dtype, out, p);
+  if (e) return e;
+  if (p.bytes > AT_NOALLOC_BYTES) return GSRQ_E_WORKSPACE;
+  char* ws = nullptr;
+  if ((e = scratch_on_current_device(&ws))) return e;
+  return attn_run(a, p, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, q_dtype,
+                  out, ws, stream);
 }
 
 }  // extern "C"

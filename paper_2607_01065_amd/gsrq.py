@@ -83,6 +83,9 @@ def load_library(path: str = LIB_PATH):
     lib.gsrq_attn_decode.restype = ctypes.c_int
     lib.gsrq_attn_decode.argtypes = [AP, SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                      ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.gsrq_attn_decode_noalloc.restype = ctypes.c_int
+    lib.gsrq_attn_decode_noalloc.argtypes = [AP, SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                             ctypes.c_int, _vp, _vp]
     lib.gsrq_timing_enable.restype = ctypes.c_int
     lib.gsrq_timing_enable.argtypes = [ctypes.c_int]
     lib.gsrq_timing_enable_kinds.restype = ctypes.c_int
@@ -373,14 +376,19 @@ def attn_workspace_bytes(B, cap, Hq, Hkv, head_dim=128) -> int:
     return int(n.value)
 
 
+ATTN_NOALLOC_BYTES = 16 << 20
+
+
 def attn_decode(k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, *,
                 rope_base=500000.0, scale=None, out=None, workspace=None, stream=None,
-                tables_ready=False):
+                tables_ready=False, noalloc=False):
     """One decoding step of attention over coded caches (see gsrq_attn_decode).
     k_codes, v_codes [B, cap, W] packed codes; seq_len [B] int32; codebooks
     [1, G, 256] / [1, G, 256, 8]; q [B, Hq, 128] (float16/float32).  Returns
     out [B, Hq, 128] float32.  tables_ready: the given workspace holds the
-    tables of these codebooks from an earlier call (GSRQ_ATTN_TABLES_READY)."""
+    tables of these codebooks from an earlier call (GSRQ_ATTN_TABLES_READY).
+    noalloc: gsrq_attn_decode_noalloc (the library's per-GPU scratch instead
+    of a workspace; workspace must then be None)."""
     torch = _torch()
     lib = load_library()
     B, cap, W = k_codes.shape
@@ -399,12 +407,21 @@ def attn_decode(k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, 
     ash = make_attn_shape(B, cap, Hq, Hkv, hd, rope_base, scale,
                           GSRQ_ATTN_TABLES_READY if tables_ready else 0)
     sh = make_shape(B * cap, D, d, K, M)
+    if out is None:
+        out = torch.empty((B, Hq, hd), dtype=torch.float32, device=q.device)
+    if noalloc:
+        if workspace is not None:
+            raise ValueError("noalloc takes no workspace")
+        st = lib.gsrq_attn_decode_noalloc(
+            ctypes.byref(ash), ctypes.byref(sh), _ptr(k_codes), _ptr(v_codes), _ptr(seq_len),
+            _ptr(k_gain), _ptr(k_shape), _ptr(v_gain), _ptr(v_shape), _ptr(q), _dtype_code(q),
+            _ptr(out), _stream_handle(stream))
+        _check(st, "gsrq_attn_decode_noalloc")
+        return out
     n = ctypes.c_size_t()
     _check(lib.gsrq_attn_workspace_bytes(ctypes.byref(ash), ctypes.byref(n)),
            "gsrq_attn_workspace_bytes")
     ws = _workspace(n.value, q.device, workspace)
-    if out is None:
-        out = torch.empty((B, Hq, hd), dtype=torch.float32, device=q.device)
     st = lib.gsrq_attn_decode(ctypes.byref(ash), ctypes.byref(sh), _ptr(k_codes), _ptr(v_codes),
                               _ptr(seq_len), _ptr(k_gain), _ptr(k_shape), _ptr(v_gain),
                               _ptr(v_shape), _ptr(q), _dtype_code(q), _ptr(out), _ptr(ws),

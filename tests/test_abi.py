@@ -193,9 +193,25 @@ def test_attn_decode_validation_before_any_hip_call():
     assert call(ws=D + 16) == B.GSRQ_E_ARG                      # workspace alignment
     assert call(ws_bytes=1) == B.GSRQ_E_WORKSPACE
     assert call(a=dict(flags=2)) == B.GSRQ_E_ARG                # unknown flag
+    # the no-allocation variant validates the same way, and rejects a shape
+    # whose workspace exceeds its scratch, before any HIP call
+    def call_noalloc(a=None, kv=None, **ptr):
+        ash = B.make_attn_shape(**{**a0, **(a or {})})
+        p = {n: D for n in ("kc", "vc", "len", "kg", "ks", "vg", "vs", "q", "out")}
+        p.update(ptr)
+        return lib.gsrq_attn_decode_noalloc(ctypes.byref(ash), ctypes.byref(kv or kv0), p["kc"],
+                                            p["vc"], p["len"], p["kg"], p["ks"], p["vg"], p["vs"],
+                                            p["q"], B.GSRQ_F16, p["out"], None)
+
+    assert call_noalloc(a=dict(B=0)) == B.GSRQ_E_ARG
+    assert call_noalloc(q=None) == B.GSRQ_E_ARG
+    assert call_noalloc(kv=B.make_shape(200, 1024, 8, 256, 2)) == B.GSRQ_E_UNSUPPORTED
+    big = dict(Hkv=128, Hq=512)                                  # 16 MiB of tables alone
+    assert call_noalloc(a=big, kv=B.make_shape(200, 16384, 8, 256, 1)) == B.GSRQ_E_WORKSPACE
     ash = B.make_attn_shape(**a0)
     n = ctypes.c_size_t()
     assert lib.gsrq_attn_workspace_bytes(ctypes.byref(ash), ctypes.byref(n)) == B.GSRQ_OK
+    assert n.value <= B.ATTN_NOALLOC_BYTES
     assert n.value >= 2 * 8 * 4 * 130 * 4
     bad = B.make_attn_shape(**a0, rope_base=0.0)
     assert lib.gsrq_attn_workspace_bytes(ctypes.byref(bad), ctypes.byref(n)) == B.GSRQ_E_ARG
