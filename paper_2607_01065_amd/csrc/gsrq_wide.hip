@@ -73,7 +73,8 @@ static_assert(w_sreg(W_CMAX) * W_THREADS >= w_frags(W_CMAX) * 64, "staging holds
 
 // sigma exponent of each codebook: 2^sig >= its largest gain (unit_gain: 1).
 // Also records the codebook's smallest gain (gmin, for the exact kernel's
-// pruning) and clears the deferred-row state of its subspace (xcount,
+// pruning) and its largest one (gmin[ncb + cb], for the single pass's error
+// bound), and clears the deferred-row state of its subspace (xcount,
 // xchanged, xobj) before a scoring launch.
 __global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ gain, int K,
                                                       int unit_gain, const int* __restrict__ done,
@@ -81,7 +82,8 @@ __global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ 
                                                       float* __restrict__ gmin,
                                                       int* __restrict__ xcount,
                                                       int* __restrict__ xchanged,
-                                                      double* __restrict__ xobj) {
+                                                      double* __restrict__ xobj,
+                                                      int* __restrict__ hcount) {
   __shared__ float wm[4], wn[4];
   const int cb = cb0 + blockIdx.x;
   if (done && done[blockIdx.x % G]) return;
@@ -104,19 +106,22 @@ __global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ 
   if (threadIdx.x == 0) {
     sig[cb] = sigma_exp(fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3])));
     gmin[blockIdx.x] = fminf(fminf(wn[0], wn[1]), fminf(wn[2], wn[3]));
+    gmin[gridDim.x + blockIdx.x] = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
     xcount[blockIdx.x] = 0;
     xchanged[blockIdx.x] = 0;
     xobj[blockIdx.x] = 0.0;
+    if (hcount) hcount[blockIdx.x] = 0;
   }
 }
 
 // Operand fragments of one 32-codeword tile (grid: tiles x codebooks, one
 // wave).  Lane = codeword c (0..31) + 32 h; lane half h covers the 8-element
 // group 2p + h of pair p.  With a_j = -2 g s_j 2^SA / sigma and
-// gg = (g / sigma)^2 2^SA, the tile's fragments are, per lane:
+// gg = (g / sigma)^2 2^SA, the tile's fragments are, per lane, in order:
 //   HI_p (p < P)   hi(a[16p + 8h, 16p + 8h + 8))
-//   LO_p (p < P)   lo(a[16p + 8h, 16p + 8h + 8))
 //   bias           h0 [hi(gg) lo(gg) 2^SA 2^SA 0 0 0 0], h1 zero
+//   LO_p (p < P)   lo(a[16p + 8h, 16p + 8h + 8))
+// so the single-pass scoring kernel stages the first P + 1 of them only.
 // Padding codewords (k >= K) have a = 0 and a float16-max g^2 slot.
 __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ gain,
                                                     const float* __restrict__ shape, int d, int K,
@@ -147,11 +152,11 @@ __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ ga
       lo[j] = (_Float16)(av - (float)hi[j]);
     }
     out[p * 64 + lane] = pack_h8(hi);
-    out[(P + p) * 64 + lane] = pack_h8(lo);
+    out[(P + 1 + p) * 64 + lane] = pack_h8(lo);
   }
   const float gs = ldexpf(g, -ex);
   const float gg = ldexpf(gs * gs, SA);
-  out[2 * P * 64 + lane] = h ? (u4){0u, 0u, 0u, 0u} : bias_codeword(real, gg);
+  out[P * 64 + lane] = h ? (u4){0u, 0u, 0u, 0u} : bias_codeword(real, gg);
 }
 
 // Seed shapes s_k = x_r / (||x_r|| + eps) from rows of the row-major input.
@@ -184,11 +189,16 @@ struct WScoreArgs {
   int cb0;                // codebook index (gain, shape, sig) of subspace 0: m G
   int fcb0;               // codebook index of fragment-table entry 0
   const u4* frag;         // [ncb][tiles][QF][64]
-  const float* gmin;      // [ncb] smallest gain (same indexing as frag)
+  const float* gmin;      // [ncb] smallest gain (same indexing as frag), then [ncb] largest
   int* xcount;            // [G] rows deferred to the exact kernel (reset with sigma)
   int* xrows;             // [G][N] their row indices
   int* xchanged;          // [G] exact kernel: some deferred row changed code
   double* xobj;           // [G] exact kernel: their weighted distortion
+  int* hcount;            // [G] rows the single pass lists for the hi/lo pass
+  int* hrows;             // [G][N] their row indices
+  unsigned long long* hbest;  // [G][N] hi/lo pass: best (distance key, codeword) per listed row
+  float* hrr;             // [G][N] hi/lo pass: the row term rr, or -1 if it needs float64
+  int nslice, tps;        // hi/lo pass: tile slices and tiles per slice
   const int* sig;         // [ncb]
   const float* gain;      // [ncb][K]
   const float* shape;     // [ncb][K][d]
@@ -267,7 +277,7 @@ template <typename T, int P> struct WRaw {
 template <typename T, int P>
 __device__ __forceinline__ void w_make_b(const WRaw<T, P>& raw, int d, bool valid, int ex, int h,
                                          u4 (&bx)[P], u4 (&blo)[P], u4& bias, float& rr,
-                                         bool& need_exact) {
+                                         bool& need_exact, float& eD) {
   constexpr bool F16 = sizeof(T) == 2;
   int sr;
   if (F16) {
@@ -290,6 +300,8 @@ __device__ __forceinline__ void w_make_b(const WRaw<T, P>& raw, int d, bool vali
     sr = ex;
     rr = ldexpf(ss, -ex);
     need_exact = ex > 15 || ex < -14 || !(rr < 32768.f);
+    // single-pass error bound in D units: 2^-10 g ||x|| 2^SA / sigma, g <= sigma
+    eD = ldexpf(sqrtf(ss), SA - 10) * (1.f + 0x1p-9f);
   } else {
     float mx = 0.f, ss = 0.f;
 #pragma unroll
@@ -314,6 +326,8 @@ __device__ __forceinline__ void w_make_b(const WRaw<T, P>& raw, int d, bool vali
     sr = ex - er + SB;
     rr = ldexpf(ss, SB - ex - er);
     need_exact = tiny || !(mx > 0.f) || sr < -14 || !(rr < 32768.f);
+    // single-pass error bound in D units: 2^-9 g ||x|| 2^(SA+SB) / (sigma rho)
+    eD = ldexpf(sqrtf(ss), SA + SB - 9 - er) * (1.f + 0x1p-9f);
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       _Float16 hi[8], lo[8];
@@ -337,7 +351,7 @@ __device__ __forceinline__ void w_make_b(const WRaw<T, P>& raw, int d, bool vali
 template <typename T, int P>
 __device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bool valid, int ex, int h,
                                          u4 (&bx)[P], u4 (&blo)[P], u4& bias, float& rr,
-                                         bool& need_exact) {
+                                         bool& need_exact, float& eD) {
   constexpr bool F16 = sizeof(T) == 2;
   int sr;
   if (F16) {
@@ -369,6 +383,8 @@ __device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bo
     sr = ex;
     rr = ldexpf(ss, -ex);
     need_exact = ex > 15 || ex < -14 || !(rr < 32768.f);
+    // single-pass error bound in D units: 2^-10 g ||x|| 2^SA / sigma, g <= sigma
+    eD = ldexpf(sqrtf(ss), SA - 10) * (1.f + 0x1p-9f);
   } else {
     // pass 1: the row's scale; pass 2 re-reads the (cached) row and splits it
     float mx = 0.f, ss = 0.f;
@@ -397,6 +413,8 @@ __device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bo
     sr = ex - er + SB;
     rr = ldexpf(ss, SB - ex - er);
     need_exact = tiny || !(mx > 0.f) || sr < -14 || !(rr < 32768.f);
+    // single-pass error bound in D units: 2^-9 g ||x|| 2^(SA+SB) / (sigma rho)
+    eD = ldexpf(sqrtf(ss), SA + SB - 9 - er) * (1.f + 0x1p-9f);
 #pragma unroll
     for (int p = 0; p < P; ++p) {
       const int e0 = 16 * p + 8 * h;
@@ -430,12 +448,25 @@ __device__ __forceinline__ f16v w_tile(const u4* ta, const u4 (&bx)[P], const u4
   for (int p = 0; p < P; ++p) {
     const h8 ahi = as_h8(ta[p * 64]);
     acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi, as_h8(bx[p]), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[(P + p) * 64]), as_h8(bx[p]), acc, 0,
-                                                 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[(P + 1 + p) * 64]), as_h8(bx[p]), acc,
+                                                 0, 0, 0);
     if (!F16) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi, as_h8(blo[p]), acc, 0, 0, 0);
   }
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[2 * P * 64]), as_h8(bias), acc, 0, 0,
-                                                0);
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[P * 64]), as_h8(bias), acc, 0, 0, 0);
+}
+
+// Single-pass distances of one tile: hi(a) against the row's float16
+// operand (the row itself, or hi(b) of a float32 row) per pair, then the
+// bias terms (P + 1 MFMAs instead of 2P + 1 or 3P + 1).  The dropped lo
+// parts bound the error: |D~ - D| <= 2^-10 (1 + 2^-11) sum |a_j b_j| for
+// float16 rows, 2^-9 (1 + 2^-12) sum |a_j b_j| for float32 rows.
+template <int P>
+__device__ __forceinline__ f16v w_tile_sp(const u4* ta, const u4 (&bx)[P], u4 bias) {
+  f16v acc = {};
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[p * 64]), as_h8(bx[p]), acc, 0, 0, 0);
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[P * 64]), as_h8(bias), acc, 0, 0, 0);
 }
 
 // Smallest packed key of a tile: the low 4 bits of each distance carry its
@@ -454,6 +485,36 @@ __device__ __forceinline__ int w_tile_key(const f16v& c) {
 // best only with a strictly smaller distance, so ties keep the lower index.
 __device__ __forceinline__ void w_take(int key, int t, int& best, int& bt) {
   if (key < (best & ~15)) { best = key; bt = t; }
+}
+
+__device__ __forceinline__ int med3i(int a, int b, int c) {
+  int r;
+  asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
+// The two smallest packed keys of a tile (b <= s), streamed: each key
+// moves the second smallest to med3(b, s, key) and the smallest to
+// min(b, key).
+__device__ __forceinline__ void w_tile_key2(const f16v& c, int& b, int& s) {
+  constexpr int MASK = ~15;
+  const int k0 = __float_as_int(c[0]) & MASK, k1 = (__float_as_int(c[1]) & MASK) | 1;
+  b = min(k0, k1);
+  s = max(k0, k1);
+#pragma unroll
+  for (int j = 2; j < 16; ++j) {
+    const int k = (__float_as_int(c[j]) & MASK) | j;
+    s = med3i(b, s, k);
+    b = min(b, k);
+  }
+}
+
+// Running best (with its tile) and second-smallest key over tiles: the
+// second smallest of {best, second, b, s} is med3(best, b, min(second, s))
+// when best <= second and b <= s.
+__device__ __forceinline__ void w_take2(int b, int s, int t, int& best, int& bt, int& second) {
+  second = med3i(best, b, min(second, s));
+  w_take(b, t, best, bt);
 }
 
 // The loads never branch (indices past n are clamped and their values never
@@ -536,7 +597,19 @@ __device__ __forceinline__ void w_put_code(uint32_t* wp, int64_t bit, int b, int
 // Waves per SIMD: four (two workgroups per CU) with a resident table and
 // narrow rows; two when d >= 64 (row operands up to 68 VGPRs) or when the
 // table is streamed (staging registers).
-template <typename T, int C, int MODE, bool RESIDENT>
+// SP (single pass, d >= 64): P + 1 MFMAs per tile on the float16 operands
+// (w_tile_sp); the two smallest keys of every row are kept, and a row whose
+// second-best distance lies within twice the error bound of its best (or
+// whose keys cannot separate a 1e-4 margin) is listed for the hi/lo pass
+// instead of being decided here.
+// IND (indirect, the hi/lo pass after SP): the rows are the subspace's
+// listed ones (hrows, hcount) and the codebook is split into slices of tps
+// tiles, each kept whole in LDS by its workgroups; workgroup (g, slice, r0)
+// scores rounds r0, r0 + nwg, ... of the list against its slice and merges
+// every row's best (distance key, codeword) into hbest with a 64-bit
+// atomic minimum (lowest codeword on equal keys); w_listed_finish_kernel
+// then writes the outputs.
+template <typename T, int C, int MODE, bool RESIDENT, bool SP, bool IND>
 __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
     w_score_kernel(WScoreArgs a) {
   extern __shared__ __align__(16) u4 wtab[];
@@ -544,16 +617,20 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   __shared__ int red_changed;
   constexpr bool F16 = sizeof(T) == 2;
   constexpr int P = w_pairs(C);
-  constexpr int QU = w_frags(C);
+  constexpr int QU = SP ? P + 1 : w_frags(C);
   // two tiles' MFMA chains in flight, and the next round's row prefetched,
   // while the row operands are small enough to leave registers for both
-  constexpr bool PAIR_TILES = C <= 4;
-  constexpr bool PREFETCH = C <= 2;
+  constexpr bool PAIR_TILES = C <= 4 || SP;
+  constexpr bool PREFETCH = C <= 2 && !IND;
 
-  int g, rc;
+  int g, rc, slice = 0;
   {
     const int id = blockIdx.x;
-    if (a.map_xcd) {
+    if (IND) {
+      g = id % a.G;
+      slice = (id / a.G) % a.nslice;
+      rc = id / (a.G * a.nslice);
+    } else if (a.map_xcd) {
       const int xcd = id & 7, slot = id >> 3, gpx = a.G >> 3;
       const int j = slot % gpx;
       rc = slot / gpx;
@@ -564,12 +641,20 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
     }
   }
   if (a.done && a.done[g]) return;
+  // indirect rows: this workgroup takes rounds rc, rc + nwg, ... of the list
+  const int hcnt = IND ? a.hcount[g] : 0;
+  if (IND && rc * W_ROWS >= hcnt) return;
+  const int nrounds = IND ? (hcnt - rc * W_ROWS + a.nwg * W_ROWS - 1) / (a.nwg * W_ROWS)
+                          : a.rounds;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i = lane & 31, h = lane >> 5;
-  const int d = a.d, K = a.K, tiles = a.tiles;
+  const int d = a.d, K = a.K;
+  // this workgroup's tiles: all, or (IND) its slice
+  const int tb = IND ? slice * a.tps : 0;
+  const int tiles = IND ? min(a.tiles - tb, a.tps) : a.tiles;
   const int cb = a.cb0 + g;
   const int ex = a.sig[cb];
-  const u4* ftab = a.frag + (size_t)(cb - a.fcb0) * tiles * a.QF * 64;
+  const u4* ftab = a.frag + ((size_t)(cb - a.fcb0) * a.tiles + tb) * a.QF * 64;
   const float* gcb = a.gain + (size_t)cb * K;
   const float* scb = a.shape + (size_t)cb * K * d;
   const T* X = (const T*)a.x;
@@ -591,36 +676,62 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
 
   double obj = 0.0;
   bool any_changed = false;
-  // this lane's row of round rd
-  auto row_of = [&](int rd) -> int64_t {
-    return ((int64_t)rc * a.rounds + rd) * W_ROWS + (int64_t)wave * RB + i;
+  // this lane's row of round rd (valid: below N, or within the list)
+  auto row_of = [&](int rd, bool& valid) -> int64_t {
+    if (IND) {
+      const int idx = (rc + rd * a.nwg) * W_ROWS + wave * RB + i;
+      valid = idx < hcnt;
+      return a.hrows[(size_t)g * a.N + (valid ? idx : 0)];
+    }
+    const int64_t row = ((int64_t)rc * a.rounds + rd) * W_ROWS + (int64_t)wave * RB + i;
+    valid = row < a.N;
+    return row;
   };
   auto row_ptr = [&](int64_t row) -> const T* {
     return X + (row < a.N ? row : 0) * a.ldx + (int64_t)g * d;
   };
   WRaw<T, P> raw;
-  if (PREFETCH) raw.load(row_ptr(row_of(0)), d, vec, h);
-  for (int rd = 0; rd < a.rounds; ++rd) {
-    const int64_t r0 = row_of(rd) - i;
-    const int64_t row = r0 + i;
-    const bool valid = row < a.N;
+  if (PREFETCH) {
+    bool v0;
+    raw.load(row_ptr(row_of(0, v0)), d, vec, h);
+  }
+  for (int rd = 0; rd < nrounds; ++rd) {
+    bool valid;
+    const int64_t row = row_of(rd, valid);
     const T* xp = row_ptr(row);
     u4 bx[P], blo[P], bias;
-    float rr;
+    float rr, eD;
     bool need_exact;
     if (PREFETCH)
-      w_make_b<T, P>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact);
+      w_make_b<T, P>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact, eD);
     else
-      w_make_b_direct<T, P>(xp, d, vec, valid, ex, h, bx, blo, bias, rr, need_exact);
+      w_make_b_direct<T, P>(xp, d, vec, valid, ex, h, bx, blo, bias, rr, need_exact, eD);
     // the next round's row is fetched while this one is scored
-    if (PREFETCH && rd + 1 < a.rounds) raw.load(row_ptr(row_of(rd + 1)), d, vec, h);
+    if (PREFETCH && rd + 1 < nrounds) {
+      bool v1;
+      raw.load(row_ptr(row_of(rd + 1, v1)), d, vec, h);
+    }
 
-    int best = 0x7fffffff, bt = 0;
-    if (RESIDENT) {
-      for (int t = 0; t < tiles; t += (PAIR_TILES ? 2 : 1)) {
-        const u4* ta = wtab + (size_t)t * QU * 64 + lane;
+    int best = 0x7fffffff, bt = 0, second = 0x7fffffff;
+    // scores of tiles t and t + 1 (when present) into the running best
+    auto score = [&](const u4* ta, int t, bool pair) {
+      if (SP) {
+        const f16v c0 = w_tile_sp<P>(ta, bx, bias);
+        if (pair) {
+          const f16v c1 = w_tile_sp<P>(ta + QU * 64, bx, bias);
+          int b0, s0, b1, s1;
+          w_tile_key2(c0, b0, s0);
+          w_take2(b0, s0, t, best, bt, second);
+          w_tile_key2(c1, b1, s1);
+          w_take2(b1, s1, t + 1, best, bt, second);
+        } else {
+          int b0, s0;
+          w_tile_key2(c0, b0, s0);
+          w_take2(b0, s0, t, best, bt, second);
+        }
+      } else {
         const f16v c0 = w_tile<F16, P>(ta, bx, blo, bias);
-        if (PAIR_TILES && t + 1 < tiles) {
+        if (pair) {
           const f16v c1 = w_tile<F16, P>(ta + QU * 64, bx, blo, bias);
           w_take(w_tile_key(c0), t, best, bt);
           w_take(w_tile_key(c1), t + 1, best, bt);
@@ -628,6 +739,10 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
           w_take(w_tile_key(c0), t, best, bt);
         }
       }
+    };
+    if (RESIDENT) {
+      for (int t = 0; t < tiles; t += (PAIR_TILES ? 2 : 1))
+        score(wtab + (size_t)t * QU * 64 + lane, tb + t, PAIR_TILES && t + 1 < tiles);
     } else {
       const int tpc = a.tpc;
       const int nch = (tiles + tpc - 1) / tpc;
@@ -645,17 +760,8 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
         const int n_next = (c + 1 < nch) ? min(tpc, tiles - t0 - tpc) * QU * 64 : 0;
         if (n_next) w_stage_load<QU>(ftab, a.QF, t0 + tpc, n_next, reg);
         const u4* buf = wtab + (size_t)(c & 1) * chunk_u4;
-        for (int tt = 0; tt < nt; tt += (PAIR_TILES ? 2 : 1)) {
-          const u4* ta = buf + (size_t)tt * QU * 64 + lane;
-          const f16v c0 = w_tile<F16, P>(ta, bx, blo, bias);
-          if (PAIR_TILES && tt + 1 < nt) {
-            const f16v c1 = w_tile<F16, P>(ta + QU * 64, bx, blo, bias);
-            w_take(w_tile_key(c0), t0 + tt, best, bt);
-            w_take(w_tile_key(c1), t0 + tt + 1, best, bt);
-          } else {
-            w_take(w_tile_key(c0), t0 + tt, best, bt);
-          }
-        }
+        for (int tt = 0; tt < nt; tt += (PAIR_TILES ? 2 : 1))
+          score(buf + (size_t)tt * QU * 64 + lane, tb + t0 + tt, PAIR_TILES && tt + 1 < nt);
         if (n_next) w_stage_store(wtab + (size_t)((c + 1) & 1) * chunk_u4, n_next, reg);
         __syncthreads();
       }
@@ -665,6 +771,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
     // lowest codeword index
     int kstar;
     float dhat;
+    bool ambiguous = false;
     {
       const int j = best & 15;
       const int kidx = bt * CW + (j >> 2) * 8 + h * 4 + (j & 3);
@@ -676,6 +783,35 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       const long long v = v0 < v1 ? v0 : v1;
       dhat = __int_as_float((int)(v >> 32) << 4);
       kstar = (int)(v & 0xffffffffll);
+      if (SP) {
+        // second smallest over both halves: med3(b0, b1, min(s0, s1)); a
+        // row is decided when it lies beyond twice the error bound (the
+        // single-pass bound, float32 accumulation and key truncation)
+        // The bound of a codeword scales with its gain (eD is the bound at
+        // g = sigma): the best's own gain on its side, the codebook's
+        // largest gain for every other codeword.
+        const auto sb = __builtin_amdgcn_permlane32_swap(best, best, false, false);
+        const auto ss2 = __builtin_amdgcn_permlane32_swap(second, second, false, false);
+        const int srow = med3i(sb[0], sb[1], min(ss2[0], ss2[1]));
+        const float sv = __int_as_float(srow & ~15);
+        const float gb = a.unit_gain ? 1.f : gcb[kstar < K ? kstar : K - 1];
+        const float gx = a.unit_gain ? 1.f : a.gmin[a.G + (cb - a.fcb0)];
+        const float md = ldexpf(eD * (gb + gx), -ex) * 1.0625f +
+                         ldexpf(dhat + ldexpf(rr, SA + 1), -15) + 0x1p-3f;
+        ambiguous = !(sv - dhat > md);
+      }
+    }
+    if (IND) {
+      // this slice's best into the row's running minimum; the finish kernel
+      // decides the row (64-bit keys: the distance key with its sign bit
+      // flipped, so signed order is unsigned order, then the codeword)
+      if (valid && h == 0) {
+        const size_t idx = (size_t)g * a.N + (size_t)((rc + rd * a.nwg) * W_ROWS + wave * RB + i);
+        const uint32_t hv = (uint32_t)(__float_as_int(dhat) >> 4) ^ 0x80000000u;
+        atomicMin(a.hbest + idx, ((unsigned long long)hv << 32) | (uint32_t)kstar);
+        if (slice == 0) a.hrr[idx] = need_exact ? -1.f : rr;
+      }
+      continue;
     }
     need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
     // rows the key cannot decide go to the subspace's list for the exact
@@ -692,8 +828,24 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
         if (defer && h == 0) a.xrows[(size_t)g * a.N + base + rank] = (int)row;
       }
     }
+    // single pass: rows within the error bound go to the hi/lo pass
+    const bool relist = SP && valid && !defer && ambiguous;
+    if (SP) {
+      const unsigned long long fb = __ballot(relist && h == 0);
+      if (fb) {
+        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(fb >> 32),
+                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)fb, 0u));
+        int base = 0;
+        if (lane == 0) base = atomicAdd(a.hcount + g, __popcll(fb));
+        base = __shfl(base, 0);
+        if (relist && h == 0) {
+          a.hrows[(size_t)g * a.N + base + rank] = (int)row;
+          a.hbest[(size_t)g * a.N + base + rank] = ~0ull;
+        }
+      }
+    }
     if (kstar >= K) kstar = K - 1;   // deferred rows and rows past N only
-    const bool own = valid && !defer;
+    const bool own = valid && !defer && !relist;
 
     const float gk = a.unit_gain ? 1.f : gcb[kstar];
     const float* sk = scb + (size_t)kstar * d;
@@ -722,19 +874,17 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       }
     }
   }
-  if (MODE == W_TRAIN) {
+  if (MODE == W_TRAIN && !IND) {
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) obj += __shfl_xor(obj, off);
     if (lane == 0) red_obj[wave] = obj;
     if (__ballot(any_changed) && lane == 0) atomicOr(&red_changed, 1);
     __syncthreads();
     if (tid == 0) {
+      double s = 0.0;
+      for (int w = 0; w < W_WAVES; ++w) s += red_obj[w];
       a.changed[(size_t)g * a.nwg + rc] = red_changed;
-      if (a.obj) {
-        double s = 0.0;
-        for (int w = 0; w < W_WAVES; ++w) s += red_obj[w];
-        a.obj[(size_t)g * a.nwg + rc] = s;
-      }
+      if (a.obj) a.obj[(size_t)g * a.nwg + rc] = s;
     }
   }
 }
@@ -829,7 +979,8 @@ __global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_kernel(WFusedArgs
       u4 bx[1], blo[1], bias;
       float rr;
       bool need_exact;
-      w_make_b<float, 1>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact);
+      float eD;
+      w_make_b<float, 1>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact, eD);
       int best = 0x7fffffff, bt = 0;
       for (int t = 0; t < a.tiles; t += 2) {
         const u4* ta = wtab + (size_t)t * QU * 64 + lane;
@@ -924,6 +1075,68 @@ __global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_kernel(WFusedArgs
       } else {
 #pragma unroll
         for (int j = 0; j < 8; ++j) dst[j] = r[rd][j];
+      }
+    }
+  }
+}
+
+// Outputs of the rows the single pass listed, after the sliced hi/lo pass:
+// each row's best (distance key, codeword) from hbest is checked like a row
+// of the scoring kernel (operands in the float16 range, best distance at
+// most twice the row's energy) and either appended to the exact kernel's
+// list or written out: training the assignment, the stop flag (xchanged)
+// and the weighted distortion (xobj); encode the code bits and the
+// residual.  One wave per listed row, grid-stride over the list.
+template <typename T, int MODE>
+__global__ void __launch_bounds__(256) w_listed_finish_kernel(WScoreArgs a) {
+  const int g = blockIdx.y;
+  if (a.done && a.done[g]) return;
+  const int cnt = a.hcount[g];
+  const int lane = threadIdx.x & 63, wpb = blockDim.x >> 6;
+  const int d = a.d, K = a.K;
+  const int cb = a.cb0 + g;
+  const float* gcb = a.gain + (size_t)cb * K;
+  const float* scb = a.shape + (size_t)cb * K * d;
+  const T* X = (const T*)a.x;
+  for (int idx = blockIdx.x * wpb + (int)(threadIdx.x >> 6); idx < cnt; idx += gridDim.x * wpb) {
+    const size_t li = (size_t)g * a.N + idx;
+    const int64_t row = a.hrows[li];
+    const unsigned long long key = a.hbest[li];
+    const float rr = a.hrr[li];
+    const int kstar = (int)(uint32_t)key;
+    const float dhat = __int_as_float((int)((uint32_t)(key >> 32) ^ 0x80000000u) << 4);
+    if (!(rr >= 0.f) || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K) {
+      if (lane == 0) {
+        const int pos = atomicAdd(a.xcount + g, 1);
+        a.xrows[(size_t)g * a.N + pos] = (int)row;
+      }
+      continue;
+    }
+    const float gk = a.unit_gain ? 1.f : gcb[kstar];
+    const float* sk = scb + (size_t)kstar * d;
+    const T* xp = X + row * a.ldx + (int64_t)g * d;
+    if (MODE == W_TRAIN) {
+      if (a.obj) {
+        float dist = 0.f;
+        for (int j = lane; j < d; j += 64) {
+          const float r = fmaf(-gk, sk[j], (float)xp[j]);
+          dist = fmaf(r, r, dist);
+        }
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) dist += __shfl_xor(dist, off);
+        if (lane == 0) atomicAdd(a.xobj + g, (double)(a.w ? a.w[row] : 1.f) * (double)dist);
+      }
+      if (lane == 0) {
+        uint16_t* ap = a.assign + (size_t)g * a.N + row;
+        if (*ap != (uint16_t)kstar) a.xchanged[g] = 1;
+        *ap = (uint16_t)kstar;
+      }
+    } else {
+      if (lane == 0 && a.codes)
+        w_put_code(a.codes + row * a.words, ((int64_t)a.m * a.G + g) * a.b, a.b, kstar);
+      if (a.res_out) {
+        float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d;
+        for (int j = lane; j < d; j += 64) dst[j] = fmaf(-gk, sk[j], (float)xp[j]);
       }
     }
   }
@@ -1684,27 +1897,43 @@ struct WLayout {
   int C, QF, tiles, nwg, rounds, tpc, map_xcd, lg;
   size_t frag_bytes;
   bool resident;
+  bool sp;              // single-pass scoring (d >= 64), then the hi/lo pass
   int Qu;
   size_t lds;
 };
 
-// Launch geometry of the scoring kernel for one stage input type.
-WLayout w_score_layout(const gsrq_shape* s, size_t x_elt, bool f16rows) {
+// Subvectors of at least 64 elements are scored in a single float16 pass
+// (P + 1 MFMAs per tile), the few rows it cannot decide in the hi/lo pass.
+// Narrower ones, and codebooks below 1024 codewords, keep the hi/lo pass
+// alone: there the MFMA chain is short (or the launch is bound by the rows'
+// traffic) and the single pass's second-best bookkeeping and second pass
+// would cost more than the MFMAs it saves.
+constexpr int W_SP_MIN_C = 8;
+constexpr int W_SP_MIN_TILES = 32;   // K >= 1024: below, scoring is not MFMA-bound
+constexpr int W_HP_WGS = 1024;  // workgroups of the hi/lo pass over listed rows
+constexpr int W_HP_SLICES = 8;  // codebook slices of that pass
+constexpr int W_SP_RESIDENT_BYTES = 78 * 1024;   // single-pass table kept whole in LDS
+
+// Launch geometry of the scoring kernel for one stage input type; hp: the
+// hi/lo pass (every fragment staged) even where the single pass applies.
+WLayout w_score_layout(const gsrq_shape* s, size_t x_elt, bool f16rows, bool hp = false) {
   WLayout L;
   const int64_t G = s->D / s->d;
   L.C = w_cwidth(s->d);
   L.QF = w_frags(L.C);
   L.tiles = (s->K + CW - 1) / CW;
   L.frag_bytes = (size_t)L.tiles * L.QF * 64 * sizeof(u4);
-  L.Qu = L.QF;
+  L.sp = !hp && L.C >= W_SP_MIN_C && L.tiles >= W_SP_MIN_TILES;
+  L.Qu = L.sp ? w_pairs(L.C) + 1 : L.QF;
   (void)f16rows;
   const size_t used = (size_t)L.tiles * L.Qu * 64 * sizeof(u4);
-  L.resident = used <= (size_t)W_RESIDENT_BYTES;
+  // single pass: two workgroups per CU share 160 KiB of LDS
+  L.resident = used <= (size_t)(L.sp ? W_SP_RESIDENT_BYTES : W_RESIDENT_BYTES);
   const int64_t row_rounds = (s->N + W_ROWS - 1) / W_ROWS;
   if (L.resident) {
     // enough rounds per workgroup to amortise the table load, while
     // keeping about four workgroups per CU in the grid
-    int64_t r = (row_rounds * G + 1023) / 1024;
+    int64_t r = (row_rounds * G + (L.sp ? 511 : 1023)) / (L.sp ? 512 : 1024);
     if (r < 1) r = 1;
     L.rounds = (int)r;
     L.tpc = 0;
@@ -1725,22 +1954,53 @@ size_t w_stream_need(const WLayout& L) {
   return 2 * (size_t)L.tpc * L.Qu * 64 * sizeof(u4);
 }
 
-template <typename T, int C, int MODE>
-gsrq_status w_score_launch_c(const WScoreArgs& a, const WLayout& L, hipStream_t st) {
-  const dim3 grid((unsigned)(a.G * L.nwg));
+template <typename T, int C, int MODE, bool SP, bool IND>
+gsrq_status w_score_launch_v(const WScoreArgs& a, const WLayout& L, hipStream_t st) {
+  const dim3 grid((unsigned)(a.G * a.nwg * (IND ? a.nslice : 1)));
   // a streamed d = 256 tile pair (2 x 33 KiB) exceeds the default 64 KiB of
   // dynamic LDS
-  const void* fn = L.resident ? (const void*)w_score_kernel<T, C, MODE, true>
-                              : (const void*)w_score_kernel<T, C, MODE, false>;
+  const void* fn = L.resident ? (const void*)w_score_kernel<T, C, MODE, true, SP, IND>
+                              : (const void*)w_score_kernel<T, C, MODE, false, SP, IND>;
   if (L.lds > 65536 &&
       hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)L.lds) !=
           hipSuccess)
     return GSRQ_E_HIP;
   if (L.resident)
-    w_score_kernel<T, C, MODE, true><<<grid, W_THREADS, L.lds, st>>>(a);
+    w_score_kernel<T, C, MODE, true, SP, IND><<<grid, W_THREADS, L.lds, st>>>(a);
   else
-    w_score_kernel<T, C, MODE, false><<<grid, W_THREADS, L.lds, st>>>(a);
+    w_score_kernel<T, C, MODE, false, SP, IND><<<grid, W_THREADS, L.lds, st>>>(a);
   return launch_ok();
+}
+
+// The scoring launch(es) of one pass: the hi/lo kernel over every row, or
+// (d >= 64) the single pass over every row and then the hi/lo kernel over
+// the rows it listed.
+template <typename T, int C, int MODE>
+gsrq_status w_score_launch_c(const WScoreArgs& a, const WLayout& L, hipStream_t st) {
+  if constexpr (C >= W_SP_MIN_C) {
+    if (L.sp) {
+      gsrq_status e = w_score_launch_v<T, C, MODE, true, false>(a, L, st);
+      if (e) return e;
+      // hi/lo pass over the listed rows: the codebook in W_HP_SLICES
+      // slices (streamed through LDS), about W_HP_WGS workgroups in all
+      gsrq_shape s1 = {a.N, a.G * a.d, a.d, a.K, 1};
+      WLayout H = w_score_layout(&s1, sizeof(T), sizeof(T) == 2, true);
+      const int tile_bytes = H.Qu * 64 * (int)sizeof(u4);
+      WScoreArgs b = a;
+      b.nslice = std::min(W_HP_SLICES, a.tiles);
+      b.tps = (a.tiles + b.nslice - 1) / b.nslice;
+      b.nslice = (a.tiles + b.tps - 1) / b.tps;
+      b.nwg = std::max(1, W_HP_WGS / (a.G * b.nslice));
+      b.map_xcd = 0;
+      H.resident = (size_t)b.tps * tile_bytes <= (size_t)W_RESIDENT_BYTES;
+      if (H.resident) H.lds = (size_t)b.tps * tile_bytes;
+      b.tpc = H.tpc;
+      if ((e = w_score_launch_v<T, C, MODE, false, true>(b, H, st))) return e;
+      w_listed_finish_kernel<T, MODE><<<dim3(64, a.G), 256, 0, st>>>(a);
+      return launch_ok();
+    }
+  }
+  return w_score_launch_v<T, C, MODE, false, false>(a, L, st);
 }
 
 template <typename T, int MODE>
@@ -1760,11 +2020,15 @@ gsrq_status w_score_launch(const WScoreArgs& a, const WLayout& L, hipStream_t st
 // gains, row lists and what the exact kernel adds to the stop test and the
 // objective.
 struct WDefer {
-  float* gmin;      // [G]
+  float* gmin;      // [G] smallest gains, then [G] largest
   int* xcount;      // [G]
   int* xrows;       // [G][N]
   int* xchanged;    // [G]
   double* xobj;     // [G]
+  int* hcount;      // [G] rows listed by the single pass (null: no single pass)
+  int* hrows;       // [G][N]
+  unsigned long long* hbest;   // [G][N]
+  float* hrr;       // [G][N]
 };
 
 // Fragment tables (and sigma, smallest gain, cleared deferred-row state) of
@@ -1774,7 +2038,7 @@ gsrq_status w_build_frags(const float* gain, const float* shape, int d, int K, i
                           const WDefer& X, hipStream_t st) {
   TimedLaunch tl(GSRQ_KERNEL_FRAGMENTS, st);
   w_sigma_kernel<<<ncb, 256, 0, st>>>(gain, K, unit_gain ? 1 : 0, done, G, cb0, sig, X.gmin,
-                                      X.xcount, X.xchanged, X.xobj);
+                                      X.xcount, X.xchanged, X.xobj, X.hcount);
   gsrq_status e = launch_ok();
   if (e) return e;
   const int tiles = (K + CW - 1) / CW;
@@ -1830,8 +2094,8 @@ WAccLayout w_acc_layout(const gsrq_shape* s) {
 }
 
 struct WTrainWs {
-  size_t frag, gmin, xcount, xrows, xchanged, xobj, sig, part, changed, obj, assign, done, iters,
-      seednorm, seeds, sorted, boff, total;
+  size_t frag, gmin, xcount, xrows, xchanged, xobj, hcount, hrows, hbest, hrr, sig, part,
+      changed, obj, assign, done, iters, seednorm, seeds, sorted, boff, total;
 };
 
 WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
@@ -1842,11 +2106,15 @@ WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
   const WAccLayout A = w_acc_layout(s);
   size_t off = 0;
   W.frag = off; off = align256(off + (size_t)G * L16.frag_bytes);
-  W.gmin = off; off = align256(off + (size_t)G * sizeof(float));
+  W.gmin = off; off = align256(off + 2 * (size_t)G * sizeof(float));
   W.xcount = off; off = align256(off + (size_t)G * sizeof(int));
   W.xrows = off; off = align256(off + (size_t)G * s->N * sizeof(int));
   W.xchanged = off; off = align256(off + (size_t)G * sizeof(int));
   W.xobj = off; off = align256(off + (size_t)G * sizeof(double));
+  W.hcount = off; off = align256(off + (L16.sp ? (size_t)G * sizeof(int) : 0));
+  W.hrows = off; off = align256(off + (L16.sp ? (size_t)G * s->N * sizeof(int) : 0));
+  W.hbest = off; off = align256(off + (L16.sp ? (size_t)G * s->N * 8 : 0));
+  W.hrr = off; off = align256(off + (L16.sp ? (size_t)G * s->N * sizeof(float) : 0));
   W.sig = off; off = align256(off + (size_t)G * sizeof(int));
   W.part = off;
   off = align256(off + (size_t)G * A.rchunks * s->K * (2 * s->d + 2) * sizeof(double));
@@ -1864,7 +2132,8 @@ WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
 }
 
 struct WEncWs {
-  size_t frag, gmin, xcount, xrows, xchanged, xobj, sig, res0, res1, total;
+  size_t frag, gmin, xcount, xrows, xchanged, xobj, hcount, hrows, hbest, hrr, sig, res0, res1,
+      total;
 };
 
 // Several stages of narrow wide rows (d <= 16) with resident fragment
@@ -1884,22 +2153,27 @@ WEncWs w_encode_ws(const gsrq_shape* s) {
     // buffers and no deferred-row lists
     const size_t ncb = (size_t)s->M * G;
     W.frag = off; off = align256(off + ncb * L.frag_bytes);
-    W.gmin = off; off = align256(off + ncb * sizeof(float));
+    W.gmin = off; off = align256(off + 2 * ncb * sizeof(float));
     W.xcount = off; off = align256(off + ncb * sizeof(int));
     W.xrows = off;
     W.xchanged = off; off = align256(off + ncb * sizeof(int));
     W.xobj = off; off = align256(off + ncb * sizeof(double));
+    W.hcount = W.hrows = W.hbest = W.hrr = off;
     W.sig = off; off = align256(off + ncb * sizeof(int));
     W.res0 = W.res1 = off;
     W.total = std::max(off, (size_t)256);
     return W;
   }
   W.frag = off; off = align256(off + (size_t)G * L.frag_bytes);
-  W.gmin = off; off = align256(off + (size_t)G * sizeof(float));
+  W.gmin = off; off = align256(off + 2 * (size_t)G * sizeof(float));
   W.xcount = off; off = align256(off + (size_t)G * sizeof(int));
   W.xrows = off; off = align256(off + (size_t)G * s->N * sizeof(int));
   W.xchanged = off; off = align256(off + (size_t)G * sizeof(int));
   W.xobj = off; off = align256(off + (size_t)G * sizeof(double));
+  W.hcount = off; off = align256(off + (L.sp ? (size_t)G * sizeof(int) : 0));
+  W.hrows = off; off = align256(off + (L.sp ? (size_t)G * s->N * sizeof(int) : 0));
+  W.hbest = off; off = align256(off + (L.sp ? (size_t)G * s->N * 8 : 0));
+  W.hrr = off; off = align256(off + (L.sp ? (size_t)G * s->N * sizeof(float) : 0));
   W.sig = off; off = align256(off + (size_t)s->M * G * sizeof(int));
   W.res0 = W.res1 = off;
   if (s->M > 1) {
@@ -1924,7 +2198,7 @@ gsrq_status w_encode_stage(const gsrq_shape* s, int m, const void* x, int64_t ld
   a.tiles = L.tiles; a.QF = L.QF; a.cb0 = m * a.G; a.fcb0 = m * a.G;
   a.frag = frag; a.sig = sig; a.gain = gain; a.shape = shape; a.unit_gain = 0;
   a.gmin = X.gmin; a.xcount = X.xcount; a.xrows = X.xrows; a.xchanged = X.xchanged;
-  a.xobj = X.xobj;
+  a.xobj = X.xobj; a.hcount = X.hcount; a.hrows = X.hrows; a.hbest = X.hbest; a.hrr = X.hrr;
   a.codes = codes; a.words = words; a.b = log2i(s->K); a.m = m; a.res_out = res_out;
   a.nwg = L.nwg; a.rounds = L.rounds; a.tpc = L.tpc; a.map_xcd = L.map_xcd; a.lg = L.lg;
   return w_score_and_exact<T, W_ENCODE>(a, L, GSRQ_KERNEL_ENCODE, st);
@@ -1944,7 +2218,11 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   char* base = (char*)ws;
   u4* frag = (u4*)(base + W.frag);
   const WDefer XD = {(float*)(base + W.gmin), (int*)(base + W.xcount), (int*)(base + W.xrows),
-                     (int*)(base + W.xchanged), (double*)(base + W.xobj)};
+                     (int*)(base + W.xchanged), (double*)(base + W.xobj),
+                     W.hrows > W.hcount ? (int*)(base + W.hcount) : nullptr,
+                     W.hrows > W.hcount ? (int*)(base + W.hrows) : nullptr,
+                     W.hrows > W.hcount ? (unsigned long long*)(base + W.hbest) : nullptr,
+                     W.hrows > W.hcount ? (float*)(base + W.hrr) : nullptr};
   int* sig = (int*)(base + W.sig);
   double* part = (double*)(base + W.part);
   int* changed = (int*)(base + W.changed);
@@ -1964,7 +2242,8 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   sa.x = X; sa.ldx = ldx; sa.N = s->N; sa.d = d; sa.K = K; sa.G = G;
   sa.tiles = L.tiles; sa.QF = L.QF; sa.cb0 = 0; sa.fcb0 = 0; sa.frag = frag; sa.sig = sig;
   sa.gmin = XD.gmin; sa.xcount = XD.xcount; sa.xrows = XD.xrows; sa.xchanged = XD.xchanged;
-  sa.xobj = XD.xobj;
+  sa.xobj = XD.xobj; sa.hcount = XD.hcount; sa.hrows = XD.hrows; sa.hbest = XD.hbest;
+  sa.hrr = XD.hrr;
   sa.gain = gain; sa.shape = shape; sa.w = w; sa.done = done; sa.assign = assign;
   sa.changed = changed; sa.obj = nullptr;
   sa.nwg = L.nwg; sa.rounds = L.rounds; sa.tpc = L.tpc; sa.map_xcd = L.map_xcd; sa.lg = L.lg;
@@ -2109,7 +2388,11 @@ gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64
   char* base = (char*)workspace;
   u4* frag = (u4*)(base + W.frag);
   const WDefer XD = {(float*)(base + W.gmin), (int*)(base + W.xcount), (int*)(base + W.xrows),
-                     (int*)(base + W.xchanged), (double*)(base + W.xobj)};
+                     (int*)(base + W.xchanged), (double*)(base + W.xobj),
+                     W.hrows > W.hcount ? (int*)(base + W.hcount) : nullptr,
+                     W.hrows > W.hcount ? (int*)(base + W.hrows) : nullptr,
+                     W.hrows > W.hcount ? (unsigned long long*)(base + W.hbest) : nullptr,
+                     W.hrows > W.hcount ? (float*)(base + W.hrr) : nullptr};
   int* sig = (int*)(base + W.sig);
   float* res[2] = {(float*)(base + W.res0), (float*)(base + W.res1)};
   const int words = (int)((s->M * (int64_t)G * log2i(s->K) + 31) / 32);

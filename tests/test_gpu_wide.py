@@ -37,6 +37,8 @@ def _gpu():
     (1300, 32, 8, 1024),     # streamed, one group (d = 8, K > 256)
     (130, 128, 64, 32),      # one tile
     (400, 512, 256, 256),    # streamed, d = 256 (two heads per subvector)
+    (3000, 256, 128, 1024),  # single float16 pass (d >= 64, K >= 1024) + listed rows
+    (2500, 128, 64, 2048),   # single pass, d = 64
 ])
 def test_wide_encode_single_stage(dtype, N, D, d, K):
     say("wide encode single stage", dtype.__name__, N, D, d, K)
@@ -68,6 +70,7 @@ def test_wide_encode_single_stage(dtype, N, D, d, K):
     (np.float16, 2, 256, 128, 256, 400, False),  # one launch per stage (d = 128)
     (np.float16, 4, 16, 32, 64, 301, False),     # one launch per stage (d = 32)
     (np.float32, 3, 128, 256, 512, 300, False),  # one launch per stage (d = 256)
+    (np.float32, 2, 1024, 128, 128, 2200, None), # single pass + listed rows, per stage
 ])
 def test_wide_encode_multi_stage_teacher_forced(dtype, M, K, d, D, N, exact_rows):
     """Stage m is checked on the residual the GPU's own earlier choices leave.
@@ -192,6 +195,8 @@ def test_wide_decode(M, K, d, D, N):
     (np.float16, 4100, 16, 8, 512, False),
     (np.float32, 1500, 64, 32, 32, True),
     (np.float16, 1200, 512, 256, 128, True),
+    (np.float32, 3000, 128, 128, 1024, True),   # single pass + listed rows
+    (np.float16, 2600, 128, 64, 1024, False),   # single pass, d = 64
 ])
 def test_wide_train_teacher_forced(dtype, N, D, d, K, weighted):
     say("wide train teacher forced", dtype.__name__, N, D, d, K, weighted)
@@ -269,7 +274,8 @@ def test_wide_train_stop_rule_and_residual():
     assert np.all(r2.iters.cpu().numpy() == 5)
 
 
-@pytest.mark.parametrize("N,D,d,K", [(700, 32, 8, 256), (700, 64, 16, 256), (300, 256, 128, 512)])
+@pytest.mark.parametrize("N,D,d,K", [(700, 32, 8, 256), (700, 64, 16, 256), (300, 256, 128, 512),
+                                     (300, 256, 128, 2048)])
 def test_rows_far_below_codebook_scale(N, D, d, K):
     """Float32 rows (residuals) 1e3 to 1e5 times smaller than the largest
     gains, as late residual stages produce: indices follow the margin rule
