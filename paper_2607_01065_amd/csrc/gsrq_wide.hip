@@ -68,6 +68,15 @@ __host__ __device__ constexpr int w_sreg(int C) {
              : (w_frags(C) * 64 + W_THREADS - 1) / W_THREADS;
 }
 static_assert(w_sreg(W_CMAX) * W_THREADS >= w_frags(W_CMAX) * 64, "staging holds one tile");
+// The single pass stages P + 1 fragments per tile through larger chunks
+// (fewer barriers per round); two workgroups per CU still fit in LDS.
+constexpr int W_SP_STREAM_BYTES = 36864;
+__host__ __device__ constexpr int w_sp_sreg(int C) {
+  return (W_SP_STREAM_BYTES / 16 + W_THREADS - 1) / W_THREADS >
+                 ((w_pairs(C) + 1) * 64 + W_THREADS - 1) / W_THREADS
+             ? (W_SP_STREAM_BYTES / 16 + W_THREADS - 1) / W_THREADS
+             : ((w_pairs(C) + 1) * 64 + W_THREADS - 1) / W_THREADS;
+}
 
 // ------------------------------------------------------------------ kernels
 
@@ -517,18 +526,28 @@ __device__ __forceinline__ void w_take2(int b, int s, int t, int& best, int& bt,
   w_take(b, t, best, bt);
 }
 
-// The loads never branch (indices past n are clamped and their values never
-// stored), so they stay in flight while the current chunk is scored.
-template <int QU, int SR>
-__device__ __forceinline__ void w_stage_load(const u4* ftab, int QF, int t0, int n,
-                                             u4 (&reg)[SR]) {
+// Staging of a chunk of fragment tiles: thread slot r holds element
+// e = r W_THREADS + tid of the chunk, i.e. entry o of its tile tr (both
+// fixed per thread, computed once).  The loads never branch: a slot past
+// the chunk's last tile reads that tile again and is never stored, so the
+// loads stay in flight while the current chunk is scored.
+template <int QU, int SR> struct WStage {
+  int tr[SR], o[SR];
+  __device__ __forceinline__ WStage() {
 #pragma unroll
-  for (int r = 0; r < SR; ++r) {
-    const int e = min(r * W_THREADS + (int)threadIdx.x, n - 1);
-    const int t = e / (QU * 64), o = e - t * (QU * 64);
-    reg[r] = ftab[((size_t)(t0 + t) * QF) * 64 + o];
+    for (int r = 0; r < SR; ++r) {
+      const int e = r * W_THREADS + (int)threadIdx.x;
+      tr[r] = e / (QU * 64);
+      o[r] = e - tr[r] * (QU * 64);
+    }
   }
-}
+  __device__ __forceinline__ void load(const u4* ftab, int QF, int t0, int nt,
+                                       u4 (&reg)[SR]) const {
+#pragma unroll
+    for (int r = 0; r < SR; ++r)
+      reg[r] = ftab[(uint32_t)((t0 + min(tr[r], nt - 1)) * QF * 64 + o[r])];
+  }
+};
 template <int SR>
 __device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[SR]) {
 #pragma unroll
@@ -716,8 +735,8 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
     // scores of tiles t and t + 1 (when present) into the running best
     auto score = [&](const u4* ta, int t, bool pair) {
       if (SP) {
-        const f16v c0 = w_tile_sp<P>(ta, bx, bias);
         if (pair) {
+          const f16v c0 = w_tile_sp<P>(ta, bx, bias);
           const f16v c1 = w_tile_sp<P>(ta + QU * 64, bx, bias);
           int b0, s0, b1, s1;
           w_tile_key2(c0, b0, s0);
@@ -725,6 +744,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
           w_tile_key2(c1, b1, s1);
           w_take2(b1, s1, t + 1, best, bt, second);
         } else {
+          const f16v c0 = w_tile_sp<P>(ta, bx, bias);
           int b0, s0;
           w_tile_key2(c0, b0, s0);
           w_take2(b0, s0, t, best, bt, second);
@@ -747,18 +767,21 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       const int tpc = a.tpc;
       const int nch = (tiles + tpc - 1) / tpc;
       const int chunk_u4 = tpc * QU * 64;
-      u4 reg[w_sreg(C)];
+      constexpr int SR = SP ? w_sp_sreg(C) : w_sreg(C);
+      const WStage<QU, SR> stg;
+      u4 reg[SR];
       {
-        const int n = min(tpc, tiles) * QU * 64;
-        w_stage_load<QU>(ftab, a.QF, 0, n, reg);
-        w_stage_store(wtab, n, reg);
+        const int nt0 = min(tpc, tiles);
+        stg.load(ftab, a.QF, 0, nt0, reg);
+        w_stage_store(wtab, nt0 * QU * 64, reg);
       }
       __syncthreads();
       for (int c = 0; c < nch; ++c) {
         const int t0 = c * tpc;
         const int nt = min(tpc, tiles - t0);
-        const int n_next = (c + 1 < nch) ? min(tpc, tiles - t0 - tpc) * QU * 64 : 0;
-        if (n_next) w_stage_load<QU>(ftab, a.QF, t0 + tpc, n_next, reg);
+        const int nt_next = (c + 1 < nch) ? min(tpc, tiles - t0 - tpc) : 0;
+        const int n_next = nt_next * QU * 64;
+        if (n_next) stg.load(ftab, a.QF, t0 + tpc, nt_next, reg);
         const u4* buf = wtab + (size_t)(c & 1) * chunk_u4;
         for (int tt = 0; tt < nt; tt += (PAIR_TILES ? 2 : 1))
           score(buf + (size_t)tt * QU * 64 + lane, tb + t0 + tt, PAIR_TILES && tt + 1 < nt);
@@ -1940,7 +1963,8 @@ WLayout w_score_layout(const gsrq_shape* s, size_t x_elt, bool f16rows, bool hp 
     L.lds = used;
   } else {
     L.rounds = 1;
-    L.tpc = std::max(1, (int)(W_STREAM_BYTES / (L.Qu * 64 * sizeof(u4))));
+    L.tpc = std::max(1, (int)((L.sp ? W_SP_STREAM_BYTES : W_STREAM_BYTES) /
+                              (L.Qu * 64 * sizeof(u4))));
     L.lds = 2 * (size_t)L.tpc * L.Qu * 64 * sizeof(u4);
   }
   L.nwg = (int)((row_rounds + L.rounds - 1) / L.rounds);
