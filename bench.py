@@ -218,7 +218,8 @@ def extra_paths(B, cache, wl, dev, reps=50):
     us = e0.elapsed_time(e1) / reps * 1e3
     out["row_weights"] = {"us": us, "tokens": wl.N, "grad_GBps": G.numel() * 2 / (us * 1e-6) / 1e9}
     del G
-    app = {}
+    app, app_p, app_k = {}, {}, {}
+    prep = B.prepare_codebook(cache["gain"], cache["shape"]) if wl.d <= 8 and wl.K <= 256 else None
     for n in (1, 8, 64):
         X = cache["X"][:n].contiguous()
         codes = torch.empty((n, cache["codes"].shape[1]), dtype=torch.int32, device=dev)
@@ -232,7 +233,26 @@ def extra_paths(B, cache, wl, dev, reps=50):
         e1.record()
         torch.cuda.synchronize()
         app[str(n)] = e0.elapsed_time(e1) / reps * 1e3
+        if prep is not None:
+            B.encode_prepared(X, prep, codes=codes)
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                B.encode_prepared(X, prep, codes=codes)
+            e1.record()
+            torch.cuda.synchronize()
+            app_p[str(n)] = e0.elapsed_time(e1) / reps * 1e3
+            # kernel time alone (launch timing of the encode kind)
+            B.timing_enable(True, kinds=["encode"])
+            for _ in range(reps):
+                B.encode_prepared(X, prep, codes=codes)
+            B.timing_enable(False)
+            ms, cnt = B.timing_read()["encode"]
+            app_k[str(n)] = ms / max(cnt, 1) * 1e3
     out["append_encode_us"] = app
+    if prep is not None:
+        out["append_encode_prepared_us"] = app_p
+        out["append_encode_prepared_kernel_us"] = app_k
     out.update(attention_measure(B, dev))
     return out
 

@@ -188,6 +188,41 @@ gsrq_status gsrq_encode(const gsrq_shape* s,
                         void* workspace, size_t ws_bytes, void* stream);
 
 /*
+ * Prepared codebooks: encoding a few rows at a time (the tokens appended at
+ * every step of autoregressive decoding, which the paper's fused kernel
+ * quantises and bit-packs as they are generated, Appendix C) is bound by
+ * the per-call preparation of the codebook's MFMA operand tables.  A
+ * prepared codebook holds those tables, built once, with a copy of the
+ * codebook itself, in one caller-owned device buffer; gsrq_encode_prepared
+ * then encodes without rebuilding them.  The narrow family only (d <= 8,
+ * K <= 256; other shapes GSRQ_E_UNSUPPORTED).
+ *
+ * gsrq_prepared_bytes -- bytes of a prepared codebook for shape s (all M
+ * stages, G codebooks each).
+ */
+gsrq_status gsrq_prepared_bytes(const gsrq_shape* s, size_t* bytes);
+
+/*
+ * gsrq_encode_prepare -- build the prepared codebook of gain [M][G][K],
+ * shape [M][G][K][d] into `prepared` (>= gsrq_prepared_bytes(s) bytes,
+ * 256-byte aligned).  The codebook is copied: later changes to gain/shape
+ * need a new prepare.  A header records M, G, d and K.
+ */
+gsrq_status gsrq_encode_prepare(const gsrq_shape* s, const float* gain, const float* shape,
+                                void* prepared, size_t bytes, void* stream);
+
+/*
+ * gsrq_encode_prepared -- gsrq_encode (same codes, residual and index
+ * agreement) with the tables and codebook of a prepared codebook; no
+ * workspace.  M <= 8 stages.  The kernel checks the header against s: a
+ * buffer not prepared for this shape (or not prepared at all) gives code
+ * fields of all ones and a NaN residual instead of plausible codes.
+ */
+gsrq_status gsrq_encode_prepared(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype,
+                                 int64_t ldx, const void* prepared, uint32_t* codes,
+                                 float* residual, void* stream);
+
+/*
  * gsrq_decode -- reconstruction as the sum over the first M_use stages of
  * gain[m][g][k] * shape[m][g][k][:] (Sec. 3; prefix decoding, Sec. 1): each
  * stage's codeword is rounded to float32 and the stages are summed in

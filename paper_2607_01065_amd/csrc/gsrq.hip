@@ -378,9 +378,30 @@ __global__ void seed_kernel(const T* __restrict__ Xt, int64_t N, int d, int K,
 }
 
 // Operand tiles for ncb codebooks into a table (used by multi-stage encode).
+// Header of a prepared codebook (gsrq_encode_prepare): magic, M, G, d, K,
+// then zeros, and the complement of the magic in the last word.
+constexpr uint32_t PREP_MAGIC = 0x50525147u;
+constexpr int PREP_WORDS = 16;
+struct PrepTag {
+  uint32_t w[PREP_WORDS];
+};
+
+__host__ __device__ inline PrepTag prep_tag(int M, int G, int d, int K) {
+  PrepTag t = {};
+  t.w[0] = PREP_MAGIC;
+  t.w[1] = (uint32_t)M;
+  t.w[2] = (uint32_t)G;
+  t.w[3] = (uint32_t)d;
+  t.w[4] = (uint32_t)K;
+  t.w[PREP_WORDS - 1] = ~PREP_MAGIC;
+  return t;
+}
+
 __global__ void __launch_bounds__(64) tiles_kernel(const float* __restrict__ gain,
                                                    const float* __restrict__ shape, int d, int K,
-                                                   u4* __restrict__ frag, int* __restrict__ sig) {
+                                                   u4* __restrict__ frag, int* __restrict__ sig,
+                                                   uint32_t* __restrict__ tagp, PrepTag tag) {
+  if (tagp && blockIdx.x == 0 && threadIdx.x < PREP_WORDS) tagp[threadIdx.x] = tag.w[threadIdx.x];
   __shared__ float cbg[KMAX];
   __shared__ float cbs[KMAX * DP];
   __shared__ int red;
@@ -825,6 +846,8 @@ struct EncodeArgs {
   int byte_codes;        // b == 8: plain byte stores, else atomic OR
   int lds_codes;         // byte codes of 4 whole subspaces per block: LDS-staged
   int vec_rows;          // d == 8 and 16-byte aligned rows: vector loads
+  const uint32_t* ptag;  // prepared codebook header to check, or null
+  PrepTag etag;          // the header this call expects
 };
 
 // A row's subvector from row-major X, loaded raw (prefetch) and widened
@@ -905,6 +928,38 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
     build_tiles(tl, mg, ms, K, ex0, false, lane);
   }
   const bool lds_codes = a.lds_codes != 0;
+  if (MULTI && a.ptag) {
+    // a prepared codebook whose header does not match this call: every code
+    // field of the block's rows is set to all ones and the residual to NaN
+    bool ok = true;
+#pragma unroll
+    for (int w = 0; w < PREP_WORDS; ++w) ok &= a.ptag[w] == a.etag.w[w];
+    if (!ok) {
+      if (gvalid && lane < 32) {
+        for (int64_t row = row_begin + lane; row < row_end; row += 32) {
+          if (a.codes) {
+            for (int m = 0; m < a.M; ++m) {
+              const int64_t bit = ((int64_t)m * G + g) * a.b;
+              if (a.byte_codes) {
+                ((uint8_t*)(a.codes + row * a.words))[bit / 8] = 0xffu;
+              } else {   // words zeroed beforehand
+                uint32_t* wp = a.codes + row * a.words + bit / 32;
+                const int off = (int)(bit % 32);
+                const uint32_t ones = (1u << a.b) - 1u;
+                atomicOr(wp, ones << off);
+                if (off + a.b > 32) atomicOr(wp + 1, ones >> (32 - off));
+              }
+            }
+          }
+          if (a.residual) {
+            float* dst = a.residual + row * (int64_t)(G * d) + (int64_t)g * d;
+            for (int j = 0; j < d; ++j) dst[j] = __builtin_nanf("");
+          }
+        }
+      }
+      return;   // uniform over the workgroup (every wave reads the same header)
+    }
+  }
   if (!gvalid) {
     // the flush at the end needs every wave at its barrier
     __syncthreads();
@@ -919,6 +974,16 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
     nx.load(X + row * a.ldx + (int64_t)g * d, d);
   };
   fetch(row_begin);
+  // a single stage keeps its tables in registers for every row block
+  if (MULTI && a.M == 1) {
+    const u4* fr = a.frag + (size_t)g * NT * 2 * 64;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      tl.a1[t] = fr[(t * 2 + 0) * 64 + lane];
+      tl.a2[t] = fr[(t * 2 + 1) * 64 + lane];
+    }
+    ex0 = a.sig[g];
+  }
   for (int64_t r0 = row_begin; r0 < row_end; r0 += RB) {
     const int64_t row = r0 + i;
     const bool valid = row < row_end;
@@ -929,7 +994,7 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
     for (int m = 0; m < a.M; ++m) {
       const int cb = m * G + g;
       int ex = ex0;
-      if (MULTI) {
+      if (MULTI && a.M > 1) {
         const u4* fr = a.frag + (size_t)cb * NT * 2 * 64;
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
@@ -1358,10 +1423,29 @@ size_t encode_ws(const gsrq_shape* s) {
          align256((size_t)s->M * G * sizeof(int));
 }
 
+// Layout of a prepared codebook: header, sigma exponents [M G], operand
+// tiles [M G][NT][2][64], then copies of the gains [M][G][K] and shapes
+// [M][G][K][d] it was built from.
+struct PrepLayout {
+  size_t sig, frag, gain, shape, total;
+};
+
+PrepLayout prep_layout(const gsrq_shape* s) {
+  const int64_t ncb = (int64_t)s->M * (s->D / s->d);
+  PrepLayout P;
+  size_t off = 256;
+  P.sig = off; off = align256(off + ncb * sizeof(int));
+  P.frag = off; off = align256(off + ncb * NT * 2 * 64 * sizeof(u4));
+  P.gain = off; off = align256(off + ncb * s->K * sizeof(float));
+  P.shape = off; off = align256(off + ncb * s->K * s->d * sizeof(float));
+  P.total = off;
+  return P;
+}
+
 template <typename T>
 gsrq_status encode_launch(const gsrq_shape* s, const void* X, int64_t ldx, const float* gain,
                           const float* shape, int M, uint32_t* codes, float* residual, void* ws,
-                          hipStream_t st) {
+                          hipStream_t st, const void* prepared = nullptr) {
   EncodeArgs a;
   a.x = X; a.ldx = ldx; a.N = s->N; a.d = s->d; a.K = s->K; a.G = s->D / s->d; a.M = M;
   a.b = log2i(s->K);
@@ -1372,14 +1456,28 @@ gsrq_status encode_launch(const gsrq_shape* s, const void* X, int64_t ldx, const
   a.lds_codes = codes && a.byte_codes && (a.G % ENC_WAVES == 0) && M <= ENC_MAX_STAGES;
   const size_t esz = sizeof(T);
   a.vec_rows = (s->d == 8) && ((uintptr_t)X % 16 == 0) && ((ldx * esz) % 16 == 0);
+  a.ptag = nullptr;
+  a.etag = prep_tag(M, a.G, s->d, s->K);
   gsrq_status e;
+  // prepared codebook: tables and codebook from the buffer, header checked
+  const bool multi = M > 1 || prepared;
+  if (prepared) {
+    const PrepLayout P = prep_layout(s);
+    const char* pb = (const char*)prepared;
+    a.ptag = (const uint32_t*)pb;
+    a.sig = (const int*)(pb + P.sig);
+    a.frag = (const u4*)(pb + P.frag);
+    a.gain = (const float*)(pb + P.gain);
+    a.shape = (const float*)(pb + P.shape);
+  }
   if (codes && !a.byte_codes) {
     if ((e = fill_u32(codes, (size_t)s->N * a.words, 0u, st))) return e;
   }
-  if (M > 1) {
+  if (M > 1 && !prepared) {
     u4* frag = (u4*)ws;
     int* sig = (int*)((char*)ws + align256((size_t)M * a.G * NT * 2 * 64 * sizeof(u4)));
-    tiles_kernel<<<(unsigned)(M * a.G), 64, 0, st>>>(gain, shape, s->d, s->K, frag, sig);
+    tiles_kernel<<<(unsigned)(M * a.G), 64, 0, st>>>(gain, shape, s->d, s->K, frag, sig, nullptr,
+                                                     a.etag);
     if ((e = launch_ok())) return e;
     a.frag = frag;
     a.sig = sig;
@@ -1387,7 +1485,7 @@ gsrq_status encode_launch(const gsrq_shape* s, const void* X, int64_t ldx, const
   dim3 grid((unsigned)((s->N + ENC_CHUNK_ROWS - 1) / ENC_CHUNK_ROWS),
             (unsigned)((a.G + ENC_WAVES - 1) / ENC_WAVES));
   TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
-  if (M > 1) {
+  if (multi) {
     if (a.vec_rows)
       encode_kernel<T, true, true><<<grid, ENC_WAVES * 64, 0, st>>>(a);
     else
@@ -1671,6 +1769,60 @@ gsrq_status gsrq_encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, 
   if (x_dtype == GSRQ_F16)
     return encode_launch<_Float16>(s, X, ldx, gain, shape, s->M, codes, residual, workspace, st);
   return encode_launch<float>(s, X, ldx, gain, shape, s->M, codes, residual, workspace, st);
+}
+
+gsrq_status gsrq_prepared_bytes(const gsrq_shape* s, size_t* bytes) {
+  gsrq_status e = check_shape(s, true);
+  if (e) return e;
+  if (!bytes) return GSRQ_E_ARG;
+  if ((e = check_supported(s))) return e;
+  if (!narrow(s)) return GSRQ_E_UNSUPPORTED;
+  *bytes = prep_layout(s).total;
+  return GSRQ_OK;
+}
+
+gsrq_status gsrq_encode_prepare(const gsrq_shape* s, const float* gain, const float* shape,
+                                void* prepared, size_t bytes, void* stream) {
+  gsrq_status e = check_shape(s, true);
+  if (e) return e;
+  if (!gain || !shape || !prepared) return GSRQ_E_ARG;
+  if (((uintptr_t)prepared & 255) != 0) return GSRQ_E_ARG;
+  if ((e = check_supported(s))) return e;
+  if (!narrow(s)) return GSRQ_E_UNSUPPORTED;
+  const PrepLayout P = prep_layout(s);
+  if (bytes < P.total) return GSRQ_E_WORKSPACE;
+  hipStream_t st = (hipStream_t)stream;
+  char* pb = (char*)prepared;
+  const int64_t ncb = (int64_t)s->M * (s->D / s->d);
+  if (hipMemcpyAsync(pb + P.gain, gain, ncb * s->K * sizeof(float), hipMemcpyDeviceToDevice,
+                     st) != hipSuccess ||
+      hipMemcpyAsync(pb + P.shape, shape, ncb * s->K * s->d * sizeof(float),
+                     hipMemcpyDeviceToDevice, st) != hipSuccess)
+    return GSRQ_E_HIP;
+  tiles_kernel<<<(unsigned)ncb, 64, 0, st>>>((const float*)(pb + P.gain),
+                                             (const float*)(pb + P.shape), s->d, s->K,
+                                             (u4*)(pb + P.frag), (int*)(pb + P.sig),
+                                             (uint32_t*)pb,
+                                             prep_tag(s->M, (int)(s->D / s->d), s->d, s->K));
+  return launch_ok();
+}
+
+gsrq_status gsrq_encode_prepared(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype,
+                                 int64_t ldx, const void* prepared, uint32_t* codes,
+                                 float* residual, void* stream) {
+  gsrq_status e = check_shape(s, true);
+  if (e) return e;
+  if (!X || !prepared || (!codes && !residual)) return GSRQ_E_ARG;
+  if (x_dtype != GSRQ_F32 && x_dtype != GSRQ_F16) return GSRQ_E_ARG;
+  if (ldx < s->D || ((uintptr_t)prepared & 255) != 0) return GSRQ_E_ARG;
+  if ((e = check_supported(s))) return e;
+  if (!narrow(s) || s->M > ENC_MAX_STAGES) return GSRQ_E_UNSUPPORTED;
+  hipStream_t st = (hipStream_t)stream;
+  if (x_dtype == GSRQ_F16)
+    return encode_launch<_Float16>(s, X, ldx, nullptr, nullptr, s->M, codes, residual, nullptr,
+                                   st, prepared);
+  return encode_launch<float>(s, X, ldx, nullptr, nullptr, s->M, codes, residual, nullptr, st,
+                              prepared);
 }
 
 gsrq_status gsrq_decode(const gsrq_shape* s, const uint32_t* codes, int32_t M_use,

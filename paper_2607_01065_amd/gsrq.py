@@ -71,6 +71,13 @@ def load_library(path: str = LIB_PATH):
     lib.gsrq_encode.restype = ctypes.c_int
     lib.gsrq_encode.argtypes = [SP, _vp, ctypes.c_int, ctypes.c_int64, _vp, _vp, _vp, _vp,
                                 _vp, ctypes.c_size_t, _vp]
+    lib.gsrq_prepared_bytes.restype = ctypes.c_int
+    lib.gsrq_prepared_bytes.argtypes = [SP, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gsrq_encode_prepare.restype = ctypes.c_int
+    lib.gsrq_encode_prepare.argtypes = [SP, _vp, _vp, _vp, ctypes.c_size_t, _vp]
+    lib.gsrq_encode_prepared.restype = ctypes.c_int
+    lib.gsrq_encode_prepared.argtypes = [SP, _vp, ctypes.c_int, ctypes.c_int64, _vp, _vp, _vp,
+                                         _vp]
     lib.gsrq_decode.restype = ctypes.c_int
     lib.gsrq_decode.argtypes = [SP, _vp, ctypes.c_int32, _vp, _vp, _vp, ctypes.c_int,
                                 ctypes.c_int64, _vp]
@@ -306,6 +313,54 @@ def encode(X, gain, shape, *, codes=None, residual=False, workspace=None, stream
                          _ptr(shape), _ptr(codes), _ptr(res), _ptr(ws),
                          ws.numel() * ws.element_size(), _stream_handle(stream))
     _check(st, "gsrq_encode")
+    return codes, res
+
+
+@dataclass
+class Prepared:
+    """A prepared codebook (gsrq_encode_prepare): the device buffer and the
+    shape it was built for."""
+    buf: object
+    D: int
+    d: int
+    K: int
+    M: int
+
+
+def prepare_codebook(gain, shape, *, stream=None) -> Prepared:
+    """Prepared codebook of gain [M, G, K], shape [M, G, K, d] (narrow
+    family, d <= 8, K <= 256) for encode_prepared."""
+    torch = _torch()
+    lib = load_library()
+    M, G, K = gain.shape
+    d = shape.shape[-1]
+    _need(gain, "gain", (torch.float32,), gain.device)
+    _need(shape, "shape", (torch.float32,), gain.device, (M, G, K, d))
+    sh = make_shape(1, G * d, d, K, M)
+    n = ctypes.c_size_t(0)
+    _check(lib.gsrq_prepared_bytes(ctypes.byref(sh), ctypes.byref(n)), "gsrq_prepared_bytes")
+    buf = torch.empty(n.value, dtype=torch.uint8, device=gain.device)
+    _check(lib.gsrq_encode_prepare(ctypes.byref(sh), _ptr(gain), _ptr(shape), _ptr(buf), n.value,
+                                   _stream_handle(stream)), "gsrq_encode_prepare")
+    return Prepared(buf, G * d, d, K, M)
+
+
+def encode_prepared(X, prep: Prepared, *, codes=None, residual=False, stream=None):
+    """encode() with a prepared codebook (no operand-table build per call)."""
+    torch = _torch()
+    lib = load_library()
+    N, D, ldx = _rows(X)
+    if D != prep.D:
+        raise ValueError("X does not match the prepared codebook's vector length")
+    sh = make_shape(N, D, prep.d, prep.K, prep.M)
+    W = int(lib.gsrq_code_words(ctypes.byref(sh)))
+    if codes is None:
+        codes = torch.empty((N, max(W, 1)), dtype=torch.int32, device=X.device)
+    _need(codes, "codes", (torch.int32, torch.uint32), X.device, (N, max(W, 1)))
+    res = torch.empty((N, D), dtype=torch.float32, device=X.device) if residual else None
+    st = lib.gsrq_encode_prepared(ctypes.byref(sh), _ptr(X), _dtype_code(X), ldx, _ptr(prep.buf),
+                                  _ptr(codes), _ptr(res), _stream_handle(stream))
+    _check(st, "gsrq_encode_prepared")
     return codes, res
 
 

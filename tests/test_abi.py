@@ -146,6 +146,30 @@ def test_encode_decode_validation_before_any_hip_call():
     assert dec(dt=5) == B.GSRQ_E_ARG
 
 
+def test_prepared_encode_validation_before_any_hip_call():
+    lib = B.load_library()
+    sh = B.make_shape(100, 64, 8, 256, 2)
+    n = ctypes.c_size_t(0)
+    assert lib.gsrq_prepared_bytes(ctypes.byref(sh), ctypes.byref(n)) == B.GSRQ_OK
+    # header, sigma, 16 KiB of tables and the codebook copy per codebook
+    assert n.value >= 2 * 8 * (16384 + 256 * 9 * 4)
+    wide = B.make_shape(100, 256, 128, 256, 1)
+    assert lib.gsrq_prepared_bytes(ctypes.byref(wide), ctypes.byref(n)) == B.GSRQ_E_UNSUPPORTED
+    D = DUMMY
+    assert lib.gsrq_encode_prepare(ctypes.byref(sh), None, D, D * 16, 1 << 30, None) == B.GSRQ_E_ARG
+    assert lib.gsrq_encode_prepare(ctypes.byref(sh), D, D, D * 16 + 8, 1 << 30, None) == B.GSRQ_E_ARG
+    assert lib.gsrq_encode_prepare(ctypes.byref(sh), D, D, D * 16, 10, None) == B.GSRQ_E_WORKSPACE
+    assert lib.gsrq_encode_prepared(ctypes.byref(sh), D, B.GSRQ_F16, 63, D * 16, D, None,
+                                    None) == B.GSRQ_E_ARG                      # ldx < D
+    assert lib.gsrq_encode_prepared(ctypes.byref(sh), D, B.GSRQ_F16, 64, D * 16, None, None,
+                                    None) == B.GSRQ_E_ARG                      # no output
+    assert lib.gsrq_encode_prepared(ctypes.byref(sh), D, 5, 64, D * 16, D, None,
+                                    None) == B.GSRQ_E_ARG                      # dtype
+    deep = B.make_shape(100, 64, 8, 256, 9)
+    assert lib.gsrq_encode_prepared(ctypes.byref(deep), D, B.GSRQ_F16, 64, D * 16, D, None,
+                                    None) == B.GSRQ_E_UNSUPPORTED              # M > 8
+
+
 def test_row_weights_validation_before_any_hip_call():
     lib = B.load_library()
     f = lib.gsrq_row_weights

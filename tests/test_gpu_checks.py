@@ -282,3 +282,68 @@ def test_attn_workspace_contents_do_not_leak_into_outputs():
     torch.cuda.synchronize()
     assert torch.all(torch.isfinite(dirty))
     assert torch.equal(dirty, clean)
+
+
+@pytest.mark.parametrize("N,D,d,K,M,dtype", [(1, 1024, 8, 256, 1, np.float16),
+                                             (8, 1024, 8, 256, 1, np.float16),
+                                             (64, 1024, 8, 256, 2, np.float32),
+                                             (2049, 256, 8, 256, 3, np.float16),
+                                             (777, 24, 4, 16, 2, np.float32)])
+def test_prepared_encode_matches_encode(N, D, d, K, M, dtype):
+    """gsrq_encode_prepared gives gsrq_encode's codes and residual bit for
+    bit (the same operand tables, built once), including the append sizes
+    1, 8 and 64."""
+    say("prepared encode", N, D, d, K, M, dtype.__name__)
+    X, w, seeds = synth.small_case(max(N, 2 * K), D, d, K, M, seed=31, dtype=dtype)
+    G = D // d
+    rng = np.random.default_rng(31)
+    sh = rng.standard_normal((M, G, K, d))
+    sh /= np.linalg.norm(sh, axis=-1, keepdims=True)
+    gain = (np.median(np.linalg.norm(X.astype(np.float64).reshape(-1, G, d), axis=-1))
+            * rng.uniform(0.3, 1.5, size=(M, G, K)) / (1 + np.arange(M))[:, None, None])
+    gd, sd = _dev(gain.astype(np.float32)), _dev(sh.astype(np.float32))
+    prep = B.prepare_codebook(gd, sd)
+    Xd = _dev(X[:N])
+    c1, r1 = B.encode(Xd, gd, sd, residual=True)
+    c2, r2 = B.encode_prepared(Xd, prep, residual=True)
+    torch.cuda.synchronize()
+    assert torch.equal(c1, c2) and torch.equal(r1, r2)
+    k = O.unpack_codes(c2.cpu().numpy().view(np.uint32), M, G, K)
+    R = X[:N].astype(np.float64)
+    for m in range(M):
+        for g in range(G):
+            cols = slice(g * d, (g + 1) * d)
+            check_assignment(R[:, cols], gain[m, g].astype(np.float32), sh[m, g].astype(np.float32),
+                             k[:, m, g], what=f"prepared m={m} g={g}")
+            kk = k[:, m, g]
+            R[:, cols] -= gain[m, g].astype(np.float32)[kk, None].astype(np.float64) * \
+                sh[m, g].astype(np.float32)[kk].astype(np.float64)
+
+
+def test_prepared_encode_checks_its_header():
+    """A buffer prepared for another shape, or never prepared, gives all-ones
+    code fields and a NaN residual instead of plausible codes."""
+    import ctypes
+    N, D, d, K = 100, 64, 8, 256
+    X, _, _ = synth.small_case(2 * K, D, d, K, 1, seed=32, dtype=np.float16)
+    rng = np.random.default_rng(32)
+    sh = rng.standard_normal((1, D // d, K, d))
+    sh /= np.linalg.norm(sh, axis=-1, keepdims=True)
+    gd = _dev(np.full((1, D // d, K), 2.0, np.float32))
+    sd = _dev(sh.astype(np.float32))
+    prep = B.prepare_codebook(gd, sd)
+    lib = B.load_library()
+    Xd = _dev(X[:N])
+    for what, buf, K2 in (("other K", prep.buf, 128),
+                          ("never prepared", torch.zeros_like(prep.buf), K)):
+        s = B.make_shape(N, D, d, K2, 1)
+        W = B.code_words(N, D, d, K2, 1)
+        codes = torch.zeros((N, W), dtype=torch.int32, device="cuda")
+        res = torch.zeros((N, D), dtype=torch.float32, device="cuda")
+        st = lib.gsrq_encode_prepared(ctypes.byref(s), Xd.data_ptr(), B.GSRQ_F16, D,
+                                      buf.data_ptr(), codes.data_ptr(), res.data_ptr(), None)
+        assert st == B.GSRQ_OK, what
+        torch.cuda.synchronize()
+        k = O.unpack_codes(codes.cpu().numpy().view(np.uint32), 1, D // d, K2)
+        assert np.all(k == K2 - 1), what            # every code field all ones
+        assert torch.all(torch.isnan(res)), what
