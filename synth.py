@@ -247,3 +247,13 @@ def attn_case(B: int, cap: int, lens, Hkv: int, GQ: int, seed: int = 0, q_dtype=
     return dict(k_codes=np.ascontiguousarray(k_codes), v_codes=np.ascontiguousarray(v_codes),
                 lens=np.asarray(lens, np.int32), k_gain=k_gain, k_shape=k_shape,
                 v_gain=v_gain, v_shape=v_shape, q=q, Hkv=Hkv, GQ=GQ)
+
+
+def gaussian_case(N: int, D: int, K: int, seed: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+    """The random-normal inputs of Sec. 6.1: X [N, D] float32 with i.i.d.
+    rows x ~ N(0, I_D), and K distinct seed row indices [K] drawn after X
+    from the same stream (one stream per (seed, N, D, K))."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, N, D, K, 61])))
+    X = rng.standard_normal((N, D), dtype=np.float32)
+    seeds = rng.choice(N, size=K, replace=False).astype(np.int64)
+    return X, seeds

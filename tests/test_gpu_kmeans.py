@@ -8,7 +8,7 @@ GSKM tests: indices follow the margin rule, updates are compared
 teacher-forced (the oracle's update applied to the GPU's own assignment and
 previous centroids) to 1e-5 relative, and a free-running comparison is made
 only on planted clusters, where no near-tie can flip the trajectory.  The
-last test checks the ordering the paper reports on x ~ N(0, I) (GSKM above
+last tests check the ordering the paper reports on x ~ N(0, I) (GSKM above
 K-means in cosine, below it in gain error), computed from the GPU's own
 codebooks, encodings and reconstructions.
 """
@@ -132,29 +132,50 @@ def test_kmeans_free_running_planted(d, K, G):
         assert np.allclose(res[:, cols], res_ref, atol=1e-5)
 
 
-@pytest.mark.parametrize("d,K", [(128, 256)])
-def test_gskm_vs_kmeans_ordering_on_gaussian(d, K):
-    """Sec. 6.1, random-normal sweep (N = 10,000 samples of N(0, I_d)): at
-    d = 128, K = 256 GSKM's reconstruction has higher cosine similarity and
-    lower gain error than K-means' (float64 oracle on the same inputs: cosine
-    0.333 against 0.316, gain error 7.53 against 7.72).  Both are trained,
-    encoded and decoded on the GPU from the same seed rows; the metrics of
-    Sec. 6.1 come from the oracle's metric definitions.  With this reading
-    the two methods are within noise of each other for small K on isotropic
-    data, so the ordering is asserted only where its gap is clear."""
-    rng = _rng(33, d, K)
-    N = 10000
-    X = rng.standard_normal((N, d)).astype(np.float32)
-    seeds = rng.choice(N, size=(1, K), replace=False).astype(np.int32)
+def _gaussian_metrics(d, K, seed=0):
+    """Sec. 6.1 metrics of K-means and GSKM on N = 10,000 samples of
+    N(0, I_d) (synth.gaussian_case), both trained (T = 100, stop rule),
+    encoded and decoded on the GPU from the same seed rows."""
+    X, seeds = synth.gaussian_case(10000, d, K, seed=seed)
     Xd = to_dev(X)
     out = {}
     for name, km in (("gskm", False), ("kmeans", True)):
-        r = B.train_stage(Xd, d, K, 20, seed_rows=seeds, kmeans=km)
+        r = B.train_stage(Xd, d, K, 100, seed_rows=seeds[None].astype(np.int32), kmeans=km)
         gain, shape = r.gain[None].contiguous(), r.shape[None].contiguous()
         codes, _ = B.encode(Xd, gain, shape)
         xh = B.decode(codes, gain, shape, d, out_dtype=torch.float32)
         torch.cuda.synchronize()
         out[name] = O.metrics(X.astype(np.float64), xh.cpu().numpy().astype(np.float64))
+    return out
+
+
+@pytest.mark.parametrize("d,K,gap", [(128, 256, 0.04), (256, 1024, 0.10), (64, 2048, 0.03)])
+def test_gskm_vs_kmeans_ordering_on_gaussian(d, K, gap):
+    """Sec. 6.1, random-normal sweeps: where a codeword serves a few to a
+    few tens of samples, GSKM's reconstruction has clearly higher cosine
+    similarity and lower gain error than K-means'.  The full sweep (D at
+    K = 2048, K at D = 256, three seeds, with float64-oracle spot checks)
+    is tests/sweep_gaussian.py; its cosine gaps at (256, 1024) and
+    (64, 2048) are +14.5% (+14.2 .. +15.1 over seeds) and +5.6%
+    (+5.2 .. +5.9); at (128, 256) the float64 oracle gives +6.1% on this
+    seed (cosine 0.3320 against 0.3128).  The asserted gaps sit below the
+    measured ones by more than their spread over seeds."""
+    out = _gaussian_metrics(d, K)
     say("fig4", d, K, out)
-    assert out["gskm"]["cos"] > out["kmeans"]["cos"]
-    assert out["gskm"]["gain_err"] < out["kmeans"]["gain_err"]
+    g, k = out["gskm"], out["kmeans"]
+    assert g["cos"] > (1.0 + gap) * k["cos"]
+    assert g["gain_err"] < k["gain_err"]
+    assert g["mse"] < k["mse"]
+
+
+def test_gskm_and_kmeans_tie_at_small_k_on_gaussian():
+    """The capacity sweep's other end (D = 256, K = 8, about 1,250 samples
+    per codeword): the two methods are within 1% of each other in every
+    metric, in either direction, which is this reading's departure from the
+    paper's largest gap at small K (each centroid then averages so many
+    isotropic samples that its direction is equally poor for both)."""
+    out = _gaussian_metrics(256, 8)
+    say("fig4 tie", out)
+    for key in ("mse", "gain_err", "cos"):
+        a, b = out["gskm"][key], out["kmeans"][key]
+        assert abs(a - b) <= 0.01 * abs(b), key
