@@ -524,16 +524,20 @@ __device__ __forceinline__ double update_codeword(bool init, bool kmeans, const 
   if (!init && kmeans) {
     if (W > 0.0) {
       double c[DP], cn = 0.0, s2 = 0.0;
+      // one float64 division per quotient vector, then products (within
+      // an ulp of dividing every element)
+      const double iw = 1.0 / W;
 #pragma unroll
       for (int j = 0; j < DP; ++j) {
-        c[j] = s[8 + j] / W;
+        c[j] = s[8 + j] * iw;
         cn = fma(c[j], c[j], cn);
         s2 = fma(s[8 + j], s[8 + j], s2);
       }
-      term += s2 / W;
+      term += s2 * iw;
       cn = sqrt(cn);
+      const double icn = cn > 0.0 ? 1.0 / cn : 0.0;
 #pragma unroll
-      for (int j = 0; j < DP; ++j) sn[j] = cn > 0.0 ? c[j] / cn : 0.0;
+      for (int j = 0; j < DP; ++j) sn[j] = c[j] * icn;
       gnew = cn;
     }
     return term;
@@ -555,8 +559,9 @@ __device__ __forceinline__ double update_codeword(bool init, bool kmeans, const 
       for (int j = 0; j < DP; ++j) mn = fma(s[j], s[j], mn);
       mn = sqrt(mn);
       if (mn > SHAPE_KEEP_REL * W) {
+        const double imn = 1.0 / mn;
 #pragma unroll
-        for (int j = 0; j < DP; ++j) sn[j] = s[j] / mn;
+        for (int j = 0; j < DP; ++j) sn[j] = s[j] * imn;
       }
     }
     double pr = 0.0;
@@ -663,11 +668,13 @@ assign_accumulate_kernel(AssignArgs a) {
   __shared__ u4 tiles_l[NT * 2 * 64];
   __shared__ double objw[TRAIN_WAVES];
   __shared__ uint16_t codes_l[TRAIN_CHUNK_MAX];   // this chunk's new assignment
-  __shared__ int changed, red;
+  __shared__ int changed, red, next_blk;
 
   const int g = blockIdx.y;
   const int chunk = blockIdx.x;
-  if (a.done[g]) return;
+  // a stopped subspace returns; the test waits until this launch's first
+  // loads are in flight, so their latency overlaps that of the flag
+  const int stopped = a.done[g];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K;
@@ -713,8 +720,9 @@ assign_accumulate_kernel(AssignArgs a) {
 #pragma unroll
     for (int j = 0; j < DP; ++j) sold[j] = so[j < d ? j : 0];
     const float gold = init ? a.seednorm[(size_t)g * K + kmine] : a.old_gain[(size_t)g * K + kmine];
-    if (tid == 0) red = 0;
     sum_partials<TRAIN_WAVES * 64>(a, g, acc);   // acc holds the dense sums for now
+    if (stopped) return;   // uniform over the workgroup
+    if (tid == 0) red = 0;
     __syncthreads();
     double term = 0.0;
     if (tid < KMAX) {
@@ -744,11 +752,15 @@ assign_accumulate_kernel(AssignArgs a) {
     __syncthreads();
     ex = sigma_exp(__int_as_float(red));
   } else {
+    if (stopped) return;   // uniform over the workgroup
     ex = load_codebook(a.gain + (size_t)g * K, a.shape + (size_t)g * K * d, d, K,
                        MODE == MODE_INIT, cbg, cbs, &red);
   }
   for (int e = tid; e < KMAX * ACC_LDS; e += blockDim.x) acc[e] = 0.0;
-  if (tid == 0) changed = a.force_changed;
+  if (tid == 0) {
+    changed = a.force_changed;
+    next_blk = TRAIN_WAVES;   // wave w starts with block w
+  }
   // operand tiles built once per workgroup (one (tile, lane) entry per
   // thread), then read by every wave into its registers
   for (int e = tid; e < NT * 64; e += blockDim.x) {
@@ -766,11 +778,25 @@ assign_accumulate_kernel(AssignArgs a) {
     tl.a1[t] = tiles_l[(2 * t) * 64 + lane];
     tl.a2[t] = tiles_l[(2 * t + 1) * 64 + lane];
   }
-
+  // the tile loads complete here, once: left pending into the loop, they
+  // made the compiler wait for every LDS operation in flight (this wave's
+  // float64 accumulations of the previous block) before each block's MFMAs
+  lgkm_wait_all();
 
   double obj = 0.0;
   bool any_changed = false;
-  for (int rb = wave; rb < nblk; rb += TRAIN_WAVES) {
+  // Blocks are handed out one at a time from an LDS counter, claimed one
+  // block ahead so their rows can be prefetched.  A static round-robin split
+  // left the youngest wave of each SIMD running alone for the last third of
+  // the launch (the oldest wave issues first and finishes first); claimed
+  // blocks keep all waves of a SIMD busy until the chunk is done.
+  auto claim = [&]() {
+    int v = 0;
+    if (lane == 0) v = atomicAdd(&next_blk, 1);
+    return __builtin_amdgcn_readfirstlane(v);
+  };
+  int rb_next = wave < nblk ? claim() : nblk;
+  for (int rb = wave; rb < nblk;) {
     const int r = rb * RB + i;
     const bool valid = r < nrows;
     float x[8];
@@ -778,7 +804,8 @@ assign_accumulate_kernel(AssignArgs a) {
     const u4 raw = nx.raw16();
     const float wcur = has_w ? nw : 1.f;
     const uint16_t old = nold;
-    if (rb + TRAIN_WAVES < nblk) fetch(rb + TRAIN_WAVES);
+    if (rb_next < nblk) fetch(rb_next);
+    const int rb_after = rb_next < nblk ? claim() : nblk;
 
     h8 b1, b2;
     float rr, ss;
@@ -789,7 +816,12 @@ assign_accumulate_kernel(AssignArgs a) {
     int kstar = reduce_rows(key, h, dhat);
     need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
     const unsigned long long fb = __ballot(valid && need_exact && h == 0);
-    if (fb) exact_rows(fb, x, d, DP, K, cbg, cbs, MODE == MODE_INIT, kstar);
+    if (fb) {
+      exact_rows(fb, x, d, DP, K, cbg, cbs, MODE == MODE_INIT, kstar);
+      // the rare path's LDS reads end here, so the common path's
+      // accumulations below are not held up waiting for them
+      lgkm_wait_all();
+    }
     if (kstar >= K) kstar = K - 1;   // only discarded rows can get here
     if (valid) {
       // lane half 0 adds w y (y = x / ||x||) and W, half 1 adds w x and the
@@ -815,6 +847,8 @@ assign_accumulate_kernel(AssignArgs a) {
         codes_l[r] = (uint16_t)kstar;
       }
     }
+    rb = rb_next;
+    rb_next = rb_after;
   }
   // wave sums of the objective and changed flag
 #pragma unroll

@@ -68,6 +68,10 @@ __device__ __forceinline__ int sigma_exp(float maxg) {
   return e;
 }
 
+// Wait until this wave's LDS (and scalar memory) operations have completed:
+// s_waitcnt lgkmcnt(0), leaving the vector-memory and export counters alone.
+__device__ __forceinline__ void lgkm_wait_all() { __builtin_amdgcn_s_waitcnt(0xc07f); }
+
 __device__ __forceinline__ int min3i(int a, int b, int c) {
   int r;
   asm volatile("v_min3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));

@@ -52,6 +52,10 @@ def load_library(path: str = LIB_PATH):
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built; run `python -c 'import __graft_entry__ as g; g.build()'`")
+    # torch first: the library then binds to the HIP runtime torch ships and
+    # uses, instead of loading a second runtime that cannot see torch's
+    # device memory
+    _torch()
     lib = ctypes.CDLL(path)
     SP = ctypes.POINTER(Shape)
     lib.gsrq_status_string.restype = ctypes.c_char_p
