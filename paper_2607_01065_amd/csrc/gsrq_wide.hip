@@ -31,6 +31,7 @@
 //    residual passes between stages through HBM (a d = 128 residual does
 //    not fit in registers next to the operands).
 #include <algorithm>
+#include <type_traits>
 
 #include "gsrq_common.h"
 #include "gsrq_wide.h"
@@ -60,6 +61,11 @@ enum { W_TRAIN = 0, W_ENCODE = 1 };
 __host__ __device__ constexpr int w_pairs(int C) { return (C + 1) / 2; }
 // Fragments per tile: HI_p, LO_p for every pair, then the bias fragment.
 __host__ __device__ constexpr int w_frags(int C) { return 2 * w_pairs(C) + 1; }
+// Row blocks a wave scores per round: two for the streamed single pass
+// while their operands fit the register budget (d <= 128), else one.
+__host__ __device__ constexpr int w_row_blocks(int C, bool resident, bool sp, bool ind) {
+  return (sp && !ind && !resident && C <= 16) ? 2 : 1;
+}
 // Staged u4 per thread of a streamed chunk: a chunk holds at least one whole
 // tile (33 fragments at d = 256 exceed the W_STREAM_BYTES budget).
 __host__ __device__ constexpr int w_sreg(int C) {
@@ -355,6 +361,37 @@ __device__ __forceinline__ void w_make_b(const WRaw<T, P>& raw, int d, bool vali
   bias = h ? (u4){0u, 0u, 0u, 0u} : bias_row(sr, rr);
 }
 
+// Elements [e0, e0 + 8) of a float32 row as float (zero past d or for an
+// invalid row): two vector loads when vec (d a multiple of 8, 16-byte
+// aligned), else element loads with clamped indices.
+__device__ __forceinline__ void w_row_group(const float* xp, int e0, int d, bool vec, bool valid,
+                                            float (&xv)[8]) {
+  const bool live = valid && e0 < d;
+  if (vec) {
+    const int q = e0 < d ? e0 : 0;   // a lone last group (d = 8): read group 0
+    const f4 a = *(const f4*)(xp + q), b = *(const f4*)(xp + q + 4);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      xv[u] = live ? a[u] : 0.f;
+      xv[4 + u] = live ? b[u] : 0.f;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int e = e0 + j;
+      xv[j] = (valid && e < d) ? xp[e < d ? e : 0] : 0.f;
+    }
+  }
+}
+__device__ __forceinline__ void w_row_group(const _Float16* xp, int e0, int d, bool vec,
+                                            bool valid, float (&xv)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int e = e0 + j;
+    xv[j] = (valid && e < d) ? (float)xp[e < d ? e : 0] : 0.f;
+  }
+}
+
 // The same operands loaded straight from memory (no prefetch): fewer live
 // registers for wide rows, where a workgroup scores a single round.
 template <typename T, int P>
@@ -363,7 +400,7 @@ __device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bo
                                          bool& need_exact, float& eD) {
   constexpr bool F16 = sizeof(T) == 2;
   int sr;
-  if (F16) {
+  if constexpr (F16) {
     typedef _Float16 h2 __attribute__((ext_vector_type(2)));
     float ss = 0.f;
 #pragma unroll
@@ -394,7 +431,68 @@ __device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bo
     need_exact = ex > 15 || ex < -14 || !(rr < 32768.f);
     // single-pass error bound in D units: 2^-10 g ||x|| 2^SA / sigma, g <= sigma
     eD = ldexpf(sqrtf(ss), SA - 10) * (1.f + 0x1p-9f);
-  } else {
+  } else if constexpr (P <= 8) {
+    // pass 1: the row's scale, from vector loads (element loads came back a
+    // few at a time and made this the slowest part of a float32-row launch)
+    float mx = 0.f, ss = 0.f;
+    // the vector / element choice is made once per pass, so that a pass's
+    // loads share one basic block and are issued together
+    auto scale_pass = [&](auto vec_c) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        float xv[8];
+        w_row_group(xp, 16 * p + 8 * h, d, decltype(vec_c)::value, valid, xv);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          mx = fmaxf(mx, fabsf(xv[j]));
+          ss = fmaf(xv[j], xv[j], ss);
+        }
+        // at most four groups' loads in flight (bounds the registers)
+        if (p % 4 == 3) asm volatile("" ::: "memory");
+      }
+    };
+    if (vec) scale_pass(std::true_type{});
+    else scale_pass(std::false_type{});
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    ss += __shfl_xor(ss, 32);
+    int er = 0;
+    frexpf(mx, &er);
+    // a row far below the codebook's scale is scaled relative to sigma
+    // instead (keeps 2^sr in float16 range; b and rr shrink with it, D stays
+    // a positive multiple of the distance); rows so small that b would
+    // leave float16's normal range are re-scored exactly
+    const int er_min = ex + SB - 15;
+    const bool tiny = er < er_min - 12;
+    er = er > er_min ? er : er_min;
+    sr = ex - er + SB;
+    rr = ldexpf(ss, SB - ex - er);
+    need_exact = tiny || !(mx > 0.f) || sr < -14 || !(rr < 32768.f);
+    // single-pass error bound in D units: 2^-9 g ||x|| 2^(SA+SB) / (sigma rho)
+    eD = ldexpf(sqrtf(ss), SA + SB - 9 - er) * (1.f + 0x1p-9f);
+    // pass 2 re-reads the row (cache hits): holding pass 1's values across
+    // the reduction would take 8 P registers per row block
+    asm volatile("" ::: "memory");
+    auto split_pass = [&](auto vec_c) {
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        float xv[8];
+        w_row_group(xp, 16 * p + 8 * h, d, decltype(vec_c)::value, valid, xv);
+        _Float16 hi[8], lo[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float v = ldexpf(xv[j], SB - er);
+          hi[j] = (_Float16)v;
+          lo[j] = (_Float16)(v - (float)hi[j]);
+        }
+        bx[p] = pack_h8(hi);
+        blo[p] = pack_h8(lo);
+        if (p % 4 == 3) asm volatile("" ::: "memory");
+      }
+    };
+    if (vec) split_pass(std::true_type{});
+    else split_pass(std::false_type{});
+    } else {
+    // wider rows (d = 256): element loads keep the registers of a pass low
     // pass 1: the row's scale; pass 2 re-reads the (cached) row and splits it
     float mx = 0.f, ss = 0.f;
 #pragma unroll
@@ -439,7 +537,7 @@ __device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bo
       bx[p] = pack_h8(hi);
       blo[p] = pack_h8(lo);
     }
-  }
+    }
   rr = fminf(rr, 32768.f);
   sr = sr < -14 ? -14 : (sr > 15 ? 15 : sr);
   bias = h ? (u4){0u, 0u, 0u, 0u} : bias_row(sr, rr);
@@ -476,6 +574,28 @@ __device__ __forceinline__ f16v w_tile_sp(const u4* ta, const u4 (&bx)[P], u4 bi
   for (int p = 0; p < P; ++p)
     acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[p * 64]), as_h8(bx[p]), acc, 0, 0, 0);
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[P * 64]), as_h8(bias), acc, 0, 0, 0);
+}
+
+// Single-pass distances of one tile for two row blocks: each fragment is
+// read from LDS once and feeds both blocks' MFMA chains, which halves the
+// LDS traffic per MFMA (with one block per wave the fragment reads alone
+// would take the whole LDS bandwidth at full MFMA rate).
+template <int P>
+__device__ __forceinline__ void w_tile_sp2(const u4* ta, const u4 (&bx0)[P], const u4 (&bx1)[P],
+                                           u4 bias0, u4 bias1, f16v& c0, f16v& c1) {
+  f16v a0 = {}, a1 = {};
+  // fragment p + 1 is read while fragment p's two MFMAs run (one read
+  // register set alone would expose every LDS read's latency)
+  h8 f = as_h8(ta[0]);
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    const h8 fn = as_h8(ta[(p + 1) * 64]);
+    a0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(f, as_h8(bx0[p]), a0, 0, 0, 0);
+    a1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(f, as_h8(bx1[p]), a1, 0, 0, 0);
+    f = fn;
+  }
+  c0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(f, as_h8(bias0), a0, 0, 0, 0);
+  c1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(f, as_h8(bias1), a1, 0, 0, 0);
 }
 
 // Smallest packed key of a tile: the low 4 bits of each distance carry its
@@ -637,10 +757,14 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   constexpr bool F16 = sizeof(T) == 2;
   constexpr int P = w_pairs(C);
   constexpr int QU = SP ? P + 1 : w_frags(C);
-  // two tiles' MFMA chains in flight, and the next round's row prefetched,
-  // while the row operands are small enough to leave registers for both
-  constexpr bool PAIR_TILES = C <= 4 || SP;
+  // R row blocks per wave and round (two for the streamed single pass:
+  // every fragment read from LDS feeds two MFMAs); with one, two tiles'
+  // MFMA chains in flight, and the next round's row prefetched, while the
+  // row operands are small enough to leave registers for both
+  constexpr int R = w_row_blocks(C, RESIDENT, SP, IND);
+  constexpr bool PAIR_TILES = (C <= 4 || SP) && R == 1;
   constexpr bool PREFETCH = C <= 2 && !IND;
+  static_assert(!PREFETCH || R == 1, "the row prefetch holds one row block");
 
   int g, rc, slice = 0;
   {
@@ -695,14 +819,16 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
 
   double obj = 0.0;
   bool any_changed = false;
-  // this lane's row of round rd (valid: below N, or within the list)
-  auto row_of = [&](int rd, bool& valid) -> int64_t {
+  // this lane's row of round rd, row block r of the wave (valid: below N,
+  // or within the list)
+  auto row_of = [&](int rd, int r, bool& valid) -> int64_t {
     if (IND) {
       const int idx = (rc + rd * a.nwg) * W_ROWS + wave * RB + i;
       valid = idx < hcnt;
       return a.hrows[(size_t)g * a.N + (valid ? idx : 0)];
     }
-    const int64_t row = ((int64_t)rc * a.rounds + rd) * W_ROWS + (int64_t)wave * RB + i;
+    const int64_t row = ((int64_t)rc * a.rounds + rd) * (W_ROWS * R) +
+                        (int64_t)(wave * R + r) * RB + i;
     valid = row < a.N;
     return row;
   };
@@ -712,51 +838,69 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   WRaw<T, P> raw;
   if (PREFETCH) {
     bool v0;
-    raw.load(row_ptr(row_of(0, v0)), d, vec, h);
+    raw.load(row_ptr(row_of(0, 0, v0)), d, vec, h);
   }
   for (int rd = 0; rd < nrounds; ++rd) {
-    bool valid;
-    const int64_t row = row_of(rd, valid);
-    const T* xp = row_ptr(row);
-    u4 bx[P], blo[P], bias;
-    float rr, eD;
-    bool need_exact;
-    if (PREFETCH)
-      w_make_b<T, P>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact, eD);
-    else
-      w_make_b_direct<T, P>(xp, d, vec, valid, ex, h, bx, blo, bias, rr, need_exact, eD);
+    bool valid[R];
+    int64_t row[R];
+    const T* xp[R];
+    u4 bx[R][P], blo[R][P], bias[R];
+    float rr[R], eD[R];
+    bool need_exact[R];
+    auto make_block = [&](int r) {
+      row[r] = row_of(rd, r, valid[r]);
+      xp[r] = row_ptr(row[r]);
+      if (PREFETCH)
+        w_make_b<T, P>(raw, d, valid[r], ex, h, bx[r], blo[r], bias[r], rr[r], need_exact[r],
+                       eD[r]);
+      else
+        w_make_b_direct<T, P>(xp[r], d, vec, valid[r], ex, h, bx[r], blo[r], bias[r], rr[r],
+                              need_exact[r], eD[r]);
+    };
+    make_block(0);
+    if constexpr (R == 2) make_block(1);
     // the next round's row is fetched while this one is scored
     if (PREFETCH && rd + 1 < nrounds) {
       bool v1;
-      raw.load(row_ptr(row_of(rd + 1, v1)), d, vec, h);
+      raw.load(row_ptr(row_of(rd + 1, 0, v1)), d, vec, h);
     }
 
-    int best = 0x7fffffff, bt = 0, second = 0x7fffffff;
+    int best[R], bt[R], second[R];
+    best[0] = 0x7fffffff, bt[0] = 0, second[0] = 0x7fffffff;
+    if constexpr (R == 2) best[R - 1] = 0x7fffffff, bt[R - 1] = 0, second[R - 1] = 0x7fffffff;
     // scores of tiles t and t + 1 (when present) into the running best
     auto score = [&](const u4* ta, int t, bool pair) {
-      if (SP) {
+      if constexpr (SP && R == 2) {
+        f16v c0, c1;
+        w_tile_sp2<P>(ta, bx[0], bx[R - 1], bias[0], bias[R - 1], c0, c1);
+        int b0, s0, b1, s1;
+        w_tile_key2(c0, b0, s0);
+        w_take2(b0, s0, t, best[0], bt[0], second[0]);
+        w_tile_key2(c1, b1, s1);
+        w_take2(b1, s1, t, best[R - 1], bt[R - 1], second[R - 1]);
+      } else if constexpr (SP) {
         if (pair) {
-          const f16v c0 = w_tile_sp<P>(ta, bx, bias);
-          const f16v c1 = w_tile_sp<P>(ta + QU * 64, bx, bias);
+          const f16v c0 = w_tile_sp<P>(ta, bx[0], bias[0]);
+          const f16v c1 = w_tile_sp<P>(ta + QU * 64, bx[0], bias[0]);
           int b0, s0, b1, s1;
           w_tile_key2(c0, b0, s0);
-          w_take2(b0, s0, t, best, bt, second);
+          w_take2(b0, s0, t, best[0], bt[0], second[0]);
           w_tile_key2(c1, b1, s1);
-          w_take2(b1, s1, t + 1, best, bt, second);
+          w_take2(b1, s1, t + 1, best[0], bt[0], second[0]);
         } else {
-          const f16v c0 = w_tile_sp<P>(ta, bx, bias);
+          const f16v c0 = w_tile_sp<P>(ta, bx[0], bias[0]);
           int b0, s0;
           w_tile_key2(c0, b0, s0);
-          w_take2(b0, s0, t, best, bt, second);
+          w_take2(b0, s0, t, best[0], bt[0], second[0]);
         }
       } else {
-        const f16v c0 = w_tile<F16, P>(ta, bx, blo, bias);
+        const f16v c0 = w_tile<F16, P>(ta, bx[0], blo[0], bias[0]);
         if (pair) {
-          const f16v c1 = w_tile<F16, P>(ta + QU * 64, bx, blo, bias);
-          w_take(w_tile_key(c0), t, best, bt);
-          w_take(w_tile_key(c1), t + 1, best, bt);
+          const f16v c1 = w_tile<F16, P>(ta + QU * 64, bx[0], blo[0], bias[0]);
+          w_take(w_tile_key(c0), t, best[0], bt[0]);
+          w_take(w_tile_key(c1), t + 1, best[0], bt[0]);
         } else {
-          w_take(w_tile_key(c0), t, best, bt);
+          w_take(w_tile_key(c0), t, best[0], bt[0]);
         }
       }
     };
@@ -790,112 +934,118 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       }
     }
 
-    // combine the two lane halves of each row: smallest distance, then the
-    // lowest codeword index
-    int kstar;
-    float dhat;
-    bool ambiguous = false;
-    {
-      const int j = best & 15;
-      const int kidx = bt * CW + (j >> 2) * 8 + h * 4 + (j & 3);
-      const int hv = best >> 4;
-      const auto sh = __builtin_amdgcn_permlane32_swap(hv, hv, false, false);
-      const auto sk = __builtin_amdgcn_permlane32_swap(kidx, kidx, false, false);
-      const long long v0 = (long long)(int)sh[0] * 4294967296ll + (long long)(unsigned)sk[0];
-      const long long v1 = (long long)(int)sh[1] * 4294967296ll + (long long)(unsigned)sk[1];
-      const long long v = v0 < v1 ? v0 : v1;
-      dhat = __int_as_float((int)(v >> 32) << 4);
-      kstar = (int)(v & 0xffffffffll);
-      if (SP) {
-        // second smallest over both halves: med3(b0, b1, min(s0, s1)); a
-        // row is decided when it lies beyond twice the error bound (the
-        // single-pass bound, float32 accumulation and key truncation)
-        // The bound of a codeword scales with its gain (eD is the bound at
-        // g = sigma): the best's own gain on its side, the codebook's
-        // largest gain for every other codeword.
-        const auto sb = __builtin_amdgcn_permlane32_swap(best, best, false, false);
-        const auto ss2 = __builtin_amdgcn_permlane32_swap(second, second, false, false);
-        const int srow = med3i(sb[0], sb[1], min(ss2[0], ss2[1]));
-        const float sv = __int_as_float(srow & ~15);
-        const float gb = a.unit_gain ? 1.f : gcb[kstar < K ? kstar : K - 1];
-        const float gx = a.unit_gain ? 1.f : a.gmin[a.G + (cb - a.fcb0)];
-        const float md = ldexpf(eD * (gb + gx), -ex) * 1.0625f +
-                         ldexpf(dhat + ldexpf(rr, SA + 1), -15) + 0x1p-3f;
-        ambiguous = !(sv - dhat > md);
-      }
-    }
-    if (IND) {
-      // this slice's best into the row's running minimum; the finish kernel
-      // decides the row (64-bit keys: the distance key with its sign bit
-      // flipped, so signed order is unsigned order, then the codeword)
-      if (valid && h == 0) {
-        const size_t idx = (size_t)g * a.N + (size_t)((rc + rd * a.nwg) * W_ROWS + wave * RB + i);
-        const uint32_t hv = (uint32_t)(__float_as_int(dhat) >> 4) ^ 0x80000000u;
-        atomicMin(a.hbest + idx, ((unsigned long long)hv << 32) | (uint32_t)kstar);
-        if (slice == 0) a.hrr[idx] = need_exact ? -1.f : rr;
-      }
-      continue;
-    }
-    need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
-    // rows the key cannot decide go to the subspace's list for the exact
-    // kernel, which also writes their outputs; here they are skipped
-    const bool defer = valid && need_exact;
-    {
-      const unsigned long long fb = __ballot(defer && h == 0);
-      if (fb) {
-        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(fb >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)fb, 0u));
-        int base = 0;
-        if (lane == 0) base = atomicAdd(a.xcount + g, __popcll(fb));
-        base = __shfl(base, 0);
-        if (defer && h == 0) a.xrows[(size_t)g * a.N + base + rank] = (int)row;
-      }
-    }
-    // single pass: rows within the error bound go to the hi/lo pass
-    const bool relist = SP && valid && !defer && ambiguous;
-    if (SP) {
-      const unsigned long long fb = __ballot(relist && h == 0);
-      if (fb) {
-        const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(fb >> 32),
-                                                   __builtin_amdgcn_mbcnt_lo((uint32_t)fb, 0u));
-        int base = 0;
-        if (lane == 0) base = atomicAdd(a.hcount + g, __popcll(fb));
-        base = __shfl(base, 0);
-        if (relist && h == 0) {
-          a.hrows[(size_t)g * a.N + base + rank] = (int)row;
-          a.hbest[(size_t)g * a.N + base + rank] = ~0ull;
+    // per row block: combine the two lane halves of each row, then the
+    // mode's outputs
+    auto finish_block = [&](int r) {
+      // combine the two lane halves of each row: smallest distance, then the
+      // lowest codeword index
+      int kstar;
+      float dhat;
+      bool ambiguous = false;
+      {
+        const int j = best[r] & 15;
+        const int kidx = bt[r] * CW + (j >> 2) * 8 + h * 4 + (j & 3);
+        const int hv = best[r] >> 4;
+        const auto sh = __builtin_amdgcn_permlane32_swap(hv, hv, false, false);
+        const auto sk = __builtin_amdgcn_permlane32_swap(kidx, kidx, false, false);
+        const long long v0 = (long long)(int)sh[0] * 4294967296ll + (long long)(unsigned)sk[0];
+        const long long v1 = (long long)(int)sh[1] * 4294967296ll + (long long)(unsigned)sk[1];
+        const long long v = v0 < v1 ? v0 : v1;
+        dhat = __int_as_float((int)(v >> 32) << 4);
+        kstar = (int)(v & 0xffffffffll);
+        if (SP) {
+          // second smallest over both halves: med3(b0, b1, min(s0, s1)); a
+          // row is decided when it lies beyond twice the error bound (the
+          // single-pass bound, float32 accumulation and key truncation)
+          // The bound of a codeword scales with its gain (eD is the bound at
+          // g = sigma): the best's own gain on its side, the codebook's
+          // largest gain for every other codeword.
+          const auto sb = __builtin_amdgcn_permlane32_swap(best[r], best[r], false, false);
+          const auto ss2 = __builtin_amdgcn_permlane32_swap(second[r], second[r], false, false);
+          const int srow = med3i(sb[0], sb[1], min(ss2[0], ss2[1]));
+          const float sv = __int_as_float(srow & ~15);
+          const float gb = a.unit_gain ? 1.f : gcb[kstar < K ? kstar : K - 1];
+          const float gx = a.unit_gain ? 1.f : a.gmin[a.G + (cb - a.fcb0)];
+          const float md = ldexpf(eD[r] * (gb + gx), -ex) * 1.0625f +
+                           ldexpf(dhat + ldexpf(rr[r], SA + 1), -15) + 0x1p-3f;
+          ambiguous = !(sv - dhat > md);
         }
       }
-    }
-    if (kstar >= K) kstar = K - 1;   // deferred rows and rows past N only
-    const bool own = valid && !defer && !relist;
+      if (IND) {
+        // this slice's best into the row's running minimum; the finish kernel
+        // decides the row (64-bit keys: the distance key with its sign bit
+        // flipped, so signed order is unsigned order, then the codeword)
+        if (valid[r] && h == 0) {
+          const size_t idx = (size_t)g * a.N + (size_t)((rc + rd * a.nwg) * W_ROWS + wave * RB + i);
+          const uint32_t hv = (uint32_t)(__float_as_int(dhat) >> 4) ^ 0x80000000u;
+          atomicMin(a.hbest + idx, ((unsigned long long)hv << 32) | (uint32_t)kstar);
+          if (slice == 0) a.hrr[idx] = need_exact[r] ? -1.f : rr[r];
+        }
+        return;
+      }
+      need_exact[r] = need_exact[r] || !(dhat <= ldexpf(rr[r], SA + 1)) || kstar >= K;
+      // rows the key cannot decide go to the subspace's list for the exact
+      // kernel, which also writes their outputs; here they are skipped
+      const bool defer = valid[r] && need_exact[r];
+      {
+        const unsigned long long fb = __ballot(defer && h == 0);
+        if (fb) {
+          const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(fb >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)fb, 0u));
+          int base = 0;
+          if (lane == 0) base = atomicAdd(a.xcount + g, __popcll(fb));
+          base = __shfl(base, 0);
+          if (defer && h == 0) a.xrows[(size_t)g * a.N + base + rank] = (int)row[r];
+        }
+      }
+      // single pass: rows within the error bound go to the hi/lo pass
+      const bool relist = SP && valid[r] && !defer && ambiguous;
+      if (SP) {
+        const unsigned long long fb = __ballot(relist && h == 0);
+        if (fb) {
+          const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(fb >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((uint32_t)fb, 0u));
+          int base = 0;
+          if (lane == 0) base = atomicAdd(a.hcount + g, __popcll(fb));
+          base = __shfl(base, 0);
+          if (relist && h == 0) {
+            a.hrows[(size_t)g * a.N + base + rank] = (int)row[r];
+            a.hbest[(size_t)g * a.N + base + rank] = ~0ull;
+          }
+        }
+      }
+      if (kstar >= K) kstar = K - 1;   // deferred rows and rows past N only
+      const bool own = valid[r] && !defer && !relist;
 
-    const float gk = a.unit_gain ? 1.f : gcb[kstar];
-    const float* sk = scb + (size_t)kstar * d;
-    if (MODE == W_TRAIN) {
-      if (own && h == 0) {
-        uint16_t* ap = a.assign + (size_t)g * a.N + row;
-        if (*ap != (uint16_t)kstar) any_changed = true;
-        *ap = (uint16_t)kstar;
+      const float gk = a.unit_gain ? 1.f : gcb[kstar];
+      const float* sk = scb + (size_t)kstar * d;
+      if (MODE == W_TRAIN) {
+        if (own && h == 0) {
+          uint16_t* ap = a.assign + (size_t)g * a.N + row[r];
+          if (*ap != (uint16_t)kstar) any_changed = true;
+          *ap = (uint16_t)kstar;
+        }
+        if (a.obj) {
+          // weighted distortion of this assignment under the scoring codebook;
+          // each lane half sums half of the elements
+          const int jb = h * (d / 2);
+          float dist = w_residual<T>(xp[r] + jb, sk + jb, gk, d / 2, rvec, nullptr);
+          dist += __shfl_xor(dist, 32);
+          if (own && h == 0) obj += (double)(a.w ? a.w[row[r]] : 1.f) * (double)dist;
+        }
+      } else {
+        if (own && h == 0 && a.codes)
+          w_put_code(a.codes + row[r] * a.words, ((int64_t)a.m * a.G + g) * a.b, a.b, kstar);
+        if (own && a.res_out) {
+          // each lane half writes its half of the row's residual
+          const int jb = h * (d / 2);
+          float* dst = a.res_out + row[r] * ((int64_t)a.G * d) + (int64_t)g * d + jb;
+          w_residual<T>(xp[r] + jb, sk + jb, gk, d / 2, rvec, dst);
+        }
       }
-      if (a.obj) {
-        // weighted distortion of this assignment under the scoring codebook;
-        // each lane half sums half of the elements
-        const int jb = h * (d / 2);
-        float dist = w_residual<T>(xp + jb, sk + jb, gk, d / 2, rvec, nullptr);
-        dist += __shfl_xor(dist, 32);
-        if (own && h == 0) obj += (double)(a.w ? a.w[row] : 1.f) * (double)dist;
-      }
-    } else {
-      if (own && h == 0 && a.codes)
-        w_put_code(a.codes + row * a.words, ((int64_t)a.m * a.G + g) * a.b, a.b, kstar);
-      if (own && a.res_out) {
-        // each lane half writes its half of the row's residual
-        const int jb = h * (d / 2);
-        float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d + jb;
-        w_residual<T>(xp + jb, sk + jb, gk, d / 2, rvec, dst);
-      }
-    }
+    };
+    finish_block(0);
+    if constexpr (R == 2) finish_block(1);
   }
   if (MODE == W_TRAIN && !IND) {
 #pragma unroll
@@ -1952,7 +2102,9 @@ WLayout w_score_layout(const gsrq_shape* s, size_t x_elt, bool f16rows, bool hp 
   const size_t used = (size_t)L.tiles * L.Qu * 64 * sizeof(u4);
   // single pass: two workgroups per CU share 160 KiB of LDS
   L.resident = used <= (size_t)(L.sp ? W_SP_RESIDENT_BYTES : W_RESIDENT_BYTES);
-  const int64_t row_rounds = (s->N + W_ROWS - 1) / W_ROWS;
+  // rows per workgroup round: W_ROWS per row block a wave scores at once
+  const int64_t rows_round = (int64_t)W_ROWS * w_row_blocks(L.C, L.resident, L.sp, false);
+  const int64_t row_rounds = (s->N + rows_round - 1) / rows_round;
   if (L.resident) {
     // enough rounds per workgroup to amortise the table load, while
     // keeping about four workgroups per CU in the grid
