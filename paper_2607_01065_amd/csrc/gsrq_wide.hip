@@ -690,12 +690,36 @@ __device__ __forceinline__ f4 w_load4(const _Float16* p) {
 // a row), written to dst when dst is non-null; returns ||r||^2 (float32).
 // vec: n % 4 == 0 and x, s, dst 16-byte (float16 x: 8-byte) aligned, so
 // every access is a vector access; otherwise element by element.
-template <typename T>
+template <typename T, bool BATCH = false>
 __device__ __forceinline__ float w_residual(const T* xp, const float* sk, float gk, int n,
                                             bool vec, float* dst) {
   float dist = 0.f;
   if (vec) {
-    for (int j = 0; j < n; j += 4) {
+    int j0 = 0;
+    if constexpr (BATCH) {
+      // eight vector loads of each operand in flight per batch (one load
+      // pair per iteration waited for each pair in turn: the encode
+      // epilogue's slowest part)
+      for (; j0 + 32 <= n; j0 += 32) {
+        f4 x[8], sv[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          x[u] = w_load4(xp + j0 + 4 * u);
+          sv[u] = *(const f4*)(sk + j0 + 4 * u);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          f4 r;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            r[q] = fmaf(-gk, sv[u][q], x[u][q]);
+            dist = fmaf(r[q], r[q], dist);
+          }
+          if (dst) *(f4*)(dst + j0 + 4 * u) = r;
+        }
+      }
+    }
+    for (int j = j0; j < n; j += 4) {
       const f4 x = w_load4(xp + j), sv = *(const f4*)(sk + j);
       f4 r;
 #pragma unroll
@@ -1029,7 +1053,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
           // weighted distortion of this assignment under the scoring codebook;
           // each lane half sums half of the elements
           const int jb = h * (d / 2);
-          float dist = w_residual<T>(xp[r] + jb, sk + jb, gk, d / 2, rvec, nullptr);
+          float dist = w_residual<T, (P <= 8)>(xp[r] + jb, sk + jb, gk, d / 2, rvec, nullptr);
           dist += __shfl_xor(dist, 32);
           if (own && h == 0) obj += (double)(a.w ? a.w[row[r]] : 1.f) * (double)dist;
         }
@@ -1040,7 +1064,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
           // each lane half writes its half of the row's residual
           const int jb = h * (d / 2);
           float* dst = a.res_out + row[r] * ((int64_t)a.G * d) + (int64_t)g * d + jb;
-          w_residual<T>(xp[r] + jb, sk + jb, gk, d / 2, rvec, dst);
+          w_residual<T, (P <= 8)>(xp[r] + jb, sk + jb, gk, d / 2, rvec, dst);
         }
       }
     };
