@@ -1684,6 +1684,111 @@ __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
   for (int e = tid; e < n; e += W_THREADS) out[e] = wacc[e];
 }
 
+// Weighted sums of eqs. 6-8 from the rows bucketed by codeword (d >= 64):
+// one wave per codeword walks the codeword's members in bucket order and
+// keeps the sums in float64 registers, written once as the single partial
+// of the subspace (no LDS atomics: in bucket order consecutive members share
+// a codeword, so atomics into one LDS slice all hit the same addresses).
+// Lane groups of 16 lanes take one member each (four members side by side,
+// W_SMEMBERS per group in flight), lane i of a group holding elements
+// [E i, E i + E) of the row (E = d / 16, vector loads); a member's norm is
+// a 16-lane reduction, and the four groups' sums are added once at the end.
+// The per-member products are formed as in w_acc_members.
+constexpr int W_SMEMBERS = 4;
+template <typename T> struct WVec;
+template <> struct WVec<_Float16> {
+  // E consecutive float16 elements (E a multiple of 4) as float
+  template <int E> static __device__ __forceinline__ void load(const _Float16* p, float (&v)[E]) {
+    typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+    for (int q = 0; q < E / 4; ++q) {
+      const h4 x = ((const h4*)p)[q];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[4 * q + u] = (float)x[u];
+    }
+  }
+};
+template <> struct WVec<float> {
+  template <int E> static __device__ __forceinline__ void load(const float* p, float (&v)[E]) {
+#pragma unroll
+    for (int q = 0; q < E / 4; ++q) {
+      const f4 x = ((const f4*)p)[q];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[4 * q + u] = x[u];
+    }
+  }
+};
+
+template <typename T, int E>
+__global__ void __launch_bounds__(256) w_accumulate_sorted_kernel(WAccArgs a) {
+  const int g = blockIdx.y;
+  if (a.done && a.done[g]) return;
+  const int lane = threadIdx.x & 63, grp = lane >> 4, li = lane & 15;
+  // the wave's codeword, in a scalar register (its bucket bounds are then
+  // scalar loads)
+  const int k = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (k >= a.K) return;   // uniform per wave
+  const int d = a.d, S = 2 * d + 2;
+  const int* bo = a.boff + (size_t)g * (a.K + 1);
+  const int m0 = bo[k], m1 = bo[k + 1];
+  const int* srt = a.sorted + (size_t)g * a.N;
+  const T* X = (const T*)a.x + (int64_t)g * d + E * li;
+  double sy[E], sx[E], wsum = 0.0;
+#pragma unroll
+  for (int e = 0; e < E; ++e) sy[e] = sx[e] = 0.0;
+  constexpr int STEP = 4 * W_SMEMBERS;   // members per batch and wave
+  for (int m = m0; m < m1; m += STEP) {
+    float xv[W_SMEMBERS][E], wt[W_SMEMBERS];
+    // member m + 4 u + grp of the batch (past the bucket's end a slot
+    // re-reads the last member and adds nothing)
+#pragma unroll
+    for (int u = 0; u < W_SMEMBERS; ++u) {
+      const int64_t row = srt[min(m + 4 * u + grp, m1 - 1)];
+      WVec<T>::template load<E>(X + row * a.ldx, xv[u]);
+      wt[u] = a.w ? a.w[row] : 1.f;
+    }
+#pragma unroll
+    for (int u = 0; u < W_SMEMBERS; ++u) {
+      float ss = xv[u][E - 1] * xv[u][E - 1];
+#pragma unroll
+      for (int e = E - 2; e >= 0; --e) ss = fmaf(xv[u][e], xv[u][e], ss);
+#pragma unroll
+      for (int off = 8; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+      if (m + 4 * u + grp < m1) {
+        const float inv = __builtin_amdgcn_rcpf(__builtin_amdgcn_sqrtf(ss) + Y_EPS);
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          sy[e] += (double)(xv[u][e] * (wt[u] * inv));
+          sx[e] += (double)(xv[u][e] * wt[u]);
+        }
+        wsum += (double)wt[u];
+      }
+    }
+  }
+  // the four lane groups' sums (members of the same codeword)
+#pragma unroll
+  for (int off = 16; off < 64; off <<= 1) {
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      sy[e] += __shfl_xor(sy[e], off);
+      sx[e] += __shfl_xor(sx[e], off);
+    }
+    wsum += __shfl_xor(wsum, off);
+  }
+  if (grp == 0) {
+    double* out = a.part + ((size_t)g * a.rchunks * a.K + k) * S;
+#pragma unroll
+    for (int e = 0; e < E; ++e) {
+      out[E * li + e] = sy[e];
+      out[d + E * li + e] = sx[e];
+    }
+    if (li == 0) {
+      out[2 * d] = wsum;
+      out[2 * d + 1] = (double)(m1 - m0);
+    }
+  }
+}
+
 struct WFinArgs {
   int d, K, G, rchunks, T;
   int t;                  // iteration (1-based); 0 for the initial gains
@@ -2270,6 +2375,7 @@ struct WAccLayout {
   int64_t rows_per_chunk;
   size_t lds;
   bool bucket;          // rows bucketed by codeword before accumulating
+  bool sorted_sums;     // bucketed sums by w_accumulate_sorted_kernel
 };
 
 WAccLayout w_acc_layout(const gsrq_shape* s) {
@@ -2290,6 +2396,13 @@ WAccLayout w_acc_layout(const gsrq_shape* s) {
   // several slices: bucket the rows by codeword once per pass instead of
   // every slice scanning every row (the histogram is K ints of LDS)
   A.bucket = A.slices > 1 && s->K <= W_BUCKET_KMAX;
+  // bucketed rows with d >= 64: one wave per codeword sums in registers
+  // (w_accumulate_sorted_kernel), one partial per subspace
+  A.sorted_sums = A.bucket && s->d >= 64 && s->d <= 256;
+  if (A.sorted_sums) {
+    A.rchunks = 1;
+    A.rows_per_chunk = s->N;
+  }
   return A;
 }
 
@@ -2482,10 +2595,23 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
             assign, s->N, K, aa.done, (int*)(base + W.boff), (int*)(base + W.sorted));
         if ((e2 = launch_ok())) return e2;
       }
-      if (e4)
+      // the register kernel reads E consecutive elements with vector loads:
+      // 16-byte aligned rows (else the LDS kernel, with the same single
+      // row chunk)
+      const bool svec = ((uintptr_t)X % 16 == 0) && ((ldx * (int64_t)sizeof(T)) % 16 == 0);
+      if (A.sorted_sums && svec) {
+        const dim3 sgrid((unsigned)((K + 3) / 4), (unsigned)G);
+        if (d == 64)
+          w_accumulate_sorted_kernel<T, 4><<<sgrid, 256, 0, st>>>(aa);
+        else if (d == 128)
+          w_accumulate_sorted_kernel<T, 8><<<sgrid, 256, 0, st>>>(aa);
+        else
+          w_accumulate_sorted_kernel<T, 16><<<sgrid, 256, 0, st>>>(aa);
+      } else if (e4) {
         w_accumulate_kernel<T, 4><<<agrid, W_THREADS, A.lds, st>>>(aa);
-      else
+      } else {
         w_accumulate_kernel<T, 2><<<agrid, W_THREADS, A.lds, st>>>(aa);
+      }
     }
     if ((e2 = launch_ok())) return e2;
     {
