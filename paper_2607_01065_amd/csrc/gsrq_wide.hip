@@ -1520,31 +1520,59 @@ struct WAccArgs {
   const int* boff;         // [G][K + 1] bucket offsets into sorted
 };
 
-// Rows of each subspace bucketed by codeword (a counting sort): boff[g][k]
-// is the first position of codeword k's members in sorted[g], boff[g][K] =
-// N.  One workgroup per subspace; the histogram and the bucket cursors live
-// in LDS (K ints).  The order within a bucket is that of LDS atomics (the
-// sums built from it are then exact up to float64 rounding order).
-__global__ void __launch_bounds__(1024) w_bucket_kernel(const uint16_t* __restrict__ assign,
-                                                        int64_t N, int K,
-                                                        const int* __restrict__ done,
-                                                        int* __restrict__ boff,
-                                                        int* __restrict__ sorted) {
+// Rows of each subspace bucketed by codeword, a counting sort in three
+// launches over row chunks of bch rows (one workgroup per chunk and
+// subspace, so the whole GPU takes part; w_bucket_rows sizes the chunks):
+//   count:   cnt[g][c][k] = members of codeword k in chunk c (LDS histogram);
+//   scan:    boff[g][k] = first position of codeword k's members in
+//            sorted[g] (boff[g][K] = N), and cnt[g][c][k] becomes the first
+//            position of chunk c's members of k;
+//   scatter: every row of chunk c goes to the next position of its codeword.
+// Buckets hold their members chunk by chunk; within a chunk the order is
+// that of LDS atomics (the sums built from it are then exact up to float64
+// rounding order).
+constexpr int W_BCH = 2048;
+// Rows per bucketing chunk: W_BCH, doubled while the scan's chunks x K
+// entries per subspace exceed 32768 (the scan is one workgroup per subspace).
+inline int64_t w_bucket_rows(int64_t N, int K) {
+  int64_t bch = W_BCH;
+  while (bch < N && ((N + bch - 1) / bch) * (int64_t)K > 32768) bch *= 2;
+  return bch;
+}
+__global__ void __launch_bounds__(256) w_bucket_count_kernel(const uint16_t* __restrict__ assign,
+                                                             int64_t N, int K, int64_t bch,
+                                                             const int* __restrict__ done,
+                                                             int* __restrict__ cnt) {
   extern __shared__ int hist[];
+  const int g = blockIdx.y, c = blockIdx.x;
+  if (done && done[g]) return;
+  const int tid = threadIdx.x;
+  for (int k = tid; k < K; k += 256) hist[k] = 0;
+  __syncthreads();
+  const uint16_t* asg = assign + (size_t)g * N;
+  const int64_t r1 = min(N, (int64_t)(c + 1) * bch);
+  for (int64_t r = (int64_t)c * bch + tid; r < r1; r += 256) atomicAdd(&hist[asg[r]], 1);
+  __syncthreads();
+  int* out = cnt + ((size_t)g * gridDim.x + c) * K;
+  for (int k = tid; k < K; k += 256) out[k] = hist[k];
+}
+
+__global__ void __launch_bounds__(1024) w_bucket_scan_kernel(int64_t N, int K, int chunks,
+                                                             const int* __restrict__ done,
+                                                             int* __restrict__ cnt,
+                                                             int* __restrict__ boff) {
   __shared__ int wsum[16];
   const int g = blockIdx.x;
   if (done && done[g]) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const uint16_t* asg = assign + (size_t)g * N;
-  for (int k = tid; k < K; k += 1024) hist[k] = 0;
-  __syncthreads();
-  for (int64_t r = tid; r < N; r += 1024) atomicAdd(&hist[asg[r]], 1);
-  __syncthreads();
-  // exclusive scan: thread tid owns bins [b, e)
+  int* cg = cnt + (size_t)g * chunks * K;
+  // thread tid owns bins [b, e): their totals over the chunks, then an
+  // exclusive scan of the totals over the workgroup
   const int per = (K + 1023) / 1024;
   const int b = min(K, tid * per), e = min(K, b + per);
   int tot = 0;
-  for (int k = b; k < e; ++k) tot += hist[k];
+  for (int k = b; k < e; ++k)
+    for (int c = 0; c < chunks; ++c) tot += cg[(size_t)c * K + k];
   int inc = tot;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
@@ -1557,15 +1585,33 @@ __global__ void __launch_bounds__(1024) w_bucket_kernel(const uint16_t* __restri
   for (int w2 = 0; w2 < wave; ++w2) base += wsum[w2];
   int* bo = boff + (size_t)g * (K + 1);
   for (int k = b; k < e; ++k) {
-    const int c = hist[k];
     bo[k] = base;
-    hist[k] = base;
-    base += c;
+    for (int c = 0; c < chunks; ++c) {
+      const int n = cg[(size_t)c * K + k];
+      cg[(size_t)c * K + k] = base;
+      base += n;
+    }
   }
   if (tid == 0) bo[K] = (int)N;
+}
+
+__global__ void __launch_bounds__(256) w_bucket_scatter_kernel(const uint16_t* __restrict__ assign,
+                                                               int64_t N, int K, int64_t bch,
+                                                               const int* __restrict__ done,
+                                                               const int* __restrict__ cnt,
+                                                               int* __restrict__ sorted) {
+  extern __shared__ int cur[];
+  const int g = blockIdx.y, c = blockIdx.x;
+  if (done && done[g]) return;
+  const int tid = threadIdx.x;
+  const int* in = cnt + ((size_t)g * gridDim.x + c) * K;
+  for (int k = tid; k < K; k += 256) cur[k] = in[k];
   __syncthreads();
+  const uint16_t* asg = assign + (size_t)g * N;
   int* srt = sorted + (size_t)g * N;
-  for (int64_t r = tid; r < N; r += 1024) srt[atomicAdd(&hist[asg[r]], 1)] = (int)r;
+  const int64_t r1 = min(N, (int64_t)(c + 1) * bch);
+  for (int64_t r = (int64_t)c * bch + tid; r < r1; r += 256)
+    srt[atomicAdd(&cur[asg[r]], 1)] = (int)r;
 }
 
 // Batched member loop of the accumulation: members [0, n), member `it` is
@@ -2408,7 +2454,7 @@ WAccLayout w_acc_layout(const gsrq_shape* s) {
 
 struct WTrainWs {
   size_t frag, gmin, xcount, xrows, xchanged, xobj, hcount, hrows, hbest, hrr, sig, part,
-      changed, obj, assign, done, iters, seednorm, seeds, sorted, boff, total;
+      changed, obj, assign, done, iters, seednorm, seeds, sorted, boff, bcnt, total;
 };
 
 WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
@@ -2440,6 +2486,9 @@ WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
   W.seeds = off; off = align256(off + (size_t)G * s->K * sizeof(int32_t));
   W.sorted = off; off = align256(off + (A.bucket ? (size_t)G * s->N * sizeof(int) : 0));
   W.boff = off; off = align256(off + (A.bucket ? (size_t)G * (s->K + 1) * sizeof(int) : 0));
+  W.bcnt = off;
+  const int64_t bch = w_bucket_rows(s->N, s->K);
+  off = align256(off + (A.bucket ? (size_t)G * ((s->N + bch - 1) / bch) * s->K * sizeof(int) : 0));
   W.total = off;
   return W;
 }
@@ -2591,8 +2640,15 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
     {
       TimedLaunch tl(GSRQ_KERNEL_ACCUMULATE, st);
       if (A.bucket) {
-        w_bucket_kernel<<<G, 1024, (size_t)K * sizeof(int), st>>>(
-            assign, s->N, K, aa.done, (int*)(base + W.boff), (int*)(base + W.sorted));
+        const int64_t bch = w_bucket_rows(s->N, K);
+        const int bchunks = (int)((s->N + bch - 1) / bch);
+        int* bcnt = (int*)(base + W.bcnt);
+        w_bucket_count_kernel<<<dim3(bchunks, G), 256, (size_t)K * sizeof(int), st>>>(
+            assign, s->N, K, bch, aa.done, bcnt);
+        w_bucket_scan_kernel<<<G, 1024, 0, st>>>(s->N, K, bchunks, aa.done, bcnt,
+                                                 (int*)(base + W.boff));
+        w_bucket_scatter_kernel<<<dim3(bchunks, G), 256, (size_t)K * sizeof(int), st>>>(
+            assign, s->N, K, bch, aa.done, bcnt, (int*)(base + W.sorted));
         if ((e2 = launch_ok())) return e2;
       }
       // the register kernel reads E consecutive elements with vector loads:
