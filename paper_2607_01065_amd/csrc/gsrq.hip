@@ -44,8 +44,9 @@ constexpr int WAVES_PER_SIMD = 3;      // 168 VGPRs: operand tiles stay in regis
 constexpr int TRAIN_CHUNK_MAX = 16384;  // rows of one (chunk, subspace) workgroup, at most
 constexpr int TRAIN_CHUNK_MIN = 2048;   // and at least (unless N is smaller)
 constexpr int TRAIN_SLOTS = 256;        // workgroups resident at once (one per CU)
-constexpr int ENC_WAVES = 4;           // one subspace per wave, three workgroups per CU
-constexpr int ENC_CHUNK_ROWS = 1024;
+constexpr int ENC_SUBS = 4;            // subspaces per encode workgroup
+constexpr int ENC_WAVES = 12;          // three waves per subspace, one workgroup per CU
+constexpr int ENC_CODES_WORDS = 16384; // LDS-staged code words: stages x chunk rows, at most
 constexpr int ENC_MAX_STAGES = 8;      // stages staged in LDS by one encode launch
 constexpr int KEY_BITS = 7;               // (tile, slot) bits packed into a key
 
@@ -882,6 +883,7 @@ struct EncodeArgs {
   int vec_rows;          // d == 8 and 16-byte aligned rows: vector loads
   const uint32_t* ptag;  // prepared codebook header to check, or null
   PrepTag etag;          // the header this call expects
+  int64_t chunk_rows;    // rows per workgroup (a multiple of RB)
 };
 
 // A row's subvector from row-major X, loaded raw (prefetch) and widened
@@ -920,46 +922,60 @@ template <typename T, bool VEC> struct RowRaw {
   }
 };
 
-// Stage-fused encoder: one subspace per wave; the residual of a 32-row block
-// stays in registers through all M stages.  A single-stage launch keeps the
-// wave's codebook in LDS and its operand tiles in registers for the whole
+// Stage-fused encoder: a workgroup encodes a chunk of rows for ENC_SUBS
+// consecutive subspaces, three waves per subspace; the residual of a 32-row
+// block stays in registers through all M stages.  The waves of a subspace
+// claim its blocks one at a time from an LDS counter, one block ahead (a
+// static split left the youngest wave of each SIMD running alone at the
+// end of every workgroup).  A single-stage launch keeps the subspaces'
+// codebooks in LDS and each wave's operand tiles in registers for the whole
 // launch; a multi-stage launch reloads each stage's tiles from a table.
 template <typename T, bool MULTI, bool VEC>
 __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(EncodeArgs a) {
   constexpr bool F16IN = sizeof(T) == 2;
-  __shared__ float cbl[MULTI ? 1 : ENC_WAVES * KMAX * (DP + 1)];
-  // byte codes of this block, [stage][row][wave]; written out at the end so
-  // that no global store sits in the loop (stores share vmcnt with loads)
-  __shared__ uint32_t codes_l[(MULTI ? ENC_MAX_STAGES : 1) * ENC_CHUNK_ROWS];
+  __shared__ float cbl[MULTI ? 1 : ENC_SUBS * KMAX * (DP + 1)];
+  // byte codes of this chunk, [stage][row][subspace]; written out at the end
+  // so that no global store sits in the loop (stores share vmcnt with loads)
+  __shared__ uint32_t codes_l[ENC_CODES_WORDS];
+  __shared__ int next_blk[ENC_SUBS];
   const int lane = wave_lane(), wave = threadIdx.x >> 6;
-  const int g = blockIdx.y * ENC_WAVES + wave;
+  const int sg = wave % ENC_SUBS;   // this wave's subspace within the group
+  const int g = blockIdx.y * ENC_SUBS + sg;
   const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K, G = a.G;
   const bool gvalid = g < G;
-  const int64_t row_begin = (int64_t)blockIdx.x * ENC_CHUNK_ROWS;
-  const int64_t row_end = row_begin + ENC_CHUNK_ROWS < a.N ? row_begin + ENC_CHUNK_ROWS : a.N;
-  float* mg = cbl + (MULTI ? 0 : wave * KMAX * (DP + 1));   // gains [KMAX]
-  float* ms = mg + KMAX;                                      // shapes [KMAX][DP]
+  const int64_t row_begin = (int64_t)blockIdx.x * a.chunk_rows;
+  const int64_t row_end = row_begin + a.chunk_rows < a.N ? row_begin + a.chunk_rows : a.N;
+  const int nblk = (int)((row_end - row_begin + RB - 1) / RB);
+  float* mg = cbl + (MULTI ? 0 : sg * KMAX * (DP + 1));   // gains [KMAX]
+  float* ms = mg + KMAX;                                    // shapes [KMAX][DP]
+  // waves sg, sg + ENC_SUBS, ... start with blocks 0, 1, ...
+  if (threadIdx.x < ENC_SUBS) next_blk[threadIdx.x] = ENC_WAVES / ENC_SUBS;
   Tiles tl;
   int ex0 = 0;
   if (!MULTI) {
-    // this wave's codebook into its LDS slice; sigma from the max gain
-    float m = 0.f;
+    // the group's codebooks into LDS (the first wave of each subspace);
+    // sigma from the subspace's largest gain
     const int gc = gvalid ? g : 0;
-    for (int k = lane; k < KMAX; k += 64) {
-      float gv, sv[DP];
-      read_codeword(a.gain + (size_t)gc * K, a.shape + (size_t)gc * K * d, d, K, k, false, gv,
-                    sv);
-      mg[k] = gv;
-      m = fmaxf(m, gv);
+    if (wave < ENC_SUBS) {
+      for (int k = lane; k < KMAX; k += 64) {
+        float gv, sv[DP];
+        read_codeword(a.gain + (size_t)gc * K, a.shape + (size_t)gc * K * d, d, K, k, false, gv,
+                      sv);
+        mg[k] = gv;
 #pragma unroll
-      for (int j = 0; j < DP; ++j) ms[k * DP + j] = sv[j];
+        for (int j = 0; j < DP; ++j) ms[k * DP + j] = sv[j];
+      }
     }
+    __syncthreads();
+    float m = 0.f;
+    for (int k = lane; k < KMAX; k += 64) m = fmaxf(m, mg[k]);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
     ex0 = sigma_exp(m);
-    __syncthreads();
     build_tiles(tl, mg, ms, K, ex0, false, lane);
+  } else {
+    __syncthreads();   // the block counters
   }
   const bool lds_codes = a.lds_codes != 0;
   if (MULTI && a.ptag) {
@@ -969,7 +985,7 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
 #pragma unroll
     for (int w = 0; w < PREP_WORDS; ++w) ok &= a.ptag[w] == a.etag.w[w];
     if (!ok) {
-      if (gvalid && lane < 32) {
+      if (gvalid && wave < ENC_SUBS && lane < 32) {
         for (int64_t row = row_begin + lane; row < row_end; row += 32) {
           if (a.codes) {
             for (int m = 0; m < a.M; ++m) {
@@ -1002,12 +1018,18 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
   {
   const T* X = (const T*)a.x;
   RowRaw<T, VEC> nx;
-  auto fetch = [&](int64_t r0) {
-    int64_t row = r0 + i;
+  auto fetch = [&](int rb) {
+    int64_t row = row_begin + (int64_t)rb * RB + i;
     row = row < row_end ? row : row_begin;
     nx.load(X + row * a.ldx + (int64_t)g * d, d);
   };
-  fetch(row_begin);
+  auto claim = [&]() {
+    int v = 0;
+    if (lane == 0) v = atomicAdd(&next_blk[sg], 1);
+    return __builtin_amdgcn_readfirstlane(v);
+  };
+  int rb = wave / ENC_SUBS;
+  if (rb < nblk) fetch(rb);
   // a single stage keeps its tables in registers for every row block
   if (MULTI && a.M == 1) {
     const u4* fr = a.frag + (size_t)g * NT * 2 * 64;
@@ -1018,13 +1040,16 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
     }
     ex0 = a.sig[g];
   }
-  for (int64_t r0 = row_begin; r0 < row_end; r0 += RB) {
+  int rb_next = rb < nblk ? claim() : nblk;
+  while (rb < nblk) {
+    const int64_t r0 = row_begin + (int64_t)rb * RB;
     const int64_t row = r0 + i;
     const bool valid = row < row_end;
     float x[8];
     nx.get(x, d, valid);
     const u4 raw = nx.raw16(x, valid);
-    if (r0 + RB < row_end) fetch(r0 + RB);
+    if (rb_next < nblk) fetch(rb_next);
+    const int rb_after = rb_next < nblk ? claim() : nblk;
     for (int m = 0; m < a.M; ++m) {
       const int cb = m * G + g;
       int ex = ex0;
@@ -1071,7 +1096,7 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
       if (valid && h == 0 && a.codes) {
         const int64_t t = (int64_t)m * G + g;
         if (lds_codes) {
-          ((uint8_t*)(codes_l + m * ENC_CHUNK_ROWS + (row - row_begin)))[wave] = (uint8_t)kstar;
+          ((uint8_t*)(codes_l + m * a.chunk_rows + (row - row_begin)))[sg] = (uint8_t)kstar;
         } else if (a.byte_codes) {
           ((uint8_t*)(a.codes + row * a.words))[t] = (uint8_t)kstar;
         } else {
@@ -1087,6 +1112,8 @@ __global__ void __launch_bounds__(ENC_WAVES * 64, WAVES_PER_SIMD) encode_kernel(
       float* dst = a.residual + row * (int64_t)(G * d) + (int64_t)g * d;
       for (int j = 0; j < d; ++j) dst[j] = x[j];
     }
+    rb = rb_next;
+    rb_next = rb_after;
   }
   __syncthreads();
   }
@@ -1094,12 +1121,12 @@ flush:
   if (lds_codes) {
     // one 32-bit word per (stage, row): the codes of this block's four
     // consecutive subspaces
-    const int64_t g0 = (int64_t)blockIdx.y * ENC_WAVES;
+    const int64_t g0 = (int64_t)blockIdx.y * ENC_SUBS;
     const int nrows = (int)(row_end - row_begin);
     for (int e = threadIdx.x; e < a.M * nrows; e += blockDim.x) {
       const int m = e / nrows, r = e % nrows;
       uint32_t* dst = (uint32_t*)((uint8_t*)(a.codes + (row_begin + r) * a.words) + m * G + g0);
-      *dst = codes_l[m * ENC_CHUNK_ROWS + r];
+      *dst = codes_l[m * a.chunk_rows + r];
     }
   }
 }
@@ -1487,7 +1514,7 @@ gsrq_status encode_launch(const gsrq_shape* s, const void* X, int64_t ldx, const
   a.gain = gain; a.shape = shape; a.frag = nullptr; a.sig = nullptr;
   a.codes = codes; a.residual = residual;
   a.byte_codes = (a.b == 8) && ((M * (int64_t)a.G) % 4 == 0);
-  a.lds_codes = codes && a.byte_codes && (a.G % ENC_WAVES == 0) && M <= ENC_MAX_STAGES;
+  a.lds_codes = codes && a.byte_codes && (a.G % ENC_SUBS == 0) && M <= ENC_MAX_STAGES;
   const size_t esz = sizeof(T);
   a.vec_rows = (s->d == 8) && ((uintptr_t)X % 16 == 0) && ((ldx * esz) % 16 == 0);
   a.ptag = nullptr;
@@ -1516,8 +1543,19 @@ gsrq_status encode_launch(const gsrq_shape* s, const void* X, int64_t ldx, const
     a.frag = frag;
     a.sig = sig;
   }
-  dim3 grid((unsigned)((s->N + ENC_CHUNK_ROWS - 1) / ENC_CHUNK_ROWS),
-            (unsigned)((a.G + ENC_WAVES - 1) / ENC_WAVES));
+  // about one workgroup per CU: rows split into chunks so that the groups
+  // of ENC_SUBS subspaces times the chunks fill the 256 CUs once; a chunk's
+  // LDS-staged codes (M words per row) bound its rows
+  const int64_t groups = (a.G + ENC_SUBS - 1) / ENC_SUBS;
+  int64_t chunks = std::max<int64_t>(1, (256 + groups - 1) / groups);
+  int64_t cr = (s->N + chunks - 1) / chunks;
+  cr = (cr + RB - 1) / RB * RB;
+  const int64_t cap = (int64_t)ENC_CODES_WORDS / std::max(1, M) / RB * RB;
+  if (cr > cap) cr = cap;
+  a.chunk_rows = cr;
+  chunks = (s->N + cr - 1) / cr;
+  if (chunks > 0x7fffffff) return GSRQ_E_UNSUPPORTED;
+  dim3 grid((unsigned)chunks, (unsigned)groups);
   TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
   if (multi) {
     if (a.vec_rows)
