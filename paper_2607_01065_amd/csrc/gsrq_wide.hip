@@ -1277,6 +1277,201 @@ __global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_kernel(WFusedArgs
   }
 }
 
+// Stage-fused encode for d = 64 and 128 with the hi/lo pass (K <= 512): a
+// wave keeps the float32 residual of its 32-row block in registers through
+// all M stages (lane half h holds groups 2p + h of its row: elements
+// [16p + 8h, 16p + 8h + 8)), so no residual crosses HBM between stages.
+// Per stage the stage's whole fragment table is copied into LDS, every
+// tile scored (float32 operand path, two tiles' MFMA chains in flight), the
+// row's code written, and the winning codeword subtracted in place; rows
+// the key cannot decide are re-scored in float64 by the whole wave (eq. 5
+// form over every codeword; rare).  The residual leaves the registers only
+// at the end, when it is requested.
+constexpr int W_FW_LDS_MAX = 144 * 1024;   // a stage's fragment table, at most
+constexpr int W_FW_KMAX = 512;             // codewords of the float64 re-score, at most
+template <typename T, int C>
+__global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_wide_kernel(WFusedArgs a) {
+  extern __shared__ __align__(16) u4 wtab[];
+  static_assert(C == 8 || C == 16, "d = 64 or 128");
+  constexpr int P = w_pairs(C);
+  constexpr int QU = w_frags(C);
+  int g, rc;
+  {
+    const int id = blockIdx.x;
+    if (a.map_xcd) {
+      const int xcd = id & 7, slot = id >> 3, gpx = a.G >> 3;
+      const int j = slot % gpx;
+      rc = slot / gpx;
+      g = ((j / a.lg) * 8 + xcd) * a.lg + (j % a.lg);
+    } else {
+      g = id % a.G;
+      rc = id / a.G;
+    }
+  }
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i = lane & 31, h = lane >> 5;
+  const int d = a.d, K = a.K, G = a.G;
+  const int64_t row = (int64_t)rc * W_ROWS + (int64_t)wave * RB + i;
+  const bool valid = row < a.N;
+  float r[P][8];
+  {
+    const T* xp = (const T*)a.x + (valid ? row : 0) * a.ldx + (int64_t)g * d + 8 * h;
+    const bool xvec = ((a.ldx * (int64_t)sizeof(T)) % 16 == 0) && (((uintptr_t)a.x) % 16 == 0);
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      float v[8];
+      if (xvec) {
+        if (sizeof(T) == 2) {
+          const h8 x8 = as_h8(*(const u4*)(xp + 16 * p));
+#pragma unroll
+          for (int j = 0; j < 8; ++j) v[j] = (float)x8[j];
+        } else {
+          const f4 lo = *(const f4*)(xp + 16 * p), hi = *(const f4*)(xp + 16 * p + 4);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) { v[j] = lo[j]; v[4 + j] = hi[j]; }
+        }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) v[j] = (float)xp[16 * p + j];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) r[p][j] = valid ? v[j] : 0.f;
+    }
+  }
+  for (int m = 0; m < a.M; ++m) {
+    const int cb = m * G + g;
+    const int ex = a.sig[cb];
+    const float* gcb = a.gain + (size_t)cb * K;
+    const float* scb = a.shape + (size_t)cb * K * d;
+    {
+      const u4* ftab = a.frag + (size_t)cb * a.tiles * a.QF * 64;
+      const int n = a.tiles * QU * 64;
+      __syncthreads();                      // the previous stage's table is no longer read
+      for (int e = tid; e < n; e += W_THREADS) {
+        const int t = e / (QU * 64), o = e - t * (QU * 64);
+        wtab[e] = ftab[(size_t)t * a.QF * 64 + o];
+      }
+      __syncthreads();
+    }
+    u4 bx[P], blo[P], bias;
+    float rr, eD;
+    bool need_exact;
+    {
+      WRaw<float, P> raw;
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        raw.v[2 * p] = (u4){__float_as_uint(r[p][0]), __float_as_uint(r[p][1]),
+                            __float_as_uint(r[p][2]), __float_as_uint(r[p][3])};
+        raw.v[2 * p + 1] = (u4){__float_as_uint(r[p][4]), __float_as_uint(r[p][5]),
+                                __float_as_uint(r[p][6]), __float_as_uint(r[p][7])};
+      }
+      w_make_b<float, P>(raw, d, valid, ex, h, bx, blo, bias, rr, need_exact, eD);
+    }
+    int best = 0x7fffffff, bt = 0;
+    for (int t = 0; t < a.tiles; t += 2) {
+      const u4* ta = wtab + (size_t)t * QU * 64 + lane;
+      const f16v c0 = w_tile<false, P>(ta, bx, blo, bias);
+      if (t + 1 < a.tiles) {
+        const f16v c1 = w_tile<false, P>(ta + QU * 64, bx, blo, bias);
+        w_take(w_tile_key(c0), t, best, bt);
+        w_take(w_tile_key(c1), t + 1, best, bt);
+      } else {
+        w_take(w_tile_key(c0), t, best, bt);
+      }
+    }
+    int kstar;
+    float dhat;
+    {
+      const int j = best & 15;
+      const int kidx = bt * CW + (j >> 2) * 8 + h * 4 + (j & 3);
+      const int hv = best >> 4;
+      const auto sh = __builtin_amdgcn_permlane32_swap(hv, hv, false, false);
+      const auto sk = __builtin_amdgcn_permlane32_swap(kidx, kidx, false, false);
+      const long long v0 = (long long)(int)sh[0] * 4294967296ll + (long long)(unsigned)sk[0];
+      const long long v1 = (long long)(int)sh[1] * 4294967296ll + (long long)(unsigned)sk[1];
+      const long long v = v0 < v1 ? v0 : v1;
+      dhat = __int_as_float((int)(v >> 32) << 4);
+      kstar = (int)(v & 0xffffffffll);
+    }
+    need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
+    unsigned long long fb = __ballot(valid && need_exact && h == 0);
+    while (fb) {
+      // the whole wave re-scores row L in float64: g^2 - 2 g s.x over all
+      // K codewords (lane l takes codewords l, l + 64, ...), the row's
+      // elements broadcast one at a time from lanes L and L + 32
+      const int L = __ffsll((long long)fb) - 1;
+      fb &= fb - 1;
+      constexpr int KQ = W_FW_KMAX / 64;
+      double dot[KQ];
+#pragma unroll
+      for (int q = 0; q < KQ; ++q) dot[q] = 0.0;
+#pragma unroll
+      for (int p = 0; p < P; ++p)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const double xj = (double)__shfl(r[p][j & 7], L + 32 * (j >> 3));
+          const int e = 16 * p + j;
+#pragma unroll
+          for (int q = 0; q < KQ; ++q) {
+            const int k = lane + 64 * q;
+            if (k < K) dot[q] = fma(xj, (double)scb[(size_t)k * d + e], dot[q]);
+          }
+        }
+      double bd = INFINITY;
+      int bk = 0x7fffffff;
+#pragma unroll
+      for (int q = 0; q < KQ; ++q) {
+        const int k = lane + 64 * q;
+        if (k < K) {
+          const double gk = (double)gcb[k];
+          const double dist = fma(-2.0 * gk, dot[q], gk * gk);
+          if (dist < bd) { bd = dist; bk = k; }
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const double od = __shfl_xor(bd, off);
+        const int ok = __shfl_xor(bk, off);
+        if (od < bd || (od == bd && ok < bk)) { bd = od; bk = ok; }
+      }
+      if (i == L) kstar = bk;
+    }
+    if (kstar >= K) kstar = K - 1;        // rows past N only
+    if (valid && h == 0 && a.codes)
+      w_put_code(a.codes + row * a.words, ((int64_t)m * G + g) * a.b, a.b, kstar);
+    // subtract the codeword: this lane half's groups of g s
+    const float gk = gcb[kstar];
+    const float* sp = scb + (size_t)kstar * d + 8 * h;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      float sv[8];
+      if (a.svec) {
+        const f4 lo = *(const f4*)(sp + 16 * p), hi = *(const f4*)(sp + 16 * p + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) { sv[j] = lo[j]; sv[4 + j] = hi[j]; }
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sv[j] = sp[16 * p + j];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) r[p][j] = fmaf(-gk, sv[j], r[p][j]);
+    }
+  }
+  if (a.res_out && valid) {
+    float* dst = a.res_out + row * ((int64_t)G * d) + (int64_t)g * d + 8 * h;
+#pragma unroll
+    for (int p = 0; p < P; ++p) {
+      if (a.res_vec) {
+        ((f4*)(dst + 16 * p))[0] = (f4){r[p][0], r[p][1], r[p][2], r[p][3]};
+        ((f4*)(dst + 16 * p))[1] = (f4){r[p][4], r[p][5], r[p][6], r[p][7]};
+      } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) dst[16 * p + j] = r[p][j];
+      }
+    }
+  }
+}
+
 // Outputs of the rows the single pass listed, after the sliced hi/lo pass:
 // each row's best (distance key, codeword) from hbest is checked like a row
 // of the scoring kernel (operands in the float16 range, best distance at
@@ -2505,12 +2700,21 @@ bool w_fused(const gsrq_shape* s) {
   return w_score_layout(s, 4, false).resident;
 }
 
+// Several stages at d = 64 or 128 scored by the hi/lo pass (K <= 512) whose
+// stage table fits in LDS: one stage-fused launch (w_encode_fused_wide_kernel).
+bool w_fused_wide(const gsrq_shape* s) {
+  const int C = w_cwidth(s->d);
+  if (s->M <= 1 || (C != 8 && C != 16) || s->K > W_FW_KMAX) return false;
+  const WLayout L = w_score_layout(s, 4, false);
+  return !L.sp && (size_t)L.tiles * L.QF * 64 * sizeof(u4) <= (size_t)W_FW_LDS_MAX;
+}
+
 WEncWs w_encode_ws(const gsrq_shape* s) {
   WEncWs W;
   const int64_t G = s->D / s->d;
   const WLayout L = w_score_layout(s, 4, false);
   size_t off = 0;
-  if (w_fused(s)) {
+  if (w_fused(s) || w_fused_wide(s)) {
     // every stage's fragment table, per-codebook sigma state; no residual
     // buffers and no deferred-row lists
     const size_t ncb = (size_t)s->M * G;
@@ -2806,6 +3010,42 @@ gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64
       else w_encode_fused_kernel<float, 2><<<grid, W_THREADS, L.lds, st>>>(a);
     }
     return launch_ok();
+  }
+  if (w_fused_wide(s)) {
+    // all stages' fragment tables, then one launch: one 32-row block per
+    // wave, its residual in registers through every stage
+    if ((e = w_build_frags(gain, shape, s->d, s->K, C, s->M * G, 0, false, nullptr, G, sig, frag,
+                           XD, st)))
+      return e;
+    const WLayout L = w_score_layout(s, 4, false);
+    WFusedArgs a;
+    a.x = X; a.ldx = ldx; a.N = s->N; a.d = s->d; a.K = s->K; a.G = G; a.M = s->M;
+    a.tiles = L.tiles; a.QF = L.QF; a.b = log2i(s->K); a.words = words;
+    a.frag = frag; a.sig = sig; a.gain = gain; a.shape = shape; a.codes = codes;
+    a.res_out = residual; a.res_vec = ((uintptr_t)residual % 16) == 0;
+    a.svec = ((uintptr_t)shape % 16) == 0;
+    a.nwg = (int)((s->N + W_ROWS - 1) / W_ROWS);
+    a.map_xcd = L.map_xcd; a.lg = L.lg;
+    const dim3 grid((unsigned)(G * a.nwg));
+    const size_t lds = (size_t)L.tiles * w_frags(C) * 64 * sizeof(u4);
+    auto go = [&](const void* fn, auto kern) -> gsrq_status {
+      if (lds > 65536 &&
+          hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
+              hipSuccess)
+        return GSRQ_E_HIP;
+      kern<<<grid, W_THREADS, lds, st>>>(a);
+      return launch_ok();
+    };
+    TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
+    if (x_dtype == GSRQ_F16)
+      return C == 8 ? go((const void*)w_encode_fused_wide_kernel<_Float16, 8>,
+                         w_encode_fused_wide_kernel<_Float16, 8>)
+                    : go((const void*)w_encode_fused_wide_kernel<_Float16, 16>,
+                         w_encode_fused_wide_kernel<_Float16, 16>);
+    return C == 8 ? go((const void*)w_encode_fused_wide_kernel<float, 8>,
+                       w_encode_fused_wide_kernel<float, 8>)
+                  : go((const void*)w_encode_fused_wide_kernel<float, 16>,
+                       w_encode_fused_wide_kernel<float, 16>);
   }
   for (int m = 0; m < s->M; ++m) {
     if ((e = w_build_frags(gain, shape, s->d, s->K, C, G, m * G, false, nullptr, G, sig, frag,
