@@ -67,7 +67,11 @@ def test_wide_encode_single_stage(dtype, N, D, d, K):
     (np.float16, 4, 256, 16, 128, 2000, False),  # stage-fused, the rate-sweep shape
     (np.float32, 3, 512, 8, 32, 700, None),      # stage-fused, d = 8 with K > 256
     (np.float16, 3, 256, 16, 64, 900, True),     # stage-fused, rows re-scored in float64
-    (np.float16, 2, 256, 128, 256, 400, False),  # one launch per stage (d = 128)
+    (np.float16, 2, 256, 128, 256, 400, False),  # stage-fused, d = 128 (residual in registers)
+    (np.float32, 3, 256, 128, 256, 613, False),  # stage-fused d = 128, float32 rows, ragged N
+    (np.float16, 3, 256, 128, 128, 700, True),   # stage-fused d = 128, rows re-scored in float64
+    (np.float16, 3, 512, 64, 128, 700, None),    # stage-fused d = 64, table at the LDS limit
+    (np.float32, 4, 32, 64, 192, 333, None),     # stage-fused d = 64, one tile (odd tile count)
     (np.float16, 4, 16, 32, 64, 301, False),     # one launch per stage (d = 32)
     (np.float32, 3, 128, 256, 512, 300, False),  # one launch per stage (d = 256)
     (np.float32, 2, 1024, 128, 128, 2200, None), # single pass + listed rows, per stage
