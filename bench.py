@@ -193,6 +193,8 @@ def full_cache(args, wl):
         "kernels_us_source": "encode: HIP events around its launches in the first timed "
                              "step; others: one instrumented step after the timed region",
     }
+    if args.copy_ref_mib > 0:
+        out["copy_ref_bytes"] = copy_reference(args.copy_ref_mib, dev)
     print(json.dumps(out), flush=True)
 
 
@@ -555,7 +557,9 @@ def main():
         "kernels_us": {k: {"avg_us": avg_us(k), "launches": tim[k][1]} for k in tim},
         "kernels_us_source": "assign: HIP events around its launches in the first timed "
                              "step; others: one instrumented step after the timed region",
-        "roofline": {"kernel": "assign_accumulate (eq. 5 scores + argmin + weighted sums)",
+        "roofline": {"kernel": ("assign_accumulate (eq. 5 scores + argmin + weighted sums)"
+                               if d <= 8 and K <= 256 else
+                               "w_score (eq. 5 scores + argmin; training pass)"),
                      "bound": "mfma", "achieved": achieved, "peak": PEAK_MFMA_F16_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / PEAK_MFMA_F16_TFLOPS,
                      "traffic": traffic, "traffic_unit": "HBM bytes per launch",

@@ -1289,8 +1289,14 @@ __global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_kernel(WFusedArgs
 // at the end, when it is requested.
 constexpr int W_FW_LDS_MAX = 144 * 1024;   // a stage's fragment table, at most
 constexpr int W_FW_KMAX = 512;             // codewords of the float64 re-score, at most
+// eight waves share a stage's table: two per SIMD, so one wave's argmin and
+// table reads overlap another's MFMA chains even when the table leaves room
+// for a single workgroup per CU, and each table copy serves 256 rows
+constexpr int W_FW_WAVES = 8;
+constexpr int W_FW_THREADS = W_FW_WAVES * 64;
+constexpr int W_FW_ROWS = W_FW_WAVES * RB;
 template <typename T, int C>
-__global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_wide_kernel(WFusedArgs a) {
+__global__ void __launch_bounds__(W_FW_THREADS, 1) w_encode_fused_wide_kernel(WFusedArgs a) {
   extern __shared__ __align__(16) u4 wtab[];
   static_assert(C == 8 || C == 16, "d = 64 or 128");
   constexpr int P = w_pairs(C);
@@ -1311,7 +1317,7 @@ __global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_wide_kernel(WFuse
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i = lane & 31, h = lane >> 5;
   const int d = a.d, K = a.K, G = a.G;
-  const int64_t row = (int64_t)rc * W_ROWS + (int64_t)wave * RB + i;
+  const int64_t row = (int64_t)rc * W_FW_ROWS + (int64_t)wave * RB + i;
   const bool valid = row < a.N;
   float r[P][8];
   {
@@ -1346,10 +1352,19 @@ __global__ void __launch_bounds__(W_THREADS, 2) w_encode_fused_wide_kernel(WFuse
     {
       const u4* ftab = a.frag + (size_t)cb * a.tiles * a.QF * 64;
       const int n = a.tiles * QU * 64;
+      constexpr int UN = 4;                 // loads in flight per thread
       __syncthreads();                      // the previous stage's table is no longer read
-      for (int e = tid; e < n; e += W_THREADS) {
-        const int t = e / (QU * 64), o = e - t * (QU * 64);
-        wtab[e] = ftab[(size_t)t * a.QF * 64 + o];
+      for (int e0 = tid; e0 < n; e0 += UN * W_FW_THREADS) {
+        u4 v[UN];
+#pragma unroll
+        for (int u = 0; u < UN; ++u) {
+          const int e = e0 + u * W_FW_THREADS;
+          const int t = e / (QU * 64), o = e - t * (QU * 64);
+          if (e < n) v[u] = ftab[(size_t)t * a.QF * 64 + o];
+        }
+#pragma unroll
+        for (int u = 0; u < UN; ++u)
+          if (e0 + u * W_FW_THREADS < n) wtab[e0 + u * W_FW_THREADS] = v[u];
       }
       __syncthreads();
     }
@@ -3024,7 +3039,7 @@ gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64
     a.frag = frag; a.sig = sig; a.gain = gain; a.shape = shape; a.codes = codes;
     a.res_out = residual; a.res_vec = ((uintptr_t)residual % 16) == 0;
     a.svec = ((uintptr_t)shape % 16) == 0;
-    a.nwg = (int)((s->N + W_ROWS - 1) / W_ROWS);
+    a.nwg = (int)((s->N + W_FW_ROWS - 1) / W_FW_ROWS);
     a.map_xcd = L.map_xcd; a.lg = L.lg;
     const dim3 grid((unsigned)(G * a.nwg));
     const size_t lds = (size_t)L.tiles * w_frags(C) * 64 * sizeof(u4);
@@ -3033,7 +3048,7 @@ gsrq_status encode(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype, int64
           hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) !=
               hipSuccess)
         return GSRQ_E_HIP;
-      kern<<<grid, W_THREADS, lds, st>>>(a);
+      kern<<<grid, W_FW_THREADS, lds, st>>>(a);
       return launch_ok();
     };
     TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
