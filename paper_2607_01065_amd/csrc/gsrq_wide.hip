@@ -137,10 +137,13 @@ __global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ 
 //   bias           h0 [hi(gg) lo(gg) 2^SA 2^SA 0 0 0 0], h1 zero
 //   LO_p (p < P)   lo(a[16p + 8h, 16p + 8h + 8))
 // so the single-pass scoring kernel stages the first P + 1 of them only.
-// Padding codewords (k >= K) have a = 0 and a float16-max g^2 slot.
+// Padding codewords (k >= K) have a = 0 and a float16-max g^2 slot.  P is
+// a template argument so that all of a lane's shape loads are issued
+// together (a runtime pair loop waited for each pair's loads in turn).
+template <int P>
 __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ gain,
                                                     const float* __restrict__ shape, int d, int K,
-                                                    int C, int unit_gain,
+                                                    int unit_gain,
                                                     const int* __restrict__ sig,
                                                     const int* __restrict__ done, int G, int cb0,
                                                     u4* __restrict__ frag) {
@@ -154,15 +157,22 @@ __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ ga
   const float g = real ? (unit_gain ? 1.f : gain[(size_t)cb * K + kk]) : 0.f;
   const int ex = sig[cb];
   const float* s = shape + ((size_t)cb * K + kk) * d;
-  const int P = w_pairs(C);
-  u4* out = frag + ((size_t)cbl * tiles + t) * w_frags(C) * 64;
+  u4* out = frag + ((size_t)cbl * tiles + t) * (2 * P + 1) * 64;
+  float sv[P][8];
+#pragma unroll
+  for (int p = 0; p < P; ++p)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const int e = 16 * p + 8 * h + j;
+      sv[p][j] = s[min(e, d - 1)];            // in bounds; masked below
+    }
+#pragma unroll
   for (int p = 0; p < P; ++p) {
     _Float16 hi[8], lo[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const int e = 16 * p + 8 * h + j;
-      const float sv = (real && e < d) ? s[e] : 0.f;
-      const float av = ldexpf(-2.f * g * sv, SA - ex);
+      const float av = ldexpf(-2.f * g * ((real && e < d) ? sv[p][j] : 0.f), SA - ex);
       hi[j] = (_Float16)av;
       lo[j] = (_Float16)(av - (float)hi[j]);
     }
@@ -1585,15 +1595,35 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
     if (tid < W_XROWS) rows[tid] = a.xrows[(size_t)g * a.N + b0 + min(tid, nb - 1)];
     if (tid == 0) ncand = 0;
     __syncthreads();
-    for (int e = tid; e < W_XROWS * 8 * W_CMAX; e += W_XTHREADS) {
-      const int i = e / (8 * W_CMAX), j = e % (8 * W_CMAX);
-      xs[i][j] = j < d ? to_f(X[(int64_t)rows[i] * a.ldx + (int64_t)g * d + j]) : 0.f;
+    {
+      // the rows' d elements (slots past nb repeat the last row), eight
+      // unconditional loads in flight per thread: the batch is latency-bound
+      const int ld = 31 - __clz(d), n = W_XROWS << ld;
+      constexpr int UN = 8;
+      for (int e0 = tid; e0 < n; e0 += UN * W_XTHREADS) {
+        float v[UN];
+#pragma unroll
+        for (int u = 0; u < UN; ++u) {
+          const int e = min(e0 + u * W_XTHREADS, n - 1);
+          v[u] = to_f(X[(int64_t)rows[e >> ld] * a.ldx + (int64_t)g * d + (e & (d - 1))]);
+        }
+#pragma unroll
+        for (int u = 0; u < UN; ++u) {
+          const int e = e0 + u * W_XTHREADS;
+          if (e < n) xs[e >> ld][e & (d - 1)] = v[u];
+        }
+      }
     }
     __syncthreads();
-    if (tid < W_XROWS) {
+    // row norms: wave w sums rows 4w .. 4w + 3 across its lanes
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float* xr = xs[wave * 4 + r];
       double q = 0.0;
-      for (int j = 0; j < d; ++j) q = fma((double)xs[tid][j], (double)xs[tid][j], q);
-      xn[tid] = sqrt(q);
+      for (int j = lane; j < d; j += 64) q = fma((double)xr[j], (double)xr[j], q);
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) q += __shfl_xor(q, off);
+      if (lane == 0) xn[wave * 4 + r] = sqrt(q);
     }
     __syncthreads();
     double xmax = 0.0;
@@ -1633,13 +1663,24 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
       for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int q = 0; q < 4; ++q) acc[r][q] = 0.0;
+      // codeword elements of step j0 + 8 are loaded while step j0's
+      // products run (the last step reloads its own)
+      f4 sv[4][2], sn[4][2];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const f4* sp = (const f4*)(scb + (size_t)kk[q] * d);
+        sn[q][0] = sp[0];
+        sn[q][1] = sp[1];
+      }
       for (int j0 = 0; j0 < d; j0 += 8) {
-        f4 sv[4][2];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) { sv[q][0] = sn[q][0]; sv[q][1] = sn[q][1]; }
+        const int jn = min(j0 + 8, d - 8);
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const f4* sp = (const f4*)(scb + (size_t)kk[q] * d + j0);
-          sv[q][0] = sp[0];
-          sv[q][1] = sp[1];
+          const f4* sp = (const f4*)(scb + (size_t)kk[q] * d + jn);
+          sn[q][0] = sp[0];
+          sn[q][1] = sp[1];
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
@@ -1771,18 +1812,33 @@ __global__ void __launch_bounds__(1024) w_bucket_scan_kernel(int64_t N, int K, i
                                                              const int* __restrict__ done,
                                                              int* __restrict__ cnt,
                                                              int* __restrict__ boff) {
+  extern __shared__ int sc[];               // [chunks][K] counts, staged
   __shared__ int wsum[16];
   const int g = blockIdx.x;
   if (done && done[g]) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int* cg = cnt + (size_t)g * chunks * K;
+  {
+    // the counts into LDS, eight loads in flight per thread
+    const int n = chunks * K;
+    constexpr int UN = 8;
+    for (int e0 = tid; e0 < n; e0 += UN * 1024) {
+      int v[UN];
+#pragma unroll
+      for (int u = 0; u < UN; ++u) v[u] = cg[min(e0 + u * 1024, n - 1)];
+#pragma unroll
+      for (int u = 0; u < UN; ++u)
+        if (e0 + u * 1024 < n) sc[e0 + u * 1024] = v[u];
+    }
+  }
+  __syncthreads();
   // thread tid owns bins [b, e): their totals over the chunks, then an
   // exclusive scan of the totals over the workgroup
   const int per = (K + 1023) / 1024;
   const int b = min(K, tid * per), e = min(K, b + per);
   int tot = 0;
   for (int k = b; k < e; ++k)
-    for (int c = 0; c < chunks; ++c) tot += cg[(size_t)c * K + k];
+    for (int c = 0; c < chunks; ++c) tot += sc[c * K + k];
   int inc = tot;
 #pragma unroll
   for (int off = 1; off < 64; off <<= 1) {
@@ -1797,7 +1853,7 @@ __global__ void __launch_bounds__(1024) w_bucket_scan_kernel(int64_t N, int K, i
   for (int k = b; k < e; ++k) {
     bo[k] = base;
     for (int c = 0; c < chunks; ++c) {
-      const int n = cg[(size_t)c * K + k];
+      const int n = sc[c * K + k];
       cg[(size_t)c * K + k] = base;
       base += n;
     }
@@ -2156,16 +2212,25 @@ __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
     for (int e = 0; e < E; ++e) sk[E * li + e] = (float)sv[e];
     if (li == 0) *gk = (float)gnew;
   }
-  if (a.t > 0 && blockIdx.x == 0 && tid == 0) {
-    int ch = a.force_changed | a.xchanged[g];
-    double obj = a.obj ? a.xobj[g] : 0.0;
-    for (int c = 0; c < a.nwg; ++c) {
+  if (a.t > 0 && blockIdx.x == 0 && tid < 64) {
+    // stop test: the scoring workgroups' changed flags and objectives,
+    // strided over the first wave and reduced in a fixed order
+    int ch = 0;
+    double obj = 0.0;
+    for (int c = tid; c < a.nwg; c += 64) {
       ch |= a.changed[(size_t)g * a.nwg + c];
       if (a.obj) obj += a.obj[(size_t)g * a.nwg + c];
     }
-    if (a.trace) atomicAdd(a.trace + (size_t)g * a.T + (a.t - 1), obj);
-    a.iters[g] = a.t;
-    if (!ch && !a.no_early_stop) a.done[g] = a.t;
+    const bool any = __ballot(ch != 0) != 0ull;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) obj += __shfl_xor(obj, off);
+    if (tid == 0) {
+      const bool changed = any || a.force_changed || a.xchanged[g];
+      if (a.obj) obj += a.xobj[g];
+      if (a.trace) atomicAdd(a.trace + (size_t)g * a.T + (a.t - 1), obj);
+      a.iters[g] = a.t;
+      if (!changed && !a.no_early_stop) a.done[g] = a.t;
+    }
   }
 }
 
@@ -2603,8 +2668,19 @@ gsrq_status w_build_frags(const float* gain, const float* shape, int d, int K, i
   gsrq_status e = launch_ok();
   if (e) return e;
   const int tiles = (K + CW - 1) / CW;
-  w_frag_kernel<<<dim3(tiles, ncb), 64, 0, st>>>(gain, shape, d, K, C, unit_gain ? 1 : 0, sig,
-                                                 done, G, cb0, frag);
+  const dim3 fgrid(tiles, ncb);
+  const int ug = unit_gain ? 1 : 0;
+  auto go = [&](auto kern) {
+    kern<<<fgrid, 64, 0, st>>>(gain, shape, d, K, ug, sig, done, G, cb0, frag);
+  };
+  switch (w_pairs(C)) {
+    case 1: go(w_frag_kernel<1>); break;
+    case 2: go(w_frag_kernel<2>); break;
+    case 4: go(w_frag_kernel<4>); break;
+    case 8: go(w_frag_kernel<8>); break;
+    case 16: go(w_frag_kernel<16>); break;
+    default: return GSRQ_E_UNSUPPORTED;
+  }
   return launch_ok();
 }
 
@@ -2864,8 +2940,14 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
         int* bcnt = (int*)(base + W.bcnt);
         w_bucket_count_kernel<<<dim3(bchunks, G), 256, (size_t)K * sizeof(int), st>>>(
             assign, s->N, K, bch, aa.done, bcnt);
-        w_bucket_scan_kernel<<<G, 1024, 0, st>>>(s->N, K, bchunks, aa.done, bcnt,
-                                                 (int*)(base + W.boff));
+        const size_t slds = (size_t)bchunks * K * sizeof(int);   // <= 128 KiB
+        if (slds > 65536 &&
+            hipFuncSetAttribute((const void*)w_bucket_scan_kernel,
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                (int)slds) != hipSuccess)
+          return GSRQ_E_HIP;
+        w_bucket_scan_kernel<<<G, 1024, slds, st>>>(s->N, K, bchunks, aa.done, bcnt,
+                                                    (int*)(base + W.boff));
         w_bucket_scatter_kernel<<<dim3(bchunks, G), 256, (size_t)K * sizeof(int), st>>>(
             assign, s->N, K, bch, aa.done, bcnt, (int*)(base + W.sorted));
         if ((e2 = launch_ok())) return e2;
