@@ -1566,17 +1566,25 @@ __global__ void __launch_bounds__(256) w_listed_finish_kernel(WScoreArgs a) {
 // E_k = ||x||^2 + g_k^2 - 2 g_k s_k.x and |s_k.x| <= ||x|| (shapes of norm at
 // most 1), (g_k - ||x||)^2 <= E_k <= (g_k + ||x||)^2, so a codeword with
 // g_k > gmin + 2 max ||x|| (1e-5 relative slack) wins for no row of the
-// batch.  The survivors' s_k.x are accumulated in float64 by 4 waves, wave w
-// holding rows 4w..4w+3 and each lane 4 codewords at a time (a 4 x 4
-// register block over 8-element steps).
+// batch.  The survivors' s_k.x are accumulated in float64, one codeword per
+// lane at a time spread over all four waves (a batch of a few rows, the
+// usual case, then costs one pass over each codeword's elements instead of
+// a 4 x 4 block walk by one wave); each lane keeps the dot products of the
+// batch's rows (in groups of four, only the groups the batch fills) in
+// element order 0 .. d - 1, streaming its codeword in double-buffered
+// 32-element blocks against rows held in LDS as float64.  The per-row
+// minimum (lowest index on ties) is taken over lanes, then over waves.
 constexpr int W_XROWS = 16;
 constexpr int W_XTHREADS = 256;
 constexpr int W_XKMAX = 4096;    // candidate list capacity (codewords)
 
 template <typename T, int MODE>
 __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
-  __shared__ __align__(16) float xs[W_XROWS][8 * W_CMAX];
+  __shared__ __align__(16) double xsd[W_XROWS][8 * W_CMAX];
   __shared__ double xn[W_XROWS];
+  __shared__ double wbd[W_XTHREADS / 64][W_XROWS];
+  __shared__ int wbk[W_XTHREADS / 64][W_XROWS];
+  __shared__ int bestk[W_XROWS];
   __shared__ int rows[W_XROWS];
   __shared__ int cand[W_XKMAX];
   __shared__ int ncand;
@@ -1610,7 +1618,7 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
 #pragma unroll
         for (int u = 0; u < UN; ++u) {
           const int e = e0 + u * W_XTHREADS;
-          if (e < n) xs[e >> ld][e & (d - 1)] = v[u];
+          if (e < n) xsd[e >> ld][e & (d - 1)] = (double)v[u];
         }
       }
     }
@@ -1618,9 +1626,9 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
     // row norms: wave w sums rows 4w .. 4w + 3 across its lanes
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float* xr = xs[wave * 4 + r];
+      const double* xr = xsd[wave * 4 + r];
       double q = 0.0;
-      for (int j = lane; j < d; j += 64) q = fma((double)xr[j], (double)xr[j], q);
+      for (int j = lane; j < d; j += 64) q = fma(xr[j], xr[j], q);
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) q += __shfl_xor(q, off);
       if (lane == 0) xn[wave * 4 + r] = sqrt(q);
@@ -1645,93 +1653,126 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
     // a list that overflowed falls back to every codeword
     const int nc = ncand <= W_XKMAX ? ncand : K;
     const bool all = ncand > W_XKMAX;
-    double bd[4];
-    int bk[4];
+    const int nr4 = (nb + 3) >> 2;          // row groups of four the batch fills
+    double bd[4][4];
+    int bk[4][4];
 #pragma unroll
-    for (int r = 0; r < 4; ++r) { bd[r] = INFINITY; bk[r] = 0x7fffffff; }
-    for (int c0 = lane * 4; c0 < nc; c0 += 64 * 4) {
-      int kk[4];
-      double gk[4];
+    for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int ci = min(c0 + q, nc - 1);
-        kk[q] = all ? ci : cand[ci];
-        gk[q] = a.unit_gain ? 1.0 : (double)gcb[kk[q]];
-      }
+      for (int r = 0; r < 4; ++r) { bd[rg][r] = INFINITY; bk[rg][r] = 0x7fffffff; }
+    constexpr int JB = 32;                  // codeword elements per block
+    for (int c0 = wave * 64 + lane; c0 - lane < nc; c0 += W_XTHREADS) {
+      const bool live = c0 < nc;
+      const int kq = all ? min(c0, K - 1) : cand[min(c0, nc - 1)];
+      const double gq = a.unit_gain ? 1.0 : (double)gcb[kq];
+      const float* sp = scb + (size_t)kq * d;
       double acc[4][4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
+      for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) acc[r][q] = 0.0;
-      // codeword elements of step j0 + 8 are loaded while step j0's
-      // products run (the last step reloads its own)
-      f4 sv[4][2], sn[4][2];
+        for (int r = 0; r < 4; ++r) acc[rg][r] = 0.0;
+      f4 ca[JB / 4], cz[JB / 4];             // the two block buffers
+      const int nbk = (d + JB - 1) / JB;
+      auto load = [&](f4 (&buf)[JB / 4], int jb) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const f4* sp = (const f4*)(scb + (size_t)kk[q] * d);
-        sn[q][0] = sp[0];
-        sn[q][1] = sp[1];
-      }
-      for (int j0 = 0; j0 < d; j0 += 8) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) { sv[q][0] = sn[q][0]; sv[q][1] = sn[q][1]; }
-        const int jn = min(j0 + 8, d - 8);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f4* sp = (const f4*)(scb + (size_t)kk[q] * d + jn);
-          sn[q][0] = sp[0];
-          sn[q][1] = sp[1];
+        for (int v = 0; v < JB / 4; ++v) {
+          const int j = min(jb + 4 * v, d - 4);          // in bounds; unused past d
+          buf[v] = *(const f4*)(sp + j);
         }
+      };
+      auto block = [&](const f4 (&buf)[JB / 4], int jb) {
+        const int je = min(JB, d - jb);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const f4* xp = (const f4*)&xs[wave * 4 + r][j0];
-          const f4 x0 = xp[0], x1 = xp[1];
+        for (int rg = 0; rg < 4; ++rg) {
+          if (rg >= nr4) break;
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
+          for (int v = 0; v < JB / 4; ++v) {
+            if (4 * v >= je) break;
+            const double c0d = (double)buf[v][0], c1d = (double)buf[v][1];
+            const double c2d = (double)buf[v][2], c3d = (double)buf[v][3];
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              acc[r][q] = fma((double)x0[j], (double)sv[q][0][j], acc[r][q]);
-              acc[r][q] = fma((double)x1[j], (double)sv[q][1][j], acc[r][q]);
+            for (int r = 0; r < 4; ++r) {
+              const double* xr = &xsd[rg * 4 + r][jb + 4 * v];
+              const double2 xa = *(const double2*)xr, xb = *(const double2*)(xr + 2);
+              double t = acc[rg][r];
+              t = fma(xa.x, c0d, t);
+              t = fma(xa.y, c1d, t);
+              t = fma(xb.x, c2d, t);
+              t = fma(xb.y, c3d, t);
+              acc[rg][r] = t;
             }
+          }
+        }
+      };
+      load(ca, 0);
+      for (int bi = 0; bi < nbk; bi += 2) {
+        if (bi + 1 < nbk) load(cz, (bi + 1) * JB);
+        block(ca, bi * JB);
+        if (bi + 1 < nbk) {
+          if (bi + 2 < nbk) load(ca, (bi + 2) * JB);
+          block(cz, (bi + 1) * JB);
         }
       }
+      if (live) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        if (c0 + q >= nc) break;
+        for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          // eq. (5) up to the row constant ||x||^2: g^2 - 2 g s.x
-          const double e = fma(-2.0 * gk[q], acc[r][q], gk[q] * gk[q]);
-          if (e < bd[r] || (e == bd[r] && kk[q] < bk[r])) {
-            bd[r] = e;
-            bk[r] = kk[q];
+          for (int r = 0; r < 4; ++r) {
+            // eq. (5) up to the row constant ||x||^2: g^2 - 2 g s.x
+            const double e = fma(-2.0 * gq, acc[rg][r], gq * gq);
+            if (e < bd[rg][r] || (e == bd[rg][r] && kq < bk[rg][r])) {
+              bd[rg][r] = e;
+              bk[rg][r] = kq;
+            }
           }
+      }
+    }
+    // minimum per row over the wave's lanes, then over the four waves
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      if (rg >= nr4) break;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        double b = bd[rg][r];
+        int k = bk[rg][r];
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) {
+          const double od = __shfl_xor(b, off);
+          const int ok = __shfl_xor(k, off);
+          if (od < b || (od == b && ok < k)) { b = od; k = ok; }
+        }
+        if (lane == 0) {
+          wbd[wave][rg * 4 + r] = b;
+          wbk[wave][rg * 4 + r] = k;
         }
       }
     }
-    // wave minimum per row, lowest index on ties
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int off = 32; off > 0; off >>= 1) {
-        const double od = __shfl_xor(bd[r], off);
-        const int ok = __shfl_xor(bk[r], off);
-        if (od < bd[r] || (od == bd[r] && ok < bk[r])) { bd[r] = od; bk[r] = ok; }
+    __syncthreads();
+    if (tid < nb) {
+      double b = wbd[0][tid];
+      int k = wbk[0][tid];
+      for (int w2 = 1; w2 < W_XTHREADS / 64; ++w2) {
+        const double od = wbd[w2][tid];
+        const int ok = wbk[w2][tid];
+        if (od < b || (od == b && ok < k)) { b = od; k = ok; }
       }
-    // outputs of this wave's rows
+      bestk[tid] = k < K ? k : 0;           // (a non-empty list always sets k)
+    }
+    __syncthreads();
+    // outputs: wave w writes rows w, w + 4, w + 8, w + 12
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int i = wave * 4 + r;
+      const int i = wave + 4 * r;
       if (i >= nb) break;
       const int64_t row = rows[i];
-      const int k = bk[r];
+      const int k = bestk[i];
       if (MODE == W_TRAIN) {
         if (a.obj) {
           // weighted distortion ||x - g s||^2 of the chosen codeword
           const double gk = a.unit_gain ? 1.0 : (double)gcb[k];
           double dist = 0.0;
           for (int j = lane; j < d; j += 64) {
-            const double e = (double)xs[i][j] - gk * (double)scb[(size_t)k * d + j];
+            const double e = xsd[i][j] - gk * (double)scb[(size_t)k * d + j];
             dist = fma(e, e, dist);
           }
 #pragma unroll
@@ -1749,7 +1790,8 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
         if (a.res_out) {
           const float gk = gcb[k];
           float* dst = a.res_out + row * ((int64_t)a.G * d) + (int64_t)g * d;
-          for (int j = lane; j < d; j += 64) dst[j] = fmaf(-gk, scb[(size_t)k * d + j], xs[i][j]);
+          for (int j = lane; j < d; j += 64)
+            dst[j] = fmaf(-gk, scb[(size_t)k * d + j], (float)xsd[i][j]);
         }
       }
     }
