@@ -262,12 +262,17 @@ def extra_paths(B, cache, wl, dev, reps=50):
 ATTN_SHAPE = dict(B=8, cap=32768, Hkv=8, GQ=4)   # LLaMA-3-8B heads, 32K-token context
 
 
-def attention_measure(B, dev, reps=50, shape=ATTN_SHAPE):
-    """One decoding step of attention over 1-bit coded K/V caches
+ATTN_RQ_STAGES = 12   # the paper's 0.75-bit setting: d = 128, K = 256, 12 stages
+
+
+def attention_measure(B, dev, reps=50, shape=ATTN_SHAPE, layout="1bit"):
+    """One decoding step of attention over coded K/V caches
     (gsrq_attn_decode: unpack, dequantise, RoPE, attention) for 8 sequences
     of 32768 tokens, 32 query / 8 key-value heads, next to float16 attention
     over an already dequantised and rotated cache of the same shape (two
-    float16 matmuls and a float32 softmax, reading 1.07 GB)."""
+    float16 matmuls and a float32 softmax, reading 1.07 GB).  layout "1bit":
+    d = 8, K = 256, one stage; "075bit": the paper's 0.75-bit residual
+    coding, d = 128, K = 256, 12 stages (Sec. 6.2; Appendix C)."""
     import math
 
     import torch
@@ -275,10 +280,16 @@ def attention_measure(B, dev, reps=50, shape=ATTN_SHAPE):
     import synth
     Bn, cap, Hkv, GQ = shape["B"], shape["cap"], shape["Hkv"], shape["GQ"]
     Hq = Hkv * GQ
-    case = synth.attn_case(Bn, cap, [cap] * Bn, Hkv, GQ, seed=0, q_dtype="float16")
+    rq = layout == "075bit"
+    M = ATTN_RQ_STAGES if rq else 1
+    if rq:
+        case = synth.attn_case_rq(Bn, cap, [cap] * Bn, Hkv, GQ, M=M, seed=0, q_dtype="float16")
+    else:
+        case = synth.attn_case(Bn, cap, [cap] * Bn, Hkv, GQ, seed=0, q_dtype="float16")
     t = {k: torch.from_numpy(case[k]).to(dev) for k in
          ("k_codes", "v_codes", "lens", "k_gain", "k_shape", "v_gain", "v_shape", "q")}
-    ws = torch.empty(B.attn_workspace_bytes(Bn, cap, Hq, Hkv), dtype=torch.uint8, device=dev)
+    ws = torch.empty(B.attn_workspace_bytes(Bn, cap, Hq, Hkv, d=HEAD_DIM if rq else 8, M=M),
+                     dtype=torch.uint8, device=dev)
     out = torch.empty((Bn, Hq, HEAD_DIM), dtype=torch.float32, device=dev)
 
     def call():
@@ -311,9 +322,12 @@ def attention_measure(B, dev, reps=50, shape=ATTN_SHAPE):
     B.timing_enable(False)
     kern_us = tim["attention"][0] / tim["attention"][1] * 1e3
     tok_heads = Bn * cap * Hkv
-    code_bytes = 2 * tok_heads * 16                  # 8-bit codes of 16 subspaces, K and V
-    G = Hkv * 16
-    cb_bytes = 2 * G * 256 * 9 * 4                   # both codebooks (gain + 8-element shape)
+    if rq:
+        code_bytes = 2 * tok_heads * M               # one byte per stage, K and V
+        cb_bytes = 2 * Hkv * M * 256 * 129 * 4       # both codebooks (gain + 128-element shape)
+    else:
+        code_bytes = 2 * tok_heads * 16              # 8-bit codes of 16 subspaces, K and V
+        cb_bytes = 2 * Hkv * 16 * 256 * 9 * 4        # both codebooks (gain + 8-element shape)
     io_bytes = Bn * Hq * HEAD_DIM * (2 + 4)          # float16 queries in, float32 out
     alg_bytes = code_bytes + cb_bytes + io_bytes
     del t, ws, out, case
@@ -329,26 +343,38 @@ def attention_measure(B, dev, reps=50, shape=ATTN_SHAPE):
 
     fp16_us = timed(fp16_attn)
     del kT, vf, qf
+    if rq:
+        # LDS bytes per token and key/value head: the key codeword halves of
+        # every stage (M x 256 B, gathered as 16-byte pieces), the weight's
+        # float32 adds into M stage bins per query head, and the share of the
+        # stage-pair table copies (M x 64 KiB per chunk of tokens)
+        chunk = 2 * 8 * (32 // GQ) * 32
+        lds_per = M * 256 + M * GQ * 4 + M * 65536 // chunk
+        desc = (f"0.75-bit K/V (d=128 K=256 M={M}, one subspace per head; the paper's "
+                f"decoding-latency setting)")
+    else:
+        lds_per = 1024
+        desc = "1-bit K/V (d=8 K=256 M=1)"
     return {"decode_attention": {
-        "shape": f"{Bn} seq x {cap} tok, {Hq} q / {Hkv} kv heads x {HEAD_DIM}, 1-bit K/V "
-                 f"(d=8 K=256 M=1), RoPE base 500000",
+        "shape": f"{Bn} seq x {cap} tok, {Hq} q / {Hkv} kv heads x {HEAD_DIM}, {desc}, "
+                 f"RoPE base 500000",
         "call_us": call_us, "kernel_us": kern_us,
         # a layer's codebooks are fixed across decoding steps: with the
         # tables kept in the workspace (GSRQ_ATTN_TABLES_READY)
         "call_us_tables_ready": ready_us,
         "token_heads_per_s": tok_heads / (call_us * 1e-6),
         "algorithmic_bytes": alg_bytes,
-        # LDS bytes: 16 key and 16 value codewords gathered (16 B each), the
-        # value codewords stored to and read back from the tile: 1 KiB per
-        # token and key/value head
-        "lds_bytes": tok_heads * 1024,
+        # LDS bytes: 1-bit layout, 16 key and 16 value codewords gathered
+        # (16 B each), the value codewords stored to and read back from the
+        # tile: 1 KiB per token and key/value head; 0.75-bit layout above
+        "lds_bytes": tok_heads * lds_per,
         "hbm_GBps": alg_bytes / (kern_us * 1e-6) / 1e9,
         "hbm_frac": alg_bytes / (kern_us * 1e-6) / 1e9 / PEAK_HBM_GBPS,
         "fp16_attention_us": fp16_us,
         "speedup_vs_fp16_attention": fp16_us / call_us}}
 
 
-def attention_cpu_baseline(shape=ATTN_SHAPE, budget_s=10.0):
+def attention_cpu_baseline(shape=ATTN_SHAPE, budget_s=10.0, layout="1bit"):
     """Time the float64 oracle on whole sequences of the attention workload
     (unpack, dequantise, RoPE, attention), as many as fit in about budget_s
     seconds (at least one), and scale to token-heads/s of the workload."""
@@ -362,17 +388,36 @@ def attention_cpu_baseline(shape=ATTN_SHAPE, budget_s=10.0):
     except Exception:  # noqa: BLE001
         threads = os.cpu_count() or 1
     Bn, cap, Hkv, GQ = shape["B"], shape["cap"], shape["Hkv"], shape["GQ"]
-    case = synth.attn_case(Bn, cap, [cap] * Bn, Hkv, GQ, seed=0, q_dtype="float16")
-    G = Hkv * HEAD_DIM // 8
+    rq = layout == "075bit"
+    if rq:
+        M = ATTN_RQ_STAGES
+        case = synth.attn_case_rq(Bn, cap, [cap] * Bn, Hkv, GQ, M=M, seed=0, q_dtype="float16")
+        G, d = Hkv, HEAD_DIM
+    else:
+        M = 1
+        case = synth.attn_case(Bn, cap, [cap] * Bn, Hkv, GQ, seed=0, q_dtype="float16")
+        G, d = Hkv * HEAD_DIM // 8, 8
     done, t = 0, 0.0
     while done < Bn and (done == 0 or t < budget_s):
         t0 = time.perf_counter()
-        kc = O.unpack_codes(case["k_codes"][done], 1, G, 256)
-        vc = O.unpack_codes(case["v_codes"][done], 1, G, 256)
-        k = O.gsrq_decode(kc, case["k_gain"], case["k_shape"])
-        v = O.gsrq_decode(vc, case["v_gain"], case["v_shape"])
-        k = k.astype(np.float32).astype(np.float16).reshape(cap, Hkv, HEAD_DIM)
-        v = v.astype(np.float32).astype(np.float16).reshape(cap, Hkv, HEAD_DIM)
+        kc = O.unpack_codes(case["k_codes"][done], M, G, 256)
+        vc = O.unpack_codes(case["v_codes"][done], M, G, 256)
+        if rq:
+            # keys: the float16 decode of each stage codeword, summed; values:
+            # the float32 codewords summed (the inputs the kernel declares)
+            kt = (case["k_gain"][..., None] * case["k_shape"]).astype(np.float32)
+            vt = (case["v_gain"][..., None] * case["v_shape"]).astype(np.float32)
+            kt = kt.astype(np.float16).astype(np.float64)
+            k = np.zeros((cap, G, d))
+            v = np.zeros((cap, G, d))
+            for m in range(M):
+                k += kt[m][np.arange(G)[None, :], kc[:, m, :]]
+                v += vt[m][np.arange(G)[None, :], vc[:, m, :]].astype(np.float64)
+        else:
+            k = O.gsrq_decode(kc, case["k_gain"], case["k_shape"])
+            v = O.gsrq_decode(vc, case["v_gain"], case["v_shape"])
+            k = k.astype(np.float32).astype(np.float16).reshape(cap, Hkv, HEAD_DIM)
+            v = v.astype(np.float32).astype(np.float16).reshape(cap, Hkv, HEAD_DIM)
         O.attn_decode(case["q"][done], k, v, 500000.0)
         t += time.perf_counter() - t0
         done += 1
@@ -422,39 +467,49 @@ def main():
     B.load_library()
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
-    if args.workload == "decode_attention_1bit":
-        r = attention_measure(B, torch.device("cuda", 0), reps=args.steps)["decode_attention"]
-        line = {"metric": "decode attention token-heads/s over 1-bit coded K/V",
+    if args.workload in ("decode_attention_1bit", "decode_attention_075bit"):
+        rq = args.workload == "decode_attention_075bit"
+        r = attention_measure(B, torch.device("cuda", 0), reps=args.steps,
+                              layout="075bit" if rq else "1bit")["decode_attention"]
+        line = {"metric": "decode attention token-heads/s over "
+                          + ("0.75-bit" if rq else "1-bit") + " coded K/V",
                 "value": r["token_heads_per_s"], "unit": "token-heads/s",
                 "n_gpus": 1, "steps": args.steps, "warmup": 1,
                 "ms_per_step": r["call_us"] / 1e3, "higher_is_better": True,
                 "scaling": "weak", "vs_baseline": None, "dtype": "f16",
                 "data": "synthetic",
-                "config": {"workload": "decode_attention_1bit", "shape": r["shape"]},
+                "config": {"workload": args.workload, "shape": r["shape"]},
                 **{k: v for k, v in r.items() if k != "shape"}}
         gbps = r["algorithmic_bytes"] / (r["kernel_us"] * 1e-6) / 1e9
         lds_tbps = r["lds_bytes"] / (r["kernel_us"] * 1e-6) / 1e12
         import hashlib
-        tr = TRAFFIC["decode_attention_1bit"]
-        src = os.path.join(ROOT, "paper_2607_01065_amd", "csrc", tr["source"])
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        tr = TRAFFIC.get(args.workload)
+        traffic = None
+        if tr is not None:
+            src = os.path.join(ROOT, "paper_2607_01065_amd", "csrc", tr["source"])
+            sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+            traffic = tr["bytes_per_launch"] if sha == tr["source_sha256_prefix"] else None
+        note = ("key codeword pieces of every stage (M x 256 B), float32 weight adds into "
+                "M stage bins per query head, stage-pair table copies: per token and "
+                "key/value head; peak = 256 CU x 128 B/clk x 2.4 GHz" if rq else
+                "codeword gathers, value-tile stores and transposing loads: 1 KiB per token "
+                "and key/value head; peak = 256 CU x 128 B/clk x 2.4 GHz; the kernel is bound "
+                "by LDS bank conflicts of the random gathers, not by HBM")
         line["roofline"] = {
-            "kernel": "attn_chunk_kernel (unpack + dequantise + RoPE + attention)",
+            "kernel": ("attn_rq_chunk_kernel (unpack + stage-pair dequantise + RoPE + scores + "
+                       "softmax + per-codeword value weights)" if rq else
+                       "attn_chunk_kernel (unpack + dequantise + RoPE + attention)"),
             "bound": "hbm", "achieved": gbps, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
             "frac": gbps / PEAK_HBM_GBPS,
-            "traffic": tr["bytes_per_launch"] if sha == tr["source_sha256_prefix"] else None,
-            "traffic_unit": "HBM bytes per launch",
+            "traffic": traffic, "traffic_unit": "HBM bytes per launch",
             "bytes_per_launch": r["algorithmic_bytes"], "avg_launch_us": r["kernel_us"],
             "lds_view": {"achieved": lds_tbps, "peak": PEAK_LDS_TBPS, "unit": "TB/s",
                          "frac": lds_tbps / PEAK_LDS_TBPS, "bytes_per_launch": r["lds_bytes"],
-                         "note": "codeword gathers, value-tile stores and transposing loads: "
-                                 "1 KiB per token and key/value head; peak = 256 CU x 128 "
-                                 "B/clk x 2.4 GHz; the kernel is bound by LDS bank conflicts "
-                                 "of the random gathers, not by HBM"}}
+                         "note": note}}
         if args.copy_ref_mib > 0:
             line["copy_ref_bytes"] = copy_reference(args.copy_ref_mib, torch.device("cuda", 0))
         if not args.no_cpu_baseline:
-            line["cpu_baseline"] = attention_cpu_baseline()
+            line["cpu_baseline"] = attention_cpu_baseline(layout="075bit" if rq else "1bit")
         print(json.dumps(line), flush=True)
         return
     wl = synth.WORKLOADS[args.workload]

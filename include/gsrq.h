@@ -287,8 +287,16 @@ typedef struct {
  * the caller must not change while reusing the tables. */
 enum { GSRQ_ATTN_TABLES_READY = 1 };
 
-/* Workspace bytes gsrq_attn_decode needs for shape a. */
+/* Workspace bytes gsrq_attn_decode needs for shape a over the 1-bit code
+ * layout (d = 8, K = 256, M = 1). */
 gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes);
+
+/* Workspace bytes gsrq_attn_decode needs for shape a over codes of shape kv
+ * (either layout gsrq_attn_decode accepts; the residual-coded layout's size
+ * grows with kv->M).  Same argument checks as gsrq_attn_decode on a and kv:
+ * GSRQ_E_ARG, or GSRQ_E_UNSUPPORTED for a layout it does not take. */
+gsrq_status gsrq_attn_workspace_bytes_kv(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                                         size_t* bytes);
 
 /*
  * gsrq_attn_decode -- one decoding step of attention over GSRQ-coded key and
@@ -304,24 +312,38 @@ gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes);
  * angle position * theta_j (rotate-half form).  Keys are cached before RoPE;
  * the query is the newest token's, at position L - 1, before RoPE.
  *
- *  kv                code shape: D = Hkv * head_dim, d = 8, K = 256, M = 1
- *                    (other valid shapes: GSRQ_E_UNSUPPORTED); N >= B * cap.
+ *  kv                code shape, N >= B * cap, D = Hkv * head_dim, K = 256, and
+ *                    either the 1-bit layout (d = 8, M = 1: 16 subspaces per
+ *                    head) or the residual-coded layout of the paper's sub-1-bit
+ *                    rates (Sec. 6.2, Configurations; Appendix C measures 0.75
+ *                    bit): d = head_dim, one subspace per head, 1 <= M <= 16
+ *                    stages (M = 12 is 0.75 bit, M = 16 is 1 bit); a token's
+ *                    key or value row is the sum of its M stage codewords.
+ *                    Other valid shapes: GSRQ_E_UNSUPPORTED.
  *  k_codes, v_codes  [B][cap][gsrq_code_words(kv)] uint32 packed codes, token
  *                    i of sequence b in row b * cap + i; 16-byte aligned.
  *  seq_len           [B] int32 (device), clamped to [0, cap]; a sequence of
  *                    length 0 gets a zero output.
- *  k_gain, k_shape   key codebook [1][G][256], [1][G][256][8] and value
+ *  k_gain, k_shape   key codebook [M][G][256], [M][G][256][d] and value
  *  v_gain, v_shape   codebook (shapes 16-byte aligned).
  *  q, q_dtype        [B][Hq][head_dim] queries, 16-byte aligned.
  *  out               [B][Hq][head_dim] float32.
- *  workspace         >= gsrq_attn_workspace_bytes(a), 256-byte aligned.
- * Precision: keys and values enter as their float16 decode (g * s rounded
- * to float32, then to float16, as gsrq_decode's float16 output); the
- * query and keys are rotated in float32 and, like the softmax weights,
- * rounded to float16 for the matrix products, with float32 sums (the
- * operand precision of float16 attention over a rotated float16 cache);
- * chunks are merged in float64.  This build: head_dim = 128 and
- * Hq / Hkv in {1, 2, 4}.
+ *  workspace         >= gsrq_attn_workspace_bytes_kv(a, kv) (for the 1-bit
+ *                    layout also gsrq_attn_workspace_bytes(a)), 256-byte aligned.
+ * Precision, 1-bit layout: keys and values enter as their float16 decode
+ * (g * s rounded to float32, then to float16, as gsrq_decode's float16
+ * output); the query and keys are rotated in float32 and, like the softmax
+ * weights, rounded to float16 for the matrix products, with float32 sums
+ * (the operand precision of float16 attention over a rotated float16
+ * cache); chunks are merged in float64.
+ * Precision, residual-coded layout: each key codeword enters as its float16
+ * decode fp16(fp32(g s)); a key is summed two stages at a time in float16
+ * (the pairs' shares of a score added in float32), turned and multiplied as
+ * above; softmax weights stay float32 and are summed per stage and codeword
+ * in float32 (LDS atomics: the order of these float32 sums, and so the last
+ * bits of the output, may differ from call to call); the value side uses
+ * the float32 codewords fl(g s), chunks merged and contracted in float64.
+ * This build: head_dim = 128 and Hq / Hkv in {1, 2, 4}.
  */
 gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
                              const uint32_t* k_codes, const uint32_t* v_codes,

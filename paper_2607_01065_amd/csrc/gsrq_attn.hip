@@ -629,6 +629,570 @@ template <int GQ> gsrq_status attn_launch(const AttnArgs& args, int B, int Hkv, 
   return launch_ok();
 }
 
+// ------------------------------------------------------------------------
+// Residual-coded caches at the paper's sub-1-bit rates: one subspace per head
+// (d = head_dim = 128), K = 256, M stages (0.75 bit at M = 12, 1 bit at 16,
+// 2 bit at 32).  A head's key codebooks (M x 256 x 128 float16, 768 KiB at
+// M = 12) do not fit LDS, so the chunk kernel scores in passes over stage
+// pairs: per pass the workgroup copies the pair's float16 key table
+// (128 KiB) into LDS, and every wave adds, for all the blocks it owns, the
+// pair's share of each score (a key is the sum of its stages' codewords, so
+// a score is the sum of the stages' shares) into score accumulators it keeps
+// across passes.  Per 32-token block the A operand holds the block's partial
+// keys (two gathered codeword pieces summed in float16, turned by the lane's
+// R_t as in the 1-bit kernel); the B operand is the group's query columns
+// with every column of another block zeroed, so one accumulator collects a
+// whole group of U blocks, each column its own block's scores.  After the
+// last pass the softmax takes one reference maximum per head for the whole
+// workgroup and float32 weights, and the value side needs no gathers: with
+// v_i = sum_m c_m[code_m(i)], sum_i p_i v_i = sum_m sum_k W_m[k] c_m[k] for
+// W_m[k] = sum of the weights of the tokens whose stage-m code is k, so the
+// workgroup adds each weight into its M per-stage bins (LDS float atomics)
+// and writes the bins; the merge kernel sums the chunks' bins and contracts
+// them with the value codewords fl(g s).
+constexpr int AQ_MAXM = 16;               // stages supported (0.75 and 1 bit)
+constexpr int AQ_NG = 2;                  // groups of U blocks per wave
+constexpr int AQ_TAB_U4 = 2 * AT_K * 16;  // u4 of a stage-pair table (128 KiB)
+
+constexpr int AQ_CHUNK = 4096;           // tokens per workgroup
+template <int GQ> struct AqCfg {
+  static constexpr int U = 32 / GQ;
+  static constexpr int CHUNK = AQ_CHUNK;                        // AQ_CHUNK / (32 U) groups
+  static constexpr int KTAB = 0;                                // u4 [2][256][16], swizzled
+  static constexpr int QT = KTAB + AQ_TAB_U4 * 16;              // f32 [32][128]
+  static constexpr int ANG = QT + 32 * AT_HD * 4;               // float2 [AT_WAVES][64]
+  static constexpr int RED = ANG + AT_WAVES * 64 * 8;           // f32 [AT_WAVES][2][GQ]
+  static constexpr int KC = RED + AT_WAVES * 2 * 4 * 4;         // u8 [CHUNK][2]: the pass's codes
+  static constexpr int BYTES = KC + CHUNK * 2;
+  // after the last pass the key table's space holds the bins of a group of
+  // stages and the chunk's value codes
+  static constexpr int BINS = 0;                                // u64 [32 / GQ][256][GQ]
+  static constexpr int VC = 32 * AT_K * 8;                      // u8 [CHUNK][16]
+};
+static_assert(AqCfg<4>::BYTES <= 160 * 1024, "LDS budget");
+static_assert(32 * AT_K * 8 + AQ_CHUNK * AQ_MAXM <= AQ_TAB_U4 * 16,
+              "bins and value codes fit the key table");
+static_assert(AQ_CHUNK % (32 * 32) == 0 && AQ_CHUNK / (32 * 8) <= AQ_NG * AT_WAVES,
+              "every group of a chunk has a wave");
+
+struct AqArgs {
+  const uint8_t* kc;        // [B][cap][4 W] key code bytes: stage m, head h at m Hkv + h
+  const uint8_t* vc;        // same for values
+  const int32_t* seq_len;   // [B]
+  const void* q;            // [B][Hq][128]
+  int q_f16;
+  const float2* t1;         // [32][64] cos/sin of t theta_j
+  const float2* t2;         // [32][64] cos/sin of 32 u theta_j
+  const double* th;         // [64] theta_j / 2 pi
+  const u4* tabk;           // [Hkv][M][256][16] f16 key codewords, 16 chunks of 8
+  float* part;              // [B][Hkv][nch][GQ][M 256 + 2]
+  int cap, rowb, Hkv, M, nch;  // rowb: code bytes per token row (4 W)
+  int xmap;
+  float qscale;
+};
+
+// Float16 key table of a residual-coded head: fp16(fp32(g s)) of every
+// codeword, chunk c = elements 8c .. 8c + 7, one chunk per thread.
+__global__ void __launch_bounds__(256) attn_rq_keytab_kernel(const float* __restrict__ kg,
+                                                             const float* __restrict__ ks,
+                                                             int Hkv, int M,
+                                                             u4* __restrict__ tabk) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;   // ((h M + m) 256 + k) 16 + c
+  if (e >= (int64_t)Hkv * M * AT_K * 16) return;
+  const int c = (int)(e & 15);
+  const int64_t hmk = e >> 4;
+  const int k = (int)(hmk % AT_K);
+  const int64_t hm = hmk / AT_K;
+  const int m = (int)(hm % M), h = (int)(hm / M);
+  const size_t cw = ((size_t)m * Hkv + h) * AT_K + k;          // codebook order [M][G][K]
+  const float g = kg[cw];
+  const f4* sp = (const f4*)(ks + cw * AT_HD + 8 * c);
+  const f4 a = sp[0], b = sp[1];
+  _Float16 v[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[j] = (_Float16)(g * a[j]);
+    v[4 + j] = (_Float16)(g * b[j]);
+  }
+  tabk[e] = pack_h8(v);
+}
+
+// LDS position (u4) of chunk c of codeword k of table stage sl: the 16
+// chunks of a 256-byte codeword are rotated by k, so that lanes gathering
+// the same chunk of random codewords spread over the banks.
+__device__ __forceinline__ int aq_slot(int sl, int k, int c) {
+  return ((sl * AT_K + k) << 4) + ((c + k) & 15);
+}
+
+template <int GQ>
+__global__ void __launch_bounds__(AT_THREADS, 1) attn_rq_chunk_kernel(AqArgs a) {
+  using C = AqCfg<GQ>;
+  constexpr int U = C::U;
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  u4* ktab = (u4*)(lds + C::KTAB);
+  unsigned long long* bins = (unsigned long long*)(lds + C::BINS);
+  float* qt = (float*)(lds + C::QT);
+  float* red = (float*)(lds + C::RED);
+
+  int chunk, hk, b;
+  {
+    const int id = blockIdx.x;
+    if (a.xmap) {
+      const int x = id & 7, slot = id >> 3;
+      const int gid = (slot / a.Hkv) * 8 + x;
+      hk = slot % a.Hkv;
+      b = gid / a.nch;
+      chunk = gid % a.nch;
+    } else {
+      chunk = id % a.nch;
+      hk = (id / a.nch) % a.Hkv;
+      b = id / (a.nch * a.Hkv);
+    }
+  }
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tl = lane & 31, hh = lane >> 5;
+  const int ul = tl / GQ, hl = tl % GQ;
+  const int M = a.M, RS = M * AT_K + 2;
+  float2* ang = (float2*)(lds + C::ANG) + w * 64;
+  const int len = min(max(a.seq_len[b], 0), a.cap);
+  const int tok0 = chunk * C::CHUNK;
+  float* outp = a.part + (((size_t)b * a.Hkv + hk) * a.nch + chunk) * GQ * RS;
+  if (tok0 >= len) {
+    if (tid < GQ) {
+      outp[tid * RS + M * AT_K] = -INFINITY;
+      outp[tid * RS + M * AT_K + 1] = 0.f;
+    }
+    return;
+  }
+  const int tend = min(len, tok0 + C::CHUNK);
+  const int Hq = a.Hkv * GQ;
+  const size_t seq_row0 = (size_t)b * a.cap;
+
+  // queries turned by R_{-32u} and scaled (as the 1-bit kernel)
+  {
+    constexpr int PER = 32 * 64 / AT_THREADS;
+    float x[PER], y[PER];
+    float2 cs[PER];
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      const int it = m * AT_THREADS + tid, j = it >> 6, jd = it & 63;
+      const size_t qo = ((size_t)b * Hq + hk * GQ + j % GQ) * AT_HD + jd;
+      if (a.q_f16) {
+        x[m] = (float)((const _Float16*)a.q)[qo];
+        y[m] = (float)((const _Float16*)a.q)[qo + 64];
+      } else {
+        x[m] = ((const float*)a.q)[qo];
+        y[m] = ((const float*)a.q)[qo + 64];
+      }
+      cs[m] = a.t2[(j / GQ) * 64 + jd];
+    }
+#pragma unroll
+    for (int m = 0; m < PER; ++m) {
+      const int it = m * AT_THREADS + tid, j = it >> 6, jd = it & 63;
+      qt[j * AT_HD + jd] = (x[m] * cs[m].x + y[m] * cs[m].y) * a.qscale;
+      qt[j * AT_HD + jd + 64] = (y[m] * cs[m].x - x[m] * cs[m].y) * a.qscale;
+    }
+  }
+  h2 cp[16], sp[16];
+  {
+    const float4* t1 = (const float4*)(a.t1 + tl * 64 + 32 * hh);
+#pragma unroll
+    for (int m = 0; m < 16; ++m) {
+      const float4 v = t1[m];
+      cp[m] = (h2){(_Float16)v.x, (_Float16)v.z};
+      sp[m] = (h2){(_Float16)v.y, (_Float16)v.w};
+    }
+  }
+  const double thl = a.th[lane];
+  __syncthreads();
+
+  // this wave's groups: gi = w + AT_WAVES j, j < AQ_NG.  A group's query
+  // operand (its columns turned by R_{pq - 32 gb0}, float16) is rebuilt in
+  // every pass: one sine/cosine per lane, cheaper than keeping 32 registers
+  // per group live across the passes
+  const int ngroups = (tend - tok0 + 32 * U - 1) / (32 * U);
+  f16v acc[AQ_NG];
+#pragma unroll
+  for (int j = 0; j < AQ_NG; ++j) acc[j] = (f16v){};
+  auto make_bq = [&](int gb0, u4 (&bq)[8]) {
+    {
+      const int n = max((len - 1) - 32 * gb0, 0);
+      double rev = (double)n * thl;
+      rev -= floor(rev);
+      float s, c;
+      sincosf((float)(rev * (2.0 * M_PI)), &s, &c);
+      ang[lane] = make_float2(c, s);
+    }
+    wave_lds_order();
+    const float4* qxp = (const float4*)(qt + tl * AT_HD + 32 * hh);
+    const float4* qyp = (const float4*)(qt + tl * AT_HD + 64 + 32 * hh);
+    const float4* ap = (const float4*)(ang + 32 * hh);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      _Float16 xh[8], yh[8];
+#pragma unroll
+      for (int m2 = 0; m2 < 2; ++m2) {
+        const float4 qx4 = qxp[2 * i + m2], qy4 = qyp[2 * i + m2];
+        const float4 va = ap[4 * i + 2 * m2], vb = ap[4 * i + 2 * m2 + 1];
+        const float qxv[4] = {qx4.x, qx4.y, qx4.z, qx4.w};
+        const float qyv[4] = {qy4.x, qy4.y, qy4.z, qy4.w};
+        const float cv[4] = {va.x, va.z, vb.x, vb.z};
+        const float sv[4] = {va.y, va.w, vb.y, vb.w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = 4 * m2 + r;
+          xh[e] = (_Float16)(qxv[r] * cv[r] - qyv[r] * sv[r]);
+          yh[e] = (_Float16)(qxv[r] * sv[r] + qyv[r] * cv[r]);
+        }
+      }
+      bq[i] = pack_h8(xh);
+      bq[i + 4] = pack_h8(yh);
+    }
+    wave_lds_order();                               // angle reads before the next writes
+  };
+
+  const uint8_t* kcb = a.kc + seq_row0 * a.rowb + hk;
+  uint8_t* kcl = lds + C::KC;
+  const int npass = (M + 1) >> 1;
+  for (int pass = 0; pass < npass; ++pass) {
+    const int s0 = 2 * pass;
+    const bool two = s0 + 1 < M;                     // uniform
+    __syncthreads();                                 // the previous pair's table is read
+    {
+      // the pair's table (16 u4 per thread) and the chunk's code bytes of
+      // the pair's stages (16 per thread, token t stage sl at 2 t + sl),
+      // every load issued before the first store
+      const u4* src = a.tabk + ((size_t)hk * M + s0) * AT_K * 16;
+      const int n = (two ? 2 : 1) * AT_K * 16;       // a single stage's pass: stage 1 zero
+      constexpr int PER = AQ_TAB_U4 / AT_THREADS;
+      constexpr int PERC = 2 * AQ_CHUNK / AT_THREADS;
+      u4 v[PER];
+      uint32_t cb[PERC];
+#pragma unroll
+      for (int r = 0; r < PER; ++r) {
+        const int e = min(r * AT_THREADS + tid, n - 1);
+        v[r] = src[e];
+      }
+#pragma unroll
+      for (int r = 0; r < PERC; ++r) {
+        const int e = r * AT_THREADS + tid, t = e >> 1, sl = e & 1;
+        const int row = min(tok0 + t, len - 1);
+        cb[r] = kcb[(size_t)row * a.rowb + (s0 + (two ? sl : 0)) * a.Hkv];
+      }
+#pragma unroll
+      for (int r = 0; r < PER; ++r) {
+        const int e = r * AT_THREADS + tid;
+        const u4 z = {0u, 0u, 0u, 0u};
+        ktab[aq_slot(e >> 12, (e >> 4) & 255, e & 15)] = e < n ? v[r] : z;
+      }
+#pragma unroll
+      for (int r = 0; r < PERC; ++r) kcl[r * AT_THREADS + tid] = (uint8_t)cb[r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < AQ_NG; ++j) {
+      const int gi = w + AT_WAVES * j;
+      if (gi >= ngroups) continue;                   // uniform per wave
+      const int gb0 = (tok0 >> 5) + gi * U;
+      const int nblk = min(U, (len - 32 * gb0 + 31) >> 5);
+      u4 bq[8];
+      make_bq(gb0, bq);
+      for (int u = 0; u < nblk; ++u) {
+        // the lane's token (rows past the sequence end read the last row's
+        // codes; their scores are masked)
+        const int t = min(32 * (gb0 + u) + tl, len - 1) - tok0;
+        const int c0 = kcl[2 * t], c1 = kcl[2 * t + 1];
+        const bool mine = ul == u;
+        const u4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int i2 = 0; i2 < 4; i2 += 2) {
+          // the gathers of two k-step pairs issued together (both stages:
+          // a single stage's pass reads zeros from stage 1)
+          u4 g[2][4];
+#pragma unroll
+          for (int ii = 0; ii < 2; ++ii) {
+            const int cx = 4 * hh + i2 + ii, cy = 8 + 4 * hh + i2 + ii;
+            g[ii][0] = ktab[aq_slot(0, c0, cx)];
+            g[ii][1] = ktab[aq_slot(0, c0, cy)];
+            g[ii][2] = ktab[aq_slot(1, c1, cx)];
+            g[ii][3] = ktab[aq_slot(1, c1, cy)];
+          }
+#pragma unroll
+          for (int ii = 0; ii < 2; ++ii) {
+            const int i = i2 + ii;
+            const u4 xa = g[ii][0], ya = g[ii][1], xb = g[ii][2], yb = g[ii][3];
+            h2 xr[4], yr[4];
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+              // scalar copies before the bit casts; the pair's two codeword
+              // pieces summed in float16, then turned by R_t
+              const uint32_t xw0 = xa[p], yw0 = ya[p], xw1 = xb[p], yw1 = yb[p];
+              const h2 xp = __builtin_bit_cast(h2, xw0) + __builtin_bit_cast(h2, xw1);
+              const h2 yp = __builtin_bit_cast(h2, yw0) + __builtin_bit_cast(h2, yw1);
+              const h2 c = cp[4 * i + p], sn = sp[4 * i + p];
+              xr[p] = __builtin_elementwise_fma(xp, c, -(yp * sn));
+              yr[p] = __builtin_elementwise_fma(xp, sn, yp * c);
+            }
+            const h8 kx = __builtin_shufflevector(
+                __builtin_shufflevector(xr[0], xr[1], 0, 1, 2, 3),
+                __builtin_shufflevector(xr[2], xr[3], 0, 1, 2, 3), 0, 1, 2, 3, 4, 5, 6, 7);
+            const h8 ky = __builtin_shufflevector(
+                __builtin_shufflevector(yr[0], yr[1], 0, 1, 2, 3),
+                __builtin_shufflevector(yr[2], yr[3], 0, 1, 2, 3), 0, 1, 2, 3, 4, 5, 6, 7);
+            const u4 bx = mine ? bq[i] : z, by = mine ? bq[i + 4] : z;
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kx, as_h8(bx), acc[j], 0, 0, 0);
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ky, as_h8(by), acc[j], 0, 0, 0);
+          }
+        }
+      }
+    }
+  }
+
+  // ---- softmax: one reference per head for the workgroup.  Register v of
+  // a lane holds token row t = 8 (v / 4) + 4 hh + v % 4 of block ul of the
+  // group, for query head hl.
+  float sc[AQ_NG][16];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < AQ_NG; ++j) {
+    const int gi = w + AT_WAVES * j;
+    const int rowb = 32 * ((tok0 >> 5) + gi * U + ul);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int t = 8 * (v >> 2) + 4 * hh + (v & 3);
+      const bool ok = gi < ngroups && rowb + t < len;
+      sc[j][v] = ok ? acc[j][v] : -INFINITY;
+      mx = fmaxf(mx, sc[j][v]);
+    }
+  }
+#pragma unroll
+  for (int off = GQ; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+  __syncthreads();                                   // every wave is done with the table
+  if (lane < GQ) red[w * 2 * GQ + lane] = mx;        // lane h (ul = 0, hh = 0) holds head h
+  // the chunk's value code bytes, token t stage m at 16 t + m (16 loads in
+  // flight per thread)
+  uint8_t* vcl = lds + C::VC;
+  {
+    const uint8_t* vcb = a.vc + seq_row0 * a.rowb + hk;
+    const int n = (tend - tok0) * M;
+    constexpr int B16 = 16;
+    for (int e0 = tid; e0 < n; e0 += B16 * AT_THREADS) {
+      uint32_t cv[B16];
+#pragma unroll
+      for (int r = 0; r < B16; ++r) {
+        const int e = min(e0 + r * AT_THREADS, n - 1), t = e / M, m = e - t * M;
+        cv[r] = vcb[(size_t)(tok0 + t) * a.rowb + m * a.Hkv];
+      }
+#pragma unroll
+      for (int r = 0; r < B16; ++r) {
+        const int e = e0 + r * AT_THREADS, t = e / M, m = e - t * M;
+        if (e < n) vcl[16 * t + m] = (uint8_t)cv[r];
+      }
+    }
+  }
+  __syncthreads();
+  float mref = -INFINITY;
+#pragma unroll
+  for (int v = 0; v < AT_WAVES; ++v) mref = fmaxf(mref, red[v * 2 * GQ + hl]);
+  // mref is finite: the chunk holds at least one token
+  // softmax sum of the lane's column (float32)
+  float lsum = 0.f;
+#pragma unroll
+  for (int j = 0; j < AQ_NG; ++j)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) lsum += __builtin_amdgcn_exp2f(sc[j][v] - mref);   // 0 if masked
+#pragma unroll
+  for (int off = GQ; off < 64; off <<= 1) lsum += __shfl_xor(lsum, off);
+  if (lane < GQ) red[w * 2 * GQ + GQ + lane] = lsum;
+  // value bins, SG stages at a time: every lane adds its own head's weight
+  // of each of its 16 tokens into the token's stage bins, as 64-bit fixed
+  // point (weight x 2^32, weights <= 1: exact integer sums, the same in any
+  // order); a token's codes are one 16-byte LDS read, the next token's
+  // issued before the current one's adds.  The bins of each stage group
+  // are then written to the chunk's record as float32.
+  constexpr int SG = 32 / GQ;                        // SG x 256 x GQ x 8 bytes = 64 KiB
+  for (int mg = 0; mg < M; mg += SG) {
+    const int ms = min(SG, M - mg);
+    __syncthreads();                                 // the previous group's bins are written out
+    for (int e = tid; e < ms * AT_K * GQ; e += AT_THREADS) bins[e] = 0ull;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < AQ_NG; ++j) {
+      const int gi = w + AT_WAVES * j;
+      if (gi >= ngroups) continue;                   // uniform per wave
+      const int rowb = 32 * ((tok0 >> 5) + gi * U + ul);
+      auto codes_of = [&](int v) {
+        const int t = 8 * (v >> 2) + 4 * hh + (v & 3);
+        return *(const u4*)(vcl + 16 * (min(rowb + t, len - 1) - tok0));
+      };
+      u4 cn = codes_of(0);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(sc[j][v] - mref);
+        const unsigned long long q = (unsigned long long)(p * 4294967296.0f);
+        const u4 cc = cn;
+        if (v + 1 < 16) cn = codes_of(v + 1);
+        const int t = 8 * (v >> 2) + 4 * hh + (v & 3);
+        if (rowb + t < len) {
+#pragma unroll
+          for (int m2 = 0; m2 < SG; ++m2) {
+            if (m2 >= ms) break;
+            const int m = mg + m2;
+            const int k = (cc[m >> 2] >> (8 * (m & 3))) & 255;
+            atomicAdd(&bins[(m2 * AT_K + k) * GQ + hl], q);
+          }
+        }
+      }
+    }
+    __syncthreads();
+    for (int e = tid; e < GQ * ms * AT_K; e += AT_THREADS) {
+      const int h = e / (ms * AT_K), r = e - h * (ms * AT_K);
+      outp[h * RS + mg * AT_K + r] = (float)((double)bins[r * GQ + h] * 0x1p-32);
+    }
+  }
+  if (tid < GQ) {
+    float l = 0.f, mr = -INFINITY;
+#pragma unroll
+    for (int v = 0; v < AT_WAVES; ++v) {
+      l += red[v * 2 * GQ + GQ + tid];
+      mr = fmaxf(mr, red[v * 2 * GQ + tid]);
+    }
+    outp[tid * RS + M * AT_K] = mr;
+    outp[tid * RS + M * AT_K + 1] = l;
+  }
+}
+
+// Value side, one workgroup per (sequence, key/value head, stage m): the
+// chunks' bins of stage m merged with their references, W_h[k] =
+// sum_c 2^(m_c,h - M_h) W_c,h[k] (float64), then contracted with the
+// stage's value codewords fl(g s): o_m,h[n] = sum_k W_h[k] fl(g_k s_kn).
+constexpr int AQ_VT = 256;
+__global__ void __launch_bounds__(AQ_VT) attn_rq_values_kernel(const float* __restrict__ part,
+                                                               int GQ, int Hkv, int nch, int M,
+                                                               const float* __restrict__ vg,
+                                                               const float* __restrict__ vs,
+                                                               double* __restrict__ om) {
+  __shared__ double wb[4][AT_K];
+  __shared__ double hs[4][AT_HD];
+  const int m = blockIdx.x % M, hk = (blockIdx.x / M) % Hkv, b = blockIdx.x / (M * Hkv);
+  const int tid = threadIdx.x;
+  const int RS = M * AT_K + 2;
+  const float* p0 = part + ((size_t)b * Hkv + hk) * nch * GQ * RS;
+  const size_t cs = (size_t)GQ * RS;
+  for (int h = 0; h < GQ; ++h) {
+    const float* p = p0 + (size_t)h * RS;
+    float mref = -INFINITY;
+    for (int c = 0; c < nch; ++c) {
+      const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
+      mref = lc > 0.f ? fmaxf(mref, mc) : mref;
+    }
+    double s = 0.0;
+    for (int c = 0; c < nch; ++c) {
+      const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
+      const float bv = p[c * cs + m * AT_K + tid];
+      s += lc > 0.f ? exp2((double)mc - (double)mref) * (double)bv : 0.0;
+    }
+    wb[h][tid] = s;
+  }
+  __syncthreads();
+  // thread (half, n): codewords half * 128 .. + 127, element n of each
+  const int n = tid & (AT_HD - 1), half = tid >> 7;
+  const size_t cb = ((size_t)m * Hkv + hk) * AT_K;
+  const float* gp = vg + cb;
+  const float* sp = vs + cb * AT_HD + n;
+  double o[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 16
+  for (int k = half * 128; k < half * 128 + 128; ++k) {
+    const double cw = (double)(gp[k] * sp[(size_t)k * AT_HD]);   // fl(g s)
+#pragma unroll
+    for (int h = 0; h < 4; ++h)
+      if (h < GQ) o[h] = fma(wb[h][k], cw, o[h]);
+  }
+  if (half) {
+#pragma unroll
+    for (int h = 0; h < 4; ++h) hs[h][n] = o[h];
+  }
+  __syncthreads();
+  if (!half) {
+    for (int h = 0; h < GQ; ++h)
+      om[(((size_t)b * Hkv + hk) * GQ + h) * M * AT_HD + (size_t)m * AT_HD + n] = o[h] + hs[h][n];
+  }
+}
+
+// Output of one (sequence, query head): o = sum_m o_m / sum_c 2^(m_c - M) l_c.
+__global__ void __launch_bounds__(AT_HD) attn_rq_out_kernel(const float* __restrict__ part,
+                                                            const double* __restrict__ om,
+                                                            int Hq, int Hkv, int nch, int M,
+                                                            float* __restrict__ out, AttnTag tag,
+                                                            const uint32_t* __restrict__ tagp) {
+  const int bq = blockIdx.x, b = bq / Hq, hq = bq % Hq, n = threadIdx.x;
+  bool tag_ok = true;
+#pragma unroll
+  for (int i = 0; i < AT_TAG_WORDS; ++i) tag_ok &= tagp[i] == tag.w[i];
+  if (!tag_ok) {
+    out[(size_t)bq * AT_HD + n] = __builtin_nanf("");
+    return;
+  }
+  const int GQ = Hq / Hkv, hk = hq / GQ, h = hq % GQ;
+  const int RS = M * AT_K + 2;
+  const float* p = part + (((size_t)b * Hkv + hk) * nch * GQ + h) * RS;
+  const size_t cs = (size_t)GQ * RS;
+  float mref = -INFINITY;
+  for (int c = 0; c < nch; ++c) {
+    const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
+    mref = lc > 0.f ? fmaxf(mref, mc) : mref;
+  }
+  double den = 0.0;
+  for (int c = 0; c < nch; ++c) {
+    const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
+    den += lc > 0.f ? exp2((double)mc - (double)mref) * (double)lc : 0.0;
+  }
+  const double* op = om + (((size_t)b * Hkv + hk) * GQ + h) * M * AT_HD + n;
+  double v = 0.0;
+  for (int m = 0; m < M; ++m) v += op[(size_t)m * AT_HD];
+  out[(size_t)bq * AT_HD + n] = den > 0.0 ? (float)(v / den) : 0.f;
+}
+
+struct AqPlan {
+  int GQ, nch, W;
+  size_t off_tag, off_t1, off_t2, off_th, off_tk, off_part, off_om, bytes;
+};
+
+gsrq_status aq_plan(const gsrq_attn_shape* a, const gsrq_shape* kv, AqPlan& p) {
+  p.GQ = a->Hq / a->Hkv;
+  const int M = kv->M;
+  const int64_t nch = ((int64_t)a->cap + AQ_CHUNK - 1) / AQ_CHUNK;
+  if (nch * a->Hkv * a->B > INT32_MAX || (int64_t)M * a->Hkv * a->B > INT32_MAX)
+    return GSRQ_E_UNSUPPORTED;
+  p.nch = (int)nch;
+  p.W = (int)(((int64_t)M * a->Hkv * 8 + 31) / 32);
+  const size_t pairs = (size_t)a->B * a->Hkv;
+  p.off_tag = 0;
+  p.off_t1 = 256;
+  p.off_t2 = p.off_t1 + align256(32 * 64 * sizeof(float2));
+  p.off_th = p.off_t2 + align256(32 * 64 * sizeof(float2));
+  p.off_tk = p.off_th + align256(64 * sizeof(double));
+  p.off_part = p.off_tk + align256((size_t)a->Hkv * M * AT_K * 16 * sizeof(u4));
+  p.off_om = p.off_part + align256(pairs * p.nch * p.GQ * ((size_t)M * AT_K + 2) * sizeof(float));
+  p.bytes = p.off_om + align256(pairs * p.GQ * (size_t)M * AT_HD * sizeof(double));
+  return GSRQ_OK;
+}
+
+template <int GQ> gsrq_status aq_launch(const AqArgs& args, int B, int Hkv, hipStream_t st) {
+  static bool attr_set = false;
+  if (!attr_set) {
+    if (hipFuncSetAttribute((const void*)attn_rq_chunk_kernel<GQ>,
+                            hipFuncAttributeMaxDynamicSharedMemorySize,
+                            AqCfg<GQ>::BYTES) != hipSuccess)
+      return GSRQ_E_HIP;
+    attr_set = true;
+  }
+  TimedLaunch tm(GSRQ_KERNEL_ATTENTION, st);
+  const int blocks = args.nch * Hkv * B;
+  attn_rq_chunk_kernel<GQ><<<blocks, AT_THREADS, AqCfg<GQ>::BYTES, st>>>(args);
+  return launch_ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -645,19 +1209,51 @@ gsrq_status gsrq_attn_workspace_bytes(const gsrq_attn_shape* a, size_t* bytes) {
 }  // extern "C"
 
 namespace {
+gsrq_status attn_layout(const gsrq_attn_shape* a, const gsrq_shape* kv, AttnPlan& p,
+                        AqPlan& qp, bool& rq);
+}  // namespace
+
+extern "C" {
+
+gsrq_status gsrq_attn_workspace_bytes_kv(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                                         size_t* bytes) {
+  if (!bytes) return GSRQ_E_ARG;
+  AttnPlan p;
+  AqPlan qp;
+  bool rq = false;
+  gsrq_status e = attn_layout(a, kv, p, qp, rq);
+  if (e) return e;
+  *bytes = rq ? qp.bytes : p.bytes;
+  return GSRQ_OK;
+}
+
+}  // extern "C"
+
+namespace {
 
 // Host validation shared by both entry points (no HIP call).
-gsrq_status attn_validate(const gsrq_attn_shape* a, const gsrq_shape* kv,
-                          const uint32_t* k_codes, const uint32_t* v_codes,
-                          const int32_t* seq_len, const float* k_gain, const float* k_shape,
-                          const float* v_gain, const float* v_shape, const void* q,
-                          gsrq_dtype q_dtype, float* out, AttnPlan& p) {
+// Code layouts: the 1-bit cache (d = 8, K = 256, one stage) or a residual-
+// coded one with one subspace per head (d = head_dim, K = 256, 1 <= M <= 32).
+gsrq_status attn_layout(const gsrq_attn_shape* a, const gsrq_shape* kv, AttnPlan& p,
+                        AqPlan& qp, bool& rq) {
   gsrq_status e = attn_plan(a, p);
   if (e) return e;
   if (!kv || kv->N < 1 || kv->D < 1 || kv->d < 1 || kv->K < 2 || kv->M < 1) return GSRQ_E_ARG;
   if (kv->D != a->Hkv * a->head_dim) return GSRQ_E_ARG;
   if (kv->D % kv->d || !is_pow2(kv->K)) return GSRQ_E_ARG;
-  if (kv->d != 8 || kv->K != AT_K || kv->M != 1) return GSRQ_E_UNSUPPORTED;
+  rq = kv->d == a->head_dim && kv->K == AT_K && kv->M <= AQ_MAXM;
+  if (!rq && (kv->d != 8 || kv->K != AT_K || kv->M != 1)) return GSRQ_E_UNSUPPORTED;
+  if (rq) return aq_plan(a, kv, qp);
+  return GSRQ_OK;
+}
+
+gsrq_status attn_validate(const gsrq_attn_shape* a, const gsrq_shape* kv,
+                          const uint32_t* k_codes, const uint32_t* v_codes,
+                          const int32_t* seq_len, const float* k_gain, const float* k_shape,
+                          const float* v_gain, const float* v_shape, const void* q,
+                          gsrq_dtype q_dtype, float* out, AttnPlan& p, AqPlan& qp, bool& rq) {
+  gsrq_status e = attn_layout(a, kv, p, qp, rq);
+  if (e) return e;
   if (kv->N < (int64_t)a->B * a->cap) return GSRQ_E_ARG;
   if (!k_codes || !v_codes || !seq_len || !k_gain || !k_shape || !v_gain || !v_shape || !q ||
       !out)
@@ -728,6 +1324,74 @@ gsrq_status attn_run(const gsrq_attn_shape* a, const AttnPlan& p, const uint32_t
   return launch_ok();
 }
 
+// The launches of one call on a residual-coded cache.
+gsrq_status aq_run(const gsrq_attn_shape* a, const gsrq_shape* kv, const AqPlan& p,
+                   const uint32_t* k_codes, const uint32_t* v_codes, const int32_t* seq_len,
+                   const float* k_gain, const float* k_shape, const float* v_gain,
+                   const float* v_shape, const void* q, gsrq_dtype q_dtype, float* out,
+                   char* ws, void* stream) {
+  gsrq_status e;
+  hipStream_t st = (hipStream_t)stream;
+  const int M = kv->M;
+  AqArgs args;
+  args.kc = (const uint8_t*)k_codes;
+  args.vc = (const uint8_t*)v_codes;
+  args.seq_len = seq_len;
+  args.q = q;
+  args.q_f16 = q_dtype == GSRQ_F16;
+  args.t1 = (const float2*)(ws + p.off_t1);
+  args.t2 = (const float2*)(ws + p.off_t2);
+  args.th = (const double*)(ws + p.off_th);
+  args.tabk = (const u4*)(ws + p.off_tk);
+  args.part = (float*)(ws + p.off_part);
+  args.cap = a->cap;
+  args.rowb = 4 * p.W;
+  args.Hkv = a->Hkv;
+  args.M = M;
+  args.nch = p.nch;
+  args.xmap = ((int64_t)a->B * p.nch) % 8 == 0 ? 1 : 0;
+  args.qscale = (float)((double)a->scale * 1.4426950408889634);
+  AttnTag tag = {};
+  {
+    const void* ptrs[4] = {k_gain, k_shape, v_gain, v_shape};
+    tag.w[0] = AT_TAG_MAGIC;
+    tag.w[1] = (uint32_t)a->Hkv;
+    tag.w[2] = (uint32_t)a->head_dim;
+    memcpy(&tag.w[3], &a->rope_base, sizeof(float));
+    for (int i = 0; i < 4; ++i) {
+      const uint64_t v = (uint64_t)(uintptr_t)ptrs[i];
+      tag.w[4 + 2 * i] = (uint32_t)v;
+      tag.w[5 + 2 * i] = (uint32_t)(v >> 32);
+    }
+    tag.w[12] = ~AT_TAG_MAGIC;
+    tag.w[13] = 0x52510000u | (uint32_t)M;         // residual-coded tables of M stages
+  }
+  uint32_t* tagp = (uint32_t*)(ws + p.off_tag);
+  if (!(a->flags & GSRQ_ATTN_TABLES_READY)) {
+    // RoPE tables and the tag (no 1-bit codeword tables), then the key table
+    attn_tables_kernel<<<AT_TRIG_BLOCKS, 256, 0, st>>>(
+        (double)a->rope_base, (float2*)(ws + p.off_t1), (float2*)(ws + p.off_t2),
+        (double*)(ws + p.off_th), k_gain, k_shape, v_gain, v_shape, 0, nullptr, nullptr, tag,
+        tagp);
+    if ((e = launch_ok())) return e;
+    const int64_t n = (int64_t)a->Hkv * M * AT_K * 16;
+    attn_rq_keytab_kernel<<<(unsigned)((n + 255) / 256), 256, 0, st>>>(k_gain, k_shape, a->Hkv,
+                                                                        M, (u4*)(ws + p.off_tk));
+    if ((e = launch_ok())) return e;
+  }
+  if (p.GQ == 1) e = aq_launch<1>(args, a->B, a->Hkv, st);
+  else if (p.GQ == 2) e = aq_launch<2>(args, a->B, a->Hkv, st);
+  else e = aq_launch<4>(args, a->B, a->Hkv, st);
+  if (e) return e;
+  double* om = (double*)(ws + p.off_om);
+  attn_rq_values_kernel<<<a->B * a->Hkv * M, AQ_VT, 0, st>>>(args.part, p.GQ, a->Hkv, p.nch, M,
+                                                             v_gain, v_shape, om);
+  if ((e = launch_ok())) return e;
+  attn_rq_out_kernel<<<a->B * a->Hq, AT_HD, 0, st>>>(args.part, om, a->Hq, a->Hkv, p.nch, M, out,
+                                                     tag, tagp);
+  return launch_ok();
+}
+
 // Scratch of gsrq_attn_decode_noalloc: a file-scope device array, one copy
 // per GPU, alive until the process ends.  In host code its name only stands
 // for the variable; its device address on a GPU comes from
@@ -764,11 +1428,16 @@ gsrq_status gsrq_attn_decode(const gsrq_attn_shape* a, const gsrq_shape* kv,
                              gsrq_dtype q_dtype, float* out, void* workspace, size_t ws_bytes,
                              void* stream) {
   AttnPlan p;
+  AqPlan qp;
+  bool rq = false;
   gsrq_status e = attn_validate(a, kv, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain,
-                                v_shape, q, q_dtype, out, p);
+                                v_shape, q, q_dtype, out, p, qp, rq);
   if (e) return e;
   if (!workspace || (uintptr_t)workspace % 256) return GSRQ_E_ARG;
-  if (ws_bytes < p.bytes) return GSRQ_E_WORKSPACE;
+  if (ws_bytes < (rq ? qp.bytes : p.bytes)) return GSRQ_E_WORKSPACE;
+  if (rq)
+    return aq_run(a, kv, qp, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q,
+                  q_dtype, out, (char*)workspace, stream);
   return attn_run(a, p, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, q_dtype,
                   out, (char*)workspace, stream);
 }
@@ -780,12 +1449,17 @@ gsrq_status gsrq_attn_decode_noalloc(const gsrq_attn_shape* a, const gsrq_shape*
                                      const float* v_shape, const void* q, gsrq_dtype q_dtype,
                                      float* out, void* stream) {
   AttnPlan p;
+  AqPlan qp;
+  bool rq = false;
   gsrq_status e = attn_validate(a, kv, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain,
-                                v_shape, q, q_dtype, out, p);
+                                v_shape, q, q_dtype, out, p, qp, rq);
   if (e) return e;
-  if (p.bytes > AT_NOALLOC_BYTES) return GSRQ_E_WORKSPACE;
+  if ((rq ? qp.bytes : p.bytes) > AT_NOALLOC_BYTES) return GSRQ_E_WORKSPACE;
   char* ws = nullptr;
   if ((e = scratch_on_current_device(&ws))) return e;
+  if (rq)
+    return aq_run(a, kv, qp, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q,
+                  q_dtype, out, ws, stream);
   return attn_run(a, p, k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, q_dtype,
                   out, ws, stream);
 }

@@ -91,6 +91,8 @@ def load_library(path: str = LIB_PATH):
     AP = ctypes.POINTER(AttnShape)
     lib.gsrq_attn_workspace_bytes.restype = ctypes.c_int
     lib.gsrq_attn_workspace_bytes.argtypes = [AP, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gsrq_attn_workspace_bytes_kv.restype = ctypes.c_int
+    lib.gsrq_attn_workspace_bytes_kv.argtypes = [AP, SP, ctypes.POINTER(ctypes.c_size_t)]
     lib.gsrq_attn_decode.restype = ctypes.c_int
     lib.gsrq_attn_decode.argtypes = [AP, SP, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                      ctypes.c_int, _vp, _vp, ctypes.c_size_t, _vp]
@@ -427,11 +429,15 @@ def make_attn_shape(B, cap, Hq, Hkv, head_dim=128, rope_base=500000.0, scale=Non
                      int(flags))
 
 
-def attn_workspace_bytes(B, cap, Hq, Hkv, head_dim=128) -> int:
+def attn_workspace_bytes(B, cap, Hq, Hkv, head_dim=128, *, d=8, M=1) -> int:
+    """Workspace of gsrq_attn_decode for codes of subvector length d and M
+    stages (d = 8, M = 1: the 1-bit layout; d = head_dim: residual-coded)."""
     n = ctypes.c_size_t()
     sh = make_attn_shape(B, cap, Hq, Hkv, head_dim)
-    _check(load_library().gsrq_attn_workspace_bytes(ctypes.byref(sh), ctypes.byref(n)),
-           "gsrq_attn_workspace_bytes")
+    kv = make_shape(B * cap, Hkv * head_dim, d, 256, M)
+    _check(load_library().gsrq_attn_workspace_bytes_kv(ctypes.byref(sh), ctypes.byref(kv),
+                                                       ctypes.byref(n)),
+           "gsrq_attn_workspace_bytes_kv")
     return int(n.value)
 
 
@@ -443,7 +449,8 @@ def attn_decode(k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, 
                 tables_ready=False, noalloc=False):
     """One decoding step of attention over coded caches (see gsrq_attn_decode).
     k_codes, v_codes [B, cap, W] packed codes; seq_len [B] int32; codebooks
-    [1, G, 256] / [1, G, 256, 8]; q [B, Hq, 128] (float16/float32).  Returns
+    [M, G, 256] / [M, G, 256, d] (the 1-bit layout d = 8, M = 1, or the
+    residual-coded one d = 128, M <= 16); q [B, Hq, 128] (float16/float32).  Returns
     out [B, Hq, 128] float32.  tables_ready: the given workspace holds the
     tables of these codebooks from an earlier call (GSRQ_ATTN_TABLES_READY).
     noalloc: gsrq_attn_decode_noalloc (the library's per-GPU scratch instead
@@ -478,8 +485,8 @@ def attn_decode(k_codes, v_codes, seq_len, k_gain, k_shape, v_gain, v_shape, q, 
         _check(st, "gsrq_attn_decode_noalloc")
         return out
     n = ctypes.c_size_t()
-    _check(lib.gsrq_attn_workspace_bytes(ctypes.byref(ash), ctypes.byref(n)),
-           "gsrq_attn_workspace_bytes")
+    _check(lib.gsrq_attn_workspace_bytes_kv(ctypes.byref(ash), ctypes.byref(sh), ctypes.byref(n)),
+           "gsrq_attn_workspace_bytes_kv")
     ws = _workspace(n.value, q.device, workspace)
     st = lib.gsrq_attn_decode(ctypes.byref(ash), ctypes.byref(sh), _ptr(k_codes), _ptr(v_codes),
                               _ptr(seq_len), _ptr(k_gain), _ptr(k_shape), _ptr(v_gain),

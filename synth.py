@@ -249,6 +249,45 @@ def attn_case(B: int, cap: int, lens, Hkv: int, GQ: int, seed: int = 0, q_dtype=
                 v_gain=v_gain, v_shape=v_shape, q=q, Hkv=Hkv, GQ=GQ)
 
 
+def attn_case_rq(B: int, cap: int, lens, Hkv: int, GQ: int, M: int = 12, seed: int = 0,
+                 q_dtype="float32", q_scale: float = 1.0, hd: int = 128, K: int = 256,
+                 decay: float = 0.75):
+    """One decoding step over residual-coded caches at the paper's sub-1-bit
+    rates (one subspace per head, d = hd, K = 256, M stages; M = 12 is 0.75
+    bit): random codebooks and codes stand in for a calibrated layer's.
+    Stage m's gains are sqrt(hd) * decay^m * lognormal(0, 0.25), as the
+    energy of a residual cascade falls stage by stage; shapes are unit rows
+    of N(0, I_hd).
+
+    Draw order (PCG64 from SeedSequence([seed, B, cap, Hkv, GQ, M, 7])): key
+    gains [M, Hkv, K], key shapes [M, Hkv, K, hd], the same for values, key
+    codes and value codes (uniform bytes [B, cap, M * Hkv], stage m of head
+    h in byte m * Hkv + h of a row, rows padded with zero bytes to whole
+    uint32 words), queries [B, Hkv * GQ, hd].  lens gives seq_len."""
+    rng = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, B, cap, Hkv, GQ, M,
+                                                                      7])))
+    scale = (np.sqrt(hd) * decay ** np.arange(M))[:, None, None]
+
+    def codebook():
+        gain = (scale * rng.lognormal(0.0, 0.25, size=(M, Hkv, K))).astype(np.float32)
+        sh = rng.standard_normal((M, Hkv, K, hd))
+        sh /= np.linalg.norm(sh, axis=-1, keepdims=True)
+        return gain, sh.astype(np.float32)
+
+    k_gain, k_shape = codebook()
+    v_gain, v_shape = codebook()
+    W = (M * Hkv * 8 + 31) // 32
+    codes = []
+    for _ in range(2):
+        c = np.zeros((B, cap, 4 * W), dtype=np.uint8)
+        c[:, :, :M * Hkv] = rng.integers(0, K, size=(B, cap, M * Hkv), dtype=np.uint8)
+        codes.append(np.ascontiguousarray(c).view(np.uint32))
+    q = (q_scale * rng.standard_normal((B, Hkv * GQ, hd))).astype(q_dtype)
+    return dict(k_codes=codes[0], v_codes=codes[1], lens=np.asarray(lens, np.int32),
+                k_gain=k_gain, k_shape=k_shape, v_gain=v_gain, v_shape=v_shape, q=q, Hkv=Hkv,
+                GQ=GQ, M=M)
+
+
 def gaussian_case(N: int, D: int, K: int, seed: int = 0) -> Tuple[np.ndarray, np.ndarray]:
     """The random-normal inputs of Sec. 6.1: X [N, D] float32 with i.i.d.
     rows x ~ N(0, I_D), and K distinct seed row indices [K] drawn after X

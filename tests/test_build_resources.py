@@ -20,11 +20,15 @@ HOT = re.compile(r"(assign_accumulate_kernel|encode_kernel|decode_lds_kernel|fin
                  r"w_score_kernel|w_accumulate_kernel|w_exact_kernel|w_decode|w_encode_fused|"
                  r"wnorm_kernel|wselect_kernel|attn_merge_kernel)")
 MAX_SCRATCH = 16   # bytes per lane
+# The single-stage narrow encoder runs three waves per SIMD (168 registers)
+# and keeps some set-up values of its prologue in scratch: allowed, provided
+# that no scratch access lies inside a loop (its block loop reloads nothing).
+PROLOGUE_ONLY = re.compile(r"13encode_kernel")
 # Kernels allowed to spill outside their innermost loop: the decode-attention
-# kernel runs two waves per SIMD (256 registers) and spills a few group-level
-# values (reloaded once per 8 token blocks); its per-block loop (loop depth 2)
-# must touch no scratch.
-LOOP_CHECKED = re.compile(r"attn_chunk_kernel")
+# kernels run two waves per SIMD (256 registers) and spill a few group- or
+# pass-level values (reloaded once per 8 token blocks, or once per stage-pair
+# pass and group); their per-block loop (loop depth 2) must touch no scratch.
+LOOP_CHECKED = re.compile(r"attn_(rq_)?chunk_kernel")
 
 
 def _remarks(src):
@@ -51,7 +55,7 @@ def _remarks(src):
 @pytest.mark.parametrize("tu", BUILD.SRCS)
 def test_hot_kernels_do_not_spill(tu):
     scratch = _remarks(tu)
-    hot = {k: v for k, v in scratch.items() if HOT.search(k)}
+    hot = {k: v for k, v in scratch.items() if HOT.search(k) and not PROLOGUE_ONLY.search(k)}
     assert hot, "no hot kernels found in the resource remarks"
     bad = {k: v for k, v in hot.items() if v > MAX_SCRATCH}
     assert not bad, f"kernels spilling to scratch: {bad}"
@@ -97,6 +101,16 @@ def _scratch_loop_depths(src):
 def test_attention_block_loop_does_not_spill():
     src = [f for f in BUILD.SRCS if f.endswith("gsrq_attn.hip")][0]
     depths = {k: v for k, v in _scratch_loop_depths(src).items() if LOOP_CHECKED.search(k)}
-    assert len(depths) == 3, sorted(depths)            # GQ = 1, 2, 4
+    assert len(depths) == 6, sorted(depths)            # GQ = 1, 2, 4; 1-bit and residual
     bad = {k: max(v) for k, v in depths.items() if v and max(v) >= 2}
     assert not bad, f"scratch accesses inside the token-block loop: {bad}"
+
+
+@pytest.mark.skipif(shutil.which("hipcc") is None and not os.path.exists("/opt/rocm/bin/hipcc"),
+                    reason="hipcc not available")
+def test_encoder_scratch_only_in_prologue():
+    src = [f for f in BUILD.SRCS if f.endswith("gsrq.hip")][0]
+    depths = {k: v for k, v in _scratch_loop_depths(src).items() if PROLOGUE_ONLY.search(k)}
+    assert len(depths) >= 4, sorted(depths)            # float16 / float32 rows, both loaders
+    bad = {k: max(v) for k, v in depths.items() if v and max(v) >= 1}
+    assert not bad, f"scratch accesses inside a loop of the encoder: {bad}"
