@@ -862,6 +862,11 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_rq_chunk_kernel(AqArgs a) 
       // the pair's table (16 u4 per thread) and the chunk's code bytes of
       // the pair's stages (16 per thread, token t stage sl at 2 t + sl),
       // every load issued before the first store
+      // the thread index made opaque per pass, so that the addresses
+      // derived from it are recomputed here rather than hoisted out of the
+      // pass loop and held (spilled) across it
+      int tq = tid;
+      asm volatile("" : "+v"(tq));
       const u4* src = a.tabk + ((size_t)hk * M + s0) * AT_K * 16;
       const int n = (two ? 2 : 1) * AT_K * 16;       // a single stage's pass: stage 1 zero
       constexpr int PER = AQ_TAB_U4 / AT_THREADS;
@@ -870,23 +875,30 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_rq_chunk_kernel(AqArgs a) 
       uint32_t cb[PERC];
 #pragma unroll
       for (int r = 0; r < PER; ++r) {
-        const int e = min(r * AT_THREADS + tid, n - 1);
+        const int e = min(r * AT_THREADS + tq, n - 1);
         v[r] = src[e];
       }
+      {
+        const int sl = tq & 1, s = s0 + (two ? sl : 0);
+        const uint8_t* cp0 = kcb + (size_t)s * a.Hkv;
 #pragma unroll
-      for (int r = 0; r < PERC; ++r) {
-        const int e = r * AT_THREADS + tid, t = e >> 1, sl = e & 1;
-        const int row = min(tok0 + t, len - 1);
-        cb[r] = kcb[(size_t)row * a.rowb + (s0 + (two ? sl : 0)) * a.Hkv];
+        for (int r = 0; r < PERC; ++r) {
+          const int row = min(tok0 + r * (AT_THREADS / 2) + (tq >> 1), len - 1);
+          cb[r] = cp0[(size_t)row * a.rowb];
+        }
       }
-#pragma unroll
-      for (int r = 0; r < PER; ++r) {
-        const int e = r * AT_THREADS + tid;
+      {
+        // entry e = r * AT_THREADS + tid is chunk tid % 16 of codeword
+        // (tid / 16 + 32 r) % 256 of stage r / 8; 32 r leaves the chunk
+        // rotation (c + k) % 16 unchanged, so its slot is base + 512 r
+        const int kq = tq >> 4, c = tq & 15;
+        u4* dst = ktab + (kq << 4) + ((c + kq) & 15);
         const u4 z = {0u, 0u, 0u, 0u};
-        ktab[aq_slot(e >> 12, (e >> 4) & 255, e & 15)] = e < n ? v[r] : z;
+#pragma unroll
+        for (int r = 0; r < PER; ++r) dst[512 * r] = r * AT_THREADS + tq < n ? v[r] : z;
       }
 #pragma unroll
-      for (int r = 0; r < PERC; ++r) kcl[r * AT_THREADS + tid] = (uint8_t)cb[r];
+      for (int r = 0; r < PERC; ++r) kcl[r * AT_THREADS + tq] = (uint8_t)cb[r];
     }
     __syncthreads();
 #pragma unroll
@@ -1067,6 +1079,7 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_rq_chunk_kernel(AqArgs a) 
 // sum_c 2^(m_c,h - M_h) W_c,h[k] (float64), then contracted with the
 // stage's value codewords fl(g s): o_m,h[n] = sum_k W_h[k] fl(g_k s_kn).
 constexpr int AQ_VT = 256;
+constexpr int AQ_VCH = 64;      // chunks merged per round (LDS factors [4][AQ_VCH])
 __global__ void __launch_bounds__(AQ_VT) attn_rq_values_kernel(const float* __restrict__ part,
                                                                int GQ, int Hkv, int nch, int M,
                                                                const float* __restrict__ vg,
@@ -1074,39 +1087,76 @@ __global__ void __launch_bounds__(AQ_VT) attn_rq_values_kernel(const float* __re
                                                                double* __restrict__ om) {
   __shared__ double wb[4][AT_K];
   __shared__ double hs[4][AT_HD];
+  __shared__ double fac[4][AQ_VCH];
+  __shared__ float mrefs[4];
+  __shared__ float gl[AT_K];
   const int m = blockIdx.x % M, hk = (blockIdx.x / M) % Hkv, b = blockIdx.x / (M * Hkv);
   const int tid = threadIdx.x;
   const int RS = M * AT_K + 2;
   const float* p0 = part + ((size_t)b * Hkv + hk) * nch * GQ * RS;
   const size_t cs = (size_t)GQ * RS;
-  for (int h = 0; h < GQ; ++h) {
-    const float* p = p0 + (size_t)h * RS;
-    float mref = -INFINITY;
-    for (int c = 0; c < nch; ++c) {
-      const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
-      mref = lc > 0.f ? fmaxf(mref, mc) : mref;
-    }
-    double s = 0.0;
-    for (int c = 0; c < nch; ++c) {
-      const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
-      const float bv = p[c * cs + m * AT_K + tid];
-      s += lc > 0.f ? exp2((double)mc - (double)mref) * (double)bv : 0.0;
-    }
-    wb[h][tid] = s;
-  }
-  __syncthreads();
-  // thread (half, n): codewords half * 128 .. + 127, element n of each
-  const int n = tid & (AT_HD - 1), half = tid >> 7;
   const size_t cb = ((size_t)m * Hkv + hk) * AT_K;
-  const float* gp = vg + cb;
+  gl[tid] = vg[cb + tid];                            // the stage's gains
+  // reference per head: the largest chunk reference among chunks with tokens
+  if (tid < GQ) {
+    const float* p = p0 + (size_t)tid * RS;
+    float mr = -INFINITY;
+    for (int c = 0; c < nch; ++c) {
+      const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
+      mr = lc > 0.f ? fmaxf(mr, mc) : mr;
+    }
+    mrefs[tid] = mr;
+  }
+  double acc[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int c0 = 0; c0 < nch; c0 += AQ_VCH) {
+    const int nc = min(AQ_VCH, nch - c0);
+    __syncthreads();                                 // mrefs written, previous factors read
+    if (tid < GQ * nc) {
+      const int h = tid / nc, c = c0 + tid % nc;
+      const float* p = p0 + (size_t)h * RS + c * cs;
+      const float mc = p[M * AT_K], lc = p[M * AT_K + 1];
+      fac[h][tid % nc] = lc > 0.f ? exp2((double)mc - (double)mrefs[h]) : 0.0;
+    }
+    __syncthreads();
+    // thread k: codeword k of stage m, every head, the round's chunks (all
+    // loads of a head's chunks issued together)
+    for (int h = 0; h < GQ; ++h) {
+      const float* p = p0 + (size_t)h * RS + (size_t)m * AT_K + tid;
+      constexpr int UN = 8;
+      for (int c1 = 0; c1 < nc; c1 += UN) {
+        float bv[UN];
+#pragma unroll
+        for (int u = 0; u < UN; ++u) bv[u] = p[(size_t)(c0 + min(c1 + u, nc - 1)) * cs];
+#pragma unroll
+        for (int u = 0; u < UN; ++u)
+          if (c1 + u < nc) {
+            // a chunk without tokens (factor 0) never wrote its bins: the
+            // slots hold stale workspace contents, kept out of the sum
+            const double f = fac[h][c1 + u];
+            acc[h] += f > 0.0 ? f * (double)bv[u] : 0.0;
+          }
+      }
+    }
+  }
+  for (int h = 0; h < GQ; ++h) wb[h][tid] = acc[h];
+  __syncthreads();
+  // contraction: thread (half, n) takes codewords half * 128 .. + 127,
+  // element n of each, 16 loads in flight
+  const int n = tid & (AT_HD - 1), half = tid >> 7;
   const float* sp = vs + cb * AT_HD + n;
   double o[4] = {0.0, 0.0, 0.0, 0.0};
-#pragma unroll 16
-  for (int k = half * 128; k < half * 128 + 128; ++k) {
-    const double cw = (double)(gp[k] * sp[(size_t)k * AT_HD]);   // fl(g s)
+  constexpr int UK = 16;
+  for (int k0 = half * 128; k0 < half * 128 + 128; k0 += UK) {
+    float sv[UK];
 #pragma unroll
-    for (int h = 0; h < 4; ++h)
-      if (h < GQ) o[h] = fma(wb[h][k], cw, o[h]);
+    for (int u = 0; u < UK; ++u) sv[u] = sp[(size_t)(k0 + u) * AT_HD];
+#pragma unroll
+    for (int u = 0; u < UK; ++u) {
+      const double cw = (double)(gl[k0 + u] * sv[u]);                // fl(g s)
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        if (h < GQ) o[h] = fma(wb[h][k0 + u], cw, o[h]);
+    }
   }
   if (half) {
 #pragma unroll
