@@ -28,12 +28,19 @@ METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline
 # scaled x2.000 and writes x1.000 against a 256 MiB reference copy).  Valid
 # only for the kernel source those passes measured; other workloads: null.
 TRAFFIC = {
-    "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "b9e95e6ffcbefa9f",
-                             "bytes_per_launch": 116571824},
-    "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "9e1c64146ab1d392",
-                            "bytes_per_launch": 411513874},
-    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "581f5ff42648ad4d",
-                              "bytes_per_launch": 89589400},
+    "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "0d014ab61c969346",
+                             "bytes_per_launch": 116569746},
+    "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",
+                            "bytes_per_launch": 350753513},
+    "paper_rates_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",
+                         "bytes_per_launch": 141466069},
+    "rate_sweep_d16": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",
+                       "bytes_per_launch": 290122945},
+    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "9f651509c117ea68",
+                              "bytes_per_launch": 89573888},
+    "decode_attention_075bit": {"source": "gsrq_attn.hip",
+                                "source_sha256_prefix": "9f651509c117ea68",
+                                "bytes_per_launch": 177593902},
 }
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E
