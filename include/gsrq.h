@@ -213,10 +213,13 @@ gsrq_status gsrq_encode_prepare(const gsrq_shape* s, const float* gain, const fl
 
 /*
  * gsrq_encode_prepared -- gsrq_encode (same codes, residual and index
- * agreement) with the tables and codebook of a prepared codebook; no
- * workspace.  M <= 8 stages.  The kernel checks the header against s: a
- * buffer not prepared for this shape (or not prepared at all) gives code
- * fields of all ones and a NaN residual instead of plausible codes.
+ * agreement, bit for bit) with the tables and codebook of a prepared
+ * codebook; no workspace.  M <= 8 stages.  Up to 256 rows it runs a
+ * latency kernel (one wave per 32-row block and subspace, nothing shared,
+ * every load of a stage issued together); above that the stage-fused
+ * encoder.  The kernel checks the header against s: a buffer not prepared
+ * for this shape (or not prepared at all) gives code fields of all ones
+ * and a NaN residual instead of plausible codes.
  */
 gsrq_status gsrq_encode_prepared(const gsrq_shape* s, const void* X, gsrq_dtype x_dtype,
                                  int64_t ldx, const void* prepared, uint32_t* codes,

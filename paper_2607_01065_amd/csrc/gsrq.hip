@@ -48,6 +48,8 @@ constexpr int ENC_SUBS = 4;            // subspaces per encode workgroup
 constexpr int ENC_WAVES = 12;          // three waves per subspace, one workgroup per CU
 constexpr int ENC_CODES_WORDS = 16384; // LDS-staged code words: stages x chunk rows, at most
 constexpr int ENC_MAX_STAGES = 8;      // stages staged in LDS by one encode launch
+constexpr int ENC_SMALL_ROWS = 256;    // prepared encode of at most this many rows: latency kernel
+constexpr int ENC_SMALL_WAVES = 4;     // (row block, subspace) waves per latency-kernel workgroup
 constexpr int KEY_BITS = 7;               // (tile, slot) bits packed into a key
 
 enum { MODE_INIT = 0, MODE_ITER = 1 };
@@ -252,6 +254,70 @@ __device__ __forceinline__ void exact_rows(unsigned long long mask, const float 
     if ((lane & 31) == L) kstar = bk;
   }
 }
+
+// exact_rows for a codebook in global memory ([K] gains, [K][d] shapes),
+// in two parts: load() fetches this lane's codewords k = lane + 64 j, all in
+// flight together (one memory round trip; the loop form pays one per
+// codeword and per row), and rows() scores the flagged rows with
+// exact_rows' arithmetic, order and tie rule.
+struct ExactCodebook {
+  static constexpr int KJ = KMAX / 64;
+  float cg[KJ], cs[KJ][8];
+  // D8: d == 8 with a 16-byte aligned shape array (two 16-byte loads per
+  // codeword)
+  template <bool D8>
+  __device__ __forceinline__ void load(const float* gain, const float* shape, int d, int K) {
+    const int lane = wave_lane();
+#pragma unroll
+    for (int j = 0; j < KJ; ++j) {
+      const int k = lane + 64 * j;
+      const int kc = k < K ? k : K - 1;
+      cg[j] = gain[kc];
+      if (D8) {
+        const float4* p4 = (const float4*)(shape + (size_t)kc * 8);
+        const float4 u = p4[0], v = p4[1];
+        cs[j][0] = u.x; cs[j][1] = u.y; cs[j][2] = u.z; cs[j][3] = u.w;
+        cs[j][4] = v.x; cs[j][5] = v.y; cs[j][6] = v.z; cs[j][7] = v.w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cs[j][e] = shape[(size_t)kc * d + (e < d ? e : 0)];
+      }
+    }
+  }
+  __device__ __forceinline__ void rows(unsigned long long mask, const float (&x)[8], int d, int K,
+                                       int& kstar) const {
+    const int lane = wave_lane();
+    while (mask) {
+      const int L = __ffsll((long long)mask) - 1;
+      mask &= mask - 1;
+      double xr[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) xr[e] = (double)__shfl(x[e], L);
+      double bd = INFINITY;
+      int bk = 0x7fffffff;
+#pragma unroll
+      for (int j = 0; j < KJ; ++j) {
+        const int k = lane + 64 * j;
+        if (k < K) {
+          const double g = (double)cg[j];
+          double dot = 0.0;
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (e < d) dot = fma(xr[e], (double)cs[j][e], dot);
+          const double dist = fma(-2.0 * g, dot, g * g);
+          if (dist < bd) { bd = dist; bk = k; }
+        }
+      }
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) {
+        const double od = __shfl_xor(bd, off);
+        const int ok = __shfl_xor(bk, off);
+        if (od < bd || (od == bd && ok < bk)) { bd = od; bk = ok; }
+      }
+      if ((lane & 31) == L) kstar = bk;
+    }
+  }
+};
 
 // Eight subvector elements of one row in their storage type, kept packed in
 // registers between a prefetch and their use.
@@ -1131,6 +1197,121 @@ flush:
   }
 }
 
+// Latency encoder for a few rows with a prepared codebook (the tokens
+// appended to a cache at each decoding step): one wave per (32-row block,
+// subspace), no LDS, no barriers and no block claiming, so a launch of 1 to
+// a few hundred rows costs little more than its loads.  The header check,
+// the operand tables of the first stage and the rows are loaded together;
+// the arithmetic is the stage-fused encoder's (same operand tables, same
+// keys, same float64 re-scoring and residual update), so codes and residuals
+// agree with it bit for bit.
+template <typename T, bool VEC>
+__global__ void __launch_bounds__(ENC_SMALL_WAVES * 64) encode_small_kernel(EncodeArgs a) {
+  constexpr bool F16IN = sizeof(T) == 2;
+  const int lane = wave_lane();
+  const int G = a.G, d = a.d, K = a.K;
+  const int wid =
+      __builtin_amdgcn_readfirstlane((int)blockIdx.x * ENC_SMALL_WAVES + (int)(threadIdx.x >> 6));
+  const int g = wid % G, rb = wid / G;
+  const int nblk = (int)((a.N + RB - 1) / RB);
+  if (rb >= nblk) return;   // uniform over the wave; no barrier follows
+  const int i = lane & 31, h = lane >> 5;
+  const int64_t row = (int64_t)rb * RB + i;
+  const bool valid = row < a.N;
+  RowRaw<T, VEC> nx;
+  nx.load((const T*)a.x + (valid ? row : 0) * a.ldx + (int64_t)g * d, d);
+  Tiles tl;
+  {
+    const u4* fr = a.frag + (size_t)g * NT * 2 * 64;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      tl.a1[t] = fr[(t * 2 + 0) * 64 + lane];
+      tl.a2[t] = fr[(t * 2 + 1) * 64 + lane];
+    }
+  }
+  // the header is compared here but acted on only at the stores (a buffer
+  // prepared for another shape is read only where this call's shape places
+  // its parts, and gives all-ones code fields and a NaN residual)
+  uint32_t tag[PREP_WORDS];
+#pragma unroll
+  for (int w = 0; w < PREP_WORDS; ++w) tag[w] = a.ptag[w];
+  int ex = a.sig[g];
+  // one wait for the row, the first stage's tables and the header together
+  // (left to itself the compiler waits for each before it issues the next)
+  {
+    uint32_t* rw = (uint32_t*)nx.v;
+#pragma unroll
+    for (int j = 0; j < (int)sizeof(nx.v) / 4; ++j) asm volatile("" : "+v"(rw[j]));
+#pragma unroll
+    for (int t = 0; t < NT; ++t) asm volatile("" : "+v"(tl.a1[t]), "+v"(tl.a2[t]));
+#pragma unroll
+    for (int w = 0; w < PREP_WORDS; ++w) asm volatile("" : "+v"(tag[w]));
+    asm volatile("" : "+v"(ex));
+  }
+  bool ok = true;
+#pragma unroll
+  for (int w = 0; w < PREP_WORDS; ++w) ok &= tag[w] == a.etag.w[w];
+  float x[8];
+  nx.get(x, d, valid);
+  const u4 raw = nx.raw16(x, valid);
+  for (int m = 0; m < a.M; ++m) {
+    const int cb = m * G + g;
+    if (m > 0) {
+      const u4* fr = a.frag + (size_t)cb * NT * 2 * 64;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        tl.a1[t] = fr[(t * 2 + 0) * 64 + lane];
+        tl.a2[t] = fr[(t * 2 + 1) * 64 + lane];
+      }
+      ex = a.sig[cb];
+    }
+    h8 b1, b2;
+    float rr, ss;
+    bool need_exact;
+    if (F16IN && m == 0)
+      make_b<true>(x, raw, ex, h, b1, b2, rr, need_exact, ss);
+    else
+      make_b<false>(x, raw, ex, h, b1, b2, rr, need_exact, ss);
+    const int key = min_key(tl, b1, b2);
+    float dhat;
+    int kstar = reduce_rows(key, h, dhat);
+    need_exact = need_exact || !(dhat <= ldexpf(rr, SA + 1)) || kstar >= K;
+    const unsigned long long fb = __ballot(valid && need_exact && h == 0);
+    const float* gcb = a.gain + (size_t)cb * K;
+    const float* scb = a.shape + (size_t)cb * K * d;
+    if (fb) {
+      ExactCodebook xc;
+      // VEC implies d == 8; a prepared buffer's shapes are 256-byte aligned
+      xc.load<VEC>(gcb, scb, d, K);
+      xc.rows(fb, x, d, K, kstar);
+    }
+    if (kstar >= K) kstar = K - 1;   // only rows past N can get here
+    if (a.residual || m + 1 < a.M) {
+      const float gk = gcb[kstar];
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (j < d) x[j] = fmaf(-gk, scb[(size_t)kstar * d + j], x[j]);
+    }
+    if (valid && h == 0 && a.codes) {
+      const int64_t t = (int64_t)m * G + g;
+      const uint32_t code = ok ? (uint32_t)kstar : (uint32_t)K - 1u;   // K = 2^b
+      if (a.byte_codes) {
+        ((uint8_t*)(a.codes + row * a.words))[t] = (uint8_t)code;
+      } else {   // words zeroed beforehand
+        const int64_t bit = t * a.b;
+        uint32_t* wp = a.codes + row * a.words + bit / 32;
+        const int off = (int)(bit % 32);
+        atomicOr(wp, code << off);
+        if (off + a.b > 32) atomicOr(wp + 1, code >> (32 - off));
+      }
+    }
+  }
+  if (valid && a.residual && h == 0) {
+    float* dst = a.residual + row * (int64_t)(G * d) + (int64_t)g * d;
+    for (int j = 0; j < d; ++j) dst[j] = ok ? x[j] : __builtin_nanf("");
+  }
+}
+
 struct DecodeArgs {
   const uint32_t* codes;
   int64_t N, ldo;
@@ -1542,6 +1723,17 @@ gsrq_status encode_launch(const gsrq_shape* s, const void* X, int64_t ldx, const
     if ((e = launch_ok())) return e;
     a.frag = frag;
     a.sig = sig;
+  }
+  if (prepared && s->N <= ENC_SMALL_ROWS) {
+    // a few rows: one wave per (row block, subspace), nothing shared
+    const int64_t waves = (s->N + RB - 1) / RB * a.G;
+    const unsigned wgs = (unsigned)((waves + ENC_SMALL_WAVES - 1) / ENC_SMALL_WAVES);
+    TimedLaunch tl(GSRQ_KERNEL_ENCODE, st);
+    if (a.vec_rows)
+      encode_small_kernel<T, true><<<wgs, ENC_SMALL_WAVES * 64, 0, st>>>(a);
+    else
+      encode_small_kernel<T, false><<<wgs, ENC_SMALL_WAVES * 64, 0, st>>>(a);
+    return launch_ok();
   }
   // about one workgroup per CU: rows split into chunks so that the groups
   // of ENC_SUBS subspaces times the chunks fill the 256 CUs once; a chunk's

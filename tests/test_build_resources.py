@@ -16,7 +16,7 @@ import pytest
 
 from paper_2607_01065_amd import build as BUILD
 
-HOT = re.compile(r"(assign_accumulate_kernel|encode_kernel|decode_lds_kernel|finalize_kernel|update_kernel|"
+HOT = re.compile(r"(assign_accumulate_kernel|encode_kernel|encode_small_kernel|decode_lds_kernel|finalize_kernel|update_kernel|"
                  r"w_score_kernel|w_accumulate_kernel|w_exact_kernel|w_decode|w_encode_fused|"
                  r"wnorm_kernel|wselect_kernel|attn_merge_kernel)")
 MAX_SCRATCH = 16   # bytes per lane

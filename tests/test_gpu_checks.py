@@ -287,12 +287,17 @@ def test_attn_workspace_contents_do_not_leak_into_outputs():
 @pytest.mark.parametrize("N,D,d,K,M,dtype", [(1, 1024, 8, 256, 1, np.float16),
                                              (8, 1024, 8, 256, 1, np.float16),
                                              (64, 1024, 8, 256, 2, np.float32),
+                                             (256, 1024, 8, 256, 1, np.float16),
+                                             (257, 1024, 8, 256, 1, np.float16),
+                                             (33, 24, 4, 16, 3, np.float32),
                                              (2049, 256, 8, 256, 3, np.float16),
                                              (777, 24, 4, 16, 2, np.float32)])
 def test_prepared_encode_matches_encode(N, D, d, K, M, dtype):
     """gsrq_encode_prepared gives gsrq_encode's codes and residual bit for
     bit (the same operand tables, built once), including the append sizes
-    1, 8 and 64."""
+    1, 8 and 64: up to 256 rows it runs the latency kernel (one wave per
+    row block and subspace), above that the stage-fused encoder; 4-bit codes
+    (K = 16) are OR'd into zeroed words."""
     say("prepared encode", N, D, d, K, M, dtype.__name__)
     X, w, seeds = synth.small_case(max(N, 2 * K), D, d, K, M, seed=31, dtype=dtype)
     G = D // d
