@@ -74,6 +74,23 @@ __host__ __device__ constexpr int w_sreg(int C) {
              : (w_frags(C) * 64 + W_THREADS - 1) / W_THREADS;
 }
 static_assert(w_sreg(W_CMAX) * W_THREADS >= w_frags(W_CMAX) * 64, "staging holds one tile");
+// Waves of a scoring workgroup.  The streamed hi/lo pass at d <= 128 runs
+// four: each workgroup then scores one round of 128 rows and streams the
+// table once for them, and two or three workgroups share a CU, so that one's
+// row loads and barriers overlap another's MFMAs (eight-wave workgroups held
+// a CU alone).  Resident tables, the single pass and the listed-row pass
+// keep eight.
+__host__ __device__ constexpr int w_score_waves(int C, bool resident, bool sp, bool ind) {
+  return (!resident && !sp && !ind && C <= 16) ? 4 : W_WAVES;
+}
+// Tiles per streamed chunk of the hi/lo pass, and the staged u4 per thread
+// for a workgroup of nth threads.
+__host__ __device__ constexpr int w_stream_tiles(int C) {
+  return W_STREAM_BYTES / (w_frags(C) * 1024) > 1 ? W_STREAM_BYTES / (w_frags(C) * 1024) : 1;
+}
+__host__ __device__ constexpr int w_sreg_n(int C, int nth) {
+  return (w_stream_tiles(C) * w_frags(C) * 64 + nth - 1) / nth;
+}
 // The single pass stages P + 1 fragments per tile through larger chunks
 // (fewer barriers per round); two workgroups per CU still fit in LDS.
 constexpr int W_SP_STREAM_BYTES = 36864;
@@ -86,48 +103,15 @@ __host__ __device__ constexpr int w_sp_sreg(int C) {
 
 // ------------------------------------------------------------------ kernels
 
-// sigma exponent of each codebook: 2^sig >= its largest gain (unit_gain: 1).
-// Also records the codebook's smallest gain (gmin, for the exact kernel's
-// pruning) and its largest one (gmin[ncb + cb], for the single pass's error
-// bound), and clears the deferred-row state of its subspace (xcount,
-// xchanged, xobj) before a scoring launch.
-__global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ gain, int K,
-                                                      int unit_gain, const int* __restrict__ done,
-                                                      int G, int cb0, int* __restrict__ sig,
-                                                      float* __restrict__ gmin,
-                                                      int* __restrict__ xcount,
-                                                      int* __restrict__ xchanged,
-                                                      double* __restrict__ xobj,
-                                                      int* __restrict__ hcount) {
-  __shared__ float wm[4], wn[4];
-  const int cb = cb0 + blockIdx.x;
-  if (done && done[blockIdx.x % G]) return;
-  float m = 0.f, n = INFINITY;
-  for (int k = threadIdx.x; k < K; k += blockDim.x) {
-    const float v = unit_gain ? 1.f : gain[(size_t)cb * K + k];
-    m = fmaxf(m, v);
-    n = fminf(n, v);
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    m = fmaxf(m, __shfl_xor(m, off));
-    n = fminf(n, __shfl_xor(n, off));
-  }
-  if ((threadIdx.x & 63) == 0) {
-    wm[threadIdx.x >> 6] = m;
-    wn[threadIdx.x >> 6] = n;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    sig[cb] = sigma_exp(fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3])));
-    gmin[blockIdx.x] = fminf(fminf(wn[0], wn[1]), fminf(wn[2], wn[3]));
-    gmin[gridDim.x + blockIdx.x] = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
-    xcount[blockIdx.x] = 0;
-    xchanged[blockIdx.x] = 0;
-    xobj[blockIdx.x] = 0.0;
-    if (hcount) hcount[blockIdx.x] = 0;
-  }
-}
+// Per-codebook state the fragment launch writes besides the tables: smallest
+// gain and largest gain ([2][ncb]), and the deferred-row counters it clears.
+struct WDeferPtrs {
+  float* gmin;
+  int* xcount;
+  int* xchanged;
+  double* xobj;
+  int* hcount;   // null: no single pass
+};
 
 // Operand fragments of one 32-codeword tile (grid: tiles x codebooks, one
 // wave).  Lane = codeword c (0..31) + 32 h; lane half h covers the 8-element
@@ -143,10 +127,9 @@ __global__ void __launch_bounds__(256) w_sigma_kernel(const float* __restrict__ 
 template <int P>
 __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ gain,
                                                     const float* __restrict__ shape, int d, int K,
-                                                    int unit_gain,
-                                                    const int* __restrict__ sig,
+                                                    int unit_gain, int* __restrict__ sig,
                                                     const int* __restrict__ done, int G, int cb0,
-                                                    u4* __restrict__ frag) {
+                                                    u4* __restrict__ frag, WDeferPtrs X) {
   const int t = blockIdx.x, tiles = gridDim.x;
   const int cbl = blockIdx.y, cb = cb0 + cbl;
   if (done && done[cbl % G]) return;
@@ -155,8 +138,41 @@ __global__ void __launch_bounds__(64) w_frag_kernel(const float* __restrict__ ga
   const bool real = k < K;
   const int kk = real ? k : K - 1;
   const float g = real ? (unit_gain ? 1.f : gain[(size_t)cb * K + kk]) : 0.f;
-  const int ex = sig[cb];
   const float* s = shape + ((size_t)cb * K + kk) * d;
+  // sigma (from the largest gain) and the smallest gain, found by every
+  // wave of the codebook (max and min are exact in any order, so all agree);
+  // the wave of tile 0 records them and clears the deferred-row state
+  float m = 0.f, n = INFINITY;
+  for (int q0 = 0; q0 < K; q0 += 8 * 64) {
+    // eight loads in flight per lane; indexes past K repeat gain K - 1,
+    // which changes neither extreme
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int q = min(q0 + 64 * u + lane, K - 1);
+      v[u] = unit_gain ? 1.f : gain[(size_t)cb * K + q];
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      m = fmaxf(m, v[u]);
+      n = fminf(n, v[u]);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    m = fmaxf(m, __shfl_xor(m, off));
+    n = fminf(n, __shfl_xor(n, off));
+  }
+  const int ex = sigma_exp(m);
+  if (t == 0 && lane == 0) {
+    sig[cb] = ex;
+    X.gmin[cbl] = n;
+    X.gmin[gridDim.y + cbl] = m;
+    X.xcount[cbl] = 0;
+    X.xchanged[cbl] = 0;
+    X.xobj[cbl] = 0.0;
+    if (X.hcount) X.hcount[cbl] = 0;
+  }
   u4* out = frag + ((size_t)cbl * tiles + t) * (2 * P + 1) * 64;
   float sv[P][8];
 #pragma unroll
@@ -661,12 +677,12 @@ __device__ __forceinline__ void w_take2(int b, int s, int t, int& best, int& bt,
 // fixed per thread, computed once).  The loads never branch: a slot past
 // the chunk's last tile reads that tile again and is never stored, so the
 // loads stay in flight while the current chunk is scored.
-template <int QU, int SR> struct WStage {
+template <int QU, int SR, int NTH = W_THREADS> struct WStage {
   int tr[SR], o[SR];
   __device__ __forceinline__ WStage() {
 #pragma unroll
     for (int r = 0; r < SR; ++r) {
-      const int e = r * W_THREADS + (int)threadIdx.x;
+      const int e = r * NTH + (int)threadIdx.x;
       tr[r] = e / (QU * 64);
       o[r] = e - tr[r] * (QU * 64);
     }
@@ -678,11 +694,11 @@ template <int QU, int SR> struct WStage {
       reg[r] = ftab[(uint32_t)((t0 + min(tr[r], nt - 1)) * QF * 64 + o[r])];
   }
 };
-template <int SR>
+template <int SR, int NTH = W_THREADS>
 __device__ __forceinline__ void w_stage_store(u4* buf, int n, const u4 (&reg)[SR]) {
 #pragma unroll
   for (int r = 0; r < SR; ++r) {
-    const int e = r * W_THREADS + (int)threadIdx.x;
+    const int e = r * NTH + (int)threadIdx.x;
     if (e < n) buf[e] = reg[r];
   }
 }
@@ -783,10 +799,13 @@ __device__ __forceinline__ void w_put_code(uint32_t* wp, int64_t bit, int b, int
 // atomic minimum (lowest codeword on equal keys); w_listed_finish_kernel
 // then writes the outputs.
 template <typename T, int C, int MODE, bool RESIDENT, bool SP, bool IND>
-__global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
+__global__ void __launch_bounds__(w_score_waves(C, RESIDENT, SP, IND) * 64, (RESIDENT && C <= 4) ? 4 : 2)
     w_score_kernel(WScoreArgs a) {
+  constexpr int NW = w_score_waves(C, RESIDENT, SP, IND);
+  constexpr int NTH = NW * 64;
+  constexpr int WR = NW * RB;   // rows of a round per row block of the waves
   extern __shared__ __align__(16) u4 wtab[];
-  __shared__ double red_obj[W_WAVES];
+  __shared__ double red_obj[NW];
   __shared__ int red_changed;
   constexpr bool F16 = sizeof(T) == 2;
   constexpr int P = w_pairs(C);
@@ -820,8 +839,8 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   if (a.done && a.done[g]) return;
   // indirect rows: this workgroup takes rounds rc, rc + nwg, ... of the list
   const int hcnt = IND ? a.hcount[g] : 0;
-  if (IND && rc * W_ROWS >= hcnt) return;
-  const int nrounds = IND ? (hcnt - rc * W_ROWS + a.nwg * W_ROWS - 1) / (a.nwg * W_ROWS)
+  if (IND && rc * WR >= hcnt) return;
+  const int nrounds = IND ? (hcnt - rc * WR + a.nwg * WR - 1) / (a.nwg * WR)
                           : a.rounds;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int i = lane & 31, h = lane >> 5;
@@ -844,7 +863,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   if (tid == 0) red_changed = 0;
   if (RESIDENT) {
     const int n = tiles * QU * 64;
-    for (int e = tid; e < n; e += W_THREADS) {
+    for (int e = tid; e < n; e += NTH) {
       const int t = e / (QU * 64), o = e - t * (QU * 64);
       wtab[e] = ftab[(size_t)t * a.QF * 64 + o];
     }
@@ -857,11 +876,11 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
   // or within the list)
   auto row_of = [&](int rd, int r, bool& valid) -> int64_t {
     if (IND) {
-      const int idx = (rc + rd * a.nwg) * W_ROWS + wave * RB + i;
+      const int idx = (rc + rd * a.nwg) * WR + wave * RB + i;
       valid = idx < hcnt;
       return a.hrows[(size_t)g * a.N + (valid ? idx : 0)];
     }
-    const int64_t row = ((int64_t)rc * a.rounds + rd) * (W_ROWS * R) +
+    const int64_t row = ((int64_t)rc * a.rounds + rd) * (WR * R) +
                         (int64_t)(wave * R + r) * RB + i;
     valid = row < a.N;
     return row;
@@ -945,13 +964,13 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
       const int tpc = a.tpc;
       const int nch = (tiles + tpc - 1) / tpc;
       const int chunk_u4 = tpc * QU * 64;
-      constexpr int SR = SP ? w_sp_sreg(C) : w_sreg(C);
-      const WStage<QU, SR> stg;
+      constexpr int SR = SP ? w_sp_sreg(C) : (NW == W_WAVES ? w_sreg(C) : w_sreg_n(C, NTH));
+      const WStage<QU, SR, NTH> stg;
       u4 reg[SR];
       {
         const int nt0 = min(tpc, tiles);
         stg.load(ftab, a.QF, 0, nt0, reg);
-        w_stage_store(wtab, nt0 * QU * 64, reg);
+        w_stage_store<SR, NTH>(wtab, nt0 * QU * 64, reg);
       }
       __syncthreads();
       for (int c = 0; c < nch; ++c) {
@@ -963,7 +982,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
         const u4* buf = wtab + (size_t)(c & 1) * chunk_u4;
         for (int tt = 0; tt < nt; tt += (PAIR_TILES ? 2 : 1))
           score(buf + (size_t)tt * QU * 64 + lane, tb + t0 + tt, PAIR_TILES && tt + 1 < nt);
-        if (n_next) w_stage_store(wtab + (size_t)((c + 1) & 1) * chunk_u4, n_next, reg);
+        if (n_next) w_stage_store<SR, NTH>(wtab + (size_t)((c + 1) & 1) * chunk_u4, n_next, reg);
         __syncthreads();
       }
     }
@@ -1010,7 +1029,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
         // decides the row (64-bit keys: the distance key with its sign bit
         // flipped, so signed order is unsigned order, then the codeword)
         if (valid[r] && h == 0) {
-          const size_t idx = (size_t)g * a.N + (size_t)((rc + rd * a.nwg) * W_ROWS + wave * RB + i);
+          const size_t idx = (size_t)g * a.N + (size_t)((rc + rd * a.nwg) * WR + wave * RB + i);
           const uint32_t hv = (uint32_t)(__float_as_int(dhat) >> 4) ^ 0x80000000u;
           atomicMin(a.hbest + idx, ((unsigned long long)hv << 32) | (uint32_t)kstar);
           if (slice == 0) a.hrr[idx] = need_exact[r] ? -1.f : rr[r];
@@ -1089,7 +1108,7 @@ __global__ void __launch_bounds__(W_THREADS, (RESIDENT && C <= 4) ? 4 : 2)
     __syncthreads();
     if (tid == 0) {
       double s = 0.0;
-      for (int w = 0; w < W_WAVES; ++w) s += red_obj[w];
+      for (int w = 0; w < NW; ++w) s += red_obj[w];
       a.changed[(size_t)g * a.nwg + rc] = red_changed;
       if (a.obj) a.obj[(size_t)g * a.nwg + rc] = s;
     }
@@ -2595,7 +2614,8 @@ WLayout w_score_layout(const gsrq_shape* s, size_t x_elt, bool f16rows, bool hp 
   // single pass: two workgroups per CU share 160 KiB of LDS
   L.resident = used <= (size_t)(L.sp ? W_SP_RESIDENT_BYTES : W_RESIDENT_BYTES);
   // rows per workgroup round: W_ROWS per row block a wave scores at once
-  const int64_t rows_round = (int64_t)W_ROWS * w_row_blocks(L.C, L.resident, L.sp, false);
+  const int64_t rows_round = (int64_t)RB * w_score_waves(L.C, L.resident, L.sp, false) *
+                             w_row_blocks(L.C, L.resident, L.sp, false);
   const int64_t row_rounds = (s->N + rows_round - 1) / rows_round;
   if (L.resident) {
     // enough rounds per workgroup to amortise the table load, while
@@ -2634,9 +2654,11 @@ gsrq_status w_score_launch_v(const WScoreArgs& a, const WLayout& L, hipStream_t 
           hipSuccess)
     return GSRQ_E_HIP;
   if (L.resident)
-    w_score_kernel<T, C, MODE, true, SP, IND><<<grid, W_THREADS, L.lds, st>>>(a);
+    w_score_kernel<T, C, MODE, true, SP, IND>
+        <<<grid, w_score_waves(C, true, SP, IND) * 64, L.lds, st>>>(a);
   else
-    w_score_kernel<T, C, MODE, false, SP, IND><<<grid, W_THREADS, L.lds, st>>>(a);
+    w_score_kernel<T, C, MODE, false, SP, IND>
+        <<<grid, w_score_waves(C, false, SP, IND) * 64, L.lds, st>>>(a);
   return launch_ok();
 }
 
@@ -2705,15 +2727,12 @@ gsrq_status w_build_frags(const float* gain, const float* shape, int d, int K, i
                           int cb0, bool unit_gain, const int* done, int G, int* sig, u4* frag,
                           const WDefer& X, hipStream_t st) {
   TimedLaunch tl(GSRQ_KERNEL_FRAGMENTS, st);
-  w_sigma_kernel<<<ncb, 256, 0, st>>>(gain, K, unit_gain ? 1 : 0, done, G, cb0, sig, X.gmin,
-                                      X.xcount, X.xchanged, X.xobj, X.hcount);
-  gsrq_status e = launch_ok();
-  if (e) return e;
   const int tiles = (K + CW - 1) / CW;
   const dim3 fgrid(tiles, ncb);
   const int ug = unit_gain ? 1 : 0;
+  const WDeferPtrs xp{X.gmin, X.xcount, X.xchanged, X.xobj, X.hcount};
   auto go = [&](auto kern) {
-    kern<<<fgrid, 64, 0, st>>>(gain, shape, d, K, ug, sig, done, G, cb0, frag);
+    kern<<<fgrid, 64, 0, st>>>(gain, shape, d, K, ug, sig, done, G, cb0, frag, xp);
   };
   switch (w_pairs(C)) {
     case 1: go(w_frag_kernel<1>); break;
