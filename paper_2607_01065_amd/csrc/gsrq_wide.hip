@@ -576,16 +576,41 @@ __device__ __forceinline__ void w_make_b_direct(const T* xp, int d, bool vec, bo
 template <bool F16, int P>
 __device__ __forceinline__ f16v w_tile(const u4* ta, const u4 (&bx)[P], const u4 (&blo)[P],
                                        u4 bias) {
+  // the fragments of pair p + AH are read while pair p's MFMAs run (with
+  // the reads next to their MFMAs, two read registers exposed an LDS round
+  // trip every two or three MFMAs)
+  constexpr int AH = P < 2 ? P : 2;
+  u4 fh[P], fl[P], fb;
+#pragma unroll
+  for (int q = 0; q < AH; ++q) {
+    fh[q] = ta[q * 64];
+    fl[q] = ta[(P + 1 + q) * 64];
+  }
+  if (AH == P) fb = ta[P * 64];
   f16v acc = {};
 #pragma unroll
   for (int p = 0; p < P; ++p) {
-    const h8 ahi = as_h8(ta[p * 64]);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi, as_h8(bx[p]), acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[(P + 1 + p) * 64]), as_h8(bx[p]), acc,
-                                                 0, 0, 0);
-    if (!F16) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(ahi, as_h8(blo[p]), acc, 0, 0, 0);
+    if (p + AH < P) {
+      fh[p + AH] = ta[(p + AH) * 64];
+      fl[p + AH] = ta[(P + 1 + p + AH) * 64];
+    } else if (p + AH == P && AH < P) {
+      fb = ta[P * 64];
+    }
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(fh[p]), as_h8(bx[p]), acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(fl[p]), as_h8(bx[p]), acc, 0, 0, 0);
+    if (!F16) acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(fh[p]), as_h8(blo[p]), acc, 0, 0, 0);
   }
-  return __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(ta[P * 64]), as_h8(bias), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_32x32x16_f16(as_h8(fb), as_h8(bias), acc, 0, 0, 0);
+  // the schedule: the first AH pairs' reads, then per pair its MFMAs and two
+  // reads ahead (left alone the scheduler moves each read next to its MFMA)
+  __builtin_amdgcn_sched_group_barrier(0x100, 2 * AH, 0);
+#pragma unroll
+  for (int p = 0; p < P; ++p) {
+    __builtin_amdgcn_sched_group_barrier(0x008, F16 ? 2 : 3, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+  return acc;
 }
 
 // Single-pass distances of one tile: hi(a) against the row's float16
