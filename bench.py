@@ -28,8 +28,8 @@ METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline
 # scaled x2.000 and writes x1.000 against a 256 MiB reference copy).  Valid
 # only for the kernel source those passes measured; other workloads: null.
 TRAFFIC = {
-    "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "034ae2415b2c5e86",
-                             "bytes_per_launch": 116563937},
+    "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "e934fc2cab0ffa18",
+                             "bytes_per_launch": 116563167},
     "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "eb0a907ea125f516",
                             "bytes_per_launch": 351216734},
     "paper_rates_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",

@@ -28,9 +28,14 @@ def hipcc():
 # Flags of single translation units.  The attention kernel keeps its MFMA
 # accumulators in ordinary VGPRs: with them in AGPRs, the rare rescaling of
 # the output sums (VALU work) made the compiler copy all 64 accumulators to
-# VGPRs on every token block.
+# VGPRs on every token block.  The narrow family's block claims are single-
+# lane LDS atomics that the atomic optimizer would wrap in a wave-wide
+# count-and-broadcast sequence (six VALU and six SALU instructions per
+# block); its few multi-lane same-address atomics reduce over the wave
+# themselves.
 SRC_FLAGS = {
     "gsrq_attn.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "gsrq.hip": ["-mllvm", "-amdgpu-atomic-optimizer-strategy=None"],
 }
 
 

@@ -377,19 +377,29 @@ __device__ __forceinline__ void read_codeword(const float* gain, const float* sh
 
 // Load a codebook (gain [K], shape [K][d]) into zero-padded LDS arrays and
 // return sigma's exponent (every thread of the block calls this).
+// The maximum of v over the workgroup into *red (LDS, cleared beforehand):
+// a wave reduction, then one atomic per wave.  Every thread calls it.
+__device__ __forceinline__ void block_max_into(int v, int* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = max(v, __shfl_xor(v, off));
+  if ((threadIdx.x & 63) == 0 && v > 0) atomicMax(red, v);
+}
+
 __device__ int load_codebook(const float* gain, const float* shape, int d, int K, bool unit_gain,
                              float* cbg, float* cbs, int* red) {
   const int tid = threadIdx.x;
   if (tid == 0) *red = 0;
   __syncthreads();
+  int gm = 0;   // gains >= 0 order as ints
   for (int k = tid; k < KMAX; k += blockDim.x) {
     float g, sv[DP];
     read_codeword(gain, shape, d, K, k, unit_gain, g, sv);
     cbg[k] = g;
 #pragma unroll
     for (int j = 0; j < DP; ++j) cbs[k * DP + j] = sv[j];
-    if (g > 0.f) atomicMax(red, __float_as_int(g));   // gains >= 0 order as ints
+    if (g > 0.f) gm = max(gm, __float_as_int(g));
   }
+  block_max_into(gm, red);
   __syncthreads();
   return sigma_exp(__int_as_float(*red));
 }
@@ -765,10 +775,12 @@ assign_accumulate_kernel(AssignArgs a) {
   float nw = 0.f;
   uint16_t nold = 0;
   auto fetch = [&](int rb) {
-    int r = rb * RB + i;
-    r = r < nrows ? r : 0;
-    nx.load(xc + r * 8);
-    nw = wc[r * wstride];
+    // unsigned 32-bit offsets from the chunk's uniform bases (no 64-bit
+    // address arithmetic per lane)
+    const uint32_t r0 = (uint32_t)(rb * RB + i);
+    const uint32_t r = r0 < (uint32_t)nrows ? r0 : 0u;
+    nx.load(xc + r * 8u);
+    nw = wc[r * (uint32_t)wstride];
     if (MODE == MODE_ITER) nold = ac[r];
   };
   // the first block's loads are issued before the codebook is ready, so
@@ -792,6 +804,7 @@ assign_accumulate_kernel(AssignArgs a) {
     if (tid == 0) red = 0;
     __syncthreads();
     double term = 0.0;
+    int gm = 0;
     if (tid < KMAX) {
       const bool real = tid < K;
       double sn[DP];
@@ -802,12 +815,13 @@ assign_accumulate_kernel(AssignArgs a) {
       cbg[tid] = (float)gnew;
 #pragma unroll
       for (int j = 0; j < DP; ++j) cbs[tid * DP + j] = (float)sn[j];
-      if ((float)gnew > 0.f) atomicMax(&red, __float_as_int((float)gnew));
+      if ((float)gnew > 0.f) gm = __float_as_int((float)gnew);
       if (chunk == 0 && real) {
         a.new_gain[(size_t)g * K + tid] = (float)gnew;
         for (int j = 0; j < d; ++j) a.new_shape[((size_t)g * K + tid) * d + j] = (float)sn[j];
       }
     }
+    block_max_into(gm, &red);
     const double wxx_p = acc[KMAX * ACC], chg = acc[KMAX * ACC + 1];
     const double terms = block_sum<TRAIN_WAVES * 64>(term, objw);
     if (chunk == 0 && tid == 0) {
