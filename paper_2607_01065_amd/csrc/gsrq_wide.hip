@@ -1625,31 +1625,54 @@ constexpr int W_XKMAX = 4096;    // candidate list capacity (codewords)
 template <typename T, int MODE>
 __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
   __shared__ __align__(16) double xsd[W_XROWS][8 * W_CMAX];
-  __shared__ double xn[W_XROWS];
+  __shared__ double xn[W_XROWS], xq[W_XROWS];
   __shared__ double wbd[W_XTHREADS / 64][W_XROWS];
   __shared__ int wbk[W_XTHREADS / 64][W_XROWS];
+  __shared__ double bestd[W_XROWS];
   __shared__ int bestk[W_XROWS];
   __shared__ int rows[W_XROWS];
+  __shared__ int olda[W_XROWS];
   __shared__ int cand[W_XKMAX];
   __shared__ int ncand;
   const int g = blockIdx.y;
-  if (a.done && a.done[g]) return;
-  const int cnt = a.xcount[g];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int d = a.d, K = a.K;
   const int cb = a.cb0 + g;
   const float* gcb = a.gain + (size_t)cb * K;
   const float* scb = a.shape + (size_t)cb * K * d;
-  const double gmin = (double)a.gmin[cb - a.fcb0];
   const T* X = (const T*)a.x;
+  // A launch is mostly latency.  The workgroup of a subspace's first batch
+  // (the others are usually empty) fetches what does not depend on the list
+  // together with its count: that batch's row ids, read before the count is
+  // known (entries past it are in bounds and unused), and with
+  // K <= W_XTHREADS the gain of codeword tid for the candidate test.
+  const bool small = K <= W_XTHREADS;
+  const bool ahead = blockIdx.x == 0;
+  float gpre = 1.f;
+  if (small && ahead && !a.unit_gain) gpre = gcb[min(tid, K - 1)];
+  int rid = 0;
+  if (ahead && tid < W_XROWS) rid = a.xrows[(size_t)g * a.N + min((int64_t)tid, a.N - 1)];
+  const int cnt = a.xcount[g];
+  if (a.done && a.done[g]) return;
+  const double gmin = (double)a.gmin[cb - a.fcb0];
+  bool first = true;
   for (int b0 = blockIdx.x * W_XROWS; b0 < cnt; b0 += gridDim.x * W_XROWS) {
     const int nb = min(W_XROWS, cnt - b0);
-    if (tid < W_XROWS) rows[tid] = a.xrows[(size_t)g * a.N + b0 + min(tid, nb - 1)];
+    if (!(first && ahead) && tid < W_XROWS)
+      rid = a.xrows[(size_t)g * a.N + b0 + min(tid, nb - 1)];
+    // slots past nb repeat the last row (wave 0 holds all W_XROWS ids)
+    {
+      const int r = __shfl(rid, min(lane, nb - 1));
+      if (tid < W_XROWS) rows[tid] = r;
+    }
     if (tid == 0) ncand = 0;
     __syncthreads();
     {
       // the rows' d elements (slots past nb repeat the last row), eight
-      // unconditional loads in flight per thread: the batch is latency-bound
+      // unconditional loads in flight per thread, and the rows' previous
+      // assignments: the batch is latency-bound
+      int oa = 0;
+      if (MODE == W_TRAIN && tid < W_XROWS) oa = a.assign[(size_t)g * a.N + rows[tid]];
       const int ld = 31 - __clz(d), n = W_XROWS << ld;
       constexpr int UN = 8;
       for (int e0 = tid; e0 < n; e0 += UN * W_XTHREADS) {
@@ -1665,6 +1688,7 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
           if (e < n) xsd[e >> ld][e & (d - 1)] = (double)v[u];
         }
       }
+      if (MODE == W_TRAIN && tid < W_XROWS) olda[tid] = oa;
     }
     __syncthreads();
     // row norms: wave w sums rows 4w .. 4w + 3 across its lanes
@@ -1675,16 +1699,23 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
       for (int j = lane; j < d; j += 64) q = fma(xr[j], xr[j], q);
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) q += __shfl_xor(q, off);
-      if (lane == 0) xn[wave * 4 + r] = sqrt(q);
+      if (lane == 0) {
+        xq[wave * 4 + r] = q;
+        xn[wave * 4 + r] = sqrt(q);
+      }
     }
     __syncthreads();
     double xmax = 0.0;
     for (int i = 0; i < W_XROWS; ++i) xmax = fmax(xmax, xn[i]);
     const double thr = (gmin + 2.0 * xmax) * (1.0 + 1e-5);
-    // candidate list (any order; ties are broken by index below)
+    // candidate list (any order; ties are broken by index below): codewords
+    // with g > g_min + 2 max ||x|| cannot win
     for (int k0 = 0; k0 < K; k0 += W_XTHREADS) {
       const int k = k0 + tid;
-      const bool c = k < K && (a.unit_gain ? 1.0 : (double)gcb[k]) <= thr;
+      const double gk = a.unit_gain ? 1.0
+                                    : (double)(small && ahead && first ? gpre
+                                                                       : gcb[min(k, K - 1)]);
+      const bool c = k < K && gk <= thr;
       const unsigned long long m = __ballot(c);
       const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
                                                  __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
@@ -1698,13 +1729,13 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
     const int nc = ncand <= W_XKMAX ? ncand : K;
     const bool all = ncand > W_XKMAX;
     const int nr4 = (nb + 3) >> 2;          // row groups of four the batch fills
+    constexpr int JB = 32;                  // codeword elements per block
     double bd[4][4];
     int bk[4][4];
 #pragma unroll
     for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
       for (int r = 0; r < 4; ++r) { bd[rg][r] = INFINITY; bk[rg][r] = 0x7fffffff; }
-    constexpr int JB = 32;                  // codeword elements per block
     for (int c0 = wave * 64 + lane; c0 - lane < nc; c0 += W_XTHREADS) {
       const bool live = c0 < nc;
       const int kq = all ? min(c0, K - 1) : cand[min(c0, nc - 1)];
@@ -1715,15 +1746,6 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
       for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
         for (int r = 0; r < 4; ++r) acc[rg][r] = 0.0;
-      f4 ca[JB / 4], cz[JB / 4];             // the two block buffers
-      const int nbk = (d + JB - 1) / JB;
-      auto load = [&](f4 (&buf)[JB / 4], int jb) {
-#pragma unroll
-        for (int v = 0; v < JB / 4; ++v) {
-          const int j = min(jb + 4 * v, d - 4);          // in bounds; unused past d
-          buf[v] = *(const f4*)(sp + j);
-        }
-      };
       auto block = [&](const f4 (&buf)[JB / 4], int jb) {
         const int je = min(JB, d - jb);
 #pragma unroll
@@ -1746,6 +1768,15 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
               acc[rg][r] = t;
             }
           }
+        }
+      };
+      f4 ca[JB / 4], cz[JB / 4];             // the two block buffers
+      const int nbk = (d + JB - 1) / JB;
+      auto load = [&](f4 (&buf)[JB / 4], int jb) {
+#pragma unroll
+        for (int v = 0; v < JB / 4; ++v) {
+          const int j = min(jb + 4 * v, d - 4);          // in bounds; unused past d
+          buf[v] = *(const f4*)(sp + j);
         }
       };
       load(ca, 0);
@@ -1771,6 +1802,7 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
           }
       }
     }
+    first = false;
     // minimum per row over the wave's lanes, then over the four waves
 #pragma unroll
     for (int rg = 0; rg < 4; ++rg) {
@@ -1801,6 +1833,7 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
         if (od < b || (od == b && ok < k)) { b = od; k = ok; }
       }
       bestk[tid] = k < K ? k : 0;           // (a non-empty list always sets k)
+      bestd[tid] = b;
     }
     __syncthreads();
     // outputs: wave w writes rows w, w + 4, w + 8, w + 12
@@ -1811,22 +1844,13 @@ __global__ void __launch_bounds__(W_XTHREADS) w_exact_kernel(WScoreArgs a) {
       const int64_t row = rows[i];
       const int k = bestk[i];
       if (MODE == W_TRAIN) {
-        if (a.obj) {
-          // weighted distortion ||x - g s||^2 of the chosen codeword
-          const double gk = a.unit_gain ? 1.0 : (double)gcb[k];
-          double dist = 0.0;
-          for (int j = lane; j < d; j += 64) {
-            const double e = xsd[i][j] - gk * (double)scb[(size_t)k * d + j];
-            dist = fma(e, e, dist);
-          }
-#pragma unroll
-          for (int off = 32; off > 0; off >>= 1) dist += __shfl_xor(dist, off);
-          if (lane == 0) atomicAdd(a.xobj + g, (double)(a.w ? a.w[row] : 1.f) * dist);
-        }
         if (lane == 0) {
-          uint16_t* ap = a.assign + (size_t)g * a.N + row;
-          if (*ap != (uint16_t)k) a.xchanged[g] = 1;
-          *ap = (uint16_t)k;
+          // weighted distortion ||x - g s||^2 = ||x||^2 + (g^2 - 2 g s.x)
+          // of the chosen codeword, both terms in float64
+          if (a.obj)
+            atomicAdd(a.xobj + g, (double)(a.w ? a.w[row] : 1.f) * (xq[i] + bestd[i]));
+          if (olda[i] != k) a.xchanged[g] = 1;
+          a.assign[(size_t)g * a.N + row] = (uint16_t)k;
         }
       } else {
         if (lane == 0 && a.codes)
