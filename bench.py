@@ -36,11 +36,11 @@ TRAFFIC = {
                          "bytes_per_launch": 141466069},
     "rate_sweep_d16": {"source": "gsrq_wide.hip", "source_sha256_prefix": "abcb487eed333c56",
                        "bytes_per_launch": 289971558},
-    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "9f651509c117ea68",
-                              "bytes_per_launch": 89573888},
+    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "d995f1d8859cd8bb",
+                              "bytes_per_launch": 89574476},
     "decode_attention_075bit": {"source": "gsrq_attn.hip",
-                                "source_sha256_prefix": "9f651509c117ea68",
-                                "bytes_per_launch": 177593902},
+                                "source_sha256_prefix": "d995f1d8859cd8bb",
+                                "bytes_per_launch": 177590240},
 }
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E

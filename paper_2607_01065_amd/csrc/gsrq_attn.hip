@@ -717,11 +717,14 @@ __global__ void __launch_bounds__(256) attn_rq_keytab_kernel(const float* __rest
   tabk[e] = pack_h8(v);
 }
 
-// LDS position (u4) of chunk c of codeword k of table stage sl: the 16
-// chunks of a 256-byte codeword are rotated by k, so that lanes gathering
-// the same chunk of random codewords spread over the banks.
-__device__ __forceinline__ int aq_slot(int sl, int k, int c) {
-  return ((sl * AT_K + k) << 4) + ((c + k) & 15);
+// LDS layout of a stage-pair key table: chunk c of codeword k of stage sl
+// sits in u4 slot ((sl K + k) << 4) | (c ^ (k & 15)), so that lanes gathering
+// the same chunk of random codewords spread over the banks.  A lane of half
+// hh reads chunks 4 hh + i and 8 + 4 hh + i (i < 4); with
+// base = ((sl K + k) << 8) | (((4 hh) ^ (k & 15)) << 4) their byte offsets are
+// base ^ (i << 4) and base ^ ((8 | i) << 4): one XOR per gather.
+__device__ __forceinline__ uint32_t aq_base(int sl, int k, int hh) {
+  return ((uint32_t)(sl * AT_K + k) << 8) | ((uint32_t)((4 * hh) ^ (k & 15)) << 4);
 }
 
 template <int GQ>
@@ -889,10 +892,10 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_rq_chunk_kernel(AqArgs a) 
       }
       {
         // entry e = r * AT_THREADS + tid is chunk tid % 16 of codeword
-        // (tid / 16 + 32 r) % 256 of stage r / 8; 32 r leaves the chunk
-        // rotation (c + k) % 16 unchanged, so its slot is base + 512 r
+        // (tid / 16 + 32 r) % 256 of stage r / 8; 32 r leaves k & 15 and
+        // so the chunk's slot c ^ (k & 15) unchanged: base + 512 r
         const int kq = tq >> 4, c = tq & 15;
-        u4* dst = ktab + (kq << 4) + ((c + kq) & 15);
+        u4* dst = ktab + (kq << 4) + (c ^ (kq & 15));
         const u4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
         for (int r = 0; r < PER; ++r) dst[512 * r] = r * AT_THREADS + tq < n ? v[r] : z;
@@ -914,6 +917,8 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_rq_chunk_kernel(AqArgs a) 
         // codes; their scores are masked)
         const int t = min(32 * (gb0 + u) + tl, len - 1) - tok0;
         const int c0 = kcl[2 * t], c1 = kcl[2 * t + 1];
+        const uint32_t kb0 = aq_base(0, c0, hh), kb1 = aq_base(1, c1, hh);
+        const unsigned char* kt8 = lds + C::KTAB;
         const bool mine = ul == u;
         const u4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
@@ -923,11 +928,11 @@ __global__ void __launch_bounds__(AT_THREADS, 1) attn_rq_chunk_kernel(AqArgs a) 
           u4 g[2][4];
 #pragma unroll
           for (int ii = 0; ii < 2; ++ii) {
-            const int cx = 4 * hh + i2 + ii, cy = 8 + 4 * hh + i2 + ii;
-            g[ii][0] = ktab[aq_slot(0, c0, cx)];
-            g[ii][1] = ktab[aq_slot(0, c0, cy)];
-            g[ii][2] = ktab[aq_slot(1, c1, cx)];
-            g[ii][3] = ktab[aq_slot(1, c1, cy)];
+            const uint32_t ox = (uint32_t)(i2 + ii) << 4, oy = (uint32_t)(8 | (i2 + ii)) << 4;
+            g[ii][0] = *(const u4*)(kt8 + (kb0 ^ ox));
+            g[ii][1] = *(const u4*)(kt8 + (kb0 ^ oy));
+            g[ii][2] = *(const u4*)(kt8 + (kb1 ^ ox));
+            g[ii][3] = *(const u4*)(kt8 + (kb1 ^ oy));
           }
 #pragma unroll
           for (int ii = 0; ii < 2; ++ii) {
