@@ -2112,11 +2112,13 @@ __global__ void __launch_bounds__(W_THREADS) w_accumulate_kernel(WAccArgs a) {
 // of the subspace (no LDS atomics: in bucket order consecutive members share
 // a codeword, so atomics into one LDS slice all hit the same addresses).
 // Lane groups of 16 lanes take one member each (four members side by side,
-// W_SMEMBERS per group in flight), lane i of a group holding elements
+// w_smembers(E) per group in flight), lane i of a group holding elements
 // [E i, E i + E) of the row (E = d / 16, vector loads); a member's norm is
 // a 16-lane reduction, and the four groups' sums are added once at the end.
 // The per-member products are formed as in w_acc_members.
-constexpr int W_SMEMBERS = 4;
+// members per lane group in flight: eight up to d = 128, four at d = 256
+// (where eight would leave two waves per SIMD)
+__host__ __device__ constexpr int w_smembers(int E) { return E <= 8 ? 8 : 4; }
 template <typename T> struct WVec;
 template <> struct WVec<_Float16> {
   // E consecutive float16 elements (E a multiple of 4) as float
@@ -2143,6 +2145,7 @@ template <> struct WVec<float> {
 
 template <typename T, int E>
 __global__ void __launch_bounds__(256) w_accumulate_sorted_kernel(WAccArgs a) {
+  constexpr int SM = w_smembers(E);
   const int g = blockIdx.y;
   if (a.done && a.done[g]) return;
   const int lane = threadIdx.x & 63, grp = lane >> 4, li = lane & 15;
@@ -2158,19 +2161,30 @@ __global__ void __launch_bounds__(256) w_accumulate_sorted_kernel(WAccArgs a) {
   double sy[E], sx[E], wsum = 0.0;
 #pragma unroll
   for (int e = 0; e < E; ++e) sy[e] = sx[e] = 0.0;
-  constexpr int STEP = 4 * W_SMEMBERS;   // members per batch and wave
-  for (int m = m0; m < m1; m += STEP) {
-    float xv[W_SMEMBERS][E], wt[W_SMEMBERS];
-    // member m + 4 u + grp of the batch (past the bucket's end a slot
-    // re-reads the last member and adds nothing)
+  constexpr int STEP = 4 * SM;   // members per batch and wave
+  // member m + 4 u + grp of a batch (past the bucket's end a slot re-reads
+  // the last member and adds nothing); the next batch's member ids are read
+  // while this batch's rows are in flight, so a batch costs one memory round
+  // trip (a crowded codeword is walked by its one wave alone)
+  int rid[SM];
+  if (m0 < m1) {
 #pragma unroll
-    for (int u = 0; u < W_SMEMBERS; ++u) {
-      const int64_t row = srt[min(m + 4 * u + grp, m1 - 1)];
+    for (int u = 0; u < SM; ++u) rid[u] = srt[min(m0 + 4 * u + grp, m1 - 1)];
+  }
+  for (int m = m0; m < m1; m += STEP) {
+    float xv[SM][E], wt[SM];
+#pragma unroll
+    for (int u = 0; u < SM; ++u) {
+      const int64_t row = rid[u];
       WVec<T>::template load<E>(X + row * a.ldx, xv[u]);
       wt[u] = a.w ? a.w[row] : 1.f;
     }
+    if (m + STEP < m1) {
 #pragma unroll
-    for (int u = 0; u < W_SMEMBERS; ++u) {
+      for (int u = 0; u < SM; ++u) rid[u] = srt[min(m + STEP + 4 * u + grp, m1 - 1)];
+    }
+#pragma unroll
+    for (int u = 0; u < SM; ++u) {
       float ss = xv[u][E - 1] * xv[u][E - 1];
 #pragma unroll
       for (int e = E - 2; e >= 0; --e) ss = fmaf(xv[u][e], xv[u][e], ss);
