@@ -81,7 +81,7 @@ static_assert(w_sreg(W_CMAX) * W_THREADS >= w_frags(W_CMAX) * 64, "staging holds
 // a CU alone).  Resident tables, the single pass and the listed-row pass
 // keep eight.
 __host__ __device__ constexpr int w_score_waves(int C, bool resident, bool sp, bool ind) {
-  return (!resident && !sp && !ind && C <= 16) ? 4 : W_WAVES;
+  return (!resident && !sp && C <= 16) ? 4 : W_WAVES;
 }
 // Tiles per streamed chunk of the hi/lo pass, and the staged u4 per thread
 // for a workgroup of nth threads.
@@ -2743,7 +2743,8 @@ gsrq_status w_score_launch_c(const WScoreArgs& a, const WLayout& L, hipStream_t 
       b.nslice = std::min(W_HP_SLICES, a.tiles);
       b.tps = (a.tiles + b.nslice - 1) / b.nslice;
       b.nslice = (a.tiles + b.tps - 1) / b.tps;
-      b.nwg = std::max(1, W_HP_WGS / (a.G * b.nslice));
+      b.nwg = std::max(1, W_HP_WGS * (W_WAVES / w_score_waves(C, false, false, true)) /
+                              (a.G * b.nslice));
       b.map_xcd = 0;
       H.resident = (size_t)b.tps * tile_bytes <= (size_t)W_RESIDENT_BYTES;
       if (H.resident) H.lds = (size_t)b.tps * tile_bytes;
