@@ -30,12 +30,12 @@ METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline
 TRAFFIC = {
     "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "e934fc2cab0ffa18",
                              "bytes_per_launch": 116563167},
-    "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "d1c5a770f43a58e3",
-                            "bytes_per_launch": 352232113},
+    "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "a3570c702de78195",
+                            "bytes_per_launch": 334869431},
     "paper_rates_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",
                          "bytes_per_launch": 141466069},
-    "rate_sweep_d16": {"source": "gsrq_wide.hip", "source_sha256_prefix": "d1c5a770f43a58e3",
-                       "bytes_per_launch": 289927577},
+    "rate_sweep_d16": {"source": "gsrq_wide.hip", "source_sha256_prefix": "a3570c702de78195",
+                       "bytes_per_launch": 289902833},
     "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "d995f1d8859cd8bb",
                               "bytes_per_launch": 89574476},
     "decode_attention_075bit": {"source": "gsrq_attn.hip",

@@ -74,14 +74,14 @@ __host__ __device__ constexpr int w_sreg(int C) {
              : (w_frags(C) * 64 + W_THREADS - 1) / W_THREADS;
 }
 static_assert(w_sreg(W_CMAX) * W_THREADS >= w_frags(W_CMAX) * 64, "staging holds one tile");
-// Waves of a scoring workgroup.  The streamed hi/lo pass at d <= 128 runs
-// four: each workgroup then scores one round of 128 rows and streams the
-// table once for them, and two or three workgroups share a CU, so that one's
-// row loads and barriers overlap another's MFMAs (eight-wave workgroups held
-// a CU alone).  Resident tables, the single pass and the listed-row pass
-// keep eight.
+// Waves of a scoring workgroup.  With a streamed table at d <= 128 (the
+// hi/lo pass, the single pass and the pass over listed rows) it runs four:
+// each workgroup then scores one round of rows and streams the table once
+// for them, and two or three workgroups share a CU, so that one's row loads
+// and barriers overlap another's MFMAs (eight-wave workgroups held a CU
+// alone).  Resident tables keep eight.
 __host__ __device__ constexpr int w_score_waves(int C, bool resident, bool sp, bool ind) {
-  return (!resident && !sp && C <= 16) ? 4 : W_WAVES;
+  return (!resident && C <= 16) ? 4 : W_WAVES;
 }
 // Tiles per streamed chunk of the hi/lo pass, and the staged u4 per thread
 // for a workgroup of nth threads.
@@ -94,6 +94,18 @@ __host__ __device__ constexpr int w_sreg_n(int C, int nth) {
 // The single pass stages P + 1 fragments per tile through larger chunks
 // (fewer barriers per round); two workgroups per CU still fit in LDS.
 constexpr int W_SP_STREAM_BYTES = 36864;
+// a four-wave single-pass workgroup stages half-size chunks (five staged
+// u4 per thread; full-size ones measured no faster and spill in one
+// instantiation); its registers allow two such workgroups per CU
+__host__ __device__ constexpr int w_sp_stream_bytes(int nw) {
+  return nw == W_WAVES ? W_SP_STREAM_BYTES : W_SP_STREAM_BYTES / 2;
+}
+__host__ __device__ constexpr int w_sp_sreg_n(int C, int nw) {
+  return (w_sp_stream_bytes(nw) / 16 + nw * 64 - 1) / (nw * 64) >
+                 ((w_pairs(C) + 1) * 64 + nw * 64 - 1) / (nw * 64)
+             ? (w_sp_stream_bytes(nw) / 16 + nw * 64 - 1) / (nw * 64)
+             : ((w_pairs(C) + 1) * 64 + nw * 64 - 1) / (nw * 64);
+}
 __host__ __device__ constexpr int w_sp_sreg(int C) {
   return (W_SP_STREAM_BYTES / 16 + W_THREADS - 1) / W_THREADS >
                  ((w_pairs(C) + 1) * 64 + W_THREADS - 1) / W_THREADS
@@ -989,7 +1001,7 @@ __global__ void __launch_bounds__(w_score_waves(C, RESIDENT, SP, IND) * 64, (RES
       const int tpc = a.tpc;
       const int nch = (tiles + tpc - 1) / tpc;
       const int chunk_u4 = tpc * QU * 64;
-      constexpr int SR = SP ? w_sp_sreg(C) : (NW == W_WAVES ? w_sreg(C) : w_sreg_n(C, NTH));
+      constexpr int SR = SP ? w_sp_sreg_n(C, NW) : (NW == W_WAVES ? w_sreg(C) : w_sreg_n(C, NTH));
       const WStage<QU, SR, NTH> stg;
       u4 reg[SR];
       {
@@ -2690,7 +2702,8 @@ WLayout w_score_layout(const gsrq_shape* s, size_t x_elt, bool f16rows, bool hp 
     L.lds = used;
   } else {
     L.rounds = 1;
-    L.tpc = std::max(1, (int)((L.sp ? W_SP_STREAM_BYTES : W_STREAM_BYTES) /
+    L.tpc = std::max(1, (int)((L.sp ? w_sp_stream_bytes(w_score_waves(L.C, false, true, false))
+                                    : W_STREAM_BYTES) /
                               (L.Qu * 64 * sizeof(u4))));
     L.lds = 2 * (size_t)L.tpc * L.Qu * 64 * sizeof(u4);
   }
