@@ -28,8 +28,8 @@ METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline
 # scaled x2.000 and writes x1.000 against a 256 MiB reference copy).  Valid
 # only for the kernel source those passes measured; other workloads: null.
 TRAFFIC = {
-    "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "e934fc2cab0ffa18",
-                             "bytes_per_launch": 116563167},
+    "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "e3353425db29e5d4",
+                             "bytes_per_launch": 116563529},
     "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "a3570c702de78195",
                             "bytes_per_launch": 334869431},
     "paper_rates_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",

@@ -1214,9 +1214,9 @@ flush:
 // Latency encoder for a few rows with a prepared codebook (the tokens
 // appended to a cache at each decoding step): one wave per (32-row block,
 // subspace), no LDS, no barriers and no block claiming, so a launch of 1 to
-// a few hundred rows costs little more than its loads.  The header check,
-// the operand tables of the first stage and the rows are loaded together;
-// the arithmetic is the stage-fused encoder's (same operand tables, same
+// a few hundred rows costs little more than its loads: the header and the
+// rows in one round trip, then (the header matching) the first stage's
+// operand tables in a second; the arithmetic is the stage-fused encoder's (same operand tables, same
 // keys, same float64 re-scoring and residual update), so codes and residuals
 // agree with it bit for bit.
 template <typename T, bool VEC>
@@ -1234,6 +1234,49 @@ __global__ void __launch_bounds__(ENC_SMALL_WAVES * 64) encode_small_kernel(Enco
   const bool valid = row < a.N;
   RowRaw<T, VEC> nx;
   nx.load((const T*)a.x + (valid ? row : 0) * a.ldx + (int64_t)g * d, d);
+  // the header first, fetched with the row: a buffer prepared for another
+  // shape may be smaller than this shape's tables, so nothing else is read
+  // from it before the header matches (a mismatch gives all-ones code fields
+  // and a NaN residual)
+  uint32_t tag[PREP_WORDS];
+#pragma unroll
+  for (int w = 0; w < PREP_WORDS; ++w) tag[w] = a.ptag[w];
+  {
+    // one wait for the row and the header together (left to itself the
+    // compiler issues the row after the branch, or waits for it before it
+    // fetches the header)
+    uint32_t* rw = (uint32_t*)nx.v;
+#pragma unroll
+    for (int j = 0; j < (int)sizeof(nx.v) / 4; ++j) asm volatile("" : "+v"(rw[j]));
+#pragma unroll
+    for (int w = 0; w < PREP_WORDS; ++w) asm volatile("" : "+v"(tag[w]));
+  }
+  bool ok = true;
+#pragma unroll
+  for (int w = 0; w < PREP_WORDS; ++w) ok &= tag[w] == a.etag.w[w];
+  if (!ok) {   // uniform over the wave: every lane read the same header
+    if (valid && h == 0) {
+      for (int m = 0; m < a.M; ++m) {
+        if (!a.codes) break;
+        const int64_t bit = ((int64_t)m * G + g) * a.b;
+        if (a.byte_codes) {
+          ((uint8_t*)(a.codes + row * a.words))[bit / 8] = 0xffu;
+        } else {   // words zeroed beforehand
+          uint32_t* wp = a.codes + row * a.words + bit / 32;
+          const int off = (int)(bit % 32);
+          const uint32_t ones = (1u << a.b) - 1u;
+          atomicOr(wp, ones << off);
+          if (off + a.b > 32) atomicOr(wp + 1, ones >> (32 - off));
+        }
+      }
+      if (a.residual) {
+        float* dst = a.residual + row * (int64_t)(G * d) + (int64_t)g * d;
+        for (int j = 0; j < d; ++j) dst[j] = __builtin_nanf("");
+      }
+    }
+    return;
+  }
+  // then the first stage's tables and sigma, all in flight together
   Tiles tl;
   {
     const u4* fr = a.frag + (size_t)g * NT * 2 * 64;
@@ -1243,28 +1286,7 @@ __global__ void __launch_bounds__(ENC_SMALL_WAVES * 64) encode_small_kernel(Enco
       tl.a2[t] = fr[(t * 2 + 1) * 64 + lane];
     }
   }
-  // the header is compared here but acted on only at the stores (a buffer
-  // prepared for another shape is read only where this call's shape places
-  // its parts, and gives all-ones code fields and a NaN residual)
-  uint32_t tag[PREP_WORDS];
-#pragma unroll
-  for (int w = 0; w < PREP_WORDS; ++w) tag[w] = a.ptag[w];
   int ex = a.sig[g];
-  // one wait for the row, the first stage's tables and the header together
-  // (left to itself the compiler waits for each before it issues the next)
-  {
-    uint32_t* rw = (uint32_t*)nx.v;
-#pragma unroll
-    for (int j = 0; j < (int)sizeof(nx.v) / 4; ++j) asm volatile("" : "+v"(rw[j]));
-#pragma unroll
-    for (int t = 0; t < NT; ++t) asm volatile("" : "+v"(tl.a1[t]), "+v"(tl.a2[t]));
-#pragma unroll
-    for (int w = 0; w < PREP_WORDS; ++w) asm volatile("" : "+v"(tag[w]));
-    asm volatile("" : "+v"(ex));
-  }
-  bool ok = true;
-#pragma unroll
-  for (int w = 0; w < PREP_WORDS; ++w) ok &= tag[w] == a.etag.w[w];
   float x[8];
   nx.get(x, d, valid);
   const u4 raw = nx.raw16(x, valid);
@@ -1308,7 +1330,7 @@ __global__ void __launch_bounds__(ENC_SMALL_WAVES * 64) encode_small_kernel(Enco
     }
     if (valid && h == 0 && a.codes) {
       const int64_t t = (int64_t)m * G + g;
-      const uint32_t code = ok ? (uint32_t)kstar : (uint32_t)K - 1u;   // K = 2^b
+      const uint32_t code = (uint32_t)kstar;
       if (a.byte_codes) {
         ((uint8_t*)(a.codes + row * a.words))[t] = (uint8_t)code;
       } else {   // words zeroed beforehand
@@ -1322,7 +1344,7 @@ __global__ void __launch_bounds__(ENC_SMALL_WAVES * 64) encode_small_kernel(Enco
   }
   if (valid && a.residual && h == 0) {
     float* dst = a.residual + row * (int64_t)(G * d) + (int64_t)g * d;
-    for (int j = 0; j < d; ++j) dst[j] = ok ? x[j] : __builtin_nanf("");
+    for (int j = 0; j < d; ++j) dst[j] = x[j];
   }
 }
 
