@@ -30,6 +30,8 @@ METRIC = "GSRQ encode vectors/s + GSKM iter/s at 1-bit; % of MFMA / HBM roofline
 TRAFFIC = {
     "llama3_8b_layer_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "e3353425db29e5d4",
                              "bytes_per_launch": 116563529},
+    "llama3_8b_cache_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "e3353425db29e5d4",
+                             "bytes_per_launch": 321209405},
     "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "a3570c702de78195",
                             "bytes_per_launch": 334869431},
     "paper_rates_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",
@@ -110,6 +112,54 @@ def cpu_baseline(kv, wl, n_groups):
                    f"init + {n_iter} GSKM iterations + encode + decode each ({sample_s:.1f} s), "
                    f"scaled to {T} iterations, {wl.G} subspaces, {wl.M} stage(s) and both "
                    f"caches (K, V)"),
+        "est_step_s": step_s,
+    }
+
+
+def measured_traffic(name):
+    """HBM bytes per launch of the workload's dominant kernel from its
+    committed counter summary, or None when its source has changed since."""
+    import hashlib
+    tr = TRAFFIC.get(name)
+    if tr is None:
+        return None
+    src = os.path.join(ROOT, "paper_2607_01065_amd", "csrc", tr["source"])
+    sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    return tr["bytes_per_launch"] if sha == tr["source_sha256_prefix"] else None
+
+
+def cache_cpu_baseline(X, gain, shape, wl, budget_s=10.0, rows=32768):
+    """The float64 oracle's encode + decode of one layer's key rows with the
+    layer's codebook, on a bounded sample (the first `rows` tokens of as many
+    subspaces as fit the time budget), scaled to vectors/s of the whole step
+    (every layer, K and V, all tokens and subspaces)."""
+    import numpy as np
+    from oracle import gsrq_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        threads = os.cpu_count() or 1
+    d, G = wl.d, wl.D // wl.d
+    rows = min(rows, wl.N)
+    Xs = X[:rows].float().cpu().numpy().astype(np.float64)
+    gs = gain[0].cpu().numpy().astype(np.float64)
+    ss = shape[0].cpu().numpy().astype(np.float64)
+    spent, n = 0.0, 0
+    while n < G and spent < budget_s:
+        Xg = Xs[:, n * d:(n + 1) * d]
+        t0 = time.perf_counter()
+        codes, _ = O.gsrq_encode(Xg, gs[n][None, None], ss[n][None, None])
+        O.gsrq_decode(codes, gs[n][None, None], ss[n][None, None])
+        spent += time.perf_counter() - t0
+        n += 1
+    step_s = spent / (n * rows) * wl.N * G * 2 * wl.layers
+    vectors = wl.layers * 2 * wl.N * (wl.D // HEAD_DIM)
+    return {
+        "value": vectors / step_s, "unit": "vectors/s", "cores": int(threads), "kind": "oracle",
+        "sample": (f"float64 oracle encode + decode of {rows} tokens of {n} of {G} key subspaces "
+                   f"of layer 0 with the layer's codebook ({spent:.1f} s), scaled to "
+                   f"{wl.N} tokens, {G} subspaces, K and V and {wl.layers} layers"),
         "est_step_s": step_s,
     }
 
@@ -200,8 +250,21 @@ def full_cache(args, wl):
         "kernels_us_source": "encode: HIP events around its launches in the first timed "
                              "step; others: one instrumented step after the timed region",
     }
+    # the dominant kernel is the encoder (one launch per layer and cache):
+    # eq. (5) scores of every row against every codeword, 2 N D K flops
+    enc_flops = 2.0 * N * D * K
+    achieved = enc_flops / (e_us * 1e-6) / 1e12
+    out["roofline"] = {"kernel": "encode (eq. 5 scores + argmin + bit-pack, one stage)",
+                       "bound": "mfma", "achieved": achieved, "peak": PEAK_MFMA_F16_TFLOPS,
+                       "unit": "TFLOP/s", "frac": achieved / PEAK_MFMA_F16_TFLOPS,
+                       "traffic": measured_traffic(wl.name),
+                       "traffic_unit": "HBM bytes per launch", "flops_per_launch": enc_flops,
+                       "avg_launch_us": e_us}
     if args.copy_ref_mib > 0:
         out["copy_ref_bytes"] = copy_reference(args.copy_ref_mib, dev)
+    if not args.no_cpu_baseline:
+        c = layers[0][0]
+        out["cpu_baseline"] = cache_cpu_baseline(c["X"], c["gain"], c["shape"], wl)
     print(json.dumps(out), flush=True)
 
 
