@@ -38,11 +38,11 @@ TRAFFIC = {
                          "bytes_per_launch": 141466069},
     "rate_sweep_d16": {"source": "gsrq_wide.hip", "source_sha256_prefix": "a3570c702de78195",
                        "bytes_per_launch": 289902833},
-    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "d995f1d8859cd8bb",
-                              "bytes_per_launch": 89574476},
+    "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "123617164b1ac182",
+                              "bytes_per_launch": 89763895},
     "decode_attention_075bit": {"source": "gsrq_attn.hip",
-                                "source_sha256_prefix": "d995f1d8859cd8bb",
-                                "bytes_per_launch": 177590240},
+                                "source_sha256_prefix": "123617164b1ac182",
+                                "bytes_per_launch": 177580762},
 }
 PEAK_MFMA_F16_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
 PEAK_HBM_GBPS = 8000.0          # MI355X HBM3E

@@ -1093,6 +1093,7 @@ __global__ void __launch_bounds__(AQ_VT) attn_rq_values_kernel(const float* __re
   __shared__ double wb[4][AT_K];
   __shared__ double hs[4][AT_HD];
   __shared__ double fac[4][AQ_VCH];
+  __shared__ float mcl[4][AQ_VCH], lcl[4][AQ_VCH];
   __shared__ float mrefs[4];
   __shared__ float gl[AT_K];
   const int m = blockIdx.x % M, hk = (blockIdx.x / M) % Hkv, b = blockIdx.x / (M * Hkv);
@@ -1101,16 +1102,27 @@ __global__ void __launch_bounds__(AQ_VT) attn_rq_values_kernel(const float* __re
   const float* p0 = part + ((size_t)b * Hkv + hk) * nch * GQ * RS;
   const size_t cs = (size_t)GQ * RS;
   const size_t cb = ((size_t)m * Hkv + hk) * AT_K;
+  // a launch is a chain of dependent loads: each step below issues all of
+  // its loads together (the chunk records one per thread, every head's bins
+  // of a round, 64 codeword elements per thread)
   gl[tid] = vg[cb + tid];                            // the stage's gains
-  // reference per head: the largest chunk reference among chunks with tokens
-  if (tid < GQ) {
-    const float* p = p0 + (size_t)tid * RS;
+  // reference per head: the largest record among chunks with tokens
+  {
     float mr = -INFINITY;
-    for (int c = 0; c < nch; ++c) {
-      const float mc = p[c * cs + M * AT_K], lc = p[c * cs + M * AT_K + 1];
-      mr = lc > 0.f ? fmaxf(mr, mc) : mr;
+    for (int c0 = 0; c0 < nch; c0 += AQ_VCH) {
+      const int nc = min(AQ_VCH, nch - c0);
+      if (tid < GQ * nc) {
+        const int h = tid / nc, c = c0 + tid % nc;
+        const float* p = p0 + (size_t)h * RS + c * cs;
+        mcl[h][tid % nc] = p[M * AT_K];
+        lcl[h][tid % nc] = p[M * AT_K + 1];
+      }
+      __syncthreads();
+      if (tid < GQ)
+        for (int c = 0; c < nc; ++c) mr = lcl[tid][c] > 0.f ? fmaxf(mr, mcl[tid][c]) : mr;
+      __syncthreads();
     }
-    mrefs[tid] = mr;
+    if (tid < GQ) mrefs[tid] = mr;
   }
   double acc[4] = {0.0, 0.0, 0.0, 0.0};
   for (int c0 = 0; c0 < nch; c0 += AQ_VCH) {
@@ -1118,39 +1130,51 @@ __global__ void __launch_bounds__(AQ_VT) attn_rq_values_kernel(const float* __re
     __syncthreads();                                 // mrefs written, previous factors read
     if (tid < GQ * nc) {
       const int h = tid / nc, c = c0 + tid % nc;
-      const float* p = p0 + (size_t)h * RS + c * cs;
-      const float mc = p[M * AT_K], lc = p[M * AT_K + 1];
+      float mc, lc;
+      if (nch <= AQ_VCH) {                           // one round: the records are in LDS
+        mc = mcl[h][tid % nc];
+        lc = lcl[h][tid % nc];
+      } else {
+        const float* p = p0 + (size_t)h * RS + c * cs;
+        mc = p[M * AT_K];
+        lc = p[M * AT_K + 1];
+      }
       fac[h][tid % nc] = lc > 0.f ? exp2((double)mc - (double)mrefs[h]) : 0.0;
     }
     __syncthreads();
-    // thread k: codeword k of stage m, every head, the round's chunks (all
-    // loads of a head's chunks issued together)
-    for (int h = 0; h < GQ; ++h) {
-      const float* p = p0 + (size_t)h * RS + (size_t)m * AT_K + tid;
-      constexpr int UN = 8;
-      for (int c1 = 0; c1 < nc; c1 += UN) {
-        float bv[UN];
+    // thread k: codeword k of stage m, every head, the round's chunks, eight
+    // chunks of every head in flight
+    constexpr int UN = 8;
+    for (int c1 = 0; c1 < nc; c1 += UN) {
+      float bv[4][UN];
 #pragma unroll
-        for (int u = 0; u < UN; ++u) bv[u] = p[(size_t)(c0 + min(c1 + u, nc - 1)) * cs];
+      for (int h = 0; h < 4; ++h) {
+        const float* p = p0 + (size_t)min(h, GQ - 1) * RS + (size_t)m * AT_K + tid;
 #pragma unroll
-        for (int u = 0; u < UN; ++u)
-          if (c1 + u < nc) {
-            // a chunk without tokens (factor 0) never wrote its bins: the
-            // slots hold stale workspace contents, kept out of the sum
-            const double f = fac[h][c1 + u];
-            acc[h] += f > 0.0 ? f * (double)bv[u] : 0.0;
-          }
+        for (int u = 0; u < UN; ++u) bv[h][u] = p[(size_t)(c0 + min(c1 + u, nc - 1)) * cs];
       }
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+        if (h < GQ) {
+#pragma unroll
+          for (int u = 0; u < UN; ++u)
+            if (c1 + u < nc) {
+              // a chunk without tokens (factor 0) never wrote its bins: the
+              // slots hold stale workspace contents, kept out of the sum
+              const double f = fac[h][c1 + u];
+              acc[h] += f > 0.0 ? f * (double)bv[h][u] : 0.0;
+            }
+        }
     }
   }
   for (int h = 0; h < GQ; ++h) wb[h][tid] = acc[h];
   __syncthreads();
   // contraction: thread (half, n) takes codewords half * 128 .. + 127,
-  // element n of each, 16 loads in flight
+  // element n of each, 64 loads in flight
   const int n = tid & (AT_HD - 1), half = tid >> 7;
   const float* sp = vs + cb * AT_HD + n;
   double o[4] = {0.0, 0.0, 0.0, 0.0};
-  constexpr int UK = 16;
+  constexpr int UK = 64;
   for (int k0 = half * 128; k0 < half * 128 + 128; k0 += UK) {
     float sv[UK];
 #pragma unroll

@@ -77,6 +77,7 @@ def _check(case, out, pairs=None, what=""):
     (1, 700, [700], 1, 4, 1, "float32"),            # one stage
     (2, 9000, [9000, 8191], 8, 4, 12, "float16"),   # 8 heads, three chunks
     (2, 700, [900, -3], 1, 4, 12, "float32"),       # lengths clamped to [0, cap]
+    (1, 266300, [266300], 1, 1, 2, "float32"),      # 66 chunks: the value merge in two rounds
 ])
 def test_attn_rq_parity(Bn, cap, lens, Hkv, GQ, M, qdt):
     say("attn rq parity", Bn, cap, lens, Hkv, GQ, M, qdt)
