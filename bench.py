@@ -32,12 +32,12 @@ TRAFFIC = {
                              "bytes_per_launch": 116563529},
     "llama3_8b_cache_1bit": {"source": "gsrq.hip", "source_sha256_prefix": "e3353425db29e5d4",
                              "bytes_per_launch": 321209405},
-    "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "a3570c702de78195",
-                            "bytes_per_launch": 334869431},
+    "large_codebook_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "363b3302a7802544",
+                            "bytes_per_launch": 334662782},
     "paper_rates_d128": {"source": "gsrq_wide.hip", "source_sha256_prefix": "bffb1448b9cbf9bf",
                          "bytes_per_launch": 141466069},
-    "rate_sweep_d16": {"source": "gsrq_wide.hip", "source_sha256_prefix": "a3570c702de78195",
-                       "bytes_per_launch": 289902833},
+    "rate_sweep_d16": {"source": "gsrq_wide.hip", "source_sha256_prefix": "363b3302a7802544",
+                       "bytes_per_launch": 289978206},
     "decode_attention_1bit": {"source": "gsrq_attn.hip", "source_sha256_prefix": "123617164b1ac182",
                               "bytes_per_launch": 89763895},
     "decode_attention_075bit": {"source": "gsrq_attn.hip",

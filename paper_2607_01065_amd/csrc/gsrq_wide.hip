@@ -49,6 +49,14 @@ constexpr int W_ACC_LDS_BYTES = 98304;          // accumulator slice in LDS
 constexpr int W_ACC_BATCH = 4;                  // rows per thread per collection pass
 constexpr int W_ACC_MEMBERS = 8;                // member rows per lane group in flight
 constexpr int W_BUCKET_KMAX = 16384;            // codewords the bucketing histogram holds
+// Sorted sums: a codeword's wave takes its first W_SORT_Q members; the rest of
+// the bucketed rows is cut into windows of W_SORT_Q positions, each summed by
+// a wave of its own (a window meets the overflow of at most one codeword:
+// two overflows are at least W_SORT_Q positions apart)
+constexpr int W_SORT_Q = 128;
+__host__ __device__ inline int w_sort_windows(int64_t N) {
+  return (int)((N + W_SORT_Q - 1) / W_SORT_Q);
+}
 constexpr int W_FUSED_ROUNDS = 4;               // row rounds a stage-fused encode workgroup keeps
 constexpr int W_DEC_TABLE_BYTES = 131072;        // codeword table per workgroup, at most
 constexpr int W_DEC_LDS_BYTES = 152 * 1024;      // table + staged code words
@@ -1891,6 +1899,9 @@ struct WAccArgs {
   int64_t rows_per_chunk;
   const int* sorted;       // [G][N] rows bucketed by codeword, or null
   const int* boff;         // [G][K + 1] bucket offsets into sorted
+  double* ovf;             // [G][nwin][2d+2] window partials (sorted sums), or null
+  const int* wk;           // [G][nwin] the codeword whose overflow meets window i, or -1
+  int nwin;
 };
 
 // Rows of each subspace bucketed by codeword, a counting sort in three
@@ -1933,7 +1944,8 @@ __global__ void __launch_bounds__(256) w_bucket_count_kernel(const uint16_t* __r
 __global__ void __launch_bounds__(1024) w_bucket_scan_kernel(int64_t N, int K, int chunks,
                                                              const int* __restrict__ done,
                                                              int* __restrict__ cnt,
-                                                             int* __restrict__ boff) {
+                                                             int* __restrict__ boff,
+                                                             int nwin, int* __restrict__ wk) {
   extern __shared__ int sc[];               // [chunks][K] counts, staged
   __shared__ int wsum[16];
   const int g = blockIdx.x;
@@ -1953,6 +1965,9 @@ __global__ void __launch_bounds__(1024) w_bucket_scan_kernel(int64_t N, int K, i
         if (e0 + u * 1024 < n) sc[e0 + u * 1024] = v[u];
     }
   }
+  int* wkg = wk ? wk + (size_t)g * nwin : nullptr;
+  if (wkg)
+    for (int i = tid; i < nwin; i += 1024) wkg[i] = -1;
   __syncthreads();
   // thread tid owns bins [b, e): their totals over the chunks, then an
   // exclusive scan of the totals over the workgroup
@@ -1973,12 +1988,16 @@ __global__ void __launch_bounds__(1024) w_bucket_scan_kernel(int64_t N, int K, i
   for (int w2 = 0; w2 < wave; ++w2) base += wsum[w2];
   int* bo = boff + (size_t)g * (K + 1);
   for (int k = b; k < e; ++k) {
+    const int m0 = base;
     bo[k] = base;
     for (int c = 0; c < chunks; ++c) {
       const int n = sc[c * K + k];
       cg[(size_t)c * K + k] = base;
       base += n;
     }
+    // the windows that codeword k's members past its first W_SORT_Q meet
+    if (wkg && base - m0 > W_SORT_Q)
+      for (int i = (m0 + W_SORT_Q) / W_SORT_Q; i <= (base - 1) / W_SORT_Q; ++i) wkg[i] = k;
   }
   if (tid == 0) bo[K] = (int)N;
 }
@@ -2161,13 +2180,31 @@ __global__ void __launch_bounds__(256) w_accumulate_sorted_kernel(WAccArgs a) {
   const int g = blockIdx.y;
   if (a.done && a.done[g]) return;
   const int lane = threadIdx.x & 63, grp = lane >> 4, li = lane & 15;
-  // the wave's codeword, in a scalar register (its bucket bounds are then
-  // scalar loads)
-  const int k = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (k >= a.K) return;   // uniform per wave
+  // the wave's codeword, or its window of the bucketed rows past the
+  // codeword blocks, in scalar registers (the bounds are then scalar loads)
   const int d = a.d, S = 2 * d + 2;
   const int* bo = a.boff + (size_t)g * (a.K + 1);
-  const int m0 = bo[k], m1 = bo[k + 1];
+  const int nkb = (a.K + 3) / 4;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int m0, m1, mall;
+  double* out;
+  if ((int)blockIdx.x < nkb) {
+    const int k = blockIdx.x * 4 + wv;
+    if (k >= a.K) return;   // uniform per wave
+    m0 = bo[k];
+    mall = bo[k + 1];
+    m1 = a.ovf ? min(mall, m0 + W_SORT_Q) : mall;
+    out = a.part + ((size_t)g * a.rchunks * a.K + k) * S;
+  } else {
+    const int i = ((int)blockIdx.x - nkb) * 4 + wv;
+    if (i >= a.nwin) return;
+    const int k = a.wk[(size_t)g * a.nwin + i];
+    if (k < 0) return;
+    m0 = max(i * W_SORT_Q, bo[k] + W_SORT_Q);
+    m1 = min(i * W_SORT_Q + W_SORT_Q, bo[k + 1]);
+    mall = m1;
+    out = a.ovf + ((size_t)g * a.nwin + i) * S;
+  }
   const int* srt = a.sorted + (size_t)g * a.N;
   const T* X = (const T*)a.x + (int64_t)g * d + E * li;
   double sy[E], sx[E], wsum = 0.0;
@@ -2224,7 +2261,6 @@ __global__ void __launch_bounds__(256) w_accumulate_sorted_kernel(WAccArgs a) {
     wsum += __shfl_xor(wsum, off);
   }
   if (grp == 0) {
-    double* out = a.part + ((size_t)g * a.rchunks * a.K + k) * S;
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       out[E * li + e] = sy[e];
@@ -2232,7 +2268,7 @@ __global__ void __launch_bounds__(256) w_accumulate_sorted_kernel(WAccArgs a) {
     }
     if (li == 0) {
       out[2 * d] = wsum;
-      out[2 * d + 1] = (double)(m1 - m0);
+      out[2 * d + 1] = (double)(mall - m0);
     }
   }
 }
@@ -2253,6 +2289,9 @@ struct WFinArgs {
   const int* xchanged;    // [G] changed flag of the exact kernel's rows
   const double* xobj;     // [G] their objective
   int kmeans;             // K-means baseline update instead of eqs. (7)(8)
+  const double* ovf;      // [G][nwin][2d+2] window partials of the sorted sums, or null
+  const int* boff;        // [G][K + 1] bucket offsets (with ovf)
+  int nwin;
 };
 
 // Codebook update from the chunk partials (fixed order): d / E lanes per
@@ -2288,6 +2327,21 @@ __global__ void __launch_bounds__(256) w_finalize_kernel(WFinArgs a) {
       sx[e] += p[d + E * li + e];
     }
     W += p[2 * d];
+  }
+  if (a.ovf) {
+    // the codeword's members past its first W_SORT_Q, window by window
+    const int* bo = a.boff + (size_t)g * (K + 1);
+    const int m0 = bo[kk], m1 = bo[kk + 1];
+    if (m1 - m0 > W_SORT_Q)
+      for (int i = (m0 + W_SORT_Q) / W_SORT_Q; i <= (m1 - 1) / W_SORT_Q; ++i) {
+        const double* p = a.ovf + ((size_t)g * a.nwin + i) * S;
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          sy[e] += p[E * li + e];
+          sx[e] += p[d + E * li + e];
+        }
+        W += p[2 * d];
+      }
   }
   float* sk = a.shape + ((size_t)g * K + kk) * d;
   float* gk = a.gain + (size_t)g * K + kk;
@@ -2878,7 +2932,7 @@ WAccLayout w_acc_layout(const gsrq_shape* s) {
 
 struct WTrainWs {
   size_t frag, gmin, xcount, xrows, xchanged, xobj, hcount, hrows, hbest, hrr, sig, part,
-      changed, obj, assign, done, iters, seednorm, seeds, sorted, boff, bcnt, total;
+      changed, obj, assign, done, iters, seednorm, seeds, sorted, boff, bcnt, ovf, wk, total;
 };
 
 WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
@@ -2913,6 +2967,9 @@ WTrainWs w_train_ws(const gsrq_shape* s, size_t x_elt) {
   W.bcnt = off;
   const int64_t bch = w_bucket_rows(s->N, s->K);
   off = align256(off + (A.bucket ? (size_t)G * ((s->N + bch - 1) / bch) * s->K * sizeof(int) : 0));
+  const size_t nwin = A.sorted_sums ? (size_t)w_sort_windows(s->N) : 0;
+  W.ovf = off; off = align256(off + (size_t)G * nwin * (2 * s->d + 2) * sizeof(double));
+  W.wk = off; off = align256(off + (size_t)G * nwin * sizeof(int));
   W.total = off;
   return W;
 }
@@ -3049,6 +3106,9 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   aa.ks = A.ks; aa.slices = A.slices; aa.rchunks = A.rchunks; aa.rows_per_chunk = A.rows_per_chunk;
   aa.sorted = A.bucket ? (const int*)(base + W.sorted) : nullptr;
   aa.boff = A.bucket ? (const int*)(base + W.boff) : nullptr;
+  aa.nwin = A.sorted_sums ? w_sort_windows(s->N) : 0;
+  aa.wk = A.sorted_sums ? (const int*)(base + W.wk) : nullptr;
+  aa.ovf = nullptr;       // set per launch: the sorted-sum kernel only
   const dim3 agrid((unsigned)(A.slices * A.rchunks), (unsigned)G);
 
   WFinArgs fa;
@@ -3057,6 +3117,7 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
   fa.force_changed = 0; fa.nwg = L.nwg; fa.part = part; fa.changed = changed; fa.obj = nullptr;
   fa.seednorm = seednorm; fa.gain = gain; fa.shape = shape; fa.done = done; fa.iters = iters;
   fa.trace = obj_trace; fa.xchanged = XD.xchanged; fa.xobj = XD.xobj; fa.kmeans = kmeans;
+  fa.ovf = nullptr; fa.boff = aa.boff; fa.nwin = aa.nwin;
   // elements per lane of the accumulation and the update: lane groups of
   // d / E lanes, at most one wave
   const bool e4 = d > 128;
@@ -3085,7 +3146,8 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
                                 (int)slds) != hipSuccess)
           return GSRQ_E_HIP;
         w_bucket_scan_kernel<<<G, 1024, slds, st>>>(s->N, K, bchunks, aa.done, bcnt,
-                                                    (int*)(base + W.boff));
+                                                    (int*)(base + W.boff), aa.nwin,
+                                                    (int*)aa.wk);
         w_bucket_scatter_kernel<<<dim3(bchunks, G), 256, (size_t)K * sizeof(int), st>>>(
             assign, s->N, K, bch, aa.done, bcnt, (int*)(base + W.sorted));
         if ((e2 = launch_ok())) return e2;
@@ -3094,8 +3156,10 @@ gsrq_status w_train(const gsrq_shape* s, const void* X, int64_t ldx, const float
       // 16-byte aligned rows (else the LDS kernel, with the same single
       // row chunk)
       const bool svec = ((uintptr_t)X % 16 == 0) && ((ldx * (int64_t)sizeof(T)) % 16 == 0);
+      aa.ovf = (A.sorted_sums && svec) ? (double*)(base + W.ovf) : nullptr;
+      fa.ovf = aa.ovf;
       if (A.sorted_sums && svec) {
-        const dim3 sgrid((unsigned)((K + 3) / 4), (unsigned)G);
+        const dim3 sgrid((unsigned)((K + 3) / 4 + (aa.nwin + 3) / 4), (unsigned)G);
         if (d == 64)
           w_accumulate_sorted_kernel<T, 4><<<sgrid, 256, 0, st>>>(aa);
         else if (d == 128)
